@@ -1,0 +1,220 @@
+/*
+ * dyplan.h -- C ABI of the MI355X (gfx950) workflow physical-plan scorer.
+ *
+ * A workflow request is a materialised DAG whose nodes each take one
+ * implementation: a model on a backend plus a verification policy
+ * (Sec. 3.1, eq. physical-plan; tool nodes are nodes with a single
+ * implementation).  A physical plan assigns one implementation to every node.
+ * This library scores plans and, for every pressure level, selects the best
+ * plan that meets the SLO: the pressure-specialised variants of Sec. 4.4 and
+ * Algorithm gen (coefficients bound once, then one selection per level).
+ *
+ * Scoring a plan pi (i_n = implementation of node n):
+ *   corr(pi)   = prod_n (1 - w_n * (1 - p_{n,i_n}))
+ *                vulnerability-weighted correctness: residual error 1 - q
+ *                weighted by the node's vulnerability (Sec. 4.1, Sec. 4.3).
+ *   CP_k(pi)   = longest path of the DAG where node n lasts
+ *                tau_{n,i_n} / (1 - rho_{k, backend(n,i_n)})
+ *                serial dependencies add and a join waits for its latest
+ *                predecessor (Sec. 4.3, "Accounting for parallel branches";
+ *                for fixed assignments the completion time of
+ *                eq. admission-constraints is this longest path).
+ *   demand(pi) = sum_n tau_{n,i_n} * size_{n,i_n}
+ *                nominal-duration demand annotation (Sec. 4.4, D_tau),
+ *                weighted by the model-size factor.
+ * Selection at level k: the plan with the greatest corr among plans with
+ * CP_k <= slo (inclusive); equal corr goes to the lowest plan index.
+ *
+ * Plan index: mixed radix over the nodes, node 0 most significant:
+ *   index = (...((i_0 * radix_1 + i_1) * radix_2 + i_2)...) * radix_{N-1} + i_{N-1}.
+ *
+ * Numerics.  Plans are scored in fp32 on the GPU.  Selections are certified:
+ * every plan whose fp32 score could, within the proven fp32 error bound, be
+ * the exact winner is re-evaluated in fp64 with the definition above written
+ * out in node order without fused multiply-add, so the selected index and
+ * feasibility flag equal those of an fp64 evaluation of every plan, and the
+ * reported corr / cp / demand of a winner are its fp64 values rounded to the
+ * nearest fp32.  Per-plan scores (dy_plan_score) are fp32 with relative error
+ * below 2 * n_nodes * 2^-24 (corr, demand) and (n_nodes + 2) * 2^-24 (cp);
+ * their feasibility bits are exact (fp64 decides every plan whose fp32 CP is
+ * too close to the SLO to decide).
+ *
+ * Errors.  Every entry point returns DY_OK (0) or a negative status and never
+ * aborts or throws.  dy_plan_last_error(handle) describes the last failure on
+ * that handle; dy_plan_last_error(NULL) the last failure of dy_plan_create on
+ * the calling thread.  A handle may be used by one thread at a time; distinct
+ * handles are independent.
+ */
+#ifndef DYPLAN_H
+#define DYPLAN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DY_ABI_VERSION 1
+
+#define DY_MAX_NODES 32      /* nodes per problem */
+#define DY_MAX_RADIX 255     /* implementations per node (ids fit a uint8 row byte) */
+#define DY_MAX_LEVELS 32     /* pressure levels per problem */
+#define DY_MAX_BACKENDS 64   /* backends per problem */
+
+enum {
+    DY_OK = 0,
+    DY_EINVAL = -1,   /* bad argument: null pointer, NaN, value out of range, bad row id */
+    DY_ENOTDAG = -2,  /* an edge (u, v) is not u < v (the numbering must be topological) */
+    DY_ELIMIT = -3,   /* a compile-time limit above is exceeded, or a range is too long */
+    DY_ENOMEM = -4,   /* host or device allocation failed */
+    DY_EDEVICE = -5   /* a HIP runtime call failed (no device, launch failure, ...) */
+};
+
+typedef struct dy_plan dy_plan; /* opaque handle */
+
+/*
+ * One planning problem (one materialised workflow request).  All pointers are
+ * HOST pointers; dy_plan_create copies what it needs, so the caller may free
+ * them as soon as it returns.
+ *
+ *  n_nodes            N, 1..DY_MAX_NODES.
+ *  n_edges, edges     E edges as int32 pairs [E][2] = (u, v), 0 <= u < v < N
+ *                     (nodes numbered in a topological order, Sec. 3.1);
+ *                     duplicate edges are allowed and mean one edge.
+ *  radix              int32 [N], 1..DY_MAX_RADIX implementations per node.
+ *  max_radix          row stride of the tables below, >= max(radix).
+ *  p                  float [N][max_radix] success probability q of
+ *                     implementation (n, i), in [0, 1] (Sec. 4.1).
+ *  tau                float [N][max_radix] nominal duration, finite, >= 0
+ *                     (Sec. 4.2, eq. tau).
+ *  size               float [N][max_radix] model-size factor used by the
+ *                     demand annotation, finite, >= 0.
+ *  backend            int32 [N][max_radix] backend id, 0..n_backends-1.
+ *  w                  float [N] vulnerability v_n in [0, 1] (Sec. 4.3).
+ *  n_levels, rho      K levels, float [K][n_backends] pressure of backend b
+ *                     at level k, 0 <= rho < 1; a node's duration at level k
+ *                     is tau / (1 - rho_{k, backend}).
+ *  slo                critical-path bound, >= 0 (may be +inf).
+ * Table entries with i >= radix[n] are ignored.  Sum over nodes of the
+ * largest tau must stay below 1e30.
+ */
+typedef struct dy_problem {
+    int32_t n_nodes;
+    int32_t n_edges;
+    const int32_t* edges;
+    const int32_t* radix;
+    int32_t max_radix;
+    const float* p;
+    const float* tau;
+    const float* size;
+    const int32_t* backend;
+    const float* w;
+    int32_t n_levels;
+    int32_t n_backends;
+    const float* rho;
+    float slo;
+} dy_problem;
+
+enum { DY_SOURCE_RANGE = 0, DY_SOURCE_ROWS = 1 };
+
+/*
+ * Where the candidate plans of one problem come from.
+ *  kind = DY_SOURCE_RANGE: plan indices [begin, begin + count) of the
+ *         problem's mixed-radix space (count >= 1, begin + count <= the
+ *         number of plans and <= 2^64 - 1).  rows/row_stride/index_base unused.
+ *  kind = DY_SOURCE_ROWS: `count` rows in DEVICE memory, row r at
+ *         rows + r * row_stride, byte n of a row = implementation id of node n
+ *         (must be < radix[n]; a bad id makes the call fail with DY_EINVAL).
+ *         row_stride >= n_nodes.  The plan index reported for row r is
+ *         index_base + r.  The rows must stay valid until the call's stream
+ *         work completes.
+ *  problem: index of the problem in the array given to dy_plan_create.
+ * A single source may cover at most 2^40 plans.
+ */
+typedef struct dy_source {
+    int32_t kind;
+    int32_t problem;
+    uint64_t begin;
+    uint64_t count;
+    const uint8_t* rows;
+    uint64_t row_stride;
+    uint64_t index_base;
+} dy_source;
+
+/* The selected plan of one level.  index = -1 and feasible = 0 when no plan of
+ * the source meets the SLO at that level; corr, cp and demand are then NaN.
+ * cp is CP at this level. */
+typedef struct dy_choice {
+    int64_t index;
+    int32_t feasible;
+    float corr;
+    float cp;
+    float demand;
+} dy_choice;
+
+/* Statistics of the last dy_plan_select call on a handle. */
+typedef struct dy_stats {
+    uint64_t plans;          /* plans scored */
+    uint64_t candidates;     /* plans re-evaluated in fp64 for certification */
+    int32_t fallbacks;       /* (source, level) pairs decided by the exhaustive fp64 path */
+    int32_t n_jobs;          /* sources in the call */
+    float main_ms;           /* duration of the main scoring kernel(s), when timing is on */
+    float total_ms;          /* launch of the first kernel to the end of the last */
+} dy_stats;
+
+/* Options for dy_plan_set_option. */
+enum {
+    DY_OPT_TIMING = 1,          /* 1: record HIP events around the kernels of each call (default 0) */
+    DY_OPT_SAMPLE_STRIDE = 2,   /* 1 of every S work units scored by the seeding pre-pass (default 32) */
+    DY_OPT_CAND_CAPACITY = 3,   /* candidate slots per source (default 1 << 16, min 16) */
+    DY_OPT_FORCE_FP64 = 4       /* 1: decide every level with the exhaustive fp64 path (default 0) */
+};
+
+/*
+ * Validate and stage n_probs problems on HIP device `device`.  Derives, once,
+ * the fp32 tables (per-node factor 1 - w(1 - p), duration, demand term), the
+ * per-level certification bands and the DAG structure (Algorithm gen: bind
+ * coefficients once for all levels), and copies them to device memory owned
+ * by the handle.  Validation runs before any HIP call.
+ * On success *out is the new handle; on failure *out = NULL.
+ */
+int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_plan** out);
+
+/*
+ * Select, for every source, the best feasible plan of each level.
+ *  src     HOST array of n_src sources (each names a problem of the handle;
+ *          several sources may name the same problem).
+ *  out     HOST array [n_src][dy_plan_max_levels(h)]; row s, column k is level
+ *          k of source s (columns >= that problem's n_levels are untouched).
+ *  stream  a hipStream_t (NULL: the default stream); kernels run on it and
+ *          the call synchronises it before returning.
+ */
+int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream);
+
+/*
+ * Per-plan scores of one source, written asynchronously on `stream` into
+ * caller-owned DEVICE buffers (any may be NULL to skip it):
+ *  corr[count], cp[count][K] (CP at each level), demand[count],
+ *  feas_bits[count] (bit k set iff CP_k <= slo, decided exactly; K <= 32).
+ * Inputs and outputs must stay valid until the stream work completes.
+ */
+int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, float* demand,
+                  uint32_t* feas_bits, void* stream);
+
+/* Free the handle and its device memory (NULL is a no-op). */
+void dy_plan_destroy(dy_plan* h);
+
+int32_t dy_plan_max_levels(const dy_plan* h);
+int32_t dy_plan_num_problems(const dy_plan* h);
+int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value);
+int dy_plan_get_stats(const dy_plan* h, dy_stats* out);
+
+const char* dy_plan_last_error(const dy_plan* h);
+const char* dy_status_str(int status);
+int32_t dy_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DYPLAN_H */

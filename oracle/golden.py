@@ -1,0 +1,198 @@
+"""Write the stored workload SLOs and full-size expected selections.
+
+TEST INFRASTRUCTURE ONLY.  Every stored number is produced here by the fp64
+oracle (oracle.c) on inputs from the seeded workload generator; nothing comes
+from the GPU library.
+
+  SLO = 1.5 x the exact lower median (0-based rank floor((n-1)/2)) of the
+        unpressured critical path over the workload's scored plan set,
+        computed in fp64 and rounded to the nearest fp32.
+  select_<workload>.json = the oracle's per-level winners over the full
+        plan set, computed as independent single-threaded chunks merged by
+        the exact rule (greatest correctness, then lowest index).
+
+Usage:  python -m oracle.golden [--procs P] [--only name,...] [--skip-select]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import multiprocessing as mp
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from oracle import oracle as orc  # noqa: E402
+from paper_2607_02942_amd import workload as wl  # noqa: E402
+
+GOLDEN_DIR = os.path.join(ROOT, "tests", "golden")
+HIST_BITS = 24
+
+# workload -> (source kind, plan count)
+SOURCES = {
+    "chain4": ("range", 12 ** 4),
+    "forkjoin8": ("range", 12 ** 8),
+    "layered10": ("range", wl.LAYERED_RANGE),
+    "stream24": ("rows", wl.STREAM_ROWS),
+}
+
+
+def _problem(name, r=None):
+    if name == "batch6":
+        return wl.batch6_request(r, slo=0.0)
+    return {"chain4": wl.chain4, "forkjoin8": wl.forkjoin8, "layered10": wl.layered10,
+            "stream24": wl.stream24}[name](slo=0.0)
+
+
+def _rows(prob, begin, count):
+    return wl.make_rows(count, prob.n_nodes, int(prob.radix[0]), row_begin=begin, threads=1)
+
+
+def _chunks(total, size):
+    return [(b, min(size, total - b)) for b in range(0, total, size)]
+
+
+# ---- median ------------------------------------------------------------------
+
+def _hist_task(args):
+    name, kind, begin, count = args
+    prob = _problem(name)
+    op = orc.OracleProblem(prob, 0.0)
+    hist = np.zeros(1 << HIST_BITS, np.uint64)
+    if kind == "rows":
+        rows = _rows(prob, begin, count)
+        orc.lib().or_cp0_hist(op.ref, 1, rows.ctypes.data, rows.shape[1], 0, count, HIST_BITS, hist.ctypes.data)
+    else:
+        orc.lib().or_cp0_hist(op.ref, 0, None, 0, begin, count, HIST_BITS, hist.ctypes.data)
+    nz = np.nonzero(hist)[0]
+    return nz, hist[nz]
+
+
+def _collect_task(args):
+    name, kind, begin, count, bucket, cap = args
+    prob = _problem(name)
+    op = orc.OracleProblem(prob, 0.0)
+    out = np.zeros(cap, np.float64)
+    if kind == "rows":
+        rows = _rows(prob, begin, count)
+        got = orc.lib().or_cp0_collect(op.ref, 1, rows.ctypes.data, rows.shape[1], 0, count, HIST_BITS,
+                                       bucket, out.ctypes.data, cap)
+    else:
+        got = orc.lib().or_cp0_collect(op.ref, 0, None, 0, begin, count, HIST_BITS, bucket, out.ctypes.data, cap)
+    assert got <= cap, "bucket larger than the collection buffer"
+    return out[:got]
+
+
+def lower_median_cp0(name, pool, chunk):
+    kind, total = SOURCES[name]
+    tasks = [(name, kind, b, c) for b, c in _chunks(total, chunk)]
+    hist = np.zeros(1 << HIST_BITS, np.uint64)
+    for nz, v in pool.imap_unordered(_hist_task, tasks):
+        hist[nz] += v
+    rank = (total - 1) // 2
+    cum = np.cumsum(hist)
+    bucket = int(np.searchsorted(cum, rank + 1))
+    below = int(cum[bucket - 1]) if bucket > 0 else 0
+    cap = int(hist[bucket])
+    vals = np.concatenate(list(pool.imap(_collect_task, [t + (bucket, cap) for t in tasks])))
+    assert vals.size == cap
+    vals.sort()
+    return float(vals[rank - below])
+
+
+def _batch_slo_task(r):
+    prob = _problem("batch6", r)
+    vals = orc.cp0_values(prob, 0, prob.n_plans())
+    rank = (vals.size - 1) // 2
+    med = np.partition(vals, rank)[rank]
+    return r, float(np.float32(1.5 * med))
+
+
+# ---- selection -----------------------------------------------------------------
+
+def _select_task(args):
+    name, kind, begin, count, slo = args
+    prob = _problem(name)
+    if kind == "rows":
+        rows = _rows(prob, begin, count)
+        return begin, orc.select_rows(prob, rows, begin, slo=slo)
+    return begin, orc.select_range(prob, begin, count, slo=slo)
+
+
+def full_select(name, slo, pool, chunk):
+    kind, total = SOURCES[name]
+    tasks = [(name, kind, b, c, slo) for b, c in _chunks(total, chunk)]
+    parts = sorted(pool.imap_unordered(_select_task, tasks))
+    return orc.merge_choices([p for _, p in parts])
+
+
+def _batch_select_task(args):
+    r, slo = args
+    prob = _problem("batch6", r)
+    return r, orc.select_range(prob, 0, prob.n_plans(), slo=slo)
+
+
+def _fmt_choices(ch):
+    return [[int(c[0]), int(c[1]), repr(float(c[2])), repr(float(c[3])), repr(float(c[4]))] for c in ch]
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--procs", type=int, default=os.cpu_count() or 1)
+    ap.add_argument("--only", default="chain4,forkjoin8,batch6,layered10,stream24")
+    ap.add_argument("--skip-select", action="store_true")
+    args = ap.parse_args()
+    names = args.only.split(",")
+    os.makedirs(GOLDEN_DIR, exist_ok=True)
+    slo_path = os.path.join(GOLDEN_DIR, "slo.json")
+    slos = json.load(open(slo_path)) if os.path.exists(slo_path) else {}
+    chunk = {"chain4": 1 << 20, "forkjoin8": 1 << 22, "layered10": 1 << 24, "stream24": 1 << 22}
+    ctx = mp.get_context("fork")
+    with ctx.Pool(args.procs) as pool:
+        for name in names:
+            t0 = time.time()
+            if name == "batch6":
+                res = sorted(pool.imap_unordered(_batch_slo_task, range(wl.N_BATCH), chunksize=8))
+                slos["batch6"] = [s for _, s in res]
+            else:
+                med = lower_median_cp0(name, pool, chunk[name])
+                slos[name] = float(np.float32(1.5 * med))
+            json.dump(slos, open(slo_path, "w"), indent=1)
+            print(f"[golden] slo {name}: {slos[name] if name != 'batch6' else '4096 values'} "
+                  f"({time.time() - t0:.1f}s)", flush=True)
+            if args.skip_select:
+                continue
+            t0 = time.time()
+            out = {"workload": name, "generator": "paper_2607_02942_amd.workload", "oracle": "oracle/oracle.c"}
+            if name == "batch6":
+                res = sorted(pool.imap_unordered(_batch_select_task,
+                                                 [(r, slos["batch6"][r]) for r in range(wl.N_BATCH)], chunksize=8))
+                out["source"] = {"kind": "range", "begin": 0, "count": 12 ** 6, "requests": wl.N_BATCH}
+                out["choices"] = [_fmt_choices(ch) for _, ch in res]
+            else:
+                kind, total = SOURCES[name]
+                out["source"] = {"kind": kind, "begin": 0, "count": total}
+                out["slo"] = slos[name]
+                out["choices"] = _fmt_choices(full_select(name, slos[name], pool, chunk[name]))
+            path = os.path.join(GOLDEN_DIR, f"select_{name}.json")
+            with open(path, "w") as f:
+                if name == "batch6":
+                    f.write("{\n")
+                    for key in ("workload", "generator", "oracle", "source"):
+                        f.write(f" {json.dumps(key)}: {json.dumps(out[key])},\n")
+                    f.write(' "choices": [\n')
+                    f.write(",\n".join(json.dumps(c, separators=(",", ":")) for c in out["choices"]))
+                    f.write("\n ]\n}\n")
+                else:
+                    json.dump(out, f, indent=1)
+            print(f"[golden] select {name} ({time.time() - t0:.1f}s)", flush=True)
+
+
+if __name__ == "__main__":
+    main()
