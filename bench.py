@@ -1,0 +1,218 @@
+"""Benchmark: candidate plans scored per second on one MI355X.
+
+A step is one dy_plan_select over the workload's whole plan set: the seeding
+pre-pass, the fp32 scoring pass over every plan, certification of the
+candidates in fp64 and the copy of the K winners back to the host.  The
+problem tables are staged once (dy_plan_create) before timing; their staging
+time is reported separately as "stage_ms".
+
+Default workload: forkjoin8 (8-node fork-join DAG, 12 implementations per
+node, 12^8 = 429,981,696 plans, 8 pressure levels).  --workload picks another
+(chain4, layered10, batch6, stream24) for profiling.
+
+Prints one JSON line (rank 0).  The roofline object describes the dominant
+kernel, timed live with HIP events recorded by the library on the call's stream.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "candidate plans scored/sec on 1 MI355X; % of FP32 VALU (or HBM) roofline"
+PEAK_VALU = 256 * 64 * 2.4e9      # fp32 lane-ops/s without packed math or FMA counting
+PEAK_HBM = 8.0e12                 # bytes/s
+
+
+def edge_count(prob):
+    return len({(int(u), int(v)) for u, v in prob.edges})
+
+
+def sweep_work_per_plan(prob):
+    """Algorithmic fp32 operations per plan of the prefix-shared sweep.
+
+    Per plan: 1 multiply (corr), 1 add (CP), 1 compare (prefilter); per row of
+    the inner sweep (R_y plans): the add and multiply of node x and the max of
+    y's predecessors; per block (R_x R_y plans): the prefix products and one
+    max/add per prefix edge.  Counted like the full recurrence, operation by
+    operation, so the figure never exceeds the work actually done.
+    """
+    n = prob.n_nodes
+    rx = int(prob.radix[n - 2]) if n >= 2 else 1
+    ry = int(prob.radix[n - 1])
+    edges = {(int(u), int(v)) for u, v in prob.edges}
+    npre = max(n - 2, 0)
+    pre_edges = sum(1 for u, v in edges if v < npre)
+    x_pred = sum(1 for u, v in edges if v == n - 2)
+    y_pred = sum(1 for u, v in edges if v == n - 1 and u != n - 2)
+    per_plan = 3.0
+    per_row = 2.0 + (1.0 if (n - 2, n - 1) in edges and y_pred > 0 else 0.0)
+    per_block = max(npre - 1, 0) + pre_edges + x_pred + y_pred
+    return per_plan + per_row / ry + per_block / (rx * ry)
+
+
+def full_work_per_plan(prob, K):
+    """The per-plan count of the full recurrence: (N-1) mul + E max/add + K compares."""
+    return (prob.n_nodes - 1) + edge_count(prob) + K
+
+
+def cpu_baseline(prob, sample_plans=None, rows=None):
+    from oracle import oracle as orc
+    t0 = time.perf_counter()
+    if rows is not None:
+        orc.select_rows(prob, rows, 0)
+        n = rows.shape[0]
+        what = f"first {n} rows"
+    else:
+        orc.select_range(prob, 0, sample_plans)
+        n = sample_plans
+        what = f"plan indices [0, {sample_plans})"
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "plans/s", "cores": 1, "kind": "oracle",
+            "sample": f"{prob.name}: {what}, single-threaded fp64 oracle, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="forkjoin8",
+                    choices=["chain4", "forkjoin8", "layered10", "batch6", "stream24"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=1 << 26)
+    ap.add_argument("--sample-stride", type=int, default=0)
+    ap.add_argument("--calib-copy", type=int, default=0, help="MiB: run one device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the work shards by plan range; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_02942_amd import dyplan as D
+    from paper_2607_02942_amd import workload as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+
+    if args.calib_copy:
+        n = args.calib_copy << 20
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty(n, dtype=torch.uint8, device="cuda")
+        a.fill_(1)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calib_copy_bytes": n}), flush=True)
+        return
+
+    name = args.workload
+    rows_dev = None
+    rows_host = None
+    if name == "batch6":
+        probs = wl.batch6()
+        sources = [D.range_source(r, 0, 12 ** 6) for r in range(len(probs))]
+        plans = len(probs) * 12 ** 6
+    else:
+        probs = [wl.by_name(name)]
+        if name == "stream24":
+            plans = wl.STREAM_ROWS
+            rows_host = wl.make_rows(plans, 24, 36)
+            rows_dev = torch.from_numpy(rows_host).cuda()
+            sources = [D.rows_source(0, rows_dev, plans, 24, 0)]
+        else:
+            plans = wl.LAYERED_RANGE if name == "layered10" else probs[0].n_plans()
+            sources = [D.range_source(0, 0, plans)]
+    prob = probs[0]
+    K = prob.n_levels
+    for p in probs:
+        assert np.isfinite(p.slo), f"stored SLO missing for {p.name}"
+
+    t0 = time.perf_counter()
+    plan = D.Plan(probs, device=0)
+    stage_ms = (time.perf_counter() - t0) * 1e3
+    if args.sample_stride:
+        plan.set_option(D.DY_OPT_SAMPLE_STRIDE, args.sample_stride)
+    plan.set_option(D.DY_OPT_TIMING, 1)
+    srcs = (D.DySource * len(sources))(*sources)
+    out = (D.DyChoice * (len(sources) * plan.kmax))()
+
+    def step():
+        st = plan.select_raw(srcs, len(sources), out, stream)
+        if st != 0:
+            raise RuntimeError(f"select failed {st}: {D.last_error(plan._h)}")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    main_ms = []
+    cands = []
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step()
+        s = plan.stats()
+        main_ms.append(s.main_ms)
+        cands.append(s.candidates)
+        if i == 0 or (i + 1) % max(1, args.steps // 4) == 0:
+            print(f"[bench] step {i + 1}/{args.steps}", file=sys.stderr, flush=True)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = ev0.elapsed_time(ev1)
+    ms_per_step = total_ms / args.steps
+    value = plans / (ms_per_step / 1e3)
+    kern_ms = float(np.mean(main_ms))
+    kern_plans_s = plans / (kern_ms / 1e3)
+
+    if name == "stream24":
+        bytes_per_plan = 24.0
+        achieved = kern_plans_s * bytes_per_plan
+        roof = {"bound": "hbm", "kernel": "k_scan (rows)", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
+                "unit": "GB/s", "frac": achieved / PEAK_HBM, "traffic": None,
+                "per_unit": "24 B of row per plan", "kernel_ms": kern_ms}
+    else:
+        f = sweep_work_per_plan(prob)
+        achieved = kern_plans_s * f
+        roof = {"bound": "alu", "kernel": "k_sweep", "achieved": achieved / 1e12, "peak": PEAK_VALU / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_VALU, "traffic": None,
+                "per_unit": f"{f:.4f} fp32 ops per plan (prefix-shared sweep)", "kernel_ms": kern_ms,
+                "full_recurrence_ops_per_plan": full_work_per_plan(prob, K)}
+
+    res = {
+        "metric": METRIC, "value": value, "unit": "plans/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": name, "plans": plans, "nodes": prob.n_nodes, "edges": edge_count(prob),
+                   "impls_per_node": int(prob.radix[0]), "levels": K,
+                   "problems": len(probs), "parallelism": "single GPU"},
+        "roofline": roof,
+        "stage_ms": stage_ms,
+        "candidates_per_step": float(np.mean(cands)),
+    }
+    if not args.no_cpu_baseline:
+        if name == "stream24":
+            res["cpu_baseline"] = cpu_baseline(prob, rows=rows_host[: 1 << 22])
+        elif name == "batch6":
+            res["cpu_baseline"] = cpu_baseline(prob, sample_plans=12 ** 6)
+        else:
+            res["cpu_baseline"] = cpu_baseline(prob, sample_plans=min(args.cpu_sample, plans))
+    plan.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

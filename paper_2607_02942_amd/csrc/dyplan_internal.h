@@ -1,0 +1,99 @@
+// Internal layout shared by the host side (host.cpp) and the kernels
+// (kernels.hip) of the plan scorer.  Not part of the public ABI.
+#pragma once
+
+#include <stdint.h>
+
+#include "dyplan.h"
+
+namespace dyp {
+
+constexpr int WG = 256;          // threads per workgroup of the scoring kernels
+constexpr int NMAX = DY_MAX_NODES;
+constexpr int KMAX = DY_MAX_LEVELS;
+constexpr int NBINS = 64;        // lane-resident prefilter table: one bin per lane
+
+// Unsigned 32-bit division by an invariant divisor (Granlund & Montgomery,
+// PLDI 1994, Fig. 4.1): q = (t + ((x - t) >> sh1)) >> sh2, t = mulhi(m, x).
+struct Magic {
+    uint32_t m;
+    uint32_t sh1;
+    uint32_t sh2;
+    uint32_t d;
+};
+
+// Static, per problem; built once by dy_plan_create.
+struct ProbDev {
+    int32_t n, k, b, rmax;
+    int32_t npre;             // prefix nodes 0..npre-1 (the nodes before the inner pair)
+    int32_t xnode, ynode;     // inner pair x = N-2, y = N-1 (x = -1 for a 1-node DAG)
+    int32_t rx, ry;           // their radices (rx = 1 when x is virtual)
+    int32_t uniform;          // every level presses all used backends equally
+    int32_t edge_xy;          // edge x -> y exists
+    int32_t x_sink;           // x has no successor
+    uint32_t pre_sinks;       // sinks among prefix nodes (bit mask)
+    uint32_t sinks;           // sinks among all nodes
+    uint32_t pred[NMAX];      // predecessor bit mask of each node
+    int32_t radix[NMAX];
+    Magic rmag[NMAX];         // division by radix[n]
+    Magic pvmag[NMAX];        // division by the place value of prefix node n within a block index
+    uint32_t pv_big[NMAX];    // place value >= 2^32: the digit of this prefix node is 0 for 32-bit blocks
+    uint64_t pv64[NMAX];      // place value of prefix node n within a block index (saturated)
+    uint64_t n_plans;         // number of plans (saturated at 2^64-1)
+    float lo[KMAX];           // certainly feasible at level k if the fp32 CP compared is <= lo[k]
+    float hi[KMAX];           // possibly feasible at level k only if it is <= hi[k]
+    float mk[KMAX];           // uniform mode: fp32 1/(1 - rho_k), for per-plan CP outputs
+    double slo;
+    uint32_t cp_lo_bits, cp_hi_bits;  // fp32 bounds of the unpressured CP over all plans
+    int32_t bin_shift;        // prefilter bin = (bits(CP) >> bin_shift) mod 64
+    int32_t pad0;
+    // device tables
+    const float2* at;         // [n][rmax] (factor a = 1 - w(1-p), duration tau), fp32
+    const float2* atx;        // rows of x and y in `at` (x: a 1-entry (1, 0) row when virtual)
+    const float2* aty;
+    const float* dem;         // [n][rmax] demand term tau * size, fp32
+    const float* lat;         // general mode: [k][n][rmax] fp32 tau / (1 - rho_{k,b})
+    // raw inputs, for the fp64 re-evaluation
+    const float* p;
+    const float* tau;
+    const float* size;
+    const float* w;
+    const float* rho;         // [k][b]
+    const int32_t* bk;        // [n][rmax]
+};
+
+struct Cand {
+    uint64_t index;
+    float corr;
+    float cp;
+};
+
+enum JobFlags : int32_t { JF_OVERFLOW = 1, JF_BAD_ROW = 2 };
+
+// Per source, per call.
+struct JobDev {
+    const ProbDev* prob;
+    int32_t kind;             // DY_SOURCE_RANGE / DY_SOURCE_ROWS
+    int32_t big;              // RANGE: some block (or plan) index needs 64 bits
+    uint64_t begin, count;    // RANGE: plan indices [begin, begin + count); ROWS: count rows
+    const uint8_t* rows;
+    uint64_t stride;
+    uint64_t index_base;
+    uint64_t blk_first, nblk; // RANGE sweep: inner-pair blocks covering the range
+    uint64_t units;           // work units of the main kernel (blocks for the sweep, plans otherwise)
+    uint32_t sample_stride;
+    uint32_t cap;             // candidate slots
+    uint32_t* scert;          // [KMAX] best certainly-feasible fp32 corr found by the pre-pass, bits + 1 (0: none)
+    float* thr;               // [KMAX] candidate thresholds
+    uint32_t* table;          // [NBINS] prefilter thresholds (fp32 bits)
+    Cand* cand;               // [cap]
+    uint32_t* ncand;
+    int32_t* flags;
+    dy_choice* out;           // [KMAX]
+    uint64_t* fb_corr;        // [KMAX] exhaustive fp64 path: best corr bits
+    uint64_t* fb_index;       // [KMAX] exhaustive fp64 path: lowest index at that corr
+    uint32_t fb_levels;       // exhaustive path: bit mask of levels to decide
+    int32_t pad1;
+};
+
+}  // namespace dyp

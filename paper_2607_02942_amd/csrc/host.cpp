@@ -1,0 +1,862 @@
+// Host side of the plan scorer: validation, one-time table derivation
+// (Algorithm gen binds coefficients once for every level), certification
+// bands, device staging and the orchestration of a selection call.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "dyplan.h"
+#include "dyplan_internal.h"
+
+namespace dyp {
+hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s);
+hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s);
+hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_samples, int npre_max,
+                               hipStream_t s);
+hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, hipStream_t s);
+hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, hipStream_t s);
+hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStream_t s);
+hipError_t launch_certify(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s);
+hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
+hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
+                        hipStream_t s);
+}  // namespace dyp
+
+using namespace dyp;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+constexpr uint64_t kMaxSourcePlans = 1ull << 40;
+constexpr size_t kCandPoolBytes = 256ull << 20;  // candidate slots shared by the sources of one call
+constexpr double kU = 0x1p-24;                    // fp32 unit roundoff
+
+struct HostProb {
+    int n = 0, k = 0, b = 0, rmax = 0;
+    int npre = 0, rx = 1, ry = 1;
+    bool uniform = true, has_s2 = false;
+    uint64_t n_plans = 0;       // saturated
+    bool plans_saturated = false;
+};
+
+struct Scratch {
+    size_t jobs = 0;            // sources the buffers hold
+    uint32_t cap = 0;           // candidate slots per source
+    int kmax = 0;
+    char* d = nullptr;
+    size_t bytes = 0;
+    JobDev* d_jobs = nullptr;
+    JobDev* d_fb = nullptr;
+    uint32_t* scert = nullptr;
+    float* thr = nullptr;
+    uint32_t* table = nullptr;
+    uint32_t* ncand = nullptr;
+    int32_t* flags = nullptr;
+    dy_choice* out = nullptr;
+    uint64_t* fb_corr = nullptr;
+    uint64_t* fb_index = nullptr;
+    Cand* cand = nullptr;
+    // pinned host mirrors
+    JobDev* h_jobs = nullptr;
+    JobDev* h_fb = nullptr;
+    dy_choice* h_out = nullptr;
+    uint32_t* h_ncand = nullptr;
+    int32_t* h_flags = nullptr;
+};
+
+uint32_t f2u(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    return u;
+}
+
+float round_down(double x) {
+    float f = (float)x;
+    if ((double)f > x) f = std::nextafter(f, -INFINITY);
+    return f;
+}
+
+float round_up(double x) {
+    float f = (float)x;
+    if ((double)f < x) f = std::nextafter(f, INFINITY);
+    return f;
+}
+
+Magic make_magic(uint64_t d) {
+    Magic g{0u, 0u, 0u, (uint32_t)d};
+    int l = 0;
+    while ((1ull << l) < d) ++l;
+    unsigned __int128 num = ((unsigned __int128)1 << 32) * (unsigned __int128)((1ull << l) - d);
+    g.m = (uint32_t)(num / d + 1);
+    g.sh1 = l < 1 ? (uint32_t)l : 1u;
+    g.sh2 = l > 1 ? (uint32_t)(l - 1) : 0u;
+    return g;
+}
+
+uint32_t magic_div(uint32_t x, const Magic& g) {
+    uint32_t t = (uint32_t)(((uint64_t)g.m * x) >> 32);
+    return (t + ((x - t) >> g.sh1)) >> g.sh2;
+}
+
+uint64_t sat_mul(uint64_t a, uint64_t b, bool* sat) {
+    unsigned __int128 r = (unsigned __int128)a * b;
+    if (r > (unsigned __int128)UINT64_MAX) {
+        *sat = true;
+        return UINT64_MAX;
+    }
+    return (uint64_t)r;
+}
+
+bool finite_f(float x) { return std::isfinite(x); }
+
+int fail(std::string* err, int status, const char* fmt, int a = 0, int b = 0, int c = 0) {
+    char buf[256];
+    std::snprintf(buf, sizeof buf, fmt, a, b, c);
+    *err = buf;
+    return status;
+}
+
+int validate_problem(const dy_problem& pb, int idx, std::string* err) {
+    const int N = pb.n_nodes;
+    if (N < 1) return fail(err, DY_EINVAL, "problem %d: n_nodes must be >= 1", idx);
+    if (N > DY_MAX_NODES) return fail(err, DY_ELIMIT, "problem %d: n_nodes %d exceeds %d", idx, N, DY_MAX_NODES);
+    if (pb.n_edges < 0) return fail(err, DY_EINVAL, "problem %d: negative n_edges", idx);
+    if (pb.n_edges > 0 && !pb.edges) return fail(err, DY_EINVAL, "problem %d: edges is NULL", idx);
+    if (pb.n_edges > DY_MAX_NODES * DY_MAX_NODES)
+        return fail(err, DY_ELIMIT, "problem %d: too many edges", idx);
+    if (!pb.radix || !pb.p || !pb.tau || !pb.size || !pb.backend || !pb.w || !pb.rho)
+        return fail(err, DY_EINVAL, "problem %d: a table pointer is NULL", idx);
+    if (pb.n_levels < 1) return fail(err, DY_EINVAL, "problem %d: n_levels must be >= 1", idx);
+    if (pb.n_levels > DY_MAX_LEVELS)
+        return fail(err, DY_ELIMIT, "problem %d: n_levels %d exceeds %d", idx, pb.n_levels, DY_MAX_LEVELS);
+    if (pb.n_backends < 1) return fail(err, DY_EINVAL, "problem %d: n_backends must be >= 1", idx);
+    if (pb.n_backends > DY_MAX_BACKENDS)
+        return fail(err, DY_ELIMIT, "problem %d: n_backends %d exceeds %d", idx, pb.n_backends, DY_MAX_BACKENDS);
+    int rmax = 0;
+    for (int n = 0; n < N; ++n) {
+        if (pb.radix[n] < 1) return fail(err, DY_EINVAL, "problem %d: radix[%d] < 1", idx, n);
+        if (pb.radix[n] > DY_MAX_RADIX)
+            return fail(err, DY_ELIMIT, "problem %d: radix[%d] exceeds %d", idx, n, DY_MAX_RADIX);
+        rmax = std::max(rmax, pb.radix[n]);
+    }
+    if (pb.max_radix < rmax || pb.max_radix > (1 << 16))
+        return fail(err, DY_EINVAL, "problem %d: max_radix %d must be in [max radix, 65536]", idx, pb.max_radix);
+    for (int e = 0; e < pb.n_edges; ++e) {
+        int u = pb.edges[2 * e], v = pb.edges[2 * e + 1];
+        if (u < 0 || v < 0 || u >= N || v >= N)
+            return fail(err, DY_EINVAL, "problem %d: edge %d names a node out of range", idx, e);
+        if (u >= v)
+            return fail(err, DY_ENOTDAG, "problem %d: edge %d is not (u, v) with u < v (topological numbering)", idx, e);
+    }
+    double sum_tau = 0.0, sum_dem = 0.0;
+    for (int n = 0; n < N; ++n) {
+        float w = pb.w[n];
+        if (!(w >= 0.0f && w <= 1.0f)) return fail(err, DY_EINVAL, "problem %d: w[%d] not in [0, 1]", idx, n);
+        double mt = 0.0, md = 0.0;
+        for (int i = 0; i < pb.radix[n]; ++i) {
+            size_t e = (size_t)n * pb.max_radix + i;
+            float p = pb.p[e], t = pb.tau[e], s = pb.size[e];
+            int b = pb.backend[e];
+            if (!(p >= 0.0f && p <= 1.0f))
+                return fail(err, DY_EINVAL, "problem %d: p[%d][%d] not in [0, 1]", idx, n, i);
+            if (!finite_f(t) || t < 0.0f)
+                return fail(err, DY_EINVAL, "problem %d: tau[%d][%d] must be finite and >= 0", idx, n, i);
+            if (!finite_f(s) || s < 0.0f)
+                return fail(err, DY_EINVAL, "problem %d: size[%d][%d] must be finite and >= 0", idx, n, i);
+            if (b < 0 || b >= pb.n_backends)
+                return fail(err, DY_EINVAL, "problem %d: backend[%d][%d] out of range", idx, n, i);
+            mt = std::max(mt, (double)t);
+            md = std::max(md, (double)t * (double)s);
+        }
+        sum_tau += mt;
+        sum_dem += md;
+    }
+    for (int k = 0; k < pb.n_levels; ++k)
+        for (int b = 0; b < pb.n_backends; ++b) {
+            float r = pb.rho[k * pb.n_backends + b];
+            if (!(r >= 0.0f && r < 1.0f))
+                return fail(err, DY_EINVAL, "problem %d: rho[%d][%d] not in [0, 1)", idx, k, b);
+            if (sum_tau / (1.0 - (double)r) > 1e30)
+                return fail(err, DY_EINVAL, "problem %d: durations too large at level %d", idx, k);
+        }
+    if (sum_dem > 1e30) return fail(err, DY_EINVAL, "problem %d: demand terms too large", idx);
+    if (!(pb.slo >= 0.0f)) return fail(err, DY_EINVAL, "problem %d: slo must be >= 0 (and not NaN)", idx);
+    return DY_OK;
+}
+
+// fp32 longest path with one duration per node (the kernels' recurrence).
+float cp32(int N, const uint32_t* pred, uint32_t sinks, const float* d) {
+    float f[DY_MAX_NODES];
+    float best = 0.0f;
+    for (int n = 0; n < N; ++n) {
+        float m = 0.0f;
+        for (int u = 0; u < n; ++u)
+            if (pred[n] >> u & 1u) m = std::max(m, f[u]);
+        f[n] = d[n] + m;
+        if (sinks >> n & 1u) best = std::max(best, f[n]);
+    }
+    return best;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace
+
+struct dy_plan {
+    int device = 0;
+    int kmax = 0;
+    std::vector<HostProb> hp;
+    char* d_arena = nullptr;
+    ProbDev* d_probs = nullptr;
+    Scratch sc;
+    int timing = 0;
+    uint32_t sample_stride = 32;
+    uint32_t cand_cap = 1u << 16;
+    int force_fp64 = 0;
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    dy_stats stats{};
+    std::string err;
+};
+
+namespace {
+
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        ok = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+int hip_fail(std::string* err, hipError_t e, const char* what) {
+    *err = std::string(what) + ": " + hipGetErrorString(e);
+    return e == hipErrorOutOfMemory ? DY_ENOMEM : DY_EDEVICE;
+}
+
+void free_scratch(Scratch& s) {
+    if (s.d) (void)hipFree(s.d);
+    if (s.h_jobs) (void)hipHostFree(s.h_jobs);
+    if (s.h_fb) (void)hipHostFree(s.h_fb);
+    if (s.h_out) (void)hipHostFree(s.h_out);
+    if (s.h_ncand) (void)hipHostFree(s.h_ncand);
+    if (s.h_flags) (void)hipHostFree(s.h_flags);
+    s = Scratch{};
+}
+
+int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
+    Scratch& s = h->sc;
+    if (s.d && s.jobs >= njobs && s.cap >= cap && s.kmax == h->kmax) return DY_OK;
+    free_scratch(s);
+    const int km = h->kmax;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = align_up(off, 256);
+        off = o + bytes;
+        return o;
+    };
+    size_t o_jobs = take(njobs * sizeof(JobDev));
+    size_t o_fb = take(njobs * sizeof(JobDev));
+    size_t o_scert = take(njobs * KMAX * sizeof(uint32_t));
+    size_t o_thr = take(njobs * KMAX * sizeof(float));
+    size_t o_table = take(njobs * NBINS * sizeof(uint32_t));
+    size_t o_ncand = take(njobs * sizeof(uint32_t));
+    size_t o_flags = take(njobs * sizeof(int32_t));
+    size_t o_out = take(njobs * km * sizeof(dy_choice));
+    size_t o_fbc = take(njobs * KMAX * sizeof(uint64_t));
+    size_t o_fbi = take(njobs * KMAX * sizeof(uint64_t));
+    size_t o_cand = take(njobs * (size_t)cap * sizeof(Cand));
+    hipError_t e = hipMalloc((void**)&s.d, off);
+    if (e != hipSuccess) {
+        s.d = nullptr;
+        return hip_fail(&h->err, e, "hipMalloc(scratch)");
+    }
+    s.bytes = off;
+    s.jobs = njobs;
+    s.cap = cap;
+    s.kmax = km;
+    s.d_jobs = (JobDev*)(s.d + o_jobs);
+    s.d_fb = (JobDev*)(s.d + o_fb);
+    s.scert = (uint32_t*)(s.d + o_scert);
+    s.thr = (float*)(s.d + o_thr);
+    s.table = (uint32_t*)(s.d + o_table);
+    s.ncand = (uint32_t*)(s.d + o_ncand);
+    s.flags = (int32_t*)(s.d + o_flags);
+    s.out = (dy_choice*)(s.d + o_out);
+    s.fb_corr = (uint64_t*)(s.d + o_fbc);
+    s.fb_index = (uint64_t*)(s.d + o_fbi);
+    s.cand = (Cand*)(s.d + o_cand);
+    if ((e = hipHostMalloc((void**)&s.h_jobs, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
+        (e = hipHostMalloc((void**)&s.h_fb, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
+        (e = hipHostMalloc((void**)&s.h_out, njobs * km * sizeof(dy_choice), hipHostMallocDefault)) != hipSuccess ||
+        (e = hipHostMalloc((void**)&s.h_ncand, njobs * sizeof(uint32_t), hipHostMallocDefault)) != hipSuccess ||
+        (e = hipHostMalloc((void**)&s.h_flags, njobs * sizeof(int32_t), hipHostMallocDefault)) != hipSuccess) {
+        free_scratch(s);
+        return hip_fail(&h->err, e, "hipHostMalloc(scratch)");
+    }
+    return DY_OK;
+}
+
+// Builds the device image of every problem: ProbDev descriptors + tables.
+int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::string* err) {
+    struct Layout {
+        size_t at, atx, dem, lat, p, tau, size, w, rho, bk;
+    };
+    std::vector<Layout> lay(n_probs);
+    size_t off = align_up((size_t)n_probs * sizeof(ProbDev), 256);
+    auto take = [&](size_t bytes) {
+        size_t o = align_up(off, 256);
+        off = o + bytes;
+        return o;
+    };
+    h->hp.resize(n_probs);
+    h->kmax = 0;
+    for (int j = 0; j < n_probs; ++j) {
+        const dy_problem& pb = probs[j];
+        const size_t NR = (size_t)pb.n_nodes * pb.max_radix;
+        Layout& L = lay[j];
+        L.at = take(NR * sizeof(float2));
+        L.atx = take(sizeof(float2));
+        L.dem = take(NR * sizeof(float));
+        L.p = take(NR * sizeof(float));
+        L.tau = take(NR * sizeof(float));
+        L.size = take(NR * sizeof(float));
+        L.w = take((size_t)pb.n_nodes * sizeof(float));
+        L.rho = take((size_t)pb.n_levels * pb.n_backends * sizeof(float));
+        L.bk = take(NR * sizeof(int32_t));
+        L.lat = take((size_t)pb.n_levels * NR * sizeof(float));
+        h->kmax = std::max(h->kmax, pb.n_levels);
+    }
+    std::vector<char> img(off, 0);
+    hipError_t e = hipMalloc((void**)&h->d_arena, off);
+    if (e != hipSuccess) {
+        h->d_arena = nullptr;
+        return hip_fail(err, e, "hipMalloc(tables)");
+    }
+    h->d_probs = (ProbDev*)h->d_arena;
+    ProbDev* descs = (ProbDev*)img.data();
+    for (int j = 0; j < n_probs; ++j) {
+        const dy_problem& pb = probs[j];
+        const Layout& L = lay[j];
+        const int N = pb.n_nodes, R = pb.max_radix, K = pb.n_levels, B = pb.n_backends;
+        ProbDev& D = descs[j];
+        std::memset(&D, 0, sizeof D);
+        HostProb& H = h->hp[j];
+        D.n = N;
+        D.k = K;
+        D.b = B;
+        D.rmax = R;
+        // structure
+        uint32_t succ = 0;
+        for (int e2 = 0; e2 < pb.n_edges; ++e2) {
+            int u = pb.edges[2 * e2], v = pb.edges[2 * e2 + 1];
+            D.pred[v] |= 1u << u;
+            succ |= 1u << u;
+        }
+        const uint32_t all = N == 32 ? 0xffffffffu : ((1u << N) - 1u);
+        D.sinks = all & ~succ;
+        D.npre = N >= 2 ? N - 2 : 0;
+        D.xnode = N >= 2 ? N - 2 : -1;
+        D.ynode = N - 1;
+        D.rx = N >= 2 ? pb.radix[N - 2] : 1;
+        D.ry = pb.radix[N - 1];
+        D.edge_xy = (N >= 2 && (D.pred[N - 1] >> (N - 2) & 1u)) ? 1 : 0;
+        D.x_sink = N >= 2 ? (int)((D.sinks >> (N - 2)) & 1u) : 1;
+        D.pre_sinks = D.npre > 0 ? (D.sinks & ((1u << D.npre) - 1u)) : 0u;
+        for (int n = 0; n < N; ++n) {
+            D.radix[n] = pb.radix[n];
+            D.rmag[n] = make_magic((uint64_t)pb.radix[n]);
+        }
+        // place values of prefix nodes inside a block index (product of later prefix radices)
+        for (int n = 0; n < D.npre; ++n) {
+            bool sat = false;
+            uint64_t pv = 1;
+            for (int m = n + 1; m < D.npre; ++m) pv = sat_mul(pv, (uint64_t)pb.radix[m], &sat);
+            D.pv64[n] = sat ? UINT64_MAX : pv;
+            D.pv_big[n] = (sat || pv > 0xffffffffull) ? 1u : 0u;
+            D.pvmag[n] = D.pv_big[n] ? Magic{0, 0, 0, 0} : make_magic(pv);
+        }
+        bool sat = false;
+        uint64_t np = 1;
+        for (int n = 0; n < N; ++n) np = sat_mul(np, (uint64_t)pb.radix[n], &sat);
+        D.n_plans = np;
+        H.n_plans = np;
+        H.plans_saturated = sat;
+        // pressure: uniform when every used backend of a level has the same rho
+        uint64_t used = 0;
+        for (int n = 0; n < N; ++n)
+            for (int i = 0; i < pb.radix[n]; ++i) used |= 1ull << pb.backend[(size_t)n * R + i];
+        bool uniform = true;
+        std::vector<double> rho_k(K, 0.0);
+        for (int k = 0; k < K; ++k) {
+            bool first = true;
+            float r0 = 0.0f;
+            for (int b = 0; b < B; ++b) {
+                if (!(used >> b & 1ull)) continue;
+                float r = pb.rho[k * B + b];
+                if (first) {
+                    r0 = r;
+                    first = false;
+                } else if (f2u(r) != f2u(r0)) {
+                    uniform = false;
+                }
+            }
+            rho_k[k] = (double)r0;
+        }
+        D.uniform = uniform ? 1 : 0;
+        D.slo = (double)pb.slo;
+        const double slo = (double)pb.slo;
+        // certification bands (fp32 CP error <= (N-1) u relative, fp64 oracle error
+        // ~ (N+3) 2^-53; the margin (N+1) u covers both, (N+2) u with rounded latencies)
+        for (int k = 0; k < K; ++k) {
+            if (uniform) {
+                const double th = slo * (1.0 - rho_k[k]);
+                D.lo[k] = round_down(th * (1.0 - (N + 1) * kU));
+                D.hi[k] = round_up(th * (1.0 + (N + 1) * kU));
+                D.mk[k] = (float)(1.0 / (1.0 - rho_k[k]));
+            } else {
+                D.lo[k] = round_down(slo * (1.0 - (N + 2) * kU));
+                D.hi[k] = round_up(slo * (1.0 + (N + 2) * kU));
+                D.mk[k] = 1.0f;
+            }
+        }
+        // tables
+        float2* at = (float2*)(img.data() + L.at);
+        float* dem = (float*)(img.data() + L.dem);
+        float* lat = (float*)(img.data() + L.lat);
+        float dmin[DY_MAX_NODES], dmax[DY_MAX_NODES];
+        for (int n = 0; n < N; ++n) {
+            double w = (double)pb.w[n];
+            dmin[n] = INFINITY;
+            dmax[n] = 0.0f;
+            for (int i = 0; i < pb.radix[n]; ++i) {
+                size_t e2 = (size_t)n * R + i;
+                double t = 1.0 - (double)pb.p[e2];
+                t = w * t;
+                float a = (float)(1.0 - t);
+                float tau = pb.tau[e2] == 0.0f ? 0.0f : pb.tau[e2];
+                at[e2] = make_float2(a, tau);
+                dem[e2] = (float)((double)tau * (double)pb.size[e2]);
+                dmin[n] = std::min(dmin[n], tau);
+                dmax[n] = std::max(dmax[n], tau);
+                for (int k = 0; k < K; ++k) {
+                    double r = (double)pb.rho[k * B + pb.backend[e2]];
+                    lat[(size_t)k * N * R + e2] = (float)((double)tau / (1.0 - r));
+                }
+            }
+        }
+        float2* atx = (float2*)(img.data() + L.atx);
+        *atx = make_float2(1.0f, 0.0f);
+        std::memcpy(img.data() + L.p, pb.p, (size_t)N * R * sizeof(float));
+        std::memcpy(img.data() + L.tau, pb.tau, (size_t)N * R * sizeof(float));
+        std::memcpy(img.data() + L.size, pb.size, (size_t)N * R * sizeof(float));
+        std::memcpy(img.data() + L.w, pb.w, (size_t)N * sizeof(float));
+        std::memcpy(img.data() + L.rho, pb.rho, (size_t)K * B * sizeof(float));
+        std::memcpy(img.data() + L.bk, pb.backend, (size_t)N * R * sizeof(int32_t));
+        // fp32 bounds of the unpressured CP (the recurrence is monotone in every duration)
+        const float clo = cp32(N, D.pred, D.sinks, dmin);
+        const float chi = cp32(N, D.pred, D.sinks, dmax);
+        D.cp_lo_bits = f2u(clo);
+        D.cp_hi_bits = f2u(chi);
+        int s = 2;
+        while (s < 31 && ((D.cp_hi_bits >> s) - (D.cp_lo_bits >> s)) > 62u) ++s;
+        D.bin_shift = s;
+        char* base = h->d_arena;
+        D.at = (const float2*)(base + L.at);
+        D.atx = N >= 2 ? (const float2*)(base + L.at) + (size_t)(N - 2) * R : (const float2*)(base + L.atx);
+        D.aty = (const float2*)(base + L.at) + (size_t)(N - 1) * R;
+        D.dem = (const float*)(base + L.dem);
+        D.lat = (const float*)(base + L.lat);
+        D.p = (const float*)(base + L.p);
+        D.tau = (const float*)(base + L.tau);
+        D.size = (const float*)(base + L.size);
+        D.w = (const float*)(base + L.w);
+        D.rho = (const float*)(base + L.rho);
+        D.bk = (const int32_t*)(base + L.bk);
+        H.n = N;
+        H.k = K;
+        H.b = B;
+        H.rmax = R;
+        H.npre = D.npre;
+        H.rx = D.rx;
+        H.ry = D.ry;
+        H.uniform = uniform;
+        H.has_s2 = D.pre_sinks != 0 || !D.edge_xy;
+    }
+    e = hipMemcpy(h->d_arena, img.data(), off, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(err, e, "hipMemcpy(tables)");
+    return DY_OK;
+}
+
+int check_source(const dy_plan* h, const dy_source& s, int idx, std::string* err) {
+    if (s.problem < 0 || s.problem >= (int)h->hp.size())
+        return fail(err, DY_EINVAL, "source %d: problem %d out of range", idx, s.problem);
+    const HostProb& H = h->hp[s.problem];
+    if (s.count < 1) return fail(err, DY_EINVAL, "source %d: count must be >= 1", idx);
+    if (s.count > kMaxSourcePlans) return fail(err, DY_ELIMIT, "source %d: more than 2^40 plans", idx);
+    if (s.kind == DY_SOURCE_RANGE) {
+        if (s.begin > UINT64_MAX - s.count)
+            return fail(err, DY_EINVAL, "source %d: begin + count overflows", idx);
+        if (!H.plans_saturated && s.begin + s.count > H.n_plans)
+            return fail(err, DY_EINVAL, "source %d: range exceeds the problem's plan count", idx);
+        if (s.begin + s.count - 1 > (uint64_t)INT64_MAX)
+            return fail(err, DY_ELIMIT, "source %d: plan index exceeds 2^63-1", idx);
+    } else if (s.kind == DY_SOURCE_ROWS) {
+        if (!s.rows) return fail(err, DY_EINVAL, "source %d: rows is NULL", idx);
+        if (s.row_stride < (uint64_t)H.n) return fail(err, DY_EINVAL, "source %d: row_stride < n_nodes", idx);
+        if (s.index_base > (uint64_t)INT64_MAX - (s.count - 1))
+            return fail(err, DY_ELIMIT, "source %d: plan index exceeds 2^63-1", idx);
+    } else {
+        return fail(err, DY_EINVAL, "source %d: unknown kind", idx);
+    }
+    return DY_OK;
+}
+
+JobDev make_job(const dy_plan* h, const dy_source& s) {
+    const HostProb& H = h->hp[s.problem];
+    JobDev J;
+    std::memset(&J, 0, sizeof J);
+    J.prob = h->d_probs + s.problem;
+    J.kind = s.kind;
+    J.begin = s.begin;
+    J.count = s.count;
+    J.rows = s.rows;
+    J.stride = s.row_stride;
+    J.index_base = s.index_base;
+    J.sample_stride = h->sample_stride;
+    if (s.kind == DY_SOURCE_RANGE) {
+        const uint64_t inner = (uint64_t)H.rx * (uint64_t)H.ry;
+        J.blk_first = s.begin / inner;
+        const uint64_t blk_last = (s.begin + s.count - 1) / inner;
+        J.nblk = blk_last - J.blk_first + 1;
+        J.big = (blk_last > 0xffffffffull || s.begin + s.count - 1 > 0xffffffffull) ? 1 : 0;
+    }
+    return J;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t dy_abi_version(void) { return DY_ABI_VERSION; }
+
+const char* dy_status_str(int status) {
+    switch (status) {
+        case DY_OK: return "ok";
+        case DY_EINVAL: return "invalid argument";
+        case DY_ENOTDAG: return "edges are not in topological order";
+        case DY_ELIMIT: return "limit exceeded";
+        case DY_ENOMEM: return "out of memory";
+        case DY_EDEVICE: return "device error";
+        default: return "unknown status";
+    }
+}
+
+const char* dy_plan_last_error(const dy_plan* h) { return h ? h->err.c_str() : g_create_error.c_str(); }
+
+int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_plan** out) {
+    if (!out) {
+        g_create_error = "out is NULL";
+        return DY_EINVAL;
+    }
+    *out = nullptr;
+    if (!probs || n_probs < 1) {
+        g_create_error = "probs is NULL or n_probs < 1";
+        return DY_EINVAL;
+    }
+    for (int j = 0; j < n_probs; ++j) {
+        int st = validate_problem(probs[j], j, &g_create_error);
+        if (st != DY_OK) return st;
+    }
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess || ndev < 1) {
+        g_create_error = std::string("no HIP device: ") + hipGetErrorString(e);
+        return DY_EDEVICE;
+    }
+    if (device < 0 || device >= ndev) {
+        g_create_error = "device index out of range";
+        return DY_EDEVICE;
+    }
+    DeviceGuard g(device);
+    if (!g.ok) {
+        g_create_error = "hipSetDevice failed";
+        return DY_EDEVICE;
+    }
+    dy_plan* h = new (std::nothrow) dy_plan();
+    if (!h) {
+        g_create_error = "host allocation failed";
+        return DY_ENOMEM;
+    }
+    h->device = device;
+    int st = stage_problems(h, probs, n_probs, &g_create_error);
+    if (st == DY_OK) {
+        for (int i = 0; i < 4 && st == DY_OK; ++i)
+            if ((e = hipEventCreate(&h->ev[i])) != hipSuccess) st = hip_fail(&g_create_error, e, "hipEventCreate");
+    }
+    if (st != DY_OK) {
+        dy_plan_destroy(h);
+        return st;
+    }
+    g_create_error.clear();
+    *out = h;
+    return DY_OK;
+}
+
+void dy_plan_destroy(dy_plan* h) {
+    if (!h) return;
+    DeviceGuard g(h->device);
+    free_scratch(h->sc);
+    if (h->d_arena) (void)hipFree(h->d_arena);
+    for (int i = 0; i < 4; ++i)
+        if (h->ev[i]) (void)hipEventDestroy(h->ev[i]);
+    delete h;
+}
+
+int32_t dy_plan_max_levels(const dy_plan* h) { return h ? h->kmax : 0; }
+int32_t dy_plan_num_problems(const dy_plan* h) { return h ? (int32_t)h->hp.size() : 0; }
+
+int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value) {
+    if (!h) return DY_EINVAL;
+    switch (option) {
+        case DY_OPT_TIMING: h->timing = value ? 1 : 0; return DY_OK;
+        case DY_OPT_SAMPLE_STRIDE:
+            if (value < 1 || value > (1 << 30)) break;
+            h->sample_stride = (uint32_t)value;
+            return DY_OK;
+        case DY_OPT_CAND_CAPACITY:
+            if (value < 16 || value > (1 << 26)) break;
+            h->cand_cap = (uint32_t)value;
+            return DY_OK;
+        case DY_OPT_FORCE_FP64: h->force_fp64 = value ? 1 : 0; return DY_OK;
+        default:
+            h->err = "unknown option";
+            return DY_EINVAL;
+    }
+    h->err = "option value out of range";
+    return DY_EINVAL;
+}
+
+int dy_plan_get_stats(const dy_plan* h, dy_stats* out) {
+    if (!h || !out) return DY_EINVAL;
+    *out = h->stats;
+    return DY_OK;
+}
+
+int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream) {
+    if (!h) return DY_EINVAL;
+    if (!src || !out || n_src < 1) {
+        h->err = "src/out is NULL or n_src < 1";
+        return DY_EINVAL;
+    }
+    for (int j = 0; j < n_src; ++j) {
+        int st = check_source(h, src[j], j, &h->err);
+        if (st != DY_OK) return st;
+    }
+    DeviceGuard g(h->device);
+    if (!g.ok) {
+        h->err = "hipSetDevice failed";
+        return DY_EDEVICE;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    // candidate slots per source: the option, bounded by a shared pool
+    uint64_t cap = h->cand_cap;
+    const uint64_t pool_cap = kCandPoolBytes / sizeof(Cand) / (uint64_t)n_src;
+    if (cap > pool_cap) cap = std::max<uint64_t>(pool_cap, 1024);
+    int st = ensure_scratch(h, (size_t)n_src, (uint32_t)cap);
+    if (st != DY_OK) return st;
+    Scratch& S = h->sc;
+    const int km = h->kmax;
+
+    // order: sweep without S2, sweep with S2, generic
+    std::vector<int> order;
+    order.reserve(n_src);
+    int n_sweep[2] = {0, 0};
+    uint64_t sweep_units[2] = {0, 0}, sweep_samples[2] = {0, 0};
+    int sweep_npre[2] = {0, 0};
+    uint64_t gen_units = 0, gen_samples = 0, all_units = 0;
+    for (int pass = 0; pass < 3; ++pass)
+        for (int j = 0; j < n_src; ++j) {
+            const HostProb& H = h->hp[src[j].problem];
+            const bool sweep = !h->force_fp64 && src[j].kind == DY_SOURCE_RANGE && H.uniform;
+            const int grp = sweep ? (H.has_s2 ? 1 : 0) : 2;
+            if (grp != pass) continue;
+            order.push_back(j);
+        }
+    uint64_t plans = 0;
+    for (int q = 0; q < n_src; ++q) {
+        const int j = order[q];
+        const HostProb& H = h->hp[src[j].problem];
+        JobDev J = make_job(h, src[j]);
+        J.cap = (uint32_t)cap;
+        J.scert = S.scert + (size_t)q * KMAX;
+        J.thr = S.thr + (size_t)q * KMAX;
+        J.table = S.table + (size_t)q * NBINS;
+        J.cand = S.cand + (size_t)q * cap;
+        J.ncand = S.ncand + q;
+        J.flags = S.flags + q;
+        J.out = S.out + (size_t)j * km;
+        J.fb_corr = S.fb_corr + (size_t)q * KMAX;
+        J.fb_index = S.fb_index + (size_t)q * KMAX;
+        J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
+        const bool sweep = !h->force_fp64 && src[j].kind == DY_SOURCE_RANGE && H.uniform;
+        if (sweep) {
+            const int gi = H.has_s2 ? 1 : 0;
+            J.units = J.nblk;
+            ++n_sweep[gi];
+            sweep_units[gi] = std::max(sweep_units[gi], J.nblk);
+            sweep_samples[gi] = std::max(sweep_samples[gi], (J.nblk + h->sample_stride - 1) / h->sample_stride);
+            sweep_npre[gi] = std::max(sweep_npre[gi], H.npre);
+        } else {
+            J.units = J.count;
+            gen_units = std::max(gen_units, J.count);
+            gen_samples = std::max(gen_samples, (J.count + h->sample_stride - 1) / h->sample_stride);
+        }
+        all_units = std::max(all_units, J.count);
+        plans += J.count;
+        S.h_jobs[q] = J;
+    }
+    const int n_gen = n_src - n_sweep[0] - n_sweep[1];
+    hipError_t e = hipMemcpyAsync(S.d_jobs, S.h_jobs, (size_t)n_src * sizeof(JobDev), hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(&h->err, e, "hipMemcpyAsync(jobs)");
+    const JobDev* jA = S.d_jobs;
+    const JobDev* jB = S.d_jobs + n_sweep[0];
+    const JobDev* jG = S.d_jobs + n_sweep[0] + n_sweep[1];
+    auto chk = [&](hipError_t x, const char* what) {
+        if (x != hipSuccess && st == DY_OK) st = hip_fail(&h->err, x, what);
+    };
+    // kernels take at most 65535 sources per launch along y
+    auto chunks = [&](const JobDev* base, int n, auto&& fn) {
+        for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
+    };
+    if (h->timing) chk(hipEventRecord(h->ev[0], s), "hipEventRecord");
+    chunks(S.d_jobs, n_src, [&](const JobDev* b, int n) { chk(launch_init(const_cast<JobDev*>(b), n, s), "init"); });
+    if (!h->force_fp64) {
+        for (int gi = 0; gi < 2; ++gi) {
+            const JobDev* base = gi ? jB : jA;
+            chunks(base, n_sweep[gi], [&](const JobDev* b, int n) {
+                chk(launch_sample_sweep(b, n, gi == 1, sweep_samples[gi], sweep_npre[gi], s), "sample");
+            });
+        }
+        chunks(jG, n_gen, [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, gen_samples, s), "sample"); });
+        chunks(S.d_jobs, n_src, [&](const JobDev* b, int n) { chk(launch_table(const_cast<JobDev*>(b), n, s), "table"); });
+        if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
+        for (int gi = 0; gi < 2; ++gi) {
+            const JobDev* base = gi ? jB : jA;
+            chunks(base, n_sweep[gi], [&](const JobDev* b, int n) {
+                chk(launch_sweep(b, n, gi == 1, sweep_units[gi], sweep_npre[gi], s), "sweep");
+            });
+        }
+        chunks(jG, n_gen, [&](const JobDev* b, int n) { chk(launch_scan(b, n, gen_units, s), "scan"); });
+        if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
+        chunks(S.d_jobs, n_src, [&](const JobDev* b, int n) { chk(launch_certify(b, n, km, s), "certify"); });
+    } else {
+        if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
+        chunks(S.d_jobs, n_src, [&](const JobDev* b, int n) { chk(launch_exhaust(b, n, all_units, s), "exhaust"); });
+        if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
+    }
+    if (h->timing) chk(hipEventRecord(h->ev[3], s), "hipEventRecord");
+    chk(hipMemcpyAsync(S.h_out, S.out, (size_t)n_src * km * sizeof(dy_choice), hipMemcpyDeviceToHost, s), "copy out");
+    chk(hipMemcpyAsync(S.h_ncand, S.ncand, (size_t)n_src * sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy out");
+    chk(hipMemcpyAsync(S.h_flags, S.flags, (size_t)n_src * sizeof(int32_t), hipMemcpyDeviceToHost, s), "copy out");
+    chk(hipStreamSynchronize(s), "hipStreamSynchronize");
+    if (st != DY_OK) return st;
+
+    dy_stats stats{};
+    stats.plans = plans;
+    stats.n_jobs = n_src;
+    if (h->timing) {
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, h->ev[1], h->ev[2]) == hipSuccess) stats.main_ms = ms;
+        if (hipEventElapsedTime(&ms, h->ev[0], h->ev[3]) == hipSuccess) stats.total_ms = ms;
+    }
+    // fallback for sources whose candidate list overflowed
+    int n_fb = 0;
+    uint64_t fb_units = 0;
+    for (int q = 0; q < n_src; ++q) {
+        const int32_t fl = S.h_flags[q];
+        stats.candidates += std::min<uint64_t>(S.h_ncand[q], cap);
+        if (fl & JF_BAD_ROW) {
+            h->err = "a row holds an implementation id >= radix of its node";
+            return DY_EINVAL;
+        }
+        if ((fl & JF_OVERFLOW) && !h->force_fp64) {
+            JobDev J = S.h_jobs[q];
+            const int K = h->hp[src[order[q]].problem].k;
+            J.fb_levels = K == 32 ? 0xffffffffu : ((1u << K) - 1u);
+            S.h_fb[n_fb++] = J;
+            fb_units = std::max(fb_units, J.count);
+            stats.fallbacks += K;
+        }
+    }
+    if (h->force_fp64)
+        for (int j = 0; j < n_src; ++j) stats.fallbacks += h->hp[src[j].problem].k;
+    if (n_fb > 0) {
+        chk(hipMemcpyAsync(S.d_fb, S.h_fb, (size_t)n_fb * sizeof(JobDev), hipMemcpyHostToDevice, s), "copy fb");
+        chunks(S.d_fb, n_fb, [&](const JobDev* b, int n) { chk(launch_exhaust(b, n, fb_units, s), "exhaust"); });
+        chk(hipMemcpyAsync(S.h_out, S.out, (size_t)n_src * km * sizeof(dy_choice), hipMemcpyDeviceToHost, s),
+            "copy out");
+        chk(hipStreamSynchronize(s), "hipStreamSynchronize");
+        if (st != DY_OK) return st;
+    }
+    for (int j = 0; j < n_src; ++j) {
+        const int K = h->hp[src[j].problem].k;
+        std::memcpy(out + (size_t)j * km, S.h_out + (size_t)j * km, (size_t)K * sizeof(dy_choice));
+    }
+    h->stats = stats;
+    return DY_OK;
+}
+
+int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, float* demand, uint32_t* feas_bits,
+                  void* stream) {
+    if (!h) return DY_EINVAL;
+    if (!src) {
+        h->err = "src is NULL";
+        return DY_EINVAL;
+    }
+    int st = check_source(h, *src, 0, &h->err);
+    if (st != DY_OK) return st;
+    DeviceGuard g(h->device);
+    if (!g.ok) {
+        h->err = "hipSetDevice failed";
+        return DY_EDEVICE;
+    }
+    JobDev J = make_job(h, *src);
+    hipError_t e = launch_score(J, src->count, corr, cp, demand, feas_bits, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(&h->err, e, "score launch");
+    return DY_OK;
+}
+
+// Host-only self checks of internal helpers (no device call).  Returns the
+// number of failures.
+int dy_selftest(void) {
+    int bad = 0;
+    const uint32_t ds[] = {1, 2, 3, 5, 7, 10, 12, 36, 100, 255, 1296, 20736, 46656, 2985984, 60466176,
+                           2176782336u, 4294967295u};
+    const uint32_t xs[] = {0, 1, 2, 11, 12, 13, 143, 144, 1295, 1296, 20735, 65535, 65536, 2985983,
+                           429981695u, 2147483647u, 2147483648u, 4294967294u, 4294967295u};
+    for (uint32_t d : ds) {
+        Magic g = make_magic(d);
+        for (uint32_t x : xs)
+            if (magic_div(x, g) != x / d) ++bad;
+        uint64_t st = 0x9E3779B97F4A7C15ull;
+        for (int i = 0; i < 4096; ++i) {
+            st += 0x9E3779B97F4A7C15ull;
+            uint32_t x = (uint32_t)(st >> 17);
+            if (magic_div(x, g) != x / d) ++bad;
+        }
+    }
+    return bad;
+}
+
+}  // extern "C"

@@ -1,0 +1,937 @@
+// HIP kernels for gfx950 (CDNA4): scoring workflow physical plans and selecting
+// the best SLO-feasible plan per pressure level.
+//
+// Definitions (per plan, i_n = implementation of node n):
+//   corr   = prod_n a_{n,i_n},  a = 1 - w_n (1 - p)    (Sec. 4.1 / 4.3: residual
+//            error weighted by vulnerability, kept as a product over nodes)
+//   CP_k   = longest path with node durations tau / (1 - rho_{k,b})
+//            (Sec. 4.3 "Accounting for parallel branches"; completion time of
+//            eq. admission-constraints for fixed assignments)
+//   demand = sum_n tau * size  (Sec. 4.4, D_tau annotation)
+// Selection per level k: max corr s.t. CP_k <= SLO, ties to the lowest index
+// (one selection per level, Algorithm gen).
+//
+// Pipeline of one selection call (all on the caller's stream):
+//   k_init        zero the per-source scratch
+//   k_sample_*    seeding pre-pass: 1 in S work units, per level the best fp32
+//                 corr among plans whose fp32 CP is certainly feasible
+//   k_table       per level candidate threshold T_k (fp64 error bound on the
+//                 seed) and a 64-bin prefilter table indexed by the fp32 CP
+//   k_sweep / k_scan   the scoring pass: every plan is scored in fp32; a plan
+//                 goes to the candidate list when it could be a level's winner
+//   k_certify     fp64 re-evaluation of the candidates; exact winner per level
+//   k_exhaust*    fallback: exhaustive fp64 decision (candidate overflow)
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+#include "dyplan_internal.h"
+
+namespace dyp {
+
+// Descriptors and tables never change while a kernel runs: reading them
+// through the constant address space lets wave-uniform reads become scalar
+// loads (and the inner-sweep trip counts stay uniform).
+#if defined(__HIP_DEVICE_COMPILE__)
+#define CS __attribute__((address_space(4)))
+#else
+#define CS
+#endif
+typedef const CS ProbDev* PD;
+typedef const CS JobDev* JD;
+
+template <class T>
+__device__ __forceinline__ const CS T* cs(const T* p) {
+    return (const CS T*)p;
+}
+
+// ---------------------------------------------------------------------------
+// helpers
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ uint32_t mdiv(uint32_t x, const CS Magic& g) {
+    uint32_t t = __umulhi(g.m, x);
+    return (t + ((x - t) >> g.sh1)) >> g.sh2;
+}
+
+// Wave-wide max of an unsigned key with DPP row shifts and row broadcasts
+// (lane 63 ends with the maximum); the result is read back uniformly.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false));  // row_shr:1
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false));  // row_shr:2
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x113, 0xf, 0xf, false));  // row_shr:3
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xe, false));  // row_shr:4
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xc, false));  // row_shr:8
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false));  // row_bcast:15
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false));  // row_bcast:31
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Candidate threshold from the fp32 corr `s` of a certainly-feasible plan.
+// With |corr32 - corr64| <= g corr64 + eta for every plan (g = (2N+1) 2^-24,
+// eta = N 2^-148), the exact winner W satisfies corr32_W >= returned value.
+__device__ __forceinline__ float cand_threshold(float s, int n) {
+    if (!(s >= 0.0f)) return -INFINITY;
+    const double g = (2.0 * n + 1.0) * 0x1p-24;
+    const double eta = (double)n * 0x1p-148;
+    double t = ((double)s - eta) * (1.0 - g) / (1.0 + g) - eta;
+    t = t - fabs(t) * 0x1p-48;
+    return __double2float_rd(t);
+}
+
+// ---- fp64 re-evaluation (the definition, node order, no FMA contraction) ----
+
+__device__ double ex_corr(PD P, const uint8_t* ids) {
+    double c = 1.0;
+    for (int n = 0; n < P->n; ++n) {
+        double p = (double)P->p[n * P->rmax + ids[n]];
+        double w = (double)P->w[n];
+        double t = 1.0 - p;
+        t = w * t;
+        c = c * (1.0 - t);
+    }
+    return c;
+}
+
+__device__ double ex_cp(PD P, const uint8_t* ids, int k) {
+    double f[NMAX];
+    double cp = 0.0;
+    for (int n = 0; n < P->n; ++n) {
+        int e = n * P->rmax + ids[n];
+        double rho = (double)P->rho[k * P->b + P->bk[e]];
+        double lat = (double)P->tau[e] / (1.0 - rho);
+        double m = 0.0;
+        uint32_t pm = P->pred[n];
+        while (pm) {
+            int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            if (f[u] > m) m = f[u];
+        }
+        f[n] = lat + m;
+        if ((P->sinks >> n & 1u) && f[n] > cp) cp = f[n];
+    }
+    return cp;
+}
+
+__device__ double ex_demand(PD P, const uint8_t* ids) {
+    double d = 0.0;
+    for (int n = 0; n < P->n; ++n) {
+        int e = n * P->rmax + ids[n];
+        d = d + (double)P->tau[e] * (double)P->size[e];
+    }
+    return d;
+}
+
+// Implementation ids of plan `index` of the problem (node N-1 least significant).
+__device__ void decode64(PD P, uint64_t index, uint8_t* ids) {
+    for (int n = P->n - 1; n >= 0; --n) {
+        uint64_t r = (uint64_t)P->radix[n];
+        ids[n] = (uint8_t)(index % r);
+        index /= r;
+    }
+}
+
+// ids of a candidate or of a fallback unit; returns false for a bad row id
+__device__ bool job_ids(JD J, PD P, uint64_t index,
+                        uint8_t* ids) {
+    if (J->kind == DY_SOURCE_RANGE) {
+        decode64(P, index, ids);
+        return true;
+    }
+    const uint8_t* row = J->rows + (index - J->index_base) * J->stride;
+    bool ok = true;
+    for (int n = 0; n < P->n; ++n) {
+        uint8_t v = row[n];
+        if (v >= (uint32_t)P->radix[n]) {
+            ok = false;
+            v = 0;
+        }
+        ids[n] = v;
+    }
+    return ok;
+}
+
+__device__ __forceinline__ void append_cand(JD J, uint64_t index, float c, float cp) {
+    uint32_t slot = atomicAdd(J->ncand, 1u);
+    if (slot < J->cap) {
+        Cand* d = J->cand + slot;
+        d->index = index;
+        d->corr = c;
+        d->cp = cp;
+    } else {
+        atomicOr(J->flags, (int32_t)JF_OVERFLOW);
+    }
+}
+
+// exact per-level candidate test of the scoring pass (levels in P->k)
+__device__ __forceinline__ bool is_candidate(PD P, JD J,
+                                             float cp, float c) {
+    for (int k = 0; k < P->k; ++k)
+        if (cp <= P->hi[k] && c >= J->thr[k]) return true;
+    return false;
+}
+
+// ---------------------------------------------------------------------------
+// scratch initialisation
+// ---------------------------------------------------------------------------
+
+__global__ void k_init(JobDev* __restrict__ jobs, int njobs) {
+    int j = blockIdx.x;
+    if (j >= njobs) return;
+    JD J = cs(jobs + j);
+    int t = threadIdx.x;
+    if (t < KMAX) {
+        J->scert[t] = 0u;
+        J->thr[t] = -INFINITY;
+        J->fb_corr[t] = 0ull;
+        J->fb_index[t] = ~0ull;
+    }
+    if (t < cs(J->prob)->k) {
+        dy_choice* o = J->out + t;
+        o->index = -1;
+        o->feasible = 0;
+        o->corr = NAN;
+        o->cp = NAN;
+        o->demand = NAN;
+    }
+    if (t < NBINS) J->table[t] = 0u;
+    if (t == 0) {
+        *J->ncand = 0u;
+        *J->flags = 0;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// RANGE sources, uniform pressure: prefix-shared sweep
+//
+// Work unit = one "block": a fixed assignment of the prefix nodes 0..N-3; the
+// inner pair (x = N-2, y = N-1) is swept in lockstep by every lane of a wave,
+// so the tables of x and y are wave-uniform (scalar loads) and each plan costs
+// a multiply (corr), an add (CP) and a prefilter compare.
+// ---------------------------------------------------------------------------
+
+struct Prefix {
+    float pc, px, py, s;
+};
+
+__device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big,
+                                              float* __restrict__ s_f) {
+    const int tid = threadIdx.x;
+    const int npre = P->npre;
+    float pc = 1.0f;
+    const uint32_t b32 = (uint32_t)b;
+    for (int n = 0; n < npre; ++n) {
+        uint32_t d;
+        if (!big) {
+            uint32_t q = P->pv_big[n] ? 0u : mdiv(b32, P->pvmag[n]);
+            d = q - mdiv(q, P->rmag[n]) * (uint32_t)P->radix[n];
+        } else {
+            d = (uint32_t)((b / P->pv64[n]) % (uint64_t)P->radix[n]);
+        }
+        const float2 v = cs(P->at)[n * P->rmax + d];
+        pc = pc * v.x;
+        float m = 0.0f;
+        uint32_t pm = P->pred[n];
+        while (pm) {
+            int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            m = fmaxf(m, s_f[u * WG + tid]);
+        }
+        s_f[n * WG + tid] = v.y + m;
+    }
+    float px = 0.0f, py = 0.0f, s = 0.0f;
+    if (P->xnode >= 0) {
+        uint32_t pm = P->pred[P->xnode];
+        while (pm) {
+            int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            px = fmaxf(px, s_f[u * WG + tid]);
+        }
+    }
+    {
+        uint32_t pm = P->pred[P->ynode];
+        if (P->xnode >= 0) pm &= ~(1u << P->xnode);
+        while (pm) {
+            int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            py = fmaxf(py, s_f[u * WG + tid]);
+        }
+    }
+    {
+        uint32_t pm = P->pre_sinks;
+        while (pm) {
+            int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            s = fmaxf(s, s_f[u * WG + tid]);
+        }
+    }
+    return Prefix{pc, px, py, s};
+}
+
+#ifndef DYP_BPERM_MASK
+#define DYP_BPERM_MASK 1
+#endif
+
+// One plan of the inner sweep: corr = cx * a_y, CP = max(tau_y + M, S2); the
+// prefilter threshold of CP's bin comes from the lane-resident table (bin j in
+// lane j) through ds_bpermute, whose lane select is bits [7:2] of the address.
+template <bool HAS_S2>
+__device__ __forceinline__ uint64_t sweep_test(const float2 vy, float M, float S2, float cx, uint32_t sh, int tbl) {
+    float cp = vy.y + M;
+    if (HAS_S2) cp = fmaxf(cp, S2);
+    const float cc = cx * vy.x;
+    int addr = (int)(__float_as_uint(cp) >> sh);
+#if DYP_BPERM_MASK
+    addr &= 0xfc;
+#endif
+    const float thr = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, tbl));
+    return __ballot(cc >= thr);
+}
+
+template <bool HAS_S2>
+__global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, uint64_t unit_off) {
+    extern __shared__ float s_f[];
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    const uint64_t nblk = J->nblk;
+    const uint64_t t0 = unit_off + (uint64_t)blockIdx.x * WG;
+    if (t0 >= nblk) return;
+    const uint64_t t = t0 + threadIdx.x;
+    const bool live = t < nblk;
+    const uint64_t b = J->blk_first + (live ? t : nblk - 1);
+    const Prefix pf = prefix_eval(P, b, J->big, s_f);
+
+    const int tbl = (int)J->table[threadIdx.x & 63];
+    const uint32_t sh = (uint32_t)P->bin_shift - 2u;
+    const CS float2* atx = cs(P->atx);
+    const CS float2* aty = cs(P->aty);
+    const int rx = P->rx, ry = P->ry;
+    const bool exy = P->edge_xy != 0;
+
+    for (int ix = 0; ix < rx; ++ix) {
+        const float2 vx = atx[ix];
+        const float fx = vx.y + pf.px;
+        const float cx = pf.pc * vx.x;
+        const float M = exy ? fmaxf(pf.py, fx) : pf.py;
+        const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
+        uint64_t hit = 0;
+        int iy = 0;
+        for (; iy + 4 <= ry; iy += 4) {
+            const float2 v0 = aty[iy], v1 = aty[iy + 1], v2 = aty[iy + 2], v3 = aty[iy + 3];
+            hit |= sweep_test<HAS_S2>(v0, M, S2, cx, sh, tbl);
+            hit |= sweep_test<HAS_S2>(v1, M, S2, cx, sh, tbl);
+            hit |= sweep_test<HAS_S2>(v2, M, S2, cx, sh, tbl);
+            hit |= sweep_test<HAS_S2>(v3, M, S2, cx, sh, tbl);
+        }
+        for (; iy < ry; ++iy) hit |= sweep_test<HAS_S2>(aty[iy], M, S2, cx, sh, tbl);
+        if (hit) {
+            // rare: re-score this lane's row of the inner sweep with the exact test
+            const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
+            if (live && (hit >> (threadIdx.x & 63) & 1ull)) {
+                for (int iy = 0; iy < ry; ++iy) {
+                    const float2 vy = aty[iy];
+                    float cp = vy.y + M;
+                    if (HAS_S2) cp = fmaxf(cp, S2);
+                    const float cc = cx * vy.x;
+                    const uint64_t idx = base + (uint64_t)iy;
+                    if (idx - J->begin < J->count && is_candidate(P, J, cp, cc)) append_cand(J, idx, cc, cp);
+                }
+            }
+        }
+    }
+}
+
+// Work unit of sample j: one unit of the window [j S, min((j+1) S, n)), at a
+// hashed offset.  A fixed offset would alias with the mixed-radix digits (a
+// stride sharing factors with the radices visits only some implementation ids
+// of the low-order prefix nodes).
+__device__ __forceinline__ uint64_t sample_unit(uint64_t j, uint64_t S, uint64_t n) {
+    const uint64_t start = j * S;
+    const uint64_t width = min(S, n - start);
+    const uint32_t h = (uint32_t)(j * 0x9E3779B1ull) >> 16;
+    return start + (uint64_t)h % width;
+}
+
+// Seeding pre-pass of the sweep: one hashed block per window of S blocks.
+template <bool HAS_S2>
+__global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ jobs) {
+    extern __shared__ float s_f[];
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    const uint64_t S = J->sample_stride;
+    const uint64_t nsamp = (J->nblk + S - 1) / S;
+    const uint64_t t0 = (uint64_t)blockIdx.x * WG;
+    if (t0 >= nsamp) return;
+    const uint64_t t = t0 + threadIdx.x;
+    const bool live = t < nsamp;
+    const uint64_t b = J->blk_first + sample_unit(live ? t : nsamp - 1, S, J->nblk);
+    const Prefix pf = prefix_eval(P, b, J->big, s_f);
+    const int K = P->k;
+    float best[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) best[k] = -1.0f;
+    const CS float2* atx = cs(P->atx);
+    const CS float2* aty = cs(P->aty);
+    const int rx = P->rx, ry = P->ry;
+    const bool exy = P->edge_xy != 0;
+    for (int ix = 0; ix < rx; ++ix) {
+        const float2 vx = atx[ix];
+        const float fx = vx.y + pf.px;
+        const float cx = pf.pc * vx.x;
+        const float M = exy ? fmaxf(pf.py, fx) : pf.py;
+        const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
+        const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
+        for (int iy = 0; iy < ry; ++iy) {
+            const float2 vy = aty[iy];
+            float cp = vy.y + M;
+            if (HAS_S2) cp = fmaxf(cp, S2);
+            const float cc = cx * vy.x;
+            const bool ok = live && (base + (uint64_t)iy - J->begin < J->count);
+#pragma unroll
+            for (int k = 0; k < KMAX; ++k)
+                if (k < K && ok && cp <= P->lo[k]) best[k] = fmaxf(best[k], cc);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+        if (k < K) {
+            uint32_t e = best[k] >= 0.0f ? __float_as_uint(best[k]) + 1u : 0u;
+            e = wave_max_u32(e);
+            if ((threadIdx.x & 63) == 0 && e) atomicMax(J->scert + k, e);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// per-source threshold and prefilter table (one wave per source)
+// ---------------------------------------------------------------------------
+
+__global__ void k_table(JobDev* __restrict__ jobs, int njobs) {
+    const int j = blockIdx.x;
+    if (j >= njobs) return;
+    JD J = cs(jobs + j);
+    PD P = cs(J->prob);
+    const int lane = threadIdx.x;
+    if (lane < P->k) {
+        uint32_t e = J->scert[lane];
+        J->thr[lane] = e ? cand_threshold(__uint_as_float(e - 1u), P->n) : -INFINITY;
+    }
+    __syncthreads();
+    // bin `lane` covers fp32 patterns [B << s, (B+1) << s) with B = lane (mod 64),
+    // B in [cp_lo >> s, (cp_lo >> s) + 63]; its threshold is the lowest T_k of
+    // every level some CP in the bin may meet.
+    const uint32_t s = (uint32_t)P->bin_shift;
+    const uint32_t blo = P->cp_lo_bits >> s;
+    const uint32_t B = blo + (((uint32_t)lane - blo) & 63u);
+    uint32_t lowbits = B << s;
+    if (lowbits < P->cp_lo_bits) lowbits = P->cp_lo_bits;
+    const float low = __uint_as_float(lowbits);
+    float g = INFINITY;
+    for (int k = 0; k < P->k; ++k)
+        if (P->hi[k] >= low) g = fminf(g, J->thr[k]);
+    J->table[lane] = __float_as_uint(g);
+}
+
+// ---------------------------------------------------------------------------
+// generic per-plan path: ROWS sources, non-uniform pressure, per-plan scores
+// ---------------------------------------------------------------------------
+
+// ids of plan `j` of the source into the thread's LDS column; returns the plan
+// index; sets *bad for an out-of-range row id (the id is then read as 0).
+__device__ __forceinline__ uint64_t load_plan(JD J, PD P,
+                                              uint64_t j, uint8_t* __restrict__ s_id, bool* bad) {
+    const int tid = threadIdx.x;
+    const int N = P->n;
+    if (J->kind == DY_SOURCE_RANGE) {
+        const uint64_t idx = J->begin + j;
+        if (!J->big) {
+            uint32_t x = (uint32_t)idx;
+            for (int n = N - 1; n >= 0; --n) {
+                uint32_t q = mdiv(x, P->rmag[n]);
+                s_id[n * WG + tid] = (uint8_t)(x - q * (uint32_t)P->radix[n]);
+                x = q;
+            }
+        } else {
+            uint64_t x = idx;
+            for (int n = N - 1; n >= 0; --n) {
+                uint64_t r = (uint64_t)P->radix[n];
+                s_id[n * WG + tid] = (uint8_t)(x % r);
+                x /= r;
+            }
+        }
+        return idx;
+    }
+    const uint8_t* row = J->rows + j * J->stride;
+    bool b = false;
+    // word loads only when a row is whole words, so the last row is never over-read
+    if (((J->stride | (uint64_t)(uintptr_t)J->rows | (uint64_t)N) & 3u) == 0) {
+        const uint32_t* w = (const uint32_t*)row;
+        for (int q = 0; q < (N + 3) / 4; ++q) {
+            uint32_t v = __builtin_nontemporal_load(w + q);
+            for (int r = 0; r < 4 && 4 * q + r < N; ++r) {
+                uint32_t id = (v >> (8 * r)) & 0xffu;
+                const int n = 4 * q + r;
+                if (id >= (uint32_t)P->radix[n]) {
+                    b = true;
+                    id = 0;
+                }
+                s_id[n * WG + tid] = (uint8_t)id;
+            }
+        }
+    } else {
+        for (int n = 0; n < N; ++n) {
+            uint32_t id = row[n];
+            if (id >= (uint32_t)P->radix[n]) {
+                b = true;
+                id = 0;
+            }
+            s_id[n * WG + tid] = (uint8_t)id;
+        }
+    }
+    *bad = b;
+    return J->index_base + j;
+}
+
+// fp32 corr and the unpressured CP (uniform mode) of the plan in the LDS column.
+__device__ __forceinline__ void eval_uniform(PD P, const uint8_t* __restrict__ s_id,
+                                             float* __restrict__ s_f, float& cc, float& cp) {
+    const int tid = threadIdx.x;
+    float c = 1.0f, best = 0.0f;
+    for (int n = 0; n < P->n; ++n) {
+        const float2 v = P->at[n * P->rmax + s_id[n * WG + tid]];
+        c = c * v.x;
+        float m = 0.0f;
+        uint32_t pm = P->pred[n];
+        while (pm) {
+            int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            m = fmaxf(m, s_f[u * WG + tid]);
+        }
+        const float f = v.y + m;
+        s_f[n * WG + tid] = f;
+        if (P->sinks >> n & 1u) best = fmaxf(best, f);
+    }
+    cc = c;
+    cp = best;
+}
+
+__device__ __forceinline__ float eval_corr(PD P, const uint8_t* __restrict__ s_id) {
+    float c = 1.0f;
+    for (int n = 0; n < P->n; ++n) c = c * P->at[n * P->rmax + s_id[n * WG + threadIdx.x]].x;
+    return c;
+}
+
+// fp32 CP at level k from the general-mode latency table.
+__device__ __forceinline__ float eval_cp_level(PD P, const uint8_t* __restrict__ s_id,
+                                               float* __restrict__ s_f, int k) {
+    const int tid = threadIdx.x;
+    const float* lat = P->lat + (size_t)k * P->n * P->rmax;
+    float best = 0.0f;
+    for (int n = 0; n < P->n; ++n) {
+        float m = 0.0f;
+        uint32_t pm = P->pred[n];
+        while (pm) {
+            int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            m = fmaxf(m, s_f[u * WG + tid]);
+        }
+        const float f = lat[n * P->rmax + s_id[n * WG + tid]] + m;
+        s_f[n * WG + tid] = f;
+        if (P->sinks >> n & 1u) best = fmaxf(best, f);
+    }
+    return best;
+}
+
+__device__ __forceinline__ void col_ids(PD P, const uint8_t* __restrict__ s_id, uint8_t* ids) {
+    for (int n = 0; n < P->n; ++n) ids[n] = s_id[n * WG + threadIdx.x];
+}
+
+// Seeding pre-pass of the generic path: one hashed plan per window of S plans.
+__global__ void __launch_bounds__(WG) k_sample_generic(const JobDev* __restrict__ jobs) {
+    extern __shared__ float s_dyn[];
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    float* s_f = s_dyn;
+    uint8_t* s_id = (uint8_t*)(s_dyn + NMAX * WG);
+    const uint64_t S = J->sample_stride;
+    const uint64_t nsamp = (J->count + S - 1) / S;
+    const uint64_t t0 = (uint64_t)blockIdx.x * WG;
+    if (t0 >= nsamp) return;
+    const uint64_t t = t0 + threadIdx.x;
+    const bool live = t < nsamp;
+    bool bad = false;
+    load_plan(J, P, sample_unit(live ? t : nsamp - 1, S, J->count), s_id, &bad);
+    const int K = P->k;
+    float cc, cp0 = 0.0f;
+    if (P->uniform) {
+        eval_uniform(P, s_id, s_f, cc, cp0);
+    } else {
+        cc = eval_corr(P, s_id);
+    }
+    const bool ok = live && !bad;
+#pragma unroll 1
+    for (int k = 0; k < K; ++k) {
+        const float cp = P->uniform ? cp0 : eval_cp_level(P, s_id, s_f, k);
+        uint32_t e = (ok && cp <= P->lo[k]) ? __float_as_uint(cc) + 1u : 0u;
+        e = wave_max_u32(e);
+        if ((threadIdx.x & 63) == 0 && e) atomicMax(J->scert + k, e);
+    }
+}
+
+// Scoring pass of the generic path: one plan per thread.
+__global__ void __launch_bounds__(WG) k_scan(const JobDev* __restrict__ jobs, uint64_t unit_off) {
+    extern __shared__ float s_dyn[];
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    float* s_f = s_dyn;
+    uint8_t* s_id = (uint8_t*)(s_dyn + NMAX * WG);
+    const uint64_t n_units = J->count;
+    const uint64_t t0 = unit_off + (uint64_t)blockIdx.x * WG;
+    if (t0 >= n_units) return;
+    const uint64_t t = t0 + threadIdx.x;
+    const bool live = t < n_units;
+    bool bad = false;
+    const uint64_t idx = load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
+    if (live && bad) atomicOr(J->flags, (int32_t)JF_BAD_ROW);
+    if (P->uniform) {
+        float cc, cp;
+        eval_uniform(P, s_id, s_f, cc, cp);
+        const int tbl = (int)J->table[threadIdx.x & 63];
+        int addr = (int)(__float_as_uint(cp) >> ((uint32_t)P->bin_shift - 2u));
+#if DYP_BPERM_MASK
+        addr &= 0xfc;
+#endif
+        const float thr = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, tbl));
+        if (live && !bad && cc >= thr && is_candidate(P, J, cp, cc)) append_cand(J, idx, cc, cp);
+    } else {
+        const float cc = eval_corr(P, s_id);
+        bool want = false;
+        float cp_first = 0.0f;
+        for (int k = 0; k < P->k; ++k) {
+            const float cp = eval_cp_level(P, s_id, s_f, k);
+            if (cp <= P->hi[k] && cc >= J->thr[k]) {
+                if (!want) cp_first = cp;
+                want = true;
+            }
+        }
+        // general mode stores the CP of the first qualifying level; certification
+        // recomputes every level in fp64, so only the index matters
+        if (live && !bad && want) append_cand(J, idx, cc, cp_first);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// certification: exact fp64 winner among the candidates (one WG per level)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ bool better(double c1, uint64_t i1, double c2, uint64_t i2) {
+    return c1 > c2 || (c1 == c2 && i1 < i2);
+}
+
+__global__ void __launch_bounds__(WG) k_certify(const JobDev* __restrict__ jobs) {
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    const int k = blockIdx.x;
+    if (k >= P->k) return;
+    __shared__ float s_best[WG];
+    __shared__ double s_c[WG];
+    __shared__ uint64_t s_i[WG];
+    const int tid = threadIdx.x;
+    const uint32_t nc = min(*J->ncand, J->cap);
+    const float lo = P->lo[k], hi = P->hi[k];
+    const bool general = !P->uniform;
+
+    // tighten the threshold with certainly-feasible candidates (uniform mode
+    // stores the unpressured CP, compared against this level's band)
+    float sb = J->scert[k] ? __uint_as_float(J->scert[k] - 1u) : -1.0f;
+    if (!general)
+        for (uint32_t i = tid; i < nc; i += WG) {
+            const Cand c = J->cand[i];
+            if (c.cp <= lo) sb = fmaxf(sb, c.corr);
+        }
+    s_best[tid] = sb;
+    __syncthreads();
+    for (int o = WG / 2; o > 0; o >>= 1) {
+        if (tid < o) s_best[tid] = fmaxf(s_best[tid], s_best[tid + o]);
+        __syncthreads();
+    }
+    const float T = cand_threshold(s_best[0], P->n);
+
+    double bc = -1.0;
+    uint64_t bi = ~0ull;
+    uint8_t ids[NMAX];
+    for (uint32_t i = tid; i < nc; i += WG) {
+        const Cand c = J->cand[i];
+        if (c.corr < T) continue;
+        if (!general && !(c.cp <= hi)) continue;
+        if (!job_ids(J, P, c.index, ids)) continue;
+        const double cp = ex_cp(P, ids, k);
+        if (!(cp <= P->slo)) continue;
+        const double cr = ex_corr(P, ids);
+        if (better(cr, c.index, bc, bi)) {
+            bc = cr;
+            bi = c.index;
+        }
+    }
+    s_c[tid] = bc;
+    s_i[tid] = bi;
+    __syncthreads();
+    for (int o = WG / 2; o > 0; o >>= 1) {
+        if (tid < o && better(s_c[tid + o], s_i[tid + o], s_c[tid], s_i[tid])) {
+            s_c[tid] = s_c[tid + o];
+            s_i[tid] = s_i[tid + o];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        dy_choice* o = J->out + k;
+        if (s_i[0] != ~0ull) {
+            job_ids(J, P, s_i[0], ids);
+            o->index = (int64_t)s_i[0];
+            o->feasible = 1;
+            o->corr = (float)s_c[0];
+            o->cp = (float)ex_cp(P, ids, k);
+            o->demand = (float)ex_demand(P, ids);
+        } else {
+            o->index = -1;
+            o->feasible = 0;
+            o->corr = NAN;
+            o->cp = NAN;
+            o->demand = NAN;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// exhaustive fp64 path (candidate overflow, or forced): pass 0 finds the best
+// feasible corr of each level, pass 1 the lowest index reaching it
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(WG) k_exhaust(const JobDev* __restrict__ jobs, int pass) {
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    if (!J->fb_levels) return;
+    const uint64_t units = J->count;
+    const uint64_t stride = (uint64_t)gridDim.x * WG;
+    uint8_t ids[NMAX];
+    for (int k = 0; k < P->k; ++k) {
+        if (!(J->fb_levels >> k & 1u)) continue;
+        const uint64_t target = pass ? J->fb_corr[k] : 0ull;
+        uint64_t acc = pass ? ~0ull : 0ull;
+        for (uint64_t j = (uint64_t)blockIdx.x * WG + threadIdx.x; j < units; j += stride) {
+            const uint64_t idx = J->kind == DY_SOURCE_RANGE ? J->begin + j : J->index_base + j;
+            if (!job_ids(J, P, idx, ids)) continue;
+            const double cp = ex_cp(P, ids, k);
+            if (!(cp <= P->slo)) continue;
+            const uint64_t cb = (uint64_t)__double_as_longlong(ex_corr(P, ids));
+            if (!pass) {
+                acc = cb + 1ull > acc ? cb + 1ull : acc;  // +1: 0 means none
+            } else if (cb + 1ull == target && idx < acc) {
+                acc = idx;
+            }
+        }
+        for (int o = 32; o > 0; o >>= 1) {
+            const uint64_t v = __shfl_xor(acc, o);
+            acc = pass ? (v < acc ? v : acc) : (v > acc ? v : acc);
+        }
+        if ((threadIdx.x & 63) == 0) {
+            if (!pass) {
+                if (acc) atomicMax((unsigned long long*)(J->fb_corr + k), (unsigned long long)acc);
+            } else if (acc != ~0ull) {
+                atomicMin((unsigned long long*)(J->fb_index + k), (unsigned long long)acc);
+            }
+        }
+    }
+}
+
+__global__ void k_exhaust_final(const JobDev* __restrict__ jobs, int njobs) {
+    const int j = blockIdx.x;
+    if (j >= njobs) return;
+    JD J = cs(jobs + j);
+    PD P = cs(J->prob);
+    const int k = threadIdx.x;
+    if (k >= P->k || !(J->fb_levels >> k & 1u)) return;
+    uint8_t ids[NMAX];
+    dy_choice* o = J->out + k;
+    if (J->fb_index[k] != ~0ull && job_ids(J, P, J->fb_index[k], ids)) {
+        o->index = (int64_t)J->fb_index[k];
+        o->feasible = 1;
+        o->corr = (float)ex_corr(P, ids);
+        o->cp = (float)ex_cp(P, ids, k);
+        o->demand = (float)ex_demand(P, ids);
+    } else {
+        o->index = -1;
+        o->feasible = 0;
+        o->corr = NAN;
+        o->cp = NAN;
+        o->demand = NAN;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// per-plan scores (dy_plan_score)
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_off, float* corr, float* cpo,
+                                              float* dem, uint32_t* feas) {
+    extern __shared__ float s_dyn[];
+    JD J = cs(&job);
+    PD P = cs(J->prob);
+    float* s_f = s_dyn;
+    uint8_t* s_id = (uint8_t*)(s_dyn + NMAX * WG);
+    const uint64_t n_units = J->count;
+    const uint64_t t = unit_off + (uint64_t)blockIdx.x * WG + threadIdx.x;
+    if (unit_off + (uint64_t)blockIdx.x * WG >= n_units) return;
+    const bool live = t < n_units;
+    bool bad = false;
+    load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
+    const int K = P->k;
+    if (bad) {  // a row id out of range: NaN scores, no feasible level
+        if (!live) return;
+        for (int k = 0; k < K; ++k)
+            if (cpo) cpo[t * (uint64_t)K + k] = NAN;
+        if (corr) corr[t] = NAN;
+        if (dem) dem[t] = NAN;
+        if (feas) feas[t] = 0u;
+        return;
+    }
+    float cc, cp0 = 0.0f;
+    if (P->uniform) {
+        eval_uniform(P, s_id, s_f, cc, cp0);
+    } else {
+        cc = eval_corr(P, s_id);
+    }
+    uint32_t bits = 0;
+    uint8_t ids[NMAX];
+    bool have_ids = false;
+    for (int k = 0; k < K; ++k) {
+        const float cpc = P->uniform ? cp0 : eval_cp_level(P, s_id, s_f, k);
+        bool f;
+        if (cpc <= P->lo[k]) {
+            f = true;
+        } else if (!(cpc <= P->hi[k])) {
+            f = false;
+        } else {  // too close to the SLO for fp32: decide in fp64
+            if (!have_ids) {
+                col_ids(P, s_id, ids);
+                have_ids = true;
+            }
+            f = ex_cp(P, ids, k) <= P->slo;
+        }
+        if (f && k < 32) bits |= 1u << k;
+        if (live && cpo) cpo[t * (uint64_t)K + k] = P->uniform ? cp0 * P->mk[k] : cpc;
+    }
+    if (!live) return;
+    if (corr) corr[t] = cc;
+    if (feas) feas[t] = bits;
+    if (dem) {
+        float d = 0.0f;
+        for (int n = 0; n < P->n; ++n) d = d + P->dem[n * P->rmax + s_id[n * WG + threadIdx.x]];
+        dem[t] = d;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// launch wrappers (host)
+// ---------------------------------------------------------------------------
+
+static constexpr uint64_t MAX_GRID_X = 1ull << 22;  // workgroups per launch along x
+
+static size_t generic_lds() { return (size_t)NMAX * WG * sizeof(float) + (size_t)NMAX * WG; }
+
+hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s) {
+    hipLaunchKernelGGL(k_init, dim3(njobs), dim3(64), 0, s, d_jobs, njobs);
+    return hipGetLastError();
+}
+
+hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s) {
+    hipLaunchKernelGGL(k_table, dim3(njobs), dim3(64), 0, s, d_jobs, njobs);
+    return hipGetLastError();
+}
+
+// sweep jobs: [first, first + n) of d_jobs, all with the same HAS_S2
+hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_samples, int npre_max,
+                               hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    uint64_t gx = (max_samples + WG - 1) / WG;
+    if (gx == 0) return hipSuccess;
+    if (gx > MAX_GRID_X) return hipErrorInvalidValue;
+    size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float);
+    if (has_s2)
+        hipLaunchKernelGGL(k_sample_sweep<true>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs);
+    else
+        hipLaunchKernelGGL(k_sample_sweep<false>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs);
+    return hipGetLastError();
+}
+
+hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float);
+    for (uint64_t off = 0; off < max_units; off += MAX_GRID_X * WG) {
+        uint64_t left = max_units - off;
+        uint64_t gx = (left + WG - 1) / WG;
+        if (gx > MAX_GRID_X) gx = MAX_GRID_X;
+        if (has_s2)
+            hipLaunchKernelGGL(k_sweep<true>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs, off);
+        else
+            hipLaunchKernelGGL(k_sweep<false>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs, off);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    uint64_t gx = (max_samples + WG - 1) / WG;
+    if (gx == 0) return hipSuccess;
+    if (gx > MAX_GRID_X) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_sample_generic, dim3((uint32_t)gx, n), dim3(WG), generic_lds(), s, d_jobs);
+    return hipGetLastError();
+}
+
+hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    for (uint64_t off = 0; off < max_units; off += MAX_GRID_X * WG) {
+        uint64_t left = max_units - off;
+        uint64_t gx = (left + WG - 1) / WG;
+        if (gx > MAX_GRID_X) gx = MAX_GRID_X;
+        hipLaunchKernelGGL(k_scan, dim3((uint32_t)gx, n), dim3(WG), generic_lds(), s, d_jobs, off);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_certify(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s) {
+    hipLaunchKernelGGL(k_certify, dim3(kmax, njobs), dim3(WG), 0, s, d_jobs);
+    return hipGetLastError();
+}
+
+hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s) {
+    uint64_t gx = (max_units + WG - 1) / WG;
+    if (gx > 4096) gx = 4096;
+    if (gx == 0) gx = 1;
+    for (int pass = 0; pass < 2; ++pass) {
+        hipLaunchKernelGGL(k_exhaust, dim3((uint32_t)gx, njobs), dim3(WG), 0, s, d_jobs, pass);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_exhaust_final, dim3(njobs), dim3(KMAX), 0, s, d_jobs, njobs);
+    return hipGetLastError();
+}
+
+hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
+                        hipStream_t s) {
+    for (uint64_t off = 0; off < units; off += MAX_GRID_X * WG) {
+        uint64_t left = units - off;
+        uint64_t gx = (left + WG - 1) / WG;
+        if (gx > MAX_GRID_X) gx = MAX_GRID_X;
+        hipLaunchKernelGGL(k_score, dim3((uint32_t)gx), dim3(WG), generic_lds(), s, job, off, corr, cp, dem, feas);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace dyp

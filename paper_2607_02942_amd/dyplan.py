@@ -1,0 +1,224 @@
+"""Python binding of the C-ABI plan scorer (libdyplan.so).
+
+Argument marshalling only: every step of scoring and selection runs in the HIP
+library.  Host arrays are numpy; device buffers are passed as raw pointers
+(ints) or any object with a ``data_ptr()`` method (e.g. torch tensors), and a
+stream as a raw ``hipStream_t`` (int), an object with ``cuda_stream``, or None
+for the default stream.  The library must be built (``__graft_entry__.build()``);
+importing this module never falls back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdyplan.so")
+
+DY_OK, DY_EINVAL, DY_ENOTDAG, DY_ELIMIT, DY_ENOMEM, DY_EDEVICE = 0, -1, -2, -3, -4, -5
+DY_SOURCE_RANGE, DY_SOURCE_ROWS = 0, 1
+DY_OPT_TIMING, DY_OPT_SAMPLE_STRIDE, DY_OPT_CAND_CAPACITY, DY_OPT_FORCE_FP64 = 1, 2, 3, 4
+DY_MAX_NODES, DY_MAX_RADIX, DY_MAX_LEVELS, DY_MAX_BACKENDS = 32, 255, 32, 64
+
+EXPORTED = ("dy_plan_create", "dy_plan_select", "dy_plan_score", "dy_plan_destroy", "dy_plan_max_levels",
+            "dy_plan_num_problems", "dy_plan_set_option", "dy_plan_get_stats", "dy_plan_last_error",
+            "dy_status_str", "dy_abi_version", "dy_selftest")
+
+
+class DyProblem(ctypes.Structure):
+    _fields_ = [
+        ("n_nodes", ctypes.c_int32), ("n_edges", ctypes.c_int32), ("edges", ctypes.c_void_p),
+        ("radix", ctypes.c_void_p), ("max_radix", ctypes.c_int32), ("p", ctypes.c_void_p),
+        ("tau", ctypes.c_void_p), ("size", ctypes.c_void_p), ("backend", ctypes.c_void_p),
+        ("w", ctypes.c_void_p), ("n_levels", ctypes.c_int32), ("n_backends", ctypes.c_int32),
+        ("rho", ctypes.c_void_p), ("slo", ctypes.c_float),
+    ]
+
+
+class DySource(ctypes.Structure):
+    _fields_ = [
+        ("kind", ctypes.c_int32), ("problem", ctypes.c_int32), ("begin", ctypes.c_uint64),
+        ("count", ctypes.c_uint64), ("rows", ctypes.c_void_p), ("row_stride", ctypes.c_uint64),
+        ("index_base", ctypes.c_uint64),
+    ]
+
+
+class DyChoice(ctypes.Structure):
+    _fields_ = [("index", ctypes.c_int64), ("feasible", ctypes.c_int32), ("corr", ctypes.c_float),
+                ("cp", ctypes.c_float), ("demand", ctypes.c_float)]
+
+    def as_tuple(self):
+        return (int(self.index), int(self.feasible), float(self.corr), float(self.cp), float(self.demand))
+
+
+class DyStats(ctypes.Structure):
+    _fields_ = [("plans", ctypes.c_uint64), ("candidates", ctypes.c_uint64), ("fallbacks", ctypes.c_int32),
+                ("n_jobs", ctypes.c_int32), ("main_ms", ctypes.c_float), ("total_ms", ctypes.c_float)]
+
+
+class DyplanError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"dyplan status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libdyplan.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32 = ctypes.c_void_p, ctypes.c_int32
+        L.dy_plan_create.argtypes = [ctypes.POINTER(DyProblem), i32, i32, ctypes.POINTER(vp)]
+        L.dy_plan_create.restype = ctypes.c_int
+        L.dy_plan_select.argtypes = [vp, ctypes.POINTER(DySource), i32, ctypes.POINTER(DyChoice), vp]
+        L.dy_plan_select.restype = ctypes.c_int
+        L.dy_plan_score.argtypes = [vp, ctypes.POINTER(DySource), vp, vp, vp, vp, vp]
+        L.dy_plan_score.restype = ctypes.c_int
+        L.dy_plan_destroy.argtypes = [vp]
+        L.dy_plan_destroy.restype = None
+        L.dy_plan_max_levels.argtypes = [vp]
+        L.dy_plan_max_levels.restype = i32
+        L.dy_plan_num_problems.argtypes = [vp]
+        L.dy_plan_num_problems.restype = i32
+        L.dy_plan_set_option.argtypes = [vp, i32, ctypes.c_int64]
+        L.dy_plan_set_option.restype = ctypes.c_int
+        L.dy_plan_get_stats.argtypes = [vp, ctypes.POINTER(DyStats)]
+        L.dy_plan_get_stats.restype = ctypes.c_int
+        L.dy_plan_last_error.argtypes = [vp]
+        L.dy_plan_last_error.restype = ctypes.c_char_p
+        L.dy_status_str.argtypes = [ctypes.c_int]
+        L.dy_status_str.restype = ctypes.c_char_p
+        L.dy_abi_version.restype = i32
+        L.dy_selftest.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return int(x.data_ptr())
+    raise TypeError(f"cannot take a device pointer from {type(x)!r}")
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    if hasattr(s, "cuda_stream"):
+        return int(s.cuda_stream)
+    raise TypeError(f"cannot take a stream from {type(s)!r}")
+
+
+def range_source(problem: int, begin: int, count: int) -> DySource:
+    return DySource(DY_SOURCE_RANGE, problem, begin, count, None, 0, 0)
+
+
+def rows_source(problem: int, rows, count: int, row_stride: int, index_base: int = 0) -> DySource:
+    return DySource(DY_SOURCE_ROWS, problem, 0, count, _ptr(rows), row_stride, index_base)
+
+
+class _Arrays:
+    """Contiguous host copies kept alive while dy_plan_create reads them."""
+
+    def __init__(self, prob):
+        self.edges = np.ascontiguousarray(prob.edges, dtype=np.int32).reshape(-1, 2)
+        self.radix = np.ascontiguousarray(prob.radix, dtype=np.int32)
+        self.p = np.ascontiguousarray(prob.p, dtype=np.float32)
+        self.tau = np.ascontiguousarray(prob.tau, dtype=np.float32)
+        self.size = np.ascontiguousarray(prob.size, dtype=np.float32)
+        self.backend = np.ascontiguousarray(prob.backend, dtype=np.int32)
+        self.w = np.ascontiguousarray(prob.w, dtype=np.float32)
+        self.rho = np.ascontiguousarray(prob.rho, dtype=np.float32)
+        self.c = DyProblem(int(prob.n_nodes), int(self.edges.shape[0]),
+                           self.edges.ctypes.data if self.edges.size else None, self.radix.ctypes.data,
+                           int(self.p.shape[1]), self.p.ctypes.data, self.tau.ctypes.data, self.size.ctypes.data,
+                           self.backend.ctypes.data, self.w.ctypes.data, int(self.rho.shape[0]),
+                           int(self.rho.shape[1]), self.rho.ctypes.data, ctypes.c_float(float(prob.slo)))
+
+
+def create_raw(structs: Sequence[DyProblem], device: int = 0):
+    """dy_plan_create on prepared structs; returns (status, handle or None)."""
+    arr = (DyProblem * len(structs))(*structs)
+    h = ctypes.c_void_p()
+    st = lib().dy_plan_create(arr, len(structs), device, ctypes.byref(h))
+    return st, (h.value if st == DY_OK else None)
+
+
+def last_error(handle=None) -> str:
+    msg = lib().dy_plan_last_error(handle)
+    return msg.decode() if msg else ""
+
+
+class Plan:
+    """A handle over one or more planning problems staged on one device."""
+
+    def __init__(self, problems, device: int = 0):
+        probs = list(problems) if isinstance(problems, (list, tuple)) else [problems]
+        keep = [_Arrays(p) for p in probs]
+        st, h = create_raw([k.c for k in keep], device)
+        if st != DY_OK:
+            raise DyplanError(st, last_error(None))
+        self._h = h
+        self.n_levels = [int(p.rho.shape[0]) for p in probs]
+        self.kmax = int(lib().dy_plan_max_levels(h))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().dy_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def _check(self, st):
+        if st != DY_OK:
+            raise DyplanError(st, last_error(self._h))
+
+    def set_option(self, option: int, value: int):
+        self._check(lib().dy_plan_set_option(self._h, option, int(value)))
+
+    def select(self, sources: Sequence[DySource], stream=None) -> List[List[tuple]]:
+        """Per source, the K choices (index, feasible, corr, cp, demand)."""
+        srcs = (DySource * len(sources))(*sources)
+        out = (DyChoice * (len(sources) * self.kmax))()
+        self._check(lib().dy_plan_select(self._h, srcs, len(sources), out, _stream(stream)))
+        res = []
+        for j, s in enumerate(sources):
+            K = self.n_levels[s.problem]
+            res.append([out[j * self.kmax + k].as_tuple() for k in range(K)])
+        return res
+
+    def select_raw(self, srcs, n: int, out, stream=None) -> int:
+        """Unchecked call for timing loops: prepared ctypes arrays in and out."""
+        return lib().dy_plan_select(self._h, srcs, n, out, _stream(stream))
+
+    def score(self, source: DySource, corr=None, cp=None, demand=None, feas=None, stream=None):
+        self._check(lib().dy_plan_score(self._h, ctypes.byref(source), _ptr(corr), _ptr(cp), _ptr(demand),
+                                        _ptr(feas), _stream(stream)))
+
+    def stats(self) -> DyStats:
+        s = DyStats()
+        self._check(lib().dy_plan_get_stats(self._h, ctypes.byref(s)))
+        return s
