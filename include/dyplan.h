@@ -165,7 +165,7 @@ typedef struct dy_stats {
 /* Options for dy_plan_set_option. */
 enum {
     DY_OPT_TIMING = 1,          /* 1: record HIP events around the kernels of each call (default 0) */
-    DY_OPT_SAMPLE_STRIDE = 2,   /* 1 of every S work units scored by the seeding pre-pass (default 32) */
+    DY_OPT_SAMPLE_STRIDE = 2,   /* the seeding pre-pass scores 1 of every S work units (default 128) */
     DY_OPT_CAND_CAPACITY = 3,   /* candidate slots per source (default 1 << 16, min 16) */
     DY_OPT_FORCE_FP64 = 4       /* 1: decide every level with the exhaustive fp64 path (default 0) */
 };

@@ -12,6 +12,8 @@ constexpr int WG = 256;          // threads per workgroup of the scoring kernels
 constexpr int NMAX = DY_MAX_NODES;
 constexpr int KMAX = DY_MAX_LEVELS;
 constexpr int NBINS = 64;        // lane-resident prefilter table: one bin per lane
+constexpr int NSLOT = 64;        // per-level atomic slots of the seeding pass (spreads contention)
+constexpr int CERT_WAVES = 8;    // waves per source in certification when sources are few
 
 // Unsigned 32-bit division by an invariant divisor (Granlund & Montgomery,
 // PLDI 1994, Fig. 4.1): q = (t + ((x - t) >> sh1)) >> sh2, t = mulhi(m, x).
@@ -47,19 +49,22 @@ struct ProbDev {
     uint32_t cp_lo_bits, cp_hi_bits;  // fp32 bounds of the unpressured CP over all plans
     int32_t bin_shift;        // prefilter bin = (bits(CP) >> bin_shift) mod 64
     int32_t pad0;
+    // seeding pass (uniform mode): levels sorted by lo (descending); for a CP
+    // in bin j, jtab[j] levels of that order are certainly feasible (a lower
+    // bound: the bin's largest CP decides)
+    uint32_t jtab[NBINS];
+    int32_t lvl_order[KMAX];
     // device tables
     const float2* at;         // [n][rmax] (factor a = 1 - w(1-p), duration tau), fp32
     const float2* atx;        // rows of x and y in `at` (x: a 1-entry (1, 0) row when virtual)
     const float2* aty;
     const float* dem;         // [n][rmax] demand term tau * size, fp32
     const float* lat;         // general mode: [k][n][rmax] fp32 tau / (1 - rho_{k,b})
-    // raw inputs, for the fp64 re-evaluation
-    const float* p;
-    const float* tau;
-    const float* size;
-    const float* w;
-    const float* rho;         // [k][b]
-    const int32_t* bk;        // [n][rmax]
+    // fp64 terms of the definition, each rounded exactly as the definition
+    // writes it (the re-evaluation only multiplies, adds and compares them)
+    const double* a64;        // [n][rmax] 1 - w (1 - p)
+    const double* lat64;      // [k][n][rmax] tau / (1 - rho_{k,b})
+    const double* dem64;      // [n][rmax] tau * size
 };
 
 struct Cand {
@@ -83,7 +88,7 @@ struct JobDev {
     uint64_t units;           // work units of the main kernel (blocks for the sweep, plans otherwise)
     uint32_t sample_stride;
     uint32_t cap;             // candidate slots
-    uint32_t* scert;          // [KMAX] best certainly-feasible fp32 corr found by the pre-pass, bits + 1 (0: none)
+    uint32_t* scert;          // [KMAX][NSLOT] best certainly-feasible fp32 corr found by the pre-pass, bits + 1 (0: none)
     float* thr;               // [KMAX] candidate thresholds
     uint32_t* table;          // [NBINS] prefilter thresholds (fp32 bits)
     Cand* cand;               // [cap]
@@ -93,7 +98,11 @@ struct JobDev {
     uint64_t* fb_corr;        // [KMAX] exhaustive fp64 path: best corr bits
     uint64_t* fb_index;       // [KMAX] exhaustive fp64 path: lowest index at that corr
     uint32_t fb_levels;       // exhaustive path: bit mask of levels to decide
-    int32_t pad1;
+    int32_t cert_waves;       // waves of certification for this source
+    double* cert_c;           // [KMAX][CERT_WAVES] per-wave best fp64 corr of certification
+    uint64_t* cert_i;         // [KMAX][CERT_WAVES] its index
+    double* cert_cp;          // [KMAX][CERT_WAVES] its fp64 CP at the level
+    double* cert_d;           // [KMAX][CERT_WAVES] its fp64 demand
 };
 
 }  // namespace dyp

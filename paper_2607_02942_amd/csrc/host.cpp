@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <new>
 #include <string>
 #include <vector>
@@ -22,8 +23,9 @@ hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, hipStream_t s);
 hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, hipStream_t s);
 hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStream_t s);
-hipError_t launch_certify(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s);
+hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, hipStream_t s);
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
+hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
                         hipStream_t s);
 }  // namespace dyp
@@ -35,7 +37,8 @@ namespace {
 thread_local std::string g_create_error;
 
 constexpr uint64_t kMaxSourcePlans = 1ull << 40;
-constexpr size_t kCandPoolBytes = 256ull << 20;  // candidate slots shared by the sources of one call
+constexpr size_t kCandPoolBytes = 1ull << 30;    // candidate slots shared by the sources of one call
+constexpr uint64_t kMinSamples = 4096;           // the adaptive stride keeps at least this many samples
 constexpr double kU = 0x1p-24;                    // fp32 unit roundoff
 
 struct HostProb {
@@ -62,13 +65,20 @@ struct Scratch {
     dy_choice* out = nullptr;
     uint64_t* fb_corr = nullptr;
     uint64_t* fb_index = nullptr;
+    double* cert_c = nullptr;
+    uint64_t* cert_i = nullptr;
+    double* cert_cp = nullptr;
+    double* cert_d = nullptr;
     Cand* cand = nullptr;
+    size_t res_bytes = 0;       // out, ncand and flags are one contiguous region (one copy back)
     // pinned host mirrors
-    JobDev* h_jobs = nullptr;
+    JobDev* h_jobs = nullptr;   // the job array last uploaded
     JobDev* h_fb = nullptr;
+    char* h_res = nullptr;
     dy_choice* h_out = nullptr;
     uint32_t* h_ncand = nullptr;
     int32_t* h_flags = nullptr;
+    size_t uploaded = 0;        // jobs of h_jobs present on the device (0: none)
 };
 
 uint32_t f2u(float f) {
@@ -217,7 +227,8 @@ struct dy_plan {
     ProbDev* d_probs = nullptr;
     Scratch sc;
     int timing = 0;
-    uint32_t sample_stride = 32;
+    uint32_t sample_stride = 128;   // upper bound of the adaptive stride, or the fixed stride when set
+    bool stride_fixed = false;
     uint32_t cand_cap = 1u << 16;
     int force_fp64 = 0;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
@@ -248,9 +259,7 @@ void free_scratch(Scratch& s) {
     if (s.d) (void)hipFree(s.d);
     if (s.h_jobs) (void)hipHostFree(s.h_jobs);
     if (s.h_fb) (void)hipHostFree(s.h_fb);
-    if (s.h_out) (void)hipHostFree(s.h_out);
-    if (s.h_ncand) (void)hipHostFree(s.h_ncand);
-    if (s.h_flags) (void)hipHostFree(s.h_flags);
+    if (s.h_res) (void)hipHostFree(s.h_res);
     s = Scratch{};
 }
 
@@ -267,12 +276,18 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
     };
     size_t o_jobs = take(njobs * sizeof(JobDev));
     size_t o_fb = take(njobs * sizeof(JobDev));
-    size_t o_scert = take(njobs * KMAX * sizeof(uint32_t));
+    size_t o_scert = take(njobs * KMAX * NSLOT * sizeof(uint32_t));
+    size_t o_cc = take(njobs * KMAX * CERT_WAVES * sizeof(double));
+    size_t o_ci = take(njobs * KMAX * CERT_WAVES * sizeof(uint64_t));
+    size_t o_cp = take(njobs * KMAX * CERT_WAVES * sizeof(double));
+    size_t o_cd = take(njobs * KMAX * CERT_WAVES * sizeof(double));
     size_t o_thr = take(njobs * KMAX * sizeof(float));
     size_t o_table = take(njobs * NBINS * sizeof(uint32_t));
-    size_t o_ncand = take(njobs * sizeof(uint32_t));
-    size_t o_flags = take(njobs * sizeof(int32_t));
-    size_t o_out = take(njobs * km * sizeof(dy_choice));
+    const size_t res_out = 0;
+    const size_t res_ncand = align_up(njobs * km * sizeof(dy_choice), 8);
+    const size_t res_flags = res_ncand + njobs * sizeof(uint32_t);
+    const size_t res_bytes = res_flags + njobs * sizeof(int32_t);
+    size_t o_res = take(res_bytes);
     size_t o_fbc = take(njobs * KMAX * sizeof(uint64_t));
     size_t o_fbi = take(njobs * KMAX * sizeof(uint64_t));
     size_t o_cand = take(njobs * (size_t)cap * sizeof(Cand));
@@ -288,29 +303,36 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
     s.d_jobs = (JobDev*)(s.d + o_jobs);
     s.d_fb = (JobDev*)(s.d + o_fb);
     s.scert = (uint32_t*)(s.d + o_scert);
+    s.cert_c = (double*)(s.d + o_cc);
+    s.cert_i = (uint64_t*)(s.d + o_ci);
+    s.cert_cp = (double*)(s.d + o_cp);
+    s.cert_d = (double*)(s.d + o_cd);
     s.thr = (float*)(s.d + o_thr);
     s.table = (uint32_t*)(s.d + o_table);
-    s.ncand = (uint32_t*)(s.d + o_ncand);
-    s.flags = (int32_t*)(s.d + o_flags);
-    s.out = (dy_choice*)(s.d + o_out);
+    s.res_bytes = res_bytes;
+    s.out = (dy_choice*)(s.d + o_res + res_out);
+    s.ncand = (uint32_t*)(s.d + o_res + res_ncand);
+    s.flags = (int32_t*)(s.d + o_res + res_flags);
     s.fb_corr = (uint64_t*)(s.d + o_fbc);
     s.fb_index = (uint64_t*)(s.d + o_fbi);
     s.cand = (Cand*)(s.d + o_cand);
     if ((e = hipHostMalloc((void**)&s.h_jobs, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
         (e = hipHostMalloc((void**)&s.h_fb, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
-        (e = hipHostMalloc((void**)&s.h_out, njobs * km * sizeof(dy_choice), hipHostMallocDefault)) != hipSuccess ||
-        (e = hipHostMalloc((void**)&s.h_ncand, njobs * sizeof(uint32_t), hipHostMallocDefault)) != hipSuccess ||
-        (e = hipHostMalloc((void**)&s.h_flags, njobs * sizeof(int32_t), hipHostMallocDefault)) != hipSuccess) {
+        (e = hipHostMalloc((void**)&s.h_res, res_bytes, hipHostMallocDefault)) != hipSuccess) {
         free_scratch(s);
         return hip_fail(&h->err, e, "hipHostMalloc(scratch)");
     }
+    s.h_out = (dy_choice*)(s.h_res + res_out);
+    s.h_ncand = (uint32_t*)(s.h_res + res_ncand);
+    s.h_flags = (int32_t*)(s.h_res + res_flags);
+    s.uploaded = 0;
     return DY_OK;
 }
 
 // Builds the device image of every problem: ProbDev descriptors + tables.
 int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::string* err) {
     struct Layout {
-        size_t at, atx, dem, lat, p, tau, size, w, rho, bk;
+        size_t at, atx, dem, lat, a64, lat64, dem64;
     };
     std::vector<Layout> lay(n_probs);
     size_t off = align_up((size_t)n_probs * sizeof(ProbDev), 256);
@@ -328,13 +350,10 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         L.at = take(NR * sizeof(float2));
         L.atx = take(sizeof(float2));
         L.dem = take(NR * sizeof(float));
-        L.p = take(NR * sizeof(float));
-        L.tau = take(NR * sizeof(float));
-        L.size = take(NR * sizeof(float));
-        L.w = take((size_t)pb.n_nodes * sizeof(float));
-        L.rho = take((size_t)pb.n_levels * pb.n_backends * sizeof(float));
-        L.bk = take(NR * sizeof(int32_t));
         L.lat = take((size_t)pb.n_levels * NR * sizeof(float));
+        L.a64 = take(NR * sizeof(double));
+        L.lat64 = take((size_t)pb.n_levels * NR * sizeof(double));
+        L.dem64 = take(NR * sizeof(double));
         h->kmax = std::max(h->kmax, pb.n_levels);
     }
     std::vector<char> img(off, 0);
@@ -434,6 +453,9 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         float2* at = (float2*)(img.data() + L.at);
         float* dem = (float*)(img.data() + L.dem);
         float* lat = (float*)(img.data() + L.lat);
+        double* a64 = (double*)(img.data() + L.a64);
+        double* lat64 = (double*)(img.data() + L.lat64);
+        double* dem64 = (double*)(img.data() + L.dem64);
         float dmin[DY_MAX_NODES], dmax[DY_MAX_NODES];
         for (int n = 0; n < N; ++n) {
             double w = (double)pb.w[n];
@@ -441,28 +463,28 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
             dmax[n] = 0.0f;
             for (int i = 0; i < pb.radix[n]; ++i) {
                 size_t e2 = (size_t)n * R + i;
+                // the definition's per-node terms in fp64, operation by operation
                 double t = 1.0 - (double)pb.p[e2];
                 t = w * t;
-                float a = (float)(1.0 - t);
-                float tau = pb.tau[e2] == 0.0f ? 0.0f : pb.tau[e2];
-                at[e2] = make_float2(a, tau);
-                dem[e2] = (float)((double)tau * (double)pb.size[e2]);
+                const double a = 1.0 - t;
+                const float tau = pb.tau[e2] == 0.0f ? 0.0f : pb.tau[e2];
+                const double d = (double)tau * (double)pb.size[e2];
+                a64[e2] = a;
+                dem64[e2] = d;
+                at[e2] = make_float2((float)a, tau);
+                dem[e2] = (float)d;
                 dmin[n] = std::min(dmin[n], tau);
                 dmax[n] = std::max(dmax[n], tau);
                 for (int k = 0; k < K; ++k) {
-                    double r = (double)pb.rho[k * B + pb.backend[e2]];
-                    lat[(size_t)k * N * R + e2] = (float)((double)tau / (1.0 - r));
+                    const double r = (double)pb.rho[k * B + pb.backend[e2]];
+                    const double l = (double)tau / (1.0 - r);
+                    lat64[(size_t)k * N * R + e2] = l;
+                    lat[(size_t)k * N * R + e2] = (float)l;
                 }
             }
         }
         float2* atx = (float2*)(img.data() + L.atx);
         *atx = make_float2(1.0f, 0.0f);
-        std::memcpy(img.data() + L.p, pb.p, (size_t)N * R * sizeof(float));
-        std::memcpy(img.data() + L.tau, pb.tau, (size_t)N * R * sizeof(float));
-        std::memcpy(img.data() + L.size, pb.size, (size_t)N * R * sizeof(float));
-        std::memcpy(img.data() + L.w, pb.w, (size_t)N * sizeof(float));
-        std::memcpy(img.data() + L.rho, pb.rho, (size_t)K * B * sizeof(float));
-        std::memcpy(img.data() + L.bk, pb.backend, (size_t)N * R * sizeof(int32_t));
         // fp32 bounds of the unpressured CP (the recurrence is monotone in every duration)
         const float clo = cp32(N, D.pred, D.sinks, dmin);
         const float chi = cp32(N, D.pred, D.sinks, dmax);
@@ -471,18 +493,34 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         int s = 2;
         while (s < 31 && ((D.cp_hi_bits >> s) - (D.cp_lo_bits >> s)) > 62u) ++s;
         D.bin_shift = s;
+        // seeding pass: levels by decreasing band, and per bin how many of them
+        // every CP in the bin certainly meets (decided by the bin's largest CP)
+        std::vector<int> order(K);
+        for (int k = 0; k < K; ++k) order[k] = k;
+        std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return D.lo[x] > D.lo[y]; });
+        for (int k = 0; k < K; ++k) D.lvl_order[k] = order[k];
+        const uint32_t blo = D.cp_lo_bits >> s;
+        for (int lane = 0; lane < NBINS; ++lane) {
+            const uint64_t B = blo + (((uint32_t)lane - blo) & 63u);
+            uint64_t top = ((B + 1) << s) - 1;
+            if (top > 0x7f7fffffull) top = 0x7f7fffffull;
+            float U;
+            const uint32_t tb = (uint32_t)top;
+            std::memcpy(&U, &tb, 4);
+            uint32_t j = 0;
+            for (int k = 0; k < K; ++k)
+                if (D.lo[k] >= U) ++j;
+            D.jtab[lane] = j;
+        }
         char* base = h->d_arena;
         D.at = (const float2*)(base + L.at);
         D.atx = N >= 2 ? (const float2*)(base + L.at) + (size_t)(N - 2) * R : (const float2*)(base + L.atx);
         D.aty = (const float2*)(base + L.at) + (size_t)(N - 1) * R;
         D.dem = (const float*)(base + L.dem);
         D.lat = (const float*)(base + L.lat);
-        D.p = (const float*)(base + L.p);
-        D.tau = (const float*)(base + L.tau);
-        D.size = (const float*)(base + L.size);
-        D.w = (const float*)(base + L.w);
-        D.rho = (const float*)(base + L.rho);
-        D.bk = (const int32_t*)(base + L.bk);
+        D.a64 = (const double*)(base + L.a64);
+        D.lat64 = (const double*)(base + L.lat64);
+        D.dem64 = (const double*)(base + L.dem64);
         H.n = N;
         H.k = K;
         H.b = B;
@@ -633,6 +671,7 @@ int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value) {
         case DY_OPT_SAMPLE_STRIDE:
             if (value < 1 || value > (1 << 30)) break;
             h->sample_stride = (uint32_t)value;
+            h->stride_fixed = true;
             return DY_OK;
         case DY_OPT_CAND_CAPACITY:
             if (value < 16 || value > (1 << 26)) break;
@@ -653,7 +692,62 @@ int dy_plan_get_stats(const dy_plan* h, dy_stats* out) {
     return DY_OK;
 }
 
-int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The kernel family that scores a source.
+enum Group { G_SWEEP = 0, G_SWEEP_S2 = 1, G_GENERIC = 2 };
+
+struct PassPlan {
+    int n[3] = {0, 0, 0};                 // sources per group, stored in group order
+    uint64_t units[3] = {0, 0, 0};        // largest main-pass work of the group
+    uint64_t samples[3] = {0, 0, 0};      // largest seeding-pass work of the group
+    int npre[2] = {0, 0};
+};
+
+// Launch the scoring passes for `n` jobs stored in group order at d.
+// seed: run the seeding pre-pass (otherwise the seeds are already in place).
+void launch_passes(const JobDev* d, const PassPlan& pp, bool seed, hipStream_t s,
+                   const std::function<void(hipError_t, const char*)>& chk) {
+    auto chunks = [&](const JobDev* base, int n, auto&& fn) {
+        for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
+    };
+    const JobDev* gbase[3] = {d, d + pp.n[0], d + pp.n[0] + pp.n[1]};
+    const int ntot = pp.n[0] + pp.n[1] + pp.n[2];
+    if (seed) {
+        for (int g = 0; g < 2; ++g)
+            chunks(gbase[g], pp.n[g], [&](const JobDev* b, int n) {
+                chk(launch_sample_sweep(b, n, g == 1, pp.samples[g], pp.npre[g], s), "sample");
+            });
+        chunks(gbase[2], pp.n[2],
+               [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, pp.samples[2], s), "sample"); });
+    }
+    chunks(d, ntot, [&](const JobDev* b, int n) { chk(launch_table(const_cast<JobDev*>(b), n, s), "table"); });
+}
+
+void launch_main(const JobDev* d, const PassPlan& pp, hipStream_t s,
+                 const std::function<void(hipError_t, const char*)>& chk) {
+    auto chunks = [&](const JobDev* base, int n, auto&& fn) {
+        for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
+    };
+    const JobDev* gbase[3] = {d, d + pp.n[0], d + pp.n[0] + pp.n[1]};
+    for (int g = 0; g < 2; ++g)
+        chunks(gbase[g], pp.n[g], [&](const JobDev* b, int n) {
+            chk(launch_sweep(b, n, g == 1, pp.units[g], pp.npre[g], s), "sweep");
+        });
+    chunks(gbase[2], pp.n[2], [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[2], s), "scan"); });
+}
+
+void launch_certify_all(const JobDev* d, int ntot, int cert_waves, hipStream_t s,
+                        const std::function<void(hipError_t, const char*)>& chk) {
+    for (int c = 0; c < ntot; c += 65535)
+        chk(launch_certify(d + c, std::min(65535, ntot - c), cert_waves, s), "certify");
+}
+
+}  // namespace
+
+extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream) {
     if (!h) return DY_EINVAL;
     if (!src || !out || n_src < 1) {
         h->err = "src/out is NULL or n_src < 1";
@@ -663,8 +757,8 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
         int st = check_source(h, src[j], j, &h->err);
         if (st != DY_OK) return st;
     }
-    DeviceGuard g(h->device);
-    if (!g.ok) {
+    DeviceGuard guard(h->device);
+    if (!guard.ok) {
         h->err = "hipSetDevice failed";
         return DY_EDEVICE;
     }
@@ -677,29 +771,28 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
     if (st != DY_OK) return st;
     Scratch& S = h->sc;
     const int km = h->kmax;
+    const int cert_waves = n_src <= 64 ? CERT_WAVES : 1;
 
-    // order: sweep without S2, sweep with S2, generic
+    auto group_of = [&](int j) {
+        const HostProb& H = h->hp[src[j].problem];
+        const bool sweep = src[j].kind == DY_SOURCE_RANGE && H.uniform;
+        return sweep ? (H.has_s2 ? G_SWEEP_S2 : G_SWEEP) : G_GENERIC;
+    };
     std::vector<int> order;
     order.reserve(n_src);
-    int n_sweep[2] = {0, 0};
-    uint64_t sweep_units[2] = {0, 0}, sweep_samples[2] = {0, 0};
-    int sweep_npre[2] = {0, 0};
-    uint64_t gen_units = 0, gen_samples = 0, all_units = 0;
-    for (int pass = 0; pass < 3; ++pass)
-        for (int j = 0; j < n_src; ++j) {
-            const HostProb& H = h->hp[src[j].problem];
-            const bool sweep = !h->force_fp64 && src[j].kind == DY_SOURCE_RANGE && H.uniform;
-            const int grp = sweep ? (H.has_s2 ? 1 : 0) : 2;
-            if (grp != pass) continue;
-            order.push_back(j);
-        }
-    uint64_t plans = 0;
+    for (int g = 0; g < 3; ++g)
+        for (int j = 0; j < n_src; ++j)
+            if (group_of(j) == g) order.push_back(j);
+    uint64_t plans = 0, all_units = 0;
+    PassPlan pp;
+    std::vector<JobDev> jobs((size_t)n_src);
     for (int q = 0; q < n_src; ++q) {
         const int j = order[q];
+        const int g = group_of(j);
         const HostProb& H = h->hp[src[j].problem];
         JobDev J = make_job(h, src[j]);
         J.cap = (uint32_t)cap;
-        J.scert = S.scert + (size_t)q * KMAX;
+        J.scert = S.scert + (size_t)q * KMAX * NSLOT;
         J.thr = S.thr + (size_t)q * KMAX;
         J.table = S.table + (size_t)q * NBINS;
         J.cand = S.cand + (size_t)q * cap;
@@ -708,67 +801,58 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
         J.out = S.out + (size_t)j * km;
         J.fb_corr = S.fb_corr + (size_t)q * KMAX;
         J.fb_index = S.fb_index + (size_t)q * KMAX;
+        J.cert_waves = cert_waves;
+        J.cert_c = S.cert_c + (size_t)q * KMAX * CERT_WAVES;
+        J.cert_i = S.cert_i + (size_t)q * KMAX * CERT_WAVES;
+        J.cert_cp = S.cert_cp + (size_t)q * KMAX * CERT_WAVES;
+        J.cert_d = S.cert_d + (size_t)q * KMAX * CERT_WAVES;
         J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
-        const bool sweep = !h->force_fp64 && src[j].kind == DY_SOURCE_RANGE && H.uniform;
-        if (sweep) {
-            const int gi = H.has_s2 ? 1 : 0;
-            J.units = J.nblk;
-            ++n_sweep[gi];
-            sweep_units[gi] = std::max(sweep_units[gi], J.nblk);
-            sweep_samples[gi] = std::max(sweep_samples[gi], (J.nblk + h->sample_stride - 1) / h->sample_stride);
-            sweep_npre[gi] = std::max(sweep_npre[gi], H.npre);
-        } else {
-            J.units = J.count;
-            gen_units = std::max(gen_units, J.count);
-            gen_samples = std::max(gen_samples, (J.count + h->sample_stride - 1) / h->sample_stride);
-        }
+        // seeding work units: rows of the inner sweep, or plans
+        const uint64_t sunits = g == G_GENERIC ? J.count : J.nblk * (uint64_t)H.rx;
+        uint64_t stride = h->sample_stride;
+        if (!h->stride_fixed) stride = std::max<uint64_t>(1, std::min<uint64_t>(stride, sunits / kMinSamples));
+        J.sample_stride = (uint32_t)stride;
+        J.units = g == G_GENERIC ? J.count : J.nblk;
+        ++pp.n[g];
+        pp.units[g] = std::max(pp.units[g], J.units);
+        pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
+        if (g != G_GENERIC) pp.npre[g] = std::max(pp.npre[g], H.npre);
         all_units = std::max(all_units, J.count);
         plans += J.count;
-        S.h_jobs[q] = J;
+        jobs[q] = J;
     }
-    const int n_gen = n_src - n_sweep[0] - n_sweep[1];
-    hipError_t e = hipMemcpyAsync(S.d_jobs, S.h_jobs, (size_t)n_src * sizeof(JobDev), hipMemcpyHostToDevice, s);
-    if (e != hipSuccess) return hip_fail(&h->err, e, "hipMemcpyAsync(jobs)");
-    const JobDev* jA = S.d_jobs;
-    const JobDev* jB = S.d_jobs + n_sweep[0];
-    const JobDev* jG = S.d_jobs + n_sweep[0] + n_sweep[1];
-    auto chk = [&](hipError_t x, const char* what) {
+    // the job array is rebuilt every call but uploaded only when it changed
+    if (S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0) {
+        hipError_t e = hipStreamSynchronize(s);  // a previous upload may still read the pinned buffer
+        if (e == hipSuccess) {
+            std::memcpy(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev));
+            e = hipMemcpyAsync(S.d_jobs, S.h_jobs, (size_t)n_src * sizeof(JobDev), hipMemcpyHostToDevice, s);
+        }
+        if (e != hipSuccess) {
+            S.uploaded = 0;
+            return hip_fail(&h->err, e, "hipMemcpyAsync(jobs)");
+        }
+        S.uploaded = (size_t)n_src;
+    }
+    std::function<void(hipError_t, const char*)> chk = [&](hipError_t x, const char* what) {
         if (x != hipSuccess && st == DY_OK) st = hip_fail(&h->err, x, what);
     };
-    // kernels take at most 65535 sources per launch along y
-    auto chunks = [&](const JobDev* base, int n, auto&& fn) {
-        for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
-    };
     if (h->timing) chk(hipEventRecord(h->ev[0], s), "hipEventRecord");
-    chunks(S.d_jobs, n_src, [&](const JobDev* b, int n) { chk(launch_init(const_cast<JobDev*>(b), n, s), "init"); });
+    for (int c = 0; c < n_src; c += 65535) chk(launch_init(S.d_jobs + c, std::min(65535, n_src - c), s), "init");
     if (!h->force_fp64) {
-        for (int gi = 0; gi < 2; ++gi) {
-            const JobDev* base = gi ? jB : jA;
-            chunks(base, n_sweep[gi], [&](const JobDev* b, int n) {
-                chk(launch_sample_sweep(b, n, gi == 1, sweep_samples[gi], sweep_npre[gi], s), "sample");
-            });
-        }
-        chunks(jG, n_gen, [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, gen_samples, s), "sample"); });
-        chunks(S.d_jobs, n_src, [&](const JobDev* b, int n) { chk(launch_table(const_cast<JobDev*>(b), n, s), "table"); });
+        launch_passes(S.d_jobs, pp, true, s, chk);
         if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
-        for (int gi = 0; gi < 2; ++gi) {
-            const JobDev* base = gi ? jB : jA;
-            chunks(base, n_sweep[gi], [&](const JobDev* b, int n) {
-                chk(launch_sweep(b, n, gi == 1, sweep_units[gi], sweep_npre[gi], s), "sweep");
-            });
-        }
-        chunks(jG, n_gen, [&](const JobDev* b, int n) { chk(launch_scan(b, n, gen_units, s), "scan"); });
+        launch_main(S.d_jobs, pp, s, chk);
         if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
-        chunks(S.d_jobs, n_src, [&](const JobDev* b, int n) { chk(launch_certify(b, n, km, s), "certify"); });
+        launch_certify_all(S.d_jobs, n_src, cert_waves, s, chk);
     } else {
         if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
-        chunks(S.d_jobs, n_src, [&](const JobDev* b, int n) { chk(launch_exhaust(b, n, all_units, s), "exhaust"); });
+        for (int c = 0; c < n_src; c += 65535)
+            chk(launch_exhaust(S.d_jobs + c, std::min(65535, n_src - c), all_units, s), "exhaust");
         if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
     }
     if (h->timing) chk(hipEventRecord(h->ev[3], s), "hipEventRecord");
-    chk(hipMemcpyAsync(S.h_out, S.out, (size_t)n_src * km * sizeof(dy_choice), hipMemcpyDeviceToHost, s), "copy out");
-    chk(hipMemcpyAsync(S.h_ncand, S.ncand, (size_t)n_src * sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy out");
-    chk(hipMemcpyAsync(S.h_flags, S.flags, (size_t)n_src * sizeof(int32_t), hipMemcpyDeviceToHost, s), "copy out");
+    chk(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, s), "copy out");
     chk(hipStreamSynchronize(s), "hipStreamSynchronize");
     if (st != DY_OK) return st;
 
@@ -780,34 +864,61 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
         if (hipEventElapsedTime(&ms, h->ev[1], h->ev[2]) == hipSuccess) stats.main_ms = ms;
         if (hipEventElapsedTime(&ms, h->ev[0], h->ev[3]) == hipSuccess) stats.total_ms = ms;
     }
-    // fallback for sources whose candidate list overflowed
-    int n_fb = 0;
-    uint64_t fb_units = 0;
+    if (h->force_fp64)
+        for (int j = 0; j < n_src; ++j) stats.fallbacks += h->hp[src[j].problem].k;
     for (int q = 0; q < n_src; ++q) {
-        const int32_t fl = S.h_flags[q];
         stats.candidates += std::min<uint64_t>(S.h_ncand[q], cap);
-        if (fl & JF_BAD_ROW) {
+        if (S.h_flags[q] & JF_BAD_ROW) {
             h->err = "a row holds an implementation id >= radix of its node";
             return DY_EINVAL;
         }
-        if ((fl & JF_OVERFLOW) && !h->force_fp64) {
-            JobDev J = S.h_jobs[q];
-            const int K = h->hp[src[order[q]].problem].k;
-            J.fb_levels = K == 32 ? 0xffffffffu : ((1u << K) - 1u);
-            S.h_fb[n_fb++] = J;
-            fb_units = std::max(fb_units, J.count);
-            stats.fallbacks += K;
-        }
     }
-    if (h->force_fp64)
-        for (int j = 0; j < n_src; ++j) stats.fallbacks += h->hp[src[j].problem].k;
-    if (n_fb > 0) {
+    // candidate-list overflow: reseed from the gathered candidates and score
+    // those sources again (each round raises the thresholds); whatever still
+    // overflows after kReseedRounds is decided exhaustively
+    constexpr int kReseedRounds = 3;
+    for (int round = 0; round <= kReseedRounds && !h->force_fp64; ++round) {
+        PassPlan rp;
+        int n_fb = 0;
+        uint64_t fb_units = 0;
+        for (int g = 0; g < 3; ++g)
+            for (int q = 0; q < n_src; ++q) {
+                if (!(S.h_flags[q] & JF_OVERFLOW)) continue;
+                const int j = order[q];
+                if (group_of(j) != g) continue;
+                const HostProb& H = h->hp[src[j].problem];
+                JobDev J = jobs[q];
+                if (round < kReseedRounds && H.uniform) {
+                    ++rp.n[g];
+                    rp.units[g] = std::max(rp.units[g], J.units);
+                    if (g != G_GENERIC) rp.npre[g] = std::max(rp.npre[g], H.npre);
+                } else {
+                    J.fb_levels = H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u);
+                    stats.fallbacks += H.k;
+                    fb_units = std::max(fb_units, J.count);
+                }
+                S.h_fb[n_fb++] = J;
+            }
+        if (n_fb == 0) break;
         chk(hipMemcpyAsync(S.d_fb, S.h_fb, (size_t)n_fb * sizeof(JobDev), hipMemcpyHostToDevice, s), "copy fb");
-        chunks(S.d_fb, n_fb, [&](const JobDev* b, int n) { chk(launch_exhaust(b, n, fb_units, s), "exhaust"); });
-        chk(hipMemcpyAsync(S.h_out, S.out, (size_t)n_src * km * sizeof(dy_choice), hipMemcpyDeviceToHost, s),
-            "copy out");
+        const int n_re = rp.n[0] + rp.n[1] + rp.n[2];
+        if (n_re > 0) {  // every overflowing uniform source is rescored
+            for (int c = 0; c < n_re; c += 65535) chk(launch_reseed(S.d_fb + c, std::min(65535, n_re - c), s), "reseed");
+            launch_passes(S.d_fb, rp, false, s, chk);
+            launch_main(S.d_fb, rp, s, chk);
+            launch_certify_all(S.d_fb, n_re, cert_waves, s, chk);
+        }
+        if (n_fb > n_re) {
+            const JobDev* b = S.d_fb + n_re;
+            for (int c = 0; c < n_fb - n_re; c += 65535)
+                chk(launch_exhaust(b + c, std::min(65535, n_fb - n_re - c), fb_units, s), "exhaust");
+        }
+        chk(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, s), "copy out");
         chk(hipStreamSynchronize(s), "hipStreamSynchronize");
         if (st != DY_OK) return st;
+        if (n_re == 0) break;
+        stats.candidates = 0;
+        for (int q = 0; q < n_src; ++q) stats.candidates += std::min<uint64_t>(S.h_ncand[q], cap);
     }
     for (int j = 0; j < n_src; ++j) {
         const int K = h->hp[src[j].problem].k;
@@ -816,6 +927,8 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
     h->stats = stats;
     return DY_OK;
 }
+
+extern "C" {
 
 int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, float* demand, uint32_t* feas_bits,
                   void* stream) {

@@ -79,63 +79,67 @@ __device__ __forceinline__ float cand_threshold(float s, int n) {
     return __double2float_rd(t);
 }
 
-// ---- fp64 re-evaluation (the definition, node order, no FMA contraction) ----
+// ---- fp64 re-evaluation ------------------------------------------------------
+// The per-node terms (1 - w(1-p), tau/(1-rho), tau*size) are precomputed on the
+// host in fp64 with the same operations as the definition, so the products,
+// sums and maxima below reproduce an fp64 evaluation of the definition in
+// node order bit for bit.  ids / f are strided per-thread columns.
 
-__device__ double ex_corr(PD P, const uint8_t* ids) {
+__device__ double ex_corr(PD P, const uint8_t* ids, int is) {
+    const CS double* a = cs(P->a64);
     double c = 1.0;
-    for (int n = 0; n < P->n; ++n) {
-        double p = (double)P->p[n * P->rmax + ids[n]];
-        double w = (double)P->w[n];
-        double t = 1.0 - p;
-        t = w * t;
-        c = c * (1.0 - t);
-    }
+    for (int n = 0; n < P->n; ++n) c = c * a[n * P->rmax + ids[n * is]];
     return c;
 }
 
-__device__ double ex_cp(PD P, const uint8_t* ids, int k) {
-    double f[NMAX];
+__device__ double ex_cp(PD P, const uint8_t* ids, int is, int k, double* f, int fs) {
+    const CS double* lat = cs(P->lat64) + (size_t)k * P->n * P->rmax;
     double cp = 0.0;
     for (int n = 0; n < P->n; ++n) {
-        int e = n * P->rmax + ids[n];
-        double rho = (double)P->rho[k * P->b + P->bk[e]];
-        double lat = (double)P->tau[e] / (1.0 - rho);
         double m = 0.0;
         uint32_t pm = P->pred[n];
         while (pm) {
-            int u = __builtin_ctz(pm);
+            const int u = __builtin_ctz(pm);
             pm &= pm - 1;
-            if (f[u] > m) m = f[u];
+            const double fu = f[u * fs];
+            if (fu > m) m = fu;
         }
-        f[n] = lat + m;
-        if ((P->sinks >> n & 1u) && f[n] > cp) cp = f[n];
+        const double fn = lat[n * P->rmax + ids[n * is]] + m;
+        f[n * fs] = fn;
+        if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
     }
     return cp;
 }
 
-__device__ double ex_demand(PD P, const uint8_t* ids) {
+__device__ double ex_demand(PD P, const uint8_t* ids, int is) {
+    const CS double* d64 = cs(P->dem64);
     double d = 0.0;
-    for (int n = 0; n < P->n; ++n) {
-        int e = n * P->rmax + ids[n];
-        d = d + (double)P->tau[e] * (double)P->size[e];
-    }
+    for (int n = 0; n < P->n; ++n) d = d + d64[n * P->rmax + ids[n * is]];
     return d;
 }
 
 // Implementation ids of plan `index` of the problem (node N-1 least significant).
-__device__ void decode64(PD P, uint64_t index, uint8_t* ids) {
+__device__ void decode64(PD P, uint64_t index, uint8_t* ids, int is) {
+    if (index <= 0xffffffffull) {
+        uint32_t x = (uint32_t)index;
+        for (int n = P->n - 1; n >= 0; --n) {
+            const uint32_t q = mdiv(x, P->rmag[n]);
+            ids[n * is] = (uint8_t)(x - q * (uint32_t)P->radix[n]);
+            x = q;
+        }
+        return;
+    }
     for (int n = P->n - 1; n >= 0; --n) {
-        uint64_t r = (uint64_t)P->radix[n];
-        ids[n] = (uint8_t)(index % r);
+        const uint64_t r = (uint64_t)P->radix[n];
+        ids[n * is] = (uint8_t)(index % r);
         index /= r;
     }
 }
 
 // ids of a candidate or of a fallback unit; returns false for a bad row id
-__device__ bool job_ids(JD J, PD P, uint64_t index,
-                        uint8_t* ids) {
+__device__ bool job_ids(JD J, PD P, uint64_t index, uint8_t* ids, int is) {
     if (J->kind == DY_SOURCE_RANGE) {
-        decode64(P, index, ids);
+        decode64(P, index, ids, is);
         return true;
     }
     const uint8_t* row = J->rows + (index - J->index_base) * J->stride;
@@ -146,7 +150,7 @@ __device__ bool job_ids(JD J, PD P, uint64_t index,
             ok = false;
             v = 0;
         }
-        ids[n] = v;
+        ids[n * is] = v;
     }
     return ok;
 }
@@ -180,8 +184,8 @@ __global__ void k_init(JobDev* __restrict__ jobs, int njobs) {
     if (j >= njobs) return;
     JD J = cs(jobs + j);
     int t = threadIdx.x;
+    for (int i = t; i < KMAX * NSLOT; i += 64) J->scert[i] = 0u;
     if (t < KMAX) {
-        J->scert[t] = 0u;
         J->thr[t] = -INFINITY;
         J->fb_corr[t] = 0ull;
         J->fb_index[t] = ~0ull;
@@ -347,58 +351,82 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
 // of the low-order prefix nodes).
 __device__ __forceinline__ uint64_t sample_unit(uint64_t j, uint64_t S, uint64_t n) {
     const uint64_t start = j * S;
-    const uint64_t width = min(S, n - start);
+    const uint32_t width = (uint32_t)min(S, n - start);
     const uint32_t h = (uint32_t)(j * 0x9E3779B1ull) >> 16;
-    return start + (uint64_t)h % width;
+    return start + (uint64_t)(h % width);
 }
 
-// Seeding pre-pass of the sweep: one hashed block per window of S blocks.
+// Seeding pre-pass of the sweep: work unit = one row (block, x-implementation)
+// of R_y plans; one hashed row per window of S rows.  Per level, the best fp32
+// corr among sampled plans whose fp32 CP is certainly feasible.  A plan's CP
+// bin gives (jtab, lane-resident, through ds_bpermute) how many levels, in
+// order of decreasing band, it certainly meets; the plan updates one bucket,
+// and a suffix maximum over buckets gives every level's value.  Reduction:
+// DPP within the wave, LDS across the workgroup, then an atomic max on the
+// ordered bit pattern into one of NSLOT slots per level.
 template <bool HAS_S2>
 __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ jobs) {
-    extern __shared__ float s_f[];
+    extern __shared__ float s_dyn[];
+    __shared__ uint32_t s_red[KMAX][WG / 64];
     JD J = cs(jobs + blockIdx.y);
     PD P = cs(J->prob);
+    const int K = P->k;
+    float* s_f = s_dyn;                                  // prefix recurrence, [npre][WG]
+    float* s_b = s_dyn + (size_t)max(P->npre, 1) * WG;   // buckets, [K][WG]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint64_t S = J->sample_stride;
-    const uint64_t nsamp = (J->nblk + S - 1) / S;
+    const int rx = P->rx, ry = P->ry;
+    const uint64_t units = J->nblk * (uint64_t)rx;
+    const uint64_t nsamp = (units + S - 1) / S;
     const uint64_t t0 = (uint64_t)blockIdx.x * WG;
     if (t0 >= nsamp) return;
-    const uint64_t t = t0 + threadIdx.x;
+    const uint64_t t = t0 + tid;
     const bool live = t < nsamp;
-    const uint64_t b = J->blk_first + sample_unit(live ? t : nsamp - 1, S, J->nblk);
+    const uint64_t u = sample_unit(live ? t : nsamp - 1, S, units);
+    uint64_t b;
+    int ix;
+    if (units <= 0xffffffffull && P->xnode >= 0) {  // 32-bit split by the invariant divisor
+        const uint32_t q = mdiv((uint32_t)u, P->rmag[P->xnode]);
+        b = J->blk_first + q;
+        ix = (int)((uint32_t)u - q * (uint32_t)rx);
+    } else {
+        b = J->blk_first + u / (uint64_t)rx;
+        ix = (int)(u % (uint64_t)rx);
+    }
     const Prefix pf = prefix_eval(P, b, J->big, s_f);
-    const int K = P->k;
-    float best[KMAX];
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) best[k] = -1.0f;
-    const CS float2* atx = cs(P->atx);
-    const CS float2* aty = cs(P->aty);
-    const int rx = P->rx, ry = P->ry;
+    for (int j = 0; j < K; ++j) s_b[j * WG + tid] = -1.0f;
+    const float2 vx = cs(P->atx)[ix];
+    const float fx = vx.y + pf.px;
+    const float cx = pf.pc * vx.x;
     const bool exy = P->edge_xy != 0;
-    for (int ix = 0; ix < rx; ++ix) {
-        const float2 vx = atx[ix];
-        const float fx = vx.y + pf.px;
-        const float cx = pf.pc * vx.x;
-        const float M = exy ? fmaxf(pf.py, fx) : pf.py;
-        const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
-        const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
-        for (int iy = 0; iy < ry; ++iy) {
-            const float2 vy = aty[iy];
-            float cp = vy.y + M;
-            if (HAS_S2) cp = fmaxf(cp, S2);
-            const float cc = cx * vy.x;
-            const bool ok = live && (base + (uint64_t)iy - J->begin < J->count);
-#pragma unroll
-            for (int k = 0; k < KMAX; ++k)
-                if (k < K && ok && cp <= P->lo[k]) best[k] = fmaxf(best[k], cc);
+    const float M = exy ? fmaxf(pf.py, fx) : pf.py;
+    const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
+    const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
+    const int jt = (int)P->jtab[lane];
+    const uint32_t sh = (uint32_t)P->bin_shift - 2u;
+    const CS float2* aty = cs(P->aty);
+    for (int iy = 0; iy < ry; ++iy) {
+        const float2 vy = aty[iy];
+        float cp = vy.y + M;
+        if (HAS_S2) cp = fmaxf(cp, S2);
+        const float cc = cx * vy.x;
+        const int j = __builtin_amdgcn_ds_bpermute((int)(__float_as_uint(cp) >> sh) & 0xfc, jt);
+        if (j > 0 && live && (base + (uint64_t)iy - J->begin < J->count)) {
+            float* q = s_b + (j - 1) * WG + tid;
+            *q = fmaxf(*q, cc);
         }
     }
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) {
-        if (k < K) {
-            uint32_t e = best[k] >= 0.0f ? __float_as_uint(best[k]) + 1u : 0u;
-            e = wave_max_u32(e);
-            if ((threadIdx.x & 63) == 0 && e) atomicMax(J->scert + k, e);
-        }
+    float run = -1.0f;
+    for (int i = K - 1; i >= 0; --i) {
+        run = fmaxf(run, s_b[i * WG + tid]);
+        const uint32_t e = wave_max_u32(run >= 0.0f ? __float_as_uint(run) + 1u : 0u);
+        if (lane == 0) s_red[i][wave] = e;
+    }
+    __syncthreads();
+    if (tid < K) {
+        uint32_t e = 0;
+        for (int w = 0; w < WG / 64; ++w) e = max(e, s_red[tid][w]);
+        if (e) atomicMax(J->scert + P->lvl_order[tid] * NSLOT + (blockIdx.x % NSLOT), e);
     }
 }
 
@@ -413,7 +441,8 @@ __global__ void k_table(JobDev* __restrict__ jobs, int njobs) {
     PD P = cs(J->prob);
     const int lane = threadIdx.x;
     if (lane < P->k) {
-        uint32_t e = J->scert[lane];
+        uint32_t e = 0;
+        for (int q = 0; q < NSLOT; ++q) e = max(e, J->scert[lane * NSLOT + q]);
         J->thr[lane] = e ? cand_threshold(__uint_as_float(e - 1u), P->n) : -INFINITY;
     }
     __syncthreads();
@@ -574,7 +603,8 @@ __global__ void __launch_bounds__(WG) k_sample_generic(const JobDev* __restrict_
         const float cp = P->uniform ? cp0 : eval_cp_level(P, s_id, s_f, k);
         uint32_t e = (ok && cp <= P->lo[k]) ? __float_as_uint(cc) + 1u : 0u;
         e = wave_max_u32(e);
-        if ((threadIdx.x & 63) == 0 && e) atomicMax(J->scert + k, e);
+        if ((threadIdx.x & 63) == 0 && e)
+            atomicMax(J->scert + k * NSLOT + ((blockIdx.x * (WG / 64) + (threadIdx.x >> 6)) % NSLOT), e);
     }
 }
 
@@ -628,77 +658,218 @@ __device__ __forceinline__ bool better(double c1, uint64_t i1, double c2, uint64
     return c1 > c2 || (c1 == c2 && i1 < i2);
 }
 
-__global__ void __launch_bounds__(WG) k_certify(const JobDev* __restrict__ jobs) {
+// Wave-wide best (corr desc, index asc) through lane exchanges.
+__device__ __forceinline__ void wave_best(double& c, uint64_t& i) {
+    for (int o = 32; o > 0; o >>= 1) {
+        const double c2 = __shfl_xor(c, o);
+        const uint64_t i2 = __shfl_xor(i, o);
+        if (better(c2, i2, c, i)) {
+            c = c2;
+            i = i2;
+        }
+    }
+}
+
+// Wave-wide best (corr desc, index asc) carrying the winner's CP and demand.
+__device__ __forceinline__ void wave_best4(double& c, uint64_t& i, double& cp, double& d) {
+    for (int o = 32; o > 0; o >>= 1) {
+        const double c2 = __shfl_xor(c, o);
+        const uint64_t i2 = __shfl_xor(i, o);
+        const double p2 = __shfl_xor(cp, o);
+        const double d2 = __shfl_xor(d, o);
+        if (better(c2, i2, c, i)) {
+            c = c2;
+            i = i2;
+            cp = p2;
+            d = d2;
+        }
+    }
+}
+
+constexpr int CERT_LDS_TABLES = 32 * 1024;  // fp64 tables staged in LDS when they fit
+constexpr int CERT_CACHE = 512;             // candidates cached in LDS by each certification wave
+
+// Certification, cert_waves waves per source (grid.x).  Pass A tightens each
+// level's threshold with the candidates whose fp32 CP is certainly feasible.
+// Pass B, level by level, re-evaluates in fp64 every candidate of this wave's
+// share that could still win the level (its CP only when its corr could beat
+// the lane's current best) and keeps the feasible one with the greatest corr,
+// then the lowest index.  k_cert_final merges the waves of a source.
+__global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs) {
+    extern __shared__ double s_tab[];
+    __shared__ double s_f[NMAX * 64];
+    __shared__ uint8_t s_id[NMAX * 64];
+    __shared__ float s_T[KMAX];
+    __shared__ Cand s_cand[CERT_CACHE];
     JD J = cs(jobs + blockIdx.y);
     PD P = cs(J->prob);
-    const int k = blockIdx.x;
-    if (k >= P->k) return;
-    __shared__ float s_best[WG];
-    __shared__ double s_c[WG];
-    __shared__ uint64_t s_i[WG];
-    const int tid = threadIdx.x;
+    const int g = blockIdx.x;
+    if (g >= J->cert_waves) return;
+    const int K = P->k, N = P->n, R = P->rmax, lane = threadIdx.x;
     const uint32_t nc = min(*J->ncand, J->cap);
-    const float lo = P->lo[k], hi = P->hi[k];
     const bool general = !P->uniform;
-
-    // tighten the threshold with certainly-feasible candidates (uniform mode
-    // stores the unpressured CP, compared against this level's band)
-    float sb = J->scert[k] ? __uint_as_float(J->scert[k] - 1u) : -1.0f;
+    uint8_t* ids = s_id + lane;
+    double* f = s_f + lane;
+    const size_t NR = (size_t)N * R;
+    const double* a64 = P->a64;
+    const double* d64 = P->dem64;
+    const double* l64 = P->lat64;
+    if ((size_t)(K + 2) * NR * sizeof(double) <= (size_t)CERT_LDS_TABLES) {
+        // unrolled so that many loads are in flight before the first LDS store
+#pragma unroll 8
+        for (size_t q = lane; q < NR; q += 64) {
+            s_tab[q] = P->a64[q];
+            s_tab[NR + q] = P->dem64[q];
+        }
+#pragma unroll 16
+        for (size_t q = lane; q < (size_t)K * NR; q += 64) s_tab[2 * NR + q] = P->lat64[q];
+        a64 = s_tab;
+        d64 = s_tab + NR;
+        l64 = s_tab + 2 * NR;
+    }
+    // one round of loads: every level's seed slots (lane = slot) and the candidates
+    static_assert(NSLOT == 64, "one seed slot per lane");
+    uint32_t sl[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) sl[k] = k < K ? J->scert[k * NSLOT + lane] : 0u;
+    const uint32_t ncache = min(nc, (uint32_t)CERT_CACHE);
+#pragma unroll 8
+    for (uint32_t i = lane; i < ncache; i += 64) s_cand[i] = J->cand[i];
+    __syncthreads();
+    float sb[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) sb[k] = sl[k] ? __uint_as_float(sl[k] - 1u) : -1.0f;
     if (!general)
-        for (uint32_t i = tid; i < nc; i += WG) {
-            const Cand c = J->cand[i];
-            if (c.cp <= lo) sb = fmaxf(sb, c.corr);
+        for (uint32_t i = lane; i < nc; i += 64) {
+            const Cand c = i < ncache ? s_cand[i] : J->cand[i];
+#pragma unroll
+            for (int k = 0; k < KMAX; ++k)
+                if (k < K && c.cp <= P->lo[k]) sb[k] = fmaxf(sb[k], c.corr);
         }
-    s_best[tid] = sb;
-    __syncthreads();
-    for (int o = WG / 2; o > 0; o >>= 1) {
-        if (tid < o) s_best[tid] = fmaxf(s_best[tid], s_best[tid + o]);
-        __syncthreads();
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+        if (k < K) {
+            const uint32_t e = wave_max_u32(sb[k] >= 0.0f ? __float_as_uint(sb[k]) + 1u : 0u);
+            if (lane == 0) s_T[k] = cand_threshold(e ? __uint_as_float(e - 1u) : -1.0f, N);
+        }
     }
-    const float T = cand_threshold(s_best[0], P->n);
-
-    double bc = -1.0;
-    uint64_t bi = ~0ull;
-    uint8_t ids[NMAX];
-    for (uint32_t i = tid; i < nc; i += WG) {
-        const Cand c = J->cand[i];
-        if (c.corr < T) continue;
-        if (!general && !(c.cp <= hi)) continue;
-        if (!job_ids(J, P, c.index, ids)) continue;
-        const double cp = ex_cp(P, ids, k);
-        if (!(cp <= P->slo)) continue;
-        const double cr = ex_corr(P, ids);
-        if (better(cr, c.index, bc, bi)) {
-            bc = cr;
+    __syncthreads();
+    const uint32_t step = 64u * (uint32_t)J->cert_waves;
+    for (int k = 0; k < K; ++k) {
+        const float T = s_T[k];
+        const float hi = P->hi[k];
+        const double* lat = l64 + (size_t)k * NR;
+        double bc = -1.0, bcp = 0.0, bd = 0.0;
+        uint64_t bi = ~0ull;
+        for (uint32_t i = (uint32_t)g * 64u + lane; i < nc; i += step) {
+            const Cand c = i < ncache ? s_cand[i] : J->cand[i];
+            if (!(c.corr >= T && (general || c.cp <= hi))) continue;
+            if (!job_ids(J, P, c.index, ids, 64)) continue;
+            double corr = 1.0;
+            for (int n = 0; n < N; ++n) corr = corr * a64[n * R + ids[n * 64]];
+            if (!better(corr, c.index, bc, bi)) continue;
+            double cp = 0.0;
+            for (int n = 0; n < N; ++n) {
+                double m = 0.0;
+                uint32_t pm = P->pred[n];
+                while (pm) {
+                    const int u = __builtin_ctz(pm);
+                    pm &= pm - 1;
+                    const double fu = f[u * 64];
+                    if (fu > m) m = fu;
+                }
+                const double fn = lat[n * R + ids[n * 64]] + m;
+                f[n * 64] = fn;
+                if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
+            }
+            if (!(cp <= P->slo)) continue;
+            double d = 0.0;
+            for (int n = 0; n < N; ++n) d = d + d64[n * R + ids[n * 64]];
+            bc = corr;
             bi = c.index;
+            bcp = cp;
+            bd = d;
+        }
+        wave_best4(bc, bi, bcp, bd);
+        if (lane == 0) {
+            J->cert_c[k * CERT_WAVES + g] = bc;
+            J->cert_i[k * CERT_WAVES + g] = bi;
+            J->cert_cp[k * CERT_WAVES + g] = bcp;
+            J->cert_d[k * CERT_WAVES + g] = bd;
         }
     }
-    s_c[tid] = bc;
-    s_i[tid] = bi;
+}
+
+__global__ void __launch_bounds__(64) k_cert_final(const JobDev* __restrict__ jobs) {
+    JD J = cs(jobs + blockIdx.x);
+    PD P = cs(J->prob);
+    const int K = P->k;
+    // lane = (level, wave) pair; levels in groups of 64 / CERT_WAVES
+    constexpr int LPG = 64 / CERT_WAVES;
+    const int lane = threadIdx.x, w = lane % CERT_WAVES, kk = lane / CERT_WAVES;
+    for (int k0 = 0; k0 < K; k0 += LPG) {
+        const int k = k0 + kk;
+        double bc = -1.0, bcp = 0.0, bd = 0.0;
+        uint64_t bi = ~0ull;
+        if (k < K && w < J->cert_waves) {
+            bc = J->cert_c[k * CERT_WAVES + w];
+            bi = J->cert_i[k * CERT_WAVES + w];
+            bcp = J->cert_cp[k * CERT_WAVES + w];
+            bd = J->cert_d[k * CERT_WAVES + w];
+        }
+        for (int o = CERT_WAVES / 2; o > 0; o >>= 1) {
+            const double c2 = __shfl_xor(bc, o);
+            const uint64_t i2 = __shfl_xor(bi, o);
+            const double p2 = __shfl_xor(bcp, o);
+            const double d2 = __shfl_xor(bd, o);
+            if (better(c2, i2, bc, bi)) {
+                bc = c2;
+                bi = i2;
+                bcp = p2;
+                bd = d2;
+            }
+        }
+        if (w == 0 && k < K) {
+            dy_choice* o = J->out + k;
+            if (bi != ~0ull) {
+                o->index = (int64_t)bi;
+                o->feasible = 1;
+                o->corr = (float)bc;
+                o->cp = (float)bcp;
+                o->demand = (float)bd;
+            } else {
+                o->index = -1;
+                o->feasible = 0;
+                o->corr = NAN;
+                o->cp = NAN;
+                o->demand = NAN;
+            }
+        }
+    }
+}
+
+// Overflow recovery: the candidates gathered before the list overflowed
+// include certainly-feasible plans; fold their fp32 corr into the seeds (a
+// valid threshold comes from any certainly-feasible plan) and reset the list
+// for another scoring pass.  One wave per source; uniform pressure only.
+__global__ void __launch_bounds__(64) k_reseed(const JobDev* __restrict__ jobs) {
+    JD J = cs(jobs + blockIdx.x);
+    PD P = cs(J->prob);
+    const int lane = threadIdx.x;
+    const uint32_t nc = min(*J->ncand, J->cap);
+    for (int k = 0; k < P->k; ++k) {
+        float sb = -1.0f;
+        for (uint32_t i = lane; i < nc; i += 64) {
+            const Cand c = J->cand[i];
+            if (c.cp <= P->lo[k]) sb = fmaxf(sb, c.corr);
+        }
+        const uint32_t e = wave_max_u32(sb >= 0.0f ? __float_as_uint(sb) + 1u : 0u);
+        if (lane == 0 && e) atomicMax(J->scert + k * NSLOT, e);
+    }
     __syncthreads();
-    for (int o = WG / 2; o > 0; o >>= 1) {
-        if (tid < o && better(s_c[tid + o], s_i[tid + o], s_c[tid], s_i[tid])) {
-            s_c[tid] = s_c[tid + o];
-            s_i[tid] = s_i[tid + o];
-        }
-        __syncthreads();
-    }
-    if (tid == 0) {
-        dy_choice* o = J->out + k;
-        if (s_i[0] != ~0ull) {
-            job_ids(J, P, s_i[0], ids);
-            o->index = (int64_t)s_i[0];
-            o->feasible = 1;
-            o->corr = (float)s_c[0];
-            o->cp = (float)ex_cp(P, ids, k);
-            o->demand = (float)ex_demand(P, ids);
-        } else {
-            o->index = -1;
-            o->feasible = 0;
-            o->corr = NAN;
-            o->cp = NAN;
-            o->demand = NAN;
-        }
+    if (lane == 0) {
+        *J->ncand = 0u;
+        *J->flags = 0;
     }
 }
 
@@ -714,16 +885,17 @@ __global__ void __launch_bounds__(WG) k_exhaust(const JobDev* __restrict__ jobs,
     const uint64_t units = J->count;
     const uint64_t stride = (uint64_t)gridDim.x * WG;
     uint8_t ids[NMAX];
+    double f[NMAX];
     for (int k = 0; k < P->k; ++k) {
         if (!(J->fb_levels >> k & 1u)) continue;
         const uint64_t target = pass ? J->fb_corr[k] : 0ull;
         uint64_t acc = pass ? ~0ull : 0ull;
         for (uint64_t j = (uint64_t)blockIdx.x * WG + threadIdx.x; j < units; j += stride) {
             const uint64_t idx = J->kind == DY_SOURCE_RANGE ? J->begin + j : J->index_base + j;
-            if (!job_ids(J, P, idx, ids)) continue;
-            const double cp = ex_cp(P, ids, k);
+            if (!job_ids(J, P, idx, ids, 1)) continue;
+            const double cp = ex_cp(P, ids, 1, k, f, 1);
             if (!(cp <= P->slo)) continue;
-            const uint64_t cb = (uint64_t)__double_as_longlong(ex_corr(P, ids));
+            const uint64_t cb = (uint64_t)__double_as_longlong(ex_corr(P, ids, 1));
             if (!pass) {
                 acc = cb + 1ull > acc ? cb + 1ull : acc;  // +1: 0 means none
             } else if (cb + 1ull == target && idx < acc) {
@@ -753,12 +925,13 @@ __global__ void k_exhaust_final(const JobDev* __restrict__ jobs, int njobs) {
     if (k >= P->k || !(J->fb_levels >> k & 1u)) return;
     uint8_t ids[NMAX];
     dy_choice* o = J->out + k;
-    if (J->fb_index[k] != ~0ull && job_ids(J, P, J->fb_index[k], ids)) {
+    double f[NMAX];
+    if (J->fb_index[k] != ~0ull && job_ids(J, P, J->fb_index[k], ids, 1)) {
         o->index = (int64_t)J->fb_index[k];
         o->feasible = 1;
-        o->corr = (float)ex_corr(P, ids);
-        o->cp = (float)ex_cp(P, ids, k);
-        o->demand = (float)ex_demand(P, ids);
+        o->corr = (float)ex_corr(P, ids, 1);
+        o->cp = (float)ex_cp(P, ids, 1, k, f, 1);
+        o->demand = (float)ex_demand(P, ids, 1);
     } else {
         o->index = -1;
         o->feasible = 0;
@@ -803,6 +976,7 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
     }
     uint32_t bits = 0;
     uint8_t ids[NMAX];
+    double fx[NMAX];
     bool have_ids = false;
     for (int k = 0; k < K; ++k) {
         const float cpc = P->uniform ? cp0 : eval_cp_level(P, s_id, s_f, k);
@@ -816,7 +990,7 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
                 col_ids(P, s_id, ids);
                 have_ids = true;
             }
-            f = ex_cp(P, ids, k) <= P->slo;
+            f = ex_cp(P, ids, 1, k, fx, 1) <= P->slo;
         }
         if (f && k < 32) bits |= 1u << k;
         if (live && cpo) cpo[t * (uint64_t)K + k] = P->uniform ? cp0 * P->mk[k] : cpc;
@@ -853,10 +1027,10 @@ hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s) {
 hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_samples, int npre_max,
                                hipStream_t s) {
     if (n == 0) return hipSuccess;
-    uint64_t gx = (max_samples + WG - 1) / WG;
+    const uint64_t gx = (max_samples + WG - 1) / WG;
     if (gx == 0) return hipSuccess;
     if (gx > MAX_GRID_X) return hipErrorInvalidValue;
-    size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float);
+    const size_t lds = (size_t)((npre_max > 0 ? npre_max : 1) + KMAX) * WG * sizeof(float);
     if (has_s2)
         hipLaunchKernelGGL(k_sample_sweep<true>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs);
     else
@@ -903,8 +1077,16 @@ hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStrea
     return hipSuccess;
 }
 
-hipError_t launch_certify(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s) {
-    hipLaunchKernelGGL(k_certify, dim3(kmax, njobs), dim3(WG), 0, s, d_jobs);
+hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, hipStream_t s) {
+    hipLaunchKernelGGL(k_certify, dim3(waves, njobs), dim3(64), CERT_LDS_TABLES, s, d_jobs);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_cert_final, dim3(njobs), dim3(64), 0, s, d_jobs);
+    return hipGetLastError();
+}
+
+hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s) {
+    hipLaunchKernelGGL(k_reseed, dim3(njobs), dim3(64), 0, s, d_jobs);
     return hipGetLastError();
 }
 

@@ -361,3 +361,15 @@ def test_select_argument_errors():
                     D.DySource(7, 0, 0, 1, None, 0, 0), D.rows_source(0, 0, 10, 4)):
             with pytest.raises(D.DyplanError):
                 plan.select([src], stream=stream())
+
+
+def test_overflow_recovered_by_reseeding():
+    prob = wl.forkjoin8()
+    begin, count = 3000000, 2000000
+    with D.Plan(prob) as plan:
+        plan.set_option(D.DY_OPT_SAMPLE_STRIDE, 1 << 30)  # one seed sample: weak thresholds
+        plan.set_option(D.DY_OPT_CAND_CAPACITY, 1024)
+        got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+        st = plan.stats()
+    assert_choices(got, orc.select_range(prob, begin, count), "reseeded")
+    assert st.fallbacks == 0
