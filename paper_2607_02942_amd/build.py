@@ -37,13 +37,13 @@ def _run(cmd):
 
 def build_hip(extra_flags=(), out: str = LIB) -> str:
     objs = []
-    for src in ("kernels.hip", "host.cpp"):
+    for src in ("kernels.hip", "host.cpp", "jit_rows.cpp"):
         obj = os.path.join(CSRC, "_" + src.replace(".", "_") + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
         _run([HIPCC, *HIP_FLAGS, *extra_flags, f"-I{INCLUDE}", f"-I{CSRC}", *lang, "-c",
               os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", out])
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", out, "-lhiprtc"])
     for o in objs:
         os.remove(o)
     return out

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstddef>
 #include <cstdio>
 #include <cstring>
 #include <functional>
@@ -26,6 +27,13 @@ hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStrea
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, hipStream_t s);
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
 hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
+struct JitRows {
+    hipModule_t mod = nullptr;
+    hipFunction_t scan = nullptr;
+    hipFunction_t scan_u = nullptr;
+    hipFunction_t sample = nullptr;
+};
+bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err);
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
                         hipStream_t s);
 }  // namespace dyp
@@ -223,6 +231,11 @@ struct dy_plan {
     int device = 0;
     int kmax = 0;
     std::vector<HostProb> hp;
+    std::vector<ProbDev> hdesc;       // host copies of the device descriptors
+    std::vector<int> jit_state;       // per problem: 0 untried, 1 ready, -1 unavailable
+    std::vector<JitRows> jit;
+    int use_jit = 1;
+    int cus = 0;                      // compute units of the device
     char* d_arena = nullptr;
     ProbDev* d_probs = nullptr;
     Scratch sc;
@@ -533,6 +546,9 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
     }
     e = hipMemcpy(h->d_arena, img.data(), off, hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(err, e, "hipMemcpy(tables)");
+    h->hdesc.assign(descs, descs + n_probs);
+    h->jit_state.assign(n_probs, 0);
+    h->jit.assign(n_probs, JitRows{});
     return DY_OK;
 }
 
@@ -637,6 +653,8 @@ int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_
         return DY_ENOMEM;
     }
     h->device = device;
+    if (hipDeviceGetAttribute(&h->cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || h->cus < 1)
+        h->cus = 256;
     int st = stage_problems(h, probs, n_probs, &g_create_error);
     if (st == DY_OK) {
         for (int i = 0; i < 4 && st == DY_OK; ++i)
@@ -678,6 +696,7 @@ int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value) {
             h->cand_cap = (uint32_t)value;
             return DY_OK;
         case DY_OPT_FORCE_FP64: h->force_fp64 = value ? 1 : 0; return DY_OK;
+        case DY_OPT_JIT: h->use_jit = value ? 1 : 0; return DY_OK;
         default:
             h->err = "unknown option";
             return DY_EINVAL;
@@ -697,35 +716,75 @@ int dy_plan_get_stats(const dy_plan* h, dy_stats* out) {
 namespace {
 
 // The kernel family that scores a source.
-enum Group { G_SWEEP = 0, G_SWEEP_S2 = 1, G_GENERIC = 2 };
+enum Group { G_SWEEP = 0, G_SWEEP_S2 = 1, G_GENERIC = 2, G_JIT = 3 };
 
 struct PassPlan {
-    int n[3] = {0, 0, 0};                 // sources per group, stored in group order
+    int n[4] = {0, 0, 0, 0};              // sources per group, stored in group order
     uint64_t units[3] = {0, 0, 0};        // largest main-pass work of the group
     uint64_t samples[3] = {0, 0, 0};      // largest seeding-pass work of the group
     int npre[2] = {0, 0};
 };
 
-// Launch the scoring passes for `n` jobs stored in group order at d.
-// seed: run the seeding pre-pass (otherwise the seeds are already in place).
-void launch_passes(const JobDev* d, const PassPlan& pp, bool seed, hipStream_t s,
-                   const std::function<void(hipError_t, const char*)>& chk) {
+// Rows sources of uniform-pressure problems run the problem's generated
+// kernels (one launch per source; the host copies of the job carry the args).
+hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sample, hipStream_t s) {
+    const ProbDev& D = h->hdesc[problem];
+    const JitRows& jr = h->jit[problem];
+    const ProbDev* dp = h->d_probs + problem;
+    unsigned long long rows_stride = J.stride, count = J.count, index_base = J.index_base;
+    const unsigned char* rows = J.rows;
+    const float2* at = D.at;
+    int rmax = D.rmax, K = D.k, bin_shift = D.bin_shift;
+    int aligned = ((J.stride | (uint64_t)(uintptr_t)J.rows | (uint64_t)D.n) & 3u) == 0 ? 1 : 0;
+    const float* hi = (const float*)((const char*)dp + offsetof(ProbDev, hi));
+    const float* lo = (const float*)((const char*)dp + offsetof(ProbDev, lo));
+    if (sample) {
+        unsigned* scert = J.scert;
+        unsigned long long S = J.sample_stride;
+        void* args[] = {&rows, &rows_stride, &count, &at, &rmax, &lo, &K, &scert, &S, &aligned};
+        const unsigned long long nsamp = (count + S - 1) / S;
+        const unsigned gx = (unsigned)std::min<unsigned long long>((nsamp + 255) / 256, 1ull << 22);
+        return hipModuleLaunchKernel(jr.sample, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
+    }
+    const unsigned* table = J.table;
+    const float* thr = J.thr;
+    Cand* cand = J.cand;
+    unsigned cap = J.cap;
+    unsigned* ncand = J.ncand;
+    int* flags = J.flags;
+    void* args[] = {&rows, &rows_stride, &count, &index_base, &at, &rmax, &table, &bin_shift, &hi, &thr, &K,
+                    &cand, &cap, &ncand, &flags};
+    hipFunction_t fn = aligned ? jr.scan : jr.scan_u;
+    int per_cu = 0;
+    if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, 0) != hipSuccess || per_cu < 1)
+        per_cu = 4;
+    const unsigned long long want = (count + 255) / 256;
+    const unsigned gx = (unsigned)std::min<unsigned long long>(want, (unsigned long long)per_cu * h->cus);
+    return hipModuleLaunchKernel(fn, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
+}
+
+// Seeding pre-pass of groups 0-2 (jobs stored in group order at d).
+void launch_seed(const JobDev* d, const PassPlan& pp, hipStream_t s,
+                 const std::function<void(hipError_t, const char*)>& chk) {
     auto chunks = [&](const JobDev* base, int n, auto&& fn) {
         for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
     };
     const JobDev* gbase[3] = {d, d + pp.n[0], d + pp.n[0] + pp.n[1]};
-    const int ntot = pp.n[0] + pp.n[1] + pp.n[2];
-    if (seed) {
-        for (int g = 0; g < 2; ++g)
-            chunks(gbase[g], pp.n[g], [&](const JobDev* b, int n) {
-                chk(launch_sample_sweep(b, n, g == 1, pp.samples[g], pp.npre[g], s), "sample");
-            });
-        chunks(gbase[2], pp.n[2],
-               [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, pp.samples[2], s), "sample"); });
-    }
-    chunks(d, ntot, [&](const JobDev* b, int n) { chk(launch_table(const_cast<JobDev*>(b), n, s), "table"); });
+    for (int g = 0; g < 2; ++g)
+        chunks(gbase[g], pp.n[g], [&](const JobDev* b, int n) {
+            chk(launch_sample_sweep(b, n, g == 1, pp.samples[g], pp.npre[g], s), "sample");
+        });
+    chunks(gbase[2], pp.n[2],
+           [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, pp.samples[2], s), "sample"); });
 }
 
+void launch_table_all(const JobDev* d, int ntot, hipStream_t s,
+                      const std::function<void(hipError_t, const char*)>& chk) {
+    for (int c = 0; c < ntot; c += 65535)
+        chk(launch_table(const_cast<JobDev*>(d + c), std::min(65535, ntot - c), s), "table");
+}
+
+// Scoring pass of groups 0-2.
 void launch_main(const JobDev* d, const PassPlan& pp, hipStream_t s,
                  const std::function<void(hipError_t, const char*)>& chk) {
     auto chunks = [&](const JobDev* base, int n, auto&& fn) {
@@ -743,6 +802,16 @@ void launch_certify_all(const JobDev* d, int ntot, int cert_waves, hipStream_t s
                         const std::function<void(hipError_t, const char*)>& chk) {
     for (int c = 0; c < ntot; c += 65535)
         chk(launch_certify(d + c, std::min(65535, ntot - c), cert_waves, s), "certify");
+}
+
+// Generated rows kernels for problem p: compiled at first use.
+bool jit_ready(dy_plan* h, int p) {
+    if (!h->use_jit) return false;
+    if (h->jit_state[p] == 0) {
+        std::string why;
+        h->jit_state[p] = jit_rows_get(h->device, h->hdesc[p], &h->jit[p], &why) ? 1 : -1;
+    }
+    return h->jit_state[p] == 1;
 }
 
 }  // namespace
@@ -773,22 +842,28 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     const int km = h->kmax;
     const int cert_waves = n_src <= 64 ? CERT_WAVES : 1;
 
-    auto group_of = [&](int j) {
-        const HostProb& H = h->hp[src[j].problem];
-        const bool sweep = src[j].kind == DY_SOURCE_RANGE && H.uniform;
-        return sweep ? (H.has_s2 ? G_SWEEP_S2 : G_SWEEP) : G_GENERIC;
-    };
+    std::vector<int> grp(n_src);
+    for (int j = 0; j < n_src; ++j) {
+        const int p = src[j].problem;
+        const HostProb& H = h->hp[p];
+        if (src[j].kind == DY_SOURCE_RANGE && H.uniform)
+            grp[j] = H.has_s2 ? G_SWEEP_S2 : G_SWEEP;
+        else if (src[j].kind == DY_SOURCE_ROWS && H.uniform && !h->force_fp64 && jit_ready(h, p))
+            grp[j] = G_JIT;
+        else
+            grp[j] = G_GENERIC;
+    }
     std::vector<int> order;
     order.reserve(n_src);
-    for (int g = 0; g < 3; ++g)
+    for (int g = 0; g < 4; ++g)
         for (int j = 0; j < n_src; ++j)
-            if (group_of(j) == g) order.push_back(j);
+            if (grp[j] == g) order.push_back(j);
     uint64_t plans = 0, all_units = 0;
     PassPlan pp;
     std::vector<JobDev> jobs((size_t)n_src);
     for (int q = 0; q < n_src; ++q) {
         const int j = order[q];
-        const int g = group_of(j);
+        const int g = grp[j];
         const HostProb& H = h->hp[src[j].problem];
         JobDev J = make_job(h, src[j]);
         J.cap = (uint32_t)cap;
@@ -808,19 +883,23 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         J.cert_d = S.cert_d + (size_t)q * KMAX * CERT_WAVES;
         J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
         // seeding work units: rows of the inner sweep, or plans
-        const uint64_t sunits = g == G_GENERIC ? J.count : J.nblk * (uint64_t)H.rx;
+        const bool sweep = g == G_SWEEP || g == G_SWEEP_S2;
+        const uint64_t sunits = sweep ? J.nblk * (uint64_t)H.rx : J.count;
         uint64_t stride = h->sample_stride;
         if (!h->stride_fixed) stride = std::max<uint64_t>(1, std::min<uint64_t>(stride, sunits / kMinSamples));
         J.sample_stride = (uint32_t)stride;
-        J.units = g == G_GENERIC ? J.count : J.nblk;
+        J.units = sweep ? J.nblk : J.count;
         ++pp.n[g];
-        pp.units[g] = std::max(pp.units[g], J.units);
-        pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
-        if (g != G_GENERIC) pp.npre[g] = std::max(pp.npre[g], H.npre);
+        if (g < 3) {
+            pp.units[g] = std::max(pp.units[g], J.units);
+            pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
+        }
+        if (sweep) pp.npre[g] = std::max(pp.npre[g], H.npre);
         all_units = std::max(all_units, J.count);
         plans += J.count;
         jobs[q] = J;
     }
+    const int n3 = pp.n[0] + pp.n[1] + pp.n[2];  // jobs of groups 0-2; JIT jobs follow
     // the job array is rebuilt every call but uploaded only when it changed
     if (S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0) {
         hipError_t e = hipStreamSynchronize(s);  // a previous upload may still read the pinned buffer
@@ -837,12 +916,21 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     std::function<void(hipError_t, const char*)> chk = [&](hipError_t x, const char* what) {
         if (x != hipSuccess && st == DY_OK) st = hip_fail(&h->err, x, what);
     };
+    auto jit_pass = [&](const JobDev* hjobs, int first, int n, bool sample) {
+        for (int q = first; q < first + n; ++q) {
+            const int p = (int)(hjobs[q].prob - h->d_probs);
+            chk(launch_jit(h, hjobs[q], p, sample, s), sample ? "rows sample" : "rows scan");
+        }
+    };
     if (h->timing) chk(hipEventRecord(h->ev[0], s), "hipEventRecord");
     for (int c = 0; c < n_src; c += 65535) chk(launch_init(S.d_jobs + c, std::min(65535, n_src - c), s), "init");
     if (!h->force_fp64) {
-        launch_passes(S.d_jobs, pp, true, s, chk);
+        launch_seed(S.d_jobs, pp, s, chk);
+        jit_pass(jobs.data(), n3, pp.n[3], true);
+        launch_table_all(S.d_jobs, n_src, s, chk);
         if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
         launch_main(S.d_jobs, pp, s, chk);
+        jit_pass(jobs.data(), n3, pp.n[3], false);
         if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
         launch_certify_all(S.d_jobs, n_src, cert_waves, s, chk);
     } else {
@@ -879,39 +967,45 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     constexpr int kReseedRounds = 3;
     for (int round = 0; round <= kReseedRounds && !h->force_fp64; ++round) {
         PassPlan rp;
-        int n_fb = 0;
+        std::vector<JobDev> re, ex;
         uint64_t fb_units = 0;
-        for (int g = 0; g < 3; ++g)
+        for (int g = 0; g < 4; ++g)
             for (int q = 0; q < n_src; ++q) {
                 if (!(S.h_flags[q] & JF_OVERFLOW)) continue;
                 const int j = order[q];
-                if (group_of(j) != g) continue;
+                if (grp[j] != g) continue;
                 const HostProb& H = h->hp[src[j].problem];
                 JobDev J = jobs[q];
                 if (round < kReseedRounds && H.uniform) {
                     ++rp.n[g];
-                    rp.units[g] = std::max(rp.units[g], J.units);
-                    if (g != G_GENERIC) rp.npre[g] = std::max(rp.npre[g], H.npre);
+                    if (g < 3) rp.units[g] = std::max(rp.units[g], J.units);
+                    if (g < 2) rp.npre[g] = std::max(rp.npre[g], H.npre);
+                    re.push_back(J);
                 } else {
                     J.fb_levels = H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u);
                     stats.fallbacks += H.k;
                     fb_units = std::max(fb_units, J.count);
+                    ex.push_back(J);
                 }
-                S.h_fb[n_fb++] = J;
             }
-        if (n_fb == 0) break;
-        chk(hipMemcpyAsync(S.d_fb, S.h_fb, (size_t)n_fb * sizeof(JobDev), hipMemcpyHostToDevice, s), "copy fb");
-        const int n_re = rp.n[0] + rp.n[1] + rp.n[2];
+        const int n_re = (int)re.size(), n_ex = (int)ex.size();
+        if (n_re + n_ex == 0) break;
+        std::memcpy(S.h_fb, re.data(), (size_t)n_re * sizeof(JobDev));
+        std::memcpy(S.h_fb + n_re, ex.data(), (size_t)n_ex * sizeof(JobDev));
+        chk(hipMemcpyAsync(S.d_fb, S.h_fb, (size_t)(n_re + n_ex) * sizeof(JobDev), hipMemcpyHostToDevice, s),
+            "copy fb");
         if (n_re > 0) {  // every overflowing uniform source is rescored
-            for (int c = 0; c < n_re; c += 65535) chk(launch_reseed(S.d_fb + c, std::min(65535, n_re - c), s), "reseed");
-            launch_passes(S.d_fb, rp, false, s, chk);
+            for (int c = 0; c < n_re; c += 65535)
+                chk(launch_reseed(S.d_fb + c, std::min(65535, n_re - c), s), "reseed");
+            launch_table_all(S.d_fb, n_re, s, chk);
             launch_main(S.d_fb, rp, s, chk);
+            jit_pass(re.data(), rp.n[0] + rp.n[1] + rp.n[2], rp.n[3], false);
             launch_certify_all(S.d_fb, n_re, cert_waves, s, chk);
         }
-        if (n_fb > n_re) {
+        if (n_ex > 0) {
             const JobDev* b = S.d_fb + n_re;
-            for (int c = 0; c < n_fb - n_re; c += 65535)
-                chk(launch_exhaust(b + c, std::min(65535, n_fb - n_re - c), fb_units, s), "exhaust");
+            for (int c = 0; c < n_ex; c += 65535)
+                chk(launch_exhaust(b + c, std::min(65535, n_ex - c), fb_units, s), "exhaust");
         }
         chk(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, s), "copy out");
         chk(hipStreamSynchronize(s), "hipStreamSynchronize");

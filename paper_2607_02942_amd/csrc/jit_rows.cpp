@@ -1,0 +1,349 @@
+// DAG-specialised kernels for candidate rows (streamed plans), generated as
+// HIP source from one problem's structure and compiled at first use with
+// hiprtc for the running device.
+//
+// A row is N bytes, byte n = implementation id of node n.  Every node's table
+// (factor a = 1 - w(1 - p) and duration tau, fp32) sits lane-resident in two
+// VGPRs (entry i in lane i, R <= 64) and is gathered with ds_bpermute, whose
+// lane select is bits [7:2] of the address: the id byte only needs shifting
+// into place.  The recurrence is unrolled in node order with every f_n in a
+// register, so each plan costs N-1 multiplies, one add per node and one max
+// per extra predecessor; the rows stream through non-temporal dword loads,
+// the next row's words in flight while the current row is scored.
+//
+// Ids >= 64 are caught from the OR of the row words; ids in [R_n, 64) read
+// NaN padding and surface as a NaN corr.  The arithmetic is that of the
+// generic kernels (same fp32 operations in the same order), so both produce
+// identical scores.
+#include <hip/hip_runtime.h>
+#include <hip/hiprtc.h>
+
+#include <cstdio>
+#include <map>
+#include <mutex>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "dyplan_internal.h"
+
+namespace dyp {
+
+struct JitRows {
+    hipModule_t mod = nullptr;
+    hipFunction_t scan = nullptr;     // rows whose words are dword aligned
+    hipFunction_t scan_u = nullptr;   // any other stride / alignment (byte loads)
+    hipFunction_t sample = nullptr;
+};
+
+namespace {
+
+std::mutex g_mu;
+std::map<std::string, JitRows> g_cache;  // key: device id + generated source
+
+const char* kCommon = R"(
+struct DyCand { unsigned long long index; float corr; float cp; };
+__device__ __forceinline__ unsigned dy_wmax(unsigned v) {
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false));
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false));
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x113, 0xf, 0xf, false));
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xe, false));
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xc, false));
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false));
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false));
+  return (unsigned)__builtin_amdgcn_readlane((int)v, 63);
+}
+// Per-wave candidate queue in LDS: the scoring loop issues no global atomic or
+// store (those would make it wait for the rows in flight).  The queue goes to
+// the global candidate list at the end; a full queue raises the overflow flag,
+// which the host resolves exactly by reseeding and rescoring the source.
+#define DY_QCAP 256
+__device__ void dy_flush(DyCand* q, unsigned qn, int lane, DyCand* cand, unsigned cap, unsigned* ncand,
+                         bool* ovf) {
+  if (qn == 0) return;
+  unsigned base = 0;
+  if (lane == 0) base = atomicAdd(ncand, qn);
+  base = (unsigned)__builtin_amdgcn_readfirstlane((int)base);
+  for (unsigned i = lane; i < qn; i += 64) {
+    if (base + i < cap) cand[base + i] = q[i];
+  }
+  if (base + qn > cap) *ovf = true;
+}
+__device__ __forceinline__ unsigned long long dy_sample_row(unsigned long long j, unsigned long long S,
+                                                            unsigned long long n) {
+  const unsigned long long start = j * S;
+  const unsigned width = (unsigned)min(S, n - start);
+  const unsigned h = (unsigned)(j * 0x9E3779B1ull) >> 16;
+  return start + (unsigned long long)(h % width);
+}
+)";
+
+std::string gen_source(const ProbDev& D) {
+    const int N = D.n;
+    const int Q = (N + 3) / 4;
+    std::ostringstream o;
+    o << kCommon;
+    // lane-resident tables
+    o << "#define DY_TABLES \\\n  const int lane = threadIdx.x & 63; \\\n";
+    for (int n = 0; n < N; ++n) {
+        o << "  const float2 e" << n << " = at[" << n << " * rmax + (lane < " << D.radix[n] << " ? lane : 0)]; \\\n";
+        o << "  const int A" << n << " = lane < " << D.radix[n] << " ? __float_as_int(e" << n
+          << ".x) : 0x7fc00000; \\\n";
+        o << "  const int T" << n << " = lane < " << D.radix[n] << " ? __float_as_int(e" << n
+          << ".y) : 0x7fc00000; \\\n";
+    }
+    o << "\n";
+    // row loads: whole dwords when aligned, else bytes
+    o << "#define DY_LOAD(rr";
+    for (int q = 0; q < Q; ++q) o << ", w" << q;
+    o << ") { \\\n  const unsigned char* p_ = rows + (rr) * stride; \\\n  if (aligned) { \\\n";
+    for (int q = 0; q < Q; ++q)
+        o << "    w" << q << " = __builtin_nontemporal_load((const unsigned*)p_ + " << q << "); \\\n";
+    o << "  } else { \\\n";
+    for (int q = 0; q < Q; ++q) {
+        o << "    w" << q << " = 0u";
+        for (int b = 0; b < 4 && 4 * q + b < N; ++b) o << " | ((unsigned)p_[" << 4 * q + b << "] << " << 8 * b << ")";
+        o << "; \\\n";
+    }
+    o << "  } }\n";
+    // evaluation
+    o << "#define DY_EVAL(";
+    for (int q = 0; q < Q; ++q) o << "w" << q << ", ";
+    o << "c, cp, bad) { \\\n";
+    o << "  bad = ((0u";
+    for (int q = 0; q < Q; ++q) o << " | w" << q;
+    o << ") & 0xC0C0C0C0u) != 0u; \\\n";
+    for (int n = 0; n < N; ++n) {
+        const int q = n / 4, b = n % 4;
+        o << "  const int ad" << n << " = (int)(" << (b == 0 ? "w" + std::to_string(q) + " << 2"
+                                                       : "w" + std::to_string(q) + " >> " + std::to_string(8 * b - 2))
+          << "); \\\n";
+        o << "  const float a" << n << " = __int_as_float(__builtin_amdgcn_ds_bpermute(ad" << n << ", A" << n
+          << ")); \\\n";
+        o << "  const float t" << n << " = __int_as_float(__builtin_amdgcn_ds_bpermute(ad" << n << ", T" << n
+          << ")); \\\n";
+    }
+    o << "  c = a0; \\\n";
+    for (int n = 1; n < N; ++n) o << "  c = c * a" << n << "; \\\n";
+    for (int n = 0; n < N; ++n) {
+        std::vector<int> preds;
+        for (int u = 0; u < n; ++u)
+            if (D.pred[n] >> u & 1u) preds.push_back(u);
+        o << "  const float f" << n << " = t" << n;
+        if (!preds.empty()) {
+            std::string m = "f" + std::to_string(preds[0]);
+            for (size_t k = 1; k < preds.size(); ++k) m = "fmaxf(" + m + ", f" + std::to_string(preds[k]) + ")";
+            o << " + " << m;
+        }
+        o << "; \\\n";
+    }
+    bool first = true;
+    for (int n = 0; n < N; ++n) {
+        if (!(D.sinks >> n & 1u)) continue;
+        if (first) {
+            o << "  cp = f" << n << "; \\\n";
+            first = false;
+        } else {
+            o << "  cp = fmaxf(cp, f" << n << "); \\\n";
+        }
+    }
+    o << "  bad = bad || (c != c); }\n";
+
+    const std::string words = [&] {
+        std::string s;
+        for (int q = 0; q < Q; ++q) s += (q ? ", w" : "w") + std::to_string(q);
+        return s;
+    }();
+    // scoring pass: two register sets (A, B) ping-pong so one row's loads stay
+    // in flight while the other row is scored; the trip count is wave-uniform
+    auto wl = [&](const char* p) {
+        std::string s;
+        for (int q = 0; q < Q; ++q) s += (q ? ", " : "") + std::string(p) + std::to_string(q);
+        return s;
+    };
+    o << "#define DY_LOADP(pp, " << wl("x") << ") { const unsigned char* p_ = (pp); \\\n  if (ALIGNED) { \\\n";
+    for (int q = 0; q < Q; ++q)
+        o << "    x" << q << " = __builtin_nontemporal_load((const unsigned*)p_ + " << q << "); \\\n";
+    o << "  } else { \\\n";
+    for (int q = 0; q < Q; ++q) {
+        o << "    x" << q << " = 0u";
+        for (int b = 0; b < 4 && 4 * q + b < N; ++b) o << " | ((unsigned)p_[" << 4 * q + b << "] << " << 8 * b << ")";
+        o << "; \\\n";
+    }
+    o << "  } __builtin_amdgcn_sched_barrier(0); }\n";
+    o << "#define DY_HANDLE(" << wl("y") << ", rr) { \\\n  float c, cp; bool bad; \\\n  DY_EVAL(" << wl("y")
+      << ", c, cp, bad) \\\n";
+    o << R"(  const bool live = (rr) < count; \
+  badmask |= __ballot(live && bad); \
+  const float th = __int_as_float(__builtin_amdgcn_ds_bpermute((int)(__float_as_uint(cp) >> sh), tbl)); \
+  bool want = live && !bad && c >= th; \
+  if (__ballot(want)) { \
+    if (want) { \
+      bool w2 = false; \
+      for (int k = 0; k < K; ++k) if (cp <= hi[k] && c >= thr[k]) w2 = true; \
+      want = w2; \
+    } \
+    const unsigned long long m_ = __ballot(want); \
+    if (m_) { \
+      const unsigned n_ = (unsigned)__builtin_popcountll(m_); \
+      if (qn + n_ > DY_QCAP) { \
+        ovf = true; /* queue full: the source is rescored after reseeding */ \
+      } else { \
+        if (want) { \
+          const unsigned o_ = qn + __builtin_amdgcn_mbcnt_hi((unsigned)(m_ >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m_, 0u)); \
+          q[o_].index = index_base + (rr); q[o_].corr = c; q[o_].cp = cp; \
+        } \
+        qn += n_; \
+      } \
+    } \
+  } }
+)";
+    // The load method is a template parameter and every load is issued
+    // unconditionally (pointers clamped to the last row), so the compiler can
+    // count the loads in flight and waits only for the row it scores.
+    o << R"(
+template <int ALIGNED>
+__device__ __forceinline__ void dy_scan_body(
+    const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count,
+    unsigned long long index_base, const float2* __restrict__ at, int rmax,
+    const unsigned* __restrict__ table, int bin_shift, const float* __restrict__ hi,
+    const float* __restrict__ thr, int K, DyCand* __restrict__ cand, unsigned cap,
+    unsigned* __restrict__ ncand, int* __restrict__ flags) {
+  DY_TABLES
+  __shared__ DyCand s_q[4][DY_QCAP];  // 16 KB
+  DyCand* q = s_q[threadIdx.x >> 6];
+  unsigned qn = 0;
+  bool ovf = false;
+  unsigned long long badmask = 0;
+  const int tbl = (int)table[lane];
+  const unsigned sh = (unsigned)bin_shift - 2u;
+  const unsigned long long G = (unsigned long long)gridDim.x * 256ull;
+  const unsigned long long wbase = (unsigned long long)blockIdx.x * 256ull + (threadIdx.x & ~63u);
+  if (wbase >= count) return;
+  unsigned long long iters = (count - wbase + G - 1) / G;
+  iters = ((unsigned long long)__builtin_amdgcn_readfirstlane((int)(iters >> 32)) << 32) |
+          (unsigned)__builtin_amdgcn_readfirstlane((int)iters);
+  unsigned long long r = wbase + lane;
+  const unsigned char* const plast = rows + (count - 1) * stride;
+  const unsigned long long step = G * stride;
+  const unsigned char* p = rows + r * stride;
+  unsigned )" << wl("u0") << ", " << wl("u1") << ", " << wl("u2") << ", " << wl("u3") << R"(;
+  // ring of four row buffers: three rows in flight while one is scored
+#define DY_CLAMP(x) ((x) <= plast ? (x) : plast)
+  DY_LOADP(DY_CLAMP(p), )" << wl("u0") << R"()
+  DY_LOADP(DY_CLAMP(p + step), )" << wl("u1") << R"()
+  DY_LOADP(DY_CLAMP(p + 2 * step), )" << wl("u2") << R"()
+  for (unsigned long long it = 0; it < iters; it += 4) {
+    DY_LOADP(DY_CLAMP(p + 3 * step), )" << wl("u3") << R"()
+    DY_HANDLE()" << wl("u0") << R"(, r)
+    DY_LOADP(DY_CLAMP(p + 4 * step), )" << wl("u0") << R"()
+    if (it + 1 < iters) DY_HANDLE()" << wl("u1") << R"(, r + G)
+    DY_LOADP(DY_CLAMP(p + 5 * step), )" << wl("u1") << R"()
+    if (it + 2 < iters) DY_HANDLE()" << wl("u2") << R"(, r + 2 * G)
+    DY_LOADP(DY_CLAMP(p + 6 * step), )" << wl("u2") << R"()
+    if (it + 3 < iters) DY_HANDLE()" << wl("u3") << R"(, r + 3 * G)
+    p += 4 * step;
+    r += 4 * G;
+  }
+  dy_flush(q, qn, lane, cand, cap, ncand, &ovf);
+  if (lane == 0 && (badmask || ovf)) atomicOr(flags, (badmask ? 2 : 0) | (ovf ? 1 : 0));
+}
+
+#define DY_SCAN_ARGS \
+    const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count, \
+    unsigned long long index_base, const float2* __restrict__ at, int rmax, \
+    const unsigned* __restrict__ table, int bin_shift, const float* __restrict__ hi, \
+    const float* __restrict__ thr, int K, DyCand* __restrict__ cand, unsigned cap, \
+    unsigned* __restrict__ ncand, int* __restrict__ flags
+#define DY_SCAN_PASS rows, stride, count, index_base, at, rmax, table, bin_shift, hi, thr, K, cand, cap, ncand, flags
+extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_a(DY_SCAN_ARGS) { dy_scan_body<1>(DY_SCAN_PASS); }
+extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) { dy_scan_body<0>(DY_SCAN_PASS); }
+
+)";
+    o << R"(extern "C" __global__ void __launch_bounds__(256) dy_rows_sample(
+    const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count,
+    const float2* __restrict__ at, int rmax, const float* __restrict__ lo, int K,
+    unsigned* __restrict__ scert, unsigned long long S, int aligned) {
+  DY_TABLES
+  const unsigned long long nsamp = (count + S - 1) / S;
+  const unsigned long long t0 = (unsigned long long)blockIdx.x * 256ull;
+  if (t0 >= nsamp) return;
+  const unsigned long long t = t0 + threadIdx.x;
+  const bool live = t < nsamp;
+  const unsigned long long rr = dy_sample_row(live ? t : nsamp - 1, S, count);
+  unsigned )" << words << R"(;
+  DY_LOAD(rr, )" << words << R"()
+  float c, cp; bool bad;
+  DY_EVAL()" << words << R"(, c, cp, bad)
+  const bool ok = live && !bad;
+  for (int k = 0; k < K; ++k) {
+    const unsigned e = dy_wmax((ok && cp <= lo[k]) ? __float_as_uint(c) + 1u : 0u);
+    if (lane == 0 && e) atomicMax(scert + k * 64 + ((blockIdx.x * 4 + (threadIdx.x >> 6)) % 64), e);
+  }
+}
+)";
+    return o.str();
+}
+
+}  // namespace
+
+// Compile (or fetch from the process cache) the rows kernels of problem D for
+// `device`.  Returns false with a message when the problem does not qualify
+// or runtime compilation is unavailable.
+bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err) {
+    for (int n = 0; n < D.n; ++n)
+        if (D.radix[n] > 64) {
+            *err = "a node has more than 64 implementations";
+            return false;
+        }
+    static_assert(NSLOT == 64, "generated sampler writes 64 slots per level");
+    const std::string src = gen_source(D);
+    const std::string key = std::to_string(device) + "\n" + src;
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) {
+        *out = it->second;
+        return true;
+    }
+    hiprtcProgram prog;
+    if (hiprtcCreateProgram(&prog, src.c_str(), "dyplan_rows.hip", 0, nullptr, nullptr) != HIPRTC_SUCCESS) {
+        *err = "hiprtcCreateProgram failed";
+        return false;
+    }
+    hipDeviceProp_t prop;
+    std::string arch = "--offload-arch=gfx950";
+    if (hipGetDeviceProperties(&prop, device) == hipSuccess) arch = std::string("--offload-arch=") + prop.gcnArchName;
+    const char* opts[] = {arch.c_str(), "-O3", "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang",
+                          "-packed-fp32-ops"};
+    const hiprtcResult rc = hiprtcCompileProgram(prog, 7, opts);
+    if (rc != HIPRTC_SUCCESS) {
+        size_t n = 0;
+        hiprtcGetProgramLogSize(prog, &n);
+        std::string log(n, '\0');
+        if (n) hiprtcGetProgramLog(prog, &log[0]);
+        *err = std::string("hiprtc compile failed: ") + log.substr(0, 400);
+        hiprtcDestroyProgram(&prog);
+        return false;
+    }
+    size_t sz = 0;
+    hiprtcGetCodeSize(prog, &sz);
+    std::vector<char> code(sz);
+    hiprtcGetCode(prog, code.data());
+    hiprtcDestroyProgram(&prog);
+    JitRows j;
+    if (hipModuleLoadData(&j.mod, code.data()) != hipSuccess ||
+        hipModuleGetFunction(&j.scan, j.mod, "dy_rows_scan_a") != hipSuccess ||
+        hipModuleGetFunction(&j.scan_u, j.mod, "dy_rows_scan_u") != hipSuccess ||
+        hipModuleGetFunction(&j.sample, j.mod, "dy_rows_sample") != hipSuccess) {
+        *err = "loading the compiled rows kernels failed";
+        return false;
+    }
+    g_cache[key] = j;  // modules stay loaded for the life of the process
+    *out = j;
+    return true;
+}
+
+// Source of the kernels for a problem (diagnostics and tests).
+std::string jit_rows_source(const ProbDev& D) { return gen_source(D); }
+
+}  // namespace dyp

@@ -272,8 +272,10 @@ __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big,
     return Prefix{pc, px, py, s};
 }
 
+// ds_bpermute selects lane (address >> 2) & 63 and ignores the other address
+// bits, so the shifted CP pattern needs no mask (checked on gfx950)
 #ifndef DYP_BPERM_MASK
-#define DYP_BPERM_MASK 1
+#define DYP_BPERM_MASK 0
 #endif
 
 // One plan of the inner sweep: corr = cx * a_y, CP = max(tau_y + M, S2); the

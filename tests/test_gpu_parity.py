@@ -373,3 +373,55 @@ def test_overflow_recovered_by_reseeding():
         st = plan.stats()
     assert_choices(got, orc.select_range(prob, begin, count), "reseeded")
     assert st.fallbacks == 0
+
+
+@pytest.mark.parametrize("jit", [1, 0])
+def test_rows_generated_and_generic_kernels(jit):
+    rng = np.random.default_rng(404)
+    probs, rows_list = [], []
+    for trial in range(6):
+        n = int(rng.integers(1, 12))
+        prob = tiny_problem(rng, n, 6, int(rng.integers(1, 5)), 2, True)
+        cnt = int(rng.integers(1, 70000))
+        rows = np.stack([rng.integers(0, r, size=cnt) for r in prob.radix], axis=1).astype(np.uint8)
+        probs.append(prob)
+        rows_list.append(rows)
+    with D.Plan(probs) as plan:
+        plan.set_option(D.DY_OPT_JIT, jit)
+        for t, (prob, rows) in enumerate(zip(probs, rows_list)):
+            d = torch.from_numpy(np.ascontiguousarray(rows)).cuda()
+            got = plan.select([D.rows_source(t, d, rows.shape[0], rows.shape[1], 77)], stream=stream())[0]
+            assert_choices(got, orc.select_rows(prob, rows, 77), f"rows trial {t} jit={jit}")
+
+
+def test_rows_bad_ids_rejected_by_generated_kernel():
+    prob = wl.stream24()
+    rows = wl.make_rows(20000, 24, 36)
+    with D.Plan(prob) as plan:
+        for bad in (36, 63, 64, 200):
+            r = rows.copy()
+            r[12345, 7] = bad
+            with pytest.raises(D.DyplanError) as e:
+                plan.select([D.rows_source(0, torch.from_numpy(r).cuda(), 20000, 24)], stream=stream())
+            assert e.value.status == D.DY_EINVAL
+        got = plan.select([D.rows_source(0, torch.from_numpy(rows).cuda(), 20000, 24)], stream=stream())[0]
+        assert_choices(got, orc.select_rows(prob, rows), "after bad rows")
+
+
+def test_rows_radix_above_64_uses_generic_path():
+    rng = np.random.default_rng(505)
+    prob = tiny_problem(rng, 3, 2, 2, 2, True)
+    R = 100
+    prob.radix = np.array([R, 3, R], np.int32)
+    for name in ("p", "tau", "size", "backend"):
+        a = getattr(prob, name)
+        b = np.zeros((3, R), a.dtype)
+        b[:, :a.shape[1]] = a
+        for c in range(a.shape[1], R):
+            b[:, c] = a[:, c % a.shape[1]] * (1 if name in ("backend", "size") else 0.999)
+        setattr(prob, name, b)
+    prob.slo = 1e9
+    rows = np.stack([rng.integers(0, r, size=30000) for r in prob.radix], axis=1).astype(np.uint8)
+    with D.Plan(prob) as plan:
+        got = plan.select([D.rows_source(0, torch.from_numpy(rows).cuda(), 30000, 3)], stream=stream())[0]
+    assert_choices(got, orc.select_rows(prob, rows), "radix 100 rows")
