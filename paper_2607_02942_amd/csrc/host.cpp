@@ -734,16 +734,17 @@ hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sampl
     unsigned long long rows_stride = J.stride, count = J.count, index_base = J.index_base;
     const unsigned char* rows = J.rows;
     const float2* at = D.at;
-    int rmax = D.rmax, K = D.k, bin_shift = D.bin_shift;
+    int rmax = D.rmax, bin_shift = D.bin_shift;
     int aligned = ((J.stride | (uint64_t)(uintptr_t)J.rows | (uint64_t)D.n) & 3u) == 0 ? 1 : 0;
     const float* hi = (const float*)((const char*)dp + offsetof(ProbDev, hi));
     const float* lo = (const float*)((const char*)dp + offsetof(ProbDev, lo));
     if (sample) {
         unsigned* scert = J.scert;
         unsigned long long S = J.sample_stride;
-        void* args[] = {&rows, &rows_stride, &count, &at, &rmax, &lo, &K, &scert, &S, &aligned};
+        void* args[] = {&rows, &rows_stride, &count, &at, &rmax, &lo, &scert, &S, &aligned};
         const unsigned long long nsamp = (count + S - 1) / S;
-        const unsigned gx = (unsigned)std::min<unsigned long long>((nsamp + 255) / 256, 1ull << 22);
+        const unsigned gx = (unsigned)std::max<unsigned long long>(
+            1, std::min<unsigned long long>((nsamp + 255) / 256, 8ull * (unsigned)h->cus));
         return hipModuleLaunchKernel(jr.sample, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
     }
     const unsigned* table = J.table;
@@ -752,7 +753,7 @@ hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sampl
     unsigned cap = J.cap;
     unsigned* ncand = J.ncand;
     int* flags = J.flags;
-    void* args[] = {&rows, &rows_stride, &count, &index_base, &at, &rmax, &table, &bin_shift, &hi, &thr, &K,
+    void* args[] = {&rows, &rows_stride, &count, &index_base, &at, &rmax, &table, &bin_shift, &hi, &thr,
                     &cand, &cap, &ncand, &flags};
     hipFunction_t fn = aligned ? jr.scan : jr.scan_u;
     int per_cu = 0;

@@ -3,18 +3,20 @@
 // hiprtc for the running device.
 //
 // A row is N bytes, byte n = implementation id of node n.  Every node's table
-// (factor a = 1 - w(1 - p) and duration tau, fp32) sits lane-resident in two
-// VGPRs (entry i in lane i, R <= 64) and is gathered with ds_bpermute, whose
-// lane select is bits [7:2] of the address: the id byte only needs shifting
-// into place.  The recurrence is unrolled in node order with every f_n in a
-// register, so each plan costs N-1 multiplies, one add per node and one max
-// per extra predecessor; the rows stream through non-temporal dword loads,
-// the next row's words in flight while the current row is scored.
+// (factor a = 1 - w(1 - p) and duration tau, fp32) sits in LDS as 64 float2
+// entries, so one ds_read_b64 per node fetches both values; on gfx950 a
+// random 8-byte LDS read costs about half the issue time of a lane permute
+// and a quarter of the two permutes it replaces.  The recurrence is unrolled
+// in node order with every f_n in a register: N-1 multiplies, one add per
+// node and one max per extra predecessor.  The rows stream through
+// non-temporal dword loads, three rows in flight while one is scored.
 //
-// Ids >= 64 are caught from the OR of the row words; ids in [R_n, 64) read
-// NaN padding and surface as a NaN corr.  The arithmetic is that of the
-// generic kernels (same fp32 operations in the same order), so both produce
-// identical scores.
+// Ids outside [0, R_n) are caught per byte without a lookup: with b' = b & 127,
+// b' + (128 - R_n) has bit 7 set exactly when b' >= R_n (no carry leaves the
+// byte since R_n <= 64), and b >= 128 sets bit 7 of b itself.  Table indices
+// are taken mod 64, so every LDS read stays inside its node's table.  The
+// arithmetic is that of the generic kernels (same fp32 operations in the
+// same order), so both produce identical scores.
 #include <hip/hip_runtime.h>
 #include <hip/hiprtc.h>
 
@@ -83,53 +85,72 @@ std::string gen_source(const ProbDev& D) {
     const int Q = (N + 3) / 4;
     std::ostringstream o;
     o << kCommon;
-    // lane-resident tables
-    o << "#define DY_TABLES \\\n  const int lane = threadIdx.x & 63; \\\n";
-    for (int n = 0; n < N; ++n) {
-        o << "  const float2 e" << n << " = at[" << n << " * rmax + (lane < " << D.radix[n] << " ? lane : 0)]; \\\n";
-        o << "  const int A" << n << " = lane < " << D.radix[n] << " ? __float_as_int(e" << n
-          << ".x) : 0x7fc00000; \\\n";
-        o << "  const int T" << n << " = lane < " << D.radix[n] << " ? __float_as_int(e" << n
-          << ".y) : 0x7fc00000; \\\n";
-    }
-    o << "\n";
-    // row loads: whole dwords when aligned, else bytes
-    o << "#define DY_LOAD(rr";
-    for (int q = 0; q < Q; ++q) o << ", w" << q;
-    o << ") { \\\n  const unsigned char* p_ = rows + (rr) * stride; \\\n  if (aligned) { \\\n";
-    for (int q = 0; q < Q; ++q)
-        o << "    w" << q << " = __builtin_nontemporal_load((const unsigned*)p_ + " << q << "); \\\n";
-    o << "  } else { \\\n";
+    o << "#define DY_N " << N << "\n#define DY_K " << D.k << "\n";
+    // per-word constants of the id range check (bytes past node N-1 are zero)
     for (int q = 0; q < Q; ++q) {
-        o << "    w" << q << " = 0u";
-        for (int b = 0; b < 4 && 4 * q + b < N; ++b) o << " | ((unsigned)p_[" << 4 * q + b << "] << " << 8 * b << ")";
-        o << "; \\\n";
+        unsigned m7 = 0, kk = 0;
+        for (int b = 0; b < 4 && 4 * q + b < N; ++b) {
+            m7 |= 0x7Fu << (8 * b);
+            kk |= (unsigned)(0x80 - D.radix[4 * q + b]) << (8 * b);
+        }
+        o << "#define DY_M7_" << q << " 0x" << std::hex << m7 << "u\n#define DY_K_" << q << " 0x" << kk << std::dec
+          << "u\n";
     }
-    o << "  } }\n";
-    // evaluation
-    o << "#define DY_EVAL(";
-    for (int q = 0; q < Q; ++q) o << "w" << q << ", ";
-    o << "c, cp, bad) { \\\n";
-    o << "  bad = ((0u";
-    for (int q = 0; q < Q; ++q) o << " | w" << q;
-    o << ") & 0xC0C0C0C0u) != 0u; \\\n";
+    // node tables (and the prefilter bins) into LDS
+    o << R"(
+__device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax,
+                                         const unsigned* __restrict__ table, float2* s_tab, float* s_bins) {
+  for (int i = threadIdx.x; i < DY_N * 64; i += blockDim.x) {
+    const int n = i >> 6, e = i & 63;
+    s_tab[i] = e < rmax ? at[n * rmax + e] : make_float2(__builtin_nanf(""), __builtin_nanf(""));
+  }
+  if (table != nullptr && threadIdx.x < 64) s_bins[threadIdx.x] = __uint_as_float(table[threadIdx.x]);
+  __syncthreads();
+}
+)";
+    auto wl = [&](const char* p) {
+        std::string r;
+        for (int q = 0; q < Q; ++q) r += (q ? ", " : "") + std::string(p) + std::to_string(q);
+        return r;
+    };
+    auto load_body = [&](const char* dst, const char* cond) {
+        o << "  if (" << cond << ") { \\\n";
+        for (int q = 0; q < Q; ++q)
+            o << "    " << dst << q << " = __builtin_nontemporal_load((const unsigned*)p_ + " << q << "); \\\n";
+        o << "  } else { \\\n";
+        for (int q = 0; q < Q; ++q) {
+            o << "    " << dst << q << " = 0u";
+            for (int b = 0; b < 4 && 4 * q + b < N; ++b)
+                o << " | ((unsigned)p_[" << 4 * q + b << "] << " << 8 * b << ")";
+            o << "; \\\n";
+        }
+        o << "  }";
+    };
+    // row loads: whole dwords when aligned, else bytes
+    o << "#define DY_LOAD(rr, " << wl("w") << ") { \\\n  const unsigned char* p_ = rows + (rr) * stride; \\\n";
+    load_body("w", "aligned");
+    o << " }\n";
+    o << "#define DY_LOADP(pp, " << wl("x") << ") { const unsigned char* p_ = (pp); \\\n";
+    load_body("x", "ALIGNED");
+    o << " __builtin_amdgcn_sched_barrier(0); }\n";
+    // evaluation of one row held in words w0..
+    o << "#define DY_EVAL(" << wl("w") << ", c, cp, bad) { \\\n  unsigned bk_ = 0u; \\\n";
+    for (int q = 0; q < Q; ++q)
+        o << "  bk_ |= ((w" << q << " & DY_M7_" << q << ") + DY_K_" << q << ") | w" << q << "; \\\n";
+    o << "  bad = (bk_ & 0x80808080u) != 0u; \\\n";
     for (int n = 0; n < N; ++n) {
         const int q = n / 4, b = n % 4;
-        o << "  const int ad" << n << " = (int)(" << (b == 0 ? "w" + std::to_string(q) + " << 2"
-                                                       : "w" + std::to_string(q) + " >> " + std::to_string(8 * b - 2))
-          << "); \\\n";
-        o << "  const float a" << n << " = __int_as_float(__builtin_amdgcn_ds_bpermute(ad" << n << ", A" << n
-          << ")); \\\n";
-        o << "  const float t" << n << " = __int_as_float(__builtin_amdgcn_ds_bpermute(ad" << n << ", T" << n
-          << ")); \\\n";
+        o << "  const float2 e" << n << " = s_tab[" << n * 64 << " + ((w" << q;
+        if (b) o << " >> " << 8 * b;
+        o << ") & 63u)]; \\\n";
     }
-    o << "  c = a0; \\\n";
-    for (int n = 1; n < N; ++n) o << "  c = c * a" << n << "; \\\n";
+    o << "  c = e0.x; \\\n";
+    for (int n = 1; n < N; ++n) o << "  c = c * e" << n << ".x; \\\n";
     for (int n = 0; n < N; ++n) {
         std::vector<int> preds;
         for (int u = 0; u < n; ++u)
             if (D.pred[n] >> u & 1u) preds.push_back(u);
-        o << "  const float f" << n << " = t" << n;
+        o << "  const float f" << n << " = e" << n << ".y";
         if (!preds.empty()) {
             std::string m = "f" + std::to_string(preds[0]);
             for (size_t k = 1; k < preds.size(); ++k) m = "fmaxf(" + m + ", f" + std::to_string(preds[k]) + ")";
@@ -140,47 +161,22 @@ std::string gen_source(const ProbDev& D) {
     bool first = true;
     for (int n = 0; n < N; ++n) {
         if (!(D.sinks >> n & 1u)) continue;
-        if (first) {
-            o << "  cp = f" << n << "; \\\n";
-            first = false;
-        } else {
-            o << "  cp = fmaxf(cp, f" << n << "); \\\n";
-        }
+        o << (first ? "  cp = f" : "  cp = fmaxf(cp, f") << n << (first ? "; \\\n" : "); \\\n");
+        first = false;
     }
-    o << "  bad = bad || (c != c); }\n";
-
-    const std::string words = [&] {
-        std::string s;
-        for (int q = 0; q < Q; ++q) s += (q ? ", w" : "w") + std::to_string(q);
-        return s;
-    }();
-    // scoring pass: two register sets (A, B) ping-pong so one row's loads stay
-    // in flight while the other row is scored; the trip count is wave-uniform
-    auto wl = [&](const char* p) {
-        std::string s;
-        for (int q = 0; q < Q; ++q) s += (q ? ", " : "") + std::string(p) + std::to_string(q);
-        return s;
-    };
-    o << "#define DY_LOADP(pp, " << wl("x") << ") { const unsigned char* p_ = (pp); \\\n  if (ALIGNED) { \\\n";
-    for (int q = 0; q < Q; ++q)
-        o << "    x" << q << " = __builtin_nontemporal_load((const unsigned*)p_ + " << q << "); \\\n";
-    o << "  } else { \\\n";
-    for (int q = 0; q < Q; ++q) {
-        o << "    x" << q << " = 0u";
-        for (int b = 0; b < 4 && 4 * q + b < N; ++b) o << " | ((unsigned)p_[" << 4 * q + b << "] << " << 8 * b << ")";
-        o << "; \\\n";
-    }
-    o << "  } __builtin_amdgcn_sched_barrier(0); }\n";
+    o << "}\n";
+    // one row of the scoring pass: prefilter by the bin of its CP, exact
+    // per-level test, then the wave's LDS candidate queue
     o << "#define DY_HANDLE(" << wl("y") << ", rr) { \\\n  float c, cp; bool bad; \\\n  DY_EVAL(" << wl("y")
       << ", c, cp, bad) \\\n";
     o << R"(  const bool live = (rr) < count; \
   badmask |= __ballot(live && bad); \
-  const float th = __int_as_float(__builtin_amdgcn_ds_bpermute((int)(__float_as_uint(cp) >> sh), tbl)); \
+  const float th = s_bins[(__float_as_uint(cp) >> bin_shift) & 63u]; \
   bool want = live && !bad && c >= th; \
   if (__ballot(want)) { \
     if (want) { \
       bool w2 = false; \
-      for (int k = 0; k < K; ++k) if (cp <= hi[k] && c >= thr[k]) w2 = true; \
+      for (int k = 0; k < DY_K; ++k) if (cp <= hi[k] && c >= thr[k]) w2 = true; \
       want = w2; \
     } \
     const unsigned long long m_ = __ballot(want); \
@@ -207,16 +203,17 @@ __device__ __forceinline__ void dy_scan_body(
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count,
     unsigned long long index_base, const float2* __restrict__ at, int rmax,
     const unsigned* __restrict__ table, int bin_shift, const float* __restrict__ hi,
-    const float* __restrict__ thr, int K, DyCand* __restrict__ cand, unsigned cap,
+    const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap,
     unsigned* __restrict__ ncand, int* __restrict__ flags) {
-  DY_TABLES
-  __shared__ DyCand s_q[4][DY_QCAP];  // 16 KB
+  __shared__ float2 s_tab[DY_N * 64];
+  __shared__ float s_bins[64];
+  __shared__ DyCand s_q[4][DY_QCAP];
+  dy_stage(at, rmax, table, s_tab, s_bins);
+  const int lane = threadIdx.x & 63;
   DyCand* q = s_q[threadIdx.x >> 6];
   unsigned qn = 0;
   bool ovf = false;
   unsigned long long badmask = 0;
-  const int tbl = (int)table[lane];
-  const unsigned sh = (unsigned)bin_shift - 2u;
   const unsigned long long G = (unsigned long long)gridDim.x * 256ull;
   const unsigned long long wbase = (unsigned long long)blockIdx.x * 256ull + (threadIdx.x & ~63u);
   if (wbase >= count) return;
@@ -253,31 +250,38 @@ __device__ __forceinline__ void dy_scan_body(
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count, \
     unsigned long long index_base, const float2* __restrict__ at, int rmax, \
     const unsigned* __restrict__ table, int bin_shift, const float* __restrict__ hi, \
-    const float* __restrict__ thr, int K, DyCand* __restrict__ cand, unsigned cap, \
+    const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap, \
     unsigned* __restrict__ ncand, int* __restrict__ flags
-#define DY_SCAN_PASS rows, stride, count, index_base, at, rmax, table, bin_shift, hi, thr, K, cand, cap, ncand, flags
+#define DY_SCAN_PASS rows, stride, count, index_base, at, rmax, table, bin_shift, hi, thr, cand, cap, ncand, flags
 extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_a(DY_SCAN_ARGS) { dy_scan_body<1>(DY_SCAN_PASS); }
 extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) { dy_scan_body<0>(DY_SCAN_PASS); }
 
 )";
+    // seeding pass: hashed sample rows, grid-stride; per level the largest
+    // certified corr (ordered bits + 1) of the thread, reduced per wave at the end
     o << R"(extern "C" __global__ void __launch_bounds__(256) dy_rows_sample(
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count,
-    const float2* __restrict__ at, int rmax, const float* __restrict__ lo, int K,
+    const float2* __restrict__ at, int rmax, const float* __restrict__ lo,
     unsigned* __restrict__ scert, unsigned long long S, int aligned) {
-  DY_TABLES
+  __shared__ float2 s_tab[DY_N * 64];
+  dy_stage(at, rmax, nullptr, s_tab, nullptr);
+  const int lane = threadIdx.x & 63;
   const unsigned long long nsamp = (count + S - 1) / S;
-  const unsigned long long t0 = (unsigned long long)blockIdx.x * 256ull;
-  if (t0 >= nsamp) return;
-  const unsigned long long t = t0 + threadIdx.x;
-  const bool live = t < nsamp;
-  const unsigned long long rr = dy_sample_row(live ? t : nsamp - 1, S, count);
-  unsigned )" << words << R"(;
-  DY_LOAD(rr, )" << words << R"()
-  float c, cp; bool bad;
-  DY_EVAL()" << words << R"(, c, cp, bad)
-  const bool ok = live && !bad;
-  for (int k = 0; k < K; ++k) {
-    const unsigned e = dy_wmax((ok && cp <= lo[k]) ? __float_as_uint(c) + 1u : 0u);
+  const unsigned long long G = (unsigned long long)gridDim.x * 256ull;
+  unsigned best[DY_K];
+  for (int k = 0; k < DY_K; ++k) best[k] = 0u;
+  for (unsigned long long t = (unsigned long long)blockIdx.x * 256ull + threadIdx.x; t < nsamp; t += G) {
+    const unsigned long long rr = dy_sample_row(t, S, count);
+    unsigned )" << wl("w") << R"(;
+    DY_LOAD(rr, )" << wl("w") << R"()
+    float c, cp; bool bad;
+    DY_EVAL()" << wl("w") << R"(, c, cp, bad)
+    if (!bad)
+      for (int k = 0; k < DY_K; ++k)
+        if (cp <= lo[k]) best[k] = max(best[k], __float_as_uint(c) + 1u);
+  }
+  for (int k = 0; k < DY_K; ++k) {
+    const unsigned e = dy_wmax(best[k]);
     if (lane == 0 && e) atomicMax(scert + k * 64 + ((blockIdx.x * 4 + (threadIdx.x >> 6)) % 64), e);
   }
 }
