@@ -54,6 +54,12 @@ struct ProbDev {
     // bound: the bin's largest CP decides)
     uint32_t jtab[NBINS];
     int32_t lvl_order[KMAX];
+    // bounds for abandoning a streamed row part-way (uniform mode):
+    // corr_tail[m] >= the fp32 product of every node m..N-1's largest factor,
+    // with slack for N roundings; lat_tail[n] <= the fp32 sum of the smallest
+    // durations along the cheapest path from n's successors to a sink
+    float corr_tail[NMAX + 1];
+    float lat_tail[NMAX];
     // device tables
     const float2* at;         // [n][rmax] (factor a = 1 - w(1-p), duration tau), fp32
     const float2* atx;        // rows of x and y in `at` (x: a 1-entry (1, 0) row when virtual)

@@ -499,6 +499,26 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         float2* atx = (float2*)(img.data() + L.atx);
         *atx = make_float2(1.0f, 0.0f);
         // fp32 bounds of the unpressured CP (the recurrence is monotone in every duration)
+        // tail bounds: exact products and sums in fp64, then widened by 2^-18
+        // relative (more than N <= 32 fp32 roundings) and rounded outward
+        {
+            double tail = 1.0;
+            D.corr_tail[N] = 1.0f;
+            for (int n = N - 1; n >= 0; --n) {
+                float amax = 0.0f;
+                for (int i = 0; i < pb.radix[n]; ++i) amax = std::max(amax, at[(size_t)n * R + i].x);
+                tail *= (double)amax;
+                D.corr_tail[n] = round_up(tail * (1.0 + 0x1p-18));
+            }
+            double rest[DY_MAX_NODES];
+            for (int n = N - 1; n >= 0; --n) {
+                double best = INFINITY;
+                for (int v = n + 1; v < N; ++v)
+                    if (D.pred[v] >> n & 1u) best = std::min(best, (double)dmin[v] + rest[v]);
+                rest[n] = std::isinf(best) ? 0.0 : best;
+                D.lat_tail[n] = round_down(rest[n] * (1.0 - 0x1p-18));
+            }
+        }
         const float clo = cp32(N, D.pred, D.sinks, dmin);
         const float chi = cp32(N, D.pred, D.sinks, dmax);
         D.cp_lo_bits = f2u(clo);

@@ -8,19 +8,24 @@
 // random 8-byte LDS read costs about half the issue time of a lane permute
 // and a quarter of the two permutes it replaces.  The recurrence is unrolled
 // in node order with every f_n in a register: N-1 multiplies, one add per
-// node and one max per extra predecessor.  The rows stream through
-// non-temporal dword loads, three rows in flight while one is scored.
+// node and one max per extra predecessor.  The rows stream through plain
+// dword loads (on gfx950 non-temporal loads of 24-byte rows stream about 10%
+// slower), three rows in flight while one is scored.
 //
-// Ids outside [0, R_n) are caught per byte without a lookup: with b' = b & 127,
-// b' + (128 - R_n) has bit 7 set exactly when b' >= R_n (no carry leaves the
-// byte since R_n <= 64), and b >= 128 sets bit 7 of b itself.  Table indices
-// are taken mod 64, so every LDS read stays inside its node's table.  The
+// Ids outside [0, R_n) are caught per byte without a lookup, two operations
+// per word: bit 7 of byte n of (w + sum_n (128 - R_n) 256^n) | w is set iff
+// b_n >= R_n.  For b_n < 128 the sum b_n + 128 - R_n stays below 256 (R_n <=
+// 64, so no carry leaves the byte, and a carry coming in from a byte below
+// cannot clear bit 7 of a byte that already has it); b_n >= 128 sets bit 7 of
+// w itself.  Table indices are taken mod 64, so every LDS read stays inside
+// its node's table whatever the row holds.  The
 // arithmetic is that of the generic kernels (same fp32 operations in the
 // same order), so both produce identical scores.
 #include <hip/hip_runtime.h>
 #include <hip/hiprtc.h>
 
 #include <cstdio>
+#include <cstring>
 #include <map>
 #include <mutex>
 #include <sstream>
@@ -59,7 +64,7 @@ __device__ __forceinline__ unsigned dy_wmax(unsigned v) {
 // store (those would make it wait for the rows in flight).  The queue goes to
 // the global candidate list at the end; a full queue raises the overflow flag,
 // which the host resolves exactly by reseeding and rescoring the source.
-#define DY_QCAP 256
+#define DY_QCAP 128
 __device__ void dy_flush(DyCand* q, unsigned qn, int lane, DyCand* cand, unsigned cap, unsigned* ncand,
                          bool* ovf) {
   if (qn == 0) return;
@@ -80,6 +85,29 @@ __device__ __forceinline__ unsigned long long dy_sample_row(unsigned long long j
 }
 )";
 
+// a float as an exact hexadecimal literal
+std::string flit(float x) {
+    char buf[48];
+    std::snprintf(buf, sizeof buf, "%af", (double)x);
+    return buf;
+}
+
+float u2f(unsigned u) {
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+// nodes after which the scoring pass may abandon a wave's rows: past the
+// middle of the DAG, where the remaining factors can no longer lift most rows
+std::vector<int> checkpoints(int N) {
+    std::vector<int> cuts;
+    if (N < 8) return cuts;
+    for (int m : {N / 2 - 1, N / 2 + 1, N / 2 + 3, (3 * N) / 4})
+        if (m >= 2 && m < N - 1 && (cuts.empty() || m > cuts.back())) cuts.push_back(m);
+    return cuts;
+}
+
 std::string gen_source(const ProbDev& D) {
     const int N = D.n;
     const int Q = (N + 3) / 4;
@@ -88,13 +116,9 @@ std::string gen_source(const ProbDev& D) {
     o << "#define DY_N " << N << "\n#define DY_K " << D.k << "\n";
     // per-word constants of the id range check (bytes past node N-1 are zero)
     for (int q = 0; q < Q; ++q) {
-        unsigned m7 = 0, kk = 0;
-        for (int b = 0; b < 4 && 4 * q + b < N; ++b) {
-            m7 |= 0x7Fu << (8 * b);
-            kk |= (unsigned)(0x80 - D.radix[4 * q + b]) << (8 * b);
-        }
-        o << "#define DY_M7_" << q << " 0x" << std::hex << m7 << "u\n#define DY_K_" << q << " 0x" << kk << std::dec
-          << "u\n";
+        unsigned kk = 0;
+        for (int b = 0; b < 4 && 4 * q + b < N; ++b) kk |= (unsigned)(0x80 - D.radix[4 * q + b]) << (8 * b);
+        o << "#define DY_K_" << q << " 0x" << std::hex << kk << std::dec << "u\n";
     }
     // node tables (and the prefilter bins) into LDS
     o << R"(
@@ -116,7 +140,7 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
     auto load_body = [&](const char* dst, const char* cond) {
         o << "  if (" << cond << ") { \\\n";
         for (int q = 0; q < Q; ++q)
-            o << "    " << dst << q << " = __builtin_nontemporal_load((const unsigned*)p_ + " << q << "); \\\n";
+            o << "    " << dst << q << " = ((const unsigned*)p_)[" << q << "]; \\\n";
         o << "  } else { \\\n";
         for (int q = 0; q < Q; ++q) {
             o << "    " << dst << q << " = 0u";
@@ -136,7 +160,7 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
     // evaluation of one row held in words w0..
     o << "#define DY_EVAL(" << wl("w") << ", c, cp, bad) { \\\n  unsigned bk_ = 0u; \\\n";
     for (int q = 0; q < Q; ++q)
-        o << "  bk_ |= ((w" << q << " & DY_M7_" << q << ") + DY_K_" << q << ") | w" << q << "; \\\n";
+        o << "  bk_ |= (w" << q << " + DY_K_" << q << ") | w" << q << "; \\\n";
     o << "  bad = (bk_ & 0x80808080u) != 0u; \\\n";
     for (int n = 0; n < N; ++n) {
         const int q = n / 4, b = n % 4;
@@ -165,21 +189,82 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         first = false;
     }
     o << "}\n";
-    // one row of the scoring pass: prefilter by the bin of its CP, exact
-    // per-level test, then the wave's LDS candidate queue
-    o << "#define DY_HANDLE(" << wl("y") << ", rr) { \\\n  float c, cp; bool bad; \\\n  DY_EVAL(" << wl("y")
-      << ", c, cp, bad) \\\n";
-    o << R"(  const bool live = (rr) < count; \
-  badmask |= __ballot(live && bad); \
-  const float th = s_bins[(__float_as_uint(cp) >> bin_shift) & 63u]; \
-  bool want = live && !bad && c >= th; \
-  if (__ballot(want)) { \
+    // one row of the scoring pass.  The nodes are evaluated in segments; at
+    // the end of each but the last the wave abandons its rows when none can
+    // still become a candidate: the corr so far times corr_tail (an upper
+    // bound on the final fp32 corr) is below the prefilter threshold of a
+    // lower bound on the final fp32 CP (the largest f_n + lat_tail[n] over the
+    // evaluated nodes without an evaluated successor, less 2^-18 relative,
+    // and never below the smallest CP).  Thresholds below 2^-60 never
+    // abandon, so every product the bound reasons about is a normal number.
+    // Rows that reach the end take the prefilter by the bin of their CP, the
+    // exact per-level test, then the wave's LDS candidate queue.
+    {
+        const std::vector<int> cuts = checkpoints(N);
+        o << "#define DY_HANDLE(" << wl("y") << ", rr, LIVE) { \\\n  const bool live = (LIVE); \\\n"
+          << "  unsigned bk_ = 0u; \\\n";
+        for (int q = 0; q < Q; ++q)
+            o << "  bk_ |= (y" << q << " + DY_K_" << q << ") | y" << q << "; \\\n";
+        o << "  const bool bad = (bk_ & 0x80808080u) != 0u; \\\n  badmask |= __builtin_amdgcn_ballot_w64(live && bad); \\\n"
+          << "  const bool ok = live && !bad; \\\n  do { \\\n  float c, cp; \\\n";
+        int n0 = 0;
+        std::vector<int> ends = cuts;
+        ends.push_back(N);
+        for (int m : ends) {
+            for (int n = n0; n < m; ++n) {
+                const int q = n / 4, bb = n % 4;
+                o << "  const float2 e" << n << " = s_tab[" << n * 64 << " + ((y" << q;
+                if (bb) o << " >> " << 8 * bb;
+                o << ") & 63u)]; \\\n";
+            }
+            for (int n = n0; n < m; ++n) o << (n == 0 ? "  c = e0.x; \\\n" : "  c = c * e") << (n == 0 ? "" : std::to_string(n) + ".x; \\\n");
+            for (int n = n0; n < m; ++n) {
+                std::vector<int> preds;
+                for (int u = 0; u < n; ++u)
+                    if (D.pred[n] >> u & 1u) preds.push_back(u);
+                o << "  const float f" << n << " = e" << n << ".y";
+                if (!preds.empty()) {
+                    std::string mx = "f" + std::to_string(preds[0]);
+                    for (size_t k = 1; k < preds.size(); ++k)
+                        mx = "fmaxf(" + mx + ", f" + std::to_string(preds[k]) + ")";
+                    o << " + " << mx;
+                }
+                o << "; \\\n";
+            }
+            if (m < N) {
+                std::string lb;
+                for (int n = 0; n < m; ++n) {
+                    bool inner = false;
+                    for (int v = n + 1; v < m; ++v)
+                        if (D.pred[v] >> n & 1u) inner = true;
+                    if (inner) continue;
+                    std::string term = "f" + std::to_string(n);
+                    if (D.lat_tail[n] > 0.0f) term = "(" + term + " + " + flit(D.lat_tail[n]) + ")";
+                    lb = lb.empty() ? term : "fmaxf(" + lb + ", " + term + ")";
+                }
+                o << "  { const float lb_ = fmaxf(" << lb << " * " << flit(1.0f - 0x1p-18f) << ", "
+                  << flit(u2f(D.cp_lo_bits)) << "); \\\n"
+                  << "    const float th_ = s_bins[(__float_as_uint(lb_) >> bin_shift) & 63u]; \\\n"
+                  << "    if (!__builtin_amdgcn_ballot_w64(ok && (c * " << flit(D.corr_tail[m]) << " >= th_ || th_ < 0x1p-60f))) break; } \\\n";
+            }
+            n0 = m;
+        }
+        bool first = true;
+        for (int n = 0; n < N; ++n) {
+            if (!(D.sinks >> n & 1u)) continue;
+            o << (first ? "  cp = f" : "  cp = fmaxf(cp, f") << n << (first ? "; \\\n" : "); \\\n");
+            first = false;
+        }
+    }
+    o << R"(  const float th = s_bins[(__float_as_uint(cp) >> bin_shift) & 63u]; \
+  bool want = ok && c >= th; \
+  if (__builtin_amdgcn_ballot_w64(want)) { \
     if (want) { \
       bool w2 = false; \
       for (int k = 0; k < DY_K; ++k) if (cp <= hi[k] && c >= thr[k]) w2 = true; \
       want = w2; \
     } \
-    const unsigned long long m_ = __ballot(want); \
+    const unsigned long long m_ = __builtin_amdgcn_ballot_w64(want); \
     if (m_) { \
       const unsigned n_ = (unsigned)__builtin_popcountll(m_); \
       if (qn + n_ > DY_QCAP) { \
@@ -192,7 +277,8 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         qn += n_; \
       } \
     } \
-  } }
+  } \
+  } while (0); }
 )";
     // The load method is a template parameter and every load is issued
     // unconditionally (pointers clamped to the last row), so the compiler can
@@ -221,26 +307,37 @@ __device__ __forceinline__ void dy_scan_body(
   iters = ((unsigned long long)__builtin_amdgcn_readfirstlane((int)(iters >> 32)) << 32) |
           (unsigned)__builtin_amdgcn_readfirstlane((int)iters);
   unsigned long long r = wbase + lane;
-  const unsigned char* const plast = rows + (count - 1) * stride;
   const unsigned long long step = G * stride;
   const unsigned char* p = rows + r * stride;
   unsigned )" << wl("u0") << ", " << wl("u1") << ", " << wl("u2") << ", " << wl("u3") << R"(;
-  // ring of four row buffers: three rows in flight while one is scored
-#define DY_CLAMP(x) ((x) <= plast ? (x) : plast)
-  DY_LOADP(DY_CLAMP(p), )" << wl("u0") << R"()
-  DY_LOADP(DY_CLAMP(p + step), )" << wl("u1") << R"()
-  DY_LOADP(DY_CLAMP(p + 2 * step), )" << wl("u2") << R"()
-  for (unsigned long long it = 0; it < iters; it += 4) {
-    DY_LOADP(DY_CLAMP(p + 3 * step), )" << wl("u3") << R"()
-    DY_HANDLE()" << wl("u0") << R"(, r)
-    DY_LOADP(DY_CLAMP(p + 4 * step), )" << wl("u0") << R"()
-    if (it + 1 < iters) DY_HANDLE()" << wl("u1") << R"(, r + G)
-    DY_LOADP(DY_CLAMP(p + 5 * step), )" << wl("u1") << R"()
-    if (it + 2 < iters) DY_HANDLE()" << wl("u2") << R"(, r + 2 * G)
-    DY_LOADP(DY_CLAMP(p + 6 * step), )" << wl("u2") << R"()
-    if (it + 3 < iters) DY_HANDLE()" << wl("u3") << R"(, r + 3 * G)
-    p += 4 * step;
-    r += 4 * G;
+  // Rows j < iters - 1 of the wave are whole (every lane in range, as G >= 256),
+  // so the main loop, which touches rows up to it + 6 <= iters - 2, needs no
+  // clamp and no range test; a ring of four row buffers keeps three rows in
+  // flight while one is scored.  The last rows go one at a time.
+  unsigned long long it = 0;
+  if (iters >= 8) {
+    DY_LOADP(p, )" << wl("u0") << R"()
+    DY_LOADP(p + step, )" << wl("u1") << R"()
+    DY_LOADP(p + 2 * step, )" << wl("u2") << R"()
+    for (; it + 8 <= iters; it += 4) {
+      DY_LOADP(p + 3 * step, )" << wl("u3") << R"()
+      DY_HANDLE()" << wl("u0") << R"(, r, true)
+      DY_LOADP(p + 4 * step, )" << wl("u0") << R"()
+      DY_HANDLE()" << wl("u1") << R"(, r + G, true)
+      DY_LOADP(p + 5 * step, )" << wl("u1") << R"()
+      DY_HANDLE()" << wl("u2") << R"(, r + 2 * G, true)
+      DY_LOADP(p + 6 * step, )" << wl("u2") << R"()
+      DY_HANDLE()" << wl("u3") << R"(, r + 3 * G, true)
+      p += 4 * step;
+      r += 4 * G;
+    }
+  }
+  const unsigned char* const plast = rows + (count - 1) * stride;
+  for (; it < iters; ++it) {
+    DY_LOADP((r < count ? p : plast), )" << wl("u0") << R"()
+    DY_HANDLE()" << wl("u0") << R"(, r, r < count)
+    p += step;
+    r += G;
   }
   dy_flush(q, qn, lane, cand, cap, ncand, &ovf);
   if (lane == 0 && (badmask || ovf)) atomicOr(flags, (badmask ? 2 : 0) | (ovf ? 1 : 0));

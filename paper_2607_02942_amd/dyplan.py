@@ -127,7 +127,12 @@ def range_source(problem: int, begin: int, count: int) -> DySource:
 
 
 def rows_source(problem: int, rows, count: int, row_stride: int, index_base: int = 0) -> DySource:
-    return DySource(DY_SOURCE_ROWS, problem, 0, count, _ptr(rows), row_stride, index_base)
+    """A ROWS source over device memory.  The source keeps a reference to
+    `rows`, so a tensor passed as a temporary stays allocated while the source
+    object is alive (the library only sees its address)."""
+    src = DySource(DY_SOURCE_ROWS, problem, 0, count, _ptr(rows), row_stride, index_base)
+    src._keep = rows
+    return src
 
 
 class _Arrays:

@@ -178,6 +178,8 @@ def run_score(plan, src, n, K):
 def assert_scores(got, want, ctx):
     gc, gcp, gd, gf = got
     oc, ocp, od, of = want
+    off = np.flatnonzero(~np.isclose(gc, oc, rtol=RTOL, atol=0) | (np.isnan(gc) != np.isnan(oc)))
+    assert off.size == 0, f"{ctx}: corr differs at {off[:10].tolist()} ({off.size}): gpu {gc[off[:5]]} oracle {oc[off[:5]]}"
     np.testing.assert_allclose(gc, oc, rtol=RTOL, atol=0, err_msg=ctx)
     np.testing.assert_allclose(gcp, ocp, rtol=RTOL, atol=0, err_msg=ctx)
     np.testing.assert_allclose(gd, od, rtol=RTOL, atol=0, err_msg=ctx)
@@ -197,15 +199,16 @@ def test_score_rows_and_bad_ids():
     prob = wl.stream24()
     rows = wl.make_rows(50001, 24, 36)
     rows[77, 5] = 36  # an id out of range: NaN scores for that row only
+    d = torch.from_numpy(rows).cuda()
     with D.Plan(prob) as plan:
-        got = run_score(plan, D.rows_source(0, torch.from_numpy(rows).cuda(), 50001, 24), 50001, prob.n_levels)
+        got = run_score(plan, D.rows_source(0, d, 50001, 24), 50001, prob.n_levels)
         ok = np.ones(50001, bool)
         ok[77] = False
         want = orc.score_rows(prob, np.where(ok[:, None], rows, 0))
         assert_scores(tuple(a[ok] for a in got), tuple(a[ok] for a in want), "stream24 score")
         assert math.isnan(got[0][77]) and got[3][77] == 0
         with pytest.raises(D.DyplanError) as e:
-            plan.select([D.rows_source(0, torch.from_numpy(rows).cuda(), 50001, 24)], stream=stream())
+            plan.select([D.rows_source(0, d, 50001, 24)], stream=stream())
         assert e.value.status == D.DY_EINVAL
 
 
@@ -401,10 +404,12 @@ def test_rows_bad_ids_rejected_by_generated_kernel():
         for bad in (36, 63, 64, 200):
             r = rows.copy()
             r[12345, 7] = bad
+            dr = torch.from_numpy(r).cuda()
             with pytest.raises(D.DyplanError) as e:
-                plan.select([D.rows_source(0, torch.from_numpy(r).cuda(), 20000, 24)], stream=stream())
+                plan.select([D.rows_source(0, dr, 20000, 24)], stream=stream())
             assert e.value.status == D.DY_EINVAL
-        got = plan.select([D.rows_source(0, torch.from_numpy(rows).cuda(), 20000, 24)], stream=stream())[0]
+        d = torch.from_numpy(rows).cuda()
+        got = plan.select([D.rows_source(0, d, 20000, 24)], stream=stream())[0]
         assert_choices(got, orc.select_rows(prob, rows), "after bad rows")
 
 
@@ -423,5 +428,54 @@ def test_rows_radix_above_64_uses_generic_path():
     prob.slo = 1e9
     rows = np.stack([rng.integers(0, r, size=30000) for r in prob.radix], axis=1).astype(np.uint8)
     with D.Plan(prob) as plan:
-        got = plan.select([D.rows_source(0, torch.from_numpy(rows).cuda(), 30000, 3)], stream=stream())[0]
+        d = torch.from_numpy(rows).cuda()
+        got = plan.select([D.rows_source(0, d, 30000, 3)], stream=stream())[0]
     assert_choices(got, orc.select_rows(prob, rows), "radix 100 rows")
+
+
+def row_problem(rng, n, rmax, K, edge_p):
+    edges = np.array([(i, j) for i in range(n) for j in range(i + 1, n) if rng.random() < edge_p],
+                     np.int32).reshape(-1, 2)
+    radix = rng.integers(2, rmax + 1, size=n).astype(np.int32)
+    R = int(radix.max())
+    prob = wl.Problem(n_nodes=n, edges=edges, radix=radix,
+                      p=rng.uniform(0.5, 1.0, size=(n, R)).astype(np.float32),
+                      tau=rng.lognormal(0, 0.7, size=(n, R)).astype(np.float32),
+                      size=rng.choice([0.5, 1, 2.5, 6], size=(n, R)).astype(np.float32),
+                      backend=rng.integers(0, 2, size=(n, R)).astype(np.int32),
+                      w=rng.uniform(0, 1, size=n).astype(np.float32),
+                      rho=np.repeat(np.sort(rng.uniform(0, 0.9, size=K))[:, None], 2, axis=1).astype(np.float32),
+                      slo=0.0)
+    return prob
+
+
+def skewed_rows(rng, prob, count, p_top=0.75):
+    """Rows concentrated on each node's three highest-factor implementations, so
+    that many rows sit near the per-level thresholds and the generated kernel
+    abandons rows right at the edge of its bounds."""
+    a = 1.0 - prob.w[:, None].astype(np.float64) * (1.0 - prob.p.astype(np.float64))
+    cols = []
+    for n in range(prob.n_nodes):
+        R = int(prob.radix[n])
+        top = np.argsort(-a[n, :R], kind="stable")[:min(3, R)]
+        ids = np.where(rng.random(count) < p_top, rng.choice(top, size=count), rng.integers(0, R, size=count))
+        cols.append(ids)
+    return np.stack(cols, axis=1).astype(np.uint8)
+
+
+@pytest.mark.parametrize("n_nodes", [8, 13, 21, 32])
+def test_rows_early_exit_near_threshold(n_nodes):
+    # DAG-specialised rows kernel with mid-row abandonment (N >= 8) on rows
+    # crowded near the thresholds; tight and loose SLOs
+    rng = np.random.default_rng(600 + n_nodes)
+    for trial in range(3):
+        prob = row_problem(rng, n_nodes, int(rng.integers(4, 41)), int(rng.integers(2, 9)),
+                           float(rng.uniform(0.15, 0.5)))
+        rows = skewed_rows(rng, prob, 150000)
+        cps = orc.cp0_values(prob, rows=rows)
+        prob.slo = f32(np.quantile(cps, (0.02, 0.3, 0.8)[trial]) * 1.05)
+        want = orc.select_rows(prob, rows, index_base=5)
+        with D.Plan(prob) as plan:
+            d = torch.from_numpy(rows).cuda()
+            got = plan.select([D.rows_source(0, d, rows.shape[0], n_nodes, 5)], stream=stream())[0]
+        assert_choices(got, want, f"N={n_nodes} trial {trial}")
