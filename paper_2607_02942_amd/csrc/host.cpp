@@ -24,7 +24,7 @@ hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, hipStream_t s);
 hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, hipStream_t s);
 hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStream_t s);
-hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, hipStream_t s);
+hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, hipStream_t s);
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
 hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
 struct JitRows {
@@ -819,10 +819,10 @@ void launch_main(const JobDev* d, const PassPlan& pp, hipStream_t s,
     chunks(gbase[2], pp.n[2], [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[2], s), "scan"); });
 }
 
-void launch_certify_all(const JobDev* d, int ntot, int cert_waves, hipStream_t s,
+void launch_certify_all(const JobDev* d, int ntot, int cert_waves, int kmax, hipStream_t s,
                         const std::function<void(hipError_t, const char*)>& chk) {
     for (int c = 0; c < ntot; c += 65535)
-        chk(launch_certify(d + c, std::min(65535, ntot - c), cert_waves, s), "certify");
+        chk(launch_certify(d + c, std::min(65535, ntot - c), cert_waves, kmax, s), "certify");
 }
 
 // Generated rows kernels for problem p: compiled at first use.
@@ -953,7 +953,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         launch_main(S.d_jobs, pp, s, chk);
         jit_pass(jobs.data(), n3, pp.n[3], false);
         if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
-        launch_certify_all(S.d_jobs, n_src, cert_waves, s, chk);
+        launch_certify_all(S.d_jobs, n_src, cert_waves, h->kmax, s, chk);
     } else {
         if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
         for (int c = 0; c < n_src; c += 65535)
@@ -1021,7 +1021,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
             launch_table_all(S.d_fb, n_re, s, chk);
             launch_main(S.d_fb, rp, s, chk);
             jit_pass(re.data(), rp.n[0] + rp.n[1] + rp.n[2], rp.n[3], false);
-            launch_certify_all(S.d_fb, n_re, cert_waves, s, chk);
+            launch_certify_all(S.d_fb, n_re, cert_waves, h->kmax, s, chk);
         }
         if (n_ex > 0) {
             const JobDev* b = S.d_fb + n_re;

@@ -272,25 +272,18 @@ __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big,
     return Prefix{pc, px, py, s};
 }
 
-// ds_bpermute selects lane (address >> 2) & 63 and ignores the other address
-// bits, so the shifted CP pattern needs no mask (checked on gfx950)
-#ifndef DYP_BPERM_MASK
-#define DYP_BPERM_MASK 0
-#endif
-
 // One plan of the inner sweep: corr = cx * a_y, CP = max(tau_y + M, S2); the
-// prefilter threshold of CP's bin comes from the lane-resident table (bin j in
-// lane j) through ds_bpermute, whose lane select is bits [7:2] of the address.
+// prefilter threshold of CP's bin is read from the 64-entry LDS table (a
+// random LDS read issues in about half the time of a lane permute on gfx950):
+// byte offset = ((bits(CP) >> bin_shift) & 63) * 4, two shift/and operations.
 template <bool HAS_S2>
-__device__ __forceinline__ uint64_t sweep_test(const float2 vy, float M, float S2, float cx, uint32_t sh, int tbl) {
+__device__ __forceinline__ uint64_t sweep_test(const float2 vy, float M, float S2, float cx, uint32_t sh,
+                                               const float* s_bins) {
     float cp = vy.y + M;
     if (HAS_S2) cp = fmaxf(cp, S2);
     const float cc = cx * vy.x;
-    int addr = (int)(__float_as_uint(cp) >> sh);
-#if DYP_BPERM_MASK
-    addr &= 0xfc;
-#endif
-    const float thr = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, tbl));
+    const uint32_t off = (__float_as_uint(cp) >> sh) & 0xfcu;
+    const float thr = *(const float*)((const char*)s_bins + off);
     return __ballot(cc >= thr);
 }
 
@@ -305,9 +298,11 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
     const uint64_t t = t0 + threadIdx.x;
     const bool live = t < nblk;
     const uint64_t b = J->blk_first + (live ? t : nblk - 1);
+    __shared__ float s_bins[NBINS];
+    if (threadIdx.x < NBINS) s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
+    __syncthreads();
     const Prefix pf = prefix_eval(P, b, J->big, s_f);
 
-    const int tbl = (int)J->table[threadIdx.x & 63];
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* atx = cs(P->atx);
     const CS float2* aty = cs(P->aty);
@@ -324,12 +319,12 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
         int iy = 0;
         for (; iy + 4 <= ry; iy += 4) {
             const float2 v0 = aty[iy], v1 = aty[iy + 1], v2 = aty[iy + 2], v3 = aty[iy + 3];
-            hit |= sweep_test<HAS_S2>(v0, M, S2, cx, sh, tbl);
-            hit |= sweep_test<HAS_S2>(v1, M, S2, cx, sh, tbl);
-            hit |= sweep_test<HAS_S2>(v2, M, S2, cx, sh, tbl);
-            hit |= sweep_test<HAS_S2>(v3, M, S2, cx, sh, tbl);
+            hit |= sweep_test<HAS_S2>(v0, M, S2, cx, sh, s_bins);
+            hit |= sweep_test<HAS_S2>(v1, M, S2, cx, sh, s_bins);
+            hit |= sweep_test<HAS_S2>(v2, M, S2, cx, sh, s_bins);
+            hit |= sweep_test<HAS_S2>(v3, M, S2, cx, sh, s_bins);
         }
-        for (; iy < ry; ++iy) hit |= sweep_test<HAS_S2>(aty[iy], M, S2, cx, sh, tbl);
+        for (; iy < ry; ++iy) hit |= sweep_test<HAS_S2>(aty[iy], M, S2, cx, sh, s_bins);
         if (hit) {
             // rare: re-score this lane's row of the inner sweep with the exact test
             const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
@@ -361,7 +356,7 @@ __device__ __forceinline__ uint64_t sample_unit(uint64_t j, uint64_t S, uint64_t
 // Seeding pre-pass of the sweep: work unit = one row (block, x-implementation)
 // of R_y plans; one hashed row per window of S rows.  Per level, the best fp32
 // corr among sampled plans whose fp32 CP is certainly feasible.  A plan's CP
-// bin gives (jtab, lane-resident, through ds_bpermute) how many levels, in
+// bin gives (jtab, staged in LDS) how many levels, in
 // order of decreasing band, it certainly meets; the plan updates one bucket,
 // and a suffix maximum over buckets gives every level's value.  Reduction:
 // DPP within the wave, LDS across the workgroup, then an atomic max on the
@@ -404,7 +399,9 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
     const float M = exy ? fmaxf(pf.py, fx) : pf.py;
     const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
     const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
-    const int jt = (int)P->jtab[lane];
+    __shared__ int s_jt[NBINS];
+    if (tid < NBINS) s_jt[tid] = (int)P->jtab[tid];
+    __syncthreads();
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* aty = cs(P->aty);
     for (int iy = 0; iy < ry; ++iy) {
@@ -412,7 +409,7 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
         float cp = vy.y + M;
         if (HAS_S2) cp = fmaxf(cp, S2);
         const float cc = cx * vy.x;
-        const int j = __builtin_amdgcn_ds_bpermute((int)(__float_as_uint(cp) >> sh) & 0xfc, jt);
+        const int j = *(const int*)((const char*)s_jt + ((__float_as_uint(cp) >> sh) & 0xfcu));
         if (j > 0 && live && (base + (uint64_t)iy - J->begin < J->count)) {
             float* q = s_b + (j - 1) * WG + tid;
             *q = fmaxf(*q, cc);
@@ -628,12 +625,7 @@ __global__ void __launch_bounds__(WG) k_scan(const JobDev* __restrict__ jobs, ui
     if (P->uniform) {
         float cc, cp;
         eval_uniform(P, s_id, s_f, cc, cp);
-        const int tbl = (int)J->table[threadIdx.x & 63];
-        int addr = (int)(__float_as_uint(cp) >> ((uint32_t)P->bin_shift - 2u));
-#if DYP_BPERM_MASK
-        addr &= 0xfc;
-#endif
-        const float thr = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, tbl));
+        const float thr = __uint_as_float(J->table[(__float_as_uint(cp) >> (uint32_t)P->bin_shift) & 63u]);
         if (live && !bad && cc >= thr && is_candidate(P, J, cp, cc)) append_cand(J, idx, cc, cp);
     } else {
         const float cc = eval_corr(P, s_id);
@@ -691,23 +683,24 @@ __device__ __forceinline__ void wave_best4(double& c, uint64_t& i, double& cp, d
 constexpr int CERT_LDS_TABLES = 32 * 1024;  // fp64 tables staged in LDS when they fit
 constexpr int CERT_CACHE = 512;             // candidates cached in LDS by each certification wave
 
-// Certification, cert_waves waves per source (grid.x).  Pass A tightens each
-// level's threshold with the candidates whose fp32 CP is certainly feasible.
-// Pass B, level by level, re-evaluates in fp64 every candidate of this wave's
-// share that could still win the level (its CP only when its corr could beat
-// the lane's current best) and keeps the feasible one with the greatest corr,
-// then the lowest index.  k_cert_final merges the waves of a source.
+// Certification: grid (cert_waves, source, level), one wave per block.  Pass
+// A tightens the level's threshold with the candidates whose fp32 CP is
+// certainly feasible.  Pass B re-evaluates in fp64 every candidate of this
+// wave's share that could still win the level (its CP only when its corr
+// could beat the lane's current best) and keeps the feasible one with the
+// greatest corr, then the lowest index.  k_cert_final merges the waves of a
+// source.  Levels run in separate blocks: each lane walks its candidates once
+// per block instead of once per level.
 __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs) {
     extern __shared__ double s_tab[];
     __shared__ double s_f[NMAX * 64];
     __shared__ uint8_t s_id[NMAX * 64];
-    __shared__ float s_T[KMAX];
     __shared__ Cand s_cand[CERT_CACHE];
     JD J = cs(jobs + blockIdx.y);
     PD P = cs(J->prob);
-    const int g = blockIdx.x;
-    if (g >= J->cert_waves) return;
-    const int K = P->k, N = P->n, R = P->rmax, lane = threadIdx.x;
+    const int g = blockIdx.x, k = blockIdx.z;
+    if (g >= J->cert_waves || k >= P->k) return;
+    const int N = P->n, R = P->rmax, lane = threadIdx.x;
     const uint32_t nc = min(*J->ncand, J->cap);
     const bool general = !P->uniform;
     uint8_t* ids = s_id + lane;
@@ -715,90 +708,72 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
     const size_t NR = (size_t)N * R;
     const double* a64 = P->a64;
     const double* d64 = P->dem64;
-    const double* l64 = P->lat64;
-    if ((size_t)(K + 2) * NR * sizeof(double) <= (size_t)CERT_LDS_TABLES) {
+    const double* lat = P->lat64 + (size_t)k * NR;
+    if (3 * NR * sizeof(double) <= (size_t)CERT_LDS_TABLES) {
         // unrolled so that many loads are in flight before the first LDS store
 #pragma unroll 8
         for (size_t q = lane; q < NR; q += 64) {
-            s_tab[q] = P->a64[q];
-            s_tab[NR + q] = P->dem64[q];
+            s_tab[q] = a64[q];
+            s_tab[NR + q] = d64[q];
+            s_tab[2 * NR + q] = lat[q];
         }
-#pragma unroll 16
-        for (size_t q = lane; q < (size_t)K * NR; q += 64) s_tab[2 * NR + q] = P->lat64[q];
         a64 = s_tab;
         d64 = s_tab + NR;
-        l64 = s_tab + 2 * NR;
+        lat = s_tab + 2 * NR;
     }
-    // one round of loads: every level's seed slots (lane = slot) and the candidates
     static_assert(NSLOT == 64, "one seed slot per lane");
-    uint32_t sl[KMAX];
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) sl[k] = k < K ? J->scert[k * NSLOT + lane] : 0u;
+    const uint32_t sl = J->scert[k * NSLOT + lane];
     const uint32_t ncache = min(nc, (uint32_t)CERT_CACHE);
 #pragma unroll 8
     for (uint32_t i = lane; i < ncache; i += 64) s_cand[i] = J->cand[i];
     __syncthreads();
-    float sb[KMAX];
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) sb[k] = sl[k] ? __uint_as_float(sl[k] - 1u) : -1.0f;
+    const float lo = P->lo[k], hi = P->hi[k];
+    float sb = sl ? __uint_as_float(sl - 1u) : -1.0f;
     if (!general)
         for (uint32_t i = lane; i < nc; i += 64) {
             const Cand c = i < ncache ? s_cand[i] : J->cand[i];
-#pragma unroll
-            for (int k = 0; k < KMAX; ++k)
-                if (k < K && c.cp <= P->lo[k]) sb[k] = fmaxf(sb[k], c.corr);
+            if (c.cp <= lo) sb = fmaxf(sb, c.corr);
         }
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) {
-        if (k < K) {
-            const uint32_t e = wave_max_u32(sb[k] >= 0.0f ? __float_as_uint(sb[k]) + 1u : 0u);
-            if (lane == 0) s_T[k] = cand_threshold(e ? __uint_as_float(e - 1u) : -1.0f, N);
-        }
-    }
-    __syncthreads();
+    const uint32_t e = wave_max_u32(sb >= 0.0f ? __float_as_uint(sb) + 1u : 0u);
+    const float T = cand_threshold(e ? __uint_as_float(e - 1u) : -1.0f, N);
     const uint32_t step = 64u * (uint32_t)J->cert_waves;
-    for (int k = 0; k < K; ++k) {
-        const float T = s_T[k];
-        const float hi = P->hi[k];
-        const double* lat = l64 + (size_t)k * NR;
-        double bc = -1.0, bcp = 0.0, bd = 0.0;
-        uint64_t bi = ~0ull;
-        for (uint32_t i = (uint32_t)g * 64u + lane; i < nc; i += step) {
-            const Cand c = i < ncache ? s_cand[i] : J->cand[i];
-            if (!(c.corr >= T && (general || c.cp <= hi))) continue;
-            if (!job_ids(J, P, c.index, ids, 64)) continue;
-            double corr = 1.0;
-            for (int n = 0; n < N; ++n) corr = corr * a64[n * R + ids[n * 64]];
-            if (!better(corr, c.index, bc, bi)) continue;
-            double cp = 0.0;
-            for (int n = 0; n < N; ++n) {
-                double m = 0.0;
-                uint32_t pm = P->pred[n];
-                while (pm) {
-                    const int u = __builtin_ctz(pm);
-                    pm &= pm - 1;
-                    const double fu = f[u * 64];
-                    if (fu > m) m = fu;
-                }
-                const double fn = lat[n * R + ids[n * 64]] + m;
-                f[n * 64] = fn;
-                if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
+    double bc = -1.0, bcp = 0.0, bd = 0.0;
+    uint64_t bi = ~0ull;
+    for (uint32_t i = (uint32_t)g * 64u + lane; i < nc; i += step) {
+        const Cand c = i < ncache ? s_cand[i] : J->cand[i];
+        if (!(c.corr >= T && (general || c.cp <= hi))) continue;
+        if (!job_ids(J, P, c.index, ids, 64)) continue;
+        double corr = 1.0;
+        for (int n = 0; n < N; ++n) corr = corr * a64[n * R + ids[n * 64]];
+        if (!better(corr, c.index, bc, bi)) continue;
+        double cp = 0.0;
+        for (int n = 0; n < N; ++n) {
+            double m = 0.0;
+            uint32_t pm = P->pred[n];
+            while (pm) {
+                const int u = __builtin_ctz(pm);
+                pm &= pm - 1;
+                const double fu = f[u * 64];
+                if (fu > m) m = fu;
             }
-            if (!(cp <= P->slo)) continue;
-            double d = 0.0;
-            for (int n = 0; n < N; ++n) d = d + d64[n * R + ids[n * 64]];
-            bc = corr;
-            bi = c.index;
-            bcp = cp;
-            bd = d;
+            const double fn = lat[n * R + ids[n * 64]] + m;
+            f[n * 64] = fn;
+            if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
         }
-        wave_best4(bc, bi, bcp, bd);
-        if (lane == 0) {
-            J->cert_c[k * CERT_WAVES + g] = bc;
-            J->cert_i[k * CERT_WAVES + g] = bi;
-            J->cert_cp[k * CERT_WAVES + g] = bcp;
-            J->cert_d[k * CERT_WAVES + g] = bd;
-        }
+        if (!(cp <= P->slo)) continue;
+        double d = 0.0;
+        for (int n = 0; n < N; ++n) d = d + d64[n * R + ids[n * 64]];
+        bc = corr;
+        bi = c.index;
+        bcp = cp;
+        bd = d;
+    }
+    wave_best4(bc, bi, bcp, bd);
+    if (lane == 0) {
+        J->cert_c[k * CERT_WAVES + g] = bc;
+        J->cert_i[k * CERT_WAVES + g] = bi;
+        J->cert_cp[k * CERT_WAVES + g] = bcp;
+        J->cert_d[k * CERT_WAVES + g] = bd;
     }
 }
 
@@ -1079,8 +1054,8 @@ hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStrea
     return hipSuccess;
 }
 
-hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, hipStream_t s) {
-    hipLaunchKernelGGL(k_certify, dim3(waves, njobs), dim3(64), CERT_LDS_TABLES, s, d_jobs);
+hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, hipStream_t s) {
+    hipLaunchKernelGGL(k_certify, dim3(waves, njobs, kmax), dim3(64), CERT_LDS_TABLES, s, d_jobs);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_cert_final, dim3(njobs), dim3(64), 0, s, d_jobs);
