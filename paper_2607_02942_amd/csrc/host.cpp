@@ -20,8 +20,9 @@ namespace dyp {
 hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_samples, int npre_max,
-                               hipStream_t s);
-hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, hipStream_t s);
+                               int npre_c, int kmax, hipStream_t s);
+hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, int npre_c,
+                        int ry, hipStream_t s);
 hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, hipStream_t s);
 hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStream_t s);
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, hipStream_t s);
@@ -743,6 +744,9 @@ struct PassPlan {
     uint64_t units[3] = {0, 0, 0};        // largest main-pass work of the group
     uint64_t samples[3] = {0, 0, 0};      // largest seeding-pass work of the group
     int npre[2] = {0, 0};
+    int ry[2] = {0, 0};                   // R_y shared by every source of a sweep group, else -1
+    int npre_c[2] = {0, 0};               // prefix length shared by every source of a sweep group, else -1
+    int kmax = 1;                         // most levels of any source
 };
 
 // Rows sources of uniform-pressure problems run the problem's generated
@@ -793,7 +797,7 @@ void launch_seed(const JobDev* d, const PassPlan& pp, hipStream_t s,
     const JobDev* gbase[3] = {d, d + pp.n[0], d + pp.n[0] + pp.n[1]};
     for (int g = 0; g < 2; ++g)
         chunks(gbase[g], pp.n[g], [&](const JobDev* b, int n) {
-            chk(launch_sample_sweep(b, n, g == 1, pp.samples[g], pp.npre[g], s), "sample");
+            chk(launch_sample_sweep(b, n, g == 1, pp.samples[g], pp.npre[g], pp.npre_c[g], pp.kmax, s), "sample");
         });
     chunks(gbase[2], pp.n[2],
            [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, pp.samples[2], s), "sample"); });
@@ -814,7 +818,7 @@ void launch_main(const JobDev* d, const PassPlan& pp, hipStream_t s,
     const JobDev* gbase[3] = {d, d + pp.n[0], d + pp.n[0] + pp.n[1]};
     for (int g = 0; g < 2; ++g)
         chunks(gbase[g], pp.n[g], [&](const JobDev* b, int n) {
-            chk(launch_sweep(b, n, g == 1, pp.units[g], pp.npre[g], s), "sweep");
+            chk(launch_sweep(b, n, g == 1, pp.units[g], pp.npre[g], pp.npre_c[g], pp.ry[g], s), "sweep");
         });
     chunks(gbase[2], pp.n[2], [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[2], s), "scan"); });
 }
@@ -915,7 +919,12 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
             pp.units[g] = std::max(pp.units[g], J.units);
             pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
         }
-        if (sweep) pp.npre[g] = std::max(pp.npre[g], H.npre);
+        pp.kmax = std::max(pp.kmax, H.k);
+        if (sweep) {
+            pp.npre[g] = std::max(pp.npre[g], H.npre);
+            pp.ry[g] = pp.n[g] == 1 ? H.ry : (pp.ry[g] == H.ry ? pp.ry[g] : -1);
+            pp.npre_c[g] = pp.n[g] == 1 ? H.npre : (pp.npre_c[g] == H.npre ? pp.npre_c[g] : -1);
+        }
         all_units = std::max(all_units, J.count);
         plans += J.count;
         jobs[q] = J;

@@ -218,21 +218,70 @@ struct Prefix {
     float pc, px, py, s;
 };
 
+// The (a, tau) rows of the prefix nodes, staged in LDS by the workgroup when
+// they fit (a random LDS read instead of a global load in the decode chain).
+constexpr int PAT_MAX = 1024;  // float2 entries
+
+__device__ __forceinline__ const float2* stage_prefix_rows(PD P, float2* s_pat) {
+    const int n = P->npre * P->rmax;
+    const bool fit = n <= PAT_MAX;
+    if (fit)
+        for (int i = threadIdx.x; i < n; i += WG) s_pat[i] = cs(P->at)[i];
+    __syncthreads();
+    return fit ? s_pat : nullptr;
+}
+
+// Digit of prefix node n in block index b (node 0 most significant).
+__device__ __forceinline__ uint32_t prefix_digit(PD P, int n, uint64_t b, int big) {
+    if (!big) {
+        const uint32_t q = P->pv_big[n] ? 0u : mdiv((uint32_t)b, P->pvmag[n]);
+        return q - mdiv(q, P->rmag[n]) * (uint32_t)P->radix[n];
+    }
+    return (uint32_t)((b / P->pv64[n]) % (uint64_t)P->radix[n]);
+}
+
+// Prefix recurrence of block b.  NPRE > 0: the prefix has exactly NPRE nodes
+// (checked by the host); the loops unroll, every descriptor load is issued up
+// front and the f_n live in registers (predecessor bits are wave-uniform, so
+// each test is a scalar branch).  NPRE == 0: any length, f_n in an LDS column.
+template <int NPRE>
 __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big,
-                                              float* __restrict__ s_f) {
+                                              float* __restrict__ s_f, const float2* s_pat) {
+    if constexpr (NPRE > 0) {
+        const int rmax = P->rmax;
+        float f[NPRE];
+        float pc = 1.0f;
+#pragma unroll
+        for (int n = 0; n < NPRE; ++n) {
+            const uint32_t d = prefix_digit(P, n, b, big);
+            const float2 v = s_pat ? s_pat[n * rmax + d] : cs(P->at)[n * rmax + d];
+            pc = pc * v.x;
+            float m = 0.0f;
+            const uint32_t pm = P->pred[n];
+#pragma unroll
+            for (int u = 0; u < n; ++u)
+                if (pm >> u & 1u) m = fmaxf(m, f[u]);
+            f[n] = v.y + m;
+        }
+        float px = 0.0f, py = 0.0f, s = 0.0f;
+        const int xn = P->xnode;
+        const uint32_t pmx = xn >= 0 ? P->pred[xn] : 0u;
+        const uint32_t pmy = P->pred[P->ynode] & (xn >= 0 ? ~(1u << xn) : ~0u);
+        const uint32_t pms = P->pre_sinks;
+#pragma unroll
+        for (int u = 0; u < NPRE; ++u) {
+            if (pmx >> u & 1u) px = fmaxf(px, f[u]);
+            if (pmy >> u & 1u) py = fmaxf(py, f[u]);
+            if (pms >> u & 1u) s = fmaxf(s, f[u]);
+        }
+        return Prefix{pc, px, py, s};
+    }
     const int tid = threadIdx.x;
     const int npre = P->npre;
     float pc = 1.0f;
-    const uint32_t b32 = (uint32_t)b;
     for (int n = 0; n < npre; ++n) {
-        uint32_t d;
-        if (!big) {
-            uint32_t q = P->pv_big[n] ? 0u : mdiv(b32, P->pvmag[n]);
-            d = q - mdiv(q, P->rmag[n]) * (uint32_t)P->radix[n];
-        } else {
-            d = (uint32_t)((b / P->pv64[n]) % (uint64_t)P->radix[n]);
-        }
-        const float2 v = cs(P->at)[n * P->rmax + d];
+        const uint32_t d = prefix_digit(P, n, b, big);
+        const float2 v = s_pat ? s_pat[n * P->rmax + d] : cs(P->at)[n * P->rmax + d];
         pc = pc * v.x;
         float m = 0.0f;
         uint32_t pm = P->pred[n];
@@ -287,7 +336,10 @@ __device__ __forceinline__ uint64_t sweep_test(const float2 vy, float M, float S
     return __ballot(cc >= thr);
 }
 
-template <bool HAS_S2>
+// RY > 0: every source of the launch has R_y = RY; the y table is loaded once
+// per workgroup into scalar registers and the y loop is fully unrolled, so the
+// inner sweep issues no memory load and no wait other than its LDS bin reads.
+template <bool HAS_S2, int RY, int NPRE>
 __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, uint64_t unit_off) {
     extern __shared__ float s_f[];
     JD J = cs(jobs + blockIdx.y);
@@ -300,8 +352,8 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
     const uint64_t b = J->blk_first + (live ? t : nblk - 1);
     __shared__ float s_bins[NBINS];
     if (threadIdx.x < NBINS) s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
-    __syncthreads();
-    const Prefix pf = prefix_eval(P, b, J->big, s_f);
+    const float2* pat = stage_prefix_rows(P, (float2*)(s_f + (size_t)max(P->npre, 1) * WG));
+    const Prefix pf = prefix_eval<NPRE>(P, b, J->big, s_f, pat);
 
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* atx = cs(P->atx);
@@ -309,6 +361,11 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
     const int rx = P->rx, ry = P->ry;
     const bool exy = P->edge_xy != 0;
 
+    float2 vyr[RY > 0 ? RY : 1];
+    if (RY > 0) {
+#pragma unroll
+        for (int iy = 0; iy < RY; ++iy) vyr[iy] = aty[iy];
+    }
     for (int ix = 0; ix < rx; ++ix) {
         const float2 vx = atx[ix];
         const float fx = vx.y + pf.px;
@@ -317,6 +374,11 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
         const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
         uint64_t hit = 0;
         int iy = 0;
+        if (RY > 0) {
+#pragma unroll
+            for (int j = 0; j < (RY > 0 ? RY : 1); ++j) hit |= sweep_test<HAS_S2>(vyr[j], M, S2, cx, sh, s_bins);
+            iy = ry;
+        }
         for (; iy + 4 <= ry; iy += 4) {
             const float2 v0 = aty[iy], v1 = aty[iy + 1], v2 = aty[iy + 2], v3 = aty[iy + 3];
             hit |= sweep_test<HAS_S2>(v0, M, S2, cx, sh, s_bins);
@@ -361,7 +423,7 @@ __device__ __forceinline__ uint64_t sample_unit(uint64_t j, uint64_t S, uint64_t
 // and a suffix maximum over buckets gives every level's value.  Reduction:
 // DPP within the wave, LDS across the workgroup, then an atomic max on the
 // ordered bit pattern into one of NSLOT slots per level.
-template <bool HAS_S2>
+template <bool HAS_S2, int NPRE>
 __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ jobs) {
     extern __shared__ float s_dyn[];
     __shared__ uint32_t s_red[KMAX][WG / 64];
@@ -370,6 +432,7 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
     const int K = P->k;
     float* s_f = s_dyn;                                  // prefix recurrence, [npre][WG]
     float* s_b = s_dyn + (size_t)max(P->npre, 1) * WG;   // buckets, [K][WG]
+    float2* s_pat = (float2*)(s_b + (size_t)K * WG);     // prefix rows, PAT_MAX entries
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint64_t S = J->sample_stride;
     const int rx = P->rx, ry = P->ry;
@@ -390,7 +453,8 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
         b = J->blk_first + u / (uint64_t)rx;
         ix = (int)(u % (uint64_t)rx);
     }
-    const Prefix pf = prefix_eval(P, b, J->big, s_f);
+    const float2* pat = stage_prefix_rows(P, s_pat);
+    const Prefix pf = prefix_eval<NPRE>(P, b, J->big, s_f, pat);
     for (int j = 0; j < K; ++j) s_b[j * WG + tid] = -1.0f;
     const float2 vx = cs(P->atx)[ix];
     const float fx = vx.y + pf.px;
@@ -1002,30 +1066,66 @@ hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s) {
 
 // sweep jobs: [first, first + n) of d_jobs, all with the same HAS_S2
 hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_samples, int npre_max,
-                               hipStream_t s) {
+                               int npre_c, int kmax, hipStream_t s) {
     if (n == 0) return hipSuccess;
     const uint64_t gx = (max_samples + WG - 1) / WG;
     if (gx == 0) return hipSuccess;
     if (gx > MAX_GRID_X) return hipErrorInvalidValue;
-    const size_t lds = (size_t)((npre_max > 0 ? npre_max : 1) + KMAX) * WG * sizeof(float);
-    if (has_s2)
-        hipLaunchKernelGGL(k_sample_sweep<true>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs);
-    else
-        hipLaunchKernelGGL(k_sample_sweep<false>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs);
+    const size_t lds = (size_t)((npre_max > 0 ? npre_max : 1) + kmax) * WG * sizeof(float) +
+                       (size_t)PAT_MAX * sizeof(float2);
+    const dim3 grid((uint32_t)gx, n);
+#define DYP_SAMPLE(S2, NP) hipLaunchKernelGGL((k_sample_sweep<S2, NP>), grid, dim3(WG), lds, s, d_jobs)
+#define DYP_SAMPLE_NP(S2)       \
+    switch (npre_c) {           \
+        case 2: DYP_SAMPLE(S2, 2); break; \
+        case 4: DYP_SAMPLE(S2, 4); break; \
+        case 6: DYP_SAMPLE(S2, 6); break; \
+        case 8: DYP_SAMPLE(S2, 8); break; \
+        default: DYP_SAMPLE(S2, 0); break; \
+    }
+    if (has_s2) {
+        DYP_SAMPLE_NP(true)
+    } else {
+        DYP_SAMPLE_NP(false)
+    }
+#undef DYP_SAMPLE_NP
+#undef DYP_SAMPLE
     return hipGetLastError();
 }
 
-hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, hipStream_t s) {
+hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, int npre_c,
+                        int ry, hipStream_t s) {
     if (n == 0) return hipSuccess;
-    size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float);
+    const size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float) + (size_t)PAT_MAX * sizeof(float2);
     for (uint64_t off = 0; off < max_units; off += MAX_GRID_X * WG) {
         uint64_t left = max_units - off;
         uint64_t gx = (left + WG - 1) / WG;
         if (gx > MAX_GRID_X) gx = MAX_GRID_X;
-        if (has_s2)
-            hipLaunchKernelGGL(k_sweep<true>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs, off);
-        else
-            hipLaunchKernelGGL(k_sweep<false>, dim3((uint32_t)gx, n), dim3(WG), lds, s, d_jobs, off);
+        const dim3 grid((uint32_t)gx, n);
+#define DYP_SWEEP(S2, RYV, NP) hipLaunchKernelGGL((k_sweep<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off)
+#define DYP_SWEEP_NP(S2, RYV)            \
+    switch (npre_c) {                    \
+        case 2: DYP_SWEEP(S2, RYV, 2); break; \
+        case 4: DYP_SWEEP(S2, RYV, 4); break; \
+        case 6: DYP_SWEEP(S2, RYV, 6); break; \
+        case 8: DYP_SWEEP(S2, RYV, 8); break; \
+        default: DYP_SWEEP(S2, RYV, 0); break; \
+    }
+        if (ry == 12) {
+            if (has_s2) {
+                DYP_SWEEP_NP(true, 12)
+            } else {
+                DYP_SWEEP_NP(false, 12)
+            }
+        } else {
+            if (has_s2) {
+                DYP_SWEEP_NP(true, 0)
+            } else {
+                DYP_SWEEP_NP(false, 0)
+            }
+        }
+#undef DYP_SWEEP_NP
+#undef DYP_SWEEP
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
