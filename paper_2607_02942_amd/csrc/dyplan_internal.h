@@ -109,6 +109,7 @@ struct JobDev {
     uint64_t* cert_i;         // [KMAX][CERT_WAVES] its index
     double* cert_cp;          // [KMAX][CERT_WAVES] its fp64 CP at the level
     double* cert_d;           // [KMAX][CERT_WAVES] its fp64 demand
+    uint32_t* sync;           // certification blocks finished (re-armed to 0 by the last)
 };
 
 }  // namespace dyp

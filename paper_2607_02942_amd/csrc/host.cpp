@@ -60,6 +60,8 @@ struct HostProb {
 
 struct Scratch {
     size_t jobs = 0;            // sources the buffers hold
+    bool clean = false;         // every job slot's seeds, counters and flags are zero (no k_init needed)
+    uint32_t* sync = nullptr;   // [jobs] certification block counters
     uint32_t cap = 0;           // candidate slots per source
     int kmax = 0;
     char* d = nullptr;
@@ -246,6 +248,15 @@ struct dy_plan {
     uint32_t cand_cap = 1u << 16;
     int force_fp64 = 0;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    // A call that repeats the previous one (same job array, scratch clear) is
+    // replayed from a HIP graph of its launches: one submission instead of one
+    // per kernel, which on gfx950 costs more host time than the short kernels
+    // of a selection run.  Captured on an internal stream, launched on the
+    // caller's.
+    int use_graph = 1;
+    hipStream_t cap_stream = nullptr;
+    hipGraphExec_t graph = nullptr;
+    int graph_timing = 0;
     dy_stats stats{};
     std::string err;
 };
@@ -305,6 +316,7 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
     size_t o_fbc = take(njobs * KMAX * sizeof(uint64_t));
     size_t o_fbi = take(njobs * KMAX * sizeof(uint64_t));
     size_t o_cand = take(njobs * (size_t)cap * sizeof(Cand));
+    size_t o_sync = take(njobs * sizeof(uint32_t));
     hipError_t e = hipMalloc((void**)&s.d, off);
     if (e != hipSuccess) {
         s.d = nullptr;
@@ -327,6 +339,8 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
     s.out = (dy_choice*)(s.d + o_res + res_out);
     s.ncand = (uint32_t*)(s.d + o_res + res_ncand);
     s.flags = (int32_t*)(s.d + o_res + res_flags);
+    s.sync = (uint32_t*)(s.d + o_sync);
+    s.clean = false;  // the next call clears the scratch first
     s.fb_corr = (uint64_t*)(s.d + o_fbc);
     s.fb_index = (uint64_t*)(s.d + o_fbi);
     s.cand = (Cand*)(s.d + o_cand);
@@ -680,6 +694,8 @@ int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_
     if (st == DY_OK) {
         for (int i = 0; i < 4 && st == DY_OK; ++i)
             if ((e = hipEventCreate(&h->ev[i])) != hipSuccess) st = hip_fail(&g_create_error, e, "hipEventCreate");
+        if (st == DY_OK && (e = hipStreamCreateWithFlags(&h->cap_stream, hipStreamNonBlocking)) != hipSuccess)
+            st = hip_fail(&g_create_error, e, "hipStreamCreate");
     }
     if (st != DY_OK) {
         dy_plan_destroy(h);
@@ -697,15 +713,24 @@ void dy_plan_destroy(dy_plan* h) {
     if (h->d_arena) (void)hipFree(h->d_arena);
     for (int i = 0; i < 4; ++i)
         if (h->ev[i]) (void)hipEventDestroy(h->ev[i]);
+    if (h->graph) (void)hipGraphExecDestroy(h->graph);
+    if (h->cap_stream) (void)hipStreamDestroy(h->cap_stream);
     delete h;
 }
 
 int32_t dy_plan_max_levels(const dy_plan* h) { return h ? h->kmax : 0; }
 int32_t dy_plan_num_problems(const dy_plan* h) { return h ? (int32_t)h->hp.size() : 0; }
 
+void drop_graph(dy_plan* h) {
+    if (h->graph) (void)hipGraphExecDestroy(h->graph);
+    h->graph = nullptr;
+}
+
 int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value) {
     if (!h) return DY_EINVAL;
+    drop_graph(h);
     switch (option) {
+        case DY_OPT_GRAPH: h->use_graph = value ? 1 : 0; return DY_OK;
         case DY_OPT_TIMING: h->timing = value ? 1 : 0; return DY_OK;
         case DY_OPT_SAMPLE_STRIDE:
             if (value < 1 || value > (1 << 30)) break;
@@ -906,6 +931,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         J.cert_i = S.cert_i + (size_t)q * KMAX * CERT_WAVES;
         J.cert_cp = S.cert_cp + (size_t)q * KMAX * CERT_WAVES;
         J.cert_d = S.cert_d + (size_t)q * KMAX * CERT_WAVES;
+        J.sync = S.sync + q;
         J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
         // seeding work units: rows of the inner sweep, or plans
         const bool sweep = g == G_SWEEP || g == G_SWEEP_S2;
@@ -931,7 +957,10 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     }
     const int n3 = pp.n[0] + pp.n[1] + pp.n[2];  // jobs of groups 0-2; JIT jobs follow
     // the job array is rebuilt every call but uploaded only when it changed
-    if (S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0) {
+    const bool changed =
+        S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0;
+    if (changed) {
+        drop_graph(h);
         hipError_t e = hipStreamSynchronize(s);  // a previous upload may still read the pinned buffer
         if (e == hipSuccess) {
             std::memcpy(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev));
@@ -946,31 +975,79 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     std::function<void(hipError_t, const char*)> chk = [&](hipError_t x, const char* what) {
         if (x != hipSuccess && st == DY_OK) st = hip_fail(&h->err, x, what);
     };
-    auto jit_pass = [&](const JobDev* hjobs, int first, int n, bool sample) {
+    auto jit_pass = [&](const JobDev* hjobs, int first, int n, bool sample, hipStream_t st,
+                        const std::function<void(hipError_t, const char*)>& ck) {
         for (int q = first; q < first + n; ++q) {
             const int p = (int)(hjobs[q].prob - h->d_probs);
-            chk(launch_jit(h, hjobs[q], p, sample, s), sample ? "rows sample" : "rows scan");
+            ck(launch_jit(h, hjobs[q], p, sample, st), sample ? "rows sample" : "rows scan");
         }
     };
-    if (h->timing) chk(hipEventRecord(h->ev[0], s), "hipEventRecord");
-    for (int c = 0; c < n_src; c += 65535) chk(launch_init(S.d_jobs + c, std::min(65535, n_src - c), s), "init");
-    if (!h->force_fp64) {
-        launch_seed(S.d_jobs, pp, s, chk);
-        jit_pass(jobs.data(), n3, pp.n[3], true);
-        launch_table_all(S.d_jobs, n_src, s, chk);
-        if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
-        launch_main(S.d_jobs, pp, s, chk);
-        jit_pass(jobs.data(), n3, pp.n[3], false);
-        if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
-        launch_certify_all(S.d_jobs, n_src, cert_waves, h->kmax, s, chk);
-    } else {
-        if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
-        for (int c = 0; c < n_src; c += 65535)
-            chk(launch_exhaust(S.d_jobs + c, std::min(65535, n_src - c), all_units, s), "exhaust");
-        if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
+    // seeding, tables, scoring, certification, copy-out
+    auto issue_main = [&](hipStream_t st, const std::function<void(hipError_t, const char*)>& ck) {
+        launch_seed(S.d_jobs, pp, st, ck);
+        jit_pass(jobs.data(), n3, pp.n[3], true, st, ck);
+        launch_table_all(S.d_jobs, n_src, st, ck);
+        if (h->timing) ck(hipEventRecord(h->ev[1], st), "hipEventRecord");
+        launch_main(S.d_jobs, pp, st, ck);
+        jit_pass(jobs.data(), n3, pp.n[3], false, st, ck);
+        if (h->timing) ck(hipEventRecord(h->ev[2], st), "hipEventRecord");
+        launch_certify_all(S.d_jobs, n_src, cert_waves, h->kmax, st, ck);
+        if (h->timing) ck(hipEventRecord(h->ev[3], st), "hipEventRecord");
+        ck(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, st), "copy out");
+    };
+    bool exhausted = h->force_fp64 != 0;
+    bool launched = false;
+    if (h->use_graph && !h->force_fp64 && S.clean && !changed) {
+        if (h->graph && h->graph_timing != h->timing) drop_graph(h);
+        if (!h->graph) {  // capture once; any failure falls back to direct launches for this plan
+            bool ok = hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal) == hipSuccess;
+            if (ok) {
+                hipError_t cap_err = hipSuccess;
+                if (h->timing) (void)hipEventRecord(h->ev[0], h->cap_stream);
+                issue_main(h->cap_stream, [&](hipError_t x, const char*) {
+                    if (x != hipSuccess && cap_err == hipSuccess) cap_err = x;
+                });
+                hipGraph_t graph = nullptr;
+                ok = hipStreamEndCapture(h->cap_stream, &graph) == hipSuccess && cap_err == hipSuccess && graph;
+                if (ok) ok = hipGraphInstantiate(&h->graph, graph, nullptr, nullptr, 0) == hipSuccess;
+                if (graph) (void)hipGraphDestroy(graph);
+                if (!ok) {
+                    h->graph = nullptr;
+                    h->use_graph = 0;
+                    (void)hipGetLastError();
+                }
+                h->graph_timing = h->timing;
+            } else {
+                h->use_graph = 0;
+                (void)hipGetLastError();
+            }
+        }
+        if (h->graph) {
+            S.clean = false;
+            chk(hipGraphLaunch(h->graph, s), "hipGraphLaunch");
+            launched = true;
+        }
     }
-    if (h->timing) chk(hipEventRecord(h->ev[3], s), "hipEventRecord");
-    chk(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, s), "copy out");
+    if (!launched) {
+        if (h->timing) chk(hipEventRecord(h->ev[0], s), "hipEventRecord");
+        // A call that ends with every source certified and no flag raised leaves
+        // the scratch clear (the certification's last blocks re-zero the seeds);
+        // anything else, or a fresh allocation, clears it here.
+        if (!S.clean || h->force_fp64)
+            for (int c = 0; c < n_src; c += 65535)
+                chk(launch_init(S.d_jobs + c, std::min(65535, n_src - c), s), "init");
+        S.clean = false;
+        if (!h->force_fp64) {
+            issue_main(s, chk);
+        } else {
+            if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
+            for (int c = 0; c < n_src; c += 65535)
+                chk(launch_exhaust(S.d_jobs + c, std::min(65535, n_src - c), all_units, s), "exhaust");
+            if (h->timing) chk(hipEventRecord(h->ev[2], s), "hipEventRecord");
+            if (h->timing) chk(hipEventRecord(h->ev[3], s), "hipEventRecord");
+            chk(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, s), "copy out");
+        }
+    }
     chk(hipStreamSynchronize(s), "hipStreamSynchronize");
     if (st != DY_OK) return st;
 
@@ -1029,10 +1106,11 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
                 chk(launch_reseed(S.d_fb + c, std::min(65535, n_re - c), s), "reseed");
             launch_table_all(S.d_fb, n_re, s, chk);
             launch_main(S.d_fb, rp, s, chk);
-            jit_pass(re.data(), rp.n[0] + rp.n[1] + rp.n[2], rp.n[3], false);
+            jit_pass(re.data(), rp.n[0] + rp.n[1] + rp.n[2], rp.n[3], false, s, chk);
             launch_certify_all(S.d_fb, n_re, cert_waves, h->kmax, s, chk);
         }
         if (n_ex > 0) {
+            exhausted = true;
             const JobDev* b = S.d_fb + n_re;
             for (int c = 0; c < n_ex; c += 65535)
                 chk(launch_exhaust(b + c, std::min(65535, n_ex - c), fb_units, s), "exhaust");
@@ -1048,6 +1126,9 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         const int K = h->hp[src[j].problem].k;
         std::memcpy(out + (size_t)j * km, S.h_out + (size_t)j * km, (size_t)K * sizeof(dy_choice));
     }
+    bool flagged = false;
+    for (int q = 0; q < n_src; ++q) flagged = flagged || S.h_flags[q] != 0;
+    S.clean = !exhausted && !flagged;
     h->stats = stats;
     return DY_OK;
 }

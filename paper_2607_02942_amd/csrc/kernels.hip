@@ -20,6 +20,7 @@
 //   k_sweep / k_scan   the scoring pass: every plan is scored in fp32; a plan
 //                 goes to the candidate list when it could be a level's winner
 //   k_certify     fp64 re-evaluation of the candidates; exact winner per level
+//                 (the last block of a source merges its waves)
 //   k_exhaust*    fallback: exhaustive fp64 decision (candidate overflow)
 #include <hip/hip_runtime.h>
 
@@ -200,6 +201,62 @@ __global__ void k_init(JobDev* __restrict__ jobs, int njobs) {
     }
     if (t < NBINS) J->table[t] = 0u;
     if (t == 0) {
+        *J->ncand = 0u;
+        *J->flags = 0;
+        *J->sync = 0u;
+    }
+}
+
+// True in the block of a job that finishes a launch last (once every block of
+// the job that reaches this point has done so), with the other blocks' global
+// writes visible; that block also re-arms the counter.  Called by every thread.
+// Every block adds to one device-scope counter, and such atomics serialize
+// across the XCDs (tens of ns each): only for launches of few blocks.
+__device__ bool last_block(uint32_t* counter, uint32_t expected) {
+    __shared__ uint32_t s_last;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t prev = atomicAdd(counter, 1u);
+        s_last = prev + 1u == expected ? 1u : 0u;
+        if (s_last) atomicExch(counter, 0u);
+    }
+    __syncthreads();
+    const bool last = s_last != 0u;
+    if (last) __threadfence();
+    return last;
+}
+
+// Per level candidate threshold T_k from the seed slots, and the 64-bin
+// prefilter table; resets the job's candidate count and flags for the scoring
+// pass.  Called by every thread of one block (>= 64 threads).
+__device__ void build_table(JD J, PD P) {
+    __shared__ float s_thr[KMAX];
+    const int lane = threadIdx.x;
+    if (lane < P->k) {
+        uint32_t e = 0;
+        for (int q = 0; q < NSLOT; ++q) e = max(e, J->scert[lane * NSLOT + q]);
+        const float t = e ? cand_threshold(__uint_as_float(e - 1u), P->n) : -INFINITY;
+        s_thr[lane] = t;
+        J->thr[lane] = t;
+    }
+    __syncthreads();
+    if (lane < NBINS) {
+        // bin `lane` covers fp32 patterns [B << s, (B+1) << s) with B = lane (mod 64),
+        // B in [cp_lo >> s, (cp_lo >> s) + 63]; its threshold is the lowest T_k of
+        // every level some CP in the bin may meet.
+        const uint32_t s = (uint32_t)P->bin_shift;
+        const uint32_t blo = P->cp_lo_bits >> s;
+        const uint32_t B = blo + (((uint32_t)lane - blo) & 63u);
+        uint32_t lowbits = B << s;
+        if (lowbits < P->cp_lo_bits) lowbits = P->cp_lo_bits;
+        const float low = __uint_as_float(lowbits);
+        float g = INFINITY;
+        for (int k = 0; k < P->k; ++k)
+            if (P->hi[k] >= low) g = fminf(g, s_thr[k]);
+        J->table[lane] = __float_as_uint(g);
+    }
+    if (lane == 0) {
         *J->ncand = 0u;
         *J->flags = 0;
     }
@@ -501,27 +558,7 @@ __global__ void k_table(JobDev* __restrict__ jobs, int njobs) {
     const int j = blockIdx.x;
     if (j >= njobs) return;
     JD J = cs(jobs + j);
-    PD P = cs(J->prob);
-    const int lane = threadIdx.x;
-    if (lane < P->k) {
-        uint32_t e = 0;
-        for (int q = 0; q < NSLOT; ++q) e = max(e, J->scert[lane * NSLOT + q]);
-        J->thr[lane] = e ? cand_threshold(__uint_as_float(e - 1u), P->n) : -INFINITY;
-    }
-    __syncthreads();
-    // bin `lane` covers fp32 patterns [B << s, (B+1) << s) with B = lane (mod 64),
-    // B in [cp_lo >> s, (cp_lo >> s) + 63]; its threshold is the lowest T_k of
-    // every level some CP in the bin may meet.
-    const uint32_t s = (uint32_t)P->bin_shift;
-    const uint32_t blo = P->cp_lo_bits >> s;
-    const uint32_t B = blo + (((uint32_t)lane - blo) & 63u);
-    uint32_t lowbits = B << s;
-    if (lowbits < P->cp_lo_bits) lowbits = P->cp_lo_bits;
-    const float low = __uint_as_float(lowbits);
-    float g = INFINITY;
-    for (int k = 0; k < P->k; ++k)
-        if (P->hi[k] >= low) g = fminf(g, J->thr[k]);
-    J->table[lane] = __float_as_uint(g);
+    build_table(J, cs(J->prob));
 }
 
 // ---------------------------------------------------------------------------
@@ -747,14 +784,72 @@ __device__ __forceinline__ void wave_best4(double& c, uint64_t& i, double& cp, d
 constexpr int CERT_LDS_TABLES = 32 * 1024;  // fp64 tables staged in LDS when they fit
 constexpr int CERT_CACHE = 512;             // candidates cached in LDS by each certification wave
 
+// Merge of a source's certification waves into its K choices, by the block
+// that finishes certification last (64 threads).  When no list overflowed and
+// no row was bad, the seed slots and the fallback state are cleared for the
+// next call (a call that leaves anything else behind makes the host re-run
+// k_init first).
+__device__ void merge_cert(JD J, PD P) {
+    const int K = P->k;
+    // lane = (level, wave) pair; levels in groups of 64 / CERT_WAVES
+    constexpr int LPG = 64 / CERT_WAVES;
+    const int lane = threadIdx.x, w = lane % CERT_WAVES, kk = lane / CERT_WAVES;
+    for (int k0 = 0; k0 < K; k0 += LPG) {
+        const int k = k0 + kk;
+        double bc = -1.0, bcp = 0.0, bd = 0.0;
+        uint64_t bi = ~0ull;
+        if (k < K && w < J->cert_waves) {
+            bc = J->cert_c[k * CERT_WAVES + w];
+            bi = J->cert_i[k * CERT_WAVES + w];
+            bcp = J->cert_cp[k * CERT_WAVES + w];
+            bd = J->cert_d[k * CERT_WAVES + w];
+        }
+        for (int o = CERT_WAVES / 2; o > 0; o >>= 1) {
+            const double c2 = __shfl_xor(bc, o);
+            const uint64_t i2 = __shfl_xor(bi, o);
+            const double p2 = __shfl_xor(bcp, o);
+            const double d2 = __shfl_xor(bd, o);
+            if (better(c2, i2, bc, bi)) {
+                bc = c2;
+                bi = i2;
+                bcp = p2;
+                bd = d2;
+            }
+        }
+        if (w == 0 && k < K) {
+            dy_choice* o = J->out + k;
+            if (bi != ~0ull) {
+                o->index = (int64_t)bi;
+                o->feasible = 1;
+                o->corr = (float)bc;
+                o->cp = (float)bcp;
+                o->demand = (float)bd;
+            } else {
+                o->index = -1;
+                o->feasible = 0;
+                o->corr = NAN;
+                o->cp = NAN;
+                o->demand = NAN;
+            }
+        }
+    }
+    if (*J->flags == 0) {
+        for (int i = threadIdx.x; i < KMAX * NSLOT; i += 64) J->scert[i] = 0u;
+        if (threadIdx.x < KMAX) {
+            J->fb_corr[threadIdx.x] = 0ull;
+            J->fb_index[threadIdx.x] = ~0ull;
+        }
+    }
+}
+
 // Certification: grid (cert_waves, source, level), one wave per block.  Pass
 // A tightens the level's threshold with the candidates whose fp32 CP is
 // certainly feasible.  Pass B re-evaluates in fp64 every candidate of this
 // wave's share that could still win the level (its CP only when its corr
 // could beat the lane's current best) and keeps the feasible one with the
-// greatest corr, then the lowest index.  k_cert_final merges the waves of a
-// source.  Levels run in separate blocks: each lane walks its candidates once
-// per block instead of once per level.
+// greatest corr, then the lowest index.  The source's block that finishes
+// last merges the waves (merge_cert).  Levels run in separate blocks: each
+// lane walks its candidates once per block instead of once per level.
 __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs) {
     extern __shared__ double s_tab[];
     __shared__ double s_f[NMAX * 64];
@@ -839,54 +934,7 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
         J->cert_cp[k * CERT_WAVES + g] = bcp;
         J->cert_d[k * CERT_WAVES + g] = bd;
     }
-}
-
-__global__ void __launch_bounds__(64) k_cert_final(const JobDev* __restrict__ jobs) {
-    JD J = cs(jobs + blockIdx.x);
-    PD P = cs(J->prob);
-    const int K = P->k;
-    // lane = (level, wave) pair; levels in groups of 64 / CERT_WAVES
-    constexpr int LPG = 64 / CERT_WAVES;
-    const int lane = threadIdx.x, w = lane % CERT_WAVES, kk = lane / CERT_WAVES;
-    for (int k0 = 0; k0 < K; k0 += LPG) {
-        const int k = k0 + kk;
-        double bc = -1.0, bcp = 0.0, bd = 0.0;
-        uint64_t bi = ~0ull;
-        if (k < K && w < J->cert_waves) {
-            bc = J->cert_c[k * CERT_WAVES + w];
-            bi = J->cert_i[k * CERT_WAVES + w];
-            bcp = J->cert_cp[k * CERT_WAVES + w];
-            bd = J->cert_d[k * CERT_WAVES + w];
-        }
-        for (int o = CERT_WAVES / 2; o > 0; o >>= 1) {
-            const double c2 = __shfl_xor(bc, o);
-            const uint64_t i2 = __shfl_xor(bi, o);
-            const double p2 = __shfl_xor(bcp, o);
-            const double d2 = __shfl_xor(bd, o);
-            if (better(c2, i2, bc, bi)) {
-                bc = c2;
-                bi = i2;
-                bcp = p2;
-                bd = d2;
-            }
-        }
-        if (w == 0 && k < K) {
-            dy_choice* o = J->out + k;
-            if (bi != ~0ull) {
-                o->index = (int64_t)bi;
-                o->feasible = 1;
-                o->corr = (float)bc;
-                o->cp = (float)bcp;
-                o->demand = (float)bd;
-            } else {
-                o->index = -1;
-                o->feasible = 0;
-                o->corr = NAN;
-                o->cp = NAN;
-                o->demand = NAN;
-            }
-        }
-    }
+    if (last_block(J->sync, (uint32_t)(J->cert_waves * P->k))) merge_cert(J, P);
 }
 
 // Overflow recovery: the candidates gathered before the list overflowed
@@ -1156,9 +1204,6 @@ hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStrea
 
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, hipStream_t s) {
     hipLaunchKernelGGL(k_certify, dim3(waves, njobs, kmax), dim3(64), CERT_LDS_TABLES, s, d_jobs);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_cert_final, dim3(njobs), dim3(64), 0, s, d_jobs);
     return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libdyplan.so")
 
 DY_OK, DY_EINVAL, DY_ENOTDAG, DY_ELIMIT, DY_ENOMEM, DY_EDEVICE = 0, -1, -2, -3, -4, -5
 DY_SOURCE_RANGE, DY_SOURCE_ROWS = 0, 1
-DY_OPT_TIMING, DY_OPT_SAMPLE_STRIDE, DY_OPT_CAND_CAPACITY, DY_OPT_FORCE_FP64, DY_OPT_JIT = 1, 2, 3, 4, 5
+DY_OPT_TIMING, DY_OPT_SAMPLE_STRIDE, DY_OPT_CAND_CAPACITY, DY_OPT_FORCE_FP64, DY_OPT_JIT, DY_OPT_GRAPH = 1, 2, 3, 4, 5, 6
 DY_MAX_NODES, DY_MAX_RADIX, DY_MAX_LEVELS, DY_MAX_BACKENDS = 32, 255, 32, 64
 
 EXPORTED = ("dy_plan_create", "dy_plan_select", "dy_plan_score", "dy_plan_destroy", "dy_plan_max_levels",

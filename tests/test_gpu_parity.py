@@ -479,3 +479,29 @@ def test_rows_early_exit_near_threshold(n_nodes):
             d = torch.from_numpy(rows).cuda()
             got = plan.select([D.rows_source(0, d, rows.shape[0], n_nodes, 5)], stream=stream())[0]
         assert_choices(got, want, f"N={n_nodes} trial {trial}")
+
+
+def test_graph_replay_matches_eager_calls():
+    # repeated identical calls are replayed from a HIP graph; every replay, with
+    # eager work and synchronisations in between and a different call in the
+    # middle (which invalidates the graph), must give the oracle's answer
+    prob = wl.forkjoin8()
+    a, b = (D.range_source(0, 1000, 3000000),), (D.range_source(0, 5000000, 2000000),)
+    want_a = orc.select_range(prob, 1000, 3000000)
+    want_b = orc.select_range(prob, 5000000, 2000000)
+    rows = wl.make_rows(200000, 24, 36, row_begin=777)
+    want_r = orc.select_rows(wl.stream24(), rows, index_base=3)
+    with D.Plan([prob, wl.stream24()]) as plan:
+        d = torch.from_numpy(rows).cuda()
+        r = (D.rows_source(1, d, 200000, 24, 3),)
+        for i in range(6):
+            assert_choices(plan.select(list(a), stream=stream())[0], want_a, f"replay {i}")
+            x = torch.randn(4096, device="cuda")
+            assert torch.isfinite((x * 2).sum()).item()
+            torch.cuda.synchronize()
+            if i == 3:
+                assert_choices(plan.select(list(b), stream=stream())[0], want_b, "other range")
+            if i % 2 == 1:
+                assert_choices(plan.select(list(r), stream=stream())[0], want_r, f"rows replay {i}")
+        plan.set_option(D.DY_OPT_GRAPH, 0)
+        assert_choices(plan.select(list(a), stream=stream())[0], want_a, "eager")
