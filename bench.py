@@ -10,8 +10,17 @@ Default workload: forkjoin8 (8-node fork-join DAG, 12 implementations per
 node, 12^8 = 429,981,696 plans, 8 pressure levels).  --workload picks another
 (chain4, layered10, batch6, stream24) for profiling.
 
+Two timed loops of the same K calls: the first, as a caller runs them
+(repeated calls replay one HIP graph), gives "value" and "ms_per_step"; the
+second runs with the library's timing option, which records HIP events around
+the scoring kernel on the call's stream (timed calls launch directly, since
+events inside a graph are not updated by its replays), and gives the
+roofline's kernel duration ("ms_per_step_timed" is that loop's step time).
+
 Prints one JSON line (rank 0).  The roofline object describes the dominant
-kernel, timed live with HIP events recorded by the library on the call's stream.
+kernel; "traffic" is the HBM traffic per launch from stored rocprofv3
+FETCH_SIZE / WRITE_SIZE counters (calibrated on a device copy), reported only
+while the kernel sources are the ones the counters were taken on.
 """
 from __future__ import annotations
 
@@ -28,8 +37,79 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "candidate plans scored/sec on 1 MI355X; % of FP32 VALU (or HBM) roofline"
-PEAK_VALU = 256 * 64 * 2.4e9      # fp32 lane-ops/s without packed math or FMA counting
+# MI355X fp32 vector peak 157.3 TFLOP/s = 256 CUs x 2.4 GHz x 128 FMA lanes per
+# clock x 2 flops.  This op mix (multiply, add, max, compare) has no FMA: its
+# peak is one operation per lane slot, 256 x 2.4e9 x 128 = 78.6e12 ops/s.
+PEAK_VALU = 256 * 2.4e9 * 128
 PEAK_HBM = 8.0e12                 # bytes/s
+
+# Kernel sources whose hash keys the stored HBM-traffic counters: a stored
+# figure is reported only while these files are unchanged.
+KERNEL_SOURCES = ("paper_2607_02942_amd/csrc/kernels.hip", "paper_2607_02942_amd/csrc/jit_rows.cpp",
+                  "paper_2607_02942_amd/csrc/dyplan_internal.h")
+DOMINANT = {"stream24": "dy_rows_scan_a"}  # else the sweep kernel
+
+
+def kernel_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(workload):
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+
+
+def stored_traffic(workload):
+    """HBM bytes per launch of the dominant kernel, from the counters stored
+    for the current kernel sources (None when absent or stale)."""
+    try:
+        with open(traffic_path(workload)) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    return t["traffic_bytes_per_launch"] if t.get("source_sha") == kernel_source_sha() else None
+
+
+def _pmc_means(db, counter):
+    """{kernel name: mean per dispatch of `counter`} from a rocprofv3 counter database."""
+    import sqlite3
+    con = sqlite3.connect(db)
+    per = {}
+    for name, disp, val in con.execute(
+            "select kernel_name, dispatch_id, sum(value) from counters_collection where counter_name = ? "
+            "group by dispatch_id", (counter,)):
+        per.setdefault(name, []).append(val)
+    return {k: sum(v) / len(v) for k, v in per.items()}
+
+
+def ingest_pmc(workload, fetch_db, write_db, calib_fetch_db, calib_write_db, calib_bytes, commands):
+    """Store the dominant kernel's HBM traffic per launch: FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch), each scaled by bytes / counter of a plain
+    device copy of known size."""
+    def pick(means, key):
+        hits = [(k, v) for k, v in means.items() if key in k]
+        if not hits:
+            raise SystemExit(f"no kernel matching {key!r} in {sorted(means)}")
+        return hits[0]
+    kern = DOMINANT.get(workload, "k_sweep")
+    kname, fetch = pick(_pmc_means(fetch_db, "FETCH_SIZE"), kern)
+    _, write = pick(_pmc_means(write_db, "WRITE_SIZE"), kern)
+    _, cf = pick(_pmc_means(calib_fetch_db, "FETCH_SIZE"), "copyBuffer")
+    _, cw = pick(_pmc_means(calib_write_db, "WRITE_SIZE"), "copyBuffer")
+    ff, fw = calib_bytes / (cf * 1024.0), calib_bytes / (cw * 1024.0)
+    rec = {"workload": workload, "kernel": kname, "source_sha": kernel_source_sha(),
+           "fetch_kib_per_dispatch": fetch, "write_kib_per_dispatch": write,
+           "calib_copy_bytes": calib_bytes, "calib_fetch_kib": cf, "calib_write_kib": cw,
+           "fetch_factor": ff, "write_factor": fw,
+           "traffic_bytes_per_launch": fetch * 1024.0 * ff + write * 1024.0 * fw,
+           "commands": commands}
+    with open(traffic_path(workload), "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec), flush=True)
 
 
 def edge_count(prob):
@@ -91,7 +171,14 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=1 << 26)
     ap.add_argument("--sample-stride", type=int, default=0)
     ap.add_argument("--calib-copy", type=int, default=0, help="MiB: run one device copy (counter calibration)")
+    ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_DB", "WRITE_DB", "CALIB_FETCH_DB", "CALIB_WRITE_DB"),
+                    help="store the dominant kernel's traffic from rocprofv3 --pmc databases (no GPU needed)")
+    ap.add_argument("--calib-bytes", type=int, default=1 << 30)
+    ap.add_argument("--pmc-command", action="append", default=[], help="command that produced a database")
     args = ap.parse_args()
+    if args.ingest_pmc:
+        ingest_pmc(args.workload, *args.ingest_pmc, args.calib_bytes, args.pmc_command)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(the work shards by plan range; see DESIGN.md)", file=sys.stderr)
@@ -145,7 +232,6 @@ def main():
     stage_ms = (time.perf_counter() - t0) * 1e3
     if args.sample_stride:
         plan.set_option(D.DY_OPT_SAMPLE_STRIDE, args.sample_stride)
-    plan.set_option(D.DY_OPT_TIMING, 1)
     srcs = (D.DySource * len(sources))(*sources)
     out = (D.DyChoice * (len(sources) * plan.kmax))()
 
@@ -154,41 +240,48 @@ def main():
         if st != 0:
             raise RuntimeError(f"select failed {st}: {D.last_error(plan._h)}")
 
+    def timed_loop(tag):
+        cands, main_ms = [], []
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for i in range(args.steps):
+            step()
+            s = plan.stats()
+            main_ms.append(s.main_ms)
+            cands.append(s.candidates)
+            if i == 0 or (i + 1) % max(1, args.steps // 4) == 0:
+                print(f"[bench] {tag} step {i + 1}/{args.steps}", file=sys.stderr, flush=True)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / args.steps, main_ms, cands
+
+    # 1) the steps as a caller runs them: repeated calls replay one HIP graph
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    main_ms = []
-    cands = []
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record(stream)
-    for i in range(args.steps):
-        step()
-        s = plan.stats()
-        main_ms.append(s.main_ms)
-        cands.append(s.candidates)
-        if i == 0 or (i + 1) % max(1, args.steps // 4) == 0:
-            print(f"[bench] step {i + 1}/{args.steps}", file=sys.stderr, flush=True)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    total_ms = ev0.elapsed_time(ev1)
-    ms_per_step = total_ms / args.steps
+    ms_per_step, _, cands = timed_loop("step")
     value = plans / (ms_per_step / 1e3)
+    # 2) the same calls with the library's HIP events around the scoring kernel
+    #    (on the call's stream; timed calls launch directly, not from a graph)
+    plan.set_option(D.DY_OPT_TIMING, 1)
+    for _ in range(max(1, args.warmup // 2)):
+        step()
+    ms_per_step_timed, main_ms, _ = timed_loop("timed")
     kern_ms = float(np.mean(main_ms))
     kern_plans_s = plans / (kern_ms / 1e3)
 
     if name == "stream24":
         bytes_per_plan = 24.0
         achieved = kern_plans_s * bytes_per_plan
-        roof = {"bound": "hbm", "kernel": "k_scan (rows)", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
-                "unit": "GB/s", "frac": achieved / PEAK_HBM, "traffic": None,
-                "per_unit": "24 B of row per plan", "kernel_ms": kern_ms}
+        roof = {"bound": "hbm", "kernel": "dy_rows_scan_a (rows, generated for the DAG)", "achieved": achieved / 1e9,
+                "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": achieved / PEAK_HBM,
+                "traffic": stored_traffic(name), "per_unit": "24 B of row per plan", "kernel_ms": kern_ms}
     else:
         f = sweep_work_per_plan(prob)
         achieved = kern_plans_s * f
         roof = {"bound": "alu", "kernel": "k_sweep", "achieved": achieved / 1e12, "peak": PEAK_VALU / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_VALU, "traffic": None,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_VALU, "traffic": stored_traffic(name),
                 "per_unit": f"{f:.4f} fp32 ops per plan (prefix-shared sweep)", "kernel_ms": kern_ms,
                 "full_recurrence_ops_per_plan": full_work_per_plan(prob, K)}
 
@@ -201,6 +294,7 @@ def main():
                    "problems": len(probs), "parallelism": "single GPU"},
         "roofline": roof,
         "stage_ms": stage_ms,
+        "ms_per_step_timed": ms_per_step_timed,
         "candidates_per_step": float(np.mean(cands)),
     }
     if not args.no_cpu_baseline:

@@ -170,7 +170,8 @@ enum {
     DY_OPT_FORCE_FP64 = 4,      /* 1: decide every level with the exhaustive fp64 path (default 0) */
     DY_OPT_JIT = 5,             /* 1: score rows with kernels generated for the problem (hiprtc, default 1) */
     DY_OPT_GRAPH = 6            /* 1: replay a call that repeats the previous one (same sources) from a
-                                   HIP graph of its launches (default 1); results are identical */
+                                   HIP graph of its launches (default 1; calls with DY_OPT_TIMING on
+                                   launch directly); results are identical */
 };
 
 /*

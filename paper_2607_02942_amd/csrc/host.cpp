@@ -253,10 +253,11 @@ struct dy_plan {
     // per kernel, which on gfx950 costs more host time than the short kernels
     // of a selection run.  Captured on an internal stream, launched on the
     // caller's.
+    // Calls with timing on always launch directly: events recorded inside a
+    // captured graph are not updated by its replays on this runtime.
     int use_graph = 1;
     hipStream_t cap_stream = nullptr;
     hipGraphExec_t graph = nullptr;
-    int graph_timing = 0;
     dy_stats stats{};
     std::string err;
 };
@@ -726,6 +727,31 @@ void drop_graph(dy_plan* h) {
     h->graph = nullptr;
 }
 
+// Capture what `issue` launches on the plan's capture stream into an
+// executable graph; nullptr (and the error state cleared) when that fails.
+hipGraphExec_t capture_graph(dy_plan* h,
+                             const std::function<void(hipStream_t, const std::function<void(hipError_t, const char*)>&)>&
+                                 issue) {
+    if (hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    hipError_t cap_err = hipSuccess;
+    issue(h->cap_stream, [&](hipError_t x, const char*) {
+        if (x != hipSuccess && cap_err == hipSuccess) cap_err = x;
+    });
+    hipGraph_t graph = nullptr;
+    bool ok = hipStreamEndCapture(h->cap_stream, &graph) == hipSuccess && cap_err == hipSuccess && graph;
+    hipGraphExec_t exec = nullptr;
+    if (ok) ok = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0) == hipSuccess;
+    if (graph) (void)hipGraphDestroy(graph);
+    if (!ok) {
+        exec = nullptr;
+        (void)hipGetLastError();
+    }
+    return exec;
+}
+
 int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value) {
     if (!h) return DY_EINVAL;
     drop_graph(h);
@@ -982,45 +1008,34 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
             ck(launch_jit(h, hjobs[q], p, sample, st), sample ? "rows sample" : "rows scan");
         }
     };
-    // seeding, tables, scoring, certification, copy-out
-    auto issue_main = [&](hipStream_t st, const std::function<void(hipError_t, const char*)>& ck) {
+    using Check = std::function<void(hipError_t, const char*)>;
+    // seeding and tables; the scoring pass (between timing events); certification and copy-out
+    auto issue_pre = [&](hipStream_t st, const Check& ck) {
         launch_seed(S.d_jobs, pp, st, ck);
         jit_pass(jobs.data(), n3, pp.n[3], true, st, ck);
         launch_table_all(S.d_jobs, n_src, st, ck);
+    };
+    auto issue_mid = [&](hipStream_t st, const Check& ck) {
         if (h->timing) ck(hipEventRecord(h->ev[1], st), "hipEventRecord");
         launch_main(S.d_jobs, pp, st, ck);
         jit_pass(jobs.data(), n3, pp.n[3], false, st, ck);
         if (h->timing) ck(hipEventRecord(h->ev[2], st), "hipEventRecord");
+    };
+    auto issue_post = [&](hipStream_t st, const Check& ck) {
         launch_certify_all(S.d_jobs, n_src, cert_waves, h->kmax, st, ck);
         if (h->timing) ck(hipEventRecord(h->ev[3], st), "hipEventRecord");
         ck(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, st), "copy out");
     };
     bool exhausted = h->force_fp64 != 0;
     bool launched = false;
-    if (h->use_graph && !h->force_fp64 && S.clean && !changed) {
-        if (h->graph && h->graph_timing != h->timing) drop_graph(h);
-        if (!h->graph) {  // capture once; any failure falls back to direct launches for this plan
-            bool ok = hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal) == hipSuccess;
-            if (ok) {
-                hipError_t cap_err = hipSuccess;
-                if (h->timing) (void)hipEventRecord(h->ev[0], h->cap_stream);
-                issue_main(h->cap_stream, [&](hipError_t x, const char*) {
-                    if (x != hipSuccess && cap_err == hipSuccess) cap_err = x;
-                });
-                hipGraph_t graph = nullptr;
-                ok = hipStreamEndCapture(h->cap_stream, &graph) == hipSuccess && cap_err == hipSuccess && graph;
-                if (ok) ok = hipGraphInstantiate(&h->graph, graph, nullptr, nullptr, 0) == hipSuccess;
-                if (graph) (void)hipGraphDestroy(graph);
-                if (!ok) {
-                    h->graph = nullptr;
-                    h->use_graph = 0;
-                    (void)hipGetLastError();
-                }
-                h->graph_timing = h->timing;
-            } else {
-                h->use_graph = 0;
-                (void)hipGetLastError();
-            }
+    if (h->use_graph && !h->timing && !h->force_fp64 && S.clean && !changed) {
+        if (!h->graph) {  // capture once; a failure falls back to direct launches for this plan
+            h->graph = capture_graph(h, [&](hipStream_t st, const Check& ck) {
+                issue_pre(st, ck);
+                issue_mid(st, ck);
+                issue_post(st, ck);
+            });
+            if (!h->graph) h->use_graph = 0;
         }
         if (h->graph) {
             S.clean = false;
@@ -1038,7 +1053,9 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
                 chk(launch_init(S.d_jobs + c, std::min(65535, n_src - c), s), "init");
         S.clean = false;
         if (!h->force_fp64) {
-            issue_main(s, chk);
+            issue_pre(s, chk);
+            issue_mid(s, chk);
+            issue_post(s, chk);
         } else {
             if (h->timing) chk(hipEventRecord(h->ev[1], s), "hipEventRecord");
             for (int c = 0; c < n_src; c += 65535)

@@ -503,5 +503,9 @@ def test_graph_replay_matches_eager_calls():
                 assert_choices(plan.select(list(b), stream=stream())[0], want_b, "other range")
             if i % 2 == 1:
                 assert_choices(plan.select(list(r), stream=stream())[0], want_r, f"rows replay {i}")
+        plan.set_option(D.DY_OPT_TIMING, 1)  # timed calls launch directly
+        for i in range(3):
+            assert_choices(plan.select(list(a), stream=stream())[0], want_a, f"timed replay {i}")
+            assert plan.stats().main_ms > 0
         plan.set_option(D.DY_OPT_GRAPH, 0)
         assert_choices(plan.select(list(a), stream=stream())[0], want_a, "eager")
