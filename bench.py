@@ -181,7 +181,7 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the work shards by plan range; see DESIGN.md)", file=sys.stderr)
+              "(the work would shard by plan range or row range, one shard per GPU)", file=sys.stderr)
         sys.exit(2)
 
     import torch
