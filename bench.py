@@ -180,7 +180,7 @@ def main():
         ingest_pmc(args.workload, *args.ingest_pmc, args.calib_bytes, args.pmc_command)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(the work would shard by plan range or row range, one shard per GPU)", file=sys.stderr)
         sys.exit(2)
 
