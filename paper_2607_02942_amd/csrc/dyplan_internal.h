@@ -110,6 +110,9 @@ struct JobDev {
     double* cert_cp;          // [KMAX][CERT_WAVES] its fp64 CP at the level
     double* cert_d;           // [KMAX][CERT_WAVES] its fp64 demand
     uint32_t* sync;           // certification blocks finished (re-armed to 0 by the last)
+    dy_choice* hout;          // [KMAX] host-mapped copy of the choices (null: copied back instead)
+    uint32_t* hncand;         // host-mapped copies of ncand and flags (with hout)
+    int32_t* hflags;
 };
 
 }  // namespace dyp

@@ -48,6 +48,7 @@ thread_local std::string g_create_error;
 constexpr uint64_t kMaxSourcePlans = 1ull << 40;
 constexpr size_t kCandPoolBytes = 1ull << 30;    // candidate slots shared by the sources of one call
 constexpr uint64_t kMinSamples = 4096;           // the adaptive stride keeps at least this many samples
+constexpr int kDirectResults = 64;                // up to this many sources, results go straight to host memory
 constexpr double kU = 0x1p-24;                    // fp32 unit roundoff
 
 struct HostProb {
@@ -85,7 +86,9 @@ struct Scratch {
     // pinned host mirrors
     JobDev* h_jobs = nullptr;   // the job array last uploaded
     JobDev* h_fb = nullptr;
-    char* h_res = nullptr;
+    char* h_res = nullptr;      // pinned, host-coherent result region (choices, counters, flags)
+    char* d_hres = nullptr;     // its device address: certification writes it directly
+    size_t res_ncand_off = 0, res_flags_off = 0;
     dy_choice* h_out = nullptr;
     uint32_t* h_ncand = nullptr;
     int32_t* h_flags = nullptr;
@@ -347,13 +350,17 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
     s.cand = (Cand*)(s.d + o_cand);
     if ((e = hipHostMalloc((void**)&s.h_jobs, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
         (e = hipHostMalloc((void**)&s.h_fb, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
-        (e = hipHostMalloc((void**)&s.h_res, res_bytes, hipHostMallocDefault)) != hipSuccess) {
+        (e = hipHostMalloc((void**)&s.h_res, res_bytes, hipHostMallocMapped | hipHostMallocCoherent)) !=
+            hipSuccess ||
+        (e = hipHostGetDevicePointer((void**)&s.d_hres, s.h_res, 0)) != hipSuccess) {
         free_scratch(s);
         return hip_fail(&h->err, e, "hipHostMalloc(scratch)");
     }
     s.h_out = (dy_choice*)(s.h_res + res_out);
     s.h_ncand = (uint32_t*)(s.h_res + res_ncand);
     s.h_flags = (int32_t*)(s.h_res + res_flags);
+    s.res_ncand_off = res_ncand;
+    s.res_flags_off = res_flags;
     s.uploaded = 0;
     return DY_OK;
 }
@@ -950,6 +957,11 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         J.ncand = S.ncand + q;
         J.flags = S.flags + q;
         J.out = S.out + (size_t)j * km;
+        if (n_src <= kDirectResults) {  // few sources: certification writes the host copy directly
+            J.hout = (dy_choice*)S.d_hres + (size_t)j * km;
+            J.hncand = (uint32_t*)(S.d_hres + S.res_ncand_off) + q;
+            J.hflags = (int32_t*)(S.d_hres + S.res_flags_off) + q;
+        }
         J.fb_corr = S.fb_corr + (size_t)q * KMAX;
         J.fb_index = S.fb_index + (size_t)q * KMAX;
         J.cert_waves = cert_waves;
@@ -1024,7 +1036,8 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     auto issue_post = [&](hipStream_t st, const Check& ck) {
         launch_certify_all(S.d_jobs, n_src, cert_waves, h->kmax, st, ck);
         if (h->timing) ck(hipEventRecord(h->ev[3], st), "hipEventRecord");
-        ck(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, st), "copy out");
+        if (n_src > kDirectResults)
+            ck(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, st), "copy out");
     };
     bool exhausted = h->force_fp64 != 0;
     bool launched = false;

@@ -790,6 +790,7 @@ constexpr int CERT_CACHE = 512;             // candidates cached in LDS by each 
 // next call (a call that leaves anything else behind makes the host re-run
 // k_init first).
 __device__ void merge_cert(JD J, PD P) {
+    __shared__ dy_choice s_out[KMAX];
     const int K = P->k;
     // lane = (level, wave) pair; levels in groups of 64 / CERT_WAVES
     constexpr int LPG = 64 / CERT_WAVES;
@@ -817,20 +818,34 @@ __device__ void merge_cert(JD J, PD P) {
             }
         }
         if (w == 0 && k < K) {
-            dy_choice* o = J->out + k;
+            dy_choice c;
             if (bi != ~0ull) {
-                o->index = (int64_t)bi;
-                o->feasible = 1;
-                o->corr = (float)bc;
-                o->cp = (float)bcp;
-                o->demand = (float)bd;
+                c.index = (int64_t)bi;
+                c.feasible = 1;
+                c.corr = (float)bc;
+                c.cp = (float)bcp;
+                c.demand = (float)bd;
             } else {
-                o->index = -1;
-                o->feasible = 0;
-                o->corr = NAN;
-                o->cp = NAN;
-                o->demand = NAN;
+                c.index = -1;
+                c.feasible = 0;
+                c.corr = NAN;
+                c.cp = NAN;
+                c.demand = NAN;
             }
+            J->out[k] = c;
+            s_out[k] = c;
+        }
+    }
+    // the host-mapped copy: the K choices as consecutive dwords, then the counters
+    __syncthreads();
+    if (J->hout) {
+        static_assert(sizeof(dy_choice) == 24, "6 dwords per choice");
+        const uint32_t* src = (const uint32_t*)s_out;
+        uint32_t* dst = (uint32_t*)J->hout;
+        for (int i = threadIdx.x; i < K * 6; i += 64) dst[i] = src[i];
+        if (threadIdx.x == 0) {
+            *J->hncand = *J->ncand;
+            *J->hflags = *J->flags;
         }
     }
     if (*J->flags == 0) {
