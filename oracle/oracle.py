@@ -1,4 +1,5 @@
-"""ctypes binding of the plain fp64 CPU oracle (oracle.c).
+"""ctypes binding of the plain fp64 CPU oracle (oracle.c: corr / CP / demand
+selection; objective.c: the paper's additive objective J_L).
 
 TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
 CPU-baseline leg may use this module; the product path never does.  It shares
@@ -16,13 +17,14 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
 SRC_PATH = os.path.join(_HERE, "oracle.c")
+OBJ_PATH = os.path.join(_HERE, "objective.c")
 CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-std=c11"]
 
 
 def build(force: bool = True) -> str:
-    """Compile oracle.c into liboracle.so (plain gcc, fp64, no FMA contraction)."""
+    """Compile oracle.c and objective.c into liboracle.so (plain gcc, fp64, no FMA contraction)."""
     if force or not os.path.exists(LIB_PATH):
-        subprocess.check_call(["gcc", *CFLAGS, "-o", LIB_PATH, SRC_PATH, "-lm"])
+        subprocess.check_call(["gcc", *CFLAGS, "-o", LIB_PATH, SRC_PATH, OBJ_PATH, "-lm"])
     return LIB_PATH
 
 
@@ -34,6 +36,18 @@ class _Problem(ctypes.Structure):
         ("backend", ctypes.c_void_p), ("w", ctypes.c_void_p),
         ("n_levels", ctypes.c_int32), ("n_backends", ctypes.c_int32),
         ("rho", ctypes.c_void_p), ("slo", ctypes.c_float),
+    ]
+
+
+class _ObjProblem(ctypes.Structure):
+    _fields_ = [
+        ("n_nodes", ctypes.c_int32), ("n_edges", ctypes.c_int32),
+        ("edges", ctypes.c_void_p), ("radix", ctypes.c_void_p), ("max_radix", ctypes.c_int32),
+        ("q", ctypes.c_void_p), ("tau", ctypes.c_void_p), ("cost", ctypes.c_void_p),
+        ("v", ctypes.c_void_p), ("is_tool", ctypes.c_void_p),
+        ("lambda_f", ctypes.c_float), ("lambda_c", ctypes.c_float), ("lambda_l", ctypes.c_float),
+        ("lambda_ld", ctypes.c_float), ("beta", ctypes.c_float), ("effort", ctypes.c_float),
+        ("n_levels", ctypes.c_int32), ("levels", ctypes.c_void_p),
     ]
 
 
@@ -74,6 +88,14 @@ def lib():
         L.or_cp0_range.argtypes = [P, i32, vp, u64, u64, u64, vp]
         for f in ("or_select_range", "or_select_rows", "or_score_range", "or_score_rows",
                   "or_score_indices", "or_cp0_hist", "or_cp0_range"):
+            getattr(L, f).restype = ctypes.c_int32
+        Q = ctypes.POINTER(_ObjProblem)
+        L.op_reach.argtypes = [Q, vp]
+        L.op_eval.argtypes = [Q, vp, vp, vp, vp, vp]
+        L.op_select_range.argtypes = [Q, u64, u64, vp]
+        L.op_select_rows.argtypes = [Q, vp, u64, u64, u64, vp]
+        L.op_score.argtypes = [Q, i32, vp, u64, u64, u64, vp, vp, vp, vp]
+        for f in ("op_reach", "op_eval", "op_select_range", "op_select_rows", "op_score"):
             getattr(L, f).restype = ctypes.c_int32
         _lib = L
     return _lib
@@ -225,3 +247,98 @@ def merge_choices(parts: List[List[tuple]]) -> List[tuple]:
             if b[0] < 0 or c[2] > b[2] or (c[2] == b[2] and c[0] < b[0]):
                 best[k] = c
     return best
+
+
+# ---------------------------------------------------------------------------
+# the paper's additive objective (objective.c)
+# ---------------------------------------------------------------------------
+
+class ObjectiveProblem:
+    """C view of a problem under the additive objective: quality q = p, vulnerability
+    v = w, nominal durations tau, and the objective's costs, weights and levels."""
+
+    def __init__(self, prob, obj):
+        self.n_nodes = int(prob.n_nodes)
+        self.edges = np.ascontiguousarray(prob.edges, dtype=np.int32).reshape(-1, 2)
+        self.radix = np.ascontiguousarray(prob.radix, dtype=np.int32)
+        self.q = np.ascontiguousarray(prob.p, dtype=np.float32)
+        self.tau = np.ascontiguousarray(prob.tau, dtype=np.float32)
+        self.cost = np.ascontiguousarray(obj.cost, dtype=np.float32)
+        self.v = np.ascontiguousarray(prob.w, dtype=np.float32)
+        self.is_tool = None if obj.is_tool is None else np.ascontiguousarray(obj.is_tool, dtype=np.int32)
+        self.levels = np.ascontiguousarray(obj.levels, dtype=np.float32)
+        self.K = int(self.levels.shape[0])
+        self.c = _ObjProblem(
+            self.n_nodes, int(self.edges.shape[0]), self.edges.ctypes.data, self.radix.ctypes.data,
+            int(self.q.shape[1]), self.q.ctypes.data, self.tau.ctypes.data, self.cost.ctypes.data,
+            self.v.ctypes.data, None if self.is_tool is None else self.is_tool.ctypes.data,
+            obj.lambda_f, obj.lambda_c, obj.lambda_l, obj.lambda_ld, obj.beta, obj.effort,
+            self.K, self.levels.ctypes.data)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+class ObjChoice(ctypes.Structure):
+    _fields_ = [("index", ctypes.c_int64), ("feasible", ctypes.c_int32),
+                ("j", ctypes.c_double), ("t", ctypes.c_double), ("d", ctypes.c_double)]
+
+    def as_tuple(self):
+        return (int(self.index), int(self.feasible), float(self.j), float(self.t), float(self.d))
+
+
+def _oq(prob, obj) -> ObjectiveProblem:
+    return prob if isinstance(prob, ObjectiveProblem) else ObjectiveProblem(prob, obj)
+
+
+def obj_reach(prob, obj) -> np.ndarray:
+    q = _oq(prob, obj)
+    out = np.zeros(q.n_nodes, np.float64)
+    if lib().op_reach(q.ref, out.ctypes.data) != 0:
+        raise ValueError("bad problem")
+    return out
+
+
+def obj_eval(prob, obj, impl):
+    """(U, T, D, [J_k]) of one plan given by its implementation ids."""
+    q = _oq(prob, obj)
+    a = np.ascontiguousarray(impl, dtype=np.int32)
+    U, T, D = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    J = np.zeros(q.K, np.float64)
+    if lib().op_eval(q.ref, a.ctypes.data, ctypes.byref(U), ctypes.byref(T), ctypes.byref(D), J.ctypes.data):
+        raise ValueError("bad problem")
+    return U.value, T.value, D.value, J
+
+
+def obj_select_range(prob, obj, begin: int, count: int) -> List[tuple]:
+    q = _oq(prob, obj)
+    out = (ObjChoice * q.K)()
+    if lib().op_select_range(q.ref, int(begin), int(count), out) != 0:
+        raise ValueError("bad problem")
+    return [c.as_tuple() for c in out]
+
+
+def obj_select_rows(prob, obj, rows: np.ndarray, index_base: int = 0) -> List[tuple]:
+    q = _oq(prob, obj)
+    rows = np.ascontiguousarray(rows, dtype=np.uint8)
+    out = (ObjChoice * q.K)()
+    if lib().op_select_rows(q.ref, rows.ctypes.data, rows.shape[0], rows.shape[1], int(index_base), out) != 0:
+        raise ValueError("bad problem")
+    return [c.as_tuple() for c in out]
+
+
+def obj_score(prob, obj, begin: int = 0, count: Optional[int] = None, rows: Optional[np.ndarray] = None):
+    """Per-plan U, T, D and J[:, k] over a range or over rows."""
+    q = _oq(prob, obj)
+    if rows is not None:
+        rows = np.ascontiguousarray(rows, dtype=np.uint8)
+        n, kind, rp, st = rows.shape[0], 1, rows.ctypes.data, rows.shape[1]
+    else:
+        n, kind, rp, st = int(count), 0, None, 0
+    U, T, D = (np.zeros(n, np.float64) for _ in range(3))
+    J = np.zeros((n, q.K), np.float64)
+    if lib().op_score(q.ref, kind, rp, st, int(begin), n, U.ctypes.data, T.ctypes.data, D.ctypes.data,
+                      J.ctypes.data) != 0:
+        raise ValueError("bad problem")
+    return U, T, D, J

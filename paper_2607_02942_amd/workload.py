@@ -199,6 +199,41 @@ class Problem:
             w=self.w.copy(), rho=self.rho.copy())
 
 
+@dataclasses.dataclass
+class Objective:
+    """The paper's additive objective J_L (Sec. 4.3 eq. admission-objective,
+    Sec. 4.4 eq. variant-objective) for a Problem: quality q = Problem.p,
+    vulnerability v = Problem.w, nominal durations Problem.tau.
+
+    cost: float32 [N, R] call cost c_{n,i}; is_tool: int32 [N] (1 = tool node:
+    no quality or cost term, not in D_tau, duration kept in T) or None;
+    levels: float32 [K] the specialisation levels L_k.
+    """
+    cost: np.ndarray
+    levels: np.ndarray
+    lambda_f: float = 1.0
+    lambda_c: float = 0.01
+    lambda_l: float = 0.05
+    lambda_ld: float = 0.05
+    beta: float = 1.0
+    effort: float = 0.5
+    is_tool: Optional[np.ndarray] = None
+
+    @property
+    def n_levels(self) -> int:
+        return int(self.levels.shape[0])
+
+
+PAPER_LEVELS = (0.0, 1.5, 3.0)  # L in {0, 1.5, 3} (balanced trace, Sec. 7)
+
+
+def paper_objective(prob: Problem, levels=PAPER_LEVELS, **weights) -> Objective:
+    """Objective for `prob` with call cost c = tau * size (duration times model
+    size, computed in fp32) and the given levels and weights."""
+    cost = (prob.tau.astype(np.float32) * prob.size.astype(np.float32)).astype(np.float32)
+    return Objective(cost=cost, levels=np.asarray(levels, np.float32), **weights)
+
+
 def levels(k: int, lo: float, hi: float) -> np.ndarray:
     """k pressure levels evenly spaced on [lo, hi], endpoints included."""
     if k == 1:
