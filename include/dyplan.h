@@ -25,6 +25,19 @@
  * Selection at level k: the plan with the greatest corr among plans with
  * CP_k <= slo (inclusive); equal corr goes to the lowest plan index.
  *
+ * Objective mode (dy_problem.objective non-NULL): the paper's own additive
+ * objective, Sec. 4.3 eq. admission-objective with Sec. 4.4 eq.
+ * variant-objective, selected at each specialisation level L_k:
+ *   reach(n) = 1 + beta * e * (|R(n)| - 1) / (|V| - 1), R(n) = n and every
+ *              node reachable from it (1 for a one-node workflow);
+ *   u_{n,i}  = reach(n) p_{n,i} - lambda_f w_n (1 - p_{n,i}) - lambda_c cost_{n,i}
+ *              for LLM nodes (tool nodes carry no quality or cost term);
+ *   T(pi)    = longest path of nominal durations tau (tool nodes included);
+ *   D(pi)    = sum over LLM nodes of tau_{n,i_n} (D_tau);
+ *   J_k(pi)  = sum_{LLM n} u_{n,i_n} - lambda_l T(pi) - lambda_ld L_k D(pi),
+ * and the choice of level k is the plan with the greatest J_k (equal J to the
+ * lowest index); there is no hard constraint, rho and slo are not used.
+ *
  * Plan index: mixed radix over the nodes, node 0 most significant:
  *   index = (...((i_0 * radix_1 + i_1) * radix_2 + i_2)...) * radix_{N-1} + i_{N-1}.
  *
@@ -54,7 +67,7 @@
 extern "C" {
 #endif
 
-#define DY_ABI_VERSION 1
+#define DY_ABI_VERSION 2
 
 #define DY_MAX_NODES 32      /* nodes per problem */
 #define DY_MAX_RADIX 255     /* implementations per node (ids fit a uint8 row byte) */
@@ -95,9 +108,33 @@ typedef struct dy_plan dy_plan; /* opaque handle */
  *                     at level k, 0 <= rho < 1; a node's duration at level k
  *                     is tau / (1 - rho_{k, backend}).
  *  slo                critical-path bound, >= 0 (may be +inf).
+ *  objective          NULL for the corr / SLO selection above, else the
+ *                     paper's additive objective (then n_levels, rho, slo,
+ *                     size and backend are not read; backend and rho may be
+ *                     NULL).
  * Table entries with i >= radix[n] are ignored.  Sum over nodes of the
  * largest tau must stay below 1e30.
  */
+/*
+ * The paper's additive objective (Sec. 4.3-4.4), all values finite:
+ *  cost      float [N][max_radix] call cost c of implementation (n, i).
+ *  is_tool   int32 [N], 1 marks a tool node, or NULL (every node an LLM node).
+ *  lambda_f, lambda_c   weights of the impact-weighted error and of the cost.
+ *  lambda_l  weight of the critical path T, >= 0.
+ *  lambda_ld weight of the demand D_tau, >= 0.
+ *  beta, effort         reach weight parameters (effort e in [0, 1]).
+ *  n_levels, levels     K specialisation levels L_k >= 0, float [K].
+ * |each utility| and lambda_l T and lambda_ld L_k D must stay below 1e30.
+ */
+typedef struct dy_objective {
+    const float* cost;
+    const int32_t* is_tool;
+    float lambda_f, lambda_c, lambda_l, lambda_ld;
+    float beta, effort;
+    int32_t n_levels;
+    const float* levels;
+} dy_objective;
+
 typedef struct dy_problem {
     int32_t n_nodes;
     int32_t n_edges;
@@ -113,6 +150,7 @@ typedef struct dy_problem {
     int32_t n_backends;
     const float* rho;
     float slo;
+    const dy_objective* objective;
 } dy_problem;
 
 enum { DY_SOURCE_RANGE = 0, DY_SOURCE_ROWS = 1 };
@@ -143,7 +181,8 @@ typedef struct dy_source {
 
 /* The selected plan of one level.  index = -1 and feasible = 0 when no plan of
  * the source meets the SLO at that level; corr, cp and demand are then NaN.
- * cp is CP at this level. */
+ * cp is CP at this level.  Objective mode: feasible = 1, corr = J_k of the
+ * plan, cp = T, demand = D_tau (fp64 values rounded to the nearest fp32). */
 typedef struct dy_choice {
     int64_t index;
     int32_t feasible;
@@ -200,6 +239,8 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
  * caller-owned DEVICE buffers (any may be NULL to skip it):
  *  corr[count], cp[count][K] (CP at each level), demand[count],
  *  feas_bits[count] (bit k set iff CP_k <= slo, decided exactly; K <= 32).
+ * Objective mode: corr = sum of the utilities U, cp[.][k] = J_k, demand = D_tau
+ * (fp32; |error| below the per-level bound of the certification), every bit set.
  * Inputs and outputs must stay valid until the stream work completes.
  */
 int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, float* demand,

@@ -71,6 +71,21 @@ struct ProbDev {
     const double* a64;        // [n][rmax] 1 - w (1 - p)
     const double* lat64;      // [k][n][rmax] tau / (1 - rho_{k,b})
     const double* dem64;      // [n][rmax] tau * size
+    // Objective mode (the paper's additive objective, Sec. 4.3-4.4): the same
+    // tables hold at = (u, tau), dem = d (tau for LLM nodes, 0 for tool
+    // nodes), a64 = u in fp64, dem64 = d in fp64, lat / lat64 = tau (one
+    // level); cp_lo_bits / cp_hi_bits / bin_shift then describe the range of
+    // the fp32 D, which indexes the prefilter bins.
+    int32_t obj;
+    uint32_t llm;             // LLM nodes (bit mask): only they add utility and demand
+    float lam_l;              // lambda_l (the fp32 input)
+    int32_t pad1;
+    double lam_l64;
+    float m32[KMAX];          // lambda_ld L_k rounded to fp32
+    double m64[KMAX];         // lambda_ld L_k (exact in fp64)
+    double err2[KMAX];        // twice a bound on |estimate - J_k| for every fp32 estimate of a plan's J_k
+    const float* demx;        // rows of x and y in `dem` (x: a 1-entry 0 row when virtual)
+    const float* demy;
 };
 
 struct Cand {

@@ -19,10 +19,10 @@
 namespace dyp {
 hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s);
-hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_samples, int npre_max,
-                               int npre_c, int kmax, hipStream_t s);
-hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, int npre_c,
-                        int ry, hipStream_t s);
+hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_samples,
+                               int npre_max, int npre_c, int kmax, hipStream_t s);
+hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
+                        int npre_c, int ry, hipStream_t s);
 hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, hipStream_t s);
 hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStream_t s);
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, hipStream_t s);
@@ -55,6 +55,7 @@ struct HostProb {
     int n = 0, k = 0, b = 0, rmax = 0;
     int npre = 0, rx = 1, ry = 1;
     bool uniform = true, has_s2 = false;
+    bool obj = false;           // the paper's additive objective instead of corr / SLO
     uint64_t n_plans = 0;       // saturated
     bool plans_saturated = false;
 };
@@ -147,22 +148,110 @@ int fail(std::string* err, int status, const char* fmt, int a = 0, int b = 0, in
     return status;
 }
 
+// Objective mode: reach(n) = 1 + beta e (|R(n)| - 1) / (|V| - 1), R(n) = n and
+// every node reachable from it (Sec. 4.3, the reach weight of the utility);
+// the fp64 operations in the order the definition writes them.
+void obj_reach(const dy_problem& pb, double* reach) {
+    const int N = pb.n_nodes;
+    uint32_t desc[DY_MAX_NODES];
+    for (int n = N - 1; n >= 0; --n) {
+        desc[n] = 1u << n;
+        for (int e = 0; e < pb.n_edges; ++e)
+            if (pb.edges[2 * e] == n) desc[n] |= desc[pb.edges[2 * e + 1]];
+    }
+    const dy_objective& o = *pb.objective;
+    for (int n = 0; n < N; ++n) {
+        if (N == 1) {
+            reach[n] = 1.0;
+            continue;
+        }
+        double t = (double)o.beta * (double)o.effort;
+        t = t * (double)(__builtin_popcount(desc[n]) - 1);
+        t = t / (double)(N - 1);
+        reach[n] = 1.0 + t;
+    }
+}
+
+bool obj_is_llm(const dy_problem& pb, int n) { return !pb.objective->is_tool || pb.objective->is_tool[n] == 0; }
+
+// u = reach q - lambda_f v (1 - q) - lambda_c c of an LLM node's implementation
+// (Sec. 4.3, eq. admission-objective: quality weighted by reach, minus the
+// impact-weighted error f = v r with r = 1 - q, minus the weighted cost), in fp64,
+// one operation per statement.
+double obj_u(const dy_problem& pb, double reach, int n, size_t e) {
+    const dy_objective& o = *pb.objective;
+    const double q = (double)pb.p[e];
+    double a = reach * q;
+    double b = 1.0 - q;
+    b = (double)pb.w[n] * b;
+    b = (double)o.lambda_f * b;
+    a = a - b;
+    b = (double)o.lambda_c * (double)o.cost[e];
+    a = a - b;
+    return a;
+}
+
+int validate_objective(const dy_problem& pb, int idx, double sum_tau, std::string* err) {
+    const dy_objective& o = *pb.objective;
+    if (!o.cost || !o.levels) return fail(err, DY_EINVAL, "problem %d: objective cost or levels is NULL", idx);
+    if (o.n_levels < 1) return fail(err, DY_EINVAL, "problem %d: objective n_levels must be >= 1", idx);
+    if (o.n_levels > DY_MAX_LEVELS)
+        return fail(err, DY_ELIMIT, "problem %d: objective n_levels %d exceeds %d", idx, o.n_levels, DY_MAX_LEVELS);
+    if (!finite_f(o.lambda_f) || !finite_f(o.lambda_c) || !finite_f(o.beta))
+        return fail(err, DY_EINVAL, "problem %d: objective weights must be finite", idx);
+    if (!(o.lambda_l >= 0.0f && finite_f(o.lambda_l)) || !(o.lambda_ld >= 0.0f && finite_f(o.lambda_ld)))
+        return fail(err, DY_EINVAL, "problem %d: lambda_l and lambda_ld must be finite and >= 0", idx);
+    if (!(o.effort >= 0.0f && o.effort <= 1.0f))
+        return fail(err, DY_EINVAL, "problem %d: effort not in [0, 1]", idx);
+    double lmax = 0.0;
+    for (int k = 0; k < o.n_levels; ++k) {
+        if (!(o.levels[k] >= 0.0f && finite_f(o.levels[k])))
+            return fail(err, DY_EINVAL, "problem %d: level %d must be finite and >= 0", idx, k);
+        lmax = std::max(lmax, (double)o.levels[k]);
+    }
+    const int N = pb.n_nodes;
+    double reach[DY_MAX_NODES];
+    obj_reach(pb, reach);
+    double su = 0.0;
+    for (int n = 0; n < N; ++n) {
+        if (o.is_tool && o.is_tool[n] != 0 && o.is_tool[n] != 1)
+            return fail(err, DY_EINVAL, "problem %d: is_tool[%d] must be 0 or 1", idx, n);
+        if (!std::isfinite(reach[n])) return fail(err, DY_EINVAL, "problem %d: reach weight of node %d overflows", idx, n);
+        double mu = 0.0;
+        for (int i = 0; i < pb.radix[n]; ++i) {
+            const size_t e = (size_t)n * pb.max_radix + i;
+            if (!finite_f(o.cost[e]))
+                return fail(err, DY_EINVAL, "problem %d: cost[%d][%d] must be finite", idx, n, i);
+            if (obj_is_llm(pb, n)) mu = std::max(mu, std::fabs(obj_u(pb, reach[n], n, e)));
+        }
+        su += mu;
+    }
+    if (!(su <= 1e30)) return fail(err, DY_EINVAL, "problem %d: utilities too large", idx);
+    if ((double)o.lambda_l * sum_tau > 1e30 || (double)o.lambda_ld * lmax * sum_tau > 1e30)
+        return fail(err, DY_EINVAL, "problem %d: weighted latency or demand too large", idx);
+    return DY_OK;
+}
+
 int validate_problem(const dy_problem& pb, int idx, std::string* err) {
     const int N = pb.n_nodes;
+    const bool obj = pb.objective != nullptr;
     if (N < 1) return fail(err, DY_EINVAL, "problem %d: n_nodes must be >= 1", idx);
     if (N > DY_MAX_NODES) return fail(err, DY_ELIMIT, "problem %d: n_nodes %d exceeds %d", idx, N, DY_MAX_NODES);
     if (pb.n_edges < 0) return fail(err, DY_EINVAL, "problem %d: negative n_edges", idx);
     if (pb.n_edges > 0 && !pb.edges) return fail(err, DY_EINVAL, "problem %d: edges is NULL", idx);
     if (pb.n_edges > DY_MAX_NODES * DY_MAX_NODES)
         return fail(err, DY_ELIMIT, "problem %d: too many edges", idx);
-    if (!pb.radix || !pb.p || !pb.tau || !pb.size || !pb.backend || !pb.w || !pb.rho)
+    if (!pb.radix || !pb.p || !pb.tau || !pb.w || (!obj && (!pb.size || !pb.backend || !pb.rho)))
         return fail(err, DY_EINVAL, "problem %d: a table pointer is NULL", idx);
-    if (pb.n_levels < 1) return fail(err, DY_EINVAL, "problem %d: n_levels must be >= 1", idx);
-    if (pb.n_levels > DY_MAX_LEVELS)
-        return fail(err, DY_ELIMIT, "problem %d: n_levels %d exceeds %d", idx, pb.n_levels, DY_MAX_LEVELS);
-    if (pb.n_backends < 1) return fail(err, DY_EINVAL, "problem %d: n_backends must be >= 1", idx);
-    if (pb.n_backends > DY_MAX_BACKENDS)
-        return fail(err, DY_ELIMIT, "problem %d: n_backends %d exceeds %d", idx, pb.n_backends, DY_MAX_BACKENDS);
+    if (!obj) {
+        if (pb.n_levels < 1) return fail(err, DY_EINVAL, "problem %d: n_levels must be >= 1", idx);
+        if (pb.n_levels > DY_MAX_LEVELS)
+            return fail(err, DY_ELIMIT, "problem %d: n_levels %d exceeds %d", idx, pb.n_levels, DY_MAX_LEVELS);
+        if (pb.n_backends < 1) return fail(err, DY_EINVAL, "problem %d: n_backends must be >= 1", idx);
+        if (pb.n_backends > DY_MAX_BACKENDS)
+            return fail(err, DY_ELIMIT, "problem %d: n_backends %d exceeds %d", idx, pb.n_backends,
+                        DY_MAX_BACKENDS);
+    }
     int rmax = 0;
     for (int n = 0; n < N; ++n) {
         if (pb.radix[n] < 1) return fail(err, DY_EINVAL, "problem %d: radix[%d] < 1", idx, n);
@@ -186,22 +275,26 @@ int validate_problem(const dy_problem& pb, int idx, std::string* err) {
         double mt = 0.0, md = 0.0;
         for (int i = 0; i < pb.radix[n]; ++i) {
             size_t e = (size_t)n * pb.max_radix + i;
-            float p = pb.p[e], t = pb.tau[e], s = pb.size[e];
-            int b = pb.backend[e];
+            float p = pb.p[e], t = pb.tau[e];
             if (!(p >= 0.0f && p <= 1.0f))
                 return fail(err, DY_EINVAL, "problem %d: p[%d][%d] not in [0, 1]", idx, n, i);
             if (!finite_f(t) || t < 0.0f)
                 return fail(err, DY_EINVAL, "problem %d: tau[%d][%d] must be finite and >= 0", idx, n, i);
+            mt = std::max(mt, (double)t);
+            if (obj) continue;
+            float s = pb.size[e];
+            int b = pb.backend[e];
             if (!finite_f(s) || s < 0.0f)
                 return fail(err, DY_EINVAL, "problem %d: size[%d][%d] must be finite and >= 0", idx, n, i);
             if (b < 0 || b >= pb.n_backends)
                 return fail(err, DY_EINVAL, "problem %d: backend[%d][%d] out of range", idx, n, i);
-            mt = std::max(mt, (double)t);
             md = std::max(md, (double)t * (double)s);
         }
         sum_tau += mt;
         sum_dem += md;
     }
+    if (sum_tau > 1e30) return fail(err, DY_EINVAL, "problem %d: durations too large", idx);
+    if (obj) return validate_objective(pb, idx, sum_tau, err);
     for (int k = 0; k < pb.n_levels; ++k)
         for (int b = 0; b < pb.n_backends; ++b) {
             float r = pb.rho[k * pb.n_backends + b];
@@ -366,9 +459,82 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
 }
 
 // Builds the device image of every problem: ProbDev descriptors + tables.
+// Objective mode: tables of the per-node terms and the certification bounds.
+// An fp32 estimate of a plan's J_k (sums of the fp32-rounded terms in node
+// order, the longest path in fp32, then the weights) differs from the fp64
+// evaluation of the definition by at most E_k = (N + 6) u A_k (1 + 2^-10) +
+// (3N + 8) 2^-149 (1 + lambda_l + m_k), with A_k = sum of the largest |u| +
+// lambda_l T_max + m_k D_max, m_k = lambda_ld L_k: the sums of N terms err by
+// (N - 1) u of their magnitude, each rounded term and weight product by u more,
+// and fp64 adds (N + 3) 2^-53; the last term covers subnormal roundings.
+void stage_objective(const dy_problem& pb, ProbDev& D, float2* at, float2* atx, float* dz, float* dem, float* lat,
+                     double* a64, double* lat64, double* dem64) {
+    const dy_objective& o = *pb.objective;
+    const int N = pb.n_nodes, R = pb.max_radix, K = o.n_levels;
+    double reach[DY_MAX_NODES];
+    obj_reach(pb, reach);
+    D.obj = 1;
+    D.llm = 0;
+    float dlo = 0.0f, dhi = 0.0f;  // fp32 D of the plans with the smallest / largest d everywhere (node order)
+    float tmx[DY_MAX_NODES];
+    double su = 0.0, dsum = 0.0;
+    for (int n = 0; n < N; ++n) {
+        const bool llm = obj_is_llm(pb, n);
+        if (llm) D.llm |= 1u << n;
+        float dmn = INFINITY, dmx = 0.0f;
+        double mu = 0.0;
+        tmx[n] = 0.0f;
+        for (int i = 0; i < pb.radix[n]; ++i) {
+            const size_t e2 = (size_t)n * R + i;
+            const float tau = pb.tau[e2] == 0.0f ? 0.0f : pb.tau[e2];
+            const double u = llm ? obj_u(pb, reach[n], n, e2) : 0.0;
+            const float d = llm ? tau : 0.0f;
+            a64[e2] = u;
+            dem64[e2] = (double)d;
+            lat64[e2] = (double)tau;
+            at[e2] = make_float2((float)u, tau);
+            dem[e2] = d;
+            lat[e2] = tau;
+            mu = std::max(mu, std::fabs(u));
+            dmn = std::min(dmn, d);
+            dmx = std::max(dmx, d);
+            tmx[n] = std::max(tmx[n], tau);
+        }
+        su += mu;
+        dsum += (double)dmx;
+        dlo = dlo + dmn;
+        dhi = dhi + dmx;
+    }
+    *atx = make_float2(0.0f, 0.0f);
+    *dz = 0.0f;
+    // longest path with every node at its longest duration, fp64
+    double f[DY_MAX_NODES], tmax = 0.0;
+    for (int n = 0; n < N; ++n) {
+        double m = 0.0;
+        for (int v = 0; v < n; ++v)
+            if (D.pred[n] >> v & 1u) m = std::max(m, f[v]);
+        f[n] = (double)tmx[n] + m;
+        if (D.sinks >> n & 1u) tmax = std::max(tmax, f[n]);
+    }
+    D.cp_lo_bits = f2u(dlo);
+    D.cp_hi_bits = f2u(dhi);
+    D.lam_l = o.lambda_l;
+    D.lam_l64 = (double)o.lambda_l;
+    const double grow = 1.0 + 0x1p-20;  // magnitudes of fp32 sums exceed the fp64 ones by < N u
+    for (int k = 0; k < K; ++k) {
+        const double m = (double)o.lambda_ld * (double)o.levels[k];  // 24 x 24 bits: exact
+        D.m64[k] = m;
+        D.m32[k] = (float)m;
+        const double A = (su + D.lam_l64 * tmax + m * dsum) * grow;
+        const double E = (N + 6) * kU * A * (1.0 + 0x1p-10) + (3.0 * N + 8.0) * 0x1p-149 * (1.0 + D.lam_l64 + m);
+        D.err2[k] = 2.0 * E * (1.0 + 0x1p-40);
+        D.lvl_order[k] = k;
+    }
+}
+
 int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::string* err) {
     struct Layout {
-        size_t at, atx, dem, lat, a64, lat64, dem64;
+        size_t at, atx, dz, dem, lat, a64, lat64, dem64;
     };
     std::vector<Layout> lay(n_probs);
     size_t off = align_up((size_t)n_probs * sizeof(ProbDev), 256);
@@ -382,15 +548,18 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
     for (int j = 0; j < n_probs; ++j) {
         const dy_problem& pb = probs[j];
         const size_t NR = (size_t)pb.n_nodes * pb.max_radix;
+        // objective mode: one latency level (nominal durations)
+        const int KL = pb.objective ? 1 : pb.n_levels;
         Layout& L = lay[j];
         L.at = take(NR * sizeof(float2));
         L.atx = take(sizeof(float2));
+        L.dz = take(sizeof(float));
         L.dem = take(NR * sizeof(float));
-        L.lat = take((size_t)pb.n_levels * NR * sizeof(float));
+        L.lat = take((size_t)KL * NR * sizeof(float));
         L.a64 = take(NR * sizeof(double));
-        L.lat64 = take((size_t)pb.n_levels * NR * sizeof(double));
+        L.lat64 = take((size_t)KL * NR * sizeof(double));
         L.dem64 = take(NR * sizeof(double));
-        h->kmax = std::max(h->kmax, pb.n_levels);
+        h->kmax = std::max(h->kmax, pb.objective ? pb.objective->n_levels : pb.n_levels);
     }
     std::vector<char> img(off, 0);
     hipError_t e = hipMalloc((void**)&h->d_arena, off);
@@ -403,7 +572,9 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
     for (int j = 0; j < n_probs; ++j) {
         const dy_problem& pb = probs[j];
         const Layout& L = lay[j];
-        const int N = pb.n_nodes, R = pb.max_radix, K = pb.n_levels, B = pb.n_backends;
+        const bool obj = pb.objective != nullptr;
+        const int N = pb.n_nodes, R = pb.max_radix;
+        const int K = obj ? pb.objective->n_levels : pb.n_levels, B = obj ? 1 : pb.n_backends;
         ProbDev& D = descs[j];
         std::memset(&D, 0, sizeof D);
         HostProb& H = h->hp[j];
@@ -449,11 +620,12 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         H.plans_saturated = sat;
         // pressure: uniform when every used backend of a level has the same rho
         uint64_t used = 0;
-        for (int n = 0; n < N; ++n)
-            for (int i = 0; i < pb.radix[n]; ++i) used |= 1ull << pb.backend[(size_t)n * R + i];
+        if (!obj)
+            for (int n = 0; n < N; ++n)
+                for (int i = 0; i < pb.radix[n]; ++i) used |= 1ull << pb.backend[(size_t)n * R + i];
         bool uniform = true;
         std::vector<double> rho_k(K, 0.0);
-        for (int k = 0; k < K; ++k) {
+        for (int k = 0; k < K && !obj; ++k) {
             bool first = true;
             float r0 = 0.0f;
             for (int b = 0; b < B; ++b) {
@@ -469,12 +641,16 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
             rho_k[k] = (double)r0;
         }
         D.uniform = uniform ? 1 : 0;
-        D.slo = (double)pb.slo;
-        const double slo = (double)pb.slo;
+        D.slo = obj ? INFINITY : (double)pb.slo;
+        const double slo = D.slo;
         // certification bands (fp32 CP error <= (N-1) u relative, fp64 oracle error
         // ~ (N+3) 2^-53; the margin (N+1) u covers both, (N+2) u with rounded latencies)
         for (int k = 0; k < K; ++k) {
-            if (uniform) {
+            if (obj) {  // no hard constraint: every plan is feasible at every level
+                D.lo[k] = INFINITY;
+                D.hi[k] = INFINITY;
+                D.mk[k] = 1.0f;
+            } else if (uniform) {
                 const double th = slo * (1.0 - rho_k[k]);
                 D.lo[k] = round_down(th * (1.0 - (N + 1) * kU));
                 D.hi[k] = round_up(th * (1.0 + (N + 1) * kU));
@@ -492,6 +668,10 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         double* a64 = (double*)(img.data() + L.a64);
         double* lat64 = (double*)(img.data() + L.lat64);
         double* dem64 = (double*)(img.data() + L.dem64);
+        float2* atx = (float2*)(img.data() + L.atx);
+        if (obj) {
+            stage_objective(pb, D, at, atx, (float*)(img.data() + L.dz), dem, lat, a64, lat64, dem64);
+        } else {
         float dmin[DY_MAX_NODES], dmax[DY_MAX_NODES];
         for (int n = 0; n < N; ++n) {
             double w = (double)pb.w[n];
@@ -519,7 +699,6 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
                 }
             }
         }
-        float2* atx = (float2*)(img.data() + L.atx);
         *atx = make_float2(1.0f, 0.0f);
         // fp32 bounds of the unpressured CP (the recurrence is monotone in every duration)
         // tail bounds: exact products and sums in fp64, then widened by 2^-18
@@ -546,6 +725,7 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         const float chi = cp32(N, D.pred, D.sinks, dmax);
         D.cp_lo_bits = f2u(clo);
         D.cp_hi_bits = f2u(chi);
+        }
         int s = 2;
         while (s < 31 && ((D.cp_hi_bits >> s) - (D.cp_lo_bits >> s)) > 62u) ++s;
         D.bin_shift = s;
@@ -556,7 +736,7 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return D.lo[x] > D.lo[y]; });
         for (int k = 0; k < K; ++k) D.lvl_order[k] = order[k];
         const uint32_t blo = D.cp_lo_bits >> s;
-        for (int lane = 0; lane < NBINS; ++lane) {
+        for (int lane = 0; lane < NBINS && !obj; ++lane) {
             const uint64_t B = blo + (((uint32_t)lane - blo) & 63u);
             uint64_t top = ((B + 1) << s) - 1;
             if (top > 0x7f7fffffull) top = 0x7f7fffffull;
@@ -577,6 +757,8 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         D.a64 = (const double*)(base + L.a64);
         D.lat64 = (const double*)(base + L.lat64);
         D.dem64 = (const double*)(base + L.dem64);
+        D.demx = N >= 2 ? D.dem + (size_t)(N - 2) * R : (const float*)(base + L.dz);
+        D.demy = D.dem + (size_t)(N - 1) * R;
         H.n = N;
         H.k = K;
         H.b = B;
@@ -585,6 +767,7 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         H.rx = D.rx;
         H.ry = D.ry;
         H.uniform = uniform;
+        H.obj = obj;
         H.has_s2 = D.pre_sinks != 0 || !D.edge_xy;
     }
     e = hipMemcpy(h->d_arena, img.data(), off, hipMemcpyHostToDevice);
@@ -795,16 +978,25 @@ int dy_plan_get_stats(const dy_plan* h, dy_stats* out) {
 namespace {
 
 // The kernel family that scores a source.
-enum Group { G_SWEEP = 0, G_SWEEP_S2 = 1, G_GENERIC = 2, G_JIT = 3 };
+// Sources of one call are launched in groups: the prefix-shared sweep (RANGE,
+// uniform pressure; with or without a second sink term; corr / SLO or the
+// additive objective), the generic per-plan path, and the generated rows kernels.
+enum Group { G_SWEEP = 0, G_SWEEP_S2 = 1, G_OSWEEP = 2, G_OSWEEP_S2 = 3, G_GENERIC = 4, G_JIT = 5 };
+constexpr int kGroups = 6, kSweepGroups = 4;
 
 struct PassPlan {
-    int n[4] = {0, 0, 0, 0};              // sources per group, stored in group order
-    uint64_t units[3] = {0, 0, 0};        // largest main-pass work of the group
-    uint64_t samples[3] = {0, 0, 0};      // largest seeding-pass work of the group
-    int npre[2] = {0, 0};
-    int ry[2] = {0, 0};                   // R_y shared by every source of a sweep group, else -1
-    int npre_c[2] = {0, 0};               // prefix length shared by every source of a sweep group, else -1
+    int n[kGroups] = {};                  // sources per group, stored in group order
+    uint64_t units[G_JIT] = {};           // largest main-pass work of the group
+    uint64_t samples[G_JIT] = {};         // largest seeding-pass work of the group
+    int npre[kSweepGroups] = {};
+    int ry[kSweepGroups] = {};            // R_y shared by every source of a sweep group, else -1
+    int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
     int kmax = 1;                         // most levels of any source
+    int before(int g) const {             // jobs stored ahead of group g
+        int t = 0;
+        for (int q = 0; q < g; ++q) t += n[q];
+        return t;
+    }
 };
 
 // Rows sources of uniform-pressure problems run the problem's generated
@@ -846,19 +1038,20 @@ hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sampl
     return hipModuleLaunchKernel(fn, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
 }
 
-// Seeding pre-pass of groups 0-2 (jobs stored in group order at d).
+// Seeding pre-pass of the sweep and generic groups (jobs stored in group order at d).
 void launch_seed(const JobDev* d, const PassPlan& pp, hipStream_t s,
                  const std::function<void(hipError_t, const char*)>& chk) {
     auto chunks = [&](const JobDev* base, int n, auto&& fn) {
         for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
     };
-    const JobDev* gbase[3] = {d, d + pp.n[0], d + pp.n[0] + pp.n[1]};
-    for (int g = 0; g < 2; ++g)
-        chunks(gbase[g], pp.n[g], [&](const JobDev* b, int n) {
-            chk(launch_sample_sweep(b, n, g == 1, pp.samples[g], pp.npre[g], pp.npre_c[g], pp.kmax, s), "sample");
+    for (int g = 0; g < kSweepGroups; ++g)
+        chunks(d + pp.before(g), pp.n[g], [&](const JobDev* b, int n) {
+            chk(launch_sample_sweep(b, n, (g & 1) != 0, g >= G_OSWEEP, pp.samples[g], pp.npre[g], pp.npre_c[g],
+                                    pp.kmax, s),
+                "sample");
         });
-    chunks(gbase[2], pp.n[2],
-           [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, pp.samples[2], s), "sample"); });
+    chunks(d + pp.before(G_GENERIC), pp.n[G_GENERIC],
+           [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, pp.samples[G_GENERIC], s), "sample"); });
 }
 
 void launch_table_all(const JobDev* d, int ntot, hipStream_t s,
@@ -867,18 +1060,19 @@ void launch_table_all(const JobDev* d, int ntot, hipStream_t s,
         chk(launch_table(const_cast<JobDev*>(d + c), std::min(65535, ntot - c), s), "table");
 }
 
-// Scoring pass of groups 0-2.
+// Scoring pass of the sweep and generic groups.
 void launch_main(const JobDev* d, const PassPlan& pp, hipStream_t s,
                  const std::function<void(hipError_t, const char*)>& chk) {
     auto chunks = [&](const JobDev* base, int n, auto&& fn) {
         for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
     };
-    const JobDev* gbase[3] = {d, d + pp.n[0], d + pp.n[0] + pp.n[1]};
-    for (int g = 0; g < 2; ++g)
-        chunks(gbase[g], pp.n[g], [&](const JobDev* b, int n) {
-            chk(launch_sweep(b, n, g == 1, pp.units[g], pp.npre[g], pp.npre_c[g], pp.ry[g], s), "sweep");
+    for (int g = 0; g < kSweepGroups; ++g)
+        chunks(d + pp.before(g), pp.n[g], [&](const JobDev* b, int n) {
+            chk(launch_sweep(b, n, (g & 1) != 0, g >= G_OSWEEP, pp.units[g], pp.npre[g], pp.npre_c[g], pp.ry[g], s),
+                "sweep");
         });
-    chunks(gbase[2], pp.n[2], [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[2], s), "scan"); });
+    chunks(d + pp.before(G_GENERIC), pp.n[G_GENERIC],
+           [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[G_GENERIC], s), "scan"); });
 }
 
 void launch_certify_all(const JobDev* d, int ntot, int cert_waves, int kmax, hipStream_t s,
@@ -930,15 +1124,15 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         const int p = src[j].problem;
         const HostProb& H = h->hp[p];
         if (src[j].kind == DY_SOURCE_RANGE && H.uniform)
-            grp[j] = H.has_s2 ? G_SWEEP_S2 : G_SWEEP;
-        else if (src[j].kind == DY_SOURCE_ROWS && H.uniform && !h->force_fp64 && jit_ready(h, p))
+            grp[j] = H.obj ? (H.has_s2 ? G_OSWEEP_S2 : G_OSWEEP) : (H.has_s2 ? G_SWEEP_S2 : G_SWEEP);
+        else if (src[j].kind == DY_SOURCE_ROWS && H.uniform && !H.obj && !h->force_fp64 && jit_ready(h, p))
             grp[j] = G_JIT;
         else
             grp[j] = G_GENERIC;
     }
     std::vector<int> order;
     order.reserve(n_src);
-    for (int g = 0; g < 4; ++g)
+    for (int g = 0; g < kGroups; ++g)
         for (int j = 0; j < n_src; ++j)
             if (grp[j] == g) order.push_back(j);
     uint64_t plans = 0, all_units = 0;
@@ -972,14 +1166,14 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         J.sync = S.sync + q;
         J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
         // seeding work units: rows of the inner sweep, or plans
-        const bool sweep = g == G_SWEEP || g == G_SWEEP_S2;
+        const bool sweep = g < kSweepGroups;
         const uint64_t sunits = sweep ? J.nblk * (uint64_t)H.rx : J.count;
         uint64_t stride = h->sample_stride;
         if (!h->stride_fixed) stride = std::max<uint64_t>(1, std::min<uint64_t>(stride, sunits / kMinSamples));
         J.sample_stride = (uint32_t)stride;
         J.units = sweep ? J.nblk : J.count;
         ++pp.n[g];
-        if (g < 3) {
+        if (g < G_JIT) {
             pp.units[g] = std::max(pp.units[g], J.units);
             pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
         }
@@ -993,7 +1187,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         plans += J.count;
         jobs[q] = J;
     }
-    const int n3 = pp.n[0] + pp.n[1] + pp.n[2];  // jobs of groups 0-2; JIT jobs follow
+    const int n3 = pp.before(G_JIT);  // jobs of the other groups; JIT jobs follow
     // the job array is rebuilt every call but uploaded only when it changed
     const bool changed =
         S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0;
@@ -1024,13 +1218,13 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     // seeding and tables; the scoring pass (between timing events); certification and copy-out
     auto issue_pre = [&](hipStream_t st, const Check& ck) {
         launch_seed(S.d_jobs, pp, st, ck);
-        jit_pass(jobs.data(), n3, pp.n[3], true, st, ck);
+        jit_pass(jobs.data(), n3, pp.n[G_JIT], true, st, ck);
         launch_table_all(S.d_jobs, n_src, st, ck);
     };
     auto issue_mid = [&](hipStream_t st, const Check& ck) {
         if (h->timing) ck(hipEventRecord(h->ev[1], st), "hipEventRecord");
         launch_main(S.d_jobs, pp, st, ck);
-        jit_pass(jobs.data(), n3, pp.n[3], false, st, ck);
+        jit_pass(jobs.data(), n3, pp.n[G_JIT], false, st, ck);
         if (h->timing) ck(hipEventRecord(h->ev[2], st), "hipEventRecord");
     };
     auto issue_post = [&](hipStream_t st, const Check& ck) {
@@ -1106,7 +1300,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         PassPlan rp;
         std::vector<JobDev> re, ex;
         uint64_t fb_units = 0;
-        for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < kGroups; ++g)
             for (int q = 0; q < n_src; ++q) {
                 if (!(S.h_flags[q] & JF_OVERFLOW)) continue;
                 const int j = order[q];
@@ -1115,8 +1309,8 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
                 JobDev J = jobs[q];
                 if (round < kReseedRounds && H.uniform) {
                     ++rp.n[g];
-                    if (g < 3) rp.units[g] = std::max(rp.units[g], J.units);
-                    if (g < 2) rp.npre[g] = std::max(rp.npre[g], H.npre);
+                    if (g < G_JIT) rp.units[g] = std::max(rp.units[g], J.units);
+                    if (g < kSweepGroups) rp.npre[g] = std::max(rp.npre[g], H.npre);
                     re.push_back(J);
                 } else {
                     J.fb_levels = H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u);
@@ -1136,7 +1330,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
                 chk(launch_reseed(S.d_fb + c, std::min(65535, n_re - c), s), "reseed");
             launch_table_all(S.d_fb, n_re, s, chk);
             launch_main(S.d_fb, rp, s, chk);
-            jit_pass(re.data(), rp.n[0] + rp.n[1] + rp.n[2], rp.n[3], false, s, chk);
+            jit_pass(re.data(), rp.before(G_JIT), rp.n[G_JIT], false, s, chk);
             launch_certify_all(S.d_fb, n_re, cert_waves, h->kmax, s, chk);
         }
         if (n_ex > 0) {

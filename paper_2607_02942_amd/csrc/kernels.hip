@@ -11,6 +11,16 @@
 // Selection per level k: max corr s.t. CP_k <= SLO, ties to the lowest index
 // (one selection per level, Algorithm gen).
 //
+// Objective mode (the paper's additive objective, Sec. 4.3 eq.
+// admission-objective with the level weight of Sec. 4.4 eq. variant-objective):
+//   J_k = U - lambda_l T - lambda_ld L_k D,  U = sum of LLM utilities u,
+//   T = nominal longest path, D = sum of LLM durations;
+// max J_k per level, ties to the lowest index.  The same pipeline runs with
+// additive per-node terms: a plan is scored by G = U - lambda_l T and D in
+// fp32, and the prefilter bins index D (a level's test J_k >= T_k reads
+// G >= T_k + m_k D with m_k = lambda_ld L_k >= 0, so a bin's threshold is the
+// smallest T_k + m_k D_low over the levels).
+//
 // Pipeline of one selection call (all on the caller's stream):
 //   k_init        zero the per-source scratch
 //   k_sample_*    seeding pre-pass: 1 in S work units, per level the best fp32
@@ -80,6 +90,66 @@ __device__ __forceinline__ float cand_threshold(float s, int n) {
     return __double2float_rd(t);
 }
 
+// ---- objective mode: keys and thresholds ----------------------------------------
+
+// Order-preserving unsigned key of a float (a greater number has a greater
+// key; no number maps to 0, which marks "none").
+__device__ __forceinline__ uint32_t fkey(float x) {
+    const uint32_t b = __float_as_uint(x);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ float fkey_value(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+__device__ __forceinline__ uint64_t dkey(double x) {
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+
+// An fp32 value <= a - b (exact real difference): the fp64 difference, lowered
+// by more than its rounding error, rounded down.
+__device__ __forceinline__ float sub_rd(double a, double b) {
+    double x = a - b;
+    x = x - (fabs(a) + fabs(b)) * 0x1p-50;
+    return __double2float_rd(x);
+}
+
+// Candidate threshold of level k from the best estimate s of any plan's J_k:
+// every estimate is within err2/2 of the plan's fp64 J_k, so the winner's
+// estimate is >= s - err2.
+__device__ __forceinline__ float obj_threshold(float s, double err2) {
+    return sub_rd((double)s, err2);
+}
+
+// Prefilter bin threshold: an fp32 value <= thr + m D_low (exact), m >= 0.
+__device__ __forceinline__ float obj_bin_threshold(float thr, double m, float dlow) {
+    if (thr == -INFINITY) return -INFINITY;
+    const double md = m * (double)dlow;
+    double x = (double)thr + md;
+    x = x - (fabs((double)thr) + md) * 0x1p-50;
+    return __double2float_rd(x);
+}
+
+// exact test of the scoring passes: some level's J_k estimate G - m_k D (one
+// rounding) reaches its threshold
+__device__ __forceinline__ bool is_candidate_obj(PD P, JD J, float G, float D) {
+    for (int k = 0; k < P->k; ++k)
+        if (fma(-P->m64[k], (double)D, (double)G) >= (double)J->thr[k]) return true;
+    return false;
+}
+
+// J_k = U - lambda_l T - m_k D in fp64, operation by operation as the definition
+// writes it (no contraction into fused multiply-adds).
+__device__ __forceinline__ double obj_j(double lam_l, double m, double U, double T, double D) {
+#pragma clang fp contract(off)
+    double j = lam_l * T;
+    j = U - j;
+    const double q = m * D;
+    return j - q;
+}
+
 // ---- fp64 re-evaluation ------------------------------------------------------
 // The per-node terms (1 - w(1-p), tau/(1-rho), tau*size) are precomputed on the
 // host in fp64 with the same operations as the definition, so the products,
@@ -110,6 +180,35 @@ __device__ double ex_cp(PD P, const uint8_t* ids, int is, int k, double* f, int 
         if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
     }
     return cp;
+}
+
+// Objective mode: U (returned), T and D in fp64, node order (the definition's).
+__device__ double ex_obj(PD P, const uint8_t* ids, int is, double* f, int fs, double& T, double& D) {
+    const CS double* u64 = cs(P->a64);
+    const CS double* d64 = cs(P->dem64);
+    const CS double* t64 = cs(P->lat64);
+    double U = 0.0, d = 0.0, t = 0.0;
+    for (int n = 0; n < P->n; ++n) {
+        const int e = n * P->rmax + ids[n * is];
+        if (P->llm >> n & 1u) {
+            U = U + u64[e];
+            d = d + d64[e];
+        }
+        double m = 0.0;
+        uint32_t pm = P->pred[n];
+        while (pm) {
+            const int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            const double fu = f[u * fs];
+            if (fu > m) m = fu;
+        }
+        const double fn = t64[e] + m;
+        f[n * fs] = fn;
+        if ((P->sinks >> n & 1u) && fn > t) t = fn;
+    }
+    T = t;
+    D = d;
+    return U;
 }
 
 __device__ double ex_demand(PD P, const uint8_t* ids, int is) {
@@ -233,10 +332,12 @@ __device__ bool last_block(uint32_t* counter, uint32_t expected) {
 __device__ void build_table(JD J, PD P) {
     __shared__ float s_thr[KMAX];
     const int lane = threadIdx.x;
+    const bool obj = P->obj != 0;
     if (lane < P->k) {
         uint32_t e = 0;
         for (int q = 0; q < NSLOT; ++q) e = max(e, J->scert[lane * NSLOT + q]);
-        const float t = e ? cand_threshold(__uint_as_float(e - 1u), P->n) : -INFINITY;
+        float t = -INFINITY;
+        if (e) t = obj ? obj_threshold(fkey_value(e), P->err2[lane]) : cand_threshold(__uint_as_float(e - 1u), P->n);
         s_thr[lane] = t;
         J->thr[lane] = t;
     }
@@ -252,8 +353,12 @@ __device__ void build_table(JD J, PD P) {
         if (lowbits < P->cp_lo_bits) lowbits = P->cp_lo_bits;
         const float low = __uint_as_float(lowbits);
         float g = INFINITY;
-        for (int k = 0; k < P->k; ++k)
-            if (P->hi[k] >= low) g = fminf(g, s_thr[k]);
+        if (obj) {  // bins of D: a level's bound T_k + m_k D is smallest at the bin's low end
+            for (int k = 0; k < P->k; ++k) g = fminf(g, obj_bin_threshold(s_thr[k], P->m64[k], low));
+        } else {
+            for (int k = 0; k < P->k; ++k)
+                if (P->hi[k] >= low) g = fminf(g, s_thr[k]);
+        }
         J->table[lane] = __float_as_uint(g);
     }
     if (lane == 0) {
@@ -271,19 +376,27 @@ __device__ void build_table(JD J, PD P) {
 // a multiply (corr), an add (CP) and a prefilter compare.
 // ---------------------------------------------------------------------------
 
+// pc: product of the prefix factors (objective mode: sum of the prefix
+// utilities); px, py: longest prefix path into x and into y; s: longest prefix
+// path ending at a prefix sink; pd: objective mode, sum of the prefix d terms.
 struct Prefix {
-    float pc, px, py, s;
+    float pc, px, py, s, pd;
 };
 
-// The (a, tau) rows of the prefix nodes, staged in LDS by the workgroup when
-// they fit (a random LDS read instead of a global load in the decode chain).
-constexpr int PAT_MAX = 1024;  // float2 entries
+// The (a, tau) rows of the prefix nodes (objective mode: (u, tau) and d),
+// staged in LDS by the workgroup when they fit (a random LDS read instead of
+// a global load in the decode chain).
+constexpr int PAT_MAX = 1024;  // entries
 
-__device__ __forceinline__ const float2* stage_prefix_rows(PD P, float2* s_pat) {
+template <bool OBJ>
+__device__ __forceinline__ const float2* stage_prefix_rows(PD P, float2* s_pat, float* s_pd) {
     const int n = P->npre * P->rmax;
     const bool fit = n <= PAT_MAX;
     if (fit)
-        for (int i = threadIdx.x; i < n; i += WG) s_pat[i] = cs(P->at)[i];
+        for (int i = threadIdx.x; i < n; i += WG) {
+            s_pat[i] = cs(P->at)[i];
+            if (OBJ) s_pd[i] = cs(P->dem)[i];
+        }
     __syncthreads();
     return fit ? s_pat : nullptr;
 }
@@ -301,18 +414,23 @@ __device__ __forceinline__ uint32_t prefix_digit(PD P, int n, uint64_t b, int bi
 // (checked by the host); the loops unroll, every descriptor load is issued up
 // front and the f_n live in registers (predecessor bits are wave-uniform, so
 // each test is a scalar branch).  NPRE == 0: any length, f_n in an LDS column.
-template <int NPRE>
-__device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big,
-                                              float* __restrict__ s_f, const float2* s_pat) {
+template <int NPRE, bool OBJ>
+__device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big, float* __restrict__ s_f,
+                                              const float2* s_pat, const float* s_pd) {
     if constexpr (NPRE > 0) {
         const int rmax = P->rmax;
         float f[NPRE];
-        float pc = 1.0f;
+        float pc = OBJ ? 0.0f : 1.0f, pd = 0.0f;
 #pragma unroll
         for (int n = 0; n < NPRE; ++n) {
             const uint32_t d = prefix_digit(P, n, b, big);
             const float2 v = s_pat ? s_pat[n * rmax + d] : cs(P->at)[n * rmax + d];
-            pc = pc * v.x;
+            if (OBJ) {
+                pc = pc + v.x;
+                pd = pd + (s_pat ? s_pd[n * rmax + d] : cs(P->dem)[n * rmax + d]);
+            } else {
+                pc = pc * v.x;
+            }
             float m = 0.0f;
             const uint32_t pm = P->pred[n];
 #pragma unroll
@@ -331,15 +449,20 @@ __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big,
             if (pmy >> u & 1u) py = fmaxf(py, f[u]);
             if (pms >> u & 1u) s = fmaxf(s, f[u]);
         }
-        return Prefix{pc, px, py, s};
+        return Prefix{pc, px, py, s, pd};
     }
     const int tid = threadIdx.x;
     const int npre = P->npre;
-    float pc = 1.0f;
+    float pc = OBJ ? 0.0f : 1.0f, pd = 0.0f;
     for (int n = 0; n < npre; ++n) {
         const uint32_t d = prefix_digit(P, n, b, big);
         const float2 v = s_pat ? s_pat[n * P->rmax + d] : cs(P->at)[n * P->rmax + d];
-        pc = pc * v.x;
+        if (OBJ) {
+            pc = pc + v.x;
+            pd = pd + (s_pat ? s_pd[n * P->rmax + d] : cs(P->dem)[n * P->rmax + d]);
+        } else {
+            pc = pc * v.x;
+        }
         float m = 0.0f;
         uint32_t pm = P->pred[n];
         while (pm) {
@@ -375,7 +498,7 @@ __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big,
             s = fmaxf(s, s_f[u * WG + tid]);
         }
     }
-    return Prefix{pc, px, py, s};
+    return Prefix{pc, px, py, s, pd};
 }
 
 // One plan of the inner sweep: corr = cx * a_y, CP = max(tau_y + M, S2); the
@@ -409,8 +532,8 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
     const uint64_t b = J->blk_first + (live ? t : nblk - 1);
     __shared__ float s_bins[NBINS];
     if (threadIdx.x < NBINS) s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
-    const float2* pat = stage_prefix_rows(P, (float2*)(s_f + (size_t)max(P->npre, 1) * WG));
-    const Prefix pf = prefix_eval<NPRE>(P, b, J->big, s_f, pat);
+    const float2* pat = stage_prefix_rows<false>(P, (float2*)(s_f + (size_t)max(P->npre, 1) * WG), nullptr);
+    const Prefix pf = prefix_eval<NPRE, false>(P, b, J->big, s_f, pat, nullptr);
 
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* atx = cs(P->atx);
@@ -510,8 +633,8 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
         b = J->blk_first + u / (uint64_t)rx;
         ix = (int)(u % (uint64_t)rx);
     }
-    const float2* pat = stage_prefix_rows(P, s_pat);
-    const Prefix pf = prefix_eval<NPRE>(P, b, J->big, s_f, pat);
+    const float2* pat = stage_prefix_rows<false>(P, s_pat, nullptr);
+    const Prefix pf = prefix_eval<NPRE, false>(P, b, J->big, s_f, pat, nullptr);
     for (int j = 0; j < K; ++j) s_b[j * WG + tid] = -1.0f;
     const float2 vx = cs(P->atx)[ix];
     const float fx = vx.y + pf.px;
@@ -547,6 +670,178 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
         uint32_t e = 0;
         for (int w = 0; w < WG / 64; ++w) e = max(e, s_red[tid][w]);
         if (e) atomicMax(J->scert + P->lvl_order[tid] * NSLOT + (blockIdx.x % NSLOT), e);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// RANGE sources, objective mode: the same prefix-shared sweep with additive
+// terms.  Per plan: T = max(tau_y + M, S2), G = U_x + u_y - lambda_l T (one
+// fused rounding), D = D_x + d_y; the bin of D gives the prefilter threshold.
+// U and D are summed in node order (prefix, x, y) in fp32.
+// ---------------------------------------------------------------------------
+
+struct ObjPlan {
+    float G, D;
+};
+
+template <bool HAS_S2>
+__device__ __forceinline__ ObjPlan obj_plan(const float2 vy, float dy, float M, float S2, float ux, float dx,
+                                            float nl) {
+    float T = vy.y + M;
+    if (HAS_S2) T = fmaxf(T, S2);
+    return ObjPlan{fmaf(nl, T, ux + vy.x), dx + dy};
+}
+
+template <bool HAS_S2>
+__device__ __forceinline__ uint64_t sweep_test_obj(const float2 vy, float dy, float M, float S2, float ux, float dx,
+                                                   float nl, uint32_t sh, const float* s_bins) {
+    const ObjPlan q = obj_plan<HAS_S2>(vy, dy, M, S2, ux, dx, nl);
+    const uint32_t off = (__float_as_uint(q.D) >> sh) & 0xfcu;
+    const float thr = *(const float*)((const char*)s_bins + off);
+    return __ballot(q.G >= thr);
+}
+
+template <bool HAS_S2, int RY, int NPRE>
+__global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ jobs, uint64_t unit_off) {
+    extern __shared__ float s_f[];
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    const uint64_t nblk = J->nblk;
+    const uint64_t t0 = unit_off + (uint64_t)blockIdx.x * WG;
+    if (t0 >= nblk) return;
+    const uint64_t t = t0 + threadIdx.x;
+    const bool live = t < nblk;
+    const uint64_t b = J->blk_first + (live ? t : nblk - 1);
+    __shared__ float s_bins[NBINS];
+    if (threadIdx.x < NBINS) s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
+    float2* s_pat = (float2*)(s_f + (size_t)max(P->npre, 1) * WG);
+    float* s_pd = (float*)(s_pat + PAT_MAX);
+    const float2* pat = stage_prefix_rows<true>(P, s_pat, s_pd);
+    const Prefix pf = prefix_eval<NPRE, true>(P, b, J->big, s_f, pat, s_pd);
+
+    const uint32_t sh = (uint32_t)P->bin_shift - 2u;
+    const CS float2* atx = cs(P->atx);
+    const CS float2* aty = cs(P->aty);
+    const CS float* dxt = cs(P->demx);
+    const CS float* dyt = cs(P->demy);
+    const int rx = P->rx, ry = P->ry;
+    const bool exy = P->edge_xy != 0;
+    const float nl = -P->lam_l;
+
+    float2 vyr[RY > 0 ? RY : 1];
+    float dyr[RY > 0 ? RY : 1];
+    if (RY > 0) {
+#pragma unroll
+        for (int iy = 0; iy < RY; ++iy) {
+            vyr[iy] = aty[iy];
+            dyr[iy] = dyt[iy];
+        }
+    }
+    for (int ix = 0; ix < rx; ++ix) {
+        const float2 vx = atx[ix];
+        const float fx = vx.y + pf.px;
+        const float ux = pf.pc + vx.x;
+        const float dx = pf.pd + dxt[ix];
+        const float M = exy ? fmaxf(pf.py, fx) : pf.py;
+        const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
+        uint64_t hit = 0;
+        int iy = 0;
+        if (RY > 0) {
+#pragma unroll
+            for (int j = 0; j < (RY > 0 ? RY : 1); ++j)
+                hit |= sweep_test_obj<HAS_S2>(vyr[j], dyr[j], M, S2, ux, dx, nl, sh, s_bins);
+            iy = ry;
+        }
+        for (; iy + 4 <= ry; iy += 4) {
+            const float2 v0 = aty[iy], v1 = aty[iy + 1], v2 = aty[iy + 2], v3 = aty[iy + 3];
+            const float d0 = dyt[iy], d1 = dyt[iy + 1], d2 = dyt[iy + 2], d3 = dyt[iy + 3];
+            hit |= sweep_test_obj<HAS_S2>(v0, d0, M, S2, ux, dx, nl, sh, s_bins);
+            hit |= sweep_test_obj<HAS_S2>(v1, d1, M, S2, ux, dx, nl, sh, s_bins);
+            hit |= sweep_test_obj<HAS_S2>(v2, d2, M, S2, ux, dx, nl, sh, s_bins);
+            hit |= sweep_test_obj<HAS_S2>(v3, d3, M, S2, ux, dx, nl, sh, s_bins);
+        }
+        for (; iy < ry; ++iy) hit |= sweep_test_obj<HAS_S2>(aty[iy], dyt[iy], M, S2, ux, dx, nl, sh, s_bins);
+        if (hit) {
+            // rare: re-score this lane's row with the exact per-level test
+            const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
+            if (live && (hit >> (threadIdx.x & 63) & 1ull)) {
+                for (int iy = 0; iy < ry; ++iy) {
+                    const ObjPlan q = obj_plan<HAS_S2>(aty[iy], dyt[iy], M, S2, ux, dx, nl);
+                    const uint64_t idx = base + (uint64_t)iy;
+                    if (idx - J->begin < J->count && is_candidate_obj(P, J, q.G, q.D)) append_cand(J, idx, q.G, q.D);
+                }
+            }
+        }
+    }
+}
+
+// Seeding pre-pass of the objective sweep: one hashed row per window of S
+// rows; per level the greatest fp32 estimate fma(-m_k, D, G) of a sampled plan
+// (every plan is admissible), reduced through DPP, LDS and an atomic max on
+// its ordered key.
+template <bool HAS_S2, int NPRE>
+__global__ void __launch_bounds__(WG) k_sample_sweep_obj(const JobDev* __restrict__ jobs) {
+    extern __shared__ float s_dyn[];
+    __shared__ uint32_t s_red[KMAX][WG / 64];
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    const int K = P->k;
+    float* s_f = s_dyn;                                  // prefix recurrence, [npre][WG]
+    float* s_b = s_dyn + (size_t)max(P->npre, 1) * WG;   // best estimate per level, [K][WG]
+    float2* s_pat = (float2*)(s_b + (size_t)K * WG);     // prefix rows, PAT_MAX entries
+    float* s_pd = (float*)(s_pat + PAT_MAX);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint64_t S = J->sample_stride;
+    const int rx = P->rx, ry = P->ry;
+    const uint64_t units = J->nblk * (uint64_t)rx;
+    const uint64_t nsamp = (units + S - 1) / S;
+    const uint64_t t0 = (uint64_t)blockIdx.x * WG;
+    if (t0 >= nsamp) return;
+    const uint64_t t = t0 + tid;
+    const bool live = t < nsamp;
+    const uint64_t u = sample_unit(live ? t : nsamp - 1, S, units);
+    uint64_t b;
+    int ix;
+    if (units <= 0xffffffffull && P->xnode >= 0) {
+        const uint32_t q = mdiv((uint32_t)u, P->rmag[P->xnode]);
+        b = J->blk_first + q;
+        ix = (int)((uint32_t)u - q * (uint32_t)rx);
+    } else {
+        b = J->blk_first + u / (uint64_t)rx;
+        ix = (int)(u % (uint64_t)rx);
+    }
+    const float2* pat = stage_prefix_rows<true>(P, s_pat, s_pd);
+    const Prefix pf = prefix_eval<NPRE, true>(P, b, J->big, s_f, pat, s_pd);
+    for (int k = 0; k < K; ++k) s_b[k * WG + tid] = -INFINITY;
+    const float2 vx = cs(P->atx)[ix];
+    const float fx = vx.y + pf.px;
+    const float ux = pf.pc + vx.x;
+    const float dx = pf.pd + cs(P->demx)[ix];
+    const bool exy = P->edge_xy != 0;
+    const float M = exy ? fmaxf(pf.py, fx) : pf.py;
+    const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
+    const float nl = -P->lam_l;
+    const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
+    const CS float2* aty = cs(P->aty);
+    const CS float* dyt = cs(P->demy);
+    for (int iy = 0; iy < ry; ++iy) {
+        const ObjPlan q = obj_plan<HAS_S2>(aty[iy], dyt[iy], M, S2, ux, dx, nl);
+        if (live && (base + (uint64_t)iy - J->begin < J->count))
+            for (int k = 0; k < K; ++k) {
+                float* r = s_b + k * WG + tid;
+                *r = fmaxf(*r, fmaf(-P->m32[k], q.D, q.G));
+            }
+    }
+    for (int k = 0; k < K; ++k) {
+        const float v = s_b[k * WG + tid];
+        const uint32_t e = wave_max_u32(v > -INFINITY ? fkey(v) : 0u);
+        if (lane == 0) s_red[k][wave] = e;
+    }
+    __syncthreads();
+    if (tid < K) {
+        uint32_t e = 0;
+        for (int w = 0; w < WG / 64; ++w) e = max(e, s_red[tid][w]);
+        if (e) atomicMax(J->scert + tid * NSLOT + (blockIdx.x % NSLOT), e);
     }
 }
 
@@ -644,6 +939,33 @@ __device__ __forceinline__ void eval_uniform(PD P, const uint8_t* __restrict__ s
     cp = best;
 }
 
+// Objective mode: fp32 U, nominal T and D of the plan in the LDS column, node
+// order (tool nodes hold u = d = 0 in the tables).
+__device__ __forceinline__ void eval_obj(PD P, const uint8_t* __restrict__ s_id, float* __restrict__ s_f, float& U,
+                                         float& T, float& D) {
+    const int tid = threadIdx.x;
+    float u = 0.0f, d = 0.0f, best = 0.0f;
+    for (int n = 0; n < P->n; ++n) {
+        const int e = n * P->rmax + s_id[n * WG + tid];
+        const float2 v = P->at[e];
+        u = u + v.x;
+        d = d + P->dem[e];
+        float m = 0.0f;
+        uint32_t pm = P->pred[n];
+        while (pm) {
+            int q = __builtin_ctz(pm);
+            pm &= pm - 1;
+            m = fmaxf(m, s_f[q * WG + tid]);
+        }
+        const float f = v.y + m;
+        s_f[n * WG + tid] = f;
+        if (P->sinks >> n & 1u) best = fmaxf(best, f);
+    }
+    U = u;
+    T = best;
+    D = d;
+}
+
 __device__ __forceinline__ float eval_corr(PD P, const uint8_t* __restrict__ s_id) {
     float c = 1.0f;
     for (int n = 0; n < P->n; ++n) c = c * P->at[n * P->rmax + s_id[n * WG + threadIdx.x]].x;
@@ -691,6 +1013,20 @@ __global__ void __launch_bounds__(WG) k_sample_generic(const JobDev* __restrict_
     bool bad = false;
     load_plan(J, P, sample_unit(live ? t : nsamp - 1, S, J->count), s_id, &bad);
     const int K = P->k;
+    if (P->obj) {
+        float U, T, D;
+        eval_obj(P, s_id, s_f, U, T, D);
+        const float G = fmaf(-P->lam_l, T, U);
+        const bool ok = live && !bad;
+#pragma unroll 1
+        for (int k = 0; k < K; ++k) {
+            uint32_t e = ok ? fkey(fmaf(-P->m32[k], D, G)) : 0u;
+            e = wave_max_u32(e);
+            if ((threadIdx.x & 63) == 0 && e)
+                atomicMax(J->scert + k * NSLOT + ((blockIdx.x * (WG / 64) + (threadIdx.x >> 6)) % NSLOT), e);
+        }
+        return;
+    }
     float cc, cp0 = 0.0f;
     if (P->uniform) {
         eval_uniform(P, s_id, s_f, cc, cp0);
@@ -723,7 +1059,13 @@ __global__ void __launch_bounds__(WG) k_scan(const JobDev* __restrict__ jobs, ui
     bool bad = false;
     const uint64_t idx = load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
     if (live && bad) atomicOr(J->flags, (int32_t)JF_BAD_ROW);
-    if (P->uniform) {
+    if (P->obj) {
+        float U, T, D;
+        eval_obj(P, s_id, s_f, U, T, D);
+        const float G = fmaf(-P->lam_l, T, U);
+        const float thr = __uint_as_float(J->table[(__float_as_uint(D) >> (uint32_t)P->bin_shift) & 63u]);
+        if (live && !bad && G >= thr && is_candidate_obj(P, J, G, D)) append_cand(J, idx, G, D);
+    } else if (P->uniform) {
         float cc, cp;
         eval_uniform(P, s_id, s_f, cc, cp);
         const float thr = __uint_as_float(J->table[(__float_as_uint(cp) >> (uint32_t)P->bin_shift) & 63u]);
@@ -797,7 +1139,7 @@ __device__ void merge_cert(JD J, PD P) {
     const int lane = threadIdx.x, w = lane % CERT_WAVES, kk = lane / CERT_WAVES;
     for (int k0 = 0; k0 < K; k0 += LPG) {
         const int k = k0 + kk;
-        double bc = -1.0, bcp = 0.0, bd = 0.0;
+        double bc = -INFINITY, bcp = 0.0, bd = 0.0;
         uint64_t bi = ~0ull;
         if (k < K && w < J->cert_waves) {
             bc = J->cert_c[k * CERT_WAVES + w];
@@ -882,7 +1224,7 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
     const size_t NR = (size_t)N * R;
     const double* a64 = P->a64;
     const double* d64 = P->dem64;
-    const double* lat = P->lat64 + (size_t)k * NR;
+    const double* lat = P->lat64 + (P->obj ? (size_t)0 : (size_t)k * NR);
     if (3 * NR * sizeof(double) <= (size_t)CERT_LDS_TABLES) {
         // unrolled so that many loads are in flight before the first LDS store
 #pragma unroll 8
@@ -901,46 +1243,95 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
 #pragma unroll 8
     for (uint32_t i = lane; i < ncache; i += 64) s_cand[i] = J->cand[i];
     __syncthreads();
-    const float lo = P->lo[k], hi = P->hi[k];
-    float sb = sl ? __uint_as_float(sl - 1u) : -1.0f;
-    if (!general)
+    const uint32_t step = 64u * (uint32_t)J->cert_waves;
+    double bc = -INFINITY, bcp = 0.0, bd = 0.0;
+    uint64_t bi = ~0ull;
+    if (P->obj) {
+        // Pass A: the best estimate of J_k among the seed and the candidates
+        // (fma(-m, D, G), one rounding); Pass B: every candidate whose estimate
+        // reaches that minus 2 E_k, re-evaluated exactly.
+        const double m = P->m64[k], e2 = P->err2[k];
+        double sb = sl ? (double)fkey_value(sl) : -INFINITY;
         for (uint32_t i = lane; i < nc; i += 64) {
             const Cand c = i < ncache ? s_cand[i] : J->cand[i];
-            if (c.cp <= lo) sb = fmaxf(sb, c.corr);
+            sb = fmax(sb, fma(-m, (double)c.cp, (double)c.corr));
         }
-    const uint32_t e = wave_max_u32(sb >= 0.0f ? __float_as_uint(sb) + 1u : 0u);
-    const float T = cand_threshold(e ? __uint_as_float(e - 1u) : -1.0f, N);
-    const uint32_t step = 64u * (uint32_t)J->cert_waves;
-    double bc = -1.0, bcp = 0.0, bd = 0.0;
-    uint64_t bi = ~0ull;
-    for (uint32_t i = (uint32_t)g * 64u + lane; i < nc; i += step) {
-        const Cand c = i < ncache ? s_cand[i] : J->cand[i];
-        if (!(c.corr >= T && (general || c.cp <= hi))) continue;
-        if (!job_ids(J, P, c.index, ids, 64)) continue;
-        double corr = 1.0;
-        for (int n = 0; n < N; ++n) corr = corr * a64[n * R + ids[n * 64]];
-        if (!better(corr, c.index, bc, bi)) continue;
-        double cp = 0.0;
-        for (int n = 0; n < N; ++n) {
-            double m = 0.0;
-            uint32_t pm = P->pred[n];
-            while (pm) {
-                const int u = __builtin_ctz(pm);
-                pm &= pm - 1;
-                const double fu = f[u * 64];
-                if (fu > m) m = fu;
+        for (int o = 32; o > 0; o >>= 1) sb = fmax(sb, __shfl_xor(sb, o));
+        double T = -INFINITY;
+        if (sb > -INFINITY) {
+            T = sb - e2;
+            T = T - (fabs(sb) + e2) * 0x1p-50;
+        }
+        for (uint32_t i = (uint32_t)g * 64u + lane; i < nc; i += step) {
+            const Cand c = i < ncache ? s_cand[i] : J->cand[i];
+            if (!(fma(-m, (double)c.cp, (double)c.corr) >= T)) continue;
+            if (!job_ids(J, P, c.index, ids, 64)) continue;
+            double U = 0.0, D = 0.0, t = 0.0;
+            for (int n = 0; n < N; ++n) {
+                const int e = n * R + ids[n * 64];
+                if (P->llm >> n & 1u) {
+                    U = U + a64[e];
+                    D = D + d64[e];
+                }
+                double mx = 0.0;
+                uint32_t pm = P->pred[n];
+                while (pm) {
+                    const int u = __builtin_ctz(pm);
+                    pm &= pm - 1;
+                    const double fu = f[u * 64];
+                    if (fu > mx) mx = fu;
+                }
+                const double fn = lat[e] + mx;
+                f[n * 64] = fn;
+                if ((P->sinks >> n & 1u) && fn > t) t = fn;
             }
-            const double fn = lat[n * R + ids[n * 64]] + m;
-            f[n * 64] = fn;
-            if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
+            const double j = obj_j(P->lam_l64, m, U, t, D);
+            if (better(j, c.index, bc, bi)) {
+                bc = j;
+                bi = c.index;
+                bcp = t;
+                bd = D;
+            }
         }
-        if (!(cp <= P->slo)) continue;
-        double d = 0.0;
-        for (int n = 0; n < N; ++n) d = d + d64[n * R + ids[n * 64]];
-        bc = corr;
-        bi = c.index;
-        bcp = cp;
-        bd = d;
+    } else {
+        const float lo = P->lo[k], hi = P->hi[k];
+        float sb = sl ? __uint_as_float(sl - 1u) : -1.0f;
+        if (!general)
+            for (uint32_t i = lane; i < nc; i += 64) {
+                const Cand c = i < ncache ? s_cand[i] : J->cand[i];
+                if (c.cp <= lo) sb = fmaxf(sb, c.corr);
+            }
+        const uint32_t e = wave_max_u32(sb >= 0.0f ? __float_as_uint(sb) + 1u : 0u);
+        const float T = cand_threshold(e ? __uint_as_float(e - 1u) : -1.0f, N);
+        for (uint32_t i = (uint32_t)g * 64u + lane; i < nc; i += step) {
+            const Cand c = i < ncache ? s_cand[i] : J->cand[i];
+            if (!(c.corr >= T && (general || c.cp <= hi))) continue;
+            if (!job_ids(J, P, c.index, ids, 64)) continue;
+            double corr = 1.0;
+            for (int n = 0; n < N; ++n) corr = corr * a64[n * R + ids[n * 64]];
+            if (!better(corr, c.index, bc, bi)) continue;
+            double cp = 0.0;
+            for (int n = 0; n < N; ++n) {
+                double m = 0.0;
+                uint32_t pm = P->pred[n];
+                while (pm) {
+                    const int u = __builtin_ctz(pm);
+                    pm &= pm - 1;
+                    const double fu = f[u * 64];
+                    if (fu > m) m = fu;
+                }
+                const double fn = lat[n * R + ids[n * 64]] + m;
+                f[n * 64] = fn;
+                if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
+            }
+            if (!(cp <= P->slo)) continue;
+            double d = 0.0;
+            for (int n = 0; n < N; ++n) d = d + d64[n * R + ids[n * 64]];
+            bc = corr;
+            bi = c.index;
+            bcp = cp;
+            bd = d;
+        }
     }
     wave_best4(bc, bi, bcp, bd);
     if (lane == 0) {
@@ -962,12 +1353,22 @@ __global__ void __launch_bounds__(64) k_reseed(const JobDev* __restrict__ jobs) 
     const int lane = threadIdx.x;
     const uint32_t nc = min(*J->ncand, J->cap);
     for (int k = 0; k < P->k; ++k) {
-        float sb = -1.0f;
-        for (uint32_t i = lane; i < nc; i += 64) {
-            const Cand c = J->cand[i];
-            if (c.cp <= P->lo[k]) sb = fmaxf(sb, c.corr);
+        uint32_t e;
+        if (P->obj) {  // every candidate is admissible: its fp32 estimate of J_k
+            float sb = -INFINITY;
+            for (uint32_t i = lane; i < nc; i += 64) {
+                const Cand c = J->cand[i];
+                sb = fmaxf(sb, fmaf(-P->m32[k], c.cp, c.corr));
+            }
+            e = wave_max_u32(sb > -INFINITY ? fkey(sb) : 0u);
+        } else {
+            float sb = -1.0f;
+            for (uint32_t i = lane; i < nc; i += 64) {
+                const Cand c = J->cand[i];
+                if (c.cp <= P->lo[k]) sb = fmaxf(sb, c.corr);
+            }
+            e = wave_max_u32(sb >= 0.0f ? __float_as_uint(sb) + 1u : 0u);
         }
-        const uint32_t e = wave_max_u32(sb >= 0.0f ? __float_as_uint(sb) + 1u : 0u);
         if (lane == 0 && e) atomicMax(J->scert + k * NSLOT, e);
     }
     __syncthreads();
@@ -997,12 +1398,19 @@ __global__ void __launch_bounds__(WG) k_exhaust(const JobDev* __restrict__ jobs,
         for (uint64_t j = (uint64_t)blockIdx.x * WG + threadIdx.x; j < units; j += stride) {
             const uint64_t idx = J->kind == DY_SOURCE_RANGE ? J->begin + j : J->index_base + j;
             if (!job_ids(J, P, idx, ids, 1)) continue;
-            const double cp = ex_cp(P, ids, 1, k, f, 1);
-            if (!(cp <= P->slo)) continue;
-            const uint64_t cb = (uint64_t)__double_as_longlong(ex_corr(P, ids, 1));
+            uint64_t key;  // ordered, 0 means none
+            if (P->obj) {
+                double T, D;
+                const double U = ex_obj(P, ids, 1, f, 1, T, D);
+                key = dkey(obj_j(P->lam_l64, P->m64[k], U, T, D));
+            } else {
+                const double cp = ex_cp(P, ids, 1, k, f, 1);
+                if (!(cp <= P->slo)) continue;
+                key = (uint64_t)__double_as_longlong(ex_corr(P, ids, 1)) + 1ull;
+            }
             if (!pass) {
-                acc = cb + 1ull > acc ? cb + 1ull : acc;  // +1: 0 means none
-            } else if (cb + 1ull == target && idx < acc) {
+                acc = key > acc ? key : acc;
+            } else if (key == target && idx < acc) {
                 acc = idx;
             }
         }
@@ -1033,9 +1441,17 @@ __global__ void k_exhaust_final(const JobDev* __restrict__ jobs, int njobs) {
     if (J->fb_index[k] != ~0ull && job_ids(J, P, J->fb_index[k], ids, 1)) {
         o->index = (int64_t)J->fb_index[k];
         o->feasible = 1;
-        o->corr = (float)ex_corr(P, ids, 1);
-        o->cp = (float)ex_cp(P, ids, 1, k, f, 1);
-        o->demand = (float)ex_demand(P, ids, 1);
+        if (P->obj) {
+            double T, D;
+            const double U = ex_obj(P, ids, 1, f, 1, T, D);
+            o->corr = (float)obj_j(P->lam_l64, P->m64[k], U, T, D);
+            o->cp = (float)T;
+            o->demand = (float)D;
+        } else {
+            o->corr = (float)ex_corr(P, ids, 1);
+            o->cp = (float)ex_cp(P, ids, 1, k, f, 1);
+            o->demand = (float)ex_demand(P, ids, 1);
+        }
     } else {
         o->index = -1;
         o->feasible = 0;
@@ -1070,6 +1486,18 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
         if (corr) corr[t] = NAN;
         if (dem) dem[t] = NAN;
         if (feas) feas[t] = 0u;
+        return;
+    }
+    if (P->obj) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
+        float U, T, D;
+        eval_obj(P, s_id, s_f, U, T, D);
+        const float G = fmaf(-P->lam_l, T, U);
+        if (live && cpo)
+            for (int k = 0; k < K; ++k) cpo[t * (uint64_t)K + k] = fmaf(-P->m32[k], D, G);
+        if (!live) return;
+        if (corr) corr[t] = U;
+        if (dem) dem[t] = D;
+        if (feas) feas[t] = K >= 32 ? 0xffffffffu : ((1u << K) - 1u);
         return;
     }
     float cc, cp0 = 0.0f;
@@ -1128,16 +1556,22 @@ hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s) {
 }
 
 // sweep jobs: [first, first + n) of d_jobs, all with the same HAS_S2
-hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_samples, int npre_max,
-                               int npre_c, int kmax, hipStream_t s) {
+hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_samples,
+                               int npre_max, int npre_c, int kmax, hipStream_t s) {
     if (n == 0) return hipSuccess;
     const uint64_t gx = (max_samples + WG - 1) / WG;
     if (gx == 0) return hipSuccess;
     if (gx > MAX_GRID_X) return hipErrorInvalidValue;
     const size_t lds = (size_t)((npre_max > 0 ? npre_max : 1) + kmax) * WG * sizeof(float) +
-                       (size_t)PAT_MAX * sizeof(float2);
+                       (size_t)PAT_MAX * (sizeof(float2) + (obj ? sizeof(float) : 0));
     const dim3 grid((uint32_t)gx, n);
-#define DYP_SAMPLE(S2, NP) hipLaunchKernelGGL((k_sample_sweep<S2, NP>), grid, dim3(WG), lds, s, d_jobs)
+#define DYP_SAMPLE(S2, NP)                                                                                 \
+    do {                                                                                                   \
+        if (obj)                                                                                           \
+            hipLaunchKernelGGL((k_sample_sweep_obj<S2, NP>), grid, dim3(WG), lds, s, d_jobs);             \
+        else                                                                                               \
+            hipLaunchKernelGGL((k_sample_sweep<S2, NP>), grid, dim3(WG), lds, s, d_jobs);                 \
+    } while (0)
 #define DYP_SAMPLE_NP(S2)       \
     switch (npre_c) {           \
         case 2: DYP_SAMPLE(S2, 2); break; \
@@ -1156,16 +1590,23 @@ hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_
     return hipGetLastError();
 }
 
-hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, uint64_t max_units, int npre_max, int npre_c,
-                        int ry, hipStream_t s) {
+hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
+                        int npre_c, int ry, hipStream_t s) {
     if (n == 0) return hipSuccess;
-    const size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float) + (size_t)PAT_MAX * sizeof(float2);
+    const size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float) +
+                       (size_t)PAT_MAX * (sizeof(float2) + (obj ? sizeof(float) : 0));
     for (uint64_t off = 0; off < max_units; off += MAX_GRID_X * WG) {
         uint64_t left = max_units - off;
         uint64_t gx = (left + WG - 1) / WG;
         if (gx > MAX_GRID_X) gx = MAX_GRID_X;
         const dim3 grid((uint32_t)gx, n);
-#define DYP_SWEEP(S2, RYV, NP) hipLaunchKernelGGL((k_sweep<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off)
+#define DYP_SWEEP(S2, RYV, NP)                                                                             \
+    do {                                                                                                   \
+        if (obj)                                                                                           \
+            hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off);          \
+        else                                                                                               \
+            hipLaunchKernelGGL((k_sweep<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off);              \
+    } while (0)
 #define DYP_SWEEP_NP(S2, RYV)            \
     switch (npre_c) {                    \
         case 2: DYP_SWEEP(S2, RYV, 2); break; \

@@ -28,13 +28,22 @@ EXPORTED = ("dy_plan_create", "dy_plan_select", "dy_plan_score", "dy_plan_destro
             "dy_status_str", "dy_abi_version", "dy_selftest")
 
 
+class DyObjective(ctypes.Structure):
+    _fields_ = [
+        ("cost", ctypes.c_void_p), ("is_tool", ctypes.c_void_p), ("lambda_f", ctypes.c_float),
+        ("lambda_c", ctypes.c_float), ("lambda_l", ctypes.c_float), ("lambda_ld", ctypes.c_float),
+        ("beta", ctypes.c_float), ("effort", ctypes.c_float), ("n_levels", ctypes.c_int32),
+        ("levels", ctypes.c_void_p),
+    ]
+
+
 class DyProblem(ctypes.Structure):
     _fields_ = [
         ("n_nodes", ctypes.c_int32), ("n_edges", ctypes.c_int32), ("edges", ctypes.c_void_p),
         ("radix", ctypes.c_void_p), ("max_radix", ctypes.c_int32), ("p", ctypes.c_void_p),
         ("tau", ctypes.c_void_p), ("size", ctypes.c_void_p), ("backend", ctypes.c_void_p),
         ("w", ctypes.c_void_p), ("n_levels", ctypes.c_int32), ("n_backends", ctypes.c_int32),
-        ("rho", ctypes.c_void_p), ("slo", ctypes.c_float),
+        ("rho", ctypes.c_void_p), ("slo", ctypes.c_float), ("objective", ctypes.POINTER(DyObjective)),
     ]
 
 
@@ -136,9 +145,10 @@ def rows_source(problem: int, rows, count: int, row_stride: int, index_base: int
 
 
 class _Arrays:
-    """Contiguous host copies kept alive while dy_plan_create reads them."""
+    """Contiguous host copies kept alive while dy_plan_create reads them.
+    `obj` (a workload.Objective or None) selects the additive objective."""
 
-    def __init__(self, prob):
+    def __init__(self, prob, obj=None):
         self.edges = np.ascontiguousarray(prob.edges, dtype=np.int32).reshape(-1, 2)
         self.radix = np.ascontiguousarray(prob.radix, dtype=np.int32)
         self.p = np.ascontiguousarray(prob.p, dtype=np.float32)
@@ -152,6 +162,16 @@ class _Arrays:
                            int(self.p.shape[1]), self.p.ctypes.data, self.tau.ctypes.data, self.size.ctypes.data,
                            self.backend.ctypes.data, self.w.ctypes.data, int(self.rho.shape[0]),
                            int(self.rho.shape[1]), self.rho.ctypes.data, ctypes.c_float(float(prob.slo)))
+        self.obj = None
+        if obj is not None:
+            self.cost = np.ascontiguousarray(obj.cost, dtype=np.float32)
+            self.levels = np.ascontiguousarray(obj.levels, dtype=np.float32)
+            self.is_tool = None if obj.is_tool is None else np.ascontiguousarray(obj.is_tool, dtype=np.int32)
+            self.obj = DyObjective(self.cost.ctypes.data, None if self.is_tool is None else self.is_tool.ctypes.data,
+                                   obj.lambda_f, obj.lambda_c, obj.lambda_l, obj.lambda_ld, obj.beta, obj.effort,
+                                   int(self.levels.shape[0]), self.levels.ctypes.data)
+            self.c.objective = ctypes.pointer(self.obj)
+        self.n_levels = int(self.levels.shape[0]) if obj is not None else int(self.rho.shape[0])
 
 
 def create_raw(structs: Sequence[DyProblem], device: int = 0):
@@ -168,16 +188,20 @@ def last_error(handle=None) -> str:
 
 
 class Plan:
-    """A handle over one or more planning problems staged on one device."""
+    """A handle over one or more planning problems staged on one device.  Each
+    problem is a workload.Problem (corr / SLO selection) or a pair (Problem,
+    Objective) for the paper's additive objective."""
 
     def __init__(self, problems, device: int = 0):
+        if isinstance(problems, tuple) and len(problems) == 2 and hasattr(problems[1], "levels"):
+            problems = [problems]
         probs = list(problems) if isinstance(problems, (list, tuple)) else [problems]
-        keep = [_Arrays(p) for p in probs]
+        keep = [_Arrays(*p) if isinstance(p, tuple) else _Arrays(p) for p in probs]
         st, h = create_raw([k.c for k in keep], device)
         if st != DY_OK:
             raise DyplanError(st, last_error(None))
         self._h = h
-        self.n_levels = [int(p.rho.shape[0]) for p in probs]
+        self.n_levels = [k.n_levels for k in keep]
         self.kmax = int(lib().dy_plan_max_levels(h))
 
     def close(self):

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_status_strings_and_selftest():
     lib = D.lib()
-    assert lib.dy_abi_version() == 1
+    assert lib.dy_abi_version() == 2
     assert lib.dy_selftest() == 0
     for st in (D.DY_OK, D.DY_EINVAL, D.DY_ENOTDAG, D.DY_ELIMIT, D.DY_ENOMEM, D.DY_EDEVICE):
         assert lib.dy_status_str(st).decode() not in ("", "unknown status")
@@ -43,7 +43,8 @@ def test_abi_version_status_strings_and_selftest():
 def test_struct_layouts_match_header():
     assert ctypes.sizeof(D.DyChoice) == 24
     assert ctypes.sizeof(D.DySource) == 48
-    assert ctypes.sizeof(D.DyProblem) == 96
+    assert ctypes.sizeof(D.DyProblem) == 104
+    assert ctypes.sizeof(D.DyObjective) == 56
 
 
 def _struct(prob):
@@ -120,4 +121,63 @@ def test_validation_limits_and_null_pointers():
 @pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
 def test_valid_problem_without_device_reports_device_error():
     st, msg = _create_status(wl.chain4())
+    assert st == D.DY_EDEVICE and msg
+
+
+def _obj_status(prob, obj, mutate=None):
+    a = D._Arrays(prob, obj)
+    if mutate:
+        mutate(a)
+    st, h = D.create_raw([a.c])
+    if h:
+        D.lib().dy_plan_destroy(h)
+    return st, D.last_error(None)
+
+
+def test_objective_validation_errors_before_device():
+    import dataclasses
+    base = wl.chain4()
+    obj = wl.paper_objective(base)
+
+    def with_(**kw):
+        return dataclasses.replace(obj, **kw)
+
+    cost_nan = obj.cost.copy(); cost_nan[1, 2] = np.nan
+    cost_big = obj.cost.copy(); cost_big[0, 0] = 3e38
+    cases = [
+        ("cost NaN", with_(cost=cost_nan), None, D.DY_EINVAL),
+        ("utility too large", with_(cost=cost_big, lambda_c=1e9), None, D.DY_EINVAL),
+        ("effort > 1", with_(effort=1.5), None, D.DY_EINVAL),
+        ("lambda_l < 0", with_(lambda_l=-0.1), None, D.DY_EINVAL),
+        ("lambda_ld NaN", with_(lambda_ld=float("nan")), None, D.DY_EINVAL),
+        ("beta inf", with_(beta=float("inf")), None, D.DY_EINVAL),
+        ("level < 0", with_(levels=np.array([0.0, -1.0], np.float32)), None, D.DY_EINVAL),
+        ("33 levels", with_(levels=np.zeros(33, np.float32)), None, D.DY_ELIMIT),
+        ("is_tool 2", with_(is_tool=np.array([0, 2, 0, 0], np.int32)), None, D.DY_EINVAL),
+        ("cost NULL", obj, lambda a: setattr(a.obj, "cost", None), D.DY_EINVAL),
+        ("levels NULL", obj, lambda a: setattr(a.obj, "levels", None), D.DY_EINVAL),
+        ("n_levels 0", obj, lambda a: setattr(a.obj, "n_levels", 0), D.DY_EINVAL),
+    ]
+    for name, o, mut, want in cases:
+        st, msg = _obj_status(base, o, mut)
+        assert st == want, (name, st, msg)
+        assert msg, name
+
+
+@pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
+def test_objective_ignores_corr_only_fields():
+    # rho, size and backend are not read in objective mode (NULL is accepted), and
+    # an SLO or rho that corr / SLO selection rejects does not matter
+    base = wl.chain4()
+    obj = wl.paper_objective(base)
+
+    def strip(a):
+        a.c.rho = None
+        a.c.size = None
+        a.c.backend = None
+        a.c.slo = float("nan")
+        a.c.n_levels = 0
+        a.c.n_backends = 0
+
+    st, msg = _obj_status(base, obj, strip)
     assert st == D.DY_EDEVICE and msg

@@ -1,0 +1,303 @@
+"""GPU parity of the objective mode (the paper's additive objective J_L,
+Sec. 4.3 eq. admission-objective with Sec. 4.4 eq. variant-objective) against
+the fp64 CPU oracle (oracle/objective.c), through the C-ABI.
+
+Bar: selected indices bit-exact, every level admissible (feasible = 1); the
+winner's J_k, T and D equal its fp64 values rounded to the nearest fp32 (the
+library re-evaluates winners in fp64 in the definition's operation order).
+Per-plan fp32 scores: |J_k(fp32) - J_k(fp64)| <= 1e-5 * A_k with A_k = the sum
+over LLM nodes of the largest |u| + lambda_l T + lambda_ld L_k D (the derived
+bound is (N + 6) 2^-24 A_k <= 2.2e-6 A_k at N <= 32); U and D likewise.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import oracle as orc  # noqa: E402
+from paper_2607_02942_amd import dyplan as D  # noqa: E402
+from paper_2607_02942_amd import workload as wl  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+RTOL = 1e-5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    D.lib()
+    torch.cuda.set_device(0)
+    yield
+
+
+def stream():
+    return torch.cuda.current_stream()
+
+
+def f32(x):
+    return float(np.float32(x))
+
+
+def assert_obj_choices(got, want, ctx=""):
+    assert len(got) == len(want)
+    for k, (g, w) in enumerate(zip(got, want)):
+        assert g[0] == int(w[0]) and g[1] == 1 and int(w[1]) == 1, f"{ctx} level {k}: gpu {g} oracle {w}"
+        assert g[2] == f32(w[2]) and g[3] == f32(w[3]) and g[4] == f32(w[4]), f"{ctx} level {k}: {g} vs {w}"
+
+
+def select(prob, obj, sources, options=()):
+    with D.Plan((prob, obj)) as plan:
+        for o, v in options:
+            plan.set_option(o, v)
+        return plan.select(sources, stream=stream())
+
+
+def util_bound(prob, obj):
+    """Sum over LLM nodes of the largest |u| (a magnitude bound for U)."""
+    reach = orc.obj_reach(prob, obj)
+    q = prob.p.astype(np.float64)
+    u = reach[:, None] * q - obj.lambda_f * prob.w[:, None].astype(np.float64) * (1 - q) \
+        - obj.lambda_c * obj.cost.astype(np.float64)
+    s = 0.0
+    for n in range(prob.n_nodes):
+        if obj.is_tool is not None and obj.is_tool[n]:
+            continue
+        s += np.abs(u[n, :prob.radix[n]]).max()
+    return s
+
+
+def with_tools(obj, n, tools):
+    t = np.zeros(n, np.int32)
+    t[list(tools)] = 1
+    return dataclasses.replace(obj, is_tool=t)
+
+
+def small_dag(n, radix, seed, edges=None):
+    """A seeded random problem of n nodes (values in the paper workloads' ranges)."""
+    rng = np.random.default_rng(seed)
+    R = max(radix)
+    if edges is None:
+        edges = [(i, j) for i in range(n) for j in range(i + 1, n) if rng.random() < 0.4]
+    e = np.array(edges, np.int32).reshape(-1, 2)
+    return wl.Problem(n_nodes=n, edges=e, radix=np.array(radix, np.int32),
+                      p=rng.uniform(0.6, 0.95, (n, R)).astype(np.float32),
+                      tau=rng.lognormal(0.0, 0.5, (n, R)).astype(np.float32),
+                      size=rng.choice([1.0, 2.5, 6.0], (n, R)).astype(np.float32),
+                      backend=np.zeros((n, R), np.int32), w=rng.uniform(0.2, 1.0, n).astype(np.float32),
+                      rho=np.zeros((1, 1), np.float32), slo=np.float32(np.inf))
+
+
+# ---------------------------------------------------------------------------
+# selection, enumerated sources (the prefix-shared sweep)
+# ---------------------------------------------------------------------------
+
+def test_chain4_full_space():
+    prob = wl.chain4()
+    obj = wl.paper_objective(prob)
+    n = prob.n_plans()
+    got = select(prob, obj, [D.range_source(0, 0, n)])[0]
+    assert_obj_choices(got, orc.obj_select_range(prob, obj, 0, n), "chain4")
+
+
+@pytest.mark.parametrize("begin,count", [(0, 1 << 20), (123457, 1000003), (429981696 - 777777, 777777),
+                                         (5, 1), (144 * 1000 + 7, 143)])
+def test_forkjoin8_ragged_ranges(begin, count):
+    prob = wl.forkjoin8()
+    obj = wl.paper_objective(prob)
+    got = select(prob, obj, [D.range_source(0, begin, count)])[0]
+    assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"forkjoin8[{begin}+{count}]")
+
+
+def test_forkjoin8_tools_weights_and_many_levels():
+    prob = wl.forkjoin8()
+    obj = with_tools(wl.paper_objective(prob, levels=np.linspace(0.0, 6.0, 12), lambda_l=0.4, lambda_c=0.1,
+                                        effort=0.9), 8, (0, 7))
+    for begin, count in ((0, 1 << 19), (3 * 12 ** 6 + 11, 600011)):
+        got = select(prob, obj, [D.range_source(0, begin, count)])[0]
+        assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"tools[{begin}+{count}]")
+
+
+@pytest.mark.parametrize("begin,count", [(0, 1 << 21), ((1 << 32) - 999999, 999999)])
+def test_layered10_ranges(begin, count):
+    prob = wl.layered10()
+    obj = wl.paper_objective(prob)
+    got = select(prob, obj, [D.range_source(0, begin, count)])[0]
+    assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"layered10[{begin}+{count}]")
+
+
+@pytest.mark.parametrize("n,radix,seed", [(1, [7], 1), (2, [5, 9], 2), (3, [4, 1, 6], 3), (5, [3, 4, 2, 5, 3], 4),
+                                          (6, [12] * 6, 5), (12, [3] * 12, 6)])
+def test_small_dags_full_space(n, radix, seed):
+    prob = small_dag(n, radix, seed)
+    rng = np.random.default_rng(seed + 100)
+    obj = wl.Objective(cost=(prob.tau * prob.size).astype(np.float32),
+                       levels=rng.uniform(0, 4, 1 + seed % 5).astype(np.float32),
+                       lambda_f=float(rng.uniform(-1, 2)), lambda_c=float(rng.uniform(-0.1, 0.2)),
+                       lambda_l=float(rng.uniform(0, 0.5)), lambda_ld=float(rng.uniform(0, 0.3)),
+                       beta=float(rng.uniform(-1, 2)), effort=float(rng.uniform(0, 1)),
+                       is_tool=(rng.random(n) < 0.3).astype(np.int32))
+    total = int(np.prod(radix))
+    got = select(prob, obj, [D.range_source(0, 0, total)])[0]
+    assert_obj_choices(got, orc.obj_select_range(prob, obj, 0, total), f"dag{n}")
+
+
+def test_batch_mixed_with_corr_selection():
+    # objective and corr / SLO problems in one call: both sweep groups run together
+    probs = [wl.batch6_request(r) for r in range(4)]
+    objs = [wl.paper_objective(p) for p in probs]
+    items = [probs[0], (probs[1], objs[1]), probs[2], (probs[3], objs[3])]
+    with D.Plan(items) as plan:
+        got = plan.select([D.range_source(r, 0, 12 ** 6) for r in range(4)], stream=stream())
+    for r in (1, 3):
+        assert_obj_choices(got[r], orc.obj_select_range(probs[r], objs[r], 0, 12 ** 6), f"batch[{r}]")
+    for r in (0, 2):
+        want = orc.select_range(probs[r], 0, 12 ** 6)
+        for g, w in zip(got[r], want):
+            assert (g[0], g[1]) == (int(w[0]), int(w[1])), f"corr batch[{r}]"
+
+
+# ---------------------------------------------------------------------------
+# ties, overflow recovery and the exhaustive path
+# ---------------------------------------------------------------------------
+
+def test_exact_ties_go_to_the_lowest_index():
+    # implementations 2k and 2k+1 identical in every table: each winner has
+    # tie partners, and the lowest index must win
+    prob = wl.chain4().copy()
+    for a in ("p", "tau", "size", "backend"):
+        t = getattr(prob, a).copy()
+        t[:, 1::2] = t[:, 0::2]
+        setattr(prob, a, t)
+    obj = wl.paper_objective(prob)
+    n = prob.n_plans()
+    want = orc.obj_select_range(prob, obj, 0, n)
+    got = select(prob, obj, [D.range_source(0, 0, n)])[0]
+    assert_obj_choices(got, want, "ties")
+    for c in got:
+        impl = [(c[0] // 12 ** (3 - i)) % 12 for i in range(4)]
+        assert all(x % 2 == 0 for x in impl), impl
+
+
+def test_all_plans_tie_overflow_then_exhaustive():
+    # every implementation identical: all plans tie at every level, the candidate
+    # list overflows, reseeding cannot help, the exhaustive fp64 path decides
+    prob = wl.chain4().copy()
+    for a in ("p", "tau", "size"):
+        t = getattr(prob, a).copy()
+        t[:] = t[:, :1]
+        setattr(prob, a, t)
+    obj = wl.paper_objective(prob)
+    begin, count = 777, 5000
+    with D.Plan((prob, obj)) as plan:
+        plan.set_option(D.DY_OPT_CAND_CAPACITY, 64)
+        got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+        assert plan.stats().fallbacks == obj.n_levels
+    assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), "all tie")
+    assert all(c[0] == begin for c in got)
+
+
+def test_small_candidate_capacity_reseeds():
+    prob = wl.forkjoin8()
+    obj = wl.paper_objective(prob)
+    begin, count = 1000, 1 << 20
+    want = orc.obj_select_range(prob, obj, begin, count)
+    with D.Plan((prob, obj)) as plan:
+        plan.set_option(D.DY_OPT_CAND_CAPACITY, 16)
+        plan.set_option(D.DY_OPT_SAMPLE_STRIDE, 1 << 20)  # a poor seed: many candidates on the first pass
+        got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+    assert_obj_choices(got, want, "reseed")
+
+
+def test_force_fp64_matches():
+    prob = wl.forkjoin8()
+    obj = with_tools(wl.paper_objective(prob), 8, (3,))
+    begin, count = 4242, 300000
+    want = orc.obj_select_range(prob, obj, begin, count)
+    got = select(prob, obj, [D.range_source(0, begin, count)], options=((D.DY_OPT_FORCE_FP64, 1),))[0]
+    assert_obj_choices(got, want, "fp64")
+
+
+def test_graph_replay_matches():
+    prob = wl.forkjoin8()
+    obj = wl.paper_objective(prob)
+    src = [D.range_source(0, 99, 1 << 20)]
+    want = orc.obj_select_range(prob, obj, 99, 1 << 20)
+    with D.Plan((prob, obj)) as plan:
+        for rep in range(4):
+            assert_obj_choices(plan.select(src, stream=stream())[0], want, f"replay {rep}")
+
+
+# ---------------------------------------------------------------------------
+# ROWS sources (the generic per-plan path)
+# ---------------------------------------------------------------------------
+
+def test_stream24_rows():
+    prob = wl.stream24()
+    obj = with_tools(wl.paper_objective(prob), 24, (0, 5, 23))
+    n = 300007
+    rows = wl.make_rows(n, 24, 36, row_begin=4321)
+    want = orc.obj_select_rows(prob, obj, rows, index_base=4321)
+    with D.Plan((prob, obj)) as plan:
+        d = torch.from_numpy(rows).cuda()
+        got = plan.select([D.rows_source(0, d, n, 24, 4321)], stream=stream())[0]
+        assert_obj_choices(got, want, "stream24 rows")
+        padded = np.zeros((n, 27), np.uint8)
+        padded[:, :24] = rows
+        dp = torch.from_numpy(padded).cuda()
+        got = plan.select([D.rows_source(0, dp, n, 27, 4321)], stream=stream())[0]
+        assert_obj_choices(got, want, "stream24 rows, odd stride")
+
+
+def test_rows_bad_id_is_an_error():
+    prob = wl.chain4()
+    obj = wl.paper_objective(prob)
+    rows = np.zeros((1000, 4), np.uint8)
+    rows[517, 2] = 12
+    with D.Plan((prob, obj)) as plan:
+        d = torch.from_numpy(rows).cuda()
+        with pytest.raises(D.DyplanError):
+            plan.select([D.rows_source(0, d, 1000, 4)], stream=stream())
+
+
+# ---------------------------------------------------------------------------
+# per-plan scores
+# ---------------------------------------------------------------------------
+
+def check_scores(prob, obj, U, T, Dd, J, gu, gj, gd, gf):
+    K = obj.n_levels
+    su = util_bound(prob, obj)
+    m = obj.lambda_ld * obj.levels.astype(np.float64)
+    assert np.all(np.abs(gu - U) <= RTOL * su)
+    assert np.all(np.abs(gd - Dd) <= RTOL * Dd.max())
+    for k in range(K):
+        A = su + obj.lambda_l * T + m[k] * Dd
+        err = np.abs(gj[:, k].astype(np.float64) - J[:, k])
+        assert np.all(err <= RTOL * A), (k, float((err / A).max()))
+    assert np.all(gf == (1 << K) - 1)
+
+
+def test_score_range_and_rows():
+    prob = wl.forkjoin8()
+    obj = with_tools(wl.paper_objective(prob, levels=(0.0, 0.5, 1.5, 3.0)), 8, (7,))
+    K = obj.n_levels
+    cnt = 200003
+    with D.Plan((prob, obj)) as plan:
+        u = torch.empty(cnt, dtype=torch.float32, device="cuda")
+        j = torch.empty(cnt, K, dtype=torch.float32, device="cuda")
+        d = torch.empty(cnt, dtype=torch.float32, device="cuda")
+        f = torch.empty(cnt, dtype=torch.int32, device="cuda")
+        plan.score(D.range_source(0, 31337, cnt), u, j, d, f, stream=stream())
+        torch.cuda.synchronize()
+        U, T, Dd, J = orc.obj_score(prob, obj, 31337, cnt)
+        check_scores(prob, obj, U, T, Dd, J, u.cpu().numpy(), j.cpu().numpy(), d.cpu().numpy(),
+                     f.cpu().numpy().astype(np.uint32))
+        rows = wl.make_rows(cnt, 8, 12, row_begin=99)
+        dr = torch.from_numpy(rows).cuda()
+        plan.score(D.rows_source(0, dr, cnt, 8), u, j, d, f, stream=stream())
+        torch.cuda.synchronize()
+        U, T, Dd, J = orc.obj_score(prob, obj, rows=rows)
+        check_scores(prob, obj, U, T, Dd, J, u.cpu().numpy(), j.cpu().numpy(), d.cpu().numpy(),
+                     f.cpu().numpy().astype(np.uint32))
