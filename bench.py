@@ -8,7 +8,9 @@ time is reported separately as "stage_ms".
 
 Default workload: forkjoin8 (8-node fork-join DAG, 12 implementations per
 node, 12^8 = 429,981,696 plans, 8 pressure levels).  --workload picks another
-(chain4, layered10, batch6, stream24) for profiling.
+(chain4, layered10, batch6, stream24) for profiling; --objective scores it
+under the paper's additive objective J_L instead (levels L in {0, 1.5, 3},
+call cost c = tau * size), a separate measurement of that mode.
 
 Two timed loops of the same K calls: the first, as a caller runs them
 (repeated calls replay one HIP graph), gives "value" and "ms_per_step"; the
@@ -47,7 +49,8 @@ PEAK_HBM = 8.0e12                 # bytes/s
 # figure is reported only while these files are unchanged.
 KERNEL_SOURCES = ("paper_2607_02942_amd/csrc/kernels.hip", "paper_2607_02942_amd/csrc/jit_rows.cpp",
                   "paper_2607_02942_amd/csrc/dyplan_internal.h")
-DOMINANT = {"stream24": "dy_rows_scan_a"}  # else the sweep kernel
+DOMINANT = {"stream24": "dy_rows_scan_a", "stream24_obj": "dy_rows_scan_a"}  # else the sweep kernel
+OBJ_SWEEP = "k_sweep_obj"
 
 
 def kernel_source_sha():
@@ -95,7 +98,7 @@ def ingest_pmc(workload, fetch_db, write_db, calib_fetch_db, calib_write_db, cal
         if not hits:
             raise SystemExit(f"no kernel matching {key!r} in {sorted(means)}")
         return hits[0]
-    kern = DOMINANT.get(workload, "k_sweep")
+    kern = DOMINANT.get(workload, OBJ_SWEEP if workload.endswith("_obj") else "k_sweep")
     kname, fetch = pick(_pmc_means(fetch_db, "FETCH_SIZE"), kern)
     _, write = pick(_pmc_means(write_db, "WRITE_SIZE"), kern)
     _, cf = pick(_pmc_means(calib_fetch_db, "FETCH_SIZE"), "copyBuffer")
@@ -139,20 +142,51 @@ def sweep_work_per_plan(prob):
     return per_plan + per_row / ry + per_block / (rx * ry)
 
 
+def obj_sweep_work_per_plan(prob):
+    """Algorithmic fp32 operations per plan of the objective-mode sweep.
+
+    Per plan: the add of y's duration (T), the max with the prefix sinks' path
+    when there is one, the adds of y's utility (U) and d (D), the fused
+    multiply-add G = U - lambda_l T and the prefilter compare; per row: the
+    adds of node x (its path, utility and d) and the max of y's predecessors;
+    per block: the prefix sums of u and d and one max/add per prefix edge.
+    """
+    n = prob.n_nodes
+    rx = int(prob.radix[n - 2]) if n >= 2 else 1
+    ry = int(prob.radix[n - 1])
+    edges = {(int(u), int(v)) for u, v in prob.edges}
+    npre = max(n - 2, 0)
+    pre_edges = sum(1 for u, v in edges if v < npre)
+    x_pred = sum(1 for u, v in edges if v == n - 2)
+    y_pred = sum(1 for u, v in edges if v == n - 1 and u != n - 2)
+    pre_sinks = any(all(u != m for u, v in edges) for m in range(npre))
+    has_s2 = pre_sinks or (n - 2, n - 1) not in edges
+    per_plan = 5.0 + (1.0 if has_s2 else 0.0)
+    per_row = 3.0 + (1.0 if (n - 2, n - 1) in edges and y_pred > 0 else 0.0)
+    per_block = 2 * max(npre - 1, 0) + pre_edges + x_pred + y_pred
+    return per_plan + per_row / ry + per_block / (rx * ry)
+
+
 def full_work_per_plan(prob, K):
     """The per-plan count of the full recurrence: (N-1) mul + E max/add + K compares."""
     return (prob.n_nodes - 1) + edge_count(prob) + K
 
 
-def cpu_baseline(prob, sample_plans=None, rows=None):
+def cpu_baseline(prob, sample_plans=None, rows=None, obj=None):
     from oracle import oracle as orc
     t0 = time.perf_counter()
     if rows is not None:
-        orc.select_rows(prob, rows, 0)
+        if obj is None:
+            orc.select_rows(prob, rows, 0)
+        else:
+            orc.obj_select_rows(prob, obj, rows, 0)
         n = rows.shape[0]
         what = f"first {n} rows"
     else:
-        orc.select_range(prob, 0, sample_plans)
+        if obj is None:
+            orc.select_range(prob, 0, sample_plans)
+        else:
+            orc.obj_select_range(prob, obj, 0, sample_plans)
         n = sample_plans
         what = f"plan indices [0, {sample_plans})"
     dt = time.perf_counter() - t0
@@ -167,6 +201,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="forkjoin8",
                     choices=["chain4", "forkjoin8", "layered10", "batch6", "stream24"])
+    ap.add_argument("--objective", action="store_true",
+                    help="the paper's additive objective J_L (levels 0, 1.5, 3) instead of corr / SLO")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=1 << 26)
     ap.add_argument("--sample-stride", type=int, default=0)
@@ -176,8 +212,9 @@ def main():
     ap.add_argument("--calib-bytes", type=int, default=1 << 30)
     ap.add_argument("--pmc-command", action="append", default=[], help="command that produced a database")
     args = ap.parse_args()
+    tkey = args.workload + ("_obj" if args.objective else "")
     if args.ingest_pmc:
-        ingest_pmc(args.workload, *args.ingest_pmc, args.calib_bytes, args.pmc_command)
+        ingest_pmc(tkey, *args.ingest_pmc, args.calib_bytes, args.pmc_command)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
@@ -224,11 +261,16 @@ def main():
             sources = [D.range_source(0, 0, plans)]
     prob = probs[0]
     K = prob.n_levels
-    for p in probs:
-        assert np.isfinite(p.slo), f"stored SLO missing for {p.name}"
+    objs = None
+    if args.objective:
+        objs = [wl.paper_objective(p) for p in probs]
+        K = objs[0].n_levels
+    else:
+        for p in probs:
+            assert np.isfinite(p.slo), f"stored SLO missing for {p.name}"
 
     t0 = time.perf_counter()
-    plan = D.Plan(probs, device=0)
+    plan = D.Plan(list(zip(probs, objs)) if objs else probs, device=0)
     stage_ms = (time.perf_counter() - t0) * 1e3
     if args.sample_stride:
         plan.set_option(D.DY_OPT_SAMPLE_STRIDE, args.sample_stride)
@@ -274,16 +316,20 @@ def main():
     if name == "stream24":
         bytes_per_plan = 24.0
         achieved = kern_plans_s * bytes_per_plan
-        roof = {"bound": "hbm", "kernel": "dy_rows_scan_a (rows, generated for the DAG)", "achieved": achieved / 1e9,
+        kname = "dy_rows_scan_a (rows, generated for the DAG" + (", objective)" if objs else ")")
+        roof = {"bound": "hbm", "kernel": kname, "achieved": achieved / 1e9,
                 "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": achieved / PEAK_HBM,
-                "traffic": stored_traffic(name), "per_unit": "24 B of row per plan", "kernel_ms": kern_ms}
+                "traffic": stored_traffic(tkey), "per_unit": "24 B of row per plan", "kernel_ms": kern_ms}
     else:
-        f = sweep_work_per_plan(prob)
+        f = obj_sweep_work_per_plan(prob) if objs else sweep_work_per_plan(prob)
         achieved = kern_plans_s * f
-        roof = {"bound": "alu", "kernel": "k_sweep", "achieved": achieved / 1e12, "peak": PEAK_VALU / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_VALU, "traffic": stored_traffic(name),
-                "per_unit": f"{f:.4f} fp32 ops per plan (prefix-shared sweep)", "kernel_ms": kern_ms,
-                "full_recurrence_ops_per_plan": full_work_per_plan(prob, K)}
+        roof = {"bound": "alu", "kernel": OBJ_SWEEP if objs else "k_sweep", "achieved": achieved / 1e12,
+                "peak": PEAK_VALU / 1e12, "unit": "TFLOP/s", "frac": achieved / PEAK_VALU,
+                "traffic": stored_traffic(tkey),
+                "per_unit": f"{f:.4f} fp32 ops per plan (prefix-shared sweep{', objective' if objs else ''})",
+                "kernel_ms": kern_ms}
+        if not objs:
+            roof["full_recurrence_ops_per_plan"] = full_work_per_plan(prob, K)
 
     res = {
         "metric": METRIC, "value": value, "unit": "plans/s", "n_gpus": 1, "steps": args.steps,
@@ -291,19 +337,21 @@ def main():
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": name, "plans": plans, "nodes": prob.n_nodes, "edges": edge_count(prob),
                    "impls_per_node": int(prob.radix[0]), "levels": K,
-                   "problems": len(probs), "parallelism": "single GPU"},
+                   "problems": len(probs), "parallelism": "single GPU",
+                   "selection": "paper objective J_L, L in {0, 1.5, 3}" if objs else "max corr s.t. CP_k <= SLO"},
         "roofline": roof,
         "stage_ms": stage_ms,
         "ms_per_step_timed": ms_per_step_timed,
         "candidates_per_step": float(np.mean(cands)),
     }
     if not args.no_cpu_baseline:
+        o0 = objs[0] if objs else None
         if name == "stream24":
-            res["cpu_baseline"] = cpu_baseline(prob, rows=rows_host[: 1 << 22])
+            res["cpu_baseline"] = cpu_baseline(prob, rows=rows_host[: 1 << 22], obj=o0)
         elif name == "batch6":
-            res["cpu_baseline"] = cpu_baseline(prob, sample_plans=12 ** 6)
+            res["cpu_baseline"] = cpu_baseline(prob, sample_plans=12 ** 6, obj=o0)
         else:
-            res["cpu_baseline"] = cpu_baseline(prob, sample_plans=min(args.cpu_sample, plans))
+            res["cpu_baseline"] = cpu_baseline(prob, sample_plans=min(args.cpu_sample, plans), obj=o0)
     plan.close()
     print(json.dumps(res), flush=True)
 

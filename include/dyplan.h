@@ -124,7 +124,8 @@ typedef struct dy_plan dy_plan; /* opaque handle */
  *  lambda_ld weight of the demand D_tau, >= 0.
  *  beta, effort         reach weight parameters (effort e in [0, 1]).
  *  n_levels, levels     K specialisation levels L_k >= 0, float [K].
- * |each utility| and lambda_l T and lambda_ld L_k D must stay below 1e30.
+ * The sum over LLM nodes of the largest |u|, lambda_l times the sum of the
+ * largest durations, and lambda_ld L_k times that sum must each stay <= 1e30.
  */
 typedef struct dy_objective {
     const float* cost;

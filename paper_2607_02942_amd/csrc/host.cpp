@@ -1125,7 +1125,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         const HostProb& H = h->hp[p];
         if (src[j].kind == DY_SOURCE_RANGE && H.uniform)
             grp[j] = H.obj ? (H.has_s2 ? G_OSWEEP_S2 : G_OSWEEP) : (H.has_s2 ? G_SWEEP_S2 : G_SWEEP);
-        else if (src[j].kind == DY_SOURCE_ROWS && H.uniform && !H.obj && !h->force_fp64 && jit_ready(h, p))
+        else if (src[j].kind == DY_SOURCE_ROWS && H.uniform && !h->force_fp64 && jit_ready(h, p))
             grp[j] = G_JIT;
         else
             grp[j] = G_GENERIC;

@@ -21,6 +21,11 @@
 // its node's table whatever the row holds.  The
 // arithmetic is that of the generic kernels (same fp32 operations in the
 // same order), so both produce identical scores.
+//
+// Objective mode (the paper's additive objective): the tables hold (u, tau);
+// a row's U and D are the sums of the LLM nodes' u and tau in node order, T
+// the same recurrence, G = U - lambda_l T in one rounding, and the prefilter
+// bin is that of D.  No early abandon: every row is evaluated in full.
 #include <hip/hip_runtime.h>
 #include <hip/hiprtc.h>
 
@@ -108,6 +113,50 @@ std::vector<int> checkpoints(int N) {
     return cuts;
 }
 
+// fp64 literal
+std::string dlit(double x) {
+    char buf[48];
+    std::snprintf(buf, sizeof buf, "%a", x);
+    return buf;
+}
+
+// f_n = tau_n + max over predecessors, nodes [n0, n1), unrolled
+void emit_recurrence(std::ostringstream& o, const ProbDev& D, int n0, int n1) {
+    for (int n = n0; n < n1; ++n) {
+        std::vector<int> preds;
+        for (int u = 0; u < n; ++u)
+            if (D.pred[n] >> u & 1u) preds.push_back(u);
+        o << "  const float f" << n << " = e" << n << ".y";
+        if (!preds.empty()) {
+            std::string m = "f" + std::to_string(preds[0]);
+            for (size_t k = 1; k < preds.size(); ++k) m = "fmaxf(" + m + ", f" + std::to_string(preds[k]) + ")";
+            o << " + " << m;
+        }
+        o << "; \\\n";
+    }
+}
+
+// dst = max of f_n over the sinks (declared here when `declare`)
+void emit_sinks(std::ostringstream& o, const ProbDev& D, const char* dst, bool declare) {
+    bool first = true;
+    for (int n = 0; n < D.n; ++n) {
+        if (!(D.sinks >> n & 1u)) continue;
+        if (first)
+            o << "  " << (declare ? "float " : "") << dst << " = f" << n << "; \\\n";
+        else
+            o << "  " << dst << " = fmaxf(" << dst << ", f" << n << "); \\\n";
+        first = false;
+    }
+}
+
+// objective mode: u_ = sum of the LLM nodes' utilities, d_ = sum of their
+// durations (their d), in node order; tool nodes add nothing
+void emit_obj_sums(std::ostringstream& o, const ProbDev& D, int n0, int n1) {
+    o << "  float u_ = 0.0f, d_ = 0.0f; \\\n";
+    for (int n = n0; n < n1; ++n)
+        if (D.llm >> n & 1u) o << "  u_ = u_ + e" << n << ".x; d_ = d_ + e" << n << ".y; \\\n";
+}
+
 std::string gen_source(const ProbDev& D) {
     const int N = D.n;
     const int Q = (N + 3) / 4;
@@ -157,6 +206,18 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
     o << "#define DY_LOADP(pp, " << wl("x") << ") { const unsigned char* p_ = (pp); \\\n";
     load_body("x", "ALIGNED");
     o << " __builtin_amdgcn_sched_barrier(0); }\n";
+    // objective mode: the level weights as literals
+    if (D.obj) {
+        o << "#define DY_LAM " << flit(D.lam_l) << "\n";
+        o << "__device__ __constant__ const float dy_m32[DY_K] = {";
+        for (int k = 0; k < D.k; ++k) o << (k ? ", " : "") << flit(D.m32[k]);
+        o << "};\n__device__ __constant__ const double dy_m64[DY_K] = {";
+        for (int k = 0; k < D.k; ++k) o << (k ? ", " : "") << dlit(D.m64[k]);
+        o << "};\n";
+        o << "__device__ __forceinline__ unsigned dy_fkey(float x) {\n"
+             "  const unsigned b = __float_as_uint(x);\n"
+             "  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);\n}\n";
+    }
     // evaluation of one row held in words w0..
     o << "#define DY_EVAL(" << wl("w") << ", c, cp, bad) { \\\n  unsigned bk_ = 0u; \\\n";
     for (int q = 0; q < Q; ++q)
@@ -168,26 +229,15 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         if (b) o << " >> " << 8 * b;
         o << ") & 63u)]; \\\n";
     }
-    o << "  c = e0.x; \\\n";
-    for (int n = 1; n < N; ++n) o << "  c = c * e" << n << ".x; \\\n";
-    for (int n = 0; n < N; ++n) {
-        std::vector<int> preds;
-        for (int u = 0; u < n; ++u)
-            if (D.pred[n] >> u & 1u) preds.push_back(u);
-        o << "  const float f" << n << " = e" << n << ".y";
-        if (!preds.empty()) {
-            std::string m = "f" + std::to_string(preds[0]);
-            for (size_t k = 1; k < preds.size(); ++k) m = "fmaxf(" + m + ", f" + std::to_string(preds[k]) + ")";
-            o << " + " << m;
-        }
-        o << "; \\\n";
+    if (D.obj) {
+        emit_obj_sums(o, D, 0, N);
+    } else {
+        o << "  c = e0.x; \\\n";
+        for (int n = 1; n < N; ++n) o << "  c = c * e" << n << ".x; \\\n";
     }
-    bool first = true;
-    for (int n = 0; n < N; ++n) {
-        if (!(D.sinks >> n & 1u)) continue;
-        o << (first ? "  cp = f" : "  cp = fmaxf(cp, f") << n << (first ? "; \\\n" : "); \\\n");
-        first = false;
-    }
+    emit_recurrence(o, D, 0, N);
+    emit_sinks(o, D, D.obj ? "t_" : "cp", D.obj != 0);
+    if (D.obj) o << "  c = fmaf(-DY_LAM, t_, u_); \\\n  cp = d_; \\\n";
     o << "}\n";
     // one row of the scoring pass.  The nodes are evaluated in segments; at
     // the end of each but the last the wave abandons its rows when none can
@@ -200,7 +250,7 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
     // Rows that reach the end take the prefilter by the bin of their CP, the
     // exact per-level test, then the wave's LDS candidate queue.
     {
-        const std::vector<int> cuts = checkpoints(N);
+        const std::vector<int> cuts = D.obj ? std::vector<int>() : checkpoints(N);
         o << "#define DY_HANDLE(" << wl("y") << ", rr, LIVE) { \\\n  const bool live = (LIVE); \\\n"
           << "  unsigned bk_ = 0u; \\\n";
         for (int q = 0; q < Q; ++q)
@@ -217,20 +267,10 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
                 if (bb) o << " >> " << 8 * bb;
                 o << ") & 63u)]; \\\n";
             }
-            for (int n = n0; n < m; ++n) o << (n == 0 ? "  c = e0.x; \\\n" : "  c = c * e") << (n == 0 ? "" : std::to_string(n) + ".x; \\\n");
-            for (int n = n0; n < m; ++n) {
-                std::vector<int> preds;
-                for (int u = 0; u < n; ++u)
-                    if (D.pred[n] >> u & 1u) preds.push_back(u);
-                o << "  const float f" << n << " = e" << n << ".y";
-                if (!preds.empty()) {
-                    std::string mx = "f" + std::to_string(preds[0]);
-                    for (size_t k = 1; k < preds.size(); ++k)
-                        mx = "fmaxf(" + mx + ", f" + std::to_string(preds[k]) + ")";
-                    o << " + " << mx;
-                }
-                o << "; \\\n";
-            }
+            if (!D.obj)
+                for (int n = n0; n < m; ++n)
+                    o << (n == 0 ? "  c = e0.x; \\\n" : "  c = c * e") << (n == 0 ? "" : std::to_string(n) + ".x; \\\n");
+            emit_recurrence(o, D, n0, m);
             if (m < N) {
                 std::string lb;
                 for (int n = 0; n < m; ++n) {
@@ -249,20 +289,27 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
             }
             n0 = m;
         }
-        bool first = true;
-        for (int n = 0; n < N; ++n) {
-            if (!(D.sinks >> n & 1u)) continue;
-            o << (first ? "  cp = f" : "  cp = fmaxf(cp, f") << n << (first ? "; \\\n" : "); \\\n");
-            first = false;
+        if (D.obj) {
+            emit_obj_sums(o, D, 0, N);
+            emit_sinks(o, D, "t_", true);
+            o << "  c = fmaf(-DY_LAM, t_, u_); \\\n  cp = d_; \\\n";
+        } else {
+            emit_sinks(o, D, "cp", false);
         }
     }
+    // objective mode: c = G, cp = D, and a level's exact test is its one-rounding
+    // estimate fma(-m_k, D, G) against its threshold
     o << R"(  const float th = s_bins[(__float_as_uint(cp) >> bin_shift) & 63u]; \
   bool want = ok && c >= th; \
   if (__builtin_amdgcn_ballot_w64(want)) { \
     if (want) { \
       bool w2 = false; \
-      for (int k = 0; k < DY_K; ++k) if (cp <= hi[k] && c >= thr[k]) w2 = true; \
-      want = w2; \
+)";
+    if (D.obj)
+        o << "      for (int k = 0; k < DY_K; ++k) if (fma(-dy_m64[k], (double)cp, (double)c) >= (double)thr[k]) w2 = true; \\\n";
+    else
+        o << "      for (int k = 0; k < DY_K; ++k) if (cp <= hi[k] && c >= thr[k]) w2 = true; \\\n";
+    o << R"(      want = w2; \
     } \
     const unsigned long long m_ = __builtin_amdgcn_ballot_w64(want); \
     if (m_) { \
@@ -355,7 +402,12 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
 
 )";
     // seeding pass: hashed sample rows, grid-stride; per level the largest
-    // certified corr (ordered bits + 1) of the thread, reduced per wave at the end
+    // certified corr (ordered bits + 1) of the thread, reduced per wave at the
+    // end; objective mode: the largest estimate fma(-m_k, D, G) (ordered key)
+    if (D.obj)
+        o << "#define DY_SEED_UPDATE(k) best[k] = max(best[k], dy_fkey(fmaf(-dy_m32[k], cp, c)))\n";
+    else
+        o << "#define DY_SEED_UPDATE(k) if (cp <= lo[k]) best[k] = max(best[k], __float_as_uint(c) + 1u)\n";
     o << R"(extern "C" __global__ void __launch_bounds__(256) dy_rows_sample(
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count,
     const float2* __restrict__ at, int rmax, const float* __restrict__ lo,
@@ -375,7 +427,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
     DY_EVAL()" << wl("w") << R"(, c, cp, bad)
     if (!bad)
       for (int k = 0; k < DY_K; ++k)
-        if (cp <= lo[k]) best[k] = max(best[k], __float_as_uint(c) + 1u);
+        DY_SEED_UPDATE(k);
   }
   for (int k = 0; k < DY_K; ++k) {
     const unsigned e = dy_wmax(best[k]);

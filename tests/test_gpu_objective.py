@@ -301,3 +301,18 @@ def test_score_range_and_rows():
         U, T, Dd, J = orc.obj_score(prob, obj, rows=rows)
         check_scores(prob, obj, U, T, Dd, J, u.cpu().numpy(), j.cpu().numpy(), d.cpu().numpy(),
                      f.cpu().numpy().astype(np.uint32))
+
+
+def test_rows_generated_kernel_matches_generic_path():
+    # the DAG-specialised rows kernels and the generic per-plan path agree
+    prob = wl.stream24()
+    obj = with_tools(wl.paper_objective(prob, levels=(0.0, 0.7, 1.5, 3.0, 6.0)), 24, (2, 11))
+    n = 1 << 20
+    rows = wl.make_rows(n, 24, 36, row_begin=777)
+    want = orc.obj_select_rows(prob, obj, rows, index_base=5)
+    d = torch.from_numpy(rows).cuda()
+    for jit in (1, 0):
+        with D.Plan((prob, obj)) as plan:
+            plan.set_option(D.DY_OPT_JIT, jit)
+            got = plan.select([D.rows_source(0, d, n, 24, 5)], stream=stream())[0]
+        assert_obj_choices(got, want, f"rows jit={jit}")
