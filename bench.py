@@ -203,6 +203,8 @@ def main():
                     choices=["chain4", "forkjoin8", "layered10", "batch6", "stream24"])
     ap.add_argument("--objective", action="store_true",
                     help="the paper's additive objective J_L (levels 0, 1.5, 3) instead of corr / SLO")
+    ap.add_argument("--pressure", choices=["level", "per-class"], default="level",
+                    help="per-class: the second backend pressed at half the level's rho (per-backend pressure)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=1 << 26)
     ap.add_argument("--sample-stride", type=int, default=0)
@@ -212,7 +214,7 @@ def main():
     ap.add_argument("--calib-bytes", type=int, default=1 << 30)
     ap.add_argument("--pmc-command", action="append", default=[], help="command that produced a database")
     args = ap.parse_args()
-    tkey = args.workload + ("_obj" if args.objective else "")
+    tkey = args.workload + ("_obj" if args.objective else "") + ("_perclass" if args.pressure == "per-class" else "")
     if args.ingest_pmc:
         ingest_pmc(tkey, *args.ingest_pmc, args.calib_bytes, args.pmc_command)
         return
@@ -259,6 +261,8 @@ def main():
         else:
             plans = wl.LAYERED_RANGE if name == "layered10" else probs[0].n_plans()
             sources = [D.range_source(0, 0, plans)]
+    if args.pressure == "per-class":
+        probs = [wl.per_class(p) for p in probs]
     prob = probs[0]
     K = prob.n_levels
     objs = None
@@ -338,7 +342,8 @@ def main():
         "config": {"workload": name, "plans": plans, "nodes": prob.n_nodes, "edges": edge_count(prob),
                    "impls_per_node": int(prob.radix[0]), "levels": K,
                    "problems": len(probs), "parallelism": "single GPU",
-                   "selection": "paper objective J_L, L in {0, 1.5, 3}" if objs else "max corr s.t. CP_k <= SLO"},
+                   "selection": "paper objective J_L, L in {0, 1.5, 3}" if objs else "max corr s.t. CP_k <= SLO",
+                   "pressure": "per-class (backend 1 at rho_k / 2)" if args.pressure == "per-class" else "per level"},
         "roofline": roof,
         "stage_ms": stage_ms,
         "ms_per_step_timed": ms_per_step_timed,

@@ -86,6 +86,13 @@ struct ProbDev {
     double err2[KMAX];        // twice a bound on |estimate - J_k| for every fp32 estimate of a plan's J_k
     const float* demx;        // rows of x and y in `dem` (x: a 1-entry 0 row when virtual)
     const float* demy;
+    // Per-backend pressure (uniform == 0): lo / hi are bands on the fp32
+    // unpressured CP implied by every level's largest / smallest multiplier
+    // (a conservative prefilter, as in uniform mode); glo / ghi are the bands
+    // of the exact per-level test on the fp32 CP_k itself.
+    float glo, ghi;
+    float ay_max;             // largest factor a of node y (fp32 table)
+    float ty_min;             // smallest duration tau of node y
 };
 
 struct Cand {

@@ -624,21 +624,25 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
             for (int n = 0; n < N; ++n)
                 for (int i = 0; i < pb.radix[n]; ++i) used |= 1ull << pb.backend[(size_t)n * R + i];
         bool uniform = true;
-        std::vector<double> rho_k(K, 0.0);
+        std::vector<double> rho_k(K, 0.0), rho_lo(K, 0.0), rho_hi(K, 0.0);
         for (int k = 0; k < K && !obj; ++k) {
             bool first = true;
-            float r0 = 0.0f;
+            float r0 = 0.0f, rl = 0.0f, rh = 0.0f;
             for (int b = 0; b < B; ++b) {
                 if (!(used >> b & 1ull)) continue;
                 float r = pb.rho[k * B + b];
                 if (first) {
-                    r0 = r;
+                    r0 = rl = rh = r;
                     first = false;
-                } else if (f2u(r) != f2u(r0)) {
-                    uniform = false;
+                } else {
+                    if (f2u(r) != f2u(r0)) uniform = false;
+                    rl = std::min(rl, r);
+                    rh = std::max(rh, r);
                 }
             }
             rho_k[k] = (double)r0;
+            rho_lo[k] = (double)rl;
+            rho_hi[k] = (double)rh;
         }
         D.uniform = uniform ? 1 : 0;
         D.slo = obj ? INFINITY : (double)pb.slo;
@@ -656,11 +660,15 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
                 D.hi[k] = round_up(th * (1.0 + (N + 1) * kU));
                 D.mk[k] = (float)(1.0 / (1.0 - rho_k[k]));
             } else {
-                D.lo[k] = round_down(slo * (1.0 - (N + 2) * kU));
-                D.hi[k] = round_up(slo * (1.0 + (N + 2) * kU));
+                // CP_k <= CP_0 / (1 - largest rho of the level) and >= CP_0 / (1 - smallest):
+                // bands on the unpressured CP, widened like the per-level ones
+                D.lo[k] = round_down(slo * (1.0 - rho_hi[k]) * (1.0 - (N + 2) * kU));
+                D.hi[k] = round_up(slo * (1.0 - rho_lo[k]) * (1.0 + (N + 2) * kU));
                 D.mk[k] = 1.0f;
             }
         }
+        D.glo = round_down(slo * (1.0 - (N + 2) * kU));
+        D.ghi = round_up(slo * (1.0 + (N + 2) * kU));
         // tables
         float2* at = (float2*)(img.data() + L.at);
         float* dem = (float*)(img.data() + L.dem);
@@ -733,7 +741,8 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         // every CP in the bin certainly meets (decided by the bin's largest CP)
         std::vector<int> order(K);
         for (int k = 0; k < K; ++k) order[k] = k;
-        std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return D.lo[x] > D.lo[y]; });
+        if (uniform)
+            std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return D.lo[x] > D.lo[y]; });
         for (int k = 0; k < K; ++k) D.lvl_order[k] = order[k];
         const uint32_t blo = D.cp_lo_bits >> s;
         for (int lane = 0; lane < NBINS && !obj; ++lane) {
@@ -757,6 +766,13 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         D.a64 = (const double*)(base + L.a64);
         D.lat64 = (const double*)(base + L.lat64);
         D.dem64 = (const double*)(base + L.dem64);
+        D.ay_max = 0.0f;
+        D.ty_min = INFINITY;
+        for (int i = 0; i < pb.radix[N - 1]; ++i) {
+            const float2 v = ((const float2*)(img.data() + L.at))[(size_t)(N - 1) * R + i];
+            D.ay_max = std::max(D.ay_max, v.x);
+            D.ty_min = std::min(D.ty_min, v.y);
+        }
         D.demx = N >= 2 ? D.dem + (size_t)(N - 2) * R : (const float*)(base + L.dz);
         D.demy = D.dem + (size_t)(N - 1) * R;
         H.n = N;
@@ -1123,7 +1139,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     for (int j = 0; j < n_src; ++j) {
         const int p = src[j].problem;
         const HostProb& H = h->hp[p];
-        if (src[j].kind == DY_SOURCE_RANGE && H.uniform)
+        if (src[j].kind == DY_SOURCE_RANGE)
             grp[j] = H.obj ? (H.has_s2 ? G_OSWEEP_S2 : G_OSWEEP) : (H.has_s2 ? G_SWEEP_S2 : G_SWEEP);
         else if (src[j].kind == DY_SOURCE_ROWS && H.uniform && !h->force_fp64 && jit_ready(h, p))
             grp[j] = G_JIT;
@@ -1307,7 +1323,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
                 if (grp[j] != g) continue;
                 const HostProb& H = h->hp[src[j].problem];
                 JobDev J = jobs[q];
-                if (round < kReseedRounds && H.uniform) {
+                if (round < kReseedRounds) {
                     ++rp.n[g];
                     if (g < G_JIT) rp.units[g] = std::max(rp.units[g], J.units);
                     if (g < kSweepGroups) rp.npre[g] = std::max(rp.npre[g], H.npre);
@@ -1325,7 +1341,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         std::memcpy(S.h_fb + n_re, ex.data(), (size_t)n_ex * sizeof(JobDev));
         chk(hipMemcpyAsync(S.d_fb, S.h_fb, (size_t)(n_re + n_ex) * sizeof(JobDev), hipMemcpyHostToDevice, s),
             "copy fb");
-        if (n_re > 0) {  // every overflowing uniform source is rescored
+        if (n_re > 0) {  // every overflowing source is rescored
             for (int c = 0; c < n_re; c += 65535)
                 chk(launch_reseed(S.d_fb + c, std::min(65535, n_re - c), s), "reseed");
             launch_table_all(S.d_fb, n_re, s, chk);

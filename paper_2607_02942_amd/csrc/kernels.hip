@@ -516,6 +516,120 @@ __device__ __forceinline__ uint64_t sweep_test(const float2 vy, float M, float S
     return __ballot(cc >= thr);
 }
 
+// Per-backend pressure (not uniform): the level-k state of a row of the
+// sweep, for the exact per-level tests of the seeding pass and of the rare
+// path.  `dg` holds the prefix digits of the block.  NPRE > 0: the prefix has
+// exactly NPRE nodes, the recurrence is unrolled with every f_n in a register;
+// NPRE == 0: any length, f_n in the thread's LDS column s_f.  Returns M (the
+// path into y other than through y's own duration) and S2 (the longest path
+// ending at another sink), as the sweep forms them at level 0.
+template <int NPRE>
+__device__ void level_row(PD P, const CS float* lat, const uint32_t* dg, uint64_t b, int big, int ix,
+                          float* __restrict__ s_f, float& M, float& S2) {
+    const int R = P->rmax, xn = P->xnode;
+    const uint32_t pmx = xn >= 0 ? P->pred[xn] : 0u;
+    const uint32_t pmy = P->pred[P->ynode] & (xn >= 0 ? ~(1u << xn) : ~0u);
+    float px = 0.0f, py = 0.0f, s = 0.0f;
+    if constexpr (NPRE > 0) {
+        float f[NPRE];
+#pragma unroll
+        for (int n = 0; n < NPRE; ++n) {
+            float m = 0.0f;
+            const uint32_t pm = P->pred[n];
+#pragma unroll
+            for (int u = 0; u < n; ++u)
+                if (pm >> u & 1u) m = fmaxf(m, f[u]);
+            f[n] = lat[n * R + dg[n]] + m;
+        }
+#pragma unroll
+        for (int u = 0; u < NPRE; ++u) {
+            if (pmx >> u & 1u) px = fmaxf(px, f[u]);
+            if (pmy >> u & 1u) py = fmaxf(py, f[u]);
+            if (P->pre_sinks >> u & 1u) s = fmaxf(s, f[u]);
+        }
+    } else {
+        const int tid = threadIdx.x;
+        for (int n = 0; n < P->npre; ++n) {
+            const uint32_t d = prefix_digit(P, n, b, big);
+            float m = 0.0f;
+            uint32_t pm = P->pred[n];
+            while (pm) {
+                const int u = __builtin_ctz(pm);
+                pm &= pm - 1;
+                m = fmaxf(m, s_f[u * WG + tid]);
+            }
+            s_f[n * WG + tid] = lat[n * R + d] + m;
+        }
+        auto pmax = [&](uint32_t pm) {
+            float v = 0.0f;
+            while (pm) {
+                const int u = __builtin_ctz(pm);
+                pm &= pm - 1;
+                v = fmaxf(v, s_f[u * WG + tid]);
+            }
+            return v;
+        };
+        px = pmax(pmx);
+        py = pmax(pmy);
+        s = pmax(P->pre_sinks);
+    }
+    const float fx = (xn >= 0 ? lat[xn * R + ix] : 0.0f) + px;
+    const bool exy = P->edge_xy != 0;
+    M = exy ? fmaxf(py, fx) : py;
+    S2 = exy ? s : fmaxf(s, fx);
+}
+
+template <int NPRE>
+__device__ __forceinline__ void prefix_digits(PD P, uint64_t b, int big, uint32_t* dg) {
+    if constexpr (NPRE > 0) {
+#pragma unroll
+        for (int n = 0; n < NPRE; ++n) dg[n] = prefix_digit(P, n, b, big);
+    }
+}
+
+// Rare path of the sweep under per-backend pressure: every plan of this
+// lane's row that some level admits exactly in fp32 (CP_k <= ghi and corr >=
+// T_k) goes to the candidate list once (with its unpressured CP, the value the
+// bands of the list refer to).  A level is skipped when no plan of the row
+// can reach its threshold (cx times the largest factor of y) or its band on
+// the unpressured CP (the row's smallest unpressured CP).  R_y > 64 may list
+// a plan once per level.
+template <bool HAS_S2, int NPRE>
+__device__ void general_row(PD P, JD J, uint64_t b, int big, int ix, float cx, float M0, float S20,
+                            float* __restrict__ s_f) {
+    const int N = P->n, R = P->rmax, ry = P->ry;
+    const uint64_t base = (b * (uint64_t)P->rx + (uint64_t)ix) * (uint64_t)ry;
+    const CS float2* aty = cs(P->aty);
+    uint32_t dg[NPRE > 0 ? NPRE : 1];
+    prefix_digits<NPRE>(P, b, big, dg);
+    const float cmax = cx * P->ay_max;
+    float cp0_lb = P->ty_min + M0;
+    if (HAS_S2) cp0_lb = fmaxf(cp0_lb, S20);
+    uint64_t done = 0;
+    for (int k = 0; k < P->k; ++k) {
+        const float thr = J->thr[k];
+        if (!(cmax >= thr && cp0_lb <= P->hi[k])) continue;
+        const CS float* lat = cs(P->lat) + (size_t)k * N * R;
+        float M, S2;
+        level_row<NPRE>(P, lat, dg, b, big, ix, s_f, M, S2);
+        const CS float* laty = lat + P->ynode * R;
+        for (int iy = 0; iy < ry; ++iy) {
+            if (ry <= 64 && (done >> iy & 1ull)) continue;
+            float cp = laty[iy] + M;
+            if (HAS_S2) cp = fmaxf(cp, S2);
+            const float2 vy = aty[iy];
+            const float cc = cx * vy.x;
+            const uint64_t idx = base + (uint64_t)iy;
+            if (cp <= P->ghi && cc >= thr && idx - J->begin < J->count) {
+                float cp0 = vy.y + M0;
+                if (HAS_S2) cp0 = fmaxf(cp0, S20);
+                append_cand(J, idx, cc, cp0);
+                if (ry <= 64) done |= 1ull << iy;
+            }
+        }
+    }
+}
+
 // RY > 0: every source of the launch has R_y = RY; the y table is loaded once
 // per workgroup into scalar registers and the y loop is fully unrolled, so the
 // inner sweep issues no memory load and no wait other than its LDS bin reads.
@@ -570,7 +684,9 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
         if (hit) {
             // rare: re-score this lane's row of the inner sweep with the exact test
             const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
-            if (live && (hit >> (threadIdx.x & 63) & 1ull)) {
+            if (live && (hit >> (threadIdx.x & 63) & 1ull) && !P->uniform) {
+                general_row<HAS_S2, NPRE>(P, J, b, J->big, ix, cx, M, S2, s_f);
+            } else if (live && (hit >> (threadIdx.x & 63) & 1ull)) {
                 for (int iy = 0; iy < ry; ++iy) {
                     const float2 vy = aty[iy];
                     float cp = vy.y + M;
@@ -648,6 +764,34 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
     __syncthreads();
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* aty = cs(P->aty);
+    if (!P->uniform) {
+        // per-backend pressure: each level's exact fp32 CP_k; certainly
+        // feasible when CP_k <= glo (level k writes bucket k, no suffix maximum)
+        uint32_t dg[NPRE > 0 ? NPRE : 1];
+        prefix_digits<NPRE>(P, b, J->big, dg);
+        for (int k = 0; k < K; ++k) {
+            const CS float* lat = cs(P->lat) + (size_t)k * P->n * P->rmax;
+            float Mk, S2k;
+            level_row<NPRE>(P, lat, dg, b, J->big, ix, s_f, Mk, S2k);
+            const CS float* laty = lat + P->ynode * P->rmax;
+            float best = -1.0f;
+            for (int iy = 0; iy < ry; ++iy) {
+                float cp = laty[iy] + Mk;
+                if (HAS_S2) cp = fmaxf(cp, S2k);
+                if (cp <= P->glo && live && (base + (uint64_t)iy - J->begin < J->count))
+                    best = fmaxf(best, cx * aty[iy].x);
+            }
+            const uint32_t e = wave_max_u32(best >= 0.0f ? __float_as_uint(best) + 1u : 0u);
+            if (lane == 0) s_red[k][wave] = e;
+        }
+        __syncthreads();
+        if (tid < K) {
+            uint32_t e = 0;
+            for (int w = 0; w < WG / 64; ++w) e = max(e, s_red[tid][w]);
+            if (e) atomicMax(J->scert + tid * NSLOT + (blockIdx.x % NSLOT), e);
+        }
+        return;
+    }
     for (int iy = 0; iy < ry; ++iy) {
         const float2 vy = aty[iy];
         float cp = vy.y + M;
@@ -1037,7 +1181,7 @@ __global__ void __launch_bounds__(WG) k_sample_generic(const JobDev* __restrict_
 #pragma unroll 1
     for (int k = 0; k < K; ++k) {
         const float cp = P->uniform ? cp0 : eval_cp_level(P, s_id, s_f, k);
-        uint32_t e = (ok && cp <= P->lo[k]) ? __float_as_uint(cc) + 1u : 0u;
+        uint32_t e = (ok && cp <= (P->uniform ? P->lo[k] : P->glo)) ? __float_as_uint(cc) + 1u : 0u;
         e = wave_max_u32(e);
         if ((threadIdx.x & 63) == 0 && e)
             atomicMax(J->scert + k * NSLOT + ((blockIdx.x * (WG / 64) + (threadIdx.x >> 6)) % NSLOT), e);
@@ -1071,19 +1215,17 @@ __global__ void __launch_bounds__(WG) k_scan(const JobDev* __restrict__ jobs, ui
         const float thr = __uint_as_float(J->table[(__float_as_uint(cp) >> (uint32_t)P->bin_shift) & 63u]);
         if (live && !bad && cc >= thr && is_candidate(P, J, cp, cc)) append_cand(J, idx, cc, cp);
     } else {
-        const float cc = eval_corr(P, s_id);
+        // per-backend pressure: the unpressured CP's bands first (a conservative
+        // prefilter), then each level's exact fp32 CP_k; the candidate keeps the
+        // unpressured CP, which the list's bands refer to
+        float cc, cp0;
+        eval_uniform(P, s_id, s_f, cc, cp0);
+        const float thr = __uint_as_float(J->table[(__float_as_uint(cp0) >> (uint32_t)P->bin_shift) & 63u]);
         bool want = false;
-        float cp_first = 0.0f;
-        for (int k = 0; k < P->k; ++k) {
-            const float cp = eval_cp_level(P, s_id, s_f, k);
-            if (cp <= P->hi[k] && cc >= J->thr[k]) {
-                if (!want) cp_first = cp;
-                want = true;
-            }
-        }
-        // general mode stores the CP of the first qualifying level; certification
-        // recomputes every level in fp64, so only the index matters
-        if (live && !bad && want) append_cand(J, idx, cc, cp_first);
+        if (live && !bad && cc >= thr && is_candidate(P, J, cp0, cc))
+            for (int k = 0; k < P->k && !want; ++k)
+                if (cc >= J->thr[k]) want = eval_cp_level(P, s_id, s_f, k) <= P->ghi;
+        if (want) append_cand(J, idx, cc, cp0);
     }
 }
 
@@ -1218,7 +1360,6 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
     if (g >= J->cert_waves || k >= P->k) return;
     const int N = P->n, R = P->rmax, lane = threadIdx.x;
     const uint32_t nc = min(*J->ncand, J->cap);
-    const bool general = !P->uniform;
     uint8_t* ids = s_id + lane;
     double* f = s_f + lane;
     const size_t NR = (size_t)N * R;
@@ -1296,16 +1437,15 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
     } else {
         const float lo = P->lo[k], hi = P->hi[k];
         float sb = sl ? __uint_as_float(sl - 1u) : -1.0f;
-        if (!general)
-            for (uint32_t i = lane; i < nc; i += 64) {
-                const Cand c = i < ncache ? s_cand[i] : J->cand[i];
-                if (c.cp <= lo) sb = fmaxf(sb, c.corr);
-            }
+        for (uint32_t i = lane; i < nc; i += 64) {
+            const Cand c = i < ncache ? s_cand[i] : J->cand[i];
+            if (c.cp <= lo) sb = fmaxf(sb, c.corr);
+        }
         const uint32_t e = wave_max_u32(sb >= 0.0f ? __float_as_uint(sb) + 1u : 0u);
         const float T = cand_threshold(e ? __uint_as_float(e - 1u) : -1.0f, N);
         for (uint32_t i = (uint32_t)g * 64u + lane; i < nc; i += step) {
             const Cand c = i < ncache ? s_cand[i] : J->cand[i];
-            if (!(c.corr >= T && (general || c.cp <= hi))) continue;
+            if (!(c.corr >= T && c.cp <= hi)) continue;
             if (!job_ids(J, P, c.index, ids, 64)) continue;
             double corr = 1.0;
             for (int n = 0; n < N; ++n) corr = corr * a64[n * R + ids[n * 64]];
@@ -1512,10 +1652,11 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
     bool have_ids = false;
     for (int k = 0; k < K; ++k) {
         const float cpc = P->uniform ? cp0 : eval_cp_level(P, s_id, s_f, k);
+        const float lo = P->uniform ? P->lo[k] : P->glo, hi = P->uniform ? P->hi[k] : P->ghi;
         bool f;
-        if (cpc <= P->lo[k]) {
+        if (cpc <= lo) {
             f = true;
-        } else if (!(cpc <= P->hi[k])) {
+        } else if (!(cpc <= hi)) {
             f = false;
         } else {  // too close to the SLO for fp32: decide in fp64
             if (!have_ids) {

@@ -418,3 +418,15 @@ def make_rows_numpy(n_rows: int, n_nodes: int, radix: int, row_begin: int = 0,
 def by_name(name: str) -> Problem:
     return {"chain4": chain4, "forkjoin8": forkjoin8, "layered10": layered10,
             "stream24": stream24}[name]()
+
+
+def per_class(prob: Problem, factors=(1.0, 0.5)) -> Problem:
+    """The problem under per-backend pressure: at level k backend b gets
+    factors[b] * rho_k (rho_k = the level's value, backend 0's column), a
+    synthetic stand-in for the per-class load the runtime reads from the
+    serving backends (Sec. 5.2).  The default presses the second backend half
+    as hard as the first."""
+    p = prob.copy()
+    base = prob.rho[:, 0].astype(np.float64)
+    p.rho = np.stack([base * f for f in factors], axis=1).astype(np.float32)
+    return p
