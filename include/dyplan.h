@@ -259,6 +259,47 @@ const char* dy_plan_last_error(const dy_plan* h);
 const char* dy_status_str(int status);
 int32_t dy_abi_version(void);
 
+/*
+ * Suffix recompilation (Appendix "Suffix Recompilation and Its Timing Scope",
+ * eq. suffix-repair).  After a successful bounded recovery the committed
+ * nodes C_t (completed or in flight: their bindings are fixed) leave the
+ * choice, and the undispatched nodes U_t are selected again on the residual
+ * DAG G_t = G[U_t], whose makespan starts from zero; the updated plan is the
+ * committed bindings joined with the suffix's.  Host-only calls (no HIP).
+ *
+ * dy_suffix_create   residual problem of `full` for committed[N] (nonzero =
+ *                    committed): the nodes of U_t in their original order
+ *                    (still topological), the edges between two of them, their
+ *                    table rows; objective mode keeps the weights and levels
+ *                    and takes the nodes' cost rows and tool flags (reach
+ *                    weights then follow G_t, as for any problem); corr / SLO
+ *                    problems keep levels, pressures and SLO.  The handle owns
+ *                    copies of everything.  Fails with the status of
+ *                    dy_plan_create's checks for an invalid `full`, DY_EINVAL
+ *                    for NULL arguments or when every node is committed
+ *                    (nothing to recompile); dy_plan_last_error(NULL) then
+ *                    describes the failure.
+ * dy_suffix_problem  the residual problem, valid until dy_suffix_destroy: stage
+ *                    it with dy_plan_create and select as usual.
+ * dy_suffix_nodes    its node count; node_map (if not NULL, [count]) receives
+ *                    the full node of each residual node.
+ * dy_suffix_merge    impl_out[N] (host) = committed_impl[n] for committed n,
+ *                    else the implementation that residual plan index
+ *                    `residual_index` (mixed radix over the residual nodes,
+ *                    first node most significant) gives the node; *full_index
+ *                    (if not NULL) = the merged plan's index in `full`, or -1
+ *                    when it exceeds 2^63 - 1.  DY_EINVAL for NULL arguments, a
+ *                    committed id outside [0, radix) or an index outside the
+ *                    residual plan space; the two domains never overlap.
+ */
+typedef struct dy_suffix dy_suffix; /* opaque */
+int dy_suffix_create(const dy_problem* full, const uint8_t* committed, dy_suffix** out);
+const dy_problem* dy_suffix_problem(const dy_suffix* s);
+int32_t dy_suffix_nodes(const dy_suffix* s, int32_t* node_map);
+int dy_suffix_merge(const dy_suffix* s, const int32_t* committed_impl, int64_t residual_index, int32_t* impl_out,
+                    int64_t* full_index);
+void dy_suffix_destroy(dy_suffix* s);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1418,3 +1418,163 @@ int dy_selftest(void) {
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// suffix recompilation: the residual problem on G[U_t] and the merge
+// ---------------------------------------------------------------------------
+
+struct dy_suffix {
+    std::vector<int32_t> map;          // residual node -> full node
+    std::vector<int32_t> full_radix;
+    std::vector<int32_t> edges, radix, backend, is_tool;
+    std::vector<float> p, tau, size, w, rho, cost, levels;
+    dy_objective obj{};
+    dy_problem prob{};
+};
+
+extern "C" {
+
+int dy_suffix_create(const dy_problem* full, const uint8_t* committed, dy_suffix** out) {
+    if (!out) {
+        g_create_error = "out is NULL";
+        return DY_EINVAL;
+    }
+    *out = nullptr;
+    if (!full || !committed) {
+        g_create_error = "full or committed is NULL";
+        return DY_EINVAL;
+    }
+    std::string err;
+    const int st = validate_problem(*full, 0, &err);
+    if (st != DY_OK) {
+        g_create_error = err;
+        return st;
+    }
+    dy_suffix* S = new (std::nothrow) dy_suffix;
+    if (!S) {
+        g_create_error = "out of host memory";
+        return DY_ENOMEM;
+    }
+    try {
+        const int N = full->n_nodes, R = full->max_radix;
+        const bool obj = full->objective != nullptr;
+        std::vector<int> rid(N, -1);
+        for (int n = 0; n < N; ++n) {
+            S->full_radix.push_back(full->radix[n]);
+            if (!committed[n]) {
+                rid[n] = (int)S->map.size();
+                S->map.push_back(n);
+            }
+        }
+        const int M = (int)S->map.size();
+        if (M == 0) {
+            delete S;
+            g_create_error = "every node is committed: nothing to recompile";
+            return DY_EINVAL;
+        }
+        // edges between undispatched nodes; the renumbering keeps u < v
+        for (int e = 0; e < full->n_edges; ++e) {
+            const int u = rid[full->edges[2 * e]], v = rid[full->edges[2 * e + 1]];
+            if (u >= 0 && v >= 0) {
+                S->edges.push_back(u);
+                S->edges.push_back(v);
+            }
+        }
+        auto rows = [&](const float* t, std::vector<float>& dst) {
+            for (int r = 0; r < M; ++r) dst.insert(dst.end(), t + (size_t)S->map[r] * R, t + (size_t)(S->map[r] + 1) * R);
+        };
+        for (int r = 0; r < M; ++r) {
+            S->radix.push_back(full->radix[S->map[r]]);
+            S->w.push_back(full->w[S->map[r]]);
+        }
+        rows(full->p, S->p);
+        rows(full->tau, S->tau);
+        dy_problem& P = S->prob;
+        P.n_nodes = M;
+        P.n_edges = (int32_t)(S->edges.size() / 2);
+        P.radix = S->radix.data();
+        P.max_radix = R;
+        P.w = S->w.data();
+        if (!obj) {
+            rows(full->size, S->size);
+            for (int r = 0; r < M; ++r)
+                S->backend.insert(S->backend.end(), full->backend + (size_t)S->map[r] * R,
+                                  full->backend + (size_t)(S->map[r] + 1) * R);
+            S->rho.assign(full->rho, full->rho + (size_t)full->n_levels * full->n_backends);
+            P.size = S->size.data();
+            P.backend = S->backend.data();
+            P.n_levels = full->n_levels;
+            P.n_backends = full->n_backends;
+            P.rho = S->rho.data();
+            P.slo = full->slo;
+        } else {
+            const dy_objective& o = *full->objective;
+            rows(o.cost, S->cost);
+            if (o.is_tool)
+                for (int r = 0; r < M; ++r) S->is_tool.push_back(o.is_tool[S->map[r]]);
+            S->levels.assign(o.levels, o.levels + o.n_levels);
+            S->obj = o;
+            S->obj.cost = S->cost.data();
+            S->obj.is_tool = o.is_tool ? S->is_tool.data() : nullptr;
+            S->obj.levels = S->levels.data();
+            P.objective = &S->obj;
+            P.slo = full->slo;
+        }
+        P.edges = S->edges.empty() ? nullptr : S->edges.data();
+        P.p = S->p.data();
+        P.tau = S->tau.data();
+    } catch (const std::bad_alloc&) {
+        delete S;
+        g_create_error = "out of host memory";
+        return DY_ENOMEM;
+    }
+    *out = S;
+    return DY_OK;
+}
+
+const dy_problem* dy_suffix_problem(const dy_suffix* s) { return s ? &s->prob : nullptr; }
+
+int32_t dy_suffix_nodes(const dy_suffix* s, int32_t* node_map) {
+    if (!s) return 0;
+    if (node_map)
+        for (size_t r = 0; r < s->map.size(); ++r) node_map[r] = s->map[r];
+    return (int32_t)s->map.size();
+}
+
+int dy_suffix_merge(const dy_suffix* s, const int32_t* committed_impl, int64_t residual_index, int32_t* impl_out,
+                    int64_t* full_index) {
+    if (!s || !impl_out || residual_index < 0) return DY_EINVAL;
+    const int N = (int)s->full_radix.size(), M = (int)s->map.size();
+    std::vector<char> free_node(N, 0);
+    for (int r = 0; r < M; ++r) free_node[s->map[r]] = 1;
+    for (int n = 0; n < N; ++n) {
+        if (free_node[n]) continue;
+        if (!committed_impl || committed_impl[n] < 0 || committed_impl[n] >= s->full_radix[n]) return DY_EINVAL;
+    }
+    // decode the residual index (last residual node least significant)
+    uint64_t x = (uint64_t)residual_index;
+    std::vector<int32_t> suffix(M);
+    for (int r = M - 1; r >= 0; --r) {
+        const uint64_t rad = (uint64_t)s->radix[r];
+        suffix[r] = (int32_t)(x % rad);
+        x /= rad;
+    }
+    if (x != 0) return DY_EINVAL;
+    for (int n = 0; n < N; ++n)
+        if (!free_node[n]) impl_out[n] = committed_impl[n];
+    for (int r = 0; r < M; ++r) impl_out[s->map[r]] = suffix[r];
+    if (full_index) {
+        unsigned __int128 idx = 0;
+        bool over = false;
+        for (int n = 0; n < N && !over; ++n) {
+            idx = idx * (unsigned)s->full_radix[n] + (unsigned)impl_out[n];
+            over = idx > (unsigned __int128)INT64_MAX;
+        }
+        *full_index = over ? -1 : (int64_t)idx;
+    }
+    return DY_OK;
+}
+
+void dy_suffix_destroy(dy_suffix* s) { delete s; }
+
+}  // extern "C"

@@ -25,7 +25,8 @@ DY_MAX_NODES, DY_MAX_RADIX, DY_MAX_LEVELS, DY_MAX_BACKENDS = 32, 255, 32, 64
 
 EXPORTED = ("dy_plan_create", "dy_plan_select", "dy_plan_score", "dy_plan_destroy", "dy_plan_max_levels",
             "dy_plan_num_problems", "dy_plan_set_option", "dy_plan_get_stats", "dy_plan_last_error",
-            "dy_status_str", "dy_abi_version", "dy_selftest")
+            "dy_status_str", "dy_abi_version", "dy_selftest", "dy_suffix_create", "dy_suffix_problem",
+            "dy_suffix_nodes", "dy_suffix_merge", "dy_suffix_destroy")
 
 
 class DyObjective(ctypes.Structure):
@@ -78,11 +79,21 @@ _lib = None
 
 
 def lib():
-    """Load libdyplan.so (raises if it has not been built)."""
+    """Load libdyplan.so (raises if it has not been built).
+
+    When PyTorch is installed it is imported first: its bundled HIP runtime
+    carries this library's runtime soname, so the process then holds one HIP
+    runtime.  Loaded the other way round, torch's libraries (which name the
+    runtime without the version suffix) would load a second copy beside the
+    system one, and the two disagree about the device."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         vp, i32 = ctypes.c_void_p, ctypes.c_int32
         L.dy_plan_create.argtypes = [ctypes.POINTER(DyProblem), i32, i32, ctypes.POINTER(vp)]
@@ -107,6 +118,16 @@ def lib():
         L.dy_status_str.restype = ctypes.c_char_p
         L.dy_abi_version.restype = i32
         L.dy_selftest.restype = ctypes.c_int
+        L.dy_suffix_create.argtypes = [ctypes.POINTER(DyProblem), vp, ctypes.POINTER(vp)]
+        L.dy_suffix_create.restype = ctypes.c_int
+        L.dy_suffix_problem.argtypes = [vp]
+        L.dy_suffix_problem.restype = ctypes.POINTER(DyProblem)
+        L.dy_suffix_nodes.argtypes = [vp, vp]
+        L.dy_suffix_nodes.restype = i32
+        L.dy_suffix_merge.argtypes = [vp, vp, ctypes.c_int64, vp, ctypes.POINTER(ctypes.c_int64)]
+        L.dy_suffix_merge.restype = ctypes.c_int
+        L.dy_suffix_destroy.argtypes = [vp]
+        L.dy_suffix_destroy.restype = None
         _lib = L
     return _lib
 
@@ -192,16 +213,19 @@ class Plan:
     problem is a workload.Problem (corr / SLO selection) or a pair (Problem,
     Objective) for the paper's additive objective."""
 
-    def __init__(self, problems, device: int = 0):
-        if isinstance(problems, tuple) and len(problems) == 2 and hasattr(problems[1], "levels"):
-            problems = [problems]
-        probs = list(problems) if isinstance(problems, (list, tuple)) else [problems]
-        keep = [_Arrays(*p) if isinstance(p, tuple) else _Arrays(p) for p in probs]
-        st, h = create_raw([k.c for k in keep], device)
+    def __init__(self, problems, device: int = 0, _raw=None):
+        if _raw is not None:  # prepared DyProblem structs and their level counts
+            structs, self.n_levels = _raw
+        else:
+            if isinstance(problems, tuple) and len(problems) == 2 and hasattr(problems[1], "levels"):
+                problems = [problems]
+            probs = list(problems) if isinstance(problems, (list, tuple)) else [problems]
+            keep = [_Arrays(*p) if isinstance(p, tuple) else _Arrays(p) for p in probs]
+            structs, self.n_levels = [k.c for k in keep], [k.n_levels for k in keep]
+        st, h = create_raw(structs, device)
         if st != DY_OK:
             raise DyplanError(st, last_error(None))
         self._h = h
-        self.n_levels = [k.n_levels for k in keep]
         self.kmax = int(lib().dy_plan_max_levels(h))
 
     def close(self):
@@ -251,3 +275,51 @@ class Plan:
         s = DyStats()
         self._check(lib().dy_plan_get_stats(self._h, ctypes.byref(s)))
         return s
+
+
+class Suffix:
+    """Residual problem of suffix recompilation (dy_suffix_*): `committed[n]`
+    nonzero for completed or in-flight nodes.  plan() stages the residual
+    problem; merge() joins a residual plan index with the committed bindings."""
+
+    def __init__(self, prob, committed, obj=None):
+        self._a = _Arrays(prob, obj)
+        c = np.ascontiguousarray(committed, dtype=np.uint8)
+        h = ctypes.c_void_p()
+        st = lib().dy_suffix_create(ctypes.byref(self._a.c), c.ctypes.data, ctypes.byref(h))
+        if st != DY_OK:
+            raise DyplanError(st, last_error(None))
+        self._h = h.value
+        self.n_full = int(prob.n_nodes)
+        self.n_nodes = int(lib().dy_suffix_nodes(self._h, None))
+        self.node_map = np.zeros(self.n_nodes, np.int32)
+        lib().dy_suffix_nodes(self._h, self.node_map.ctypes.data)
+        self.n_levels = self._a.n_levels
+
+    @property
+    def problem(self) -> DyProblem:
+        return lib().dy_suffix_problem(self._h).contents
+
+    def plan(self, device: int = 0) -> "Plan":
+        return Plan(None, device, _raw=([self.problem], [self.n_levels]))
+
+    def merge(self, committed_impl, residual_index: int):
+        """(implementation per full node, full plan index or -1)."""
+        ci = np.ascontiguousarray(committed_impl, dtype=np.int32)
+        out = np.zeros(self.n_full, np.int32)
+        fi = ctypes.c_int64()
+        st = lib().dy_suffix_merge(self._h, ci.ctypes.data, int(residual_index), out.ctypes.data, ctypes.byref(fi))
+        if st != DY_OK:
+            raise DyplanError(st, "suffix merge: bad committed id or residual index")
+        return out, int(fi.value)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().dy_suffix_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
