@@ -292,6 +292,58 @@ int32_t dy_abi_version(void);
  *                    committed id outside [0, radix) or an index outside the
  *                    residual plan space; the two domains never overlap.
  */
+/*
+ * Plan-bundle annotations (Sec. 4.4; Algorithm gen attaches per-model demand
+ * and an estimated quality to each variant; Sec. 5.2: the model receiving the
+ * largest share of the planned demand is the variant's dominant model).
+ * Host-only.  For the plan impl[N] of `prob`, with model[N][max_radix] the
+ * model class (0..n_models-1) of implementation (n, i):
+ *  model_demand[n_models]  sum over LLM nodes running model m of their
+ *                          nominal duration tau (fp64, node order);
+ *  *dominant               the model with the largest demand, equal demand to
+ *                          the lowest id; -1 when the plan has no LLM node;
+ *  *quality                product over LLM nodes of 1 - v (1 - q), fp64 (the
+ *                          chance that no node makes an impact-weighted error).
+ * LLM nodes: all nodes, or those objective->is_tool leaves unflagged.
+ * DY_EINVAL for NULL pointers or an implementation / model id out of range.
+ */
+int dy_bundle_annotate(const dy_problem* prob, const int32_t* model, int32_t n_models, const int32_t* impl,
+                       double* model_demand, int32_t* dominant, double* quality);
+
+/* A variant of a bundle as the switching rules see it. */
+typedef struct dy_variant {
+    int32_t dominant;   /* dominant model (-1: none; its load then reads 0) */
+    double quality;     /* estimated quality */
+} dy_variant;
+
+/* Thresholds of load-driven switching (Sec. 5.2). */
+typedef struct dy_switch_rules {
+    double high;        /* the active variant's dominant-model load above this triggers a scan of later variants */
+    double low;         /* when it does not, return to the lowest-index variant whose dominant load is below this */
+    double tolerance;   /* largest accepted drop of estimated quality from the active variant */
+    double margin;      /* a later candidate's dominant load must be at most the active one's minus this */
+    double dwell;       /* minimum time between two switches */
+} dy_switch_rules;
+
+/*
+ * Load-driven switching over a bundle of n_variants variants ordered by
+ * level (Sec. 5.2, "Switching plan variants").  Host-only.  Starting on
+ * variant 0, for each load sample s (time times[s], non-decreasing; loads
+ * [n_steps][n_models]): within `dwell` of the last switch nothing changes;
+ * if the active variant's dominant-model load exceeds `high`, the first later
+ * variant whose dominant model differs from the active one's, is not above
+ * `high`, has load at most the active one's minus `margin` and whose quality
+ * is at most `tolerance` below the active one's becomes active; otherwise the
+ * lowest-index variant below the active one whose dominant load is below
+ * `low` and that passes the same quality check; else the selection is kept.
+ * active[n_steps] receives the variant after each sample, *n_switches (if not
+ * NULL) the number of switches.  DY_EINVAL for NULL pointers, bad counts or a
+ * dominant id outside [-1, n_models).
+ */
+int dy_switch_simulate(const dy_variant* variants, int32_t n_variants, int32_t n_models, const double* times,
+                       const double* loads, int32_t n_steps, const dy_switch_rules* rules, int32_t* active,
+                       int32_t* n_switches);
+
 typedef struct dy_suffix dy_suffix; /* opaque */
 int dy_suffix_create(const dy_problem* full, const uint8_t* committed, dy_suffix** out);
 const dy_problem* dy_suffix_problem(const dy_suffix* s);

@@ -37,7 +37,7 @@ def _run(cmd):
 
 def build_hip(extra_flags=(), out: str = LIB) -> str:
     objs = []
-    for src in ("kernels.hip", "host.cpp", "jit_rows.cpp"):
+    for src in ("kernels.hip", "host.cpp", "jit_rows.cpp", "bundle.cpp"):
         obj = os.path.join(CSRC, "_" + src.replace(".", "_") + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
         _run([HIPCC, *HIP_FLAGS, *extra_flags, f"-I{INCLUDE}", f"-I{CSRC}", *lang, "-c",

@@ -26,7 +26,8 @@ DY_MAX_NODES, DY_MAX_RADIX, DY_MAX_LEVELS, DY_MAX_BACKENDS = 32, 255, 32, 64
 EXPORTED = ("dy_plan_create", "dy_plan_select", "dy_plan_score", "dy_plan_destroy", "dy_plan_max_levels",
             "dy_plan_num_problems", "dy_plan_set_option", "dy_plan_get_stats", "dy_plan_last_error",
             "dy_status_str", "dy_abi_version", "dy_selftest", "dy_suffix_create", "dy_suffix_problem",
-            "dy_suffix_nodes", "dy_suffix_merge", "dy_suffix_destroy")
+            "dy_suffix_nodes", "dy_suffix_merge", "dy_suffix_destroy", "dy_bundle_annotate",
+            "dy_switch_simulate")
 
 
 class DyObjective(ctypes.Structure):
@@ -46,6 +47,15 @@ class DyProblem(ctypes.Structure):
         ("w", ctypes.c_void_p), ("n_levels", ctypes.c_int32), ("n_backends", ctypes.c_int32),
         ("rho", ctypes.c_void_p), ("slo", ctypes.c_float), ("objective", ctypes.POINTER(DyObjective)),
     ]
+
+
+class DyVariant(ctypes.Structure):
+    _fields_ = [("dominant", ctypes.c_int32), ("quality", ctypes.c_double)]
+
+
+class DySwitchRules(ctypes.Structure):
+    _fields_ = [("high", ctypes.c_double), ("low", ctypes.c_double), ("tolerance", ctypes.c_double),
+                ("margin", ctypes.c_double), ("dwell", ctypes.c_double)]
 
 
 class DySource(ctypes.Structure):
@@ -128,6 +138,12 @@ def lib():
         L.dy_suffix_merge.restype = ctypes.c_int
         L.dy_suffix_destroy.argtypes = [vp]
         L.dy_suffix_destroy.restype = None
+        L.dy_bundle_annotate.argtypes = [ctypes.POINTER(DyProblem), vp, i32, vp, vp, ctypes.POINTER(i32),
+                                         ctypes.POINTER(ctypes.c_double)]
+        L.dy_bundle_annotate.restype = ctypes.c_int
+        L.dy_switch_simulate.argtypes = [ctypes.POINTER(DyVariant), i32, i32, vp, vp, i32,
+                                         ctypes.POINTER(DySwitchRules), vp, ctypes.POINTER(i32)]
+        L.dy_switch_simulate.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -323,3 +339,37 @@ class Suffix:
             self.close()
         except Exception:
             pass
+
+
+def annotate(prob, impl, model, n_models: int, obj=None):
+    """dy_bundle_annotate: (per-model demand, dominant model, quality) of the
+    plan impl[N]; model[N][R] gives each implementation's model class."""
+    a = _Arrays(prob, obj)
+    m = np.ascontiguousarray(model, dtype=np.int32)
+    im = np.ascontiguousarray(impl, dtype=np.int32)
+    dem = np.zeros(n_models, np.float64)
+    dom = ctypes.c_int32()
+    q = ctypes.c_double()
+    st = lib().dy_bundle_annotate(ctypes.byref(a.c), m.ctypes.data, n_models, im.ctypes.data, dem.ctypes.data,
+                                  ctypes.byref(dom), ctypes.byref(q))
+    if st != DY_OK:
+        raise DyplanError(st, "annotate: bad implementation or model id")
+    return dem, int(dom.value), float(q.value)
+
+
+def simulate(dominant, quality, times, loads, high: float, low: float, tolerance: float, margin: float = 0.0,
+             dwell: float = 0.0):
+    """dy_switch_simulate: (active variant after each load sample, switches)."""
+    K = len(dominant)
+    vs = (DyVariant * K)(*[DyVariant(int(d), float(q)) for d, q in zip(dominant, quality)])
+    t = np.ascontiguousarray(times, dtype=np.float64)
+    L = np.ascontiguousarray(loads, dtype=np.float64)
+    n, nm = L.shape
+    act = np.zeros(n, np.int32)
+    sw = ctypes.c_int32()
+    rules = DySwitchRules(high, low, tolerance, margin, dwell)
+    st = lib().dy_switch_simulate(vs, K, nm, t.ctypes.data, L.ctypes.data, n, ctypes.byref(rules), act.ctypes.data,
+                                  ctypes.byref(sw))
+    if st != DY_OK:
+        raise DyplanError(st, "simulate: bad arguments")
+    return act, int(sw.value)

@@ -430,3 +430,11 @@ def per_class(prob: Problem, factors=(1.0, 0.5)) -> Problem:
     base = prob.rho[:, 0].astype(np.float64)
     p.rho = np.stack([base * f for f in factors], axis=1).astype(np.float32)
     return p
+
+
+def model_table(prob: Problem):
+    """(model class of every implementation [N, R] int32, number of classes):
+    the recipes give each model class its own size factor, so a class is the
+    rank of the implementation's size among the problem's distinct sizes."""
+    sizes = np.unique(prob.size)
+    return np.searchsorted(sizes, prob.size).astype(np.int32), int(sizes.shape[0])
