@@ -39,10 +39,16 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "candidate plans scored/sec on 1 MI355X; % of FP32 VALU (or HBM) roofline"
-# MI355X fp32 vector peak 157.3 TFLOP/s = 256 CUs x 2.4 GHz x 128 FMA lanes per
-# clock x 2 flops.  This op mix (multiply, add, max, compare) has no FMA: its
-# peak is one operation per lane slot, 256 x 2.4e9 x 128 = 78.6e12 ops/s.
-PEAK_VALU = 256 * 2.4e9 * 128
+# MI355X: 256 CUs x 4 SIMDs x 16 lanes at 2.4 GHz; a SIMD completes one 64-lane
+# VALU instruction every 4 cycles (the SQ counters count one quad-cycle of
+# SQ_ACTIVE_INST_VALU per instruction), so unpacked fp32 / integer operations
+# peak at 256 x 4 x 16 x 2.4e9 = 39.3e12 lane-ops/s.  The vendor's 157.3
+# TFLOP/s counts packed fp32 FMA (two lanes' worth of FMA per lane-instruction,
+# 2 flops each); packed fp32 instructions are disabled in this build and this
+# op mix has no FMA, so 39.3e12 is the ceiling; the packed-equivalent 78.6e12
+# is reported beside it.
+PEAK_VALU = 256 * 4 * 16 * 2.4e9
+PEAK_VALU_PACKED = 2 * PEAK_VALU
 PEAK_HBM = 8.0e12                 # bytes/s
 
 # Kernel sources whose hash keys the stored HBM-traffic counters: a stored
@@ -329,6 +335,7 @@ def main():
         achieved = kern_plans_s * f
         roof = {"bound": "alu", "kernel": OBJ_SWEEP if objs else "k_sweep", "achieved": achieved / 1e12,
                 "peak": PEAK_VALU / 1e12, "unit": "TFLOP/s", "frac": achieved / PEAK_VALU,
+                "peak_packed_fp32": PEAK_VALU_PACKED / 1e12, "frac_vs_packed_fp32": achieved / PEAK_VALU_PACKED,
                 "traffic": stored_traffic(tkey),
                 "per_unit": f"{f:.4f} fp32 ops per plan (prefix-shared sweep{', objective' if objs else ''})",
                 "kernel_ms": kern_ms}
