@@ -200,6 +200,43 @@ def cpu_baseline(prob, sample_plans=None, rows=None, obj=None):
             "sample": f"{prob.name}: {what}, single-threaded fp64 oracle, {dt:.1f} s"}
 
 
+def score_bench(args, torch, D, wl, stream):
+    """Per-plan scores of a forkjoin8 range into device buffers: corr, CP at each
+    level, demand and feasibility bits, 4 (3 + K) bytes per plan, write-bound."""
+    prob = wl.by_name(args.workload if args.workload != "batch6" else "forkjoin8")
+    if args.pressure == "per-class":
+        prob = wl.per_class(prob)
+    K = prob.n_levels
+    n = min(1 << 26, prob.n_plans() if args.workload != "layered10" else 1 << 32)
+    corr = torch.empty(n, dtype=torch.float32, device="cuda")
+    cp = torch.empty(n, K, dtype=torch.float32, device="cuda")
+    dem = torch.empty(n, dtype=torch.float32, device="cuda")
+    feas = torch.empty(n, dtype=torch.int32, device="cuda")
+    with D.Plan(prob) as plan:
+        src = D.range_source(0, 0, n)
+        for _ in range(args.warmup):
+            plan.score(src, corr, cp, dem, feas, stream=stream)
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for i in range(args.steps):
+            plan.score(src, corr, cp, dem, feas, stream=stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    per_plan = 4.0 * (3 + K)
+    achieved = n * per_plan / (ms / 1e3)
+    res = {"metric": "plans scored/sec by dy_plan_score on 1 MI355X (per-plan outputs)", "value": n / (ms / 1e3),
+           "unit": "plans/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": prob.name, "plans": n, "levels": K, "outputs": "corr, cp[K], demand, feas"},
+           "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
+                        "unit": "GB/s", "frac": achieved / PEAK_HBM, "per_unit": f"{per_plan:.0f} B written per plan",
+                        "traffic": None}}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,6 +248,8 @@ def main():
                     help="the paper's additive objective J_L (levels 0, 1.5, 3) instead of corr / SLO")
     ap.add_argument("--pressure", choices=["level", "per-class"], default="level",
                     help="per-class: the second backend pressed at half the level's rho (per-backend pressure)")
+    ap.add_argument("--score", action="store_true",
+                    help="time dy_plan_score (per-plan corr, CP per level, demand, feasibility bits) instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=1 << 26)
     ap.add_argument("--sample-stride", type=int, default=0)
@@ -248,6 +287,10 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"calib_copy_bytes": n}), flush=True)
+        return
+
+    if args.score:
+        score_bench(args, torch, D, wl, stream)
         return
 
     name = args.workload

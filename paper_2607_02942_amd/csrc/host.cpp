@@ -36,7 +36,7 @@ struct JitRows {
 };
 bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err);
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
-                        hipStream_t s);
+                        int n_nodes, int n_entries, hipStream_t s);
 }  // namespace dyp
 
 using namespace dyp;
@@ -1390,7 +1390,8 @@ int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, floa
         return DY_EDEVICE;
     }
     JobDev J = make_job(h, *src);
-    hipError_t e = launch_score(J, src->count, corr, cp, demand, feas_bits, (hipStream_t)stream);
+    const HostProb& H = h->hp[src->problem];
+    hipError_t e = launch_score(J, src->count, corr, cp, demand, feas_bits, H.n, H.n * H.rmax, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(&h->err, e, "score launch");
     return DY_OK;
 }

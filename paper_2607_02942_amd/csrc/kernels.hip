@@ -1605,77 +1605,171 @@ __global__ void k_exhaust_final(const JobDev* __restrict__ jobs, int njobs) {
 // per-plan scores (dy_plan_score)
 // ---------------------------------------------------------------------------
 
+// Tables of the score kernel staged in LDS when N * R_max <= SCORE_TAB entries
+// and N <= SCORE_TAB_N: larger DAGs already load the LDS with their id and
+// recurrence columns, and read the tables faster through the vector cache.
+constexpr int SCORE_TAB = 2048;
+constexpr int SCORE_TAB_N = 12;
+
+// LDS of k_score for a problem of n nodes and nr table entries: a per-thread
+// column of n floats (the fp32 recurrence), n id bytes per thread, and the
+// staged tables.
+size_t score_lds(int n, int nr) {
+    size_t b = (size_t)n * WG * sizeof(float) + (size_t)n * WG;
+    b = (b + 15) & ~(size_t)15;
+    if (nr <= SCORE_TAB && n <= SCORE_TAB_N) b += (size_t)nr * (sizeof(float2) + sizeof(float));
+    return b;
+}
+
+__device__ __forceinline__ double wave_max_f64(double v) {
+    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o));
+    return v;
+}
+
+// fp64 CP at level k of the plan held by lane L of this wave (its ids in the
+// LDS column of thread wave_base + L), computed by the whole wave: lane n
+// holds node n's f; each node takes the maximum of its predecessors' f (and
+// 0) by a wave reduction, then adds its duration.  The maximum is exact, so
+// the value equals the definition's node-order recurrence.  Every lane of the
+// wave must call it with the same L and k; lane L's result is returned to all.
+__device__ double wave_cp64(PD P, const uint8_t* __restrict__ s_id, int L, int k) {
+    const int lane = threadIdx.x & 63, N = P->n, R = P->rmax;
+    const int owner = (threadIdx.x & ~63) + L;
+    double mine = 0.0;
+    if (lane < N) mine = P->lat64[((size_t)k * N + lane) * R + s_id[lane * WG + owner]];
+    double f = 0.0;
+    for (int n = 0; n < N; ++n) {
+        const bool pred = lane < n && (P->pred[n] >> lane & 1u);
+        const double m = wave_max_f64(pred ? f : 0.0);
+        if (lane == n) f = mine + m;
+    }
+    return wave_max_f64(lane < N && (P->sinks >> lane & 1u) ? f : 0.0);
+}
+
+// Exact feasibility of the levels in `amb` (lanes whose fp32 CP fell in a
+// band) through wave_cp64, one ambiguous (lane, level) at a time; every lane
+// of the wave must take part.  Sets the feasible ones in *bits.
+__device__ void resolve_bands(PD P, const uint8_t* __restrict__ s_id, uint32_t amb, uint32_t* bits) {
+    const int lane = threadIdx.x & 63;
+    uint64_t lanes = __ballot(amb != 0u);
+    while (lanes) {
+        const int L = __builtin_ctzll(lanes);
+        lanes &= lanes - 1;
+        uint32_t lk = (uint32_t)__builtin_amdgcn_readlane((int)amb, L);
+        while (lk) {
+            const int k = __builtin_ctz(lk);
+            lk &= lk - 1;
+            const bool f = wave_cp64(P, s_id, L, k) <= P->slo;
+            if (lane == L && f) *bits |= 1u << k;
+        }
+    }
+}
+
 __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_off, float* corr, float* cpo,
                                               float* dem, uint32_t* feas) {
     extern __shared__ float s_dyn[];
     JD J = cs(&job);
     PD P = cs(J->prob);
-    float* s_f = s_dyn;
-    uint8_t* s_id = (uint8_t*)(s_dyn + NMAX * WG);
+    const int N = P->n, R = P->rmax, tid = threadIdx.x;
+    float* s_f = s_dyn;                                    // [N][WG]
+    uint8_t* s_id = (uint8_t*)(s_dyn + (size_t)N * WG);    // [N][WG]
+    const size_t head = (((size_t)N * WG * sizeof(float) + (size_t)N * WG) + 15) & ~(size_t)15;
     const uint64_t n_units = J->count;
-    const uint64_t t = unit_off + (uint64_t)blockIdx.x * WG + threadIdx.x;
+    const uint64_t t = unit_off + (uint64_t)blockIdx.x * WG + tid;
     if (unit_off + (uint64_t)blockIdx.x * WG >= n_units) return;
+    // stage the (a, tau) and demand tables
+    const int NR = N * R;
+    const float2* at = P->at;
+    const float* dm = P->dem;
+    if (NR <= SCORE_TAB && N <= SCORE_TAB_N) {
+        float2* s_at = (float2*)((char*)s_dyn + head);
+        float* s_dm = (float*)(s_at + NR);
+        for (int i = tid; i < NR; i += WG) {
+            s_at[i] = P->at[i];
+            s_dm[i] = P->dem[i];
+        }
+        at = s_at;
+        dm = s_dm;
+    }
+    __syncthreads();
     const bool live = t < n_units;
-    bool bad = false;
+    bool bad = false;  // a row id out of range (read as 0 here): NaN scores, no feasible level
     load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
     const int K = P->k;
-    if (bad) {  // a row id out of range: NaN scores, no feasible level
-        if (!live) return;
-        for (int k = 0; k < K; ++k)
-            if (cpo) cpo[t * (uint64_t)K + k] = NAN;
-        if (corr) corr[t] = NAN;
-        if (dem) dem[t] = NAN;
-        if (feas) feas[t] = 0u;
-        return;
+    const bool out = live && !bad;
+    // 16-byte stores of the K per-level values when every row of cp is 16-byte aligned
+    const bool vec = cpo && (K & 3) == 0 && ((uintptr_t)cpo & 15) == 0;
+    auto put_cp = [&](auto&& value) {
+        if (!cpo || !live) return;
+        float* row = cpo + t * (uint64_t)K;
+        if (vec) {
+            for (int k = 0; k < K; k += 4)
+                *(float4*)(row + k) = make_float4(value(k), value(k + 1), value(k + 2), value(k + 3));
+        } else {
+            for (int k = 0; k < K; ++k) row[k] = value(k);
+        }
+    };
+    // fp32 corr (objective mode: U), unpressured CP and demand from the (staged) tables
+    float cc = 1.0f, cp0 = 0.0f, d = 0.0f, U = 0.0f;
+    for (int n = 0; n < N; ++n) {
+        const int e = n * R + s_id[n * WG + tid];
+        const float2 v = at[e];
+        if (P->obj)
+            U = U + v.x;
+        else
+            cc = cc * v.x;
+        d = d + dm[e];
+        float m = 0.0f;
+        uint32_t pm = P->pred[n];
+        while (pm) {
+            const int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            m = fmaxf(m, s_f[u * WG + tid]);
+        }
+        const float f = v.y + m;
+        s_f[n * WG + tid] = f;
+        if (P->sinks >> n & 1u) cp0 = fmaxf(cp0, f);
     }
     if (P->obj) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
-        float U, T, D;
-        eval_obj(P, s_id, s_f, U, T, D);
-        const float G = fmaf(-P->lam_l, T, U);
-        if (live && cpo)
-            for (int k = 0; k < K; ++k) cpo[t * (uint64_t)K + k] = fmaf(-P->m32[k], D, G);
+        const float G = fmaf(-P->lam_l, cp0, U);
+        put_cp([&](int k) { return out ? fmaf(-P->m32[k], d, G) : NAN; });
         if (!live) return;
-        if (corr) corr[t] = U;
-        if (dem) dem[t] = D;
-        if (feas) feas[t] = K >= 32 ? 0xffffffffu : ((1u << K) - 1u);
+        if (corr) corr[t] = out ? U : NAN;
+        if (dem) dem[t] = out ? d : NAN;
+        if (feas) feas[t] = out ? (K >= 32 ? 0xffffffffu : ((1u << K) - 1u)) : 0u;
         return;
     }
-    float cc, cp0 = 0.0f;
+    // feasibility per level: certain in fp32 outside the band (lo, hi], else
+    // the definition's fp64 CP, evaluated by the wave (resolve_bands)
+    uint32_t bits = 0, amb = 0;
     if (P->uniform) {
-        eval_uniform(P, s_id, s_f, cc, cp0);
-    } else {
-        cc = eval_corr(P, s_id);
-    }
-    uint32_t bits = 0;
-    uint8_t ids[NMAX];
-    double fx[NMAX];
-    bool have_ids = false;
-    for (int k = 0; k < K; ++k) {
-        const float cpc = P->uniform ? cp0 : eval_cp_level(P, s_id, s_f, k);
-        const float lo = P->uniform ? P->lo[k] : P->glo, hi = P->uniform ? P->hi[k] : P->ghi;
-        bool f;
-        if (cpc <= lo) {
-            f = true;
-        } else if (!(cpc <= hi)) {
-            f = false;
-        } else {  // too close to the SLO for fp32: decide in fp64
-            if (!have_ids) {
-                col_ids(P, s_id, ids);
-                have_ids = true;
-            }
-            f = ex_cp(P, ids, 1, k, fx, 1) <= P->slo;
+        for (int k = 0; k < K && k < 32; ++k) {
+            if (cp0 <= P->lo[k])
+                bits |= 1u << k;
+            else if (cp0 <= P->hi[k])
+                amb |= 1u << k;
         }
-        if (f && k < 32) bits |= 1u << k;
-        if (live && cpo) cpo[t * (uint64_t)K + k] = P->uniform ? cp0 * P->mk[k] : cpc;
+        resolve_bands(P, s_id, out ? amb : 0u, &bits);
+        put_cp([&](int k) { return out ? cp0 * P->mk[k] : NAN; });
+    } else {
+        // per-backend pressure: each level's own fp32 CP, one level at a time
+        for (int k = 0; k < K; ++k) {
+            const float cpc = eval_cp_level(P, s_id, s_f, k);
+            uint32_t a = 0;
+            if (k < 32) {
+                if (cpc <= P->glo)
+                    bits |= 1u << k;
+                else if (cpc <= P->ghi)
+                    a = 1u << k;
+            }
+            resolve_bands(P, s_id, out ? a : 0u, &bits);
+            if (live && cpo) cpo[t * (uint64_t)K + k] = out ? cpc : NAN;
+        }
     }
     if (!live) return;
-    if (corr) corr[t] = cc;
-    if (feas) feas[t] = bits;
-    if (dem) {
-        float d = 0.0f;
-        for (int n = 0; n < P->n; ++n) d = d + P->dem[n * P->rmax + s_id[n * WG + threadIdx.x]];
-        dem[t] = d;
-    }
+    if (corr) corr[t] = out ? cc : NAN;
+    if (feas) feas[t] = out ? bits : 0u;
+    if (dem) dem[t] = out ? d : NAN;
 }
 
 // ---------------------------------------------------------------------------
@@ -1823,12 +1917,13 @@ hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, h
 }
 
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
-                        hipStream_t s) {
+                        int n_nodes, int n_entries, hipStream_t s) {
+    const size_t lds = score_lds(n_nodes, n_entries);
     for (uint64_t off = 0; off < units; off += MAX_GRID_X * WG) {
         uint64_t left = units - off;
         uint64_t gx = (left + WG - 1) / WG;
         if (gx > MAX_GRID_X) gx = MAX_GRID_X;
-        hipLaunchKernelGGL(k_score, dim3((uint32_t)gx), dim3(WG), generic_lds(), s, job, off, corr, cp, dem, feas);
+        hipLaunchKernelGGL(k_score, dim3((uint32_t)gx), dim3(WG), lds, s, job, off, corr, cp, dem, feas);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

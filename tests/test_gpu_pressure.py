@@ -117,3 +117,20 @@ def test_graph_replay_per_class():
     with D.Plan(prob) as plan:
         for rep in range(3):
             assert_choices(plan.select(src, stream=stream())[0], want, f"replay {rep}")
+
+
+@pytest.mark.parametrize("per_class", [False, True])
+def test_score_feasibility_on_the_slo_boundary(per_class):
+    # integer durations and the SLO on the median CP: many plans sit exactly on
+    # the SLO at some level, inside the fp32 band, so the exact fp64 check decides
+    prob = wl.forkjoin8()
+    prob.tau = np.round(prob.tau * 2).astype(np.float32)
+    if per_class:
+        prob = wl.per_class(prob, (1.0, 0.5))
+    begin, count = 777, 300007
+    cps = orc.cp0_values(prob, begin, count)
+    prob.slo = float(np.median(cps))
+    assert (cps == prob.slo).sum() > 1000
+    with D.Plan(prob) as plan:
+        got = run_score(plan, D.range_source(0, begin, count), count, prob.n_levels)
+    assert_scores(got, orc.score_range(prob, begin, count), f"boundary scores per_class={per_class}")
