@@ -23,8 +23,8 @@ hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool ob
                                int npre_max, int npre_c, int kmax, hipStream_t s);
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
                         int npre_c, int ry, hipStream_t s);
-hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, hipStream_t s);
-hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStream_t s);
+hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, int ncol, hipStream_t s);
+hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol, hipStream_t s);
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, hipStream_t s);
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
 hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
@@ -1008,6 +1008,7 @@ struct PassPlan {
     int ry[kSweepGroups] = {};            // R_y shared by every source of a sweep group, else -1
     int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
     int kmax = 1;                         // most levels of any source
+    int ncol = 1;                         // most nodes of any source of the generic group
     int before(int g) const {             // jobs stored ahead of group g
         int t = 0;
         for (int q = 0; q < g; ++q) t += n[q];
@@ -1067,7 +1068,9 @@ void launch_seed(const JobDev* d, const PassPlan& pp, hipStream_t s,
                 "sample");
         });
     chunks(d + pp.before(G_GENERIC), pp.n[G_GENERIC],
-           [&](const JobDev* b, int n) { chk(launch_sample_generic(b, n, pp.samples[G_GENERIC], s), "sample"); });
+           [&](const JobDev* b, int n) {
+               chk(launch_sample_generic(b, n, pp.samples[G_GENERIC], pp.ncol, s), "sample");
+           });
 }
 
 void launch_table_all(const JobDev* d, int ntot, hipStream_t s,
@@ -1088,7 +1091,7 @@ void launch_main(const JobDev* d, const PassPlan& pp, hipStream_t s,
                 "sweep");
         });
     chunks(d + pp.before(G_GENERIC), pp.n[G_GENERIC],
-           [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[G_GENERIC], s), "scan"); });
+           [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[G_GENERIC], pp.ncol, s), "scan"); });
 }
 
 void launch_certify_all(const JobDev* d, int ntot, int cert_waves, int kmax, hipStream_t s,
@@ -1194,6 +1197,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
             pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
         }
         pp.kmax = std::max(pp.kmax, H.k);
+        if (g == G_GENERIC) pp.ncol = std::max(pp.ncol, H.n);
         if (sweep) {
             pp.npre[g] = std::max(pp.npre[g], H.npre);
             pp.ry[g] = pp.n[g] == 1 ? H.ry : (pp.ry[g] == H.ry ? pp.ry[g] : -1);
@@ -1327,6 +1331,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
                     ++rp.n[g];
                     if (g < G_JIT) rp.units[g] = std::max(rp.units[g], J.units);
                     if (g < kSweepGroups) rp.npre[g] = std::max(rp.npre[g], H.npre);
+                    if (g == G_GENERIC) rp.ncol = std::max(rp.ncol, H.n);
                     re.push_back(J);
                 } else {
                     J.fb_levels = H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u);

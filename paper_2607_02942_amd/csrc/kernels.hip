@@ -1137,17 +1137,14 @@ __device__ __forceinline__ float eval_cp_level(PD P, const uint8_t* __restrict__
     return best;
 }
 
-__device__ __forceinline__ void col_ids(PD P, const uint8_t* __restrict__ s_id, uint8_t* ids) {
-    for (int n = 0; n < P->n; ++n) ids[n] = s_id[n * WG + threadIdx.x];
-}
-
 // Seeding pre-pass of the generic path: one hashed plan per window of S plans.
-__global__ void __launch_bounds__(WG) k_sample_generic(const JobDev* __restrict__ jobs) {
+// ncol: node columns of the per-thread LDS arrays (the launch's largest N).
+__global__ void __launch_bounds__(WG) k_sample_generic(const JobDev* __restrict__ jobs, int ncol) {
     extern __shared__ float s_dyn[];
     JD J = cs(jobs + blockIdx.y);
     PD P = cs(J->prob);
     float* s_f = s_dyn;
-    uint8_t* s_id = (uint8_t*)(s_dyn + NMAX * WG);
+    uint8_t* s_id = (uint8_t*)(s_dyn + (size_t)ncol * WG);
     const uint64_t S = J->sample_stride;
     const uint64_t nsamp = (J->count + S - 1) / S;
     const uint64_t t0 = (uint64_t)blockIdx.x * WG;
@@ -1189,12 +1186,12 @@ __global__ void __launch_bounds__(WG) k_sample_generic(const JobDev* __restrict_
 }
 
 // Scoring pass of the generic path: one plan per thread.
-__global__ void __launch_bounds__(WG) k_scan(const JobDev* __restrict__ jobs, uint64_t unit_off) {
+__global__ void __launch_bounds__(WG) k_scan(const JobDev* __restrict__ jobs, uint64_t unit_off, int ncol) {
     extern __shared__ float s_dyn[];
     JD J = cs(jobs + blockIdx.y);
     PD P = cs(J->prob);
     float* s_f = s_dyn;
-    uint8_t* s_id = (uint8_t*)(s_dyn + NMAX * WG);
+    uint8_t* s_id = (uint8_t*)(s_dyn + (size_t)ncol * WG);
     const uint64_t n_units = J->count;
     const uint64_t t0 = unit_off + (uint64_t)blockIdx.x * WG;
     if (t0 >= n_units) return;
@@ -1614,7 +1611,7 @@ constexpr int SCORE_TAB_N = 12;
 // LDS of k_score for a problem of n nodes and nr table entries: a per-thread
 // column of n floats (the fp32 recurrence), n id bytes per thread, and the
 // staged tables.
-size_t score_lds(int n, int nr) {
+static size_t score_lds(int n, int nr) {
     size_t b = (size_t)n * WG * sizeof(float) + (size_t)n * WG;
     b = (b + 15) & ~(size_t)15;
     if (nr <= SCORE_TAB && n <= SCORE_TAB_N) b += (size_t)nr * (sizeof(float2) + sizeof(float));
@@ -1778,7 +1775,8 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
 
 static constexpr uint64_t MAX_GRID_X = 1ull << 22;  // workgroups per launch along x
 
-static size_t generic_lds() { return (size_t)NMAX * WG * sizeof(float) + (size_t)NMAX * WG; }
+// per-thread LDS columns of the generic kernels: ncol floats and ncol id bytes
+static size_t generic_lds(int ncol) { return (size_t)ncol * WG * sizeof(float) + (size_t)ncol * WG; }
 
 hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s) {
     hipLaunchKernelGGL(k_init, dim3(njobs), dim3(64), 0, s, d_jobs, njobs);
@@ -1871,22 +1869,22 @@ hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint
     return hipSuccess;
 }
 
-hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, hipStream_t s) {
+hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, int ncol, hipStream_t s) {
     if (n == 0) return hipSuccess;
     uint64_t gx = (max_samples + WG - 1) / WG;
     if (gx == 0) return hipSuccess;
     if (gx > MAX_GRID_X) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_sample_generic, dim3((uint32_t)gx, n), dim3(WG), generic_lds(), s, d_jobs);
+    hipLaunchKernelGGL(k_sample_generic, dim3((uint32_t)gx, n), dim3(WG), generic_lds(ncol), s, d_jobs, ncol);
     return hipGetLastError();
 }
 
-hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, hipStream_t s) {
+hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol, hipStream_t s) {
     if (n == 0) return hipSuccess;
     for (uint64_t off = 0; off < max_units; off += MAX_GRID_X * WG) {
         uint64_t left = max_units - off;
         uint64_t gx = (left + WG - 1) / WG;
         if (gx > MAX_GRID_X) gx = MAX_GRID_X;
-        hipLaunchKernelGGL(k_scan, dim3((uint32_t)gx, n), dim3(WG), generic_lds(), s, d_jobs, off);
+        hipLaunchKernelGGL(k_scan, dim3((uint32_t)gx, n), dim3(WG), generic_lds(ncol), s, d_jobs, off, ncol);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
