@@ -56,6 +56,7 @@ PEAK_HBM = 8.0e12                 # bytes/s
 KERNEL_SOURCES = ("paper_2607_02942_amd/csrc/kernels.hip", "paper_2607_02942_amd/csrc/jit_rows.cpp",
                   "paper_2607_02942_amd/csrc/dyplan_internal.h")
 DOMINANT = {"stream24": "dy_rows_scan_a", "stream24_obj": "dy_rows_scan_a"}  # else the sweep kernel
+SCORE_KERNEL = "k_score"
 OBJ_SWEEP = "k_sweep_obj"
 
 
@@ -104,7 +105,10 @@ def ingest_pmc(workload, fetch_db, write_db, calib_fetch_db, calib_write_db, cal
         if not hits:
             raise SystemExit(f"no kernel matching {key!r} in {sorted(means)}")
         return hits[0]
-    kern = DOMINANT.get(workload, OBJ_SWEEP if workload.endswith("_obj") else "k_sweep")
+    if workload.endswith("_score"):
+        kern = SCORE_KERNEL
+    else:
+        kern = DOMINANT.get(workload, OBJ_SWEEP if workload.endswith("_obj") else "k_sweep")
     kname, fetch = pick(_pmc_means(fetch_db, "FETCH_SIZE"), kern)
     _, write = pick(_pmc_means(write_db, "WRITE_SIZE"), kern)
     _, cf = pick(_pmc_means(calib_fetch_db, "FETCH_SIZE"), "copyBuffer")
@@ -200,7 +204,7 @@ def cpu_baseline(prob, sample_plans=None, rows=None, obj=None):
             "sample": f"{prob.name}: {what}, single-threaded fp64 oracle, {dt:.1f} s"}
 
 
-def score_bench(args, torch, D, wl, stream):
+def score_bench(args, torch, D, wl, stream, tkey):
     """Per-plan scores of a forkjoin8 range into device buffers: corr, CP at each
     level, demand and feasibility bits, 4 (3 + K) bytes per plan, write-bound."""
     prob = wl.by_name(args.workload if args.workload != "batch6" else "forkjoin8")
@@ -233,7 +237,7 @@ def score_bench(args, torch, D, wl, stream):
            "config": {"workload": prob.name, "plans": n, "levels": K, "outputs": "corr, cp[K], demand, feas"},
            "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
                         "unit": "GB/s", "frac": achieved / PEAK_HBM, "per_unit": f"{per_plan:.0f} B written per plan",
-                        "traffic": None}}
+                        "traffic": stored_traffic(tkey)}}
     print(json.dumps(res), flush=True)
 
 
@@ -260,6 +264,8 @@ def main():
     ap.add_argument("--pmc-command", action="append", default=[], help="command that produced a database")
     args = ap.parse_args()
     tkey = args.workload + ("_obj" if args.objective else "") + ("_perclass" if args.pressure == "per-class" else "")
+    if args.score:
+        tkey = args.workload + ("_perclass" if args.pressure == "per-class" else "") + "_score"
     if args.ingest_pmc:
         ingest_pmc(tkey, *args.ingest_pmc, args.calib_bytes, args.pmc_command)
         return
@@ -290,7 +296,7 @@ def main():
         return
 
     if args.score:
-        score_bench(args, torch, D, wl, stream)
+        score_bench(args, torch, D, wl, stream, tkey)
         return
 
     name = args.workload
