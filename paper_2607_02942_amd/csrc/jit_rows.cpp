@@ -6,7 +6,9 @@
 // (factor a = 1 - w(1 - p) and duration tau, fp32) sits in LDS as 64 float2
 // entries, so one ds_read_b64 per node fetches both values; on gfx950 a
 // random 8-byte LDS read costs about half the issue time of a lane permute
-// and a quarter of the two permutes it replaces.  The recurrence is unrolled
+// and a quarter of the two permutes it replaces.  The read address is the
+// whole byte times 8 (one shift with a byte-select operand) plus the node's
+// table offset in the instruction's immediate field.  The recurrence is unrolled
 // in node order with every f_n in a register: N-1 multiplies, one add per
 // node and one max per extra predecessor.  The rows stream through plain
 // dword loads (on gfx950 non-temporal loads of 24-byte rows stream about 10%
@@ -17,8 +19,9 @@
 // b_n >= R_n.  For b_n < 128 the sum b_n + 128 - R_n stays below 256 (R_n <=
 // 64, so no carry leaves the byte, and a carry coming in from a byte below
 // cannot clear bit 7 of a byte that already has it); b_n >= 128 sets bit 7 of
-// w itself.  Table indices are taken mod 64, so every LDS read stays inside
-// its node's table whatever the row holds.  The
+// w itself.  The table array has 192 entries past node N-1's table, so a
+// read for any byte value stays inside the array (an id >= 64 reads a later
+// node's entries or the spare ones; its lane is dropped as invalid).  The
 // arithmetic is that of the generic kernels (same fp32 operations in the
 // same order), so both produce identical scores.
 //
@@ -81,12 +84,18 @@ __device__ void dy_flush(DyCand* q, unsigned qn, int lane, DyCand* cand, unsigne
   }
   if (base + qn > cap) *ovf = true;
 }
-__device__ __forceinline__ unsigned long long dy_sample_row(unsigned long long j, unsigned long long S,
+// Row of sample t (t < ceil(n / S)): the 64 samples of a wave read 64
+// consecutive rows of the window [64 S g, min(64 S (g + 1), n)), g = t / 64,
+// from a hashed offset and wrapping inside the window: whole cache lines of
+// rows, where one row per window of S would fetch a line for each 24 bytes.
+__device__ __forceinline__ unsigned long long dy_sample_row(unsigned long long t, unsigned long long S,
                                                             unsigned long long n) {
-  const unsigned long long start = j * S;
-  const unsigned width = (unsigned)min(S, n - start);
-  const unsigned h = (unsigned)(j * 0x9E3779B1ull) >> 16;
-  return start + (unsigned long long)(h % width);
+  const unsigned long long g = t >> 6, start = g * 64ull * S;
+  const unsigned long long width = min(64ull * S, n - start);
+  const unsigned h = (unsigned)(g * 0x9E3779B1ull) >> 16;
+  unsigned long long r = (unsigned long long)(h % (unsigned)min(width, 0xffffffffull)) + (t & 63ull);
+  if (r >= width) r %= width;
+  return start + r;
 }
 )";
 
@@ -163,6 +172,8 @@ std::string gen_source(const ProbDev& D) {
     std::ostringstream o;
     o << kCommon;
     o << "#define DY_N " << N << "\n#define DY_K " << D.k << "\n";
+    // node tables: 64 entries each, then 192 spare ones (read by byte ids past 63)
+    o << "#define DY_TAB (DY_N * 64 + 192)\n";
     // per-word constants of the id range check (bytes past node N-1 are zero)
     for (int q = 0; q < Q; ++q) {
         unsigned kk = 0;
@@ -173,9 +184,9 @@ std::string gen_source(const ProbDev& D) {
     o << R"(
 __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax,
                                          const unsigned* __restrict__ table, float2* s_tab, float* s_bins) {
-  for (int i = threadIdx.x; i < DY_N * 64; i += blockDim.x) {
+  for (int i = threadIdx.x; i < DY_TAB; i += blockDim.x) {
     const int n = i >> 6, e = i & 63;
-    s_tab[i] = e < rmax ? at[n * rmax + e] : make_float2(__builtin_nanf(""), __builtin_nanf(""));
+    s_tab[i] = n < DY_N && e < rmax ? at[n * rmax + e] : make_float2(__builtin_nanf(""), __builtin_nanf(""));
   }
   if (table != nullptr && threadIdx.x < 64) s_bins[threadIdx.x] = __uint_as_float(table[threadIdx.x]);
   __syncthreads();
@@ -227,7 +238,7 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         const int q = n / 4, b = n % 4;
         o << "  const float2 e" << n << " = s_tab[" << n * 64 << " + ((w" << q;
         if (b) o << " >> " << 8 * b;
-        o << ") & 63u)]; \\\n";
+        o << ") & 255u)]; \\\n";
     }
     if (D.obj) {
         emit_obj_sums(o, D, 0, N);
@@ -265,7 +276,7 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
                 const int q = n / 4, bb = n % 4;
                 o << "  const float2 e" << n << " = s_tab[" << n * 64 << " + ((y" << q;
                 if (bb) o << " >> " << 8 * bb;
-                o << ") & 63u)]; \\\n";
+                o << ") & 255u)]; \\\n";
             }
             if (!D.obj)
                 for (int n = n0; n < m; ++n)
@@ -338,7 +349,7 @@ __device__ __forceinline__ void dy_scan_body(
     const unsigned* __restrict__ table, int bin_shift, const float* __restrict__ hi,
     const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap,
     unsigned* __restrict__ ncand, int* __restrict__ flags) {
-  __shared__ float2 s_tab[DY_N * 64];
+  __shared__ float2 s_tab[DY_TAB];
   __shared__ float s_bins[64];
   __shared__ DyCand s_q[4][DY_QCAP];
   dy_stage(at, rmax, table, s_tab, s_bins);
@@ -412,7 +423,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count,
     const float2* __restrict__ at, int rmax, const float* __restrict__ lo,
     unsigned* __restrict__ scert, unsigned long long S, int aligned) {
-  __shared__ float2 s_tab[DY_N * 64];
+  __shared__ float2 s_tab[DY_TAB];
   dy_stage(at, rmax, nullptr, s_tab, nullptr);
   const int lane = threadIdx.x & 63;
   const unsigned long long nsamp = (count + S - 1) / S;
