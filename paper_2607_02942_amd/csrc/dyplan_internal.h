@@ -135,6 +135,7 @@ struct JobDev {
     dy_choice* hout;          // [KMAX] host-mapped copy of the choices (null: copied back instead)
     uint32_t* hncand;         // host-mapped copies of ncand and flags (with hout)
     int32_t* hflags;
+    uint32_t* hdone;          // host-mapped completion word of the call (with hout), set last
 };
 
 }  // namespace dyp

@@ -93,6 +93,8 @@ struct Scratch {
     dy_choice* h_out = nullptr;
     uint32_t* h_ncand = nullptr;
     int32_t* h_flags = nullptr;
+    uint32_t* h_done = nullptr;  // pinned, host-coherent: one completion word per source
+    uint32_t* d_done = nullptr;  // its device address
     size_t uploaded = 0;        // jobs of h_jobs present on the device (0: none)
 };
 
@@ -382,6 +384,7 @@ void free_scratch(Scratch& s) {
     if (s.h_jobs) (void)hipHostFree(s.h_jobs);
     if (s.h_fb) (void)hipHostFree(s.h_fb);
     if (s.h_res) (void)hipHostFree(s.h_res);
+    if (s.h_done) (void)hipHostFree(s.h_done);
     s = Scratch{};
 }
 
@@ -445,7 +448,10 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
         (e = hipHostMalloc((void**)&s.h_fb, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
         (e = hipHostMalloc((void**)&s.h_res, res_bytes, hipHostMallocMapped | hipHostMallocCoherent)) !=
             hipSuccess ||
-        (e = hipHostGetDevicePointer((void**)&s.d_hres, s.h_res, 0)) != hipSuccess) {
+        (e = hipHostGetDevicePointer((void**)&s.d_hres, s.h_res, 0)) != hipSuccess ||
+        (e = hipHostMalloc((void**)&s.h_done, njobs * sizeof(uint32_t), hipHostMallocMapped | hipHostMallocCoherent)) !=
+            hipSuccess ||
+        (e = hipHostGetDevicePointer((void**)&s.d_done, s.h_done, 0)) != hipSuccess) {
         free_scratch(s);
         return hip_fail(&h->err, e, "hipHostMalloc(scratch)");
     }
@@ -1181,6 +1187,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
             J.hout = (dy_choice*)S.d_hres + (size_t)j * km;
             J.hncand = (uint32_t*)(S.d_hres + S.res_ncand_off) + q;
             J.hflags = (int32_t*)(S.d_hres + S.res_flags_off) + q;
+            J.hdone = S.d_done + q;
         }
         J.fb_corr = S.fb_corr + (size_t)q * KMAX;
         J.fb_index = S.fb_index + (size_t)q * KMAX;
@@ -1260,6 +1267,13 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         if (n_src > kDirectResults)
             ck(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, st), "copy out");
     };
+    // With the results written straight to host memory, the call waits for the
+    // certification's completion words (set after the results, behind a
+    // system-scope fence) instead of the stream: they land several
+    // microseconds before the stream reports the graph complete.
+    const bool poll = n_src <= kDirectResults && !h->timing && !h->force_fp64;
+    if (poll)
+        for (int q = 0; q < n_src; ++q) __atomic_store_n(S.h_done + q, 0u, __ATOMIC_RELAXED);
     bool exhausted = h->force_fp64 != 0;
     bool launched = false;
     if (h->use_graph && !h->timing && !h->force_fp64 && S.clean && !changed) {
@@ -1299,7 +1313,24 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
             chk(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, s), "copy out");
         }
     }
-    chk(hipStreamSynchronize(s), "hipStreamSynchronize");
+    if (poll && st == DY_OK) {
+        // the stream is queried every 256 reads, so a failed launch or a
+        // fault ends the wait as well
+        for (uint32_t it = 1;; ++it) {
+            int q = 0;
+            while (q < n_src && __atomic_load_n(S.h_done + q, __ATOMIC_ACQUIRE) != 0u) ++q;
+            if (q == n_src) break;
+            if ((it & 255u) == 0u) {
+                const hipError_t qe = hipStreamQuery(s);
+                if (qe != hipErrorNotReady) {  // complete (every result visible) or failed
+                    chk(qe, "hipStreamQuery");
+                    break;
+                }
+            }
+        }
+    } else {
+        chk(hipStreamSynchronize(s), "hipStreamSynchronize");
+    }
     if (st != DY_OK) return st;
 
     dy_stats stats{};

@@ -243,14 +243,25 @@ __device__ bool job_ids(JD J, PD P, uint64_t index, uint8_t* ids, int is) {
         return true;
     }
     const uint8_t* row = J->rows + (index - J->index_base) * J->stride;
+    const int N = P->n;
     bool ok = true;
-    for (int n = 0; n < P->n; ++n) {
-        uint8_t v = row[n];
-        if (v >= (uint32_t)P->radix[n]) {
-            ok = false;
-            v = 0;
+    // eight byte loads in flight at a time (a lane otherwise waits on each)
+    for (int n0 = 0; n0 < N; n0 += 8) {
+        uint8_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = n0 + j < N ? row[n0 + j] : (uint8_t)0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int n = n0 + j;
+            if (n < N) {
+                uint8_t x = v[j];
+                if (x >= (uint32_t)P->radix[n]) {
+                    ok = false;
+                    x = 0;
+                }
+                ids[n * is] = x;
+            }
         }
-        ids[n * is] = v;
     }
     return ok;
 }
@@ -1328,6 +1339,11 @@ __device__ void merge_cert(JD J, PD P) {
             *J->hncand = *J->ncand;
             *J->hflags = *J->flags;
         }
+        if (J->hdone) {  // completion word last, behind the results
+            __threadfence_system();
+            __syncthreads();
+            if (threadIdx.x == 0) __hip_atomic_store(J->hdone, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
     }
     if (*J->flags == 0) {
         for (int i = threadIdx.x; i < KMAX * NSLOT; i += 64) J->scert[i] = 0u;
@@ -1338,12 +1354,60 @@ __device__ void merge_cert(JD J, PD P) {
     }
 }
 
+// fp64 scores of the plan whose ids sit at ids[n * 64], in node order as the
+// definitions take them: x = corr (objective: U, the LLM nodes' sum of u), cp
+// = the CP at the level's durations, d = demand (objective: D, the LLM nodes'
+// sum of tau).  The three table loads of eight nodes are issued together, so a
+// lane waits on memory about N / 8 times instead of 3 N.
+template <bool OBJ>
+__device__ __forceinline__ void cert_eval(PD P, int N, int R, const uint8_t* ids, double* f, const double* a64,
+                                          const double* d64, const double* lat, double& x, double& cp,
+                                          double& d) {
+    x = OBJ ? 0.0 : 1.0;
+    cp = 0.0;
+    d = 0.0;
+    for (int n0 = 0; n0 < N; n0 += 8) {
+        double va[8], vl[8], vd[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int n = n0 + j;
+            const int e = n < N ? n * R + ids[n * 64] : 0;
+            va[j] = a64[e];
+            vl[j] = lat[e];
+            vd[j] = d64[e];
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int n = n0 + j;
+            if (n < N) {
+                if (!OBJ) {
+                    x = x * va[j];
+                    d = d + vd[j];
+                } else if (P->llm >> n & 1u) {
+                    x = x + va[j];
+                    d = d + vd[j];
+                }
+                double m = 0.0;
+                uint32_t pm = P->pred[n];
+                while (pm) {
+                    const int u = __builtin_ctz(pm);
+                    pm &= pm - 1;
+                    const double fu = f[u * 64];
+                    if (fu > m) m = fu;
+                }
+                const double fn = vl[j] + m;
+                f[n * 64] = fn;
+                if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
+            }
+        }
+    }
+}
+
 // Certification: grid (cert_waves, source, level), one wave per block.  Pass
 // A tightens the level's threshold with the candidates whose fp32 CP is
 // certainly feasible.  Pass B re-evaluates in fp64 every candidate of this
-// wave's share that could still win the level (its CP only when its corr
-// could beat the lane's current best) and keeps the feasible one with the
-// greatest corr, then the lowest index.  The source's block that finishes
+// wave's share that could still win the level and keeps the feasible one
+// with the greatest corr, then the lowest index.  The source's block that finishes
 // last merges the waves (merge_cert).  Levels run in separate blocks: each
 // lane walks its candidates once per block instead of once per level.
 __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs) {
@@ -1404,25 +1468,8 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
             const Cand c = i < ncache ? s_cand[i] : J->cand[i];
             if (!(fma(-m, (double)c.cp, (double)c.corr) >= T)) continue;
             if (!job_ids(J, P, c.index, ids, 64)) continue;
-            double U = 0.0, D = 0.0, t = 0.0;
-            for (int n = 0; n < N; ++n) {
-                const int e = n * R + ids[n * 64];
-                if (P->llm >> n & 1u) {
-                    U = U + a64[e];
-                    D = D + d64[e];
-                }
-                double mx = 0.0;
-                uint32_t pm = P->pred[n];
-                while (pm) {
-                    const int u = __builtin_ctz(pm);
-                    pm &= pm - 1;
-                    const double fu = f[u * 64];
-                    if (fu > mx) mx = fu;
-                }
-                const double fn = lat[e] + mx;
-                f[n * 64] = fn;
-                if ((P->sinks >> n & 1u) && fn > t) t = fn;
-            }
+            double U, D, t;
+            cert_eval<true>(P, N, R, ids, f, a64, d64, lat, U, t, D);
             const double j = obj_j(P->lam_l64, m, U, t, D);
             if (better(j, c.index, bc, bi)) {
                 bc = j;
@@ -1444,26 +1491,10 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
             const Cand c = i < ncache ? s_cand[i] : J->cand[i];
             if (!(c.corr >= T && c.cp <= hi)) continue;
             if (!job_ids(J, P, c.index, ids, 64)) continue;
-            double corr = 1.0;
-            for (int n = 0; n < N; ++n) corr = corr * a64[n * R + ids[n * 64]];
+            double corr, cp, d;
+            cert_eval<false>(P, N, R, ids, f, a64, d64, lat, corr, cp, d);
             if (!better(corr, c.index, bc, bi)) continue;
-            double cp = 0.0;
-            for (int n = 0; n < N; ++n) {
-                double m = 0.0;
-                uint32_t pm = P->pred[n];
-                while (pm) {
-                    const int u = __builtin_ctz(pm);
-                    pm &= pm - 1;
-                    const double fu = f[u * 64];
-                    if (fu > m) m = fu;
-                }
-                const double fn = lat[n * R + ids[n * 64]] + m;
-                f[n * 64] = fn;
-                if ((P->sinks >> n & 1u) && fn > cp) cp = fn;
-            }
             if (!(cp <= P->slo)) continue;
-            double d = 0.0;
-            for (int n = 0; n < N; ++n) d = d + d64[n * R + ids[n * 64]];
             bc = corr;
             bi = c.index;
             bcp = cp;
