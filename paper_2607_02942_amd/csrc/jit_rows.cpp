@@ -440,9 +440,18 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
       for (int k = 0; k < DY_K; ++k)
         DY_SEED_UPDATE(k);
   }
+  // wave maxima, then the workgroup's through LDS: one atomic per level and
+  // workgroup (same-address atomics serialise across the device)
+  __shared__ unsigned s_red[DY_K][4];
   for (int k = 0; k < DY_K; ++k) {
     const unsigned e = dy_wmax(best[k]);
-    if (lane == 0 && e) atomicMax(scert + k * 64 + ((blockIdx.x * 4 + (threadIdx.x >> 6)) % 64), e);
+    if (lane == 0) s_red[k][threadIdx.x >> 6] = e;
+  }
+  __syncthreads();
+  if (threadIdx.x < DY_K) {
+    const unsigned* r = s_red[threadIdx.x];
+    const unsigned e = max(max(r[0], r[1]), max(r[2], r[3]));
+    if (e) atomicMax(scert + threadIdx.x * 64 + (blockIdx.x % 64), e);
   }
 }
 )";
