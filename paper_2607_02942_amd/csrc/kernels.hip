@@ -1693,6 +1693,12 @@ __device__ void resolve_bands(PD P, const uint8_t* __restrict__ s_id, uint32_t a
     }
 }
 
+// NU > 0: DAGs of at most NU nodes under uniform pressure or the objective
+// take an unrolled decode and recurrence (every descriptor load issued up
+// front, the f_n in registers, predecessor tests as scalar branches); other
+// problems, and NU == 0, the loops over LDS columns.  Launched with NU = 8 or
+// 16 for DAGs of up to 16 nodes, else NU = 0.
+template <int NU>
 __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_off, float* corr, float* cpo,
                                               float* dem, uint32_t* feas) {
     extern __shared__ float s_dyn[];
@@ -1722,7 +1728,21 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
     __syncthreads();
     const bool live = t < n_units;
     bool bad = false;  // a row id out of range (read as 0 here): NaN scores, no feasible level
-    load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
+    const bool unrolled = NU > 0 && N <= NU && (P->uniform || P->obj);
+    if (NU > 0 && unrolled && J->kind == DY_SOURCE_RANGE && !J->big) {
+        // digits of the plan index, node N-1 least significant
+        uint32_t x = (uint32_t)(J->begin + (live ? t : n_units - 1));
+#pragma unroll
+        for (int n = NU - 1; n >= 0; --n) {
+            if (n < N) {
+                const uint32_t q = mdiv(x, P->rmag[n]);
+                s_id[n * WG + tid] = (uint8_t)(x - q * (uint32_t)P->radix[n]);
+                x = q;
+            }
+        }
+    } else {
+        load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
+    }
     const int K = P->k;
     const bool out = live && !bad;
     // 16-byte stores of the K per-level values when every row of cp is 16-byte aligned
@@ -1739,24 +1759,50 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
     };
     // fp32 corr (objective mode: U), unpressured CP and demand from the (staged) tables
     float cc = 1.0f, cp0 = 0.0f, d = 0.0f, U = 0.0f;
-    for (int n = 0; n < N; ++n) {
-        const int e = n * R + s_id[n * WG + tid];
-        const float2 v = at[e];
-        if (P->obj)
-            U = U + v.x;
-        else
-            cc = cc * v.x;
-        d = d + dm[e];
-        float m = 0.0f;
-        uint32_t pm = P->pred[n];
-        while (pm) {
-            const int u = __builtin_ctz(pm);
-            pm &= pm - 1;
-            m = fmaxf(m, s_f[u * WG + tid]);
+    if (NU > 0 && unrolled) {
+        constexpr int NF = NU > 0 ? NU : 1;
+        float f[NF];
+        const bool obj = P->obj != 0;
+        const uint32_t sinks = P->sinks;
+#pragma unroll
+        for (int n = 0; n < NF; ++n) {
+            if (n < N) {
+                const int e = n * R + s_id[n * WG + tid];
+                const float2 v = at[e];
+                if (obj)
+                    U = U + v.x;
+                else
+                    cc = cc * v.x;
+                d = d + dm[e];
+                float m = 0.0f;
+                const uint32_t pm = P->pred[n];
+#pragma unroll
+                for (int u = 0; u < n; ++u)
+                    if (pm >> u & 1u) m = fmaxf(m, f[u]);
+                f[n] = v.y + m;
+                if (sinks >> n & 1u) cp0 = fmaxf(cp0, f[n]);
+            }
         }
-        const float f = v.y + m;
-        s_f[n * WG + tid] = f;
-        if (P->sinks >> n & 1u) cp0 = fmaxf(cp0, f);
+    } else {
+        for (int n = 0; n < N; ++n) {
+            const int e = n * R + s_id[n * WG + tid];
+            const float2 v = at[e];
+            if (P->obj)
+                U = U + v.x;
+            else
+                cc = cc * v.x;
+            d = d + dm[e];
+            float m = 0.0f;
+            uint32_t pm = P->pred[n];
+            while (pm) {
+                const int u = __builtin_ctz(pm);
+                pm &= pm - 1;
+                m = fmaxf(m, s_f[u * WG + tid]);
+            }
+            const float f = v.y + m;
+            s_f[n * WG + tid] = f;
+            if (P->sinks >> n & 1u) cp0 = fmaxf(cp0, f);
+        }
     }
     if (P->obj) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
         const float G = fmaf(-P->lam_l, cp0, U);
@@ -1952,7 +1998,13 @@ hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* c
         uint64_t left = units - off;
         uint64_t gx = (left + WG - 1) / WG;
         if (gx > MAX_GRID_X) gx = MAX_GRID_X;
-        hipLaunchKernelGGL(k_score, dim3((uint32_t)gx), dim3(WG), lds, s, job, off, corr, cp, dem, feas);
+        const dim3 grid((uint32_t)gx);
+        if (n_nodes <= 8)
+            hipLaunchKernelGGL(k_score<8>, grid, dim3(WG), lds, s, job, off, corr, cp, dem, feas);
+        else if (n_nodes <= 16)
+            hipLaunchKernelGGL(k_score<16>, grid, dim3(WG), lds, s, job, off, corr, cp, dem, feas);
+        else  // unrolled, 24 nodes took 1.5x longer: ~n^2/2 scalar predecessor tests per plan
+            hipLaunchKernelGGL(k_score<0>, grid, dim3(WG), lds, s, job, off, corr, cp, dem, feas);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
