@@ -36,7 +36,7 @@ struct JitRows {
 };
 bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err);
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
-                        int n_nodes, int n_entries, hipStream_t s);
+                        int n_nodes, int n_entries, bool simple, bool obj, hipStream_t s);
 }  // namespace dyp
 
 using namespace dyp;
@@ -1436,7 +1436,9 @@ int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, floa
     }
     JobDev J = make_job(h, *src);
     const HostProb& H = h->hp[src->problem];
-    hipError_t e = launch_score(J, src->count, corr, cp, demand, feas_bits, H.n, H.n * H.rmax, (hipStream_t)stream);
+    const ProbDev& D = h->hdesc[src->problem];
+    hipError_t e = launch_score(J, src->count, corr, cp, demand, feas_bits, H.n, H.n * H.rmax,
+                                D.uniform != 0 || D.obj != 0, D.obj != 0, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(&h->err, e, "score launch");
     return DY_OK;
 }

@@ -1642,6 +1642,8 @@ constexpr int SCORE_TAB_N = 12;
 // LDS of k_score for a problem of n nodes and nr table entries: a per-thread
 // column of n floats (the fp32 recurrence), n id bytes per thread, and the
 // staged tables.
+constexpr uint64_t SCORE_PPT = 8;  // plans per thread of k_score (the tables are staged once per block)
+
 static size_t score_lds(int n, int nr) {
     size_t b = (size_t)n * WG * sizeof(float) + (size_t)n * WG;
     b = (b + 15) & ~(size_t)15;
@@ -1693,14 +1695,8 @@ __device__ void resolve_bands(PD P, const uint8_t* __restrict__ s_id, uint32_t a
     }
 }
 
-// NU > 0: DAGs of at most NU nodes under uniform pressure or the objective
-// take an unrolled decode and recurrence (every descriptor load issued up
-// front, the f_n in registers, predecessor tests as scalar branches); other
-// problems, and NU == 0, the loops over LDS columns.  Launched with NU = 8 or
-// 16 for DAGs of up to 16 nodes, else NU = 0.
-template <int NU>
-__global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_off, float* corr, float* cpo,
-                                              float* dem, uint32_t* feas) {
+__global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_off, uint64_t unit_end, float* corr,
+                                              float* cpo, float* dem, uint32_t* feas) {
     extern __shared__ float s_dyn[];
     JD J = cs(&job);
     PD P = cs(J->prob);
@@ -1708,9 +1704,9 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
     float* s_f = s_dyn;                                    // [N][WG]
     uint8_t* s_id = (uint8_t*)(s_dyn + (size_t)N * WG);    // [N][WG]
     const size_t head = (((size_t)N * WG * sizeof(float) + (size_t)N * WG) + 15) & ~(size_t)15;
-    const uint64_t n_units = J->count;
-    const uint64_t t = unit_off + (uint64_t)blockIdx.x * WG + tid;
-    if (unit_off + (uint64_t)blockIdx.x * WG >= n_units) return;
+    const uint64_t n_units = J->count;  // plans of the source; this launch scores [unit_off, unit_end)
+    const uint64_t first = unit_off + (uint64_t)blockIdx.x * WG, stride = (uint64_t)gridDim.x * WG;
+    if (first >= unit_end) return;
     // stage the (a, tau) and demand tables
     const int NR = N * R;
     const float2* at = P->at;
@@ -1726,23 +1722,12 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
         dm = s_dm;
     }
     __syncthreads();
-    const bool live = t < n_units;
+    // several plans per thread (block-uniform loop): the table staging above is paid once
+    for (uint64_t base = first; base < unit_end; base += stride) {
+    const uint64_t t = base + tid;
+    const bool live = t < unit_end;
     bool bad = false;  // a row id out of range (read as 0 here): NaN scores, no feasible level
-    const bool unrolled = NU > 0 && N <= NU && (P->uniform || P->obj);
-    if (NU > 0 && unrolled && J->kind == DY_SOURCE_RANGE && !J->big) {
-        // digits of the plan index, node N-1 least significant
-        uint32_t x = (uint32_t)(J->begin + (live ? t : n_units - 1));
-#pragma unroll
-        for (int n = NU - 1; n >= 0; --n) {
-            if (n < N) {
-                const uint32_t q = mdiv(x, P->rmag[n]);
-                s_id[n * WG + tid] = (uint8_t)(x - q * (uint32_t)P->radix[n]);
-                x = q;
-            }
-        }
-    } else {
-        load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
-    }
+    load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
     const int K = P->k;
     const bool out = live && !bad;
     // 16-byte stores of the K per-level values when every row of cp is 16-byte aligned
@@ -1759,59 +1744,34 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
     };
     // fp32 corr (objective mode: U), unpressured CP and demand from the (staged) tables
     float cc = 1.0f, cp0 = 0.0f, d = 0.0f, U = 0.0f;
-    if (NU > 0 && unrolled) {
-        constexpr int NF = NU > 0 ? NU : 1;
-        float f[NF];
-        const bool obj = P->obj != 0;
-        const uint32_t sinks = P->sinks;
-#pragma unroll
-        for (int n = 0; n < NF; ++n) {
-            if (n < N) {
-                const int e = n * R + s_id[n * WG + tid];
-                const float2 v = at[e];
-                if (obj)
-                    U = U + v.x;
-                else
-                    cc = cc * v.x;
-                d = d + dm[e];
-                float m = 0.0f;
-                const uint32_t pm = P->pred[n];
-#pragma unroll
-                for (int u = 0; u < n; ++u)
-                    if (pm >> u & 1u) m = fmaxf(m, f[u]);
-                f[n] = v.y + m;
-                if (sinks >> n & 1u) cp0 = fmaxf(cp0, f[n]);
-            }
+    for (int n = 0; n < N; ++n) {
+        const int e = n * R + s_id[n * WG + tid];
+        const float2 v = at[e];
+        if (P->obj)
+            U = U + v.x;
+        else
+            cc = cc * v.x;
+        d = d + dm[e];
+        float m = 0.0f;
+        uint32_t pm = P->pred[n];
+        while (pm) {
+            const int u = __builtin_ctz(pm);
+            pm &= pm - 1;
+            m = fmaxf(m, s_f[u * WG + tid]);
         }
-    } else {
-        for (int n = 0; n < N; ++n) {
-            const int e = n * R + s_id[n * WG + tid];
-            const float2 v = at[e];
-            if (P->obj)
-                U = U + v.x;
-            else
-                cc = cc * v.x;
-            d = d + dm[e];
-            float m = 0.0f;
-            uint32_t pm = P->pred[n];
-            while (pm) {
-                const int u = __builtin_ctz(pm);
-                pm &= pm - 1;
-                m = fmaxf(m, s_f[u * WG + tid]);
-            }
-            const float f = v.y + m;
-            s_f[n * WG + tid] = f;
-            if (P->sinks >> n & 1u) cp0 = fmaxf(cp0, f);
-        }
+        const float f = v.y + m;
+        s_f[n * WG + tid] = f;
+        if (P->sinks >> n & 1u) cp0 = fmaxf(cp0, f);
     }
     if (P->obj) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
         const float G = fmaf(-P->lam_l, cp0, U);
         put_cp([&](int k) { return out ? fmaf(-P->m32[k], d, G) : NAN; });
-        if (!live) return;
-        if (corr) corr[t] = out ? U : NAN;
-        if (dem) dem[t] = out ? d : NAN;
-        if (feas) feas[t] = out ? (K >= 32 ? 0xffffffffu : ((1u << K) - 1u)) : 0u;
-        return;
+        if (live) {
+            if (corr) corr[t] = out ? U : NAN;
+            if (dem) dem[t] = out ? d : NAN;
+            if (feas) feas[t] = out ? (K >= 32 ? 0xffffffffu : ((1u << K) - 1u)) : 0u;
+        }
+        continue;
     }
     // feasibility per level: certain in fp32 outside the band (lo, hi], else
     // the definition's fp64 CP, evaluated by the wave (resolve_bands)
@@ -1840,10 +1800,125 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
             if (live && cpo) cpo[t * (uint64_t)K + k] = out ? cpc : NAN;
         }
     }
-    if (!live) return;
-    if (corr) corr[t] = out ? cc : NAN;
-    if (feas) feas[t] = out ? bits : 0u;
-    if (dem) dem[t] = out ? d : NAN;
+    if (live) {
+        if (corr) corr[t] = out ? cc : NAN;
+        if (feas) feas[t] = out ? bits : 0u;
+        if (dem) dem[t] = out ? d : NAN;
+    }
+    }
+}
+
+// k_score for RANGE sources whose plan indices fit 32 bits, DAGs of at most
+// NU nodes, uniform pressure (OBJ = false) or the objective (OBJ = true): the
+// same values as k_score with the per-plan loops unrolled.  The digit decode's
+// divisors and the predecessor masks sit in scalar registers, the ids and the
+// f_n in vector registers (predecessor tests are scalar branches), and a plan
+// writes its ids to LDS only when its wave has a CP inside a level's band
+// (resolve_bands reads them there).  No row can be bad, so outputs need no
+// NaN fill.
+template <int NU, bool OBJ>
+__global__ void __launch_bounds__(WG) k_score_fast(const JobDev job, uint64_t unit_off, uint64_t unit_end,
+                                                   float* corr, float* cpo, float* dem, uint32_t* feas) {
+    extern __shared__ float s_dyn[];
+    JD J = cs(&job);
+    PD P = cs(J->prob);
+    const int N = P->n, R = P->rmax, K = P->k, tid = threadIdx.x;
+    // LDS: the (a, tau) and demand tables (at most SCORE_TAB entries), then the
+    // ids [N][WG] for the band check
+    const int NR = N * R;
+    float2* at = (float2*)s_dyn;
+    float* dm = (float*)(at + NR);
+    uint8_t* s_id = (uint8_t*)(dm + NR);
+    const uint64_t first = unit_off + (uint64_t)blockIdx.x * WG, stride = (uint64_t)gridDim.x * WG;
+    if (first >= unit_end) return;
+    for (int i = tid; i < NR; i += WG) {
+        at[i] = P->at[i];
+        dm[i] = P->dem[i];
+    }
+    __syncthreads();
+    const uint32_t sinks = P->sinks;
+    const bool vec = cpo && (K & 3) == 0 && ((uintptr_t)cpo & 15) == 0;
+    for (uint64_t base = first; base < unit_end; base += stride) {
+        const uint64_t t = base + tid;
+        const bool live = t < unit_end;
+        uint32_t x = (uint32_t)(J->begin + (live ? t : unit_end - 1));
+        uint32_t id[NU];
+#pragma unroll
+        for (int n = NU - 1; n >= 0; --n) {
+            if (n < N) {
+                const uint32_t q = mdiv(x, P->rmag[n]);
+                id[n] = x - q * (uint32_t)P->radix[n];
+                x = q;
+            }
+        }
+        float cc = OBJ ? 0.0f : 1.0f, cp0 = 0.0f, d = 0.0f;
+        float f[NU];
+#pragma unroll
+        for (int n = 0; n < NU; ++n) {
+            if (n < N) {
+                const int e = n * R + (int)id[n];
+                const float2 v = at[e];
+                cc = OBJ ? cc + v.x : cc * v.x;
+                d = d + dm[e];
+                float m = 0.0f;
+                const uint32_t pm = P->pred[n];
+#pragma unroll
+                for (int u = 0; u < n; ++u)
+                    if (pm >> u & 1u) m = fmaxf(m, f[u]);
+                f[n] = v.y + m;
+                if (sinks >> n & 1u) cp0 = fmaxf(cp0, f[n]);
+            }
+        }
+        float* row = cpo ? cpo + t * (uint64_t)K : nullptr;
+        if (OBJ) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
+            const float G = fmaf(-P->lam_l, cp0, cc);
+            if (live && row) {
+                if (vec) {
+                    for (int k = 0; k < K; k += 4)
+                        *(float4*)(row + k) = make_float4(fmaf(-P->m32[k], d, G), fmaf(-P->m32[k + 1], d, G),
+                                                          fmaf(-P->m32[k + 2], d, G), fmaf(-P->m32[k + 3], d, G));
+                } else {
+                    for (int k = 0; k < K; ++k) row[k] = fmaf(-P->m32[k], d, G);
+                }
+            }
+            if (live) {
+                if (corr) corr[t] = cc;
+                if (dem) dem[t] = d;
+                if (feas) feas[t] = K >= 32 ? 0xffffffffu : ((1u << K) - 1u);
+            }
+            continue;
+        }
+        // feasibility per level: certain in fp32 outside the band (lo, hi], else
+        // the definition's fp64 CP, evaluated by the wave
+        uint32_t bits = 0, amb = 0;
+        for (int k = 0; k < K && k < 32; ++k) {
+            if (cp0 <= P->lo[k])
+                bits |= 1u << k;
+            else if (cp0 <= P->hi[k])
+                amb |= 1u << k;
+        }
+        if (!live) amb = 0u;
+        if (__ballot(amb != 0u)) {
+#pragma unroll
+            for (int n = 0; n < NU; ++n)
+                if (n < N) s_id[n * WG + tid] = (uint8_t)id[n];
+            resolve_bands(P, s_id, amb, &bits);
+        }
+        if (live && row) {
+            if (vec) {
+                for (int k = 0; k < K; k += 4)
+                    *(float4*)(row + k) = make_float4(cp0 * P->mk[k], cp0 * P->mk[k + 1], cp0 * P->mk[k + 2],
+                                                      cp0 * P->mk[k + 3]);
+            } else {
+                for (int k = 0; k < K; ++k) row[k] = cp0 * P->mk[k];
+            }
+        }
+        if (live) {
+            if (corr) corr[t] = cc;
+            if (feas) feas[t] = bits;
+            if (dem) dem[t] = d;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1992,19 +2067,27 @@ hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, h
 }
 
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
-                        int n_nodes, int n_entries, hipStream_t s) {
+                        int n_nodes, int n_entries, bool simple, bool obj, hipStream_t s) {
     const size_t lds = score_lds(n_nodes, n_entries);
+    // unrolled kernels: RANGE sources of 32-bit indices, uniform pressure or the
+    // objective, up to 16 nodes (at 24 the ~n^2/2 scalar predecessor tests per
+    // plan made an unrolled kernel 1.5x slower than the LDS loops)
+    const bool fast = simple && job.kind == DY_SOURCE_RANGE && !job.big && n_nodes <= 16 && n_entries <= SCORE_TAB;
+    const size_t lds_fast = (size_t)n_entries * (sizeof(float2) + sizeof(float)) + (size_t)n_nodes * WG;
     for (uint64_t off = 0; off < units; off += MAX_GRID_X * WG) {
-        uint64_t left = units - off;
-        uint64_t gx = (left + WG - 1) / WG;
-        if (gx > MAX_GRID_X) gx = MAX_GRID_X;
+        const uint64_t end = units - off < MAX_GRID_X * WG ? units : off + MAX_GRID_X * WG;
+        const uint64_t gx = (end - off + WG * SCORE_PPT - 1) / (WG * SCORE_PPT);
         const dim3 grid((uint32_t)gx);
-        if (n_nodes <= 8)
-            hipLaunchKernelGGL(k_score<8>, grid, dim3(WG), lds, s, job, off, corr, cp, dem, feas);
-        else if (n_nodes <= 16)
-            hipLaunchKernelGGL(k_score<16>, grid, dim3(WG), lds, s, job, off, corr, cp, dem, feas);
-        else  // unrolled, 24 nodes took 1.5x longer: ~n^2/2 scalar predecessor tests per plan
-            hipLaunchKernelGGL(k_score<0>, grid, dim3(WG), lds, s, job, off, corr, cp, dem, feas);
+        if (!fast)
+            hipLaunchKernelGGL(k_score, grid, dim3(WG), lds, s, job, off, end, corr, cp, dem, feas);
+        else if (n_nodes <= 8 && obj)
+            hipLaunchKernelGGL((k_score_fast<8, true>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, feas);
+        else if (n_nodes <= 8)
+            hipLaunchKernelGGL((k_score_fast<8, false>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, feas);
+        else if (obj)
+            hipLaunchKernelGGL((k_score_fast<16, true>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, feas);
+        else
+            hipLaunchKernelGGL((k_score_fast<16, false>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, feas);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
