@@ -1816,13 +1816,14 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
 // writes its ids to LDS only when its wave has a CP inside a level's band
 // (resolve_bands reads them there).  No row can be bad, so outputs need no
 // NaN fill.
-template <int NU, bool OBJ>
+template <int NN, bool OBJ>
 __global__ void __launch_bounds__(WG) k_score_fast(const JobDev job, uint64_t unit_off, uint64_t unit_end,
                                                    float* corr, float* cpo, float* dem, uint32_t* feas) {
     extern __shared__ float s_dyn[];
     JD J = cs(&job);
     PD P = cs(J->prob);
-    const int N = P->n, R = P->rmax, K = P->k, tid = threadIdx.x;
+    constexpr int N = NN;  // the DAG's node count (checked by the host)
+    const int R = P->rmax, K = P->k, tid = threadIdx.x;
     // LDS: the (a, tau) and demand tables (at most SCORE_TAB entries), then the
     // ids [N][WG] for the band check
     const int NR = N * R;
@@ -1842,32 +1843,28 @@ __global__ void __launch_bounds__(WG) k_score_fast(const JobDev job, uint64_t un
         const uint64_t t = base + tid;
         const bool live = t < unit_end;
         uint32_t x = (uint32_t)(J->begin + (live ? t : unit_end - 1));
-        uint32_t id[NU];
+        uint32_t id[N];
 #pragma unroll
-        for (int n = NU - 1; n >= 0; --n) {
-            if (n < N) {
-                const uint32_t q = mdiv(x, P->rmag[n]);
-                id[n] = x - q * (uint32_t)P->radix[n];
-                x = q;
-            }
+        for (int n = N - 1; n >= 0; --n) {
+            const uint32_t q = mdiv(x, P->rmag[n]);
+            id[n] = x - q * (uint32_t)P->radix[n];
+            x = q;
         }
         float cc = OBJ ? 0.0f : 1.0f, cp0 = 0.0f, d = 0.0f;
-        float f[NU];
+        float f[N];
 #pragma unroll
-        for (int n = 0; n < NU; ++n) {
-            if (n < N) {
-                const int e = n * R + (int)id[n];
-                const float2 v = at[e];
-                cc = OBJ ? cc + v.x : cc * v.x;
-                d = d + dm[e];
-                float m = 0.0f;
-                const uint32_t pm = P->pred[n];
+        for (int n = 0; n < N; ++n) {
+            const int e = n * R + (int)id[n];
+            const float2 v = at[e];
+            cc = OBJ ? cc + v.x : cc * v.x;
+            d = d + dm[e];
+            float m = 0.0f;
+            const uint32_t pm = P->pred[n];
 #pragma unroll
-                for (int u = 0; u < n; ++u)
-                    if (pm >> u & 1u) m = fmaxf(m, f[u]);
-                f[n] = v.y + m;
-                if (sinks >> n & 1u) cp0 = fmaxf(cp0, f[n]);
-            }
+            for (int u = 0; u < n; ++u)
+                if (pm >> u & 1u) m = fmaxf(m, f[u]);
+            f[n] = v.y + m;
+            if (sinks >> n & 1u) cp0 = fmaxf(cp0, f[n]);
         }
         float* row = cpo ? cpo + t * (uint64_t)K : nullptr;
         if (OBJ) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
@@ -1900,8 +1897,7 @@ __global__ void __launch_bounds__(WG) k_score_fast(const JobDev job, uint64_t un
         if (!live) amb = 0u;
         if (__ballot(amb != 0u)) {
 #pragma unroll
-            for (int n = 0; n < NU; ++n)
-                if (n < N) s_id[n * WG + tid] = (uint8_t)id[n];
+            for (int n = 0; n < N; ++n) s_id[n * WG + tid] = (uint8_t)id[n];
             resolve_bands(P, s_id, amb, &bits);
         }
         if (live && row) {
@@ -2069,25 +2065,37 @@ hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, h
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
                         int n_nodes, int n_entries, bool simple, bool obj, hipStream_t s) {
     const size_t lds = score_lds(n_nodes, n_entries);
-    // unrolled kernels: RANGE sources of 32-bit indices, uniform pressure or the
-    // objective, up to 16 nodes (at 24 the ~n^2/2 scalar predecessor tests per
-    // plan made an unrolled kernel 1.5x slower than the LDS loops)
+    // unrolled kernels, one per node count: RANGE sources of 32-bit indices,
+    // uniform pressure or the objective, up to 16 nodes (at 24 the ~n^2/2
+    // scalar predecessor tests per plan made an unrolled kernel 1.5x slower
+    // than the LDS loops)
     const bool fast = simple && job.kind == DY_SOURCE_RANGE && !job.big && n_nodes <= 16 && n_entries <= SCORE_TAB;
     const size_t lds_fast = (size_t)n_entries * (sizeof(float2) + sizeof(float)) + (size_t)n_nodes * WG;
     for (uint64_t off = 0; off < units; off += MAX_GRID_X * WG) {
         const uint64_t end = units - off < MAX_GRID_X * WG ? units : off + MAX_GRID_X * WG;
         const uint64_t gx = (end - off + WG * SCORE_PPT - 1) / (WG * SCORE_PPT);
         const dim3 grid((uint32_t)gx);
-        if (!fast)
+        if (!fast) {
             hipLaunchKernelGGL(k_score, grid, dim3(WG), lds, s, job, off, end, corr, cp, dem, feas);
-        else if (n_nodes <= 8 && obj)
-            hipLaunchKernelGGL((k_score_fast<8, true>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, feas);
-        else if (n_nodes <= 8)
-            hipLaunchKernelGGL((k_score_fast<8, false>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, feas);
-        else if (obj)
-            hipLaunchKernelGGL((k_score_fast<16, true>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, feas);
-        else
-            hipLaunchKernelGGL((k_score_fast<16, false>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, feas);
+        } else {
+            switch (n_nodes * 2 + (obj ? 1 : 0)) {
+#define DYP_SCORE_FAST(NN)                                                                                    \
+    case 2 * NN:                                                                                              \
+        hipLaunchKernelGGL((k_score_fast<NN, false>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, \
+                           feas);                                                                             \
+        break;                                                                                                \
+    case 2 * NN + 1:                                                                                          \
+        hipLaunchKernelGGL((k_score_fast<NN, true>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem,  \
+                           feas);                                                                             \
+        break;
+                DYP_SCORE_FAST(1) DYP_SCORE_FAST(2) DYP_SCORE_FAST(3) DYP_SCORE_FAST(4)
+                DYP_SCORE_FAST(5) DYP_SCORE_FAST(6) DYP_SCORE_FAST(7) DYP_SCORE_FAST(8)
+                DYP_SCORE_FAST(9) DYP_SCORE_FAST(10) DYP_SCORE_FAST(11) DYP_SCORE_FAST(12)
+                DYP_SCORE_FAST(13) DYP_SCORE_FAST(14) DYP_SCORE_FAST(15) DYP_SCORE_FAST(16)
+#undef DYP_SCORE_FAST
+                default: return hipErrorInvalidValue;
+            }
+        }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
