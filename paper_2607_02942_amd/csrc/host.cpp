@@ -25,7 +25,7 @@ hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint
                         int npre_c, int ry, hipStream_t s);
 hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, int ncol, hipStream_t s);
 hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol, hipStream_t s);
-hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, hipStream_t s);
+hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, int nmax, int nrmax, hipStream_t s);
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
 hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
 struct JitRows {
@@ -331,6 +331,7 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 struct dy_plan {
     int device = 0;
     int kmax = 0;
+    int nmax = 0, nrmax = 0;          // most nodes and node-table entries (N x R_max) of any problem
     std::vector<HostProb> hp;
     std::vector<ProbDev> hdesc;       // host copies of the device descriptors
     std::vector<int> jit_state;       // per problem: 0 untried, 1 ready, -1 unavailable
@@ -551,6 +552,8 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
     };
     h->hp.resize(n_probs);
     h->kmax = 0;
+    h->nmax = 0;
+    h->nrmax = 0;
     for (int j = 0; j < n_probs; ++j) {
         const dy_problem& pb = probs[j];
         const size_t NR = (size_t)pb.n_nodes * pb.max_radix;
@@ -566,6 +569,8 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         L.lat64 = take((size_t)KL * NR * sizeof(double));
         L.dem64 = take(NR * sizeof(double));
         h->kmax = std::max(h->kmax, pb.objective ? pb.objective->n_levels : pb.n_levels);
+        h->nmax = std::max(h->nmax, (int)pb.n_nodes);
+        h->nrmax = std::max(h->nrmax, (int)NR);
     }
     std::vector<char> img(off, 0);
     hipError_t e = hipMalloc((void**)&h->d_arena, off);
@@ -1109,10 +1114,10 @@ void launch_main(const JobDev* d, const PassPlan& pp, hipStream_t s,
            [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[G_GENERIC], pp.ncol, s), "scan"); });
 }
 
-void launch_certify_all(const JobDev* d, int ntot, int cert_waves, int kmax, hipStream_t s,
+void launch_certify_all(const JobDev* d, int ntot, int cert_waves, const dy_plan* h, hipStream_t s,
                         const std::function<void(hipError_t, const char*)>& chk) {
     for (int c = 0; c < ntot; c += 65535)
-        chk(launch_certify(d + c, std::min(65535, ntot - c), cert_waves, kmax, s), "certify");
+        chk(launch_certify(d + c, std::min(65535, ntot - c), cert_waves, h->kmax, h->nmax, h->nrmax, s), "certify");
 }
 
 // Generated rows kernels for problem p: compiled at first use.
@@ -1264,7 +1269,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         if (h->timing) ck(hipEventRecord(h->ev[2], st), "hipEventRecord");
     };
     auto issue_post = [&](hipStream_t st, const Check& ck) {
-        launch_certify_all(S.d_jobs, n_src, cert_waves, h->kmax, st, ck);
+        launch_certify_all(S.d_jobs, n_src, cert_waves, h, st, ck);
         if (h->timing) ck(hipEventRecord(h->ev[3], st), "hipEventRecord");
         if (n_src > kDirectResults)
             ck(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, st), "copy out");
@@ -1392,7 +1397,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
             launch_table_all(S.d_fb, n_re, s, chk);
             launch_main(S.d_fb, rp, s, chk);
             jit_pass(re.data(), rp.before(G_JIT), rp.n[G_JIT], false, s, chk);
-            launch_certify_all(S.d_fb, n_re, cert_waves, h->kmax, s, chk);
+            launch_certify_all(S.d_fb, n_re, cert_waves, h, s, chk);
         }
         if (n_ex > 0) {
             exhausted = true;

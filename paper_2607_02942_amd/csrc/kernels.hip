@@ -1410,10 +1410,13 @@ __device__ __forceinline__ void cert_eval(PD P, int N, int R, const uint8_t* ids
 // with the greatest corr, then the lowest index.  The source's block that finishes
 // last merges the waves (merge_cert).  Levels run in separate blocks: each
 // lane walks its candidates once per block instead of once per level.
-__global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs) {
-    extern __shared__ double s_tab[];
-    __shared__ double s_f[NMAX * 64];
-    __shared__ uint8_t s_id[NMAX * 64];
+// Dynamic LDS: tab_d doubles for the fp64 tables (0: read from global memory),
+// then the recurrence column f [nf][64] (fp64) and the ids [nf][64], nf >= N.
+__global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs, int tab_d, int nf) {
+    extern __shared__ double s_dyn64[];
+    double* s_tab = s_dyn64;
+    double* s_f = s_dyn64 + tab_d;
+    uint8_t* s_id = (uint8_t*)(s_f + (size_t)nf * 64);
     __shared__ Cand s_cand[CERT_CACHE];
     JD J = cs(jobs + blockIdx.y);
     PD P = cs(J->prob);
@@ -1427,7 +1430,7 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs)
     const double* a64 = P->a64;
     const double* d64 = P->dem64;
     const double* lat = P->lat64 + (P->obj ? (size_t)0 : (size_t)k * NR);
-    if (3 * NR * sizeof(double) <= (size_t)CERT_LDS_TABLES) {
+    if (3 * NR <= (size_t)tab_d) {
         // unrolled so that many loads are in flight before the first LDS store
 #pragma unroll 8
         for (size_t q = lane; q < NR; q += 64) {
@@ -2039,8 +2042,11 @@ hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol
     return hipSuccess;
 }
 
-hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, hipStream_t s) {
-    hipLaunchKernelGGL(k_certify, dim3(waves, njobs, kmax), dim3(64), CERT_LDS_TABLES, s, d_jobs);
+hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, int nmax, int nrmax, hipStream_t s) {
+    // LDS sized by the plan's largest DAG (a fixed 58 KB let two blocks share a CU)
+    const int tab_d = 3 * nrmax * (int)sizeof(double) <= CERT_LDS_TABLES ? 3 * nrmax : 0;
+    const size_t lds = ((size_t)tab_d + (size_t)nmax * 64) * sizeof(double) + (size_t)nmax * 64;
+    hipLaunchKernelGGL(k_certify, dim3(waves, njobs, kmax), dim3(64), lds, s, d_jobs, tab_d, nmax);
     return hipGetLastError();
 }
 
