@@ -341,7 +341,9 @@ def main():
         if st != 0:
             raise RuntimeError(f"select failed {st}: {D.last_error(plan._h)}")
 
-    def timed_loop(tag):
+    def timed_loop(tag, collect):
+        # collect: read the library's per-call statistics after every step
+        # (the caller-side loop does not, as a caller needs only the choices)
         cands, main_ms = [], []
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
@@ -349,9 +351,10 @@ def main():
         ev0.record(stream)
         for i in range(args.steps):
             step()
-            s = plan.stats()
-            main_ms.append(s.main_ms)
-            cands.append(s.candidates)
+            if collect:
+                s = plan.stats()
+                main_ms.append(s.main_ms)
+                cands.append(s.candidates)
             if i == 0 or (i + 1) % max(1, args.steps // 4) == 0:
                 print(f"[bench] {tag} step {i + 1}/{args.steps}", file=sys.stderr, flush=True)
         ev1.record(stream)
@@ -361,14 +364,14 @@ def main():
     # 1) the steps as a caller runs them: repeated calls replay one HIP graph
     for _ in range(args.warmup):
         step()
-    ms_per_step, _, cands = timed_loop("step")
+    ms_per_step, _, _ = timed_loop("step", False)
     value = plans / (ms_per_step / 1e3)
     # 2) the same calls with the library's HIP events around the scoring kernel
     #    (on the call's stream; timed calls launch directly, not from a graph)
     plan.set_option(D.DY_OPT_TIMING, 1)
     for _ in range(max(1, args.warmup // 2)):
         step()
-    ms_per_step_timed, main_ms, _ = timed_loop("timed")
+    ms_per_step_timed, main_ms, cands = timed_loop("timed", True)
     kern_ms = float(np.mean(main_ms))
     kern_plans_s = plans / (kern_ms / 1e3)
 

@@ -95,6 +95,24 @@ def test_layered10_ranges(begin, count):
     assert_choices(got, orc.select_range(prob, begin, count), f"layered10[{begin}+{count}]")
 
 
+@pytest.mark.parametrize("n_src", [1, 64, 65])
+def test_results_written_to_host_or_copied_back(n_src):
+    # up to 64 sources the certification writes the choices straight to host
+    # memory and the call waits on completion words; above, they are copied
+    # back after the stream.  Repeated calls replay the captured graph.
+    prob = wl.chain4()
+    rng = np.random.default_rng(n_src)
+    begins = rng.integers(0, 20000, n_src)
+    counts = rng.integers(1, 737, n_src)
+    srcs = [D.range_source(0, int(b), int(min(c, 20736 - b))) for b, c in zip(begins, counts)]
+    want = [orc.select_range(prob, s.begin, s.count) for s in srcs]
+    with D.Plan(prob) as plan:
+        for call in range(3):
+            got = plan.select(srcs, stream=stream())
+            for q, (g, w) in enumerate(zip(got, want)):
+                assert_choices(g, w, f"{n_src} sources, call {call}, source {q}")
+
+
 def test_batch6_first_requests_live():
     probs = [wl.batch6_request(r) for r in range(6)]
     with D.Plan(probs) as plan:
