@@ -279,6 +279,29 @@ def check_scores(prob, obj, U, T, Dd, J, gu, gj, gd, gf):
     assert np.all(gf == (1 << K) - 1)
 
 
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 11, 13, 16, 17])
+def test_score_node_counts(n):
+    # one unrolled objective kernel per node count up to 16 (17: the generic kernel)
+    rng = np.random.default_rng(70 + n)
+    r = max(2, min(12, int(round(20000 ** (1.0 / n)))))
+    prob = small_dag(n, [int(x) for x in rng.integers(1, r + 1, n)], 700 + n)
+    obj = wl.paper_objective(prob, levels=(0.0, 0.5, 1.5, 3.0))
+    if n > 2:
+        obj = with_tools(obj, n, (n // 2,))
+    K = obj.n_levels
+    cnt = prob.n_plans()
+    with D.Plan((prob, obj)) as plan:
+        u = torch.empty(cnt, dtype=torch.float32, device="cuda")
+        j = torch.empty(cnt, K, dtype=torch.float32, device="cuda")
+        d = torch.empty(cnt, dtype=torch.float32, device="cuda")
+        f = torch.empty(cnt, dtype=torch.int32, device="cuda")
+        plan.score(D.range_source(0, 0, cnt), u, j, d, f, stream=stream())
+        torch.cuda.synchronize()
+    U, T, Dd, J = orc.obj_score(prob, obj, 0, cnt)
+    check_scores(prob, obj, U, T, Dd, J, u.cpu().numpy(), j.cpu().numpy(), d.cpu().numpy(),
+                 f.cpu().numpy().astype(np.uint32))
+
+
 def test_score_range_and_rows():
     prob = wl.forkjoin8()
     obj = with_tools(wl.paper_objective(prob, levels=(0.0, 0.5, 1.5, 3.0)), 8, (7,))

@@ -213,6 +213,20 @@ def test_score_ranges(name, begin, count):
     assert_scores(got, orc.score_range(prob, begin, count), name)
 
 
+@pytest.mark.parametrize("n", list(range(1, 18)))
+def test_score_every_node_count(n):
+    # ranges of DAGs of 1..16 nodes run one unrolled kernel per node count
+    # (17: the generic kernel); whole plan spaces of up to ~2^15 plans
+    rng = np.random.default_rng(900 + n)
+    rmax = max(2, min(12, int(round(30000 ** (1.0 / n)))))
+    prob = tiny_problem(rng, n, rmax, 8, 2, True)
+    total = prob.n_plans()
+    begin = int(rng.integers(0, max(1, total // 7)))
+    with D.Plan(prob) as plan:
+        got = run_score(plan, D.range_source(0, begin, total - begin), total - begin, prob.n_levels)
+    assert_scores(got, orc.score_range(prob, begin, total - begin), f"{n} nodes")
+
+
 def test_score_rows_and_bad_ids():
     prob = wl.stream24()
     rows = wl.make_rows(50001, 24, 36)
