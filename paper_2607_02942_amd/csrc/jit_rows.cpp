@@ -49,6 +49,7 @@ struct JitRows {
     hipFunction_t scan = nullptr;     // rows whose words are dword aligned
     hipFunction_t scan_u = nullptr;   // any other stride / alignment (byte loads)
     hipFunction_t sample = nullptr;
+    hipFunction_t score = nullptr;    // per-plan scores of a RANGE source of 32-bit indices
 };
 
 namespace {
@@ -164,6 +165,99 @@ void emit_obj_sums(std::ostringstream& o, const ProbDev& D, int n0, int n1) {
     o << "  float u_ = 0.0f, d_ = 0.0f; \\\n";
     for (int n = n0; n < n1; ++n)
         if (D.llm >> n & 1u) o << "  u_ = u_ + e" << n << ".x; d_ = d_ + e" << n << ".y; \\\n";
+}
+
+// Per-plan scores of a RANGE source whose plan indices fit 32 bits (the
+// values of the library's score kernels, same fp32 operations in the same
+// order): digits by constant division, the DAG's recurrence unrolled, the
+// level constants as literals.  corr / SLO mode: a plan whose fp32 CP falls
+// in a level's band (lo_k, hi_k] takes that level's fp64 recurrence here,
+// from the fp64 duration table, against the SLO.
+void gen_score(std::ostringstream& o, const ProbDev& D) {
+    const int N = D.n, K = D.k;
+    o << R"(
+extern "C" __global__ void __launch_bounds__(256) dy_score_range(
+    unsigned long long begin, unsigned long long count, const float2* __restrict__ at,
+    const float* __restrict__ dm, int rmax, const double* __restrict__ lat64, float* __restrict__ corr,
+    float* __restrict__ cpo, float* __restrict__ demo, unsigned* __restrict__ feas, int vec) {
+  __shared__ float2 s_tab[DY_TAB];
+  __shared__ float s_dm[DY_N * 64];
+  for (int i = threadIdx.x; i < DY_N * 64; i += blockDim.x) {
+    const int n = i >> 6, e = i & 63;
+    s_dm[i] = e < rmax ? dm[n * rmax + e] : 0.0f;
+  }
+  dy_stage(at, rmax, nullptr, s_tab, nullptr);
+  const unsigned long long stride = (unsigned long long)gridDim.x * 256ull;
+  for (unsigned long long t = (unsigned long long)blockIdx.x * 256ull + threadIdx.x; t < count; t += stride) {
+    unsigned x = (unsigned)(begin + t);
+)";
+    for (int n = N - 1; n >= 0; --n) {
+        o << "    const unsigned d" << n << " = x % " << D.radix[n] << "u;";
+        if (n > 0) o << " x /= " << D.radix[n] << "u;";
+        o << "\n";
+    }
+    for (int n = 0; n < N; ++n) o << "    const float2 e" << n << " = s_tab[" << n * 64 << " + d" << n << "];\n";
+    o << "    float dd = 0.0f;\n";
+    for (int n = 0; n < N; ++n) o << "    dd = dd + s_dm[" << n * 64 << " + d" << n << "];\n";
+    o << "    float c = " << (D.obj ? "0.0f" : "1.0f") << ";\n";
+    for (int n = 0; n < N; ++n) o << "    c = c " << (D.obj ? "+" : "*") << " e" << n << ".x;\n";
+    {
+        std::ostringstream r;
+        emit_recurrence(r, D, 0, N);
+        emit_sinks(r, D, "cp", true);
+        std::string body = r.str(), line;
+        std::istringstream in(body);
+        while (std::getline(in, line)) {  // drop the macro line continuations
+            if (line.size() >= 2 && line.compare(line.size() - 2, 2, " \\") == 0) line.resize(line.size() - 2);
+            o << "  " << line << "\n";
+        }
+    }
+    o << "    if (corr) corr[t] = c;\n    if (demo) demo[t] = dd;\n";
+    if (D.obj) {
+        o << "    const float G = fmaf(-" << flit(D.lam_l) << ", cp, c);\n";
+        o << "    if (feas) feas[t] = " << (K >= 32 ? 0xffffffffu : ((1u << K) - 1u)) << "u;\n";
+        o << "    if (cpo) {\n      float* row = cpo + t * " << K << "ull;\n";
+        for (int k = 0; k < K; ++k) o << "      row[" << k << "] = fmaf(-" << flit(D.m32[k]) << ", dd, G);\n";
+        o << "    }\n";
+    } else {
+        o << "    unsigned bits = 0u, amb = 0u;\n";
+        for (int k = 0; k < K && k < 32; ++k)
+            o << "    if (cp <= " << flit(D.lo[k]) << ") bits |= " << (1u << k) << "u; else if (cp <= " << flit(D.hi[k])
+              << ") amb |= " << (1u << k) << "u;\n";
+        o << "    for (int k = 0; k < " << std::min(K, 32) << " && amb; ++k) {\n";
+        o << "      if (!(amb >> k & 1u)) continue;\n";
+        o << "      amb &= ~(1u << k);\n";
+        o << "      const double* L = lat64 + (unsigned long long)k * " << N << "ull * (unsigned long long)rmax;\n";
+        for (int n = 0; n < N; ++n) {
+            std::vector<int> preds;
+            for (int u = 0; u < n; ++u)
+                if (D.pred[n] >> u & 1u) preds.push_back(u);
+            o << "      const double g" << n << " = L[" << n << " * rmax + (int)d" << n << "]";
+            if (!preds.empty()) {
+                std::string m = "g" + std::to_string(preds[0]);
+                for (size_t q = 1; q < preds.size(); ++q) m = "fmax(" + m + ", g" + std::to_string(preds[q]) + ")";
+                o << " + " << m;
+            }
+            o << ";\n";
+        }
+        std::string c64;
+        for (int n = 0; n < N; ++n)
+            if (D.sinks >> n & 1u) c64 = c64.empty() ? "g" + std::to_string(n) : "fmax(" + c64 + ", g" + std::to_string(n) + ")";
+        o << "      if (" << c64 << " <= " << dlit(D.slo) << ") bits |= 1u << k;\n    }\n";
+        o << "    if (feas) feas[t] = bits;\n";
+        o << "    if (cpo) {\n      float* row = cpo + t * " << K << "ull;\n";
+        if (K % 4 == 0) {
+            o << "      if (vec) {\n";
+            for (int k = 0; k < K; k += 4)
+                o << "        *(float4*)(row + " << k << ") = make_float4(cp * " << flit(D.mk[k]) << ", cp * " << flit(D.mk[k + 1])
+                  << ", cp * " << flit(D.mk[k + 2]) << ", cp * " << flit(D.mk[k + 3]) << ");\n";
+            o << "      } else {\n";
+        }
+        for (int k = 0; k < K; ++k) o << "        row[" << k << "] = cp * " << flit(D.mk[k]) << ";\n";
+        if (K % 4 == 0) o << "      }\n";
+        o << "    }\n";
+    }
+    o << "  }\n}\n";
 }
 
 std::string gen_source(const ProbDev& D) {
@@ -455,6 +549,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
   }
 }
 )";
+    if (D.uniform || D.obj) gen_score(o, D);
     return o.str();
 }
 
@@ -507,7 +602,8 @@ bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err) 
     if (hipModuleLoadData(&j.mod, code.data()) != hipSuccess ||
         hipModuleGetFunction(&j.scan, j.mod, "dy_rows_scan_a") != hipSuccess ||
         hipModuleGetFunction(&j.scan_u, j.mod, "dy_rows_scan_u") != hipSuccess ||
-        hipModuleGetFunction(&j.sample, j.mod, "dy_rows_sample") != hipSuccess) {
+        hipModuleGetFunction(&j.sample, j.mod, "dy_rows_sample") != hipSuccess ||
+        ((D.uniform || D.obj) && hipModuleGetFunction(&j.score, j.mod, "dy_score_range") != hipSuccess)) {
         *err = "loading the compiled rows kernels failed";
         return false;
     }

@@ -279,9 +279,11 @@ def check_scores(prob, obj, U, T, Dd, J, gu, gj, gd, gf):
     assert np.all(gf == (1 << K) - 1)
 
 
+@pytest.mark.parametrize("jit", [1, 0])
 @pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 11, 13, 16, 17])
-def test_score_node_counts(n):
-    # one unrolled objective kernel per node count up to 16 (17: the generic kernel)
+def test_score_node_counts(n, jit):
+    # the kernel generated for the DAG (jit 1), else one unrolled objective
+    # kernel per node count up to 16 and the generic kernel beyond
     rng = np.random.default_rng(70 + n)
     r = max(2, min(12, int(round(20000 ** (1.0 / n)))))
     prob = small_dag(n, [int(x) for x in rng.integers(1, r + 1, n)], 700 + n)
@@ -291,6 +293,7 @@ def test_score_node_counts(n):
     K = obj.n_levels
     cnt = prob.n_plans()
     with D.Plan((prob, obj)) as plan:
+        plan.set_option(D.DY_OPT_JIT, jit)
         u = torch.empty(cnt, dtype=torch.float32, device="cuda")
         j = torch.empty(cnt, K, dtype=torch.float32, device="cuda")
         d = torch.empty(cnt, dtype=torch.float32, device="cuda")

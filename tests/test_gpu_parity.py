@@ -213,18 +213,44 @@ def test_score_ranges(name, begin, count):
     assert_scores(got, orc.score_range(prob, begin, count), name)
 
 
-@pytest.mark.parametrize("n", list(range(1, 18)))
-def test_score_every_node_count(n):
-    # ranges of DAGs of 1..16 nodes run one unrolled kernel per node count
-    # (17: the generic kernel); whole plan spaces of up to ~2^15 plans
+@pytest.mark.parametrize("jit", [1, 0])
+@pytest.mark.parametrize("n", list(range(1, 18)) + [20, 24, 32])
+def test_score_every_node_count(n, jit):
+    # ranges: one unrolled kernel per node count up to 16; beyond, the kernel
+    # generated for the DAG (jit 1) or the generic kernel (jit 0).  Whole plan
+    # spaces of up to ~2^17 plans, else 2^17 plans at a random offset.
     rng = np.random.default_rng(900 + n)
     rmax = max(2, min(12, int(round(30000 ** (1.0 / n)))))
-    prob = tiny_problem(rng, n, rmax, 8, 2, True)
-    total = prob.n_plans()
-    begin = int(rng.integers(0, max(1, total // 7)))
+    if n <= 17:
+        prob = tiny_problem(rng, n, rmax, 8, 2, True)
+        total = prob.n_plans()
+        begin = int(rng.integers(0, max(1, total // 7)))
+        count = total - begin
+    else:
+        prob = tiny_problem_large(rng, n, 8)
+        total = prob.n_plans()
+        count = min(total, 1 << 17)
+        begin = int(rng.integers(0, total - count + 1))
     with D.Plan(prob) as plan:
-        got = run_score(plan, D.range_source(0, begin, total - begin), total - begin, prob.n_levels)
-    assert_scores(got, orc.score_range(prob, begin, total - begin), f"{n} nodes")
+        plan.set_option(D.DY_OPT_JIT, jit)
+        got = run_score(plan, D.range_source(0, begin, count), count, prob.n_levels)
+    assert_scores(got, orc.score_range(prob, begin, count), f"{n} nodes, jit {jit}")
+
+
+def tiny_problem_large(rng, n, K):
+    # radix 1..2 per node (at most 2^32 plans), SLO near the middle of a sample's CPs
+    edges = np.array([(i, j) for i in range(n) for j in range(i + 1, n) if rng.random() < 0.2],
+                     np.int32).reshape(-1, 2)
+    radix = rng.integers(1, 3, size=n).astype(np.int32)
+    prob = wl.Problem(n_nodes=n, edges=edges, radix=radix, p=rng.uniform(0.4, 1.0, (n, 2)).astype(np.float32),
+                      tau=rng.lognormal(0, 0.6, (n, 2)).astype(np.float32),
+                      size=rng.choice([0.5, 1, 2.5, 6], (n, 2)).astype(np.float32),
+                      backend=np.zeros((n, 2), np.int32), w=rng.uniform(0, 1, n).astype(np.float32),
+                      rho=np.repeat(np.sort(rng.uniform(0, 0.9, K))[:, None], 1, axis=1).astype(np.float32),
+                      slo=0.0)
+    cps = orc.cp0_values(prob, 0, min(prob.n_plans(), 1 << 16))
+    prob.slo = f32(np.median(cps) * 1.4)
+    return prob
 
 
 def test_score_rows_and_bad_ids():
