@@ -1727,87 +1727,87 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
     __syncthreads();
     // several plans per thread (block-uniform loop): the table staging above is paid once
     for (uint64_t base = first; base < unit_end; base += stride) {
-    const uint64_t t = base + tid;
-    const bool live = t < unit_end;
-    bool bad = false;  // a row id out of range (read as 0 here): NaN scores, no feasible level
-    load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
-    const int K = P->k;
-    const bool out = live && !bad;
-    // 16-byte stores of the K per-level values when every row of cp is 16-byte aligned
-    const bool vec = cpo && (K & 3) == 0 && ((uintptr_t)cpo & 15) == 0;
-    auto put_cp = [&](auto&& value) {
-        if (!cpo || !live) return;
-        float* row = cpo + t * (uint64_t)K;
-        if (vec) {
-            for (int k = 0; k < K; k += 4)
-                *(float4*)(row + k) = make_float4(value(k), value(k + 1), value(k + 2), value(k + 3));
-        } else {
-            for (int k = 0; k < K; ++k) row[k] = value(k);
-        }
-    };
-    // fp32 corr (objective mode: U), unpressured CP and demand from the (staged) tables
-    float cc = 1.0f, cp0 = 0.0f, d = 0.0f, U = 0.0f;
-    for (int n = 0; n < N; ++n) {
-        const int e = n * R + s_id[n * WG + tid];
-        const float2 v = at[e];
-        if (P->obj)
-            U = U + v.x;
-        else
-            cc = cc * v.x;
-        d = d + dm[e];
-        float m = 0.0f;
-        uint32_t pm = P->pred[n];
-        while (pm) {
-            const int u = __builtin_ctz(pm);
-            pm &= pm - 1;
-            m = fmaxf(m, s_f[u * WG + tid]);
-        }
-        const float f = v.y + m;
-        s_f[n * WG + tid] = f;
-        if (P->sinks >> n & 1u) cp0 = fmaxf(cp0, f);
-    }
-    if (P->obj) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
-        const float G = fmaf(-P->lam_l, cp0, U);
-        put_cp([&](int k) { return out ? fmaf(-P->m32[k], d, G) : NAN; });
-        if (live) {
-            if (corr) corr[t] = out ? U : NAN;
-            if (dem) dem[t] = out ? d : NAN;
-            if (feas) feas[t] = out ? (K >= 32 ? 0xffffffffu : ((1u << K) - 1u)) : 0u;
-        }
-        continue;
-    }
-    // feasibility per level: certain in fp32 outside the band (lo, hi], else
-    // the definition's fp64 CP, evaluated by the wave (resolve_bands)
-    uint32_t bits = 0, amb = 0;
-    if (P->uniform) {
-        for (int k = 0; k < K && k < 32; ++k) {
-            if (cp0 <= P->lo[k])
-                bits |= 1u << k;
-            else if (cp0 <= P->hi[k])
-                amb |= 1u << k;
-        }
-        resolve_bands(P, s_id, out ? amb : 0u, &bits);
-        put_cp([&](int k) { return out ? cp0 * P->mk[k] : NAN; });
-    } else {
-        // per-backend pressure: each level's own fp32 CP, one level at a time
-        for (int k = 0; k < K; ++k) {
-            const float cpc = eval_cp_level(P, s_id, s_f, k);
-            uint32_t a = 0;
-            if (k < 32) {
-                if (cpc <= P->glo)
-                    bits |= 1u << k;
-                else if (cpc <= P->ghi)
-                    a = 1u << k;
+        const uint64_t t = base + tid;
+        const bool live = t < unit_end;
+        bool bad = false;  // a row id out of range (read as 0 here): NaN scores, no feasible level
+        load_plan(J, P, live ? t : n_units - 1, s_id, &bad);
+        const int K = P->k;
+        const bool out = live && !bad;
+        // 16-byte stores of the K per-level values when every row of cp is 16-byte aligned
+        const bool vec = cpo && (K & 3) == 0 && ((uintptr_t)cpo & 15) == 0;
+        auto put_cp = [&](auto&& value) {
+            if (!cpo || !live) return;
+            float* row = cpo + t * (uint64_t)K;
+            if (vec) {
+                for (int k = 0; k < K; k += 4)
+                    *(float4*)(row + k) = make_float4(value(k), value(k + 1), value(k + 2), value(k + 3));
+            } else {
+                for (int k = 0; k < K; ++k) row[k] = value(k);
             }
-            resolve_bands(P, s_id, out ? a : 0u, &bits);
-            if (live && cpo) cpo[t * (uint64_t)K + k] = out ? cpc : NAN;
+        };
+        // fp32 corr (objective mode: U), unpressured CP and demand from the (staged) tables
+        float cc = 1.0f, cp0 = 0.0f, d = 0.0f, U = 0.0f;
+        for (int n = 0; n < N; ++n) {
+            const int e = n * R + s_id[n * WG + tid];
+            const float2 v = at[e];
+            if (P->obj)
+                U = U + v.x;
+            else
+                cc = cc * v.x;
+            d = d + dm[e];
+            float m = 0.0f;
+            uint32_t pm = P->pred[n];
+            while (pm) {
+                const int u = __builtin_ctz(pm);
+                pm &= pm - 1;
+                m = fmaxf(m, s_f[u * WG + tid]);
+            }
+            const float f = v.y + m;
+            s_f[n * WG + tid] = f;
+            if (P->sinks >> n & 1u) cp0 = fmaxf(cp0, f);
         }
-    }
-    if (live) {
-        if (corr) corr[t] = out ? cc : NAN;
-        if (feas) feas[t] = out ? bits : 0u;
-        if (dem) dem[t] = out ? d : NAN;
-    }
+        if (P->obj) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
+            const float G = fmaf(-P->lam_l, cp0, U);
+            put_cp([&](int k) { return out ? fmaf(-P->m32[k], d, G) : NAN; });
+            if (live) {
+                if (corr) corr[t] = out ? U : NAN;
+                if (dem) dem[t] = out ? d : NAN;
+                if (feas) feas[t] = out ? (K >= 32 ? 0xffffffffu : ((1u << K) - 1u)) : 0u;
+            }
+            continue;
+        }
+        // feasibility per level: certain in fp32 outside the band (lo, hi], else
+        // the definition's fp64 CP, evaluated by the wave (resolve_bands)
+        uint32_t bits = 0, amb = 0;
+        if (P->uniform) {
+            for (int k = 0; k < K && k < 32; ++k) {
+                if (cp0 <= P->lo[k])
+                    bits |= 1u << k;
+                else if (cp0 <= P->hi[k])
+                    amb |= 1u << k;
+            }
+            resolve_bands(P, s_id, out ? amb : 0u, &bits);
+            put_cp([&](int k) { return out ? cp0 * P->mk[k] : NAN; });
+        } else {
+            // per-backend pressure: each level's own fp32 CP, one level at a time
+            for (int k = 0; k < K; ++k) {
+                const float cpc = eval_cp_level(P, s_id, s_f, k);
+                uint32_t a = 0;
+                if (k < 32) {
+                    if (cpc <= P->glo)
+                        bits |= 1u << k;
+                    else if (cpc <= P->ghi)
+                        a = 1u << k;
+                }
+                resolve_bands(P, s_id, out ? a : 0u, &bits);
+                if (live && cpo) cpo[t * (uint64_t)K + k] = out ? cpc : NAN;
+            }
+        }
+        if (live) {
+            if (corr) corr[t] = out ? cc : NAN;
+            if (feas) feas[t] = out ? bits : 0u;
+            if (dem) dem[t] = out ? d : NAN;
+        }
     }
 }
 
