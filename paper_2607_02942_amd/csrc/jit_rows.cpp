@@ -1,6 +1,7 @@
 // DAG-specialised kernels for candidate rows (streamed plans), generated as
 // HIP source from one problem's structure and compiled at first use with
-// hiprtc for the running device.
+// hiprtc for the running device; the same module holds a per-plan score
+// kernel for RANGE sources (gen_score).
 //
 // A row is N bytes, byte n = implementation id of node n.  Every node's table
 // (factor a = 1 - w(1 - p) and duration tau, fp32) sits in LDS as 64 float2
