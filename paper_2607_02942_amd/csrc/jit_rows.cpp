@@ -51,6 +51,7 @@ struct JitRows {
     hipFunction_t scan_u = nullptr;   // any other stride / alignment (byte loads)
     hipFunction_t sample = nullptr;
     hipFunction_t score = nullptr;    // per-plan scores of a RANGE source of 32-bit indices
+    hipFunction_t score_rows = nullptr;  // per-plan scores of rows
 };
 
 namespace {
@@ -168,35 +169,62 @@ void emit_obj_sums(std::ostringstream& o, const ProbDev& D, int n0, int n1) {
         if (D.llm >> n & 1u) o << "  u_ = u_ + e" << n << ".x; d_ = d_ + e" << n << ".y; \\\n";
 }
 
-// Per-plan scores of a RANGE source whose plan indices fit 32 bits (the
-// values of the library's score kernels, same fp32 operations in the same
-// order): digits by constant division, the DAG's recurrence unrolled, the
-// level constants as literals.  corr / SLO mode: a plan whose fp32 CP falls
-// in a level's band (lo_k, hi_k] takes that level's fp64 recurrence here,
-// from the fp64 duration table, against the SLO.
-void gen_score(std::ostringstream& o, const ProbDev& D) {
-    const int N = D.n, K = D.k;
-    o << R"(
+// Per-plan scores (the values of the library's score kernels, same fp32
+// operations in the same order) with the DAG's recurrence unrolled and the
+// level constants as literals, for a RANGE source whose plan indices fit 32
+// bits (digits by constant division; dy_score_range) or for rows
+// (dy_score_rows: a row with an id >= R_n gets NaN scores and no feasible
+// level, as in the generic kernel).  corr / SLO mode: a plan whose fp32 CP
+// falls in a level's band (lo_k, hi_k] takes that level's fp64 recurrence
+// here, from the fp64 duration table, against the SLO.
+void gen_score(std::ostringstream& o, const ProbDev& D, bool rows) {
+    const int N = D.n, K = D.k, Q = (N + 3) / 4;
+    if (rows)
+        o << R"(
+extern "C" __global__ void __launch_bounds__(256) dy_score_rows(
+    const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count, int aligned,
+    const float2* __restrict__ at, const float* __restrict__ dm, int rmax, const double* __restrict__ lat64,
+    float* __restrict__ corr, float* __restrict__ cpo, float* __restrict__ demo, unsigned* __restrict__ feas,
+    int vec) {)";
+    else
+        o << R"(
 extern "C" __global__ void __launch_bounds__(256) dy_score_range(
     unsigned long long begin, unsigned long long count, const float2* __restrict__ at,
     const float* __restrict__ dm, int rmax, const double* __restrict__ lat64, float* __restrict__ corr,
-    float* __restrict__ cpo, float* __restrict__ demo, unsigned* __restrict__ feas, int vec) {
+    float* __restrict__ cpo, float* __restrict__ demo, unsigned* __restrict__ feas, int vec) {)";
+    o << R"(
   __shared__ float2 s_tab[DY_TAB];
-  __shared__ float s_dm[DY_N * 64];
-  for (int i = threadIdx.x; i < DY_N * 64; i += blockDim.x) {
+  __shared__ float s_dm[DY_TAB];
+  for (int i = threadIdx.x; i < DY_TAB; i += blockDim.x) {
     const int n = i >> 6, e = i & 63;
-    s_dm[i] = e < rmax ? dm[n * rmax + e] : 0.0f;
+    s_dm[i] = n < DY_N && e < rmax ? dm[n * rmax + e] : 0.0f;
   }
   dy_stage(at, rmax, nullptr, s_tab, nullptr);
-  const unsigned long long stride = (unsigned long long)gridDim.x * 256ull;
-  for (unsigned long long t = (unsigned long long)blockIdx.x * 256ull + threadIdx.x; t < count; t += stride) {
-    unsigned x = (unsigned)(begin + t);
+  const unsigned long long gstride = (unsigned long long)gridDim.x * 256ull;
+  for (unsigned long long t = (unsigned long long)blockIdx.x * 256ull + threadIdx.x; t < count; t += gstride) {
 )";
-    for (int n = N - 1; n >= 0; --n) {
-        o << "    const unsigned d" << n << " = x % " << D.radix[n] << "u;";
-        if (n > 0) o << " x /= " << D.radix[n] << "u;";
-        o << "\n";
+    if (rows) {
+        o << "    unsigned ";
+        for (int q = 0; q < Q; ++q) o << (q ? ", " : "") << "w" << q;
+        o << ";\n    DY_LOAD(t";
+        for (int q = 0; q < Q; ++q) o << ", w" << q;
+        o << ")\n    unsigned bk_ = 0u;\n";
+        for (int q = 0; q < Q; ++q) o << "    bk_ |= (w" << q << " + DY_K_" << q << ") | w" << q << ";\n";
+        o << "    const bool bad = (bk_ & 0x80808080u) != 0u;\n";
+        for (int n = 0; n < N; ++n) {
+            o << "    const unsigned d" << n << " = ";
+            if (n % 4) o << "(w" << n / 4 << " >> " << 8 * (n % 4) << ") & 255u;\n";
+            else o << "w" << n / 4 << " & 255u;\n";
+        }
+    } else {
+        o << "    const bool bad = false;\n    unsigned x = (unsigned)(begin + t);\n";
+        for (int n = N - 1; n >= 0; --n) {
+            o << "    const unsigned d" << n << " = x % " << D.radix[n] << "u;";
+            if (n > 0) o << " x /= " << D.radix[n] << "u;";
+            o << "\n";
+        }
     }
+    // ids below 256: the tables' spare entries keep every read in the arrays
     for (int n = 0; n < N; ++n) o << "    const float2 e" << n << " = s_tab[" << n * 64 << " + d" << n << "];\n";
     o << "    float dd = 0.0f;\n";
     for (int n = 0; n < N; ++n) o << "    dd = dd + s_dm[" << n * 64 << " + d" << n << "];\n";
@@ -213,18 +241,20 @@ extern "C" __global__ void __launch_bounds__(256) dy_score_range(
             o << "  " << line << "\n";
         }
     }
-    o << "    if (corr) corr[t] = c;\n    if (demo) demo[t] = dd;\n";
+    o << "    const float nan_ = __builtin_nanf(\"\");\n";
+    o << "    if (corr) corr[t] = bad ? nan_ : c;\n    if (demo) demo[t] = bad ? nan_ : dd;\n";
     if (D.obj) {
         o << "    const float G = fmaf(-" << flit(D.lam_l) << ", cp, c);\n";
-        o << "    if (feas) feas[t] = " << (K >= 32 ? 0xffffffffu : ((1u << K) - 1u)) << "u;\n";
+        o << "    if (feas) feas[t] = bad ? 0u : " << (K >= 32 ? 0xffffffffu : ((1u << K) - 1u)) << "u;\n";
         o << "    if (cpo) {\n      float* row = cpo + t * " << K << "ull;\n";
-        for (int k = 0; k < K; ++k) o << "      row[" << k << "] = fmaf(-" << flit(D.m32[k]) << ", dd, G);\n";
+        for (int k = 0; k < K; ++k) o << "      row[" << k << "] = bad ? nan_ : fmaf(-" << flit(D.m32[k]) << ", dd, G);\n";
         o << "    }\n";
     } else {
         o << "    unsigned bits = 0u, amb = 0u;\n";
         for (int k = 0; k < K && k < 32; ++k)
             o << "    if (cp <= " << flit(D.lo[k]) << ") bits |= " << (1u << k) << "u; else if (cp <= " << flit(D.hi[k])
               << ") amb |= " << (1u << k) << "u;\n";
+        o << "    if (bad) bits = amb = 0u;\n";
         o << "    for (int k = 0; k < " << std::min(K, 32) << " && amb; ++k) {\n";
         o << "      if (!(amb >> k & 1u)) continue;\n";
         o << "      amb &= ~(1u << k);\n";
@@ -247,14 +277,15 @@ extern "C" __global__ void __launch_bounds__(256) dy_score_range(
         o << "      if (" << c64 << " <= " << dlit(D.slo) << ") bits |= 1u << k;\n    }\n";
         o << "    if (feas) feas[t] = bits;\n";
         o << "    if (cpo) {\n      float* row = cpo + t * " << K << "ull;\n";
+        o << "      const float cq = bad ? nan_ : cp;\n";
         if (K % 4 == 0) {
             o << "      if (vec) {\n";
             for (int k = 0; k < K; k += 4)
-                o << "        *(float4*)(row + " << k << ") = make_float4(cp * " << flit(D.mk[k]) << ", cp * " << flit(D.mk[k + 1])
-                  << ", cp * " << flit(D.mk[k + 2]) << ", cp * " << flit(D.mk[k + 3]) << ");\n";
+                o << "        *(float4*)(row + " << k << ") = make_float4(cq * " << flit(D.mk[k]) << ", cq * " << flit(D.mk[k + 1])
+                  << ", cq * " << flit(D.mk[k + 2]) << ", cq * " << flit(D.mk[k + 3]) << ");\n";
             o << "      } else {\n";
         }
-        for (int k = 0; k < K; ++k) o << "        row[" << k << "] = cp * " << flit(D.mk[k]) << ";\n";
+        for (int k = 0; k < K; ++k) o << "        row[" << k << "] = cq * " << flit(D.mk[k]) << ";\n";
         if (K % 4 == 0) o << "      }\n";
         o << "    }\n";
     }
@@ -550,7 +581,10 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
   }
 }
 )";
-    if (D.uniform || D.obj) gen_score(o, D);
+    if (D.uniform || D.obj) {
+        gen_score(o, D, false);
+        gen_score(o, D, true);
+    }
     return o.str();
 }
 
@@ -604,7 +638,8 @@ bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err) 
         hipModuleGetFunction(&j.scan, j.mod, "dy_rows_scan_a") != hipSuccess ||
         hipModuleGetFunction(&j.scan_u, j.mod, "dy_rows_scan_u") != hipSuccess ||
         hipModuleGetFunction(&j.sample, j.mod, "dy_rows_sample") != hipSuccess ||
-        ((D.uniform || D.obj) && hipModuleGetFunction(&j.score, j.mod, "dy_score_range") != hipSuccess)) {
+        ((D.uniform || D.obj) && (hipModuleGetFunction(&j.score, j.mod, "dy_score_range") != hipSuccess ||
+                                  hipModuleGetFunction(&j.score_rows, j.mod, "dy_score_rows") != hipSuccess))) {
         *err = "loading the compiled rows kernels failed";
         return false;
     }

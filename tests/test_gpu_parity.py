@@ -253,20 +253,28 @@ def tiny_problem_large(rng, n, K):
     return prob
 
 
-def test_score_rows_and_bad_ids():
+@pytest.mark.parametrize("jit,stride", [(1, 24), (1, 27), (0, 24), (0, 27)])
+def test_score_rows_and_bad_ids(jit, stride):
+    # rows through the kernel generated for the DAG (jit 1) or the generic
+    # kernel; stride 27 takes the byte-load path, its padding bytes are noise
     prob = wl.stream24()
     rows = wl.make_rows(50001, 24, 36)
     rows[77, 5] = 36  # an id out of range: NaN scores for that row only
-    d = torch.from_numpy(rows).cuda()
+    rows[901, 23] = 255
+    buf = np.random.default_rng(stride).integers(0, 256, (50001, stride)).astype(np.uint8)
+    buf[:, :24] = rows
+    d = torch.from_numpy(buf).cuda()
     with D.Plan(prob) as plan:
-        got = run_score(plan, D.rows_source(0, d, 50001, 24), 50001, prob.n_levels)
+        plan.set_option(D.DY_OPT_JIT, jit)
+        got = run_score(plan, D.rows_source(0, d, 50001, stride), 50001, prob.n_levels)
         ok = np.ones(50001, bool)
-        ok[77] = False
+        ok[[77, 901]] = False
         want = orc.score_rows(prob, np.where(ok[:, None], rows, 0))
-        assert_scores(tuple(a[ok] for a in got), tuple(a[ok] for a in want), "stream24 score")
-        assert math.isnan(got[0][77]) and got[3][77] == 0
+        assert_scores(tuple(a[ok] for a in got), tuple(a[ok] for a in want), f"stream24 score, jit {jit}")
+        for r in (77, 901):
+            assert math.isnan(got[0][r]) and math.isnan(got[2][r]) and np.isnan(got[1][r]).all() and got[3][r] == 0
         with pytest.raises(D.DyplanError) as e:
-            plan.select([D.rows_source(0, d, 50001, 24)], stream=stream())
+            plan.select([D.rows_source(0, d, 50001, stride)], stream=stream())
         assert e.value.status == D.DY_EINVAL
 
 
