@@ -1045,7 +1045,8 @@ hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sampl
     if (sample) {
         unsigned* scert = J.scert;
         unsigned long long S = J.sample_stride;
-        void* args[] = {&rows, &rows_stride, &count, &at, &rmax, &lo, &scert, &S, &aligned};
+        const float* lat = D.lat;
+        void* args[] = {&rows, &rows_stride, &count, &at, &rmax, &lo, &lat, &scert, &S, &aligned};
         const unsigned long long nsamp = (count + S - 1) / S;
         // four workgroups per CU: each adds one atomic per level at its end, and
         // those serialise across the device (8 per CU ran 1.6x longer on 2^21 samples)
@@ -1059,7 +1060,8 @@ hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sampl
     unsigned cap = J.cap;
     unsigned* ncand = J.ncand;
     int* flags = J.flags;
-    void* args[] = {&rows, &rows_stride, &count, &index_base, &at, &rmax, &table, &bin_shift, &hi, &thr,
+    const float* lat = D.lat;
+    void* args[] = {&rows, &rows_stride, &count, &index_base, &at, &rmax, &table, &bin_shift, &hi, &thr, &lat,
                     &cand, &cap, &ncand, &flags};
     hipFunction_t fn = aligned ? jr.scan : jr.scan_u;
     int per_cu = 0;
@@ -1189,7 +1191,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         const HostProb& H = h->hp[p];
         if (src[j].kind == DY_SOURCE_RANGE)
             grp[j] = H.obj ? (H.has_s2 ? G_OSWEEP_S2 : G_OSWEEP) : (H.has_s2 ? G_SWEEP_S2 : G_SWEEP);
-        else if (src[j].kind == DY_SOURCE_ROWS && H.uniform && !h->force_fp64 && jit_ready(h, p))
+        else if (src[j].kind == DY_SOURCE_ROWS && !h->force_fp64 && jit_ready(h, p))
             grp[j] = G_JIT;
         else
             grp[j] = G_GENERIC;

@@ -323,6 +323,35 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         for (int q = 0; q < Q; ++q) r += (q ? ", " : "") + std::string(p) + std::to_string(q);
         return r;
     };
+    if (!D.obj && !D.uniform) {
+        // per-backend pressure: level k's fp32 CP of the row in words w0..,
+        // from that level's durations L (the generic kernel's order)
+        o << "__device__ __noinline__ float dy_cpk(";
+        for (int q = 0; q < Q; ++q) o << "unsigned w" << q << ", ";
+        o << "const float* __restrict__ L, int rmax) {\n";
+        for (int n = 0; n < N; ++n) {
+            const int q = n / 4, b = n % 4;
+            std::vector<int> preds;
+            for (int u = 0; u < n; ++u)
+                if (D.pred[n] >> u & 1u) preds.push_back(u);
+            o << "  const float h" << n << " = L[" << n << " * rmax + (int)((w" << q;
+            if (b) o << " >> " << 8 * b;
+            o << ") & 255u)]";
+            if (!preds.empty()) {
+                std::string m = "h" + std::to_string(preds[0]);
+                for (size_t k = 1; k < preds.size(); ++k) m = "fmaxf(" + m + ", h" + std::to_string(preds[k]) + ")";
+                o << " + " << m;
+            }
+            o << ";\n";
+        }
+        std::string ck;
+        for (int n = 0; n < N; ++n)
+            if (D.sinks >> n & 1u) ck = ck.empty() ? "h" + std::to_string(n) : "fmaxf(" + ck + ", h" + std::to_string(n) + ")";
+        o << "  return " << ck << ";\n}\n";
+        o << "__device__ __constant__ const float dy_hi[DY_K] = {";
+        for (int k = 0; k < D.k; ++k) o << (k ? ", " : "") << flit(D.hi[k]);
+        o << "};\n";
+    }
     auto load_body = [&](const char* dst, const char* cond) {
         o << "  if (" << cond << ") { \\\n";
         for (int q = 0; q < Q; ++q)
@@ -446,6 +475,15 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         o << "      for (int k = 0; k < DY_K; ++k) if (fma(-dy_m64[k], (double)cp, (double)c) >= (double)thr[k]) w2 = true; \\\n";
     else
         o << "      for (int k = 0; k < DY_K; ++k) if (cp <= hi[k] && c >= thr[k]) w2 = true; \\\n";
+    if (!D.obj && !D.uniform) {
+        // per-backend pressure: the bands above are those of the unpressured
+        // CP; a row that passes them takes each level's exact fp32 CP_k (its
+        // durations from the level's table), as the generic kernel does
+        o << "      if (w2) { \\\n        w2 = false; \\\n"
+             "        for (int k = 0; k < DY_K && !w2; ++k) \\\n"
+             "          if (c >= thr[k] && dy_cpk(" << wl("y") << ", lat + (unsigned long long)k * DY_N * "
+             "(unsigned long long)rmax, rmax) <= " << flit(D.ghi) << ") w2 = true; \\\n      } \\\n";
+    }
     o << R"(      want = w2; \
     } \
     const unsigned long long m_ = __builtin_amdgcn_ballot_w64(want); \
@@ -473,7 +511,7 @@ __device__ __forceinline__ void dy_scan_body(
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count,
     unsigned long long index_base, const float2* __restrict__ at, int rmax,
     const unsigned* __restrict__ table, int bin_shift, const float* __restrict__ hi,
-    const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap,
+    const float* __restrict__ thr, const float* __restrict__ lat, DyCand* __restrict__ cand, unsigned cap,
     unsigned* __restrict__ ncand, int* __restrict__ flags) {
   __shared__ float2 s_tab[DY_TAB];
   __shared__ float s_bins[64];
@@ -531,9 +569,9 @@ __device__ __forceinline__ void dy_scan_body(
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count, \
     unsigned long long index_base, const float2* __restrict__ at, int rmax, \
     const unsigned* __restrict__ table, int bin_shift, const float* __restrict__ hi, \
-    const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap, \
+    const float* __restrict__ thr, const float* __restrict__ lat, DyCand* __restrict__ cand, unsigned cap, \
     unsigned* __restrict__ ncand, int* __restrict__ flags
-#define DY_SCAN_PASS rows, stride, count, index_base, at, rmax, table, bin_shift, hi, thr, cand, cap, ncand, flags
+#define DY_SCAN_PASS rows, stride, count, index_base, at, rmax, table, bin_shift, hi, thr, lat, cand, cap, ncand, flags
 extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_a(DY_SCAN_ARGS) { dy_scan_body<1>(DY_SCAN_PASS); }
 extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) { dy_scan_body<0>(DY_SCAN_PASS); }
 
@@ -543,11 +581,15 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
     // end; objective mode: the largest estimate fma(-m_k, D, G) (ordered key)
     if (D.obj)
         o << "#define DY_SEED_UPDATE(k) best[k] = max(best[k], dy_fkey(fmaf(-dy_m32[k], cp, c)))\n";
+    else if (!D.uniform)  // a CP inside the bands takes the level's exact fp32 CP_k against SLO (1 - (N+2)u)
+        o << "#define DY_SEED_UPDATE(k) if (cp <= lo[k] || (cp <= dy_hi[k] && dy_cpk(" << wl("w")
+          << ", lat + (unsigned long long)(k) * DY_N * (unsigned long long)rmax, rmax) <= " << flit(D.glo)
+          << ")) best[k] = max(best[k], __float_as_uint(c) + 1u)\n";
     else
         o << "#define DY_SEED_UPDATE(k) if (cp <= lo[k]) best[k] = max(best[k], __float_as_uint(c) + 1u)\n";
     o << R"(extern "C" __global__ void __launch_bounds__(256) dy_rows_sample(
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count,
-    const float2* __restrict__ at, int rmax, const float* __restrict__ lo,
+    const float2* __restrict__ at, int rmax, const float* __restrict__ lo, const float* __restrict__ lat,
     unsigned* __restrict__ scert, unsigned long long S, int aligned) {
   __shared__ float2 s_tab[DY_TAB];
   dy_stage(at, rmax, nullptr, s_tab, nullptr);

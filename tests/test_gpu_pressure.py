@@ -80,15 +80,51 @@ def test_batch_mixes_uniform_and_per_class():
         assert_choices(got[r], orc.select_range(probs[r], 0, 12 ** 6), f"batch[{r}]")
 
 
-def test_rows_per_class():
-    prob = wl.per_class(wl.stream24(), (1.0, 0.5))
+@pytest.mark.parametrize("jit", [1, 0])
+@pytest.mark.parametrize("factors", [(1.0, 0.5), (0.3, 1.0)])
+def test_rows_per_class(jit, factors):
+    # the kernel generated for the DAG (jit 1: bands of the unpressured CP,
+    # then each level's exact CP_k) or the generic kernel
+    prob = wl.per_class(wl.stream24(), factors)
     n = 300007
     rows = wl.make_rows(n, 24, 36, row_begin=999)
     want = orc.select_rows(prob, rows, index_base=999)
     with D.Plan(prob) as plan:
+        plan.set_option(D.DY_OPT_JIT, jit)
         d = torch.from_numpy(rows).cuda()
         got = plan.select([D.rows_source(0, d, n, 24, 999)], stream=stream())[0]
-    assert_choices(got, want, "stream24 per class rows")
+    assert_choices(got, want, f"stream24 per class {factors} rows, jit {jit}")
+
+
+@pytest.mark.parametrize("jit", [1, 0])
+def test_rows_random_pressure(jit):
+    # random DAGs, every (level, backend) its own rho, SLO at a CP quantile;
+    # rows drawn from the whole plan space, so boundary plans are present
+    rng = np.random.default_rng(4242)
+    for trial in range(8):
+        n = int(rng.integers(3, 10))
+        R = 6
+        edges = np.array([(i, j) for i in range(n) for j in range(i + 1, n) if rng.random() < 0.4],
+                         np.int32).reshape(-1, 2)
+        K, B = int(rng.integers(1, 9)), 3
+        prob = wl.Problem(n_nodes=n, edges=edges, radix=rng.integers(1, R + 1, n).astype(np.int32),
+                          p=rng.uniform(0.4, 1.0, (n, R)).astype(np.float32),
+                          tau=rng.integers(1, 6, (n, R)).astype(np.float32),
+                          size=rng.choice([0.5, 1, 2.5], (n, R)).astype(np.float32),
+                          backend=rng.integers(0, B, (n, R)).astype(np.int32),
+                          w=rng.uniform(0, 1, n).astype(np.float32),
+                          rho=rng.uniform(0, 0.9, (K, B)).astype(np.float32), slo=0.0)
+        total = prob.n_plans()
+        m = 40000
+        idx = rng.integers(0, total, m)
+        rows = np.stack([orc.decode(prob, int(i)) for i in idx]).astype(np.uint8)
+        cps = orc.cp0_values(prob, rows=rows)
+        prob.slo = float(np.float32(np.quantile(cps, rng.choice([0.1, 0.5])) * 1.5))
+        want = orc.select_rows(prob, rows)
+        with D.Plan(prob) as plan:
+            plan.set_option(D.DY_OPT_JIT, jit)
+            got = plan.select([D.rows_source(0, torch.from_numpy(rows).cuda(), m, n)], stream=stream())[0]
+        assert_choices(got, want, f"trial {trial}, jit {jit}")
 
 
 def test_small_capacity_reseeds_per_class():
