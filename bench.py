@@ -55,8 +55,15 @@ PEAK_HBM = 8.0e12                 # bytes/s
 # figure is reported only while these files are unchanged.
 KERNEL_SOURCES = ("paper_2607_02942_amd/csrc/kernels.hip", "paper_2607_02942_amd/csrc/jit_rows.cpp",
                   "paper_2607_02942_amd/csrc/dyplan_internal.h")
-DOMINANT = {"stream24": "dy_rows_scan_a", "stream24_obj": "dy_rows_scan_a"}  # else the sweep kernel
-SCORE_KERNEL = "k_score"
+DOMINANT = {"stream24": "dy_rows_scan_a", "stream24_obj": "dy_rows_scan_a",
+            "stream24_perclass": "dy_rows_scan_a"}  # else the sweep kernel
+
+
+def score_kernel(prob, per_class):
+    """The kernel dy_plan_score runs for a 2^26-plan range of `prob`."""
+    if per_class:
+        return "k_score"
+    return "dy_score_range" if prob.n_nodes > 16 else "k_score_fast"
 OBJ_SWEEP = "k_sweep_obj"
 
 
@@ -106,7 +113,8 @@ def ingest_pmc(workload, fetch_db, write_db, calib_fetch_db, calib_write_db, cal
             raise SystemExit(f"no kernel matching {key!r} in {sorted(means)}")
         return hits[0]
     if workload.endswith("_score"):
-        kern = SCORE_KERNEL
+        import paper_2607_02942_amd.workload as wlm
+        kern = score_kernel(wlm.by_name(workload.split("_")[0]), "_perclass" in workload)
     else:
         kern = DOMINANT.get(workload, OBJ_SWEEP if workload.endswith("_obj") else "k_sweep")
     kname, fetch = pick(_pmc_means(fetch_db, "FETCH_SIZE"), kern)
@@ -235,7 +243,8 @@ def score_bench(args, torch, D, wl, stream, tkey):
            "unit": "plans/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
            "higher_is_better": True, "dtype": "f32", "data": "synthetic",
            "config": {"workload": prob.name, "plans": n, "levels": K, "outputs": "corr, cp[K], demand, feas"},
-           "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
+           "roofline": {"bound": "hbm", "kernel": score_kernel(prob, args.pressure == "per-class"),
+                        "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9,
                         "unit": "GB/s", "frac": achieved / PEAK_HBM, "per_unit": f"{per_plan:.0f} B written per plan",
                         "traffic": stored_traffic(tkey)}}
     print(json.dumps(res), flush=True)
