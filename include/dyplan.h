@@ -208,8 +208,11 @@ enum {
     DY_OPT_SAMPLE_STRIDE = 2,   /* the seeding pre-pass scores 1 of every S work units (default 128) */
     DY_OPT_CAND_CAPACITY = 3,   /* candidate slots per source (default 1 << 16, min 16) */
     DY_OPT_FORCE_FP64 = 4,      /* 1: decide every level with the exhaustive fp64 path (default 0) */
-    DY_OPT_JIT = 5,             /* 1: score rows, and per-plan scores of RANGE sources, with kernels
-                                   generated for the problem (hiprtc, default 1) */
+    DY_OPT_JIT = 5,             /* kernels generated for the problem (hiprtc): 0 never; 1 (default) for
+                                   rows, per-plan scores of 32-bit RANGE sources of DAGs above 16 nodes,
+                                   and the sweep of 32-bit RANGE sources of at least 2^24 plans of
+                                   uniform-pressure corr / SLO problems in plans of at most 8 problems;
+                                   2 as 1 but the sweep for RANGE sources of any size */
     DY_OPT_GRAPH = 6            /* 1: replay a call that repeats the previous one (same sources) from a
                                    HIP graph of its launches (default 1; calls with DY_OPT_TIMING on
                                    launch directly); results are identical */

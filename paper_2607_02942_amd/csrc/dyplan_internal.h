@@ -12,6 +12,7 @@ constexpr int WG = 256;          // threads per workgroup of the scoring kernels
 constexpr int NMAX = DY_MAX_NODES;
 constexpr int KMAX = DY_MAX_LEVELS;
 constexpr int NBINS = 64;        // lane-resident prefilter table: one bin per lane
+constexpr int NBINS2 = 256;      // bins of the generated sweep's prefilter (one shift-and-mask operation)
 constexpr int NSLOT = 64;        // per-level atomic slots of the seeding pass (spreads contention)
 constexpr int CERT_WAVES = 8;    // waves per source in certification when sources are few
 
@@ -48,7 +49,7 @@ struct ProbDev {
     double slo;
     uint32_t cp_lo_bits, cp_hi_bits;  // fp32 bounds of the unpressured CP over all plans
     int32_t bin_shift;        // prefilter bin = (bits(CP) >> bin_shift) mod 64
-    int32_t pad0;
+    int32_t jsh;              // generated sweep: prefilter bin = (bits(CP) >> jsh) mod 256 (jsh = 18), 0: unused
     // seeding pass (uniform mode): levels sorted by lo (descending); for a CP
     // in bin j, jtab[j] levels of that order are certainly feasible (a lower
     // bound: the bin's largest CP decides)
@@ -119,6 +120,7 @@ struct JobDev {
     uint32_t* scert;          // [KMAX][NSLOT] best certainly-feasible fp32 corr found by the pre-pass, bits + 1 (0: none)
     float* thr;               // [KMAX] candidate thresholds
     uint32_t* table;          // [NBINS] prefilter thresholds (fp32 bits)
+    uint32_t* table2;         // [NBINS2] the same on the generated sweep's finer bins (P->jsh)
     Cand* cand;               // [cap]
     uint32_t* ncand;
     int32_t* flags;

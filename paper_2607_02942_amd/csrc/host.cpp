@@ -35,6 +35,7 @@ struct JitRows {
     hipFunction_t sample = nullptr;
     hipFunction_t score = nullptr;
     hipFunction_t score_rows = nullptr;
+    hipFunction_t sweep = nullptr;
 };
 bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err);
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
@@ -75,6 +76,7 @@ struct Scratch {
     uint32_t* scert = nullptr;
     float* thr = nullptr;
     uint32_t* table = nullptr;
+    uint32_t* table2 = nullptr;
     uint32_t* ncand = nullptr;
     int32_t* flags = nullptr;
     dy_choice* out = nullptr;
@@ -411,6 +413,7 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
     size_t o_cd = take(njobs * KMAX * CERT_WAVES * sizeof(double));
     size_t o_thr = take(njobs * KMAX * sizeof(float));
     size_t o_table = take(njobs * NBINS * sizeof(uint32_t));
+    size_t o_table2 = take(njobs * NBINS2 * sizeof(uint32_t));
     const size_t res_out = 0;
     const size_t res_ncand = align_up(njobs * km * sizeof(dy_choice), 8);
     const size_t res_flags = res_ncand + njobs * sizeof(uint32_t);
@@ -438,6 +441,7 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
     s.cert_d = (double*)(s.d + o_cd);
     s.thr = (float*)(s.d + o_thr);
     s.table = (uint32_t*)(s.d + o_table);
+    s.table2 = (uint32_t*)(s.d + o_table2);
     s.res_bytes = res_bytes;
     s.out = (dy_choice*)(s.d + o_res + res_out);
     s.ncand = (uint32_t*)(s.d + o_res + res_ncand);
@@ -750,6 +754,9 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         int s = 2;
         while (s < 31 && ((D.cp_hi_bits >> s) - (D.cp_lo_bits >> s)) > 62u) ++s;
         D.bin_shift = s;
+        // the generated sweep bins the CP at 2^18 patterns per bin into 256 bins
+        // (one masked half-word read forms the LDS offset) when they cover it
+        D.jsh = ((D.cp_hi_bits >> 18) - (D.cp_lo_bits >> 18)) <= (uint32_t)(NBINS2 - 2) ? 18 : 0;
         // seeding pass: levels by decreasing band, and per bin how many of them
         // every CP in the bin certainly meets (decided by the bin's largest CP)
         std::vector<int> order(K);
@@ -987,7 +994,13 @@ int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value) {
             h->cand_cap = (uint32_t)value;
             return DY_OK;
         case DY_OPT_FORCE_FP64: h->force_fp64 = value ? 1 : 0; return DY_OK;
-        case DY_OPT_JIT: h->use_jit = value ? 1 : 0; return DY_OK;
+        case DY_OPT_JIT:
+            if (value < 0 || value > 2) {
+                h->err = "DY_OPT_JIT takes 0, 1 or 2";
+                return DY_EINVAL;
+            }
+            h->use_jit = (int)value;
+            return DY_OK;
         default:
             h->err = "unknown option";
             return DY_EINVAL;
@@ -1020,6 +1033,7 @@ struct PassPlan {
     int npre[kSweepGroups] = {};
     int ry[kSweepGroups] = {};            // R_y shared by every source of a sweep group, else -1
     int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
+    int njit[kSweepGroups] = {};          // trailing sources of the group that run their generated sweep
     int kmax = 1;                         // most levels of any source
     int ncol = 1;                         // most nodes of any source of the generic group
     int before(int g) const {             // jobs stored ahead of group g
@@ -1104,16 +1118,48 @@ void launch_table_all(const JobDev* d, int ntot, hipStream_t s,
 }
 
 // Scoring pass of the sweep and generic groups.
-void launch_main(const JobDev* d, const PassPlan& pp, hipStream_t s,
+// The generated sweep of one RANGE source (host copy J of its job).
+hipError_t launch_jit_sweep(const dy_plan* h, const JobDev& J, int p, hipStream_t s) {
+    const ProbDev& D = h->hdesc[p];
+    unsigned long long blk_first = J.blk_first, nblk = J.nblk, begin = J.begin, count = J.count;
+    const float2* at = D.at;
+    const float2* atx = D.atx;
+    const float2* aty = D.aty;
+    int rmax = D.rmax;
+    const unsigned* table = D.jsh ? J.table2 : J.table;
+    const float* thr = J.thr;
+    Cand* cand = J.cand;
+    unsigned cap = J.cap;
+    unsigned* ncand = J.ncand;
+    int* flags = J.flags;
+    constexpr unsigned long long kMaxBlocks = 1ull << 22;
+    for (unsigned long long off = 0; off < nblk; off += kMaxBlocks * 256ull) {
+        unsigned long long unit_off = off;
+        const unsigned gx = (unsigned)std::min<unsigned long long>((nblk - off + 255) / 256, kMaxBlocks);
+        void* args[] = {&unit_off, &blk_first, &nblk, &begin, &count, &at, &atx, &aty, &rmax, &table, &thr,
+                        &cand, &cap, &ncand, &flags};
+        const hipError_t e = hipModuleLaunchKernel(h->jit[p].sweep, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+// Main scoring pass.  hjobs: host copies of the jobs at d (for the sources of
+// the sweep groups that run their generated sweep, the last pp.njit[g] of the
+// group); null when pp.njit is all zero.
+void launch_main(const dy_plan* h, const JobDev* d, const JobDev* hjobs, const PassPlan& pp, hipStream_t s,
                  const std::function<void(hipError_t, const char*)>& chk) {
     auto chunks = [&](const JobDev* base, int n, auto&& fn) {
         for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
     };
-    for (int g = 0; g < kSweepGroups; ++g)
-        chunks(d + pp.before(g), pp.n[g], [&](const JobDev* b, int n) {
+    for (int g = 0; g < kSweepGroups; ++g) {
+        chunks(d + pp.before(g), pp.n[g] - pp.njit[g], [&](const JobDev* b, int n) {
             chk(launch_sweep(b, n, (g & 1) != 0, g >= G_OSWEEP, pp.units[g], pp.npre[g], pp.npre_c[g], pp.ry[g], s),
                 "sweep");
         });
+        for (int q = pp.before(g) + pp.n[g] - pp.njit[g]; q < pp.before(g) + pp.n[g]; ++q)
+            chk(launch_jit_sweep(h, hjobs[q], (int)(hjobs[q].prob - h->d_probs), s), "generated sweep");
+    }
     chunks(d + pp.before(G_GENERIC), pp.n[G_GENERIC],
            [&](const JobDev* b, int n) { chk(launch_scan(b, n, pp.units[G_GENERIC], pp.ncol, s), "scan"); });
 }
@@ -1196,11 +1242,27 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         else
             grp[j] = G_GENERIC;
     }
+    // RANGE sources of 32-bit plan indices of a uniform-pressure corr / SLO
+    // problem run the sweep generated for their DAG, when the plan has few
+    // problems (one compilation each), the source is large enough to repay
+    // it (2^24 plans; every source with DY_OPT_JIT 2) and it compiles; they
+    // go last in their group, whose library sweep launch covers the others
+    std::vector<char> jsw(n_src, 0);
+    const uint64_t jit_min = h->use_jit >= 2 ? 1 : (1ull << 24);
+    if (h->use_jit && !h->force_fp64 && h->hp.size() <= 8)
+        for (int j = 0; j < n_src; ++j) {
+            const int p = src[j].problem;
+            const HostProb& H = h->hp[p];
+            if (src[j].kind == DY_SOURCE_RANGE && H.uniform && !H.obj && src[j].count >= jit_min &&
+                src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_ready(h, p) && h->jit[p].sweep)
+                jsw[j] = 1;
+        }
     std::vector<int> order;
     order.reserve(n_src);
     for (int g = 0; g < kGroups; ++g)
-        for (int j = 0; j < n_src; ++j)
-            if (grp[j] == g) order.push_back(j);
+        for (int pass = 0; pass < 2; ++pass)
+            for (int j = 0; j < n_src; ++j)
+                if (grp[j] == g && jsw[j] == pass) order.push_back(j);
     uint64_t plans = 0, all_units = 0;
     PassPlan pp;
     std::vector<JobDev> jobs((size_t)n_src);
@@ -1213,6 +1275,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         J.scert = S.scert + (size_t)q * KMAX * NSLOT;
         J.thr = S.thr + (size_t)q * KMAX;
         J.table = S.table + (size_t)q * NBINS;
+        J.table2 = S.table2 + (size_t)q * NBINS2;
         J.cand = S.cand + (size_t)q * cap;
         J.ncand = S.ncand + q;
         J.flags = S.flags + q;
@@ -1240,6 +1303,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         J.sample_stride = (uint32_t)stride;
         J.units = sweep ? J.nblk : J.count;
         ++pp.n[g];
+        if (g < kSweepGroups && jsw[j]) ++pp.njit[g];
         if (g < G_JIT) {
             pp.units[g] = std::max(pp.units[g], J.units);
             pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
@@ -1291,7 +1355,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     };
     auto issue_mid = [&](hipStream_t st, const Check& ck) {
         if (h->timing) ck(hipEventRecord(h->ev[1], st), "hipEventRecord");
-        launch_main(S.d_jobs, pp, st, ck);
+        launch_main(h, S.d_jobs, jobs.data(), pp, st, ck);
         jit_pass(jobs.data(), n3, pp.n[G_JIT], false, st, ck);
         if (h->timing) ck(hipEventRecord(h->ev[2], st), "hipEventRecord");
     };
@@ -1422,7 +1486,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
             for (int c = 0; c < n_re; c += 65535)
                 chk(launch_reseed(S.d_fb + c, std::min(65535, n_re - c), s), "reseed");
             launch_table_all(S.d_fb, n_re, s, chk);
-            launch_main(S.d_fb, rp, s, chk);
+            launch_main(h, S.d_fb, nullptr, rp, s, chk);
             jit_pass(re.data(), rp.before(G_JIT), rp.n[G_JIT], false, s, chk);
             launch_certify_all(S.d_fb, n_re, cert_waves, h, s, chk);
         }

@@ -338,8 +338,8 @@ __device__ bool last_block(uint32_t* counter, uint32_t expected) {
 }
 
 // Per level candidate threshold T_k from the seed slots, and the 64-bin
-// prefilter table; resets the job's candidate count and flags for the scoring
-// pass.  Called by every thread of one block (>= 64 threads).
+// prefilter table (and, for problems with a generated sweep, its 256-bin
+// table); resets the job's candidate count and flags for the scoring pass.  Called by every thread of one block (>= 64 threads).
 __device__ void build_table(JD J, PD P) {
     __shared__ float s_thr[KMAX];
     const int lane = threadIdx.x;
@@ -371,6 +371,22 @@ __device__ void build_table(JD J, PD P) {
                 if (P->hi[k] >= low) g = fminf(g, s_thr[k]);
         }
         J->table[lane] = __float_as_uint(g);
+    }
+    if (P->jsh != 0 && !obj) {
+        // the generated sweep's table: bin i of NBINS2 covers fp32 patterns
+        // [B << jsh, (B+1) << jsh), B = i (mod NBINS2), B >= cp_lo >> jsh
+        const uint32_t s = (uint32_t)P->jsh;
+        const uint32_t blo = P->cp_lo_bits >> s;
+        for (int i = lane; i < NBINS2; i += blockDim.x) {
+            const uint32_t B = blo + (((uint32_t)i - blo) & (uint32_t)(NBINS2 - 1));
+            uint32_t lowbits = B << s;
+            if (lowbits < P->cp_lo_bits) lowbits = P->cp_lo_bits;
+            const float low = __uint_as_float(lowbits);
+            float g = INFINITY;
+            for (int k = 0; k < P->k; ++k)
+                if (P->hi[k] >= low) g = fminf(g, s_thr[k]);
+            J->table2[i] = __float_as_uint(g);
+        }
     }
     if (lane == 0) {
         *J->ncand = 0u;

@@ -253,6 +253,35 @@ def tiny_problem_large(rng, n, K):
     return prob
 
 
+def test_generated_sweep_random_problems():
+    # DY_OPT_JIT 2: every RANGE source runs the sweep generated for its DAG
+    # (default: sources of 2^24 plans and more); ragged ranges, the SLO at
+    # a CP quantile, one or two sinks besides y, an edge x -> y or not
+    rng = np.random.default_rng(6060)
+    for trial in range(7):
+        n = int(rng.integers(3, 12))
+        rmax = min(int(rng.choice([3, 6, 12])), int(3e6 ** (1.0 / n)))  # at most ~3e6 plans
+        prob = tiny_problem(rng, n, rmax, int(rng.integers(1, 9)), 2, True, edge_p=float(rng.choice([0.2, 0.5])))
+        total = prob.n_plans()
+        begin = int(rng.integers(0, max(1, total // 5)))
+        count = int(total - begin - rng.integers(0, max(1, total // 5)))
+        want = orc.select_range(prob, begin, count)
+        with D.Plan(prob) as plan:
+            plan.set_option(D.DY_OPT_JIT, 2)
+            for call in range(2):  # the second call replays the captured graph
+                got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+                assert_choices(got, want, f"trial {trial} ({n} nodes, radix <= {rmax}), call {call}")
+
+
+@pytest.mark.parametrize("begin,count", [(0, 1 << 20), (123457, 1000003), (429981696 - 777777, 777777)])
+def test_forkjoin8_generated_sweep(begin, count):
+    prob = wl.forkjoin8()
+    with D.Plan(prob) as plan:
+        plan.set_option(D.DY_OPT_JIT, 2)
+        got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+    assert_choices(got, orc.select_range(prob, begin, count), f"forkjoin8 [{begin}+{count}] generated sweep")
+
+
 @pytest.mark.parametrize("jit,stride", [(1, 24), (1, 27), (0, 24), (0, 27)])
 def test_score_rows_and_bad_ids(jit, stride):
     # rows through the kernel generated for the DAG (jit 1) or the generic
