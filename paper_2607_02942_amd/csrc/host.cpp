@@ -1434,6 +1434,8 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     dy_stats stats{};
     stats.plans = plans;
     stats.n_jobs = n_src;
+    stats.generated_jobs = pp.n[G_JIT];
+    for (int g = 0; g < kSweepGroups; ++g) stats.generated_jobs += pp.njit[g];
     if (h->timing) {
         float ms = 0.0f;
         if (hipEventElapsedTime(&ms, h->ev[1], h->ev[2]) == hipSuccess) stats.main_ms = ms;

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_status_strings_and_selftest():
     lib = D.lib()
-    assert lib.dy_abi_version() == 2
+    assert lib.dy_abi_version() == 3
     assert lib.dy_selftest() == 0
     for st in (D.DY_OK, D.DY_EINVAL, D.DY_ENOTDAG, D.DY_ELIMIT, D.DY_ENOMEM, D.DY_EDEVICE):
         assert lib.dy_status_str(st).decode() not in ("", "unknown status")
@@ -45,6 +45,7 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(D.DySource) == 48
     assert ctypes.sizeof(D.DyProblem) == 104
     assert ctypes.sizeof(D.DyObjective) == 56
+    assert ctypes.sizeof(D.DyStats) == 40
 
 
 def _struct(prob):
