@@ -56,7 +56,7 @@ PEAK_HBM = 8.0e12                 # bytes/s
 KERNEL_SOURCES = ("paper_2607_02942_amd/csrc/kernels.hip", "paper_2607_02942_amd/csrc/jit_rows.cpp",
                   "paper_2607_02942_amd/csrc/dyplan_internal.h")
 DOMINANT = {"stream24": "dy_rows_scan_a", "stream24_obj": "dy_rows_scan_a",
-            "stream24_perclass": "dy_rows_scan_a", "forkjoin8": "dy_sweep",
+            "stream24_perclass": "dy_rows_scan_a", "forkjoin8": "dy_sweep", "forkjoin8_obj": "dy_sweep",
             "layered10": "dy_sweep"}  # else the library's sweep kernel
 
 
@@ -397,7 +397,10 @@ def main():
     else:
         f = obj_sweep_work_per_plan(prob) if objs else sweep_work_per_plan(prob)
         achieved = kern_plans_s * f
-        kname = OBJ_SWEEP if objs else ("dy_sweep (generated for the DAG)" if generated else "k_sweep")
+        if generated:
+            kname = "dy_sweep (generated for the DAG" + (", objective)" if objs else ")")
+        else:
+            kname = OBJ_SWEEP if objs else "k_sweep
         roof = {"bound": "alu", "kernel": kname, "achieved": achieved / 1e12,
                 "peak": PEAK_VALU / 1e12, "unit": "TFLOP/s", "frac": achieved / PEAK_VALU,
                 "peak_packed_fp32": PEAK_VALU_PACKED / 1e12, "frac_vs_packed_fp32": achieved / PEAK_VALU_PACKED,

@@ -1125,6 +1125,9 @@ hipError_t launch_jit_sweep(const dy_plan* h, const JobDev& J, int p, hipStream_
     const float2* at = D.at;
     const float2* atx = D.atx;
     const float2* aty = D.aty;
+    const float* dem = D.dem;
+    const float* demx = D.demx;
+    const float* demy = D.demy;
     int rmax = D.rmax;
     const unsigned* table = D.jsh ? J.table2 : J.table;
     const float* thr = J.thr;
@@ -1136,8 +1139,8 @@ hipError_t launch_jit_sweep(const dy_plan* h, const JobDev& J, int p, hipStream_
     for (unsigned long long off = 0; off < nblk; off += kMaxBlocks * 256ull) {
         unsigned long long unit_off = off;
         const unsigned gx = (unsigned)std::min<unsigned long long>((nblk - off + 255) / 256, kMaxBlocks);
-        void* args[] = {&unit_off, &blk_first, &nblk, &begin, &count, &at, &atx, &aty, &rmax, &table, &thr,
-                        &cand, &cap, &ncand, &flags};
+        void* args[] = {&unit_off, &blk_first, &nblk, &begin, &count, &at, &atx, &aty, &dem, &demx, &demy,
+                        &rmax, &table, &thr, &cand, &cap, &ncand, &flags};
         const hipError_t e = hipModuleLaunchKernel(h->jit[p].sweep, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
         if (e != hipSuccess) return e;
     }
@@ -1242,7 +1245,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         else
             grp[j] = G_GENERIC;
     }
-    // RANGE sources of 32-bit plan indices of a uniform-pressure corr / SLO
+    // RANGE sources of 32-bit plan indices of a uniform-pressure or objective
     // problem run the sweep generated for their DAG, when the plan has few
     // problems (one compilation each), the source is large enough to repay
     // it (2^24 plans; every source with DY_OPT_JIT 2) and it compiles; they
@@ -1253,7 +1256,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         for (int j = 0; j < n_src; ++j) {
             const int p = src[j].problem;
             const HostProb& H = h->hp[p];
-            if (src[j].kind == DY_SOURCE_RANGE && H.uniform && !H.obj && src[j].count >= jit_min &&
+            if (src[j].kind == DY_SOURCE_RANGE && (H.uniform || H.obj) && src[j].count >= jit_min &&
                 src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_ready(h, p) && h->jit[p].sweep)
                 jsw[j] = 1;
         }

@@ -293,20 +293,25 @@ extern "C" __global__ void __launch_bounds__(256) dy_score_range(
     o << "  }\n}\n";
 }
 
-// The prefix-shared sweep for RANGE sources of one problem under uniform
-// pressure (corr / SLO mode), block indices below 2^32: the library's k_sweep
-// with the DAG fixed at compile time.  A lane takes one prefix block (an
-// assignment of nodes 0..N-3): digits by constant division, the prefix
-// recurrence with its exact predecessor maxima (no per-edge selects), then the
-// inner pair (x, y) swept in lockstep with the y table in scalar registers;
-// per plan one multiply, one add (and a max for a second sink), the bin's
-// threshold from LDS and a compare.  A row with a hit is re-scored with the
-// exact per-level test and its candidates appended, as in k_sweep.  Same fp32
-// operations in the same order as k_sweep, so both give identical candidates.
+// The prefix-shared sweep for RANGE sources of one problem, block indices
+// below 2^32, under uniform pressure (corr / SLO mode) or the objective: the
+// library's k_sweep / k_sweep_obj with the DAG fixed at compile time.  A lane
+// takes one prefix block (an assignment of nodes 0..N-3): digits by constant
+// division, the prefix recurrence with its exact predecessor maxima (no
+// per-edge selects), then the inner pair (x, y) swept in lockstep with the y
+// table in scalar registers; per plan (corr mode) one multiply, one add (and a
+// max for a second sink), the bin's threshold from LDS and a compare.  A row
+// with a hit is re-scored with the exact per-level test and its candidates
+// appended.  Same fp32 operations in the same order as the library's sweeps,
+// so both give identical candidates.
 void gen_sweep(std::ostringstream& o, const ProbDev& D) {
-    const int N = D.n, NP = D.npre, xn = D.xnode, yn = D.ynode;
+    const int NP = D.npre, xn = D.xnode, yn = D.ynode;
+    const bool obj = D.obj != 0;
     const bool exy = D.edge_xy != 0, s2 = D.pre_sinks != 0 || !exy;
     const uint32_t pmx = D.pred[xn], pmy = D.pred[yn] & ~(1u << xn), pms = D.pre_sinks;
+    // byte offset of the bin's threshold: with 256 bins at shift 18, bits
+    // 18..25 of the binned value times 4 = (bits >> 16) & 0x3fc, one masked
+    // read of the upper half-word; else the 64 bins at the problem's shift
     const int nb = D.jsh ? NBINS2 : NBINS;
     const int sh = (D.jsh ? D.jsh : D.bin_shift) - 2;
     const unsigned msk = (unsigned)(nb - 1) << 2;
@@ -320,17 +325,22 @@ void gen_sweep(std::ostringstream& o, const ProbDev& D) {
 extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     unsigned long long unit_off, unsigned long long blk_first, unsigned long long nblk, unsigned long long begin,
     unsigned long long count, const float2* __restrict__ at, const float2* __restrict__ atx,
-    const float2* __restrict__ aty, int rmax, const unsigned* __restrict__ table, const float* __restrict__ thr,
+    const float2* __restrict__ aty, const float* __restrict__ dem, const float* __restrict__ demx,
+    const float* __restrict__ demy, int rmax, const unsigned* __restrict__ table, const float* __restrict__ thr,
     DyCand* __restrict__ cand, unsigned cap, unsigned* __restrict__ ncand, int* __restrict__ flags) {
   __shared__ float s_bins[)" << nb << R"(];
   __shared__ float2 s_pat[)" << NP << R"( * 64];
-  const unsigned long long t0 = unit_off + (unsigned long long)blockIdx.x * 256ull;
+)";
+    if (obj) o << "  __shared__ float s_pd[" << NP << " * 64];\n";
+    o << R"(  const unsigned long long t0 = unit_off + (unsigned long long)blockIdx.x * 256ull;
   if (t0 >= nblk) return;
   for (int i = threadIdx.x; i < )" << nb << R"(; i += 256) s_bins[i] = __uint_as_float(table[i]);
   for (int i = threadIdx.x; i < )" << NP << R"( * 64; i += 256) {
     const int n = i >> 6, e = i & 63;
     s_pat[i] = e < rmax ? at[n * rmax + e] : make_float2(1.0f, 0.0f);
-  }
+)";
+    if (obj) o << "    s_pd[i] = e < rmax ? dem[n * rmax + e] : 0.0f;\n";
+    o << R"(  }
   __syncthreads();
   const unsigned long long t = t0 + threadIdx.x;
   const bool live = t < nblk;
@@ -342,10 +352,14 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
         if (n > 0) o << " x_ /= " << D.radix[n] << "u;";
         o << "\n";
     }
-    o << "  float pc = 1.0f;\n";
+    // prefix: corr mode the product of the factors, objective mode the sums
+    // of u and of d (node order, as the library's prefix evaluation)
+    o << "  float pc = " << (obj ? "0.0f" : "1.0f") << ";\n";
+    if (obj) o << "  float pd = 0.0f;\n";
     for (int n = 0; n < NP; ++n) {
         o << "  const float2 v" << n << " = s_pat[" << n * 64 << " + d" << n << "];\n";
-        o << "  pc = pc * v" << n << ".x;\n";
+        o << "  pc = pc " << (obj ? "+" : "*") << " v" << n << ".x;\n";
+        if (obj) o << "  pd = pd + s_pd[" << n * 64 << " + d" << n << "];\n";
         std::string m;
         for (int u = 0; u < n; ++u)
             if (D.pred[n] >> u & 1u) m = m.empty() ? "f" + std::to_string(u) : "fmaxf(" + m + ", f" + std::to_string(u) + ")";
@@ -353,38 +367,56 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     }
     o << "  const float px = " << maxof(pmx, "f") << ", py = " << maxof(pmy, "f") << ", ps = " << maxof(pms, "f")
       << ";\n";
-    // byte offset of the bin's threshold: with 256 bins at shift 18, bits
-    // 18..25 of the CP times 4 = (bits >> 16) & 0x3fc, one masked read of the
-    // upper half-word; else the 64 bins at the problem's shift
     o << "  float2 vy[" << D.ry << "];\n";
-    o << "#pragma unroll\n  for (int j = 0; j < " << D.ry << "; ++j) vy[j] = aty[j];\n";
+    if (obj) o << "  float dy[" << D.ry << "];\n";
+    o << "#pragma unroll\n  for (int j = 0; j < " << D.ry << "; ++j) {\n    vy[j] = aty[j];\n";
+    if (obj) o << "    dy[j] = demy[j];\n";
+    o << "  }\n";
     o << "#pragma unroll 1\n";  // one copy of the row and its rare path (code size)
     o << "  for (int ix = 0; ix < " << D.rx << "; ++ix) {\n";
     o << "    const float2 vx = atx[ix];\n";
-    o << "    const float fx = vx.y + px;\n    const float cx = pc * vx.x;\n";
+    o << "    const float fx = vx.y + px;\n";
+    if (obj)
+        o << "    const float ux = pc + vx.x;\n    const float dx = pd + demx[ix];\n";
+    else
+        o << "    const float cx = pc * vx.x;\n";
     o << "    const float M = " << (exy ? "fmaxf(py, fx)" : "py") << ";\n";
     if (s2) o << "    const float S2 = " << (exy ? "ps" : "fmaxf(ps, fx)") << ";\n";
+    // one plan: corr mode (cc, cp); objective mode G = u + U_x - lambda_l T
+    // (one fused rounding) and D = D_x + d_y, binned by D
+    auto plan = [&](const char* ind) {
+        o << ind << "float cp = vy[j].y + M;\n";
+        if (s2) o << ind << "cp = fmaxf(cp, S2);\n";
+        if (obj) {
+            o << ind << "const float cc = fmaf(" << flit(-D.lam_l) << ", cp, ux + vy[j].x);\n";
+            o << ind << "const float bv = dx + dy[j];\n";
+        } else {
+            o << ind << "const float cc = cx * vy[j].x;\n";
+            o << ind << "const float bv = cp;\n";
+        }
+    };
     o << "    unsigned long long hit = 0ull;\n";
     o << "#pragma unroll\n    for (int j = 0; j < " << D.ry << "; ++j) {\n";
-    o << "      float cp = vy[j].y + M;\n";
-    if (s2) o << "      cp = fmaxf(cp, S2);\n";
-    o << "      const float cc = cx * vy[j].x;\n";
-    o << "      const float th = *(const float*)((const char*)s_bins + ((__float_as_uint(cp) >> " << sh << "u) & " << msk << "u));\n";
+    plan("      ");
+    o << "      const float th = *(const float*)((const char*)s_bins + ((__float_as_uint(bv) >> " << sh << "u) & " << msk
+      << "u));\n";
     o << "      hit |= __builtin_amdgcn_ballot_w64(cc >= th);\n    }\n";
     o << "    if (hit && live && (hit >> (threadIdx.x & 63) & 1ull)) {\n";
     o << "      const unsigned long long base = (b * " << D.rx << "ull + (unsigned long long)ix) * " << D.ry << "ull;\n";
     o << "      for (int j = 0; j < " << D.ry << "; ++j) {\n";
-    o << "        float cp = vy[j].y + M;\n";
-    if (s2) o << "        cp = fmaxf(cp, S2);\n";
-    o << "        const float cc = cx * vy[j].x;\n";
+    plan("        ");
     o << "        const unsigned long long idx = base + (unsigned long long)j;\n";
     o << "        bool want = false;\n";
-    for (int k = 0; k < D.k; ++k)
-        o << "        want = want || (cp <= " << flit(D.hi[k]) << " && cc >= thr[" << k << "]);\n";
+    for (int k = 0; k < D.k; ++k) {
+        if (obj)
+            o << "        want = want || (fma(-" << dlit(D.m64[k]) << ", (double)bv, (double)cc) >= (double)thr[" << k << "]);\n";
+        else
+            o << "        want = want || (cp <= " << flit(D.hi[k]) << " && cc >= thr[" << k << "]);\n";
+    }
     o << "        if (idx - begin < count && want) {\n";
     o << "          const unsigned slot = atomicAdd(ncand, 1u);\n";
     o << "          if (slot < cap) {\n            cand[slot].index = idx;\n            cand[slot].corr = cc;\n"
-         "            cand[slot].cp = cp;\n          } else {\n            atomicOr(flags, " << (int)JF_OVERFLOW << ");\n"
+         "            cand[slot].cp = bv;\n          } else {\n            atomicOr(flags, " << (int)JF_OVERFLOW << ");\n"
          "          }\n        }\n      }\n    }\n  }\n}\n";
 }
 
@@ -723,7 +755,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
         gen_score(o, D, false);
         gen_score(o, D, true);
     }
-    if (D.uniform && !D.obj && D.npre >= 1 && D.xnode >= 0) gen_sweep(o, D);
+    if ((D.uniform || D.obj) && D.npre >= 1 && D.xnode >= 0) gen_sweep(o, D);
     return o.str();
 }
 
@@ -779,7 +811,7 @@ bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err) 
         hipModuleGetFunction(&j.sample, j.mod, "dy_rows_sample") != hipSuccess ||
         ((D.uniform || D.obj) && (hipModuleGetFunction(&j.score, j.mod, "dy_score_range") != hipSuccess ||
                                   hipModuleGetFunction(&j.score_rows, j.mod, "dy_score_rows") != hipSuccess)) ||
-        (D.uniform && !D.obj && D.npre >= 1 && D.xnode >= 0 &&
+        ((D.uniform || D.obj) && D.npre >= 1 && D.xnode >= 0 &&
          hipModuleGetFunction(&j.sweep, j.mod, "dy_sweep") != hipSuccess)) {
         *err = "loading the compiled rows kernels failed";
         return false;

@@ -372,9 +372,10 @@ __device__ void build_table(JD J, PD P) {
         }
         J->table[lane] = __float_as_uint(g);
     }
-    if (P->jsh != 0 && !obj) {
+    if (P->jsh != 0) {
         // the generated sweep's table: bin i of NBINS2 covers fp32 patterns
         // [B << jsh, (B+1) << jsh), B = i (mod NBINS2), B >= cp_lo >> jsh
+        // (objective mode: patterns of D, as above)
         const uint32_t s = (uint32_t)P->jsh;
         const uint32_t blo = P->cp_lo_bits >> s;
         for (int i = lane; i < NBINS2; i += blockDim.x) {
@@ -383,8 +384,12 @@ __device__ void build_table(JD J, PD P) {
             if (lowbits < P->cp_lo_bits) lowbits = P->cp_lo_bits;
             const float low = __uint_as_float(lowbits);
             float g = INFINITY;
-            for (int k = 0; k < P->k; ++k)
-                if (P->hi[k] >= low) g = fminf(g, s_thr[k]);
+            if (obj) {
+                for (int k = 0; k < P->k; ++k) g = fminf(g, obj_bin_threshold(s_thr[k], P->m64[k], low));
+            } else {
+                for (int k = 0; k < P->k; ++k)
+                    if (P->hi[k] >= low) g = fminf(g, s_thr[k]);
+            }
             J->table2[i] = __float_as_uint(g);
         }
     }

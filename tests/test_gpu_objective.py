@@ -144,6 +144,37 @@ def test_small_dags_full_space(n, radix, seed):
     assert_obj_choices(got, orc.obj_select_range(prob, obj, 0, total), f"dag{n}")
 
 
+@pytest.mark.parametrize("n,radix,seed", [(3, [4, 1, 6], 3), (5, [3, 4, 2, 5, 3], 4), (6, [12] * 6, 5),
+                                          (12, [3] * 12, 6), (8, [5] * 8, 8)])
+def test_generated_sweep_small_dags(n, radix, seed):
+    # DY_OPT_JIT 2: the sweep generated for the DAG on every RANGE source
+    prob = small_dag(n, radix, seed)
+    rng = np.random.default_rng(seed + 100)
+    obj = wl.Objective(cost=(prob.tau * prob.size).astype(np.float32),
+                       levels=rng.uniform(0, 4, 1 + seed % 5).astype(np.float32),
+                       lambda_f=float(rng.uniform(-1, 2)), lambda_c=float(rng.uniform(-0.1, 0.2)),
+                       lambda_l=float(rng.uniform(0, 0.5)), lambda_ld=float(rng.uniform(0, 0.3)),
+                       beta=float(rng.uniform(-1, 2)), effort=float(rng.uniform(0, 1)),
+                       is_tool=(rng.random(n) < 0.3).astype(np.int32))
+    total = int(np.prod(radix))
+    begin, count = total // 9, total - total // 9 - total // 11
+    with D.Plan((prob, obj)) as plan:
+        plan.set_option(D.DY_OPT_JIT, 2)
+        for call in range(2):
+            got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+            assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"dag{n} call {call}")
+
+
+@pytest.mark.parametrize("begin,count", [(123457, 1000003), (429981696 - 777777, 777777)])
+def test_forkjoin8_generated_sweep(begin, count):
+    prob = wl.forkjoin8()
+    obj = with_tools(wl.paper_objective(prob, levels=np.linspace(0.0, 6.0, 12), lambda_l=0.4), 8, (0, 7))
+    with D.Plan((prob, obj)) as plan:
+        plan.set_option(D.DY_OPT_JIT, 2)
+        got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+    assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"forkjoin8[{begin}+{count}] generated")
+
+
 def test_batch_mixed_with_corr_selection():
     # objective and corr / SLO problems in one call: both sweep groups run together
     probs = [wl.batch6_request(r) for r in range(4)]
