@@ -400,7 +400,7 @@ def main():
         if generated:
             kname = "dy_sweep (generated for the DAG" + (", objective)" if objs else ")")
         else:
-            kname = OBJ_SWEEP if objs else "k_sweep
+            kname = OBJ_SWEEP if objs else "k_sweep"
         roof = {"bound": "alu", "kernel": kname, "achieved": achieved / 1e12,
                 "peak": PEAK_VALU / 1e12, "unit": "TFLOP/s", "frac": achieved / PEAK_VALU,
                 "peak_packed_fp32": PEAK_VALU_PACKED / 1e12, "frac_vs_packed_fp32": achieved / PEAK_VALU_PACKED,
