@@ -212,8 +212,8 @@ enum {
     DY_OPT_FORCE_FP64 = 4,      /* 1: decide every level with the exhaustive fp64 path (default 0) */
     DY_OPT_JIT = 5,             /* kernels generated for the problem (hiprtc): 0 never; 1 (default) for
                                    rows, per-plan scores of 32-bit RANGE sources of DAGs above 16 nodes,
-                                   and the sweep of 32-bit RANGE sources of at least 2^24 plans of
-                                   uniform-pressure or objective problems in plans of at most 8 problems;
+                                   and the sweep of 32-bit RANGE sources of at least 2^24 plans in
+                                   plans of at most 8 problems;
                                    2 as 1 but the sweep for RANGE sources of any size */
     DY_OPT_GRAPH = 6            /* 1: replay a call that repeats the previous one (same sources) from a
                                    HIP graph of its launches (default 1; calls with DY_OPT_TIMING on

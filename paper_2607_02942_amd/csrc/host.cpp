@@ -1128,6 +1128,7 @@ hipError_t launch_jit_sweep(const dy_plan* h, const JobDev& J, int p, hipStream_
     const float* dem = D.dem;
     const float* demx = D.demx;
     const float* demy = D.demy;
+    const float* lat = D.lat;
     int rmax = D.rmax;
     const unsigned* table = D.jsh ? J.table2 : J.table;
     const float* thr = J.thr;
@@ -1139,7 +1140,7 @@ hipError_t launch_jit_sweep(const dy_plan* h, const JobDev& J, int p, hipStream_
     for (unsigned long long off = 0; off < nblk; off += kMaxBlocks * 256ull) {
         unsigned long long unit_off = off;
         const unsigned gx = (unsigned)std::min<unsigned long long>((nblk - off + 255) / 256, kMaxBlocks);
-        void* args[] = {&unit_off, &blk_first, &nblk, &begin, &count, &at, &atx, &aty, &dem, &demx, &demy,
+        void* args[] = {&unit_off, &blk_first, &nblk, &begin, &count, &at, &atx, &aty, &dem, &demx, &demy, &lat,
                         &rmax, &table, &thr, &cand, &cap, &ncand, &flags};
         const hipError_t e = hipModuleLaunchKernel(h->jit[p].sweep, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
         if (e != hipSuccess) return e;
@@ -1245,8 +1246,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         else
             grp[j] = G_GENERIC;
     }
-    // RANGE sources of 32-bit plan indices of a uniform-pressure or objective
-    // problem run the sweep generated for their DAG, when the plan has few
+    // RANGE sources of 32-bit plan indices run the sweep generated for their DAG, when the plan has few
     // problems (one compilation each), the source is large enough to repay
     // it (2^24 plans; every source with DY_OPT_JIT 2) and it compiles; they
     // go last in their group, whose library sweep launch covers the others
@@ -1256,7 +1256,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         for (int j = 0; j < n_src; ++j) {
             const int p = src[j].problem;
             const HostProb& H = h->hp[p];
-            if (src[j].kind == DY_SOURCE_RANGE && (H.uniform || H.obj) && src[j].count >= jit_min &&
+            if (src[j].kind == DY_SOURCE_RANGE && src[j].count >= jit_min &&
                 src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_ready(h, p) && h->jit[p].sweep)
                 jsw[j] = 1;
         }

@@ -326,8 +326,9 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     unsigned long long unit_off, unsigned long long blk_first, unsigned long long nblk, unsigned long long begin,
     unsigned long long count, const float2* __restrict__ at, const float2* __restrict__ atx,
     const float2* __restrict__ aty, const float* __restrict__ dem, const float* __restrict__ demx,
-    const float* __restrict__ demy, int rmax, const unsigned* __restrict__ table, const float* __restrict__ thr,
-    DyCand* __restrict__ cand, unsigned cap, unsigned* __restrict__ ncand, int* __restrict__ flags) {
+    const float* __restrict__ demy, const float* __restrict__ lat, int rmax, const unsigned* __restrict__ table,
+    const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap, unsigned* __restrict__ ncand,
+    int* __restrict__ flags) {
   __shared__ float s_bins[)" << nb << R"(];
   __shared__ float2 s_pat[)" << NP << R"( * 64];
 )";
@@ -403,6 +404,54 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     o << "      hit |= __builtin_amdgcn_ballot_w64(cc >= th);\n    }\n";
     o << "    if (hit && live && (hit >> (threadIdx.x & 63) & 1ull)) {\n";
     o << "      const unsigned long long base = (b * " << D.rx << "ull + (unsigned long long)ix) * " << D.ry << "ull;\n";
+    if (!obj && !D.uniform) {
+        // per-backend pressure: per level, the row's exact fp32 CP_k from the
+        // level's durations (prefix, x and y), skipped when no plan of the row
+        // can reach the level's threshold or its band; a plan is appended
+        // once, with its unpressured CP, which the bands refer to
+        auto lmax = [&](uint32_t mask) {
+            std::string m;
+            for (int u = 0; u < NP; ++u)
+                if (mask >> u & 1u) m = m.empty() ? "g" + std::to_string(u) : "fmaxf(" + m + ", g" + std::to_string(u) + ")";
+            return m.empty() ? std::string("0.0f") : m;
+        };
+        o << "      const float cmax = cx * " << flit(D.ay_max) << ";\n";
+        o << "      float cp0_lb = " << flit(D.ty_min) << " + M;\n";
+        if (s2) o << "      cp0_lb = fmaxf(cp0_lb, S2);\n";
+        o << "      unsigned long long done = 0ull;\n";
+        o << "#pragma unroll 1\n      for (int k = 0; k < DY_K; ++k) {\n";
+        o << "        const float th_k = thr[k];\n";
+        o << "        if (!(cmax >= th_k && cp0_lb <= dy_hi[k])) continue;\n";
+        o << "        const float* L = lat + (unsigned long long)k * DY_N * (unsigned long long)rmax;\n";
+        for (int n = 0; n < NP; ++n) {
+            std::string m;
+            for (int u = 0; u < n; ++u)
+                if (D.pred[n] >> u & 1u) m = m.empty() ? "g" + std::to_string(u) : "fmaxf(" + m + ", g" + std::to_string(u) + ")";
+            o << "        const float g" << n << " = L[" << n << " * rmax + (int)d" << n << "] + " << (m.empty() ? "0.0f" : m) << ";\n";
+        }
+        o << "        const float qx = " << lmax(pmx) << ", qy = " << lmax(pmy) << ", qs = " << lmax(pms) << ";\n";
+        o << "        const float fxk = L[" << xn << " * rmax + ix] + qx;\n";
+        o << "        const float Mk = " << (exy ? "fmaxf(qy, fxk)" : "qy") << ";\n";
+        if (s2) o << "        const float S2k = " << (exy ? "qs" : "fmaxf(qs, fxk)") << ";\n";
+        // y's entries from memory, not the register copy: a loop index
+        // into it would move the whole array to scratch
+        o << "#pragma unroll 1\n        for (int j = 0; j < " << D.ry << "; ++j) {\n";
+        o << "          if (done >> j & 1ull) continue;\n";
+        o << "          float cpk = L[" << yn << " * rmax + j] + Mk;\n";
+        if (s2) o << "          cpk = fmaxf(cpk, S2k);\n";
+        o << "          const float2 wy = aty[j];\n";
+        o << "          const float cc = cx * wy.x;\n";
+        o << "          const unsigned long long idx = base + (unsigned long long)j;\n";
+        o << "          if (cpk <= " << flit(D.ghi) << " && cc >= th_k && idx - begin < count) {\n";
+        o << "            float cp0 = wy.y + M;\n";
+        if (s2) o << "            cp0 = fmaxf(cp0, S2);\n";
+        o << "            done |= 1ull << j;\n";
+        o << "            const unsigned slot = atomicAdd(ncand, 1u);\n";
+        o << "            if (slot < cap) {\n              cand[slot].index = idx;\n              cand[slot].corr = cc;\n"
+             "              cand[slot].cp = cp0;\n            } else {\n              atomicOr(flags, " << (int)JF_OVERFLOW
+          << ");\n            }\n          }\n        }\n      }\n    }\n  }\n}\n";
+        return;
+    }
     o << "      for (int j = 0; j < " << D.ry << "; ++j) {\n";
     plan("        ");
     o << "        const unsigned long long idx = base + (unsigned long long)j;\n";
@@ -755,7 +804,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
         gen_score(o, D, false);
         gen_score(o, D, true);
     }
-    if ((D.uniform || D.obj) && D.npre >= 1 && D.xnode >= 0) gen_sweep(o, D);
+    if (D.npre >= 1 && D.xnode >= 0) gen_sweep(o, D);
     return o.str();
 }
 
@@ -811,8 +860,7 @@ bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err) 
         hipModuleGetFunction(&j.sample, j.mod, "dy_rows_sample") != hipSuccess ||
         ((D.uniform || D.obj) && (hipModuleGetFunction(&j.score, j.mod, "dy_score_range") != hipSuccess ||
                                   hipModuleGetFunction(&j.score_rows, j.mod, "dy_score_rows") != hipSuccess)) ||
-        ((D.uniform || D.obj) && D.npre >= 1 && D.xnode >= 0 &&
-         hipModuleGetFunction(&j.sweep, j.mod, "dy_sweep") != hipSuccess)) {
+        (D.npre >= 1 && D.xnode >= 0 && hipModuleGetFunction(&j.sweep, j.mod, "dy_sweep") != hipSuccess)) {
         *err = "loading the compiled rows kernels failed";
         return false;
     }

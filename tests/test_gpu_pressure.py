@@ -14,7 +14,7 @@ from oracle import oracle as orc  # noqa: E402
 from paper_2607_02942_amd import dyplan as D  # noqa: E402
 from paper_2607_02942_amd import workload as wl  # noqa: E402
 
-from test_gpu_parity import assert_choices, assert_scores, run_score, select, stream  # noqa: E402
+from test_gpu_parity import assert_choices, assert_scores, run_score, select, stream, tiny_problem  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -125,6 +125,40 @@ def test_rows_random_pressure(jit):
             plan.set_option(D.DY_OPT_JIT, jit)
             got = plan.select([D.rows_source(0, torch.from_numpy(rows).cuda(), m, n)], stream=stream())[0]
         assert_choices(got, want, f"trial {trial}, jit {jit}")
+
+
+@pytest.mark.parametrize("factors", [(1.0, 0.5), (0.3, 1.0)])
+@pytest.mark.parametrize("begin,count", [(0, 1 << 20), (123457, 1000003), (429981696 - 777777, 777777)])
+def test_forkjoin8_per_class_generated_sweep(factors, begin, count):
+    # DY_OPT_JIT 2: the sweep generated for the DAG, its rare path each
+    # admitted level's exact CP_k; the library sweep (DY_OPT_JIT 0) beside it
+    prob = wl.per_class(wl.forkjoin8(), factors)
+    want = orc.select_range(prob, begin, count)
+    for jit in (2, 0):
+        with D.Plan(prob) as plan:
+            plan.set_option(D.DY_OPT_JIT, jit)
+            got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+            assert plan.stats().generated_jobs == (1 if jit else 0)
+        assert_choices(got, want, f"forkjoin8 {factors} [{begin}+{count}], jit {jit}")
+
+
+def test_generated_sweep_random_pressure():
+    # random DAGs, every (level, backend) its own rho, ragged ranges, the SLO
+    # at a CP quantile; every source through the generated sweep
+    rng = np.random.default_rng(9191)
+    for trial in range(8):
+        n = int(rng.integers(3, 12))
+        rmax = min(int(rng.choice([3, 6, 12])), int(3e6 ** (1.0 / n)))  # at most ~3e6 plans
+        prob = tiny_problem(rng, n, rmax, int(rng.integers(1, 9)), 3, False, edge_p=float(rng.choice([0.2, 0.5])))
+        total = prob.n_plans()
+        begin = int(rng.integers(0, max(1, total // 5)))
+        count = int(total - begin - rng.integers(0, max(1, total // 5)))
+        want = orc.select_range(prob, begin, count)
+        with D.Plan(prob) as plan:
+            plan.set_option(D.DY_OPT_JIT, 2)
+            for call in range(2):  # the second call replays the captured graph
+                got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+                assert_choices(got, want, f"trial {trial} ({n} nodes, radix <= {rmax}), call {call}")
 
 
 def test_small_capacity_reseeds_per_class():
