@@ -793,6 +793,14 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
             D.ay_max = std::max(D.ay_max, v.x);
             D.ty_min = std::min(D.ty_min, v.y);
         }
+        {
+            const int ry = std::min(pb.radix[N - 1], 64);
+            const float2* ay = (const float2*)(img.data() + L.at) + (size_t)(N - 1) * R;
+            std::vector<int> ord(ry);
+            for (int i = 0; i < ry; ++i) ord[i] = i;
+            std::stable_sort(ord.begin(), ord.end(), [&](int u, int v) { return ay[u].x > ay[v].x; });
+            for (int i = 0; i < 64; ++i) D.yord[i] = (uint8_t)(i < ry ? ord[i] : 0);
+        }
         D.demx = N >= 2 ? D.dem + (size_t)(N - 2) * R : (const float*)(base + L.dz);
         D.demy = D.dem + (size_t)(N - 1) * R;
         H.n = N;

@@ -435,14 +435,18 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
         if (s2) o << "        const float S2k = " << (exy ? "qs" : "fmaxf(qs, fxk)") << ";\n";
         // y's entries from memory, not the register copy: a loop index
         // into it would move the whole array to scratch
-        o << "#pragma unroll 1\n        for (int j = 0; j < " << D.ry << "; ++j) {\n";
+        // y by decreasing factor: corr falls along the loop, which stops at
+        // the first plan below the level's threshold
+        o << "#pragma unroll 1\n        for (int jj = 0; jj < " << D.ry << "; ++jj) {\n";
+        o << "          const int j = dy_yord[jj];\n";
+        o << "          const float2 wy = aty[j];\n";
+        o << "          const float cc = cx * wy.x;\n";
+        o << "          if (!(cc >= th_k)) break;\n";
         o << "          if (done >> j & 1ull) continue;\n";
         o << "          float cpk = L[" << yn << " * rmax + j] + Mk;\n";
         if (s2) o << "          cpk = fmaxf(cpk, S2k);\n";
-        o << "          const float2 wy = aty[j];\n";
-        o << "          const float cc = cx * wy.x;\n";
         o << "          const unsigned long long idx = base + (unsigned long long)j;\n";
-        o << "          if (cpk <= " << flit(D.ghi) << " && cc >= th_k && idx - begin < count) {\n";
+        o << "          if (cpk <= " << flit(D.ghi) << " && idx - begin < count) {\n";
         o << "            float cp0 = wy.y + M;\n";
         if (s2) o << "            cp0 = fmaxf(cp0, S2);\n";
         o << "            done |= 1ull << j;\n";
@@ -528,6 +532,11 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         o << "__device__ __constant__ const float dy_hi[DY_K] = {";
         for (int k = 0; k < D.k; ++k) o << (k ? ", " : "") << flit(D.hi[k]);
         o << "};\n";
+        if (D.ry >= 1 && D.ry <= 64) {
+            o << "__device__ __constant__ const unsigned char dy_yord[" << D.ry << "] = {";
+            for (int j = 0; j < D.ry; ++j) o << (j ? ", " : "") << (int)D.yord[j];
+            o << "};\n";
+        }
     }
     auto load_body = [&](const char* dst, const char* cond) {
         o << "  if (" << cond << ") { \\\n";
