@@ -57,7 +57,8 @@ KERNEL_SOURCES = ("paper_2607_02942_amd/csrc/kernels.hip", "paper_2607_02942_amd
                   "paper_2607_02942_amd/csrc/dyplan_internal.h")
 DOMINANT = {"stream24": "dy_rows_scan_a", "stream24_obj": "dy_rows_scan_a",
             "stream24_perclass": "dy_rows_scan_a", "forkjoin8": "dy_sweep", "forkjoin8_obj": "dy_sweep",
-            "layered10": "dy_sweep"}  # else the library's sweep kernel
+            "layered10": "dy_sweep", "forkjoin8_perclass": "dy_sweep",
+            "layered10_perclass": "dy_sweep"}  # else the library's sweep kernel
 
 
 def score_kernel(prob, per_class):

@@ -95,6 +95,7 @@ struct ProbDev {
     float ay_max;             // largest factor a of node y (fp32 table)
     float ty_min;             // smallest duration tau of node y
     uint8_t yord[64];         // ids of node y by decreasing fp32 factor a (ties by id), radix <= 64
+    float lymin[KMAX];        // per-backend pressure: per level, node y's smallest fp32 duration
 };
 
 struct Cand {

@@ -801,6 +801,14 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
             std::stable_sort(ord.begin(), ord.end(), [&](int u, int v) { return ay[u].x > ay[v].x; });
             for (int i = 0; i < 64; ++i) D.yord[i] = (uint8_t)(i < ry ? ord[i] : 0);
         }
+        for (int k = 0; k < KMAX; ++k) {
+            float m = INFINITY;
+            if (!obj && k < K) {
+                const float* ly = (const float*)(img.data() + L.lat) + ((size_t)k * N + (N - 1)) * R;
+                for (int i = 0; i < pb.radix[N - 1]; ++i) m = std::min(m, ly[i]);
+            }
+            D.lymin[k] = m;
+        }
         D.demx = N >= 2 ? D.dem + (size_t)(N - 2) * R : (const float*)(base + L.dz);
         D.demy = D.dem + (size_t)(N - 1) * R;
         H.n = N;

@@ -433,6 +433,9 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
         o << "        const float fxk = L[" << xn << " * rmax + ix] + qx;\n";
         o << "        const float Mk = " << (exy ? "fmaxf(qy, fxk)" : "qy") << ";\n";
         if (s2) o << "        const float S2k = " << (exy ? "qs" : "fmaxf(qs, fxk)") << ";\n";
+        // every CP_k of the row above the band when y's fastest entry is
+        o << "        if (dy_lymin[k] + Mk > " << flit(D.ghi) << ") continue;\n";
+        if (s2) o << "        if (S2k > " << flit(D.ghi) << ") continue;\n";
         // y's entries from memory, not the register copy: a loop index
         // into it would move the whole array to scratch
         // y by decreasing factor: corr falls along the loop, which stops at
@@ -531,6 +534,9 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         o << "  return " << ck << ";\n}\n";
         o << "__device__ __constant__ const float dy_hi[DY_K] = {";
         for (int k = 0; k < D.k; ++k) o << (k ? ", " : "") << flit(D.hi[k]);
+        o << "};\n";
+        o << "__device__ __constant__ const float dy_lymin[DY_K] = {";
+        for (int k = 0; k < D.k; ++k) o << (k ? ", " : "") << flit(D.lymin[k]);
         o << "};\n";
         if (D.ry >= 1 && D.ry <= 64) {
             o << "__device__ __constant__ const unsigned char dy_yord[" << D.ry << "] = {";

@@ -645,6 +645,28 @@ __device__ void general_row(PD P, JD J, uint64_t b, int big, int ix, float cx, f
         float M, S2;
         level_row<NPRE>(P, lat, dg, b, big, ix, s_f, M, S2);
         const CS float* laty = lat + P->ynode * R;
+        if (P->lymin[k] + M > P->ghi || (HAS_S2 && S2 > P->ghi)) continue;  // every CP_k of the row above
+        if (ry <= 64) {
+            // y by decreasing factor: corr falls along the loop, which stops
+            // at the first plan below the level's threshold
+            for (int jj = 0; jj < ry; ++jj) {
+                const int iy = P->yord[jj];
+                const float2 vy = aty[iy];
+                const float cc = cx * vy.x;
+                if (!(cc >= thr)) break;
+                if (done >> iy & 1ull) continue;
+                float cp = laty[iy] + M;
+                if (HAS_S2) cp = fmaxf(cp, S2);
+                const uint64_t idx = base + (uint64_t)iy;
+                if (cp <= P->ghi && idx - J->begin < J->count) {
+                    float cp0 = vy.y + M0;
+                    if (HAS_S2) cp0 = fmaxf(cp0, S20);
+                    append_cand(J, idx, cc, cp0);
+                    done |= 1ull << iy;
+                }
+            }
+            continue;
+        }
         for (int iy = 0; iy < ry; ++iy) {
             if (ry <= 64 && (done >> iy & 1ull)) continue;
             float cp = laty[iy] + M;
@@ -807,11 +829,28 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
             level_row<NPRE>(P, lat, dg, b, J->big, ix, s_f, Mk, S2k);
             const CS float* laty = lat + P->ynode * P->rmax;
             float best = -1.0f;
-            for (int iy = 0; iy < ry; ++iy) {
-                float cp = laty[iy] + Mk;
-                if (HAS_S2) cp = fmaxf(cp, S2k);
-                if (cp <= P->glo && live && (base + (uint64_t)iy - J->begin < J->count))
-                    best = fmaxf(best, cx * aty[iy].x);
+            // no plan of the row is certainly feasible when y's fastest
+            // implementation (or the other sinks) already misses the band
+            if (P->lymin[k] + Mk > P->glo || (HAS_S2 && S2k > P->glo)) {
+            } else if (ry <= 64) {
+                // y by decreasing factor: the first plan certainly feasible
+                // (and in the range) has the row's best corr at this level
+                for (int jj = 0; jj < ry; ++jj) {
+                    const int iy = P->yord[jj];
+                    float cp = laty[iy] + Mk;
+                    if (HAS_S2) cp = fmaxf(cp, S2k);
+                    if (cp <= P->glo && live && (base + (uint64_t)iy - J->begin < J->count)) {
+                        best = cx * aty[iy].x;
+                        break;
+                    }
+                }
+            } else {
+                for (int iy = 0; iy < ry; ++iy) {
+                    float cp = laty[iy] + Mk;
+                    if (HAS_S2) cp = fmaxf(cp, S2k);
+                    if (cp <= P->glo && live && (base + (uint64_t)iy - J->begin < J->count))
+                        best = fmaxf(best, cx * aty[iy].x);
+                }
             }
             const uint32_t e = wave_max_u32(best >= 0.0f ? __float_as_uint(best) + 1u : 0u);
             if (lane == 0) s_red[k][wave] = e;
