@@ -1059,7 +1059,7 @@ struct PassPlan {
     }
 };
 
-// Rows sources of uniform-pressure problems run the problem's generated
+// Rows sources run the problem's generated
 // kernels (one launch per source; the host copies of the job carry the args).
 hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sample, hipStream_t s) {
     const ProbDev& D = h->hdesc[problem];
