@@ -673,7 +673,7 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         // durations from the level's table), as the generic kernel does
         o << "      if (w2) { \\\n        w2 = false; \\\n"
              "        for (int k = 0; k < DY_K && !w2; ++k) \\\n"
-             "          if (c >= thr[k] && dy_cpk(" << wl("y") << ", lat + (unsigned long long)k * DY_N * "
+             "          if (c >= thr[k] && cp <= dy_hi[k] && dy_cpk(" << wl("y") << ", lat + (unsigned long long)k * DY_N * "
              "(unsigned long long)rmax, rmax) <= " << flit(D.ghi) << ") w2 = true; \\\n      } \\\n";
     }
     o << R"(      want = w2; \
@@ -773,10 +773,12 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
     // end; objective mode: the largest estimate fma(-m_k, D, G) (ordered key)
     if (D.obj)
         o << "#define DY_SEED_UPDATE(k) best[k] = max(best[k], dy_fkey(fmaf(-dy_m32[k], cp, c)))\n";
-    else if (!D.uniform)  // a CP inside the bands takes the level's exact fp32 CP_k against SLO (1 - (N+2)u)
-        o << "#define DY_SEED_UPDATE(k) if (cp <= lo[k] || (cp <= dy_hi[k] && dy_cpk(" << wl("w")
+    else if (!D.uniform)  // a CP inside the bands takes the level's exact fp32 CP_k against SLO (1 - (N+2)u),
+                          // only for a sample that would raise the thread's value
+        o << "#define DY_SEED_UPDATE(k) { const unsigned e_ = __float_as_uint(c) + 1u; if (e_ > best[k] && "
+             "(cp <= lo[k] || (cp <= dy_hi[k] && dy_cpk(" << wl("w")
           << ", lat + (unsigned long long)(k) * DY_N * (unsigned long long)rmax, rmax) <= " << flit(D.glo)
-          << ")) best[k] = max(best[k], __float_as_uint(c) + 1u)\n";
+          << "))) best[k] = e_; }\n";
     else
         o << "#define DY_SEED_UPDATE(k) if (cp <= lo[k]) best[k] = max(best[k], __float_as_uint(c) + 1u)\n";
     o << R"(extern "C" __global__ void __launch_bounds__(256) dy_rows_sample(
