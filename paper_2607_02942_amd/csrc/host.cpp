@@ -36,6 +36,7 @@ struct JitRows {
     hipFunction_t score = nullptr;
     hipFunction_t score_rows = nullptr;
     hipFunction_t sweep = nullptr;
+    hipFunction_t seed = nullptr;
 };
 bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err);
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
@@ -1109,18 +1110,45 @@ hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sampl
     return hipModuleLaunchKernel(fn, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
 }
 
-// Seeding pre-pass of the sweep and generic groups (jobs stored in group order at d).
-void launch_seed(const JobDev* d, const PassPlan& pp, hipStream_t s,
+// The generated seeding pass of job J (problem p), one sample per thread.
+hipError_t launch_jit_seed(const dy_plan* h, const JobDev& J, int p, hipStream_t s) {
+    const ProbDev& D = h->hdesc[p];
+    unsigned long long S = J.sample_stride, units = J.nblk * (unsigned long long)D.rx;
+    unsigned long long nsamp = (units + S - 1) / S, blk_first = J.blk_first, begin = J.begin, count = J.count;
+    const float2* at = D.at;
+    const float2* atx = D.atx;
+    const float2* aty = D.aty;
+    int rmax = D.rmax;
+    const unsigned* jtab = (const unsigned*)((const char*)(h->d_probs + p) + offsetof(ProbDev, jtab));
+    unsigned* scert = J.scert;
+    void* args[] = {&nsamp, &S, &units, &blk_first, &begin, &count, &at, &atx, &aty, &rmax, &jtab, &scert};
+    const unsigned gx = (unsigned)((nsamp + 255) / 256);
+    return hipModuleLaunchKernel(h->jit[p].seed, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
+}
+
+// Seeding pre-pass of the sweep and generic groups (jobs stored in group order at d; host copies at
+// hjobs).  Jobs of the generated sweep whose problem has a generated seeding pass take it.
+void launch_seed(const dy_plan* h, const JobDev* d, const JobDev* hjobs, const PassPlan& pp, hipStream_t s,
                  const std::function<void(hipError_t, const char*)>& chk) {
     auto chunks = [&](const JobDev* base, int n, auto&& fn) {
         for (int c = 0; c < n; c += 65535) fn(base + c, std::min(65535, n - c));
     };
-    for (int g = 0; g < kSweepGroups; ++g)
-        chunks(d + pp.before(g), pp.n[g], [&](const JobDev* b, int n) {
+    for (int g = 0; g < kSweepGroups; ++g) {
+        const int lib = pp.n[g] - pp.njit[g];
+        auto lib_launch = [&](const JobDev* b, int n) {
             chk(launch_sample_sweep(b, n, (g & 1) != 0, g >= G_OSWEEP, pp.samples[g], pp.npre[g], pp.npre_c[g],
                                     pp.kmax, s),
                 "sample");
-        });
+        };
+        chunks(d + pp.before(g), lib, lib_launch);
+        for (int q = pp.before(g) + lib; q < pp.before(g) + pp.n[g]; ++q) {
+            const int p = (int)(hjobs[q].prob - h->d_probs);
+            if (h->jit[p].seed)
+                chk(launch_jit_seed(h, hjobs[q], p, s), "generated seeding");
+            else
+                lib_launch(d + q, 1);
+        }
+    }
     chunks(d + pp.before(G_GENERIC), pp.n[G_GENERIC],
            [&](const JobDev* b, int n) {
                chk(launch_sample_generic(b, n, pp.samples[G_GENERIC], pp.ncol, s), "sample");
@@ -1271,7 +1299,6 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     if (h->use_jit && !h->force_fp64 && h->hp.size() <= 8)
         for (int j = 0; j < n_src; ++j) {
             const int p = src[j].problem;
-            const HostProb& H = h->hp[p];
             if (src[j].kind == DY_SOURCE_RANGE && src[j].count >= jit_min &&
                 src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_ready(h, p) && h->jit[p].sweep)
                 jsw[j] = 1;
@@ -1368,7 +1395,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     using Check = std::function<void(hipError_t, const char*)>;
     // seeding and tables; the scoring pass (between timing events); certification and copy-out
     auto issue_pre = [&](hipStream_t st, const Check& ck) {
-        launch_seed(S.d_jobs, pp, st, ck);
+        launch_seed(h, S.d_jobs, jobs.data(), pp, st, ck);
         jit_pass(jobs.data(), n3, pp.n[G_JIT], true, st, ck);
         launch_table_all(S.d_jobs, n_src, st, ck);
     };

@@ -52,7 +52,8 @@ struct JitRows {
     hipFunction_t sample = nullptr;
     hipFunction_t score = nullptr;    // per-plan scores of a RANGE source of 32-bit indices
     hipFunction_t score_rows = nullptr;  // per-plan scores of rows
-    hipFunction_t sweep = nullptr;    // the sweep of RANGE sources (uniform pressure, 32-bit blocks)
+    hipFunction_t sweep = nullptr;    // the sweep of RANGE sources (32-bit blocks)
+    hipFunction_t seed = nullptr;     // its seeding pass (uniform pressure, corr mode)
 };
 
 namespace {
@@ -476,6 +477,95 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
          "          }\n        }\n      }\n    }\n  }\n}\n";
 }
 
+// Seeding pass of the generated sweep (uniform pressure, corr mode): one
+// hashed row per window of S rows, as the library's; per level, the best corr
+// among the row's plans whose CP bin certainly meets it (the bin's count of
+// levels in the seeding order), reduced per workgroup into one slot.
+void gen_sweep_seed(std::ostringstream& o, const ProbDev& D) {
+    const int NP = D.npre, xn = D.xnode, yn = D.ynode, K = D.k;
+    const bool exy = D.edge_xy != 0, s2 = D.pre_sinks != 0 || !exy;
+    const uint32_t pmx = D.pred[xn], pmy = D.pred[yn] & ~(1u << xn), pms = D.pre_sinks;
+    auto maxof = [&](uint32_t mask) {
+        std::string m;
+        for (int u = 0; u < NP; ++u)
+            if (mask >> u & 1u) m = m.empty() ? "f" + std::to_string(u) : "fmaxf(" + m + ", f" + std::to_string(u) + ")";
+        return m.empty() ? std::string("0.0f") : m;
+    };
+    o << "__device__ __constant__ const int dy_lvl_order[DY_K] = {";
+    for (int k = 0; k < K; ++k) o << (k ? ", " : "") << D.lvl_order[k];
+    o << "};\n";
+    o << R"(
+extern "C" __global__ void __launch_bounds__(256) dy_sweep_seed(
+    unsigned long long nsamp, unsigned long long S, unsigned long long units, unsigned long long blk_first,
+    unsigned long long begin, unsigned long long count, const float2* __restrict__ at,
+    const float2* __restrict__ atx, const float2* __restrict__ aty, int rmax, const unsigned* __restrict__ jtab,
+    unsigned* __restrict__ scert) {
+  __shared__ float2 s_pat[)" << NP << R"( * 64];
+  __shared__ int s_jt[64];
+  __shared__ unsigned s_red[DY_K][4];
+  const unsigned long long t0 = (unsigned long long)blockIdx.x * 256ull;
+  if (t0 >= nsamp) return;
+  for (int i = threadIdx.x; i < )" << NP << R"( * 64; i += 256) {
+    const int n = i >> 6, e = i & 63;
+    s_pat[i] = e < rmax ? at[n * rmax + e] : make_float2(1.0f, 0.0f);
+  }
+  if (threadIdx.x < 64) s_jt[threadIdx.x] = (int)jtab[threadIdx.x];
+  __syncthreads();
+  const unsigned long long t = t0 + threadIdx.x;
+  const bool live = t < nsamp;
+  const unsigned long long tj = live ? t : nsamp - 1;
+  const unsigned long long st = tj * S;
+  const unsigned wd = (unsigned)(S < units - st ? S : units - st);
+  const unsigned hh = (unsigned)(tj * 0x9E3779B1ull) >> 16;
+  const unsigned u = (unsigned)(st + (unsigned long long)(hh % wd));
+  const unsigned qb = u / )" << D.rx << R"(u;
+  const int ix = (int)(u - qb * )" << D.rx << R"(u);
+  const unsigned long long b = blk_first + qb;
+  unsigned x_ = (unsigned)b;
+)";
+    for (int n = NP - 1; n >= 0; --n) {
+        o << "  const unsigned d" << n << " = x_ % " << D.radix[n] << "u;";
+        if (n > 0) o << " x_ /= " << D.radix[n] << "u;";
+        o << "\n";
+    }
+    o << "  float pc = 1.0f;\n";
+    for (int n = 0; n < NP; ++n) {
+        o << "  const float2 v" << n << " = s_pat[" << n * 64 << " + d" << n << "];\n";
+        o << "  pc = pc * v" << n << ".x;\n";
+        std::string m;
+        for (int u = 0; u < n; ++u)
+            if (D.pred[n] >> u & 1u) m = m.empty() ? "f" + std::to_string(u) : "fmaxf(" + m + ", f" + std::to_string(u) + ")";
+        o << "  const float f" << n << " = v" << n << ".y + " << (m.empty() ? "0.0f" : m) << ";\n";
+    }
+    o << "  const float px = " << maxof(pmx) << ", py = " << maxof(pmy) << ", ps = " << maxof(pms) << ";\n";
+    o << "  const float2 vx = atx[ix];\n  const float fx = vx.y + px;\n  const float cx = pc * vx.x;\n";
+    o << "  const float M = " << (exy ? "fmaxf(py, fx)" : "py") << ";\n";
+    if (s2) o << "  const float S2 = " << (exy ? "ps" : "fmaxf(ps, fx)") << ";\n";
+    o << "  const unsigned long long base = (b * " << D.rx << "ull + (unsigned long long)ix) * " << D.ry << "ull;\n";
+    for (int k = 0; k < K; ++k) o << "  float bst" << k << " = -1.0f;\n";
+    o << "#pragma unroll\n  for (int j = 0; j < " << D.ry << "; ++j) {\n";
+    o << "    const float2 vy = aty[j];\n    float cp = vy.y + M;\n";
+    if (s2) o << "    cp = fmaxf(cp, S2);\n";
+    o << "    const float cc = cx * vy.x;\n";
+    o << "    const int nj = (live && base + (unsigned long long)j - begin < count) ? s_jt[(__float_as_uint(cp) >> "
+      << D.bin_shift << "u) & 63u] : 0;\n";
+    for (int k = 0; k < K; ++k) o << "    bst" << k << " = fmaxf(bst" << k << ", nj > " << k << " ? cc : -1.0f);\n";
+    o << "  }\n";
+    o << "  const int lane = threadIdx.x & 63;\n";
+    for (int k = 0; k < K; ++k) {
+        o << "  { const unsigned e = dy_wmax(bst" << k << " >= 0.0f ? __float_as_uint(bst" << k << ") + 1u : 0u);\n";
+        o << "    if (lane == 0) s_red[" << k << "][threadIdx.x >> 6] = e; }\n";
+    }
+    o << R"(  __syncthreads();
+  if (threadIdx.x < DY_K) {
+    const unsigned* r = s_red[threadIdx.x];
+    const unsigned e = max(max(r[0], r[1]), max(r[2], r[3]));
+    if (e) atomicMax(scert + dy_lvl_order[threadIdx.x] * 64 + (blockIdx.x % 64), e);
+  }
+}
+)";
+}
+
 std::string gen_source(const ProbDev& D) {
     const int N = D.n;
     const int Q = (N + 3) / 4;
@@ -822,6 +912,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
         gen_score(o, D, true);
     }
     if (D.npre >= 1 && D.xnode >= 0) gen_sweep(o, D);
+    if (D.uniform && !D.obj && D.npre >= 1 && D.xnode >= 0) gen_sweep_seed(o, D);
     return o.str();
 }
 
@@ -877,7 +968,9 @@ bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err) 
         hipModuleGetFunction(&j.sample, j.mod, "dy_rows_sample") != hipSuccess ||
         ((D.uniform || D.obj) && (hipModuleGetFunction(&j.score, j.mod, "dy_score_range") != hipSuccess ||
                                   hipModuleGetFunction(&j.score_rows, j.mod, "dy_score_rows") != hipSuccess)) ||
-        (D.npre >= 1 && D.xnode >= 0 && hipModuleGetFunction(&j.sweep, j.mod, "dy_sweep") != hipSuccess)) {
+        (D.npre >= 1 && D.xnode >= 0 && hipModuleGetFunction(&j.sweep, j.mod, "dy_sweep") != hipSuccess) ||
+        (D.uniform && !D.obj && D.npre >= 1 && D.xnode >= 0 &&
+         hipModuleGetFunction(&j.seed, j.mod, "dy_sweep_seed") != hipSuccess)) {
         *err = "loading the compiled rows kernels failed";
         return false;
     }
