@@ -231,7 +231,13 @@ enum {
 int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_plan** out);
 
 /*
- * Select, for every source, the best feasible plan of each level.
+ * Select, for every source, the best feasible plan of each level: one
+ * pressure-specialised variant per level (Sec. 4.4, eq. variant-objective:
+ * the same bound coefficients re-solved at each level; Algorithm gen: one
+ * solve per level, the results bundled).  corr / SLO problems: the greatest
+ * corr among plans with CP_k <= slo (Sec. 4.3 longest path, inclusive bound);
+ * objective problems: the greatest J_k (Sec. 4.3 eq. admission-objective).
+ * Equal scores go to the lowest plan index.
  *  src     HOST array of n_src sources (each names a problem of the handle;
  *          several sources may name the same problem).
  *  out     HOST array [n_src][dy_plan_max_levels(h)]; row s, column k is level
@@ -242,7 +248,9 @@ int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_
 int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream);
 
 /*
- * Per-plan scores of one source, written asynchronously on `stream` into
+ * Per-plan scores of one source (the quantities Sec. 4.3 and Sec. 4.4 attach
+ * to a plan: vulnerability-weighted correctness, the longest path at every
+ * level, the D_tau demand annotation), written asynchronously on `stream` into
  * caller-owned DEVICE buffers (any may be NULL to skip it):
  *  corr[count], cp[count][K] (CP at each level), demand[count],
  *  feas_bits[count] (bit k set iff CP_k <= slo, decided exactly; K <= 32).
@@ -253,7 +261,10 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
 int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, float* demand,
                   uint32_t* feas_bits, void* stream);
 
-/* Free the handle and its device memory (NULL is a no-op). */
+/* Free the handle and its device memory (NULL is a no-op).  The compiled
+ * per-level variants live only as the choices a caller copied out
+ * (Algorithm gen returns the bundle; nothing of it stays in the handle).
+ * Calls still running on a stream must have completed. */
 void dy_plan_destroy(dy_plan* h);
 
 int32_t dy_plan_max_levels(const dy_plan* h);
@@ -264,6 +275,12 @@ int dy_plan_get_stats(const dy_plan* h, dy_stats* out);
 const char* dy_plan_last_error(const dy_plan* h);
 const char* dy_status_str(int status);
 int32_t dy_abi_version(void);
+
+/* Host-only checks of the library's internal arithmetic helpers (the
+ * invariant-divisor digit decode used for mixed-radix plan indices, the
+ * directed fp32 roundings of the certification bands).  No HIP call.
+ * Returns the number of failed checks (0: all pass). */
+int dy_selftest(void);
 
 /*
  * Suffix recompilation (Appendix "Suffix Recompilation and Its Timing Scope",

@@ -1,5 +1,8 @@
 """Write the stored workload SLOs and full-size expected selections.
 
+The SLO table goes beside the generator (paper_2607_02942_amd/workload_slo.json,
+a workload parameter); the expected selections go to tests/golden/.
+
 TEST INFRASTRUCTURE ONLY.  Every stored number is produced here by the fp64
 oracle (oracle.c) on inputs from the seeded workload generator; nothing comes
 from the GPU library.
@@ -59,40 +62,55 @@ def _chunks(total, size):
 
 
 # ---- median ------------------------------------------------------------------
+#
+# The lower median of ~1e10 values does not fit in memory, so it is found in
+# two passes over the plan set: a histogram of the top HIST_BITS bits of each
+# fp64 value's bit pattern (non-negative doubles order like their patterns),
+# then the values of the one bucket that holds the wanted rank, sorted.
 
 def _hist_task(args):
-    name, kind, begin, count = args
-    prob = _problem(name)
+    prob, kind, begin, count, bits = args
     op = orc.OracleProblem(prob, 0.0)
-    hist = np.zeros(1 << HIST_BITS, np.uint64)
+    hist = np.zeros(1 << bits, np.uint64)
     if kind == "rows":
         rows = _rows(prob, begin, count)
-        orc.lib().or_cp0_hist(op.ref, 1, rows.ctypes.data, rows.shape[1], 0, count, HIST_BITS, hist.ctypes.data)
+        orc.lib().or_cp0_hist(op.ref, 1, rows.ctypes.data, rows.shape[1], 0, count, bits, hist.ctypes.data)
     else:
-        orc.lib().or_cp0_hist(op.ref, 0, None, 0, begin, count, HIST_BITS, hist.ctypes.data)
+        orc.lib().or_cp0_hist(op.ref, 0, None, 0, begin, count, bits, hist.ctypes.data)
     nz = np.nonzero(hist)[0]
     return nz, hist[nz]
 
 
 def _collect_task(args):
-    name, kind, begin, count, bucket, cap = args
-    prob = _problem(name)
+    prob, kind, begin, count, bits, bucket, cap = args
     op = orc.OracleProblem(prob, 0.0)
     out = np.zeros(cap, np.float64)
     if kind == "rows":
         rows = _rows(prob, begin, count)
-        got = orc.lib().or_cp0_collect(op.ref, 1, rows.ctypes.data, rows.shape[1], 0, count, HIST_BITS,
+        got = orc.lib().or_cp0_collect(op.ref, 1, rows.ctypes.data, rows.shape[1], 0, count, bits,
                                        bucket, out.ctypes.data, cap)
     else:
-        got = orc.lib().or_cp0_collect(op.ref, 0, None, 0, begin, count, HIST_BITS, bucket, out.ctypes.data, cap)
+        got = orc.lib().or_cp0_collect(op.ref, 0, None, 0, begin, count, bits, bucket, out.ctypes.data, cap)
     assert got <= cap, "bucket larger than the collection buffer"
     return out[:got]
 
 
-def lower_median_cp0(name, pool, chunk):
-    kind, total = SOURCES[name]
-    tasks = [(name, kind, b, c) for b, c in _chunks(total, chunk)]
-    hist = np.zeros(1 << HIST_BITS, np.uint64)
+class SerialPool:
+    """The two pool methods lower_median_cp0 uses, run in this process."""
+
+    def imap_unordered(self, fn, tasks, chunksize=1):
+        return map(fn, tasks)
+
+    def imap(self, fn, tasks, chunksize=1):
+        return map(fn, tasks)
+
+
+def lower_median_cp0(prob, kind, total, pool, chunk, bits=HIST_BITS):
+    """Lower median (0-based rank floor((total-1)/2)) of the fp64 unpressured
+    CP over plan indices [0, total) (kind "range") or the first `total` rows
+    of the workload's row stream (kind "rows")."""
+    tasks = [(prob, kind, b, c, bits) for b, c in _chunks(total, chunk)]
+    hist = np.zeros(1 << bits, np.uint64)
     for nz, v in pool.imap_unordered(_hist_task, tasks):
         hist[nz] += v
     rank = (total - 1) // 2
@@ -150,7 +168,7 @@ def main():
     args = ap.parse_args()
     names = args.only.split(",")
     os.makedirs(GOLDEN_DIR, exist_ok=True)
-    slo_path = os.path.join(GOLDEN_DIR, "slo.json")
+    slo_path = wl.SLO_FILE
     slos = json.load(open(slo_path)) if os.path.exists(slo_path) else {}
     chunk = {"chain4": 1 << 20, "forkjoin8": 1 << 22, "layered10": 1 << 24, "stream24": 1 << 22}
     ctx = mp.get_context("fork")
@@ -161,7 +179,8 @@ def main():
                 res = sorted(pool.imap_unordered(_batch_slo_task, range(wl.N_BATCH), chunksize=8))
                 slos["batch6"] = [s for _, s in res]
             else:
-                med = lower_median_cp0(name, pool, chunk[name])
+                kind, total = SOURCES[name]
+                med = lower_median_cp0(_problem(name), kind, total, pool, chunk[name])
                 slos[name] = float(np.float32(1.5 * med))
             json.dump(slos, open(slo_path, "w"), indent=1)
             print(f"[golden] slo {name}: {slos[name] if name != 'batch6' else '4096 values'} "

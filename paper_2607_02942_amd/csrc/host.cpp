@@ -1618,6 +1618,18 @@ int dy_selftest(void) {
             if (magic_div(x, g) != x / d) ++bad;
         }
     }
+    // directed roundings of the certification bands: the nearest fp32 at or
+    // below (above) x, exact values kept
+    uint64_t st = 0x243F6A8885A308D3ull;
+    for (int i = 0; i < 4096; ++i) {
+        st += 0x9E3779B97F4A7C15ull;
+        const double x = std::ldexp((double)(st >> 11), -53 + (int)(st % 64) - 20);
+        const float dn = round_down(x), up = round_up(x);
+        if (!((double)dn <= x && (double)std::nextafter(dn, INFINITY) > x)) ++bad;
+        if (!((double)up >= x && (double)std::nextafter(up, -INFINITY) < x)) ++bad;
+        const float e = (float)x;
+        if (round_down((double)e) != e || round_up((double)e) != e) ++bad;
+    }
     return bad;
 }
 

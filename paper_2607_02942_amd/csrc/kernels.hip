@@ -1388,6 +1388,17 @@ __device__ void merge_cert(JD J, PD P) {
             s_out[k] = c;
         }
     }
+    // scratch for the next call first: a caller that returns on the completion
+    // word below may start its next call (on any stream) right away, and that
+    // call skips k_init when this one raised no flag
+    const int32_t flags = *J->flags;
+    if (flags == 0) {
+        for (int i = threadIdx.x; i < KMAX * NSLOT; i += 64) J->scert[i] = 0u;
+        if (threadIdx.x < KMAX) {
+            J->fb_corr[threadIdx.x] = 0ull;
+            J->fb_index[threadIdx.x] = ~0ull;
+        }
+    }
     // the host-mapped copy: the K choices as consecutive dwords, then the counters
     __syncthreads();
     if (J->hout) {
@@ -1397,19 +1408,12 @@ __device__ void merge_cert(JD J, PD P) {
         for (int i = threadIdx.x; i < K * 6; i += 64) dst[i] = src[i];
         if (threadIdx.x == 0) {
             *J->hncand = *J->ncand;
-            *J->hflags = *J->flags;
+            *J->hflags = flags;
         }
-        if (J->hdone) {  // completion word last, behind the results
+        if (J->hdone) {  // completion word last, behind the results and the cleared scratch
             __threadfence_system();
             __syncthreads();
             if (threadIdx.x == 0) __hip_atomic_store(J->hdone, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-        }
-    }
-    if (*J->flags == 0) {
-        for (int i = threadIdx.x; i < KMAX * NSLOT; i += 64) J->scert[i] = 0u;
-        if (threadIdx.x < KMAX) {
-            J->fb_corr[threadIdx.x] = 0ull;
-            J->fb_index[threadIdx.x] = ~0ull;
         }
     }
 }

@@ -31,6 +31,18 @@ def test_library_exports_every_declared_symbol():
     assert set(names) <= set(D.EXPORTED)
 
 
+def test_exports_equal_header_declarations():
+    # every dy_* function the library exports is declared in the header, and
+    # every declared one is exported (symbol table of the library built here)
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", D.LIB_PATH], check=True, capture_output=True,
+                         text=True).stdout
+    exported = sorted({f[2] for f in (l.split() for l in out.splitlines())
+                       if len(f) == 3 and f[1] == "T" and f[2].startswith("dy_")})
+    assert exported == header_functions()
+    assert sorted(D.EXPORTED) == exported
+
+
 def test_abi_version_status_strings_and_selftest():
     lib = D.lib()
     assert lib.dy_abi_version() == 3

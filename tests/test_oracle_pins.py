@@ -398,3 +398,120 @@ def test_score_matches_scalar_entry_points():
         for k in range(3):
             assert cp[j, k] == orc.cp(prob, impl, k)
             assert bool(feas[j] >> k & 1) == (cp[j, k] <= 3.0)
+
+
+# ---------------------------------------------------------------------------
+# Score entry points over rows and over index lists
+# ---------------------------------------------------------------------------
+
+def _digits(radix, index):
+    """Mixed-radix digits, node 0 most significant (independent of the oracle)."""
+    out = []
+    for r in reversed([int(x) for x in radix]):
+        out.append(index % r)
+        index //= r
+    return out[::-1]
+
+
+@pytest.mark.parametrize("seed", [36, 37, 38])
+def test_score_rows_and_indices_equal_score_range(seed):
+    rng = np.random.default_rng(seed)
+    prob = random_problem(rng, 5, 5, K=3, B=2)
+    prob.slo = 4.0
+    total = prob.n_plans()
+    corr, cp, dem, feas = orc.score_range(prob, 0, total)
+    # rows with a stride wider than the node count; the padding bytes hold
+    # values no id may take, so reading one would change the scores
+    stride = prob.n_nodes + 3
+    rows = np.full((total, stride), 250, np.uint8)
+    for j in range(total):
+        rows[j, :prob.n_nodes] = _digits(prob.radix, j)
+    rc, rcp, rd, rf = orc.score_rows(prob, rows)
+    assert np.array_equal(rc, corr) and np.array_equal(rcp, cp)
+    assert np.array_equal(rd, dem) and np.array_equal(rf, feas)
+    perm = rng.permutation(total).astype(np.uint64)
+    ic, icp, idm, ifs = orc.score_indices(prob, perm)
+    assert np.array_equal(ic, corr[perm]) and np.array_equal(icp, cp[perm])
+    assert np.array_equal(idm, dem[perm]) and np.array_equal(ifs, feas[perm])
+
+
+def test_score_rows_and_indices_on_workload_subsets():
+    from paper_2607_02942_amd import workload as wl
+    prob = wl.forkjoin8()
+    begin, count = 123_456_789, 4096
+    corr, cp, dem, feas = orc.score_range(prob, begin, count)
+    rows = np.array([_digits(prob.radix, begin + j) for j in range(count)], np.uint8)
+    rc, rcp, rd, rf = orc.score_rows(prob, rows)
+    assert np.array_equal(rc, corr) and np.array_equal(rcp, cp)
+    assert np.array_equal(rd, dem) and np.array_equal(rf, feas)
+    rng = np.random.default_rng(39)
+    sub = rng.permutation(count)[:1000]
+    ic, icp, idm, ifs = orc.score_indices(prob, (begin + sub).astype(np.uint64))
+    assert np.array_equal(ic, corr[sub]) and np.array_equal(icp, cp[sub])
+    assert np.array_equal(idm, dem[sub]) and np.array_equal(ifs, feas[sub])
+
+
+# ---------------------------------------------------------------------------
+# The two-pass lower median that sets the stored SLOs (R-7: 1.5 x the lower
+# median of the unpressured critical path over the scored plan set)
+# ---------------------------------------------------------------------------
+
+def _sorted_lower_median(vals):
+    return float(np.sort(vals)[(vals.size - 1) // 2])
+
+
+def test_two_pass_median_chain4_full_space():
+    from oracle import golden
+    from paper_2607_02942_amd import workload as wl
+    prob = wl.chain4(slo=0.0)
+    total = prob.n_plans()
+    got = golden.lower_median_cp0(prob, "range", total, golden.SerialPool(), 5000)
+    # a chain's unpressured CP is its durations summed in node order
+    idx = np.arange(total)
+    dig = np.stack(np.unravel_index(idx, tuple(int(r) for r in prob.radix)), axis=1)
+    t = prob.tau.astype(np.float64)
+    cp = t[0, dig[:, 0]]
+    for n in range(1, prob.n_nodes):
+        cp = cp + t[n, dig[:, n]]
+    assert got == _sorted_lower_median(cp)
+    assert total % 2 == 0
+    # an odd count: the first total - 1 plans
+    assert golden.lower_median_cp0(prob, "range", total - 1, golden.SerialPool(), 4096) == \
+        _sorted_lower_median(cp[: total - 1])
+
+
+def test_two_pass_median_forkjoin8_prefix():
+    from oracle import golden
+    from paper_2607_02942_amd import workload as wl
+    prob = wl.forkjoin8(slo=0.0)
+    total = 1 << 22
+    got = golden.lower_median_cp0(prob, "range", total, golden.SerialPool(), 1 << 20)
+    assert got == _sorted_lower_median(orc.cp0_values(prob, 0, total))
+
+
+@pytest.mark.parametrize("count", [1 << 20, (1 << 20) + 1])
+def test_two_pass_median_stream24_rows(count):
+    from oracle import golden
+    from paper_2607_02942_amd import workload as wl
+    prob = wl.stream24(slo=0.0)
+    got = golden.lower_median_cp0(prob, "rows", count, golden.SerialPool(), 1 << 18)
+    rows = wl.make_rows(count, prob.n_nodes, int(prob.radix[0]), threads=1)
+    assert got == _sorted_lower_median(orc.cp0_values(prob, rows=rows))
+
+
+@pytest.mark.parametrize("bits", [6, 24])
+def test_two_pass_median_heavy_ties(bits):
+    # integer durations: the CP takes few distinct values, so the median's
+    # bucket holds many equal values (with 6 bits also many distinct ones)
+    from oracle import golden
+    rng = np.random.default_rng(40)
+    prob = random_problem(rng, 6, 6, K=1, B=1, integer_tau=True)
+    prob.rho = np.zeros((1, 1), np.float32)
+    prob.backend = np.zeros_like(prob.backend)
+    total = prob.n_plans()
+    vals = np.array([orc.cp(prob, orc.decode(prob, j), 0) for j in range(total)])
+    ref = _sorted_lower_median(vals)
+    assert np.count_nonzero(vals == ref) > 10
+    for count in (total, total - 1):
+        got = golden.lower_median_cp0(prob, "range", count, golden.SerialPool(), max(1, count // 3), bits=bits)
+        assert got == _sorted_lower_median(vals[:count])

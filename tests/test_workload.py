@@ -96,7 +96,7 @@ def test_native_rows_match_numpy_twin():
 
 
 def test_stored_slo_is_one_and_a_half_lower_median():
-    slo = json.load(open(os.path.join(GOLDEN, "slo.json")))
+    slo = json.load(open(wl.SLO_FILE))
     prob = wl.chain4(slo=0.0)
     vals = orc.cp0_values(prob, 0, prob.n_plans())
     r = (vals.size - 1) // 2
