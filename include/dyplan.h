@@ -215,9 +215,12 @@ enum {
                                    and the sweep of 32-bit RANGE sources of at least 2^24 plans in
                                    plans of at most 8 problems;
                                    2 as 1 but the sweep for RANGE sources of any size */
-    DY_OPT_GRAPH = 6            /* 1: replay a call that repeats the previous one (same sources) from a
+    DY_OPT_GRAPH = 6,           /* 1: replay a call that repeats the previous one (same sources) from a
                                    HIP graph of its launches (default 1; calls with DY_OPT_TIMING on
                                    launch directly); results are identical */
+    DY_OPT_CLIMB = 7            /* 1 (default): RANGE sources that cover their problem's whole plan space
+                                   (corr / SLO selection) also seed each level's threshold from a local
+                                   search over the plans; 0: sampled seeds only; results are identical */
 };
 
 /*
@@ -260,6 +263,18 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
  */
 int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, float* demand,
                   uint32_t* feas_bits, void* stream);
+
+/*
+ * The HIP source of the kernels the library generates for one problem and
+ * compiles at run time with hiprtc (the streamed-rows kernels, and for DAGs
+ * of at least three nodes the range sweep and, for uniform pressure or the
+ * objective, the per-plan score kernels), with the problem's structure and
+ * constants written in.  Host-only (no HIP call): for inspection and offline
+ * compilation.  Writes at most cap bytes, NUL-terminated when cap > 0, and
+ * sets *len to the full length without the NUL.  Returns dy_plan_create's
+ * status for an invalid problem (message in dy_plan_last_error(NULL)).
+ */
+int dy_kernel_source(const dy_problem* prob, char* buf, uint64_t cap, uint64_t* len);
 
 /* Free the handle and its device memory (NULL is a no-op).  The compiled
  * per-level variants live only as the choices a caller copied out

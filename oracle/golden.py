@@ -15,6 +15,7 @@ from the GPU library.
         the exact rule (greatest correctness, then lowest index).
 
 Usage:  python -m oracle.golden [--procs P] [--only name,...] [--skip-select]
+                                [--mode level|perclass|objective]
 """
 from __future__ import annotations
 
@@ -133,27 +134,48 @@ def _batch_slo_task(r):
 
 
 # ---- selection -----------------------------------------------------------------
+#
+# mode "level": the recipes' pressure (every backend at the level's rho);
+# "perclass": workload.per_class (the second backend at half the level's rho),
+# the same SLO; "objective": the paper's additive objective J_L
+# (workload.paper_objective), every plan admissible.
 
-def _select_task(args):
-    name, kind, begin, count, slo = args
-    prob = _problem(name)
+def _moded(prob, mode):
+    if mode == "perclass":
+        return wl.per_class(prob), None
+    if mode == "objective":
+        return prob, wl.paper_objective(prob)
+    return prob, None
+
+
+def _select_part(prob, obj, kind, begin, count, slo):
     if kind == "rows":
         rows = _rows(prob, begin, count)
-        return begin, orc.select_rows(prob, rows, begin, slo=slo)
-    return begin, orc.select_range(prob, begin, count, slo=slo)
+        if obj is not None:
+            return orc.obj_select_rows(prob, obj, rows, begin)
+        return orc.select_rows(prob, rows, begin, slo=slo)
+    if obj is not None:
+        return orc.obj_select_range(prob, obj, begin, count)
+    return orc.select_range(prob, begin, count, slo=slo)
 
 
-def full_select(name, slo, pool, chunk):
+def _select_task(args):
+    name, kind, begin, count, slo, mode = args
+    prob, obj = _moded(_problem(name), mode)
+    return begin, _select_part(prob, obj, kind, begin, count, slo)
+
+
+def full_select(name, slo, pool, chunk, mode="level"):
     kind, total = SOURCES[name]
-    tasks = [(name, kind, b, c, slo) for b, c in _chunks(total, chunk)]
+    tasks = [(name, kind, b, c, slo, mode) for b, c in _chunks(total, chunk)]
     parts = sorted(pool.imap_unordered(_select_task, tasks))
     return orc.merge_choices([p for _, p in parts])
 
 
 def _batch_select_task(args):
-    r, slo = args
-    prob = _problem("batch6", r)
-    return r, orc.select_range(prob, 0, prob.n_plans(), slo=slo)
+    r, slo, mode = args
+    prob, obj = _moded(_problem("batch6", r), mode)
+    return r, _select_part(prob, obj, "range", 0, prob.n_plans(), slo)
 
 
 def _fmt_choices(ch):
@@ -165,6 +187,8 @@ def main():
     ap.add_argument("--procs", type=int, default=os.cpu_count() or 1)
     ap.add_argument("--only", default="chain4,forkjoin8,batch6,layered10,stream24")
     ap.add_argument("--skip-select", action="store_true")
+    ap.add_argument("--mode", choices=["level", "perclass", "objective"], default="level",
+                    help="selections under per-class pressure or the paper's objective (the stored SLOs are kept)")
     args = ap.parse_args()
     names = args.only.split(",")
     os.makedirs(GOLDEN_DIR, exist_ok=True)
@@ -175,35 +199,44 @@ def main():
     with ctx.Pool(args.procs) as pool:
         for name in names:
             t0 = time.time()
-            if name == "batch6":
+            if args.mode != "level":
+                pass
+            elif name == "batch6":
                 res = sorted(pool.imap_unordered(_batch_slo_task, range(wl.N_BATCH), chunksize=8))
                 slos["batch6"] = [s for _, s in res]
             else:
                 kind, total = SOURCES[name]
                 med = lower_median_cp0(_problem(name), kind, total, pool, chunk[name])
                 slos[name] = float(np.float32(1.5 * med))
-            json.dump(slos, open(slo_path, "w"), indent=1)
-            print(f"[golden] slo {name}: {slos[name] if name != 'batch6' else '4096 values'} "
-                  f"({time.time() - t0:.1f}s)", flush=True)
+            if args.mode == "level":
+                json.dump(slos, open(slo_path, "w"), indent=1)
+                print(f"[golden] slo {name}: {slos[name] if name != 'batch6' else '4096 values'} "
+                      f"({time.time() - t0:.1f}s)", flush=True)
             if args.skip_select:
                 continue
             t0 = time.time()
-            out = {"workload": name, "generator": "paper_2607_02942_amd.workload", "oracle": "oracle/oracle.c"}
+            out = {"workload": name, "generator": "paper_2607_02942_amd.workload",
+                   "oracle": "oracle/objective.c" if args.mode == "objective" else "oracle/oracle.c"}
+            if args.mode != "level":
+                out["mode"] = {"perclass": "workload.per_class: backend 1 at half the level's rho",
+                               "objective": "workload.paper_objective: J_L, L in {0, 1.5, 3}"}[args.mode]
             if name == "batch6":
                 res = sorted(pool.imap_unordered(_batch_select_task,
-                                                 [(r, slos["batch6"][r]) for r in range(wl.N_BATCH)], chunksize=8))
+                                                 [(r, slos["batch6"][r], args.mode) for r in range(wl.N_BATCH)],
+                                                 chunksize=8))
                 out["source"] = {"kind": "range", "begin": 0, "count": 12 ** 6, "requests": wl.N_BATCH}
                 out["choices"] = [_fmt_choices(ch) for _, ch in res]
             else:
                 kind, total = SOURCES[name]
                 out["source"] = {"kind": kind, "begin": 0, "count": total}
                 out["slo"] = slos[name]
-                out["choices"] = _fmt_choices(full_select(name, slos[name], pool, chunk[name]))
-            path = os.path.join(GOLDEN_DIR, f"select_{name}.json")
+                out["choices"] = _fmt_choices(full_select(name, slos[name], pool, chunk[name], args.mode))
+            tag = "" if args.mode == "level" else "_" + args.mode
+            path = os.path.join(GOLDEN_DIR, f"select_{name}{tag}.json")
             with open(path, "w") as f:
                 if name == "batch6":
                     f.write("{\n")
-                    for key in ("workload", "generator", "oracle", "source"):
+                    for key in [k for k in ("workload", "generator", "oracle", "mode", "source") if k in out]:
                         f.write(f" {json.dumps(key)}: {json.dumps(out[key])},\n")
                     f.write(' "choices": [\n')
                     f.write(",\n".join(json.dumps(c, separators=(",", ":")) for c in out["choices"]))

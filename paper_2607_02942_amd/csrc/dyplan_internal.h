@@ -140,6 +140,8 @@ struct JobDev {
     uint32_t* hncand;         // host-mapped copies of ncand and flags (with hout)
     int32_t* hflags;
     uint32_t* hdone;          // host-mapped completion word of the call (with hout), set last
+    int32_t climb;            // RANGE source over its problem's whole plan space: local-search seeds
+    int32_t pad0;
 };
 
 }  // namespace dyp

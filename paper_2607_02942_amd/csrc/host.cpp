@@ -22,12 +22,14 @@ hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_samples,
                                int npre_max, int npre_c, int kmax, hipStream_t s);
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
-                        int npre_c, int ry, hipStream_t s);
+                        int npre_c, int ry, bool b256, hipStream_t s);
 hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, int ncol, hipStream_t s);
 hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol, hipStream_t s);
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, int nmax, int nrmax, hipStream_t s);
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
 hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
+hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s);
+hipError_t static_scratch(int device, char** ptr, size_t* bytes);
 struct JitRows {
     hipModule_t mod = nullptr;
     hipFunction_t scan = nullptr;
@@ -39,6 +41,7 @@ struct JitRows {
     hipFunction_t seed = nullptr;
 };
 bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err);
+std::string jit_rows_source(const ProbDev& D);
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
                         int n_nodes, int n_entries, bool simple, bool obj, hipStream_t s);
 }  // namespace dyp
@@ -53,6 +56,9 @@ constexpr uint64_t kMaxSourcePlans = 1ull << 40;
 constexpr size_t kCandPoolBytes = 1ull << 30;    // candidate slots shared by the sources of one call
 constexpr uint64_t kMinSamples = 4096;           // the adaptive stride keeps at least this many samples
 constexpr int kDirectResults = 64;                // up to this many sources, results go straight to host memory
+constexpr int kStaticSources = 64;                // sources per dy_plan_select_static call at most
+constexpr uint32_t kStaticMinCand = 1024;         // candidate slots per source it needs at least
+constexpr int kClimbNodes = 8;                    // local-search seeds for problems of at most this many nodes
 constexpr double kU = 0x1p-24;                    // fp32 unit roundoff
 
 struct HostProb {
@@ -351,6 +357,8 @@ struct dy_plan {
     bool stride_fixed = false;
     uint32_t cand_cap = 1u << 16;
     int force_fp64 = 0;
+    int use_climb = 1;                // local-search seeds for sources over a whole plan space
+    std::vector<char> st_host;        // host copies of dy_plan_select_static's jobs and results
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     // A call that repeats the previous one (same job array, scratch clear) is
     // replayed from a HIP graph of its launches: one submission instead of one
@@ -394,11 +402,9 @@ void free_scratch(Scratch& s) {
     s = Scratch{};
 }
 
-int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
-    Scratch& s = h->sc;
-    if (s.d && s.jobs >= njobs && s.cap >= cap && s.kmax == h->kmax) return DY_OK;
-    free_scratch(s);
-    const int km = h->kmax;
+// Lays the per-call buffers of njobs sources (cap candidate slots each) out
+// from device address d (null: only the size); returns the bytes they span.
+size_t layout_scratch(Scratch& s, char* d, size_t njobs, uint32_t cap, int km) {
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t o = align_up(off, 256);
@@ -422,36 +428,50 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
     size_t o_res = take(res_bytes);
     size_t o_fbc = take(njobs * KMAX * sizeof(uint64_t));
     size_t o_fbi = take(njobs * KMAX * sizeof(uint64_t));
-    size_t o_cand = take(njobs * (size_t)cap * sizeof(Cand));
     size_t o_sync = take(njobs * sizeof(uint32_t));
-    hipError_t e = hipMalloc((void**)&s.d, off);
-    if (e != hipSuccess) {
-        s.d = nullptr;
-        return hip_fail(&h->err, e, "hipMalloc(scratch)");
-    }
+    size_t o_cand = take(njobs * (size_t)cap * sizeof(Cand));
+    off = align_up(off, 256);
+    s.res_bytes = res_bytes;
+    s.res_ncand_off = res_ncand;
+    s.res_flags_off = res_flags;
+    if (!d) return off;
+    s.d = d;
     s.bytes = off;
     s.jobs = njobs;
     s.cap = cap;
     s.kmax = km;
-    s.d_jobs = (JobDev*)(s.d + o_jobs);
-    s.d_fb = (JobDev*)(s.d + o_fb);
-    s.scert = (uint32_t*)(s.d + o_scert);
-    s.cert_c = (double*)(s.d + o_cc);
-    s.cert_i = (uint64_t*)(s.d + o_ci);
-    s.cert_cp = (double*)(s.d + o_cp);
-    s.cert_d = (double*)(s.d + o_cd);
-    s.thr = (float*)(s.d + o_thr);
-    s.table = (uint32_t*)(s.d + o_table);
-    s.table2 = (uint32_t*)(s.d + o_table2);
-    s.res_bytes = res_bytes;
-    s.out = (dy_choice*)(s.d + o_res + res_out);
-    s.ncand = (uint32_t*)(s.d + o_res + res_ncand);
-    s.flags = (int32_t*)(s.d + o_res + res_flags);
-    s.sync = (uint32_t*)(s.d + o_sync);
+    s.d_jobs = (JobDev*)(d + o_jobs);
+    s.d_fb = (JobDev*)(d + o_fb);
+    s.scert = (uint32_t*)(d + o_scert);
+    s.cert_c = (double*)(d + o_cc);
+    s.cert_i = (uint64_t*)(d + o_ci);
+    s.cert_cp = (double*)(d + o_cp);
+    s.cert_d = (double*)(d + o_cd);
+    s.thr = (float*)(d + o_thr);
+    s.table = (uint32_t*)(d + o_table);
+    s.table2 = (uint32_t*)(d + o_table2);
+    s.out = (dy_choice*)(d + o_res + res_out);
+    s.ncand = (uint32_t*)(d + o_res + res_ncand);
+    s.flags = (int32_t*)(d + o_res + res_flags);
+    s.sync = (uint32_t*)(d + o_sync);
+    s.fb_corr = (uint64_t*)(d + o_fbc);
+    s.fb_index = (uint64_t*)(d + o_fbi);
+    s.cand = (Cand*)(d + o_cand);
     s.clean = false;  // the next call clears the scratch first
-    s.fb_corr = (uint64_t*)(s.d + o_fbc);
-    s.fb_index = (uint64_t*)(s.d + o_fbi);
-    s.cand = (Cand*)(s.d + o_cand);
+    return off;
+}
+
+int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
+    Scratch& s = h->sc;
+    if (s.d && s.jobs >= njobs && s.cap >= cap && s.kmax == h->kmax) return DY_OK;
+    free_scratch(s);
+    const int km = h->kmax;
+    const size_t off = layout_scratch(s, nullptr, njobs, cap, km);
+    char* d = nullptr;
+    hipError_t e = hipMalloc((void**)&d, off);
+    if (e != hipSuccess) return hip_fail(&h->err, e, "hipMalloc(scratch)");
+    layout_scratch(s, d, njobs, cap, km);
+    const size_t res_bytes = s.res_bytes;
     if ((e = hipHostMalloc((void**)&s.h_jobs, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
         (e = hipHostMalloc((void**)&s.h_fb, njobs * sizeof(JobDev), hipHostMallocDefault)) != hipSuccess ||
         (e = hipHostMalloc((void**)&s.h_res, res_bytes, hipHostMallocMapped | hipHostMallocCoherent)) !=
@@ -463,12 +483,46 @@ int ensure_scratch(dy_plan* h, size_t njobs, uint32_t cap) {
         free_scratch(s);
         return hip_fail(&h->err, e, "hipHostMalloc(scratch)");
     }
-    s.h_out = (dy_choice*)(s.h_res + res_out);
-    s.h_ncand = (uint32_t*)(s.h_res + res_ncand);
-    s.h_flags = (int32_t*)(s.h_res + res_flags);
-    s.res_ncand_off = res_ncand;
-    s.res_flags_off = res_flags;
+    s.h_out = (dy_choice*)(s.h_res);
+    s.h_ncand = (uint32_t*)(s.h_res + s.res_ncand_off);
+    s.h_flags = (int32_t*)(s.h_res + s.res_flags_off);
     s.uploaded = 0;
+    return DY_OK;
+}
+
+// The per-call buffers of dy_plan_select_static: laid out in the library's
+// fixed device array of this device (kStaticBytes, no allocation), with the
+// host-side copies in buffers the handle allocated at creation.  The
+// candidate slots per source are what the array has left, at most `cap`.
+int static_view(dy_plan* h, size_t njobs, uint32_t cap, Scratch* s) {
+    if (njobs > (size_t)kStaticSources) {
+        h->err = "dy_plan_select_static: more than " + std::to_string(kStaticSources) +
+                 " sources in one call (the fixed scratch array holds that many)";
+        return DY_ELIMIT;
+    }
+    char* base = nullptr;
+    size_t bytes = 0;
+    const hipError_t e = static_scratch(h->device, &base, &bytes);
+    if (e != hipSuccess) return hip_fail(&h->err, e, "hipGetSymbolAddress(scratch)");
+    const int km = h->kmax;
+    const size_t fixed = layout_scratch(*s, nullptr, njobs, 0, km) + 256;
+    const uint64_t fit = fixed < bytes ? (bytes - fixed) / (njobs * sizeof(Cand)) : 0;
+    const uint32_t c = (uint32_t)std::min<uint64_t>(cap, fit);
+    if (c < kStaticMinCand) {
+        h->err = "dy_plan_select_static: the fixed scratch array is too small for this call";
+        return DY_ELIMIT;
+    }
+    layout_scratch(*s, base, njobs, c, km);
+    if (s->bytes > bytes) {
+        h->err = "dy_plan_select_static: scratch layout exceeds the fixed array";
+        return DY_ELIMIT;
+    }
+    s->h_jobs = (JobDev*)h->st_host.data();
+    s->h_fb = s->h_jobs + kStaticSources;
+    s->h_res = (char*)(s->h_fb + kStaticSources);
+    s->h_out = (dy_choice*)s->h_res;
+    s->h_ncand = (uint32_t*)(s->h_res + s->res_ncand_off);
+    s->h_flags = (int32_t*)(s->h_res + s->res_flags_off);
     return DY_OK;
 }
 
@@ -546,7 +600,9 @@ void stage_objective(const dy_problem& pb, ProbDev& D, float2* at, float2* atx, 
     }
 }
 
-int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::string* err) {
+// dry: derive the descriptors and tables on the host only (no HIP call); the
+// descriptors' table pointers then point into a host image that is discarded.
+int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::string* err, bool dry = false) {
     struct Layout {
         size_t at, atx, dz, dem, lat, a64, lat64, dem64;
     };
@@ -580,12 +636,15 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         h->nrmax = std::max(h->nrmax, (int)NR);
     }
     std::vector<char> img(off, 0);
-    hipError_t e = hipMalloc((void**)&h->d_arena, off);
-    if (e != hipSuccess) {
-        h->d_arena = nullptr;
-        return hip_fail(err, e, "hipMalloc(tables)");
+    hipError_t e = hipSuccess;
+    if (!dry) {
+        e = hipMalloc((void**)&h->d_arena, off);
+        if (e != hipSuccess) {
+            h->d_arena = nullptr;
+            return hip_fail(err, e, "hipMalloc(tables)");
+        }
+        h->d_probs = (ProbDev*)h->d_arena;
     }
-    h->d_probs = (ProbDev*)h->d_arena;
     ProbDev* descs = (ProbDev*)img.data();
     for (int j = 0; j < n_probs; ++j) {
         const dy_problem& pb = probs[j];
@@ -778,7 +837,7 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
                 if (D.lo[k] >= U) ++j;
             D.jtab[lane] = j;
         }
-        char* base = h->d_arena;
+        char* base = dry ? img.data() : h->d_arena;
         D.at = (const float2*)(base + L.at);
         D.atx = N >= 2 ? (const float2*)(base + L.at) + (size_t)(N - 2) * R : (const float2*)(base + L.atx);
         D.aty = (const float2*)(base + L.at) + (size_t)(N - 1) * R;
@@ -823,8 +882,10 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
         H.obj = obj;
         H.has_s2 = D.pre_sinks != 0 || !D.edge_xy;
     }
-    e = hipMemcpy(h->d_arena, img.data(), off, hipMemcpyHostToDevice);
-    if (e != hipSuccess) return hip_fail(err, e, "hipMemcpy(tables)");
+    if (!dry) {
+        e = hipMemcpy(h->d_arena, img.data(), off, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(err, e, "hipMemcpy(tables)");
+    }
     h->hdesc.assign(descs, descs + n_probs);
     h->jit_state.assign(n_probs, 0);
     h->jit.assign(n_probs, JitRows{});
@@ -936,6 +997,10 @@ int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_
         h->cus = 256;
     int st = stage_problems(h, probs, n_probs, &g_create_error);
     if (st == DY_OK) {
+        // host copies of dy_plan_select_static's jobs and results, sized once
+        Scratch tmp;
+        layout_scratch(tmp, nullptr, kStaticSources, 0, h->kmax);
+        h->st_host.assign(2 * (size_t)kStaticSources * sizeof(JobDev) + tmp.res_bytes, 0);
         for (int i = 0; i < 4 && st == DY_OK; ++i)
             if ((e = hipEventCreate(&h->ev[i])) != hipSuccess) st = hip_fail(&g_create_error, e, "hipEventCreate");
         if (st == DY_OK && (e = hipStreamCreateWithFlags(&h->cap_stream, hipStreamNonBlocking)) != hipSuccess)
@@ -947,6 +1012,26 @@ int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_
     }
     g_create_error.clear();
     *out = h;
+    return DY_OK;
+}
+
+int dy_kernel_source(const dy_problem* prob, char* buf, uint64_t cap, uint64_t* len) {
+    if (!prob || !len || (cap > 0 && !buf)) {
+        g_create_error = "prob/len is NULL, or buf is NULL with cap > 0";
+        return DY_EINVAL;
+    }
+    int st = validate_problem(*prob, 0, &g_create_error);
+    if (st != DY_OK) return st;
+    dy_plan h;
+    st = stage_problems(&h, prob, 1, &g_create_error, true);
+    if (st != DY_OK) return st;
+    const std::string src = jit_rows_source(h.hdesc[0]);
+    *len = src.size();
+    if (cap > 0) {
+        const size_t n = std::min<size_t>(src.size(), (size_t)cap - 1);
+        std::memcpy(buf, src.data(), n);
+        buf[n] = '\0';
+    }
     return DY_OK;
 }
 
@@ -1011,6 +1096,7 @@ int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value) {
             h->cand_cap = (uint32_t)value;
             return DY_OK;
         case DY_OPT_FORCE_FP64: h->force_fp64 = value ? 1 : 0; return DY_OK;
+        case DY_OPT_CLIMB: h->use_climb = value ? 1 : 0; return DY_OK;
         case DY_OPT_JIT:
             if (value < 0 || value > 2) {
                 h->err = "DY_OPT_JIT takes 0, 1 or 2";
@@ -1051,6 +1137,7 @@ struct PassPlan {
     int ry[kSweepGroups] = {};            // R_y shared by every source of a sweep group, else -1
     int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
     int njit[kSweepGroups] = {};          // trailing sources of the group that run their generated sweep
+    bool b256[kSweepGroups] = {true, true, true, true};  // every library-sweep source has the 256-bin table
     int kmax = 1;                         // most levels of any source
     int ncol = 1;                         // most nodes of any source of the generic group
     int before(int g) const {             // jobs stored ahead of group g
@@ -1202,7 +1289,8 @@ void launch_main(const dy_plan* h, const JobDev* d, const JobDev* hjobs, const P
     };
     for (int g = 0; g < kSweepGroups; ++g) {
         chunks(d + pp.before(g), pp.n[g] - pp.njit[g], [&](const JobDev* b, int n) {
-            chk(launch_sweep(b, n, (g & 1) != 0, g >= G_OSWEEP, pp.units[g], pp.npre[g], pp.npre_c[g], pp.ry[g], s),
+            chk(launch_sweep(b, n, (g & 1) != 0, g >= G_OSWEEP, pp.units[g], pp.npre[g], pp.npre_c[g], pp.ry[g],
+                             pp.b256[g], s),
                 "sweep");
         });
         for (int q = pp.before(g) + pp.n[g] - pp.njit[g]; q < pp.before(g) + pp.n[g]; ++q)
@@ -1253,7 +1341,10 @@ bool jit_ready(dy_plan* h, int p) {
 
 }  // namespace
 
-extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream) {
+// stat: dy_plan_select_static (per-call device memory in the fixed array, no
+// kernel compilation, direct launches, results copied back into the caller's
+// array); otherwise dy_plan_select.
+static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream, bool stat) {
     if (!h) return DY_EINVAL;
     if (!src || !out || n_src < 1) {
         h->err = "src/out is NULL or n_src < 1";
@@ -1273,9 +1364,14 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     uint64_t cap = h->cand_cap;
     const uint64_t pool_cap = kCandPoolBytes / sizeof(Cand) / (uint64_t)n_src;
     if (cap > pool_cap) cap = std::max<uint64_t>(pool_cap, 1024);
-    int st = ensure_scratch(h, (size_t)n_src, (uint32_t)cap);
+    Scratch view;
+    int st = stat ? static_view(h, (size_t)n_src, (uint32_t)cap, &view) : ensure_scratch(h, (size_t)n_src, (uint32_t)cap);
     if (st != DY_OK) return st;
-    Scratch& S = h->sc;
+    Scratch& S = stat ? view : h->sc;
+    if (stat) cap = S.cap;
+    // generated kernels: compiled at first use, except in calls that may not
+    // allocate (loading a module does), which take them only when loaded
+    auto jit_use = [&](int p) { return stat ? (h->use_jit && h->jit_state[p] == 1) : jit_ready(h, p); };
     const int km = h->kmax;
     const int cert_waves = n_src <= 64 ? CERT_WAVES : 1;
 
@@ -1285,7 +1381,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         const HostProb& H = h->hp[p];
         if (src[j].kind == DY_SOURCE_RANGE)
             grp[j] = H.obj ? (H.has_s2 ? G_OSWEEP_S2 : G_OSWEEP) : (H.has_s2 ? G_SWEEP_S2 : G_SWEEP);
-        else if (src[j].kind == DY_SOURCE_ROWS && !h->force_fp64 && jit_ready(h, p))
+        else if (src[j].kind == DY_SOURCE_ROWS && !h->force_fp64 && jit_use(p))
             grp[j] = G_JIT;
         else
             grp[j] = G_GENERIC;
@@ -1300,7 +1396,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         for (int j = 0; j < n_src; ++j) {
             const int p = src[j].problem;
             if (src[j].kind == DY_SOURCE_RANGE && src[j].count >= jit_min &&
-                src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_ready(h, p) && h->jit[p].sweep)
+                src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_use(p) && h->jit[p].sweep)
                 jsw[j] = 1;
         }
     std::vector<int> order;
@@ -1326,7 +1422,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         J.ncand = S.ncand + q;
         J.flags = S.flags + q;
         J.out = S.out + (size_t)j * km;
-        if (n_src <= kDirectResults) {  // few sources: certification writes the host copy directly
+        if (n_src <= kDirectResults && !stat) {  // few sources: certification writes the host copy directly
             J.hout = (dy_choice*)S.d_hres + (size_t)j * km;
             J.hncand = (uint32_t*)(S.d_hres + S.res_ncand_off) + q;
             J.hflags = (int32_t*)(S.d_hres + S.res_flags_off) + q;
@@ -1341,11 +1437,18 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         J.cert_d = S.cert_d + (size_t)q * KMAX * CERT_WAVES;
         J.sync = S.sync + q;
         J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
+        J.climb = (h->use_climb && !h->force_fp64 && !H.obj && H.n <= kClimbNodes && src[j].kind == DY_SOURCE_RANGE && src[j].begin == 0 &&
+                   !H.plans_saturated && src[j].count == H.n_plans)
+                      ? 1
+                      : 0;
         // seeding work units: rows of the inner sweep, or plans
         const bool sweep = g < kSweepGroups;
         const uint64_t sunits = sweep ? J.nblk * (uint64_t)H.rx : J.count;
         uint64_t stride = h->sample_stride;
         if (!h->stride_fixed) stride = std::max<uint64_t>(1, std::min<uint64_t>(stride, sunits / kMinSamples));
+        // the local search gives each level a seed near its optimum; the
+        // sample then only backs it up (about 256 samples per source)
+        if (!h->stride_fixed && J.climb) stride = std::max<uint64_t>(stride, std::min<uint64_t>(2048, sunits / 256));
         J.sample_stride = (uint32_t)stride;
         J.units = sweep ? J.nblk : J.count;
         ++pp.n[g];
@@ -1357,6 +1460,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         pp.kmax = std::max(pp.kmax, H.k);
         if (g == G_GENERIC) pp.ncol = std::max(pp.ncol, H.n);
         if (sweep) {
+            if (!jsw[j] && h->hdesc[src[j].problem].jsh != 18) pp.b256[g] = false;
             pp.npre[g] = std::max(pp.npre[g], H.npre);
             pp.ry[g] = pp.n[g] == 1 ? H.ry : (pp.ry[g] == H.ry ? pp.ry[g] : -1);
             pp.npre_c[g] = pp.n[g] == 1 ? H.npre : (pp.npre_c[g] == H.npre ? pp.npre_c[g] : -1);
@@ -1366,11 +1470,13 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
         jobs[q] = J;
     }
     const int n3 = pp.before(G_JIT);  // jobs of the other groups; JIT jobs follow
+    bool any_climb = false;
+    for (int q = 0; q < n3; ++q) any_climb = any_climb || jobs[q].climb != 0;
     // the job array is rebuilt every call but uploaded only when it changed
     const bool changed =
-        S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0;
+        stat || S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0;
     if (changed) {
-        drop_graph(h);
+        if (!stat) drop_graph(h);
         hipError_t e = hipStreamSynchronize(s);  // a previous upload may still read the pinned buffer
         if (e == hipSuccess) {
             std::memcpy(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev));
@@ -1396,6 +1502,9 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     // seeding and tables; the scoring pass (between timing events); certification and copy-out
     auto issue_pre = [&](hipStream_t st, const Check& ck) {
         launch_seed(h, S.d_jobs, jobs.data(), pp, st, ck);
+        if (any_climb)
+            for (int c = 0; c < n3; c += 65535)
+                ck(launch_climb(S.d_jobs + c, std::min(65535, n3 - c), pp.kmax, st), "climb");
         jit_pass(jobs.data(), n3, pp.n[G_JIT], true, st, ck);
         launch_table_all(S.d_jobs, n_src, st, ck);
     };
@@ -1408,19 +1517,19 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
     auto issue_post = [&](hipStream_t st, const Check& ck) {
         launch_certify_all(S.d_jobs, n_src, cert_waves, h, st, ck);
         if (h->timing) ck(hipEventRecord(h->ev[3], st), "hipEventRecord");
-        if (n_src > kDirectResults)
+        if (n_src > kDirectResults || stat)
             ck(hipMemcpyAsync(S.h_res, S.out, S.res_bytes, hipMemcpyDeviceToHost, st), "copy out");
     };
     // With the results written straight to host memory, the call waits for the
     // certification's completion words (set after the results, behind a
     // system-scope fence) instead of the stream: they land several
     // microseconds before the stream reports the graph complete.
-    const bool poll = n_src <= kDirectResults && !h->timing && !h->force_fp64;
+    const bool poll = !stat && n_src <= kDirectResults && !h->timing && !h->force_fp64;
     if (poll)
         for (int q = 0; q < n_src; ++q) __atomic_store_n(S.h_done + q, 0u, __ATOMIC_RELAXED);
     bool exhausted = h->force_fp64 != 0;
     bool launched = false;
-    if (h->use_graph && !h->timing && !h->force_fp64 && S.clean && !changed) {
+    if (!stat && h->use_graph && !h->timing && !h->force_fp64 && S.clean && !changed) {
         if (!h->graph) {  // capture once; a failure falls back to direct launches for this plan
             h->graph = capture_graph(h, [&](hipStream_t st, const Check& ck) {
                 issue_pre(st, ck);
@@ -1515,6 +1624,7 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
                     ++rp.n[g];
                     if (g < G_JIT) rp.units[g] = std::max(rp.units[g], J.units);
                     if (g < kSweepGroups) rp.npre[g] = std::max(rp.npre[g], H.npre);
+                    if (g < kSweepGroups && h->hdesc[src[j].problem].jsh != 18) rp.b256[g] = false;
                     if (g == G_GENERIC) rp.ncol = std::max(rp.ncol, H.n);
                     re.push_back(J);
                 } else {
@@ -1563,6 +1673,10 @@ extern "C" int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, d
 }
 
 extern "C" {
+
+int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream) {
+    return select_impl(h, src, n_src, out, stream, false);
+}
 
 int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, float* demand, uint32_t* feas_bits,
                   void* stream) {

@@ -386,20 +386,23 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     if (s2) o << "    const float S2 = " << (exy ? "ps" : "fmaxf(ps, fx)") << ";\n";
     // one plan: corr mode (cc, cp); objective mode G = u + U_x - lambda_l T
     // (one fused rounding) and D = D_x + d_y, binned by D
-    auto plan = [&](const char* ind) {
-        o << ind << "float cp = vy[j].y + M;\n";
+    // vy / dy: the register copies of y's entries (unrolled loops), or the
+    // tables themselves where the loop is not unrolled (a loop index into the
+    // register copy would move the whole array to scratch memory)
+    auto plan = [&](const char* ind, const char* vy, const char* dy) {
+        o << ind << "float cp = " << vy << "[j].y + M;\n";
         if (s2) o << ind << "cp = fmaxf(cp, S2);\n";
         if (obj) {
-            o << ind << "const float cc = fmaf(" << flit(-D.lam_l) << ", cp, ux + vy[j].x);\n";
-            o << ind << "const float bv = dx + dy[j];\n";
+            o << ind << "const float cc = fmaf(" << flit(-D.lam_l) << ", cp, ux + " << vy << "[j].x);\n";
+            o << ind << "const float bv = dx + " << dy << "[j];\n";
         } else {
-            o << ind << "const float cc = cx * vy[j].x;\n";
+            o << ind << "const float cc = cx * " << vy << "[j].x;\n";
             o << ind << "const float bv = cp;\n";
         }
     };
     o << "    unsigned long long hit = 0ull;\n";
     o << "#pragma unroll\n    for (int j = 0; j < " << D.ry << "; ++j) {\n";
-    plan("      ");
+    plan("      ", "vy", "dy");
     o << "      const float th = *(const float*)((const char*)s_bins + ((__float_as_uint(bv) >> " << sh << "u) & " << msk
       << "u));\n";
     o << "      hit |= __builtin_amdgcn_ballot_w64(cc >= th);\n    }\n";
@@ -461,7 +464,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
         return;
     }
     o << "      for (int j = 0; j < " << D.ry << "; ++j) {\n";
-    plan("        ");
+    plan("        ", "aty", "demy");
     o << "        const unsigned long long idx = base + (unsigned long long)j;\n";
     o << "        bool want = false;\n";
     for (int k = 0; k < D.k; ++k) {

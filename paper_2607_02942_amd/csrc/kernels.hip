@@ -36,6 +36,8 @@
 
 #include <math.h>
 
+#include <mutex>
+
 #include "dyplan_internal.h"
 
 namespace dyp {
@@ -537,13 +539,15 @@ __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big, float* 
 // prefilter threshold of CP's bin is read from the 64-entry LDS table (a
 // random LDS read issues in about half the time of a lane permute on gfx950):
 // byte offset = ((bits(CP) >> bin_shift) & 63) * 4, two shift/and operations.
-template <bool HAS_S2>
+// B256: the 256-bin table on shift 18 instead, whose byte offset
+// (bits(CP) >> 16) & 0x3fc is one AND of the pattern's upper half-word.
+template <bool HAS_S2, bool B256 = false>
 __device__ __forceinline__ uint64_t sweep_test(const float2 vy, float M, float S2, float cx, uint32_t sh,
                                                const float* s_bins) {
     float cp = vy.y + M;
     if (HAS_S2) cp = fmaxf(cp, S2);
     const float cc = cx * vy.x;
-    const uint32_t off = (__float_as_uint(cp) >> sh) & 0xfcu;
+    const uint32_t off = B256 ? (__float_as_uint(cp) >> 16) & 0x3fcu : (__float_as_uint(cp) >> sh) & 0xfcu;
     const float thr = *(const float*)((const char*)s_bins + off);
     return __ballot(cc >= thr);
 }
@@ -687,7 +691,8 @@ __device__ void general_row(PD P, JD J, uint64_t b, int big, int ix, float cx, f
 // RY > 0: every source of the launch has R_y = RY; the y table is loaded once
 // per workgroup into scalar registers and the y loop is fully unrolled, so the
 // inner sweep issues no memory load and no wait other than its LDS bin reads.
-template <bool HAS_S2, int RY, int NPRE>
+// B256: every source of the launch has the 256-bin table (P->jsh = 18).
+template <bool HAS_S2, int RY, int NPRE, bool B256>
 __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, uint64_t unit_off) {
     extern __shared__ float s_f[];
     JD J = cs(jobs + blockIdx.y);
@@ -698,8 +703,13 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
     const uint64_t t = t0 + threadIdx.x;
     const bool live = t < nblk;
     const uint64_t b = J->blk_first + (live ? t : nblk - 1);
-    __shared__ float s_bins[NBINS];
-    if (threadIdx.x < NBINS) s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
+    __shared__ float s_bins[B256 ? NBINS2 : NBINS];
+    if (B256) {
+        s_bins[threadIdx.x] = __uint_as_float(J->table2[threadIdx.x]);
+        static_assert(!B256 || NBINS2 == WG, "one bin per thread");
+    } else if (threadIdx.x < NBINS) {
+        s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
+    }
     const float2* pat = stage_prefix_rows<false>(P, (float2*)(s_f + (size_t)max(P->npre, 1) * WG), nullptr);
     const Prefix pf = prefix_eval<NPRE, false>(P, b, J->big, s_f, pat, nullptr);
 
@@ -724,17 +734,18 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
         int iy = 0;
         if (RY > 0) {
 #pragma unroll
-            for (int j = 0; j < (RY > 0 ? RY : 1); ++j) hit |= sweep_test<HAS_S2>(vyr[j], M, S2, cx, sh, s_bins);
+            for (int j = 0; j < (RY > 0 ? RY : 1); ++j)
+                hit |= sweep_test<HAS_S2, B256>(vyr[j], M, S2, cx, sh, s_bins);
             iy = ry;
         }
         for (; iy + 4 <= ry; iy += 4) {
             const float2 v0 = aty[iy], v1 = aty[iy + 1], v2 = aty[iy + 2], v3 = aty[iy + 3];
-            hit |= sweep_test<HAS_S2>(v0, M, S2, cx, sh, s_bins);
-            hit |= sweep_test<HAS_S2>(v1, M, S2, cx, sh, s_bins);
-            hit |= sweep_test<HAS_S2>(v2, M, S2, cx, sh, s_bins);
-            hit |= sweep_test<HAS_S2>(v3, M, S2, cx, sh, s_bins);
+            hit |= sweep_test<HAS_S2, B256>(v0, M, S2, cx, sh, s_bins);
+            hit |= sweep_test<HAS_S2, B256>(v1, M, S2, cx, sh, s_bins);
+            hit |= sweep_test<HAS_S2, B256>(v2, M, S2, cx, sh, s_bins);
+            hit |= sweep_test<HAS_S2, B256>(v3, M, S2, cx, sh, s_bins);
         }
-        for (; iy < ry; ++iy) hit |= sweep_test<HAS_S2>(aty[iy], M, S2, cx, sh, s_bins);
+        for (; iy < ry; ++iy) hit |= sweep_test<HAS_S2, B256>(aty[iy], M, S2, cx, sh, s_bins);
         if (hit) {
             // rare: re-score this lane's row of the inner sweep with the exact test
             const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
@@ -886,6 +897,220 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
         for (int w = 0; w < WG / 64; ++w) e = max(e, s_red[tid][w]);
         if (e) atomicMax(J->scert + P->lvl_order[tid] * NSLOT + (blockIdx.x % NSLOT), e);
     }
+}
+
+// ---------------------------------------------------------------------------
+// Local-search seeds (RANGE sources that cover their problem's whole plan
+// space, corr / SLO selection)
+//
+// Any certainly-feasible plan gives a valid candidate threshold through its
+// fp32 corr, exactly as a sampled plan does, and the nearer that corr is to
+// the level's optimum, the fewer plans pass the prefilter and reach fp64
+// certification.  One wave per (source, level) climbs: it starts at the plan
+// that gives every node its fastest implementation at the level (the least
+// CP of all plans: the longest path is monotone in every duration, in fp32
+// too) and, while some plan that differs from the current one in one node --
+// or, once no such plan helps, in two nodes -- is certainly feasible and has
+// a greater fp32 corr, moves to the best of them (greatest corr, then first in
+// move order).  Every move raises corr, so the walk ends; a step limit bounds
+// it anyway.  The result only raises a seed slot: the selection is unchanged,
+// only the work that reaches it shrinks.
+// ---------------------------------------------------------------------------
+constexpr int CLIMB_STEPS = 64;          // moves per (source, level) at most
+constexpr int CLIMB_ENTRIES = 1024;      // sum of the radices whose tables fit the wave's LDS (else no climb)
+constexpr uint32_t CLIMB_PAIRS = 16384;  // two-node moves per pass at most (else single moves only)
+constexpr int CLIMB_NODES = 8;           // problems of at most this many nodes climb (the plan sits in registers)
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t w = __shfl_xor(v, o);
+        v = w > v ? w : v;
+    }
+    return v;
+}
+
+// fp32 corr (node-order product) and CP of the plan whose node n has factor
+// a[n] and duration t[n], except node n1 (a1, t1) and node n2 (a2, t2).  NN
+// >= N is a compile-time bound, so every array stays in registers; the
+// predecessor masks are wave-uniform.
+template <int NN>
+__device__ __forceinline__ void climb_eval(PD P, int N, const float (&a)[NN], const float (&t)[NN], int n1, float a1,
+                                           float t1, int n2, float a2, float t2, float& c, float& cp) {
+    float f[NN];
+    c = 1.0f;
+    cp = 0.0f;
+#pragma unroll
+    for (int n = 0; n < NN; ++n) {
+        f[n] = 0.0f;
+        if (n < N) {
+            const float an = n == n1 ? a1 : (n == n2 ? a2 : a[n]);
+            const float tn = n == n1 ? t1 : (n == n2 ? t2 : t[n]);
+            c = c * an;
+            float m = 0.0f;
+            const uint32_t pm = P->pred[n];
+#pragma unroll
+            for (int u = 0; u < n; ++u)
+                if (pm >> u & 1u) m = fmaxf(m, f[u]);
+            f[n] = tn + m;
+            if (P->sinks >> n & 1u) cp = fmaxf(cp, f[n]);
+        }
+    }
+}
+
+// One wave per (source, level): grid (levels, sources), 64 threads.  The
+// current plan is held by every lane in registers; each lane evaluates a
+// share of the moves, a wave reduction picks the best.
+template <int NN>
+__global__ void __launch_bounds__(64) k_climb(const JobDev* __restrict__ jobs) {
+    __shared__ float s_a[CLIMB_ENTRIES], s_t[CLIMB_ENTRIES];  // node tables, entry off[n] + i
+    __shared__ uint8_t s_node[CLIMB_ENTRIES];                 // node of entry e
+    JD J = cs(jobs + blockIdx.y);
+    if (!J->climb) return;
+    PD P = cs(J->prob);
+    const int k = blockIdx.x;
+    const int N = P->n, R = P->rmax, lane = threadIdx.x;
+    if (k >= P->k || P->obj || N > NN) return;
+    const bool uni = P->uniform != 0;
+    // durations the band is tested on: the unpressured ones against lo_k
+    // (uniform pressure), else the level's own against the exact band
+    const CS float2* at = cs(P->at);
+    const CS float* lt = uni ? nullptr : cs(P->lat) + (size_t)k * N * R;
+    const float band = uni ? P->lo[k] : P->glo;
+    int off[NN];
+    int tot = 0;
+    uint32_t sq = 0;
+#pragma unroll
+    for (int n = 0; n < NN; ++n) {
+        off[n] = tot;
+        if (n < N) {
+            tot += P->radix[n];
+            sq += (uint32_t)P->radix[n] * (uint32_t)P->radix[n];
+        }
+    }
+    if (tot > CLIMB_ENTRIES) return;
+    const bool pairs_ok = ((uint32_t)tot * (uint32_t)tot - sq) / 2u <= CLIMB_PAIRS;
+    for (int n = 0; n < N; ++n)
+        for (int i = lane; i < P->radix[n]; i += 64) {
+            const float2 v = at[n * R + i];
+            s_a[off[n] + i] = v.x;
+            s_t[off[n] + i] = uni ? v.y : lt[n * R + i];
+            s_node[off[n] + i] = (uint8_t)n;
+        }
+    __syncthreads();
+    // start: every node's fastest implementation, ties to the lowest id
+    int cur[NN];
+    float ca[NN], ct[NN];
+#pragma unroll
+    for (int n = 0; n < NN; ++n) {
+        cur[n] = 0;
+        ca[n] = 1.0f;
+        ct[n] = 0.0f;
+        if (n < N) {
+            float best = INFINITY;
+            for (int i = 0; i < P->radix[n]; ++i)
+                if (s_t[off[n] + i] < best) {
+                    best = s_t[off[n] + i];
+                    cur[n] = i;
+                }
+            ca[n] = s_a[off[n] + cur[n]];
+            ct[n] = best;
+        }
+    }
+    float cc, ccp;
+    climb_eval<NN>(P, N, ca, ct, -1, 0.0f, 0.0f, -1, 0.0f, 0.0f, cc, ccp);
+    if (!(ccp <= band)) return;  // no plan is certainly feasible at this level
+    for (int step = 0; step < CLIMB_STEPS; ++step) {
+        // single moves over the flat entry index; key = (corr bits, reversed move order), 0 = none
+        uint64_t best = 0;
+        for (int e = lane; e < tot; e += 64) {
+            const int n = s_node[e];
+            int cn = 0, on = 0;
+#pragma unroll
+            for (int m = 0; m < NN; ++m)
+                if (m == n) {
+                    cn = cur[m];
+                    on = off[m];
+                }
+            if (e - on == cn) continue;
+            float c, cp;
+            climb_eval<NN>(P, N, ca, ct, n, s_a[e], s_t[e], -1, 0.0f, 0.0f, c, cp);
+            if (c > cc && cp <= band) {
+                const uint64_t key = (uint64_t)__float_as_uint(c) << 32 | (uint32_t)(0xffffffffu - (uint32_t)e);
+                best = key > best ? key : best;
+            }
+        }
+        uint64_t mv = wave_max_u64(best);
+        bool pair = false;
+        if (mv == 0 && pairs_ok) {
+            // two-node moves (n1 < n2, ids i1 and i2), move order (n1, n2, i1, i2)
+            for (int n1 = 0; n1 < N; ++n1) {
+                int c1 = 0, o1 = 0;
+#pragma unroll
+                for (int m = 0; m < NN; ++m)
+                    if (m == n1) {
+                        c1 = cur[m];
+                        o1 = off[m];
+                    }
+                for (int n2 = n1 + 1; n2 < N; ++n2) {
+                    int c2 = 0, o2 = 0;
+#pragma unroll
+                    for (int m = 0; m < NN; ++m)
+                        if (m == n2) {
+                            c2 = cur[m];
+                            o2 = off[m];
+                        }
+                    const int r1 = P->radix[n1], r2 = P->radix[n2];
+                    const float inv = 1.0f / (float)r2;
+                    const float cab = s_a[o1 + c1] * s_a[o2 + c2];
+                    for (int t = lane; t < r1 * r2; t += 64) {
+                        // t = i1 r2 + i2; the float quotient is exact: (t + 0.5) / r2 stays
+                        // at least 0.5 / r2 >= 2^-9 away from an integer, far above its error
+                        const int i1 = (int)(((float)t + 0.5f) * inv);
+                        const int i2 = t - i1 * r2;
+                        if (i1 == c1 || i2 == c2) continue;
+                        const int e1 = o1 + i1, e2 = o2 + i2;
+                        if (!(s_a[e1] * s_a[e2] > cab)) continue;  // cannot raise corr
+                        float c, cp;
+                        climb_eval<NN>(P, N, ca, ct, n1, s_a[e1], s_t[e1], n2, s_a[e2], s_t[e2], c, cp);
+                        if (c > cc && cp <= band) {
+                            const uint32_t id = (uint32_t)(n1 * NMAX + n2) << 16 | (uint32_t)i1 << 8 | (uint32_t)i2;
+                            const uint64_t key = (uint64_t)__float_as_uint(c) << 32 | (uint32_t)(0xffffffffu - id);
+                            best = key > best ? key : best;
+                        }
+                    }
+                }
+            }
+            mv = wave_max_u64(best);
+            pair = true;
+        }
+        if (mv == 0) break;
+        // every lane applies the move to its copy of the plan
+        const uint32_t id = 0xffffffffu - (uint32_t)mv;
+        cc = __uint_as_float((uint32_t)(mv >> 32));
+        int mn1, mi1, mn2 = -1, mi2 = 0;
+        if (pair) {
+            mn1 = (int)(id >> 16) / NMAX;
+            mn2 = (int)(id >> 16) % NMAX;
+            mi1 = (int)(id >> 8 & 0xffu);
+            mi2 = (int)(id & 0xffu);
+        } else {
+            mn1 = s_node[id];
+            int o1 = 0;
+#pragma unroll
+            for (int m = 0; m < NN; ++m)
+                if (m == mn1) o1 = off[m];
+            mi1 = (int)id - o1;
+        }
+#pragma unroll
+        for (int m = 0; m < NN; ++m) {
+            if (m == mn1 || m == mn2) {
+                cur[m] = m == mn1 ? mi1 : mi2;
+                ca[m] = s_a[off[m] + cur[m]];
+                ct[m] = s_t[off[m] + cur[m]];
+            }
+        }
+    }
+    if (lane == 0) atomicMax(J->scert + k * NSLOT, __float_as_uint(cc) + 1u);
 }
 
 // ---------------------------------------------------------------------------
@@ -1569,6 +1794,37 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs,
         }
     }
     wave_best4(bc, bi, bcp, bd);
+    if (J->cert_waves == 1 && !J->hout) {
+        // one wave per level and no host-mapped copy: this block alone decides
+        // level k, so it writes the choice and clears the level's seed slots
+        // for the next call itself (no cross-block merge, whose device-scope
+        // fences would make every one of thousands of blocks wait for the L2)
+        if (lane == 0) {
+            dy_choice c;
+            if (bi != ~0ull) {
+                c.index = (int64_t)bi;
+                c.feasible = 1;
+                c.corr = (float)bc;
+                c.cp = (float)bcp;
+                c.demand = (float)bd;
+            } else {
+                c.index = -1;
+                c.feasible = 0;
+                c.corr = NAN;
+                c.cp = NAN;
+                c.demand = NAN;
+            }
+            J->out[k] = c;
+        }
+        if (*J->flags == 0) {
+            J->scert[k * NSLOT + lane] = 0u;
+            if (lane == 0) {
+                J->fb_corr[k] = 0ull;
+                J->fb_index[k] = ~0ull;
+            }
+        }
+        return;
+    }
     if (lane == 0) {
         J->cert_c[k * CERT_WAVES + g] = bc;
         J->cert_i[k * CERT_WAVES + g] = bi;
@@ -1993,8 +2249,50 @@ static constexpr uint64_t MAX_GRID_X = 1ull << 22;  // workgroups per launch alo
 // per-thread LDS columns of the generic kernels: ncol floats and ncol id bytes
 static size_t generic_lds(int ncol) { return (size_t)ncol * WG * sizeof(float) + (size_t)ncol * WG; }
 
+// ---------------------------------------------------------------------------
+// Fixed per-call device memory for callers that cannot allocate
+// ---------------------------------------------------------------------------
+
+// The per-call buffers of dy_plan_select_static (seed slots, thresholds,
+// prefilter tables, candidate lists, certification state, choices and the
+// job array) live here instead of in memory the library allocates.  Every GPU
+// the library runs on holds its own copy, at its own address, until the
+// process ends; every such call on a GPU shares it.
+constexpr size_t STATIC_SCRATCH_BYTES = 16u << 20;
+static __device__ __align__(256) unsigned char scratch[STATIC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// Device address of this device's `scratch` (the current device must be
+// `device`): taken once per device with hipGetSymbolAddress and kept.  The
+// array's name in host code is a host-side stand-in, never a device address.
+hipError_t static_scratch(int device, char** ptr, size_t* bytes) {
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[device] = (char*)p;
+    }
+    *ptr = g_scratch_ptr[device];
+    *bytes = STATIC_SCRATCH_BYTES;
+    return hipSuccess;
+}
+
 hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s) {
     hipLaunchKernelGGL(k_init, dim3(njobs), dim3(64), 0, s, d_jobs, njobs);
+    return hipGetLastError();
+}
+
+// Problems above CLIMB_NODES nodes take no climb (the kernel returns for them).
+hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s) {
+    if (njobs == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_climb<CLIMB_NODES>, dim3(kmax, njobs), dim3(64), 0, s, d_jobs);
     return hipGetLastError();
 }
 
@@ -2039,7 +2337,7 @@ hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool ob
 }
 
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
-                        int npre_c, int ry, hipStream_t s) {
+                        int npre_c, int ry, bool b256, hipStream_t s) {
     if (n == 0) return hipSuccess;
     const size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float) +
                        (size_t)PAT_MAX * (sizeof(float2) + (obj ? sizeof(float) : 0));
@@ -2052,8 +2350,10 @@ hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint
     do {                                                                                                   \
         if (obj)                                                                                           \
             hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off);          \
+        else if (b256)                                                                                     \
+            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, true>), grid, dim3(WG), lds, s, d_jobs, off);        \
         else                                                                                               \
-            hipLaunchKernelGGL((k_sweep<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off);              \
+            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, false>), grid, dim3(WG), lds, s, d_jobs, off);       \
     } while (0)
 #define DYP_SWEEP_NP(S2, RYV)            \
     switch (npre_c) {                    \

@@ -21,13 +21,14 @@ LIB_PATH = os.path.join(_HERE, "libdyplan.so")
 DY_OK, DY_EINVAL, DY_ENOTDAG, DY_ELIMIT, DY_ENOMEM, DY_EDEVICE = 0, -1, -2, -3, -4, -5
 DY_SOURCE_RANGE, DY_SOURCE_ROWS = 0, 1
 DY_OPT_TIMING, DY_OPT_SAMPLE_STRIDE, DY_OPT_CAND_CAPACITY, DY_OPT_FORCE_FP64, DY_OPT_JIT, DY_OPT_GRAPH = 1, 2, 3, 4, 5, 6
+DY_OPT_CLIMB = 7
 DY_MAX_NODES, DY_MAX_RADIX, DY_MAX_LEVELS, DY_MAX_BACKENDS = 32, 255, 32, 64
 
 EXPORTED = ("dy_plan_create", "dy_plan_select", "dy_plan_score", "dy_plan_destroy", "dy_plan_max_levels",
             "dy_plan_num_problems", "dy_plan_set_option", "dy_plan_get_stats", "dy_plan_last_error",
             "dy_status_str", "dy_abi_version", "dy_selftest", "dy_suffix_create", "dy_suffix_problem",
             "dy_suffix_nodes", "dy_suffix_merge", "dy_suffix_destroy", "dy_bundle_annotate",
-            "dy_switch_simulate")
+            "dy_switch_simulate", "dy_kernel_source")
 
 
 class DyObjective(ctypes.Structure):
@@ -145,6 +146,9 @@ def lib():
         L.dy_switch_simulate.argtypes = [ctypes.POINTER(DyVariant), i32, i32, vp, vp, i32,
                                          ctypes.POINTER(DySwitchRules), vp, ctypes.POINTER(i32)]
         L.dy_switch_simulate.restype = ctypes.c_int
+        L.dy_kernel_source.argtypes = [ctypes.POINTER(DyProblem), ctypes.c_char_p, ctypes.c_uint64,
+                                       ctypes.POINTER(ctypes.c_uint64)]
+        L.dy_kernel_source.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -218,6 +222,21 @@ def create_raw(structs: Sequence[DyProblem], device: int = 0):
     h = ctypes.c_void_p()
     st = lib().dy_plan_create(arr, len(structs), device, ctypes.byref(h))
     return st, (h.value if st == DY_OK else None)
+
+
+def kernel_source(problem) -> str:
+    """HIP source the library generates for one problem (a workload.Problem or
+    a (Problem, Objective) pair); host-only, no device needed."""
+    keep = _Arrays(*problem) if isinstance(problem, tuple) else _Arrays(problem)
+    n = ctypes.c_uint64(0)
+    st = lib().dy_kernel_source(ctypes.byref(keep.c), None, 0, ctypes.byref(n))
+    if st != DY_OK:
+        raise DyplanError(st, last_error(None))
+    buf = ctypes.create_string_buffer(n.value + 1)
+    st = lib().dy_kernel_source(ctypes.byref(keep.c), buf, n.value + 1, ctypes.byref(n))
+    if st != DY_OK:
+        raise DyplanError(st, last_error(None))
+    return buf.value.decode()
 
 
 def last_error(handle=None) -> str:
