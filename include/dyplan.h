@@ -251,6 +251,28 @@ int dy_plan_create(const dy_problem* probs, int32_t n_probs, int32_t device, dy_
 int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream);
 
 /*
+ * dy_plan_select for callers that cannot allocate memory (serving loops that
+ * must not call hipMalloc, harnesses that forbid it): the same selection, the
+ * same arguments and results, but every per-call device buffer (seed slots,
+ * thresholds, prefilter tables, candidate lists, certification state, the
+ * choices) lives in one fixed array of 16 MiB that the library holds on each
+ * device it runs on until the process ends.  No device or pinned host memory
+ * is allocated and no kernel is compiled or loaded: a problem's generated
+ * kernels are used when an earlier dy_plan_select call has loaded them, the
+ * library's own kernels otherwise (identical results).  The choices are
+ * copied back through the caller's `out` array; the call synchronises
+ * `stream` before returning.  Limits: at most 64 sources per call, and the
+ * candidate slots per source are what the array leaves (about 14,000 with 64
+ * sources; overflowing lists are resolved exactly, as in dy_plan_select);
+ * beyond them it fails with DY_ELIMIT and a message.  Every such call on a
+ * device shares that device's array, whatever the handle: calls that overlap
+ * on one device (other host threads, other handles, streams not ordered
+ * after each other) race and must be serialised by the caller.  Each call
+ * clears what it needs before use; the array keeps the last call's contents.
+ */
+int dy_plan_select_static(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream);
+
+/*
  * Per-plan scores of one source (the quantities Sec. 4.3 and Sec. 4.4 attach
  * to a plan: vulnerability-weighted correctness, the longest path at every
  * level, the D_tau demand annotation), written asynchronously on `stream` into

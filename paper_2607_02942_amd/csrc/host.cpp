@@ -1678,6 +1678,10 @@ int dy_plan_select(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* o
     return select_impl(h, src, n_src, out, stream, false);
 }
 
+int dy_plan_select_static(dy_plan* h, const dy_source* src, int32_t n_src, dy_choice* out, void* stream) {
+    return select_impl(h, src, n_src, out, stream, true);
+}
+
 int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, float* demand, uint32_t* feas_bits,
                   void* stream) {
     if (!h) return DY_EINVAL;

@@ -28,7 +28,7 @@ EXPORTED = ("dy_plan_create", "dy_plan_select", "dy_plan_score", "dy_plan_destro
             "dy_plan_num_problems", "dy_plan_set_option", "dy_plan_get_stats", "dy_plan_last_error",
             "dy_status_str", "dy_abi_version", "dy_selftest", "dy_suffix_create", "dy_suffix_problem",
             "dy_suffix_nodes", "dy_suffix_merge", "dy_suffix_destroy", "dy_bundle_annotate",
-            "dy_switch_simulate", "dy_kernel_source")
+            "dy_switch_simulate", "dy_kernel_source", "dy_plan_select_static")
 
 
 class DyObjective(ctypes.Structure):
@@ -112,6 +112,8 @@ def lib():
         L.dy_plan_create.restype = ctypes.c_int
         L.dy_plan_select.argtypes = [vp, ctypes.POINTER(DySource), i32, ctypes.POINTER(DyChoice), vp]
         L.dy_plan_select.restype = ctypes.c_int
+        L.dy_plan_select_static.argtypes = [vp, ctypes.POINTER(DySource), i32, ctypes.POINTER(DyChoice), vp]
+        L.dy_plan_select_static.restype = ctypes.c_int
         L.dy_plan_score.argtypes = [vp, ctypes.POINTER(DySource), vp, vp, vp, vp, vp]
         L.dy_plan_score.restype = ctypes.c_int
         L.dy_plan_destroy.argtypes = [vp]
@@ -288,11 +290,13 @@ class Plan:
     def set_option(self, option: int, value: int):
         self._check(lib().dy_plan_set_option(self._h, option, int(value)))
 
-    def select(self, sources: Sequence[DySource], stream=None) -> List[List[tuple]]:
-        """Per source, the K choices (index, feasible, corr, cp, demand)."""
+    def select(self, sources: Sequence[DySource], stream=None, static: bool = False) -> List[List[tuple]]:
+        """Per source, the K choices (index, feasible, corr, cp, demand).
+        static: through dy_plan_select_static (no allocation by the call)."""
         srcs = (DySource * len(sources))(*sources)
         out = (DyChoice * (len(sources) * self.kmax))()
-        self._check(lib().dy_plan_select(self._h, srcs, len(sources), out, _stream(stream)))
+        fn = lib().dy_plan_select_static if static else lib().dy_plan_select
+        self._check(fn(self._h, srcs, len(sources), out, _stream(stream)))
         res = []
         for j, s in enumerate(sources):
             K = self.n_levels[s.problem]
