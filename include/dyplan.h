@@ -218,9 +218,11 @@ enum {
     DY_OPT_GRAPH = 6,           /* 1: replay a call that repeats the previous one (same sources) from a
                                    HIP graph of its launches (default 1; calls with DY_OPT_TIMING on
                                    launch directly); results are identical */
-    DY_OPT_CLIMB = 7            /* 1 (default): RANGE sources that cover their problem's whole plan space
-                                   (corr / SLO selection) also seed each level's threshold from a local
-                                   search over the plans; 0: sampled seeds only; results are identical */
+    DY_OPT_CLIMB = 7            /* local-search seeds: RANGE sources that cover the whole plan space of a
+                                   corr / SLO problem of at most 8 nodes also seed each level's threshold
+                                   from a local search over the plans (the sampling pass then thins out).
+                                   0: never; 1 (default): in calls of at least 128 such sources; 2: for
+                                   every such source.  Results are identical */
 };
 
 /*

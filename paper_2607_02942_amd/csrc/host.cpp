@@ -22,7 +22,7 @@ hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_samples,
                                int npre_max, int npre_c, int kmax, hipStream_t s);
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
-                        int npre_c, int ry, bool b256, hipStream_t s);
+                        int npre_c, int ry, bool b256, bool rad12, hipStream_t s);
 hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, int ncol, hipStream_t s);
 hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol, hipStream_t s);
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, int nmax, int nrmax, hipStream_t s);
@@ -59,6 +59,7 @@ constexpr int kDirectResults = 64;                // up to this many sources, re
 constexpr int kStaticSources = 64;                // sources per dy_plan_select_static call at most
 constexpr uint32_t kStaticMinCand = 1024;         // candidate slots per source it needs at least
 constexpr int kClimbNodes = 8;                    // local-search seeds for problems of at most this many nodes
+constexpr int kClimbMinSources = 128;             // ... in calls of at least this many such sources (DY_OPT_CLIMB 1)
 constexpr double kU = 0x1p-24;                    // fp32 unit roundoff
 
 struct HostProb {
@@ -357,7 +358,7 @@ struct dy_plan {
     bool stride_fixed = false;
     uint32_t cand_cap = 1u << 16;
     int force_fp64 = 0;
-    int use_climb = 1;                // local-search seeds for sources over a whole plan space
+    int use_climb = 1;                // local-search seeds: 0 never, 1 for calls of many sources, 2 always
     std::vector<char> st_host;        // host copies of dy_plan_select_static's jobs and results
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     // A call that repeats the previous one (same job array, scratch clear) is
@@ -1096,7 +1097,13 @@ int dy_plan_set_option(dy_plan* h, int32_t option, int64_t value) {
             h->cand_cap = (uint32_t)value;
             return DY_OK;
         case DY_OPT_FORCE_FP64: h->force_fp64 = value ? 1 : 0; return DY_OK;
-        case DY_OPT_CLIMB: h->use_climb = value ? 1 : 0; return DY_OK;
+        case DY_OPT_CLIMB:
+            if (value < 0 || value > 2) {
+                h->err = "DY_OPT_CLIMB takes 0, 1 or 2";
+                return DY_EINVAL;
+            }
+            h->use_climb = (int)value;
+            return DY_OK;
         case DY_OPT_JIT:
             if (value < 0 || value > 2) {
                 h->err = "DY_OPT_JIT takes 0, 1 or 2";
@@ -1138,6 +1145,7 @@ struct PassPlan {
     int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
     int njit[kSweepGroups] = {};          // trailing sources of the group that run their generated sweep
     bool b256[kSweepGroups] = {true, true, true, true};  // every library-sweep source has the 256-bin table
+    bool rad12[kSweepGroups] = {true, true, true, true}; // ... and 12 implementations per prefix node, 32-bit blocks
     int kmax = 1;                         // most levels of any source
     int ncol = 1;                         // most nodes of any source of the generic group
     int before(int g) const {             // jobs stored ahead of group g
@@ -1290,7 +1298,7 @@ void launch_main(const dy_plan* h, const JobDev* d, const JobDev* hjobs, const P
     for (int g = 0; g < kSweepGroups; ++g) {
         chunks(d + pp.before(g), pp.n[g] - pp.njit[g], [&](const JobDev* b, int n) {
             chk(launch_sweep(b, n, (g & 1) != 0, g >= G_OSWEEP, pp.units[g], pp.npre[g], pp.npre_c[g], pp.ry[g],
-                             pp.b256[g], s),
+                             pp.b256[g], pp.rad12[g], s),
                 "sweep");
         });
         for (int q = pp.before(g) + pp.n[g] - pp.njit[g]; q < pp.before(g) + pp.n[g]; ++q)
@@ -1399,6 +1407,18 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
                 src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_use(p) && h->jit[p].sweep)
                 jsw[j] = 1;
         }
+    // local-search seeds (whole-space RANGE sources of corr / SLO problems of at
+    // most kClimbNodes nodes): in calls of many such sources, where they replace
+    // most of the sampling and of the certification work; a call of a few
+    // sources waits for the searches' latency instead (tens of microseconds)
+    auto climb_ok = [&](int j) {
+        const HostProb& H = h->hp[src[j].problem];
+        return !h->force_fp64 && !H.obj && H.n <= kClimbNodes && src[j].kind == DY_SOURCE_RANGE &&
+               src[j].begin == 0 && !H.plans_saturated && src[j].count == H.n_plans;
+    };
+    int n_climb = 0;
+    for (int j = 0; j < n_src; ++j) n_climb += climb_ok(j) ? 1 : 0;
+    const bool climb = h->use_climb == 2 || (h->use_climb == 1 && n_climb >= kClimbMinSources);
     std::vector<int> order;
     order.reserve(n_src);
     for (int g = 0; g < kGroups; ++g)
@@ -1437,10 +1457,7 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         J.cert_d = S.cert_d + (size_t)q * KMAX * CERT_WAVES;
         J.sync = S.sync + q;
         J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
-        J.climb = (h->use_climb && !h->force_fp64 && !H.obj && H.n <= kClimbNodes && src[j].kind == DY_SOURCE_RANGE && src[j].begin == 0 &&
-                   !H.plans_saturated && src[j].count == H.n_plans)
-                      ? 1
-                      : 0;
+        J.climb = climb && climb_ok(j) ? 1 : 0;
         // seeding work units: rows of the inner sweep, or plans
         const bool sweep = g < kSweepGroups;
         const uint64_t sunits = sweep ? J.nblk * (uint64_t)H.rx : J.count;
@@ -1461,6 +1478,12 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         if (g == G_GENERIC) pp.ncol = std::max(pp.ncol, H.n);
         if (sweep) {
             if (!jsw[j] && h->hdesc[src[j].problem].jsh != 18) pp.b256[g] = false;
+            if (!jsw[j]) {
+                const ProbDev& Dp = h->hdesc[src[j].problem];
+                bool r12 = J.big == 0;
+                for (int n = 0; n < Dp.npre; ++n) r12 = r12 && Dp.radix[n] == 12;
+                if (!r12) pp.rad12[g] = false;
+            }
             pp.npre[g] = std::max(pp.npre[g], H.npre);
             pp.ry[g] = pp.n[g] == 1 ? H.ry : (pp.ry[g] == H.ry ? pp.ry[g] : -1);
             pp.npre_c[g] = pp.n[g] == 1 ? H.npre : (pp.npre_c[g] == H.npre ? pp.npre_c[g] : -1);
@@ -1625,6 +1648,7 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
                     if (g < G_JIT) rp.units[g] = std::max(rp.units[g], J.units);
                     if (g < kSweepGroups) rp.npre[g] = std::max(rp.npre[g], H.npre);
                     if (g < kSweepGroups && h->hdesc[src[j].problem].jsh != 18) rp.b256[g] = false;
+                    rp.rad12[g] = false;  // reseeded sources take the general kernel
                     if (g == G_GENERIC) rp.ncol = std::max(rp.ncol, H.n);
                     re.push_back(J);
                 } else {

@@ -78,6 +78,7 @@ __device__ __forceinline__ unsigned dy_wmax(unsigned v) {
 // the global candidate list at the end; a full queue raises the overflow flag,
 // which the host resolves exactly by reseeding and rescoring the source.
 #define DY_QCAP 128
+#define DY_RQCAP 64
 __device__ void dy_flush(DyCand* q, unsigned qn, int lane, DyCand* cand, unsigned cap, unsigned* ncand,
                          bool* ovf) {
   if (qn == 0) return;
@@ -602,8 +603,9 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
     };
     if (!D.obj && !D.uniform) {
         // per-backend pressure: level k's fp32 CP of the row in words w0..,
-        // from that level's durations L (the generic kernel's order)
-        o << "__device__ __noinline__ float dy_cpk(";
+        // from that level's durations L (the generic kernel's order), inlined
+        // at every use
+        o << "__device__ __forceinline__ float dy_cpk(";
         for (int q = 0; q < Q; ++q) o << "unsigned w" << q << ", ";
         o << "const float* __restrict__ L, int rmax) {\n";
         for (int n = 0; n < N; ++n) {
@@ -760,18 +762,31 @@ __device__ __forceinline__ void dy_stage(const float2* __restrict__ at, int rmax
         o << "      for (int k = 0; k < DY_K; ++k) if (fma(-dy_m64[k], (double)cp, (double)c) >= (double)thr[k]) w2 = true; \\\n";
     else
         o << "      for (int k = 0; k < DY_K; ++k) if (cp <= hi[k] && c >= thr[k]) w2 = true; \\\n";
-    if (!D.obj && !D.uniform) {
-        // per-backend pressure: the bands above are those of the unpressured
-        // CP; a row that passes them takes each level's exact fp32 CP_k (its
-        // durations from the level's table), as the generic kernel does
-        o << "      if (w2) { \\\n        w2 = false; \\\n"
-             "        for (int k = 0; k < DY_K && !w2; ++k) \\\n"
-             "          if (c >= thr[k] && cp <= dy_hi[k] && dy_cpk(" << wl("y") << ", lat + (unsigned long long)k * DY_N * "
-             "(unsigned long long)rmax, rmax) <= " << flit(D.ghi) << ") w2 = true; \\\n      } \\\n";
-    }
     o << R"(      want = w2; \
     } \
-    const unsigned long long m_ = __builtin_amdgcn_ballot_w64(want); \
+)";
+    if (!D.obj && !D.uniform) {
+        // per-backend pressure: the bands above are those of the unpressured
+        // CP; a row that passes them is parked in the wave's refine queue and
+        // takes each level's exact fp32 CP_k (its durations from the level's
+        // table) after the row loop, where that code adds no register
+        // pressure to the loop; a full refine queue sends the rows straight
+        // to the candidate list (certification decides them exactly)
+        o << R"(    { const unsigned long long r_ = __builtin_amdgcn_ballot_w64(want); \
+      if (r_) { \
+        const unsigned rn_ = (unsigned)__builtin_popcountll(r_); \
+        if (rqn + rn_ <= DY_RQCAP) { \
+          if (want) { \
+            const unsigned o_ = rqn + __builtin_amdgcn_mbcnt_hi((unsigned)(r_ >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)r_, 0u)); \
+            rq[o_].index = (rr); rq[o_].corr = c; rq[o_].cp = cp; \
+          } \
+          rqn += rn_; \
+          want = false; \
+        } \
+      } } \
+)";
+    }
+    o << R"(    const unsigned long long m_ = __builtin_amdgcn_ballot_w64(want); \
     if (m_) { \
       const unsigned n_ = (unsigned)__builtin_popcountll(m_); \
       if (qn + n_ > DY_QCAP) { \
@@ -801,7 +816,10 @@ __device__ __forceinline__ void dy_scan_body(
   __shared__ float2 s_tab[DY_TAB];
   __shared__ float s_bins[64];
   __shared__ DyCand s_q[4][DY_QCAP];
-  dy_stage(at, rmax, table, s_tab, s_bins);
+)";
+    if (!D.obj && !D.uniform)
+        o << "  __shared__ DyCand s_rq[4][DY_RQCAP];\n  DyCand* rq = s_rq[threadIdx.x >> 6];\n  unsigned rqn = 0;\n";
+    o << R"(  dy_stage(at, rmax, table, s_tab, s_bins);
   const int lane = threadIdx.x & 63;
   DyCand* q = s_q[threadIdx.x >> 6];
   unsigned qn = 0;
@@ -846,7 +864,41 @@ __device__ __forceinline__ void dy_scan_body(
     p += step;
     r += G;
   }
-  dy_flush(q, qn, lane, cand, cap, ncand, &ovf);
+)";
+    if (!D.obj && !D.uniform) {
+        // the parked rows: reload each, then its exact fp32 CP_k at every
+        // level whose threshold and band it meets
+        o << R"(  for (unsigned i0 = 0; i0 < rqn; i0 += 64) {
+    const unsigned i = i0 + lane;
+    bool keep = false;
+    DyCand e = {0ull, 0.0f, 0.0f};
+    if (i < rqn) {
+      e = rq[i];
+      unsigned )" << wl("v") << R"(;
+      DY_LOADP(rows + e.index * stride, )" << wl("v") << R"()
+      for (int k = 0; k < DY_K && !keep; ++k)
+        if (e.corr >= thr[k] && e.cp <= dy_hi[k] &&
+            dy_cpk()" << wl("v") << R"(, lat + (unsigned long long)k * DY_N * (unsigned long long)rmax, rmax) <= )"
+          << flit(D.ghi) << R"()
+          keep = true;
+    }
+    const unsigned long long m_ = __builtin_amdgcn_ballot_w64(keep);
+    if (m_) {
+      const unsigned n_ = (unsigned)__builtin_popcountll(m_);
+      if (qn + n_ > DY_QCAP) {
+        ovf = true;
+      } else {
+        if (keep) {
+          const unsigned o_ = qn + __builtin_amdgcn_mbcnt_hi((unsigned)(m_ >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m_, 0u));
+          q[o_].index = index_base + e.index; q[o_].corr = e.corr; q[o_].cp = e.cp;
+        }
+        qn += n_;
+      }
+    }
+  }
+)";
+    }
+    o << R"(  dy_flush(q, qn, lane, cand, cap, ncand, &ovf);
   if (lane == 0 && (badmask || ovf)) atomicOr(flags, (badmask ? 2 : 0) | (ovf ? 1 : 0));
 }
 

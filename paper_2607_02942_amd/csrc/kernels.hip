@@ -448,16 +448,28 @@ __device__ __forceinline__ uint32_t prefix_digit(PD P, int n, uint64_t b, int bi
 // (checked by the host); the loops unroll, every descriptor load is issued up
 // front and the f_n live in registers (predecessor bits are wave-uniform, so
 // each test is a scalar branch).  NPRE == 0: any length, f_n in an LDS column.
-template <int NPRE, bool OBJ>
+// RAD > 0: every prefix node has RAD implementations and block indices fit
+// 32 bits (checked by the host), so the digits come from successive divisions
+// by the constant RAD.
+template <int NPRE, bool OBJ, int RAD = 0>
 __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big, float* __restrict__ s_f,
                                               const float2* s_pat, const float* s_pd) {
     if constexpr (NPRE > 0) {
         const int rmax = P->rmax;
         float f[NPRE];
         float pc = OBJ ? 0.0f : 1.0f, pd = 0.0f;
+        uint32_t dg[NPRE];
+        if constexpr (RAD > 0) {
+            uint32_t x = (uint32_t)b;
+#pragma unroll
+            for (int n = NPRE - 1; n >= 0; --n) {
+                dg[n] = x % (uint32_t)RAD;
+                x /= (uint32_t)RAD;
+            }
+        }
 #pragma unroll
         for (int n = 0; n < NPRE; ++n) {
-            const uint32_t d = prefix_digit(P, n, b, big);
+            const uint32_t d = RAD > 0 ? dg[n] : prefix_digit(P, n, b, big);
             const float2 v = s_pat ? s_pat[n * rmax + d] : cs(P->at)[n * rmax + d];
             if (OBJ) {
                 pc = pc + v.x;
@@ -692,7 +704,9 @@ __device__ void general_row(PD P, JD J, uint64_t b, int big, int ix, float cx, f
 // per workgroup into scalar registers and the y loop is fully unrolled, so the
 // inner sweep issues no memory load and no wait other than its LDS bin reads.
 // B256: every source of the launch has the 256-bin table (P->jsh = 18).
-template <bool HAS_S2, int RY, int NPRE, bool B256>
+// RAD > 0: every prefix node of every source has RAD implementations and the
+// block indices fit 32 bits (constant-divisor digits).
+template <bool HAS_S2, int RY, int NPRE, bool B256, int RAD>
 __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, uint64_t unit_off) {
     extern __shared__ float s_f[];
     JD J = cs(jobs + blockIdx.y);
@@ -711,7 +725,7 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
         s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
     }
     const float2* pat = stage_prefix_rows<false>(P, (float2*)(s_f + (size_t)max(P->npre, 1) * WG), nullptr);
-    const Prefix pf = prefix_eval<NPRE, false>(P, b, J->big, s_f, pat, nullptr);
+    const Prefix pf = prefix_eval<NPRE, false, RAD>(P, b, J->big, s_f, pat, nullptr);
 
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* atx = cs(P->atx);
@@ -917,7 +931,7 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
 // only the work that reaches it shrinks.
 // ---------------------------------------------------------------------------
 constexpr int CLIMB_STEPS = 64;          // moves per (source, level) at most
-constexpr int CLIMB_ENTRIES = 1024;      // sum of the radices whose tables fit the wave's LDS (else no climb)
+constexpr int CLIMB_ENTRIES = 512;       // sum of the radices whose tables fit the wave's LDS (else no climb)
 constexpr uint32_t CLIMB_PAIRS = 16384;  // two-node moves per pass at most (else single moves only)
 constexpr int CLIMB_NODES = 8;           // problems of at most this many nodes climb (the plan sits in registers)
 
@@ -959,16 +973,28 @@ __device__ __forceinline__ void climb_eval(PD P, int N, const float (&a)[NN], co
 
 // One wave per (source, level): grid (levels, sources), 64 threads.  The
 // current plan is held by every lane in registers; each lane evaluates a
-// share of the moves, a wave reduction picks the best.
+// share of the moves, a wave reduction picks the best.  Moves only use each
+// node's Pareto-optimal implementations at the level (no other has both a
+// factor at least as high and a duration at least as short): an optimal
+// plan needs no other, since trading a dominated one for its dominator keeps
+// the plan feasible and its corr as high.
+// The block has blockDim.x = 64 W threads (W waves): few (source, level)
+// pairs take W = 16, so that each move pass is one short round (the pass is
+// latency-bound), many take W = 1.
 template <int NN>
-__global__ void __launch_bounds__(64) k_climb(const JobDev* __restrict__ jobs) {
+__global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs) {
     __shared__ float s_a[CLIMB_ENTRIES], s_t[CLIMB_ENTRIES];  // node tables, entry off[n] + i
     __shared__ uint8_t s_node[CLIMB_ENTRIES];                 // node of entry e
+    __shared__ uint8_t s_keep[CLIMB_ENTRIES];                 // entry e is Pareto-optimal at the level
+    __shared__ int16_t s_fe[CLIMB_ENTRIES];                   // the kept entries, node by node
+    __shared__ int32_t s_pn[NN * (NN - 1) / 2 + 1];           // pair p = (n1, n2): n1 * NMAX + n2
+    __shared__ int32_t s_po[NN * (NN - 1) / 2 + 1];           // first move of pair p (flat pair-move order)
+    __shared__ uint64_t s_red[16];
     JD J = cs(jobs + blockIdx.y);
     if (!J->climb) return;
     PD P = cs(J->prob);
     const int k = blockIdx.x;
-    const int N = P->n, R = P->rmax, lane = threadIdx.x;
+    const int N = P->n, R = P->rmax, lane = threadIdx.x & 63, tid = threadIdx.x, nt = blockDim.x;
     if (k >= P->k || P->obj || N > NN) return;
     const bool uni = P->uniform != 0;
     // durations the band is tested on: the unpressured ones against lo_k
@@ -976,28 +1002,60 @@ __global__ void __launch_bounds__(64) k_climb(const JobDev* __restrict__ jobs) {
     const CS float2* at = cs(P->at);
     const CS float* lt = uni ? nullptr : cs(P->lat) + (size_t)k * N * R;
     const float band = uni ? P->lo[k] : P->glo;
-    int off[NN];
+    int off[NN + 1];
     int tot = 0;
-    uint32_t sq = 0;
 #pragma unroll
     for (int n = 0; n < NN; ++n) {
         off[n] = tot;
-        if (n < N) {
-            tot += P->radix[n];
-            sq += (uint32_t)P->radix[n] * (uint32_t)P->radix[n];
-        }
+        if (n < N) tot += P->radix[n];
     }
+    off[NN] = tot;
     if (tot > CLIMB_ENTRIES) return;
-    const bool pairs_ok = ((uint32_t)tot * (uint32_t)tot - sq) / 2u <= CLIMB_PAIRS;
     for (int n = 0; n < N; ++n)
-        for (int i = lane; i < P->radix[n]; i += 64) {
+        for (int i = tid; i < P->radix[n]; i += nt) {
             const float2 v = at[n * R + i];
             s_a[off[n] + i] = v.x;
             s_t[off[n] + i] = uni ? v.y : lt[n * R + i];
             s_node[off[n] + i] = (uint8_t)n;
         }
     __syncthreads();
-    // start: every node's fastest implementation, ties to the lowest id
+    for (int e = tid; e < tot; e += nt) {
+        const int n = s_node[e];
+        int lo = 0, hi = 0;
+#pragma unroll
+        for (int m = 0; m < NN; ++m)
+            if (m == n) {
+                lo = off[m];
+                hi = off[m + 1];
+            }
+        const float a = s_a[e], t = s_t[e];
+        bool keep = true;
+        for (int q = lo; q < hi && keep; ++q) {
+            const float a2 = s_a[q], t2 = s_t[q];
+            if (q != e && a2 >= a && t2 <= t && (a2 > a || t2 < t || q < e)) keep = false;
+        }
+        s_keep[e] = keep ? 1 : 0;
+    }
+    __syncthreads();
+    // compact the kept entries per node (ballot and prefix count)
+    int foff[NN + 1];
+    int ftot = 0;
+#pragma unroll
+    for (int n = 0; n < NN; ++n) {
+        foff[n] = ftot;
+        if (n < N)
+            for (int c0 = off[n]; c0 < off[n + 1]; c0 += 64) {
+                const int e = c0 + lane;
+                const bool kp = e < off[n + 1] && s_keep[e];
+                const uint64_t m = __ballot(kp);
+                const int pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+                if (kp && tid < 64) s_fe[ftot + pos] = (int16_t)e;
+                ftot += __popcll(m);
+            }
+    }
+    foff[NN] = ftot;
+    __syncthreads();
+    // start: every node's fastest kept implementation (the fastest of all)
     int cur[NN];
     float ca[NN], ct[NN];
 #pragma unroll
@@ -1007,10 +1065,10 @@ __global__ void __launch_bounds__(64) k_climb(const JobDev* __restrict__ jobs) {
         ct[n] = 0.0f;
         if (n < N) {
             float best = INFINITY;
-            for (int i = 0; i < P->radix[n]; ++i)
-                if (s_t[off[n] + i] < best) {
-                    best = s_t[off[n] + i];
-                    cur[n] = i;
+            for (int f = foff[n]; f < foff[n + 1]; ++f)
+                if (s_t[s_fe[f]] < best) {
+                    best = s_t[s_fe[f]];
+                    cur[n] = s_fe[f] - off[n];
                 }
             ca[n] = s_a[off[n] + cur[n]];
             ct[n] = best;
@@ -1019,11 +1077,45 @@ __global__ void __launch_bounds__(64) k_climb(const JobDev* __restrict__ jobs) {
     float cc, ccp;
     climb_eval<NN>(P, N, ca, ct, -1, 0.0f, 0.0f, -1, 0.0f, 0.0f, cc, ccp);
     if (!(ccp <= band)) return;  // no plan is certainly feasible at this level
+    uint32_t pairs = 0;
+#pragma unroll
+    for (int n = 0; n < NN; ++n)
+        if (n < N) pairs += (uint32_t)(foff[n + 1] - foff[n]) * (uint32_t)(ftot - foff[n + 1]);
+    const bool pairs_ok = pairs <= CLIMB_PAIRS;
+    const int npairs = N * (N - 1) / 2;
+    if (tid == 0) {  // pairs in (n1, n2) order and where their moves start
+        int p = 0, o = 0;
+        for (int n1 = 0; n1 < N; ++n1)
+            for (int n2 = n1 + 1; n2 < N; ++n2) {
+                int F1 = 0, F2 = 0;
+#pragma unroll
+                for (int m = 0; m < NN; ++m) {
+                    if (m == n1) F1 = foff[m + 1] - foff[m];
+                    if (m == n2) F2 = foff[m + 1] - foff[m];
+                }
+                s_pn[p] = n1 * NMAX + n2;
+                s_po[p] = o;
+                o += F1 * F2;
+                ++p;
+            }
+        s_po[p] = o;
+    }
+    __syncthreads();
+    auto block_max = [&](uint64_t v) {
+        v = wave_max_u64(v);
+        if (nt == 64) return v;
+        if (lane == 0) s_red[tid >> 6] = v;
+        __syncthreads();
+        uint64_t b = 0;
+        for (int w = 0; w < (nt >> 6); ++w) b = s_red[w] > b ? s_red[w] : b;
+        __syncthreads();
+        return b;
+    };
     for (int step = 0; step < CLIMB_STEPS; ++step) {
-        // single moves over the flat entry index; key = (corr bits, reversed move order), 0 = none
+        // single moves over the kept entries; key = (corr bits, reversed move order), 0 = none
         uint64_t best = 0;
-        for (int e = lane; e < tot; e += 64) {
-            const int n = s_node[e];
+        for (int f = tid; f < ftot; f += nt) {
+            const int e = s_fe[f], n = s_node[e];
             int cn = 0, on = 0;
 #pragma unroll
             for (int m = 0; m < NN; ++m)
@@ -1039,48 +1131,48 @@ __global__ void __launch_bounds__(64) k_climb(const JobDev* __restrict__ jobs) {
                 best = key > best ? key : best;
             }
         }
-        uint64_t mv = wave_max_u64(best);
+        uint64_t mv = block_max(best);
         bool pair = false;
         if (mv == 0 && pairs_ok) {
-            // two-node moves (n1 < n2, ids i1 and i2), move order (n1, n2, i1, i2)
-            for (int n1 = 0; n1 < N; ++n1) {
-                int c1 = 0, o1 = 0;
+            // two-node moves (n1 < n2, kept entries e1 and e2) in one flat order
+            // (n1, n2, e1, e2); t -> pair p (its moves start at s_po[p]) -> (j1, j2)
+            const int total = s_po[npairs];
+            int p = 0;
+            for (int t = tid; t < total; t += nt) {
+                while (s_po[p + 1] <= t) ++p;
+                const int n1 = s_pn[p] / NMAX, n2 = s_pn[p] % NMAX;
+                int c1 = 0, o1 = 0, f1 = 0, c2 = 0, o2 = 0, f2 = 0, F2 = 1;
 #pragma unroll
-                for (int m = 0; m < NN; ++m)
+                for (int m = 0; m < NN; ++m) {
                     if (m == n1) {
                         c1 = cur[m];
                         o1 = off[m];
+                        f1 = foff[m];
                     }
-                for (int n2 = n1 + 1; n2 < N; ++n2) {
-                    int c2 = 0, o2 = 0;
-#pragma unroll
-                    for (int m = 0; m < NN; ++m)
-                        if (m == n2) {
-                            c2 = cur[m];
-                            o2 = off[m];
-                        }
-                    const int r1 = P->radix[n1], r2 = P->radix[n2];
-                    const float inv = 1.0f / (float)r2;
-                    const float cab = s_a[o1 + c1] * s_a[o2 + c2];
-                    for (int t = lane; t < r1 * r2; t += 64) {
-                        // t = i1 r2 + i2; the float quotient is exact: (t + 0.5) / r2 stays
-                        // at least 0.5 / r2 >= 2^-9 away from an integer, far above its error
-                        const int i1 = (int)(((float)t + 0.5f) * inv);
-                        const int i2 = t - i1 * r2;
-                        if (i1 == c1 || i2 == c2) continue;
-                        const int e1 = o1 + i1, e2 = o2 + i2;
-                        if (!(s_a[e1] * s_a[e2] > cab)) continue;  // cannot raise corr
-                        float c, cp;
-                        climb_eval<NN>(P, N, ca, ct, n1, s_a[e1], s_t[e1], n2, s_a[e2], s_t[e2], c, cp);
-                        if (c > cc && cp <= band) {
-                            const uint32_t id = (uint32_t)(n1 * NMAX + n2) << 16 | (uint32_t)i1 << 8 | (uint32_t)i2;
-                            const uint64_t key = (uint64_t)__float_as_uint(c) << 32 | (uint32_t)(0xffffffffu - id);
-                            best = key > best ? key : best;
-                        }
+                    if (m == n2) {
+                        c2 = cur[m];
+                        o2 = off[m];
+                        f2 = foff[m];
+                        F2 = foff[m + 1] - foff[m];
                     }
                 }
+                // t - s_po[p] = j1 F2 + j2; the float quotient is exact: (x + 0.5) / F2
+                // stays at least 0.5 / F2 >= 2^-10 away from an integer, far above its error
+                const int x = t - s_po[p];
+                const int j1 = (int)(((float)x + 0.5f) / (float)F2);
+                const int j2 = x - j1 * F2;
+                const int e1 = s_fe[f1 + j1], e2 = s_fe[f2 + j2];
+                if (e1 - o1 == c1 || e2 - o2 == c2) continue;
+                if (!(s_a[e1] * s_a[e2] > s_a[o1 + c1] * s_a[o2 + c2])) continue;  // cannot raise corr
+                float c, cp;
+                climb_eval<NN>(P, N, ca, ct, n1, s_a[e1], s_t[e1], n2, s_a[e2], s_t[e2], c, cp);
+                if (c > cc && cp <= band) {
+                    const uint32_t id = (uint32_t)(n1 * NMAX + n2) << 16 | (uint32_t)(e1 - o1) << 8 | (uint32_t)(e2 - o2);
+                    const uint64_t key = (uint64_t)__float_as_uint(c) << 32 | (uint32_t)(0xffffffffu - id);
+                    best = key > best ? key : best;
+                }
             }
-            mv = wave_max_u64(best);
+            mv = block_max(best);
             pair = true;
         }
         if (mv == 0) break;
@@ -1110,7 +1202,7 @@ __global__ void __launch_bounds__(64) k_climb(const JobDev* __restrict__ jobs) {
             }
         }
     }
-    if (lane == 0) atomicMax(J->scert + k * NSLOT, __float_as_uint(cc) + 1u);
+    if (tid == 0) atomicMax(J->scert + k * NSLOT, __float_as_uint(cc) + 1u);
 }
 
 // ---------------------------------------------------------------------------
@@ -2292,7 +2384,9 @@ hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s) {
 // Problems above CLIMB_NODES nodes take no climb (the kernel returns for them).
 hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s) {
     if (njobs == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_climb<CLIMB_NODES>, dim3(kmax, njobs), dim3(64), 0, s, d_jobs);
+    // few (source, level) pairs: 16 waves each (latency); many: one wave each
+    const int threads = (size_t)njobs * (size_t)kmax <= 1024 ? 1024 : 64;
+    hipLaunchKernelGGL(k_climb<CLIMB_NODES>, dim3(kmax, njobs), dim3(threads), 0, s, d_jobs);
     return hipGetLastError();
 }
 
@@ -2337,7 +2431,7 @@ hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool ob
 }
 
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
-                        int npre_c, int ry, bool b256, hipStream_t s) {
+                        int npre_c, int ry, bool b256, bool rad12, hipStream_t s) {
     if (n == 0) return hipSuccess;
     const size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float) +
                        (size_t)PAT_MAX * (sizeof(float2) + (obj ? sizeof(float) : 0));
@@ -2350,10 +2444,13 @@ hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint
     do {                                                                                                   \
         if (obj)                                                                                           \
             hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off);          \
+        else if (b256 && rad12 && RYV == 12 && NP > 0)                                                     \
+            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, true, (RYV == 12 && NP > 0) ? 12 : 0>), grid, dim3(WG), lds, \
+                               s, d_jobs, off);                                                            \
         else if (b256)                                                                                     \
-            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, true>), grid, dim3(WG), lds, s, d_jobs, off);        \
+            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, true, 0>), grid, dim3(WG), lds, s, d_jobs, off);     \
         else                                                                                               \
-            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, false>), grid, dim3(WG), lds, s, d_jobs, off);       \
+            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, false, 0>), grid, dim3(WG), lds, s, d_jobs, off);    \
     } while (0)
 #define DYP_SWEEP_NP(S2, RYV)            \
     switch (npre_c) {                    \

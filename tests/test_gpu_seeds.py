@@ -1,6 +1,6 @@
 """GPU: seeds and the state a selection call leaves behind.
 
-- Local-search seeds (DY_OPT_CLIMB) change only the work: on sources that
+- Local-search seeds (DY_OPT_CLIMB 2: every eligible source) change only the work: on sources that
   cover a whole plan space the choices equal the oracle's with and without
   them, and the candidate lists never grow (a seed only raises thresholds).
 - Consecutive calls on different streams, with rows rewritten in place at the
@@ -35,7 +35,7 @@ def _gpu():
 
 
 def select_with(plan, sources, climb):
-    plan.set_option(D.DY_OPT_CLIMB, 1 if climb else 0)
+    plan.set_option(D.DY_OPT_CLIMB, 2 if climb else 0)
     got = plan.select(sources, stream=stream())
     return got, plan.stats().candidates
 
