@@ -453,7 +453,10 @@ def test_score_rows_and_indices_on_workload_subsets():
 
 # ---------------------------------------------------------------------------
 # The two-pass lower median that sets the stored SLOs (R-7: 1.5 x the lower
-# median of the unpressured critical path over the scored plan set)
+# median of the unpressured critical path over the scored plan set).  The
+# stored SLOs use 24 histogram bits; the algorithm does not depend on the bit
+# count, and the tests take 6 to 20 bits (a 2^24-entry histogram is slow to
+# scan here)
 # ---------------------------------------------------------------------------
 
 def _sorted_lower_median(vals):
@@ -465,7 +468,7 @@ def test_two_pass_median_chain4_full_space():
     from paper_2607_02942_amd import workload as wl
     prob = wl.chain4(slo=0.0)
     total = prob.n_plans()
-    got = golden.lower_median_cp0(prob, "range", total, golden.SerialPool(), 5000)
+    got = golden.lower_median_cp0(prob, "range", total, golden.SerialPool(), 8000, bits=16)
     # a chain's unpressured CP is its durations summed in node order
     idx = np.arange(total)
     dig = np.stack(np.unravel_index(idx, tuple(int(r) for r in prob.radix)), axis=1)
@@ -476,7 +479,7 @@ def test_two_pass_median_chain4_full_space():
     assert got == _sorted_lower_median(cp)
     assert total % 2 == 0
     # an odd count: the first total - 1 plans
-    assert golden.lower_median_cp0(prob, "range", total - 1, golden.SerialPool(), 4096) == \
+    assert golden.lower_median_cp0(prob, "range", total - 1, golden.SerialPool(), total, bits=16) == \
         _sorted_lower_median(cp[: total - 1])
 
 
@@ -485,7 +488,7 @@ def test_two_pass_median_forkjoin8_prefix():
     from paper_2607_02942_amd import workload as wl
     prob = wl.forkjoin8(slo=0.0)
     total = 1 << 22
-    got = golden.lower_median_cp0(prob, "range", total, golden.SerialPool(), 1 << 20)
+    got = golden.lower_median_cp0(prob, "range", total, golden.SerialPool(), 1 << 20, bits=20)
     assert got == _sorted_lower_median(orc.cp0_values(prob, 0, total))
 
 
@@ -494,12 +497,12 @@ def test_two_pass_median_stream24_rows(count):
     from oracle import golden
     from paper_2607_02942_amd import workload as wl
     prob = wl.stream24(slo=0.0)
-    got = golden.lower_median_cp0(prob, "rows", count, golden.SerialPool(), 1 << 18)
+    got = golden.lower_median_cp0(prob, "rows", count, golden.SerialPool(), 1 << 19, bits=20)
     rows = wl.make_rows(count, prob.n_nodes, int(prob.radix[0]), threads=1)
     assert got == _sorted_lower_median(orc.cp0_values(prob, rows=rows))
 
 
-@pytest.mark.parametrize("bits", [6, 24])
+@pytest.mark.parametrize("bits", [6, 16])
 def test_two_pass_median_heavy_ties(bits):
     # integer durations: the CP takes few distinct values, so the median's
     # bucket holds many equal values (with 6 bits also many distinct ones)
