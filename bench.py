@@ -98,9 +98,7 @@ def match_kernel(names, base):
 
 def score_kernel(prob, per_class):
     """The kernel dy_plan_score runs for a 2^26-plan range of `prob`."""
-    if per_class:
-        return "k_score"
-    return "dy_score_range" if prob.n_nodes > 16 else "k_score_fast"
+    return "k_score" if per_class else "k_score_row"
 
 
 def kernel_source_sha():
@@ -265,8 +263,8 @@ def pmc_summary(dbs, kernel, title, commands, trace_db=None):
             out.append(f"- VALU issue: {g('SQ_INSTS_VALU') / (cyc * N_CU):.3f} wave-instructions per CU per cycle "
                        "(limit 1: four SIMDs, each one 64-lane instruction per 4 cycles)")
         if g("SQ_WAVE_CYCLES") is not None:
-            out.append(f"- mean resident waves per CU: {g('SQ_WAVE_CYCLES') / (cyc * N_CU):.2f} of at most 32 "
-                       "(SQ_WAVE_CYCLES / (duration x clock x CUs))")
+            out.append(f"- mean resident waves per CU: {4 * g('SQ_WAVE_CYCLES') / (cyc * N_CU):.2f} of at most 32 "
+                       "(SQ_WAVE_CYCLES counts quad-cycles: 4 SQ_WAVE_CYCLES / (duration x clock x CUs))")
         if g("SQ_ACTIVE_INST_LDS") is not None:
             out.append(f"- LDS issue: {g('SQ_ACTIVE_INST_LDS') / (cyc * N_CU):.3f} per CU per cycle")
     if g("SQ_LDS_BANK_CONFLICT") is not None and g("SQ_ACTIVE_INST_LDS"):

@@ -35,7 +35,6 @@ struct JitRows {
     hipFunction_t scan = nullptr;
     hipFunction_t scan_u = nullptr;
     hipFunction_t sample = nullptr;
-    hipFunction_t score = nullptr;
     hipFunction_t score_rows = nullptr;
     hipFunction_t sweep = nullptr;
     hipFunction_t seed = nullptr;
@@ -43,7 +42,7 @@ struct JitRows {
 bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err);
 std::string jit_rows_source(const ProbDev& D);
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
-                        int n_nodes, int n_entries, bool simple, bool obj, hipStream_t s);
+                        int n_nodes, int n_entries, int ry, bool simple, bool obj, hipStream_t s);
 }  // namespace dyp
 
 using namespace dyp;
@@ -1314,12 +1313,12 @@ void launch_certify_all(const JobDev* d, int ntot, int cert_waves, const dy_plan
         chk(launch_certify(d + c, std::min(65535, ntot - c), cert_waves, h->kmax, h->nmax, h->nrmax, s), "certify");
 }
 
-// Per-plan scores through problem p's generated kernels: a RANGE source of
-// 32-bit indices or rows (about eight plans per thread, grid-stride).
+// Per-plan scores of a ROWS source through problem p's generated kernel
+// (about eight rows per thread, grid-stride).
 hipError_t launch_jit_score(const dy_plan* h, int p, const dy_source& src, float* corr, float* cp, float* dem,
                             uint32_t* feas, hipStream_t s) {
     const ProbDev& D = h->hdesc[p];
-    unsigned long long begin = src.begin, count = src.count, stride = src.row_stride;
+    unsigned long long count = src.count, stride = src.row_stride;
     const unsigned char* rows = src.rows;
     int aligned = ((src.row_stride | (uint64_t)(uintptr_t)src.rows | (uint64_t)D.n) & 3u) == 0 ? 1 : 0;
     const float2* at = D.at;
@@ -1329,12 +1328,8 @@ hipError_t launch_jit_score(const dy_plan* h, int p, const dy_source& src, float
     int vec = (cp && (D.k & 3) == 0 && ((uintptr_t)cp & 15) == 0) ? 1 : 0;
     const unsigned long long want = (count + 256ull * 8 - 1) / (256ull * 8);
     const unsigned gx = (unsigned)std::max<unsigned long long>(1, std::min<unsigned long long>(want, 1ull << 30));
-    if (src.kind == DY_SOURCE_ROWS) {
-        void* args[] = {&rows, &stride, &count, &aligned, &at, &dm, &rmax, &lat64, &corr, &cp, &dem, &feas, &vec};
-        return hipModuleLaunchKernel(h->jit[p].score_rows, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
-    }
-    void* args[] = {&begin, &count, &at, &dm, &rmax, &lat64, &corr, &cp, &dem, &feas, &vec};
-    return hipModuleLaunchKernel(h->jit[p].score, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
+    void* args[] = {&rows, &stride, &count, &aligned, &at, &dm, &rmax, &lat64, &corr, &cp, &dem, &feas, &vec};
+    return hipModuleLaunchKernel(h->jit[p].score_rows, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
 }
 
 // Generated rows kernels for problem p: compiled at first use.
@@ -1725,17 +1720,14 @@ int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, floa
     const ProbDev& D = h->hdesc[src->problem];
     const bool simple = D.uniform != 0 || D.obj != 0;
     hipError_t e;
-    // RANGE sources of 32-bit indices, DAGs of more than 16 nodes: the problem's
-    // generated kernel when it compiles (3.5x the generic kernel at 24 nodes);
-    // up to 16 nodes the unrolled built-in kernels measured as fast or faster
-    // (layered10: 1.27 vs 1.53 ms per 2^26 plans)
-    if (src->kind == DY_SOURCE_RANGE && !J.big && simple && H.n > 16 && jit_ready(h, src->problem) &&
-        h->jit[src->problem].score)
-        e = launch_jit_score(h, src->problem, *src, corr, cp, demand, feas_bits, (hipStream_t)stream);
-    else if (src->kind == DY_SOURCE_ROWS && simple && jit_ready(h, src->problem) && h->jit[src->problem].score_rows)
+    // RANGE sources of 32-bit indices (uniform pressure or the objective) take
+    // the library's row kernel (the prefix once per row of y's plans); rows,
+    // the problem's generated kernel when it compiles; everything else the
+    // generic per-plan kernel
+    if (src->kind == DY_SOURCE_ROWS && simple && jit_ready(h, src->problem) && h->jit[src->problem].score_rows)
         e = launch_jit_score(h, src->problem, *src, corr, cp, demand, feas_bits, (hipStream_t)stream);
     else
-        e = launch_score(J, src->count, corr, cp, demand, feas_bits, H.n, H.n * H.rmax, simple, D.obj != 0,
+        e = launch_score(J, src->count, corr, cp, demand, feas_bits, H.n, H.n * H.rmax, H.ry, simple, D.obj != 0,
                          (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(&h->err, e, "score launch");
     return DY_OK;

@@ -1,7 +1,7 @@
 // DAG-specialised kernels for candidate rows (streamed plans), generated as
 // HIP source from one problem's structure and compiled at first use with
 // hiprtc for the running device; the same module holds a per-plan score
-// kernel for RANGE sources (gen_score).
+// kernel for rows (gen_score).
 //
 // A row is N bytes, byte n = implementation id of node n.  Every node's table
 // (factor a = 1 - w(1 - p) and duration tau, fp32) sits in LDS as 64 float2
@@ -50,7 +50,6 @@ struct JitRows {
     hipFunction_t scan = nullptr;     // rows whose words are dword aligned
     hipFunction_t scan_u = nullptr;   // any other stride / alignment (byte loads)
     hipFunction_t sample = nullptr;
-    hipFunction_t score = nullptr;    // per-plan scores of a RANGE source of 32-bit indices
     hipFunction_t score_rows = nullptr;  // per-plan scores of rows
     hipFunction_t sweep = nullptr;    // the sweep of RANGE sources (32-bit blocks)
     hipFunction_t seed = nullptr;     // its seeding pass (uniform pressure, corr mode)
@@ -172,29 +171,20 @@ void emit_obj_sums(std::ostringstream& o, const ProbDev& D, int n0, int n1) {
         if (D.llm >> n & 1u) o << "  u_ = u_ + e" << n << ".x; d_ = d_ + e" << n << ".y; \\\n";
 }
 
-// Per-plan scores (the values of the library's score kernels, same fp32
-// operations in the same order) with the DAG's recurrence unrolled and the
-// level constants as literals, for a RANGE source whose plan indices fit 32
-// bits (digits by constant division; dy_score_range) or for rows
-// (dy_score_rows: a row with an id >= R_n gets NaN scores and no feasible
-// level, as in the generic kernel).  corr / SLO mode: a plan whose fp32 CP
-// falls in a level's band (lo_k, hi_k] takes that level's fp64 recurrence
-// here, from the fp64 duration table, against the SLO.
-void gen_score(std::ostringstream& o, const ProbDev& D, bool rows) {
+// Per-plan scores of rows (the values of the library's score kernels, same
+// fp32 operations in the same order) with the DAG's recurrence unrolled and
+// the level constants as literals (dy_score_rows: a row with an id >= R_n gets
+// NaN scores and no feasible level, as in the generic kernel).  corr / SLO
+// mode: a plan whose fp32 CP falls in a level's band (lo_k, hi_k] takes that
+// level's fp64 recurrence here, from the fp64 duration table, against the SLO.
+void gen_score(std::ostringstream& o, const ProbDev& D) {
     const int N = D.n, K = D.k, Q = (N + 3) / 4;
-    if (rows)
-        o << R"(
+    o << R"(
 extern "C" __global__ void __launch_bounds__(256) dy_score_rows(
     const unsigned char* __restrict__ rows, unsigned long long stride, unsigned long long count, int aligned,
     const float2* __restrict__ at, const float* __restrict__ dm, int rmax, const double* __restrict__ lat64,
     float* __restrict__ corr, float* __restrict__ cpo, float* __restrict__ demo, unsigned* __restrict__ feas,
     int vec) {)";
-    else
-        o << R"(
-extern "C" __global__ void __launch_bounds__(256) dy_score_range(
-    unsigned long long begin, unsigned long long count, const float2* __restrict__ at,
-    const float* __restrict__ dm, int rmax, const double* __restrict__ lat64, float* __restrict__ corr,
-    float* __restrict__ cpo, float* __restrict__ demo, unsigned* __restrict__ feas, int vec) {)";
     o << R"(
   __shared__ float2 s_tab[DY_TAB];
   __shared__ float s_dm[DY_TAB];
@@ -206,26 +196,17 @@ extern "C" __global__ void __launch_bounds__(256) dy_score_range(
   const unsigned long long gstride = (unsigned long long)gridDim.x * 256ull;
   for (unsigned long long t = (unsigned long long)blockIdx.x * 256ull + threadIdx.x; t < count; t += gstride) {
 )";
-    if (rows) {
-        o << "    unsigned ";
-        for (int q = 0; q < Q; ++q) o << (q ? ", " : "") << "w" << q;
-        o << ";\n    DY_LOAD(t";
-        for (int q = 0; q < Q; ++q) o << ", w" << q;
-        o << ")\n    unsigned bk_ = 0u;\n";
-        for (int q = 0; q < Q; ++q) o << "    bk_ |= (w" << q << " + DY_K_" << q << ") | w" << q << ";\n";
-        o << "    const bool bad = (bk_ & 0x80808080u) != 0u;\n";
-        for (int n = 0; n < N; ++n) {
-            o << "    const unsigned d" << n << " = ";
-            if (n % 4) o << "(w" << n / 4 << " >> " << 8 * (n % 4) << ") & 255u;\n";
-            else o << "w" << n / 4 << " & 255u;\n";
-        }
-    } else {
-        o << "    const bool bad = false;\n    unsigned x = (unsigned)(begin + t);\n";
-        for (int n = N - 1; n >= 0; --n) {
-            o << "    const unsigned d" << n << " = x % " << D.radix[n] << "u;";
-            if (n > 0) o << " x /= " << D.radix[n] << "u;";
-            o << "\n";
-        }
+    o << "    unsigned ";
+    for (int q = 0; q < Q; ++q) o << (q ? ", " : "") << "w" << q;
+    o << ";\n    DY_LOAD(t";
+    for (int q = 0; q < Q; ++q) o << ", w" << q;
+    o << ")\n    unsigned bk_ = 0u;\n";
+    for (int q = 0; q < Q; ++q) o << "    bk_ |= (w" << q << " + DY_K_" << q << ") | w" << q << ";\n";
+    o << "    const bool bad = (bk_ & 0x80808080u) != 0u;\n";
+    for (int n = 0; n < N; ++n) {
+        o << "    const unsigned d" << n << " = ";
+        if (n % 4) o << "(w" << n / 4 << " >> " << 8 * (n % 4) << ") & 255u;\n";
+        else o << "w" << n / 4 << " & 255u;\n";
     }
     // ids below 256: the tables' spare entries keep every read in the arrays
     for (int n = 0; n < N; ++n) o << "    const float2 e" << n << " = s_tab[" << n * 64 << " + d" << n << "];\n";
@@ -963,8 +944,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_rows_scan_u(DY_SCAN_ARGS) {
 }
 )";
     if (D.uniform || D.obj) {
-        gen_score(o, D, false);
-        gen_score(o, D, true);
+        gen_score(o, D);
     }
     if (D.npre >= 1 && D.xnode >= 0) gen_sweep(o, D);
     if (D.uniform && !D.obj && D.npre >= 1 && D.xnode >= 0) gen_sweep_seed(o, D);
@@ -1021,8 +1001,7 @@ bool jit_rows_get(int device, const ProbDev& D, JitRows* out, std::string* err) 
         hipModuleGetFunction(&j.scan, j.mod, "dy_rows_scan_a") != hipSuccess ||
         hipModuleGetFunction(&j.scan_u, j.mod, "dy_rows_scan_u") != hipSuccess ||
         hipModuleGetFunction(&j.sample, j.mod, "dy_rows_sample") != hipSuccess ||
-        ((D.uniform || D.obj) && (hipModuleGetFunction(&j.score, j.mod, "dy_score_range") != hipSuccess ||
-                                  hipModuleGetFunction(&j.score_rows, j.mod, "dy_score_rows") != hipSuccess)) ||
+        ((D.uniform || D.obj) && hipModuleGetFunction(&j.score_rows, j.mod, "dy_score_rows") != hipSuccess) ||
         (D.npre >= 1 && D.xnode >= 0 && hipModuleGetFunction(&j.sweep, j.mod, "dy_sweep") != hipSuccess) ||
         (D.uniform && !D.obj && D.npre >= 1 && D.xnode >= 0 &&
          hipModuleGetFunction(&j.seed, j.mod, "dy_sweep_seed") != hipSuccess)) {

@@ -2058,6 +2058,9 @@ constexpr int SCORE_TAB_N = 12;
 // column of n floats (the fp32 recurrence), n id bytes per thread, and the
 // staged tables.
 constexpr uint64_t SCORE_PPT = 8;  // plans per thread of k_score (the tables are staged once per block)
+constexpr int SCORE_ROW_TAB = 2048;      // table entries (N x R_max) of k_score_row, staged in LDS
+constexpr size_t SCORE_ROW_LDS = 56 << 10;  // its dynamic LDS at most (64 KiB with the static arrays)
+constexpr uint64_t SCORE_ROWS_PT = 2;    // rows per thread of k_score_row
 
 static size_t score_lds(int n, int nr) {
     size_t b = (size_t)n * WG * sizeof(float) + (size_t)n * WG;
@@ -2223,111 +2226,200 @@ __global__ void __launch_bounds__(WG) k_score(const JobDev job, uint64_t unit_of
     }
 }
 
-// k_score for RANGE sources whose plan indices fit 32 bits, DAGs of at most
-// NU nodes, uniform pressure (OBJ = false) or the objective (OBJ = true): the
-// same values as k_score with the per-plan loops unrolled.  The digit decode's
-// divisors and the predecessor masks sit in scalar registers, the ids and the
-// f_n in vector registers (predecessor tests are scalar branches), and a plan
-// writes its ids to LDS only when its wave has a CP inside a level's band
-// (resolve_bands reads them there).  No row can be bad, so outputs need no
-// NaN fill.
-template <int NN, bool OBJ>
-__global__ void __launch_bounds__(WG) k_score_fast(const JobDev job, uint64_t unit_off, uint64_t unit_end,
-                                                   float* corr, float* cpo, float* dem, uint32_t* feas) {
+// Per-plan scores of a RANGE source of 32-bit plan indices (uniform pressure
+// or the objective) by rows: a row fixes nodes 0..N-2 and its plans are node
+// y = N-1's implementations.  Phase 1: each lane takes one row and forms its
+// digits, prefix product (objective: sums), demand sum and the longest paths
+// into y and into the other sinks, once for the row.  Phase 2: the wave
+// scores the plans of its 64 rows, which are one contiguous span of plan
+// indices, 64 consecutive plans at a time; each plan adds y's terms to its
+// row's, in the same operations and order as the per-plan kernels.  Lane =
+// plan for the per-plan outputs; the K per-level values of the 64 plans are
+// stored lane-contiguously instead (each plan's scalars pass through LDS), so
+// every store instruction covers one contiguous span.  A plan's feasibility bits come from two
+// tables per bin of its CP's fp32 pattern (the prefilter's bins): the levels
+// every CP of the bin certainly meets, and those some CP of the bin may meet
+// without certainty; only the latter are compared with the bands, and a CP
+// inside a band (lo_k, hi_k] is decided in fp64 by the wave.
+// Dynamic LDS: the recurrence column [N][WG] floats, the ids [N][WG], then the
+// (a, tau) and demand tables (N * R_max entries).
+template <bool OBJ>
+__global__ void __launch_bounds__(WG) k_score_row(const JobDev job, uint64_t row_off, uint64_t row_end, float* corr,
+                                                  float* cpo, float* dem, uint32_t* feas) {
     extern __shared__ float s_dyn[];
+    __shared__ uint32_t s_cert[NBINS2], s_chk[NBINS2];
+    __shared__ float4 s_pre[WG];  // per row: (prefix product or sum, demand sum, path into y, other sinks)
+    __shared__ float2 s_v[WG];    // per plan of a step: (cp0, or G in objective mode; demand)
+    __shared__ __align__(16) float s_mk[KMAX];  // per level: 1/(1 - rho_k), or lambda_ld L_k
+    // the band edges per level: a lane's level index is not uniform, so they
+    // are read from LDS (a global load's wait would also wait for the wave's
+    // earlier stores)
+    __shared__ float s_lo[KMAX], s_hi[KMAX];
     JD J = cs(&job);
     PD P = cs(J->prob);
-    constexpr int N = NN;  // the DAG's node count (checked by the host)
-    const int R = P->rmax, K = P->k, tid = threadIdx.x;
-    // LDS: the (a, tau) and demand tables (at most SCORE_TAB entries), then the
-    // ids [N][WG] for the band check
-    const int NR = N * R;
-    float2* at = (float2*)s_dyn;
-    float* dm = (float*)(at + NR);
-    uint8_t* s_id = (uint8_t*)(dm + NR);
-    const uint64_t first = unit_off + (uint64_t)blockIdx.x * WG, stride = (uint64_t)gridDim.x * WG;
-    if (first >= unit_end) return;
-    for (int i = tid; i < NR; i += WG) {
-        at[i] = P->at[i];
-        dm[i] = P->dem[i];
+    const int N = P->n, R = P->rmax, K = P->k, tid = threadIdx.x, lane = tid & 63, wbase = tid & ~63;
+    const int y = N - 1, ry = P->radix[y];
+    float* s_f = s_dyn;                                    // [N][WG]
+    uint8_t* s_id = (uint8_t*)(s_dyn + (size_t)N * WG);    // [N][WG]
+    const size_t head = (((size_t)N * WG * sizeof(float) + (size_t)N * WG) + 15) & ~(size_t)15;
+    float2* s_at = (float2*)((char*)s_dyn + head);
+    float* s_dm = (float*)(s_at + N * R);
+    const uint64_t first = row_off + (uint64_t)blockIdx.x * WG, stride = (uint64_t)gridDim.x * WG;
+    if (first >= row_end) return;
+    for (int i = tid; i < N * R; i += WG) {
+        s_at[i] = P->at[i];
+        s_dm[i] = P->dem[i];
     }
-    __syncthreads();
-    const uint32_t sinks = P->sinks;
+    if (tid < K) {
+        s_mk[tid] = OBJ ? P->m32[tid] : P->mk[tid];
+        s_lo[tid] = P->lo[tid];
+        s_hi[tid] = P->hi[tid];
+    }
+    // bins: 256 on shift 18 when they cover the CP range (P->jsh), else 64 on the problem's shift
+    const bool b256 = P->jsh != 0;
+    const uint32_t sh = b256 ? 18u : (uint32_t)P->bin_shift, nb = b256 ? (uint32_t)NBINS2 : (uint32_t)NBINS;
+    if (!OBJ && (uint32_t)tid < nb) {
+        const uint32_t blo = P->cp_lo_bits >> sh;
+        const uint32_t B = blo + (((uint32_t)tid - blo) & (nb - 1u));
+        uint64_t lowb = (uint64_t)B << sh, highb = (((uint64_t)B + 1) << sh) - 1;
+        if (lowb < P->cp_lo_bits) lowb = P->cp_lo_bits;
+        if (highb > 0x7f7fffffull) highb = 0x7f7fffffull;
+        const float low = __uint_as_float((uint32_t)lowb), high = __uint_as_float((uint32_t)highb);
+        uint32_t cert = 0, chk = 0;
+        for (int k = 0; k < K && k < 32; ++k) {
+            if (high <= P->lo[k])
+                cert |= 1u << k;
+            else if (low <= P->hi[k])
+                chk |= 1u << k;
+        }
+        s_cert[tid] = cert;
+        s_chk[tid] = chk;
+    }
+    const uint64_t row0 = J->begin / (uint64_t)ry, p_end = J->begin + J->count;
     const bool vec = cpo && (K & 3) == 0 && ((uintptr_t)cpo & 15) == 0;
-    for (uint64_t base = first; base < unit_end; base += stride) {
-        const uint64_t t = base + tid;
-        const bool live = t < unit_end;
-        uint32_t x = (uint32_t)(J->begin + (live ? t : unit_end - 1));
-        uint32_t id[N];
-#pragma unroll
-        for (int n = N - 1; n >= 0; --n) {
+    const uint32_t allk = K >= 32 ? 0xffffffffu : ((1u << K) - 1u);
+    const uint32_t py = P->pred[y];
+    const uint32_t kinv = (1u << 20) / (uint32_t)K + 1u;  // (f * kinv) >> 20 = f / K for f < 64 K, K <= 32
+    for (uint64_t base = first; base < row_end; base += stride) {
+        __syncthreads();  // tables staged; the previous batch's rows consumed
+        // phase 1: lane = row
+        const uint64_t rt = base + tid;
+        const uint64_t row = row0 + (rt < row_end ? rt : row_end - 1);
+        uint32_t x = (uint32_t)row;
+        for (int n = y - 1; n >= 0; --n) {
             const uint32_t q = mdiv(x, P->rmag[n]);
-            id[n] = x - q * (uint32_t)P->radix[n];
+            s_id[n * WG + tid] = (uint8_t)(x - q * (uint32_t)P->radix[n]);
             x = q;
         }
-        float cc = OBJ ? 0.0f : 1.0f, cp0 = 0.0f, d = 0.0f;
-        float f[N];
-#pragma unroll
-        for (int n = 0; n < N; ++n) {
-            const int e = n * R + (int)id[n];
-            const float2 v = at[e];
-            cc = OBJ ? cc + v.x : cc * v.x;
-            d = d + dm[e];
+        float cx = OBJ ? 0.0f : 1.0f, dx = 0.0f, M = 0.0f, S2 = 0.0f;
+        for (int n = 0; n < y; ++n) {
+            const int e = n * R + (int)s_id[n * WG + tid];
+            const float2 v = s_at[e];
+            cx = OBJ ? cx + v.x : cx * v.x;
+            dx = dx + s_dm[e];
             float m = 0.0f;
-            const uint32_t pm = P->pred[n];
-#pragma unroll
-            for (int u = 0; u < n; ++u)
-                if (pm >> u & 1u) m = fmaxf(m, f[u]);
-            f[n] = v.y + m;
-            if (sinks >> n & 1u) cp0 = fmaxf(cp0, f[n]);
+            uint32_t pm = P->pred[n];
+            while (pm) {
+                const int u = __builtin_ctz(pm);
+                pm &= pm - 1;
+                m = fmaxf(m, s_f[u * WG + tid]);
+            }
+            const float f = v.y + m;
+            s_f[n * WG + tid] = f;
+            if (py >> n & 1u) M = fmaxf(M, f);
+            if (P->sinks >> n & 1u) S2 = fmaxf(S2, f);
         }
-        float* row = cpo ? cpo + t * (uint64_t)K : nullptr;
-        if (OBJ) {  // corr = U, cp[k] = the fp32 estimate of J_k, demand = D, every level admissible
-            const float G = fmaf(-P->lam_l, cp0, cc);
-            if (live && row) {
-                if (vec) {
-                    for (int k = 0; k < K; k += 4)
-                        *(float4*)(row + k) = make_float4(fmaf(-P->m32[k], d, G), fmaf(-P->m32[k + 1], d, G),
-                                                          fmaf(-P->m32[k + 2], d, G), fmaf(-P->m32[k + 3], d, G));
-                } else {
-                    for (int k = 0; k < K; ++k) row[k] = fmaf(-P->m32[k], d, G);
+        s_pre[tid] = make_float4(cx, dx, M, S2);
+        __syncthreads();
+        // phase 2: the wave's rows are rows r0 .. r0 + 63 (those below row_end),
+        // plans r0 ry .. (r0 + 64) ry - 1; 64 consecutive plans per step
+        const uint64_t wrow = base + (uint64_t)wbase;  // the wave's first row (relative to row0)
+        if (wrow >= row_end) continue;
+        const uint32_t nrows = (uint32_t)min((uint64_t)64, row_end - wrow);
+        const uint64_t pw = (row0 + wrow) * (uint64_t)ry;
+        for (uint32_t q0 = 0; q0 < nrows * (uint32_t)ry; q0 += 64) {
+            const uint32_t q = q0 + (uint32_t)lane;
+            const uint32_t lr = mdiv(q, P->rmag[y]);  // local row
+            const int j = (int)(q - lr * (uint32_t)ry);
+            const uint64_t p = pw + q;
+            const bool live = lr < nrows && p >= J->begin && p < p_end;
+            const float4 pr = s_pre[wbase + (int)min(lr, nrows - 1)];
+            const int e = y * R + j;
+            const float2 v = s_at[e];
+            const float cc = OBJ ? pr.x + v.x : pr.x * v.x;
+            const float d = pr.y + s_dm[e];
+            const float cp0 = fmaxf(v.y + pr.z, pr.w);
+            const uint64_t o = p - J->begin;
+            float G = 0.0f;
+            uint32_t bits = allk;
+            if (OBJ) {
+                G = fmaf(-P->lam_l, cp0, cc);
+            } else {
+                const uint32_t off = b256 ? (__float_as_uint(cp0) >> 16) & 0x3fcu
+                                          : (__float_as_uint(cp0) >> (sh - 2)) & 0xfcu;
+                bits = *(const uint32_t*)((const char*)s_cert + off);
+                uint32_t chk = *(const uint32_t*)((const char*)s_chk + off), amb = 0;
+                while (chk) {
+                    const int k = __builtin_ctz(chk);
+                    chk &= chk - 1;
+                    if (cp0 <= s_lo[k])
+                        bits |= 1u << k;
+                    else if (cp0 <= s_hi[k])
+                        amb |= 1u << k;
+                }
+                if (!live) amb = 0u;
+                if (__ballot(amb != 0u)) {
+                    // the plan's ids into this lane's column of a second id array
+                    // over s_f (free in this phase): its row's digits, which phase 1
+                    // left in the row's column of s_id, and y's id
+                    uint8_t* s_pid = (uint8_t*)s_f;
+                    const int rc = wbase + (int)min(lr, nrows - 1);
+                    for (int n = 0; n < y; ++n) s_pid[n * WG + tid] = s_id[n * WG + rc];
+                    s_pid[y * WG + tid] = (uint8_t)j;
+                    __builtin_amdgcn_wave_barrier();
+                    resolve_bands(P, s_pid, amb, &bits);
+                    __builtin_amdgcn_wave_barrier();
                 }
             }
             if (live) {
-                if (corr) corr[t] = cc;
-                if (dem) dem[t] = d;
-                if (feas) feas[t] = K >= 32 ? 0xffffffffu : ((1u << K) - 1u);
+                if (corr) corr[o] = cc;
+                if (feas) feas[o] = bits;
+                if (dem) dem[o] = d;
             }
-            continue;
-        }
-        // feasibility per level: certain in fp32 outside the band (lo, hi], else
-        // the definition's fp64 CP, evaluated by the wave
-        uint32_t bits = 0, amb = 0;
-        for (int k = 0; k < K && k < 32; ++k) {
-            if (cp0 <= P->lo[k])
-                bits |= 1u << k;
-            else if (cp0 <= P->hi[k])
-                amb |= 1u << k;
-        }
-        if (!live) amb = 0u;
-        if (__ballot(amb != 0u)) {
-#pragma unroll
-            for (int n = 0; n < N; ++n) s_id[n * WG + tid] = (uint8_t)id[n];
-            resolve_bands(P, s_id, amb, &bits);
-        }
-        if (live && row) {
+            if (!cpo) continue;
+            // the K values of each of the 64 plans: uniform pressure cp0 / (1 - rho_k)
+            // in fp32 (cp0 * mk[k]), the objective G - lambda_ld L_k d (one fma);
+            // each lane stores consecutive floats of the 64 plans' rows, so every
+            // store covers one contiguous span
+            s_v[tid] = make_float2(OBJ ? G : cp0, d);
+            __builtin_amdgcn_wave_barrier();
+            const uint32_t nlive = (uint32_t)min((uint64_t)nrows * (uint64_t)ry - q0, (uint64_t)64);
+            const uint64_t p0 = pw + q0;  // plan of the step's first lane
+            const uint32_t la = p0 < J->begin ? (uint32_t)(J->begin - p0) : 0u;
+            const uint32_t lb = p0 >= p_end ? 0u : (uint32_t)min((uint64_t)nlive, p_end - p0);
+            const int64_t e0 = ((int64_t)p0 - (int64_t)J->begin) * K;  // output float of the step's lane 0 (>= 0 from lane la on)
             if (vec) {
-                for (int k = 0; k < K; k += 4)
-                    *(float4*)(row + k) = make_float4(cp0 * P->mk[k], cp0 * P->mk[k + 1], cp0 * P->mk[k + 2],
-                                                      cp0 * P->mk[k + 3]);
+                for (int m = 0; m < K; m += 4) {
+                    const uint32_t f = 4u * (uint32_t)lane + 64u * (uint32_t)m;  // float within the 64 rows
+                    const uint32_t pl = (f * kinv) >> 20, k = f - pl * (uint32_t)K;
+                    if (pl < la || pl >= lb) continue;
+                    const float2 u = s_v[wbase + (int)pl];
+                    const float4 c = *(const float4*)(s_mk + k);
+                    const float4 w = OBJ ? make_float4(fmaf(-c.x, u.y, u.x), fmaf(-c.y, u.y, u.x), fmaf(-c.z, u.y, u.x),
+                                                       fmaf(-c.w, u.y, u.x))
+                                         : make_float4(u.x * c.x, u.x * c.y, u.x * c.z, u.x * c.w);
+                    *(float4*)(cpo + e0 + f) = w;
+                }
             } else {
-                for (int k = 0; k < K; ++k) row[k] = cp0 * P->mk[k];
+                for (int m = 0; m < K; ++m) {
+                    const uint32_t f = (uint32_t)lane + 64u * (uint32_t)m;
+                    const uint32_t pl = (f * kinv) >> 20, k = f - pl * (uint32_t)K;
+                    if (pl < la || pl >= lb) continue;
+                    const float2 u = s_v[wbase + (int)pl];
+                    cpo[e0 + f] = OBJ ? fmaf(-s_mk[k], u.y, u.x) : u.x * s_mk[k];
+                }
             }
-        }
-        if (live) {
-            if (corr) corr[t] = cc;
-            if (feas) feas[t] = bits;
-            if (dem) dem[t] = d;
+            __builtin_amdgcn_wave_barrier();  // s_v is rewritten by the next step
         }
     }
 }
@@ -2529,40 +2621,37 @@ hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, h
     return hipGetLastError();
 }
 
+// ry: implementations of the DAG's last node (the plans of one row)
 hipError_t launch_score(const JobDev& job, uint64_t units, float* corr, float* cp, float* dem, uint32_t* feas,
-                        int n_nodes, int n_entries, bool simple, bool obj, hipStream_t s) {
+                        int n_nodes, int n_entries, int ry, bool simple, bool obj, hipStream_t s) {
     const size_t lds = score_lds(n_nodes, n_entries);
-    // unrolled kernels, one per node count: RANGE sources of 32-bit indices,
-    // uniform pressure or the objective, up to 16 nodes (at 24 the ~n^2/2
-    // scalar predecessor tests per plan made an unrolled kernel 1.5x slower
-    // than the LDS loops)
-    const bool fast = simple && job.kind == DY_SOURCE_RANGE && !job.big && n_nodes <= 16 && n_entries <= SCORE_TAB;
-    const size_t lds_fast = (size_t)n_entries * (sizeof(float2) + sizeof(float)) + (size_t)n_nodes * WG;
+    // rows of plans (nodes 0..N-2 fixed, y = N-1 swept; one row for a 1-node
+    // DAG): RANGE sources of 32-bit indices, uniform pressure or the
+    // objective, tables small enough for LDS
+    const size_t head = (((size_t)n_nodes * WG * sizeof(float) + (size_t)n_nodes * WG) + 15) & ~(size_t)15;
+    const size_t lds_row = head + (size_t)n_entries * (sizeof(float2) + sizeof(float));
+    if (simple && job.kind == DY_SOURCE_RANGE && !job.big && n_entries <= SCORE_ROW_TAB && lds_row <= SCORE_ROW_LDS) {
+        const uint64_t rows = (job.begin + job.count - 1) / (uint64_t)ry - job.begin / (uint64_t)ry + 1;
+        for (uint64_t off = 0; off < rows; off += MAX_GRID_X * WG) {
+            const uint64_t end = rows - off < MAX_GRID_X * WG ? rows : off + MAX_GRID_X * WG;
+            const uint64_t gx = (end - off + WG * SCORE_ROWS_PT - 1) / (WG * SCORE_ROWS_PT);
+            if (obj)
+                hipLaunchKernelGGL(k_score_row<true>, dim3((uint32_t)gx), dim3(WG), lds_row, s, job, off, end, corr, cp,
+                                   dem, feas);
+            else
+                hipLaunchKernelGGL(k_score_row<false>, dim3((uint32_t)gx), dim3(WG), lds_row, s, job, off, end, corr, cp,
+                                   dem, feas);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    }
+    // everything else (rows, per-backend pressure, 64-bit indices, large
+    // tables): the generic per-plan kernel
     for (uint64_t off = 0; off < units; off += MAX_GRID_X * WG) {
         const uint64_t end = units - off < MAX_GRID_X * WG ? units : off + MAX_GRID_X * WG;
         const uint64_t gx = (end - off + WG * SCORE_PPT - 1) / (WG * SCORE_PPT);
-        const dim3 grid((uint32_t)gx);
-        if (!fast) {
-            hipLaunchKernelGGL(k_score, grid, dim3(WG), lds, s, job, off, end, corr, cp, dem, feas);
-        } else {
-            switch (n_nodes * 2 + (obj ? 1 : 0)) {
-#define DYP_SCORE_FAST(NN)                                                                                    \
-    case 2 * NN:                                                                                              \
-        hipLaunchKernelGGL((k_score_fast<NN, false>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem, \
-                           feas);                                                                             \
-        break;                                                                                                \
-    case 2 * NN + 1:                                                                                          \
-        hipLaunchKernelGGL((k_score_fast<NN, true>), grid, dim3(WG), lds_fast, s, job, off, end, corr, cp, dem,  \
-                           feas);                                                                             \
-        break;
-                DYP_SCORE_FAST(1) DYP_SCORE_FAST(2) DYP_SCORE_FAST(3) DYP_SCORE_FAST(4)
-                DYP_SCORE_FAST(5) DYP_SCORE_FAST(6) DYP_SCORE_FAST(7) DYP_SCORE_FAST(8)
-                DYP_SCORE_FAST(9) DYP_SCORE_FAST(10) DYP_SCORE_FAST(11) DYP_SCORE_FAST(12)
-                DYP_SCORE_FAST(13) DYP_SCORE_FAST(14) DYP_SCORE_FAST(15) DYP_SCORE_FAST(16)
-#undef DYP_SCORE_FAST
-                default: return hipErrorInvalidValue;
-            }
-        }
+        hipLaunchKernelGGL(k_score, dim3((uint32_t)gx), dim3(WG), lds, s, job, off, end, corr, cp, dem, feas);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -313,8 +313,7 @@ def check_scores(prob, obj, U, T, Dd, J, gu, gj, gd, gf):
 @pytest.mark.parametrize("jit", [1, 0])
 @pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 11, 13, 16, 17])
 def test_score_node_counts(n, jit):
-    # the kernel generated for the DAG (jit 1), else one unrolled objective
-    # kernel per node count up to 16 and the generic kernel beyond
+    # a range of 32-bit plan indices: the row kernel with either JIT option
     rng = np.random.default_rng(70 + n)
     r = max(2, min(12, int(round(20000 ** (1.0 / n)))))
     prob = small_dag(n, [int(x) for x in rng.integers(1, r + 1, n)], 700 + n)
@@ -373,3 +372,23 @@ def test_rows_generated_kernel_matches_generic_path():
             plan.set_option(D.DY_OPT_JIT, jit)
             got = plan.select([D.rows_source(0, d, n, 24, 5)], stream=stream())[0]
         assert_obj_choices(got, want, f"rows jit={jit}")
+
+
+def test_score_odd_levels_unaligned_output():
+    # three levels (rows of 12 bytes) into a CP output that is not 16-byte
+    # aligned, a range that starts and ends inside rows of the last node
+    prob = wl.forkjoin8()
+    obj = with_tools(wl.paper_objective(prob, levels=(0.0, 0.7, 2.0)), 8, (3,))
+    K = obj.n_levels
+    begin, cnt = 1000005, 123457
+    with D.Plan((prob, obj)) as plan:
+        u = torch.empty(cnt, dtype=torch.float32, device="cuda")
+        buf = torch.empty(cnt * K + 1, dtype=torch.float32, device="cuda")
+        j = buf[1:].view(cnt, K)
+        d = torch.empty(cnt, dtype=torch.float32, device="cuda")
+        f = torch.empty(cnt, dtype=torch.int32, device="cuda")
+        plan.score(D.range_source(0, begin, cnt), u, j, d, f, stream=stream())
+        torch.cuda.synchronize()
+    U, T, Dd, J = orc.obj_score(prob, obj, begin, cnt)
+    check_scores(prob, obj, U, T, Dd, J, u.cpu().numpy(), j.cpu().numpy(), d.cpu().numpy(),
+                 f.cpu().numpy().astype(np.uint32))

@@ -213,12 +213,53 @@ def test_score_ranges(name, begin, count):
     assert_scores(got, orc.score_range(prob, begin, count), name)
 
 
+def wide_last_problem(rng, n, K, ry):
+    # nodes 0..n-2 of radix 1..4, the last node of radix ry; uniform pressure
+    radix = np.concatenate([rng.integers(1, 5, size=n - 1), [ry]]).astype(np.int32)
+    R = int(radix.max())
+    edges = np.array([(i, j) for i in range(n) for j in range(i + 1, n) if rng.random() < 0.4],
+                     np.int32).reshape(-1, 2)
+    prob = wl.Problem(n_nodes=n, edges=edges, radix=radix, p=rng.uniform(0.4, 1.0, (n, R)).astype(np.float32),
+                      tau=rng.lognormal(0, 0.6, (n, R)).astype(np.float32),
+                      size=rng.choice([0.5, 1, 2.5, 6], (n, R)).astype(np.float32),
+                      backend=rng.integers(0, 2, (n, R)).astype(np.int32), w=rng.uniform(0, 1, n).astype(np.float32),
+                      rho=np.repeat(np.sort(rng.uniform(0, 0.9, K))[:, None], 2, axis=1).astype(np.float32), slo=0.0)
+    prob.slo = f32(np.quantile(orc.cp0_values(prob, 0, prob.n_plans()), 0.5) * 1.3)
+    return prob
+
+
+@pytest.mark.parametrize("K", [1, 3, 4, 6, 8, 13, 32])
+def test_score_row_shapes(K):
+    # RANGE scores go by rows of the last node's implementations, the K
+    # per-level values of a wave's plans stored lane-contiguously: level counts
+    # with and without 16-byte rows, a CP output that is not 16-byte aligned,
+    # ranges that start and end inside a row, last nodes with fewer and more
+    # implementations than a wave's 64 plans
+    rng = np.random.default_rng(4200 + K)
+    for trial, ry in enumerate([1, 7, 64, 150]):
+        prob = wide_last_problem(rng, int(rng.integers(2, 6)), K, ry)
+        total = prob.n_plans()
+        begin = int(rng.integers(0, max(1, total // 6)))
+        count = max(1, int(total - begin - rng.integers(0, max(1, total // 6))))
+        ctx = f"K {K}, last radix {ry}, plans [{begin}, {begin + count})"
+        with D.Plan(prob) as plan:
+            got = run_score(plan, D.range_source(0, begin, count), count, K)
+            buf = torch.empty(count * K + 1, dtype=torch.float32, device="cuda")
+            cp = buf[1:].view(count, K)  # 4-byte aligned only
+            plan.score(D.range_source(0, begin, count), None, cp, None, None, stream=stream())
+            torch.cuda.synchronize()
+        want = orc.score_range(prob, begin, count)
+        assert_scores(got, want, ctx)
+        np.testing.assert_allclose(cp.cpu().numpy(), want[1], rtol=RTOL, atol=0, err_msg=ctx + ", unaligned cp")
+
+
 @pytest.mark.parametrize("jit", [1, 0])
 @pytest.mark.parametrize("n", list(range(1, 18)) + [20, 24, 32])
 def test_score_every_node_count(n, jit):
-    # ranges: one unrolled kernel per node count up to 16; beyond, the kernel
-    # generated for the DAG (jit 1) or the generic kernel (jit 0).  Whole plan
-    # spaces of up to ~2^17 plans, else 2^17 plans at a random offset.
+    # ranges of 32-bit plan indices take the row kernel whatever the node
+    # count and the JIT option (the generated kernels serve rows and the
+    # selection); whole plan spaces of up to ~2^17 plans, else 2^17 plans at
+    # a random offset
     rng = np.random.default_rng(900 + n)
     rmax = max(2, min(12, int(round(30000 ** (1.0 / n)))))
     if n <= 17:
