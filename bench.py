@@ -28,9 +28,10 @@ The CPU baseline (the fp64 oracle, single-threaded) runs first, in a child
 process pinned to one core with taskset, before the GPU is touched.
 
 Prints one JSON line.  The roofline object describes the dominant kernel;
-"traffic" is its HBM traffic per launch from stored rocprofv3 FETCH_SIZE /
-WRITE_SIZE counters (calibrated on a device copy), reported only while the
-kernel sources are the ones the counters were taken on.
+"traffic" is its HBM traffic per step (every launch of it in a step) from
+stored rocprofv3 FETCH_SIZE / WRITE_SIZE counters (calibrated on a device
+copy), reported only while the kernel sources are the ones the counters were
+taken on.
 
 Modes that need no GPU turn rocprofv3 output into the summaries kept under
 profiles/: --trace-summary (kernel trace), --pmc-summary (SQ counters),
@@ -65,10 +66,19 @@ PEAK_VALU = N_CU * 4 * 16 * CLOCK_HZ
 PEAK_VALU_PACKED = 2 * PEAK_VALU
 PEAK_HBM = 8.0e12                 # bytes/s
 
-# Kernel sources whose hash keys the stored HBM-traffic counters: a stored
-# figure is reported only while these files are unchanged.
-KERNEL_SOURCES = ("paper_2607_02942_amd/csrc/kernels.hip", "paper_2607_02942_amd/csrc/jit_rows.cpp",
-                  "paper_2607_02942_amd/csrc/dyplan_internal.h")
+# Sources whose hash keys a kernel's stored HBM-traffic counters: the file
+# that defines it (the library's kernels, or the generator of the per-problem
+# "dy_*" kernels), the device layout they share, and the host code that sizes
+# and launches them.  A stored figure is reported only while these files are
+# unchanged.
+CSRC = "paper_2607_02942_amd/csrc/"
+
+
+def kernel_sources(kernel):
+    own = CSRC + ("jit_rows.cpp" if kernel.startswith("dy_") else "kernels.hip")
+    return (own, CSRC + "dyplan_internal.h", CSRC + "host.cpp")
+
+
 GOLDEN_DIR = os.path.join(ROOT, "tests", "golden")
 WORKLOADS = ["chain4", "forkjoin8", "layered10", "batch6", "stream24"]
 
@@ -101,10 +111,10 @@ def score_kernel(prob, per_class):
     return "k_score" if per_class else "k_score_row"
 
 
-def kernel_source_sha():
+def kernel_source_sha(kernel):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in kernel_sources(kernel):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -115,16 +125,16 @@ def traffic_path(key):
 
 
 def stored_traffic(key, kernel):
-    """HBM bytes per launch of `kernel`, from the counters stored for the
+    """HBM bytes per step of `kernel`, from the counters stored for the
     current kernel sources (None when absent, stale or of another kernel)."""
     try:
         with open(traffic_path(key)) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    if t.get("source_sha") != kernel_source_sha() or t.get("kernel_base") != kernel:
+    if t.get("kernel_base") != kernel or t.get("source_sha") != kernel_source_sha(kernel):
         return None
-    return t["traffic_bytes_per_launch"]
+    return t["traffic_bytes_per_step"]
 
 
 # ---------------------------------------------------------------------------
@@ -144,28 +154,35 @@ def _pmc_per_dispatch(db, counter):
 
 
 def _one_kernel(per, base, db):
+    """(names, per-step value, steps) of the dispatches of the kernels whose base
+    name is `base`: one step launches each instantiation of it once (the
+    library launches one per group of sources, e.g. k_sweep with and without
+    prefix sinks), so the per-step value is the sum over the matched
+    dispatches divided by the dispatch count of the most frequent one."""
     hits = match_kernel(per.keys(), base)
-    if len(hits) != 1:
-        raise SystemExit(f"{db}: {len(hits)} kernels named {base!r} among {sorted(per)}")
-    v = per[hits[0]]
-    return hits[0], sum(v) / len(v), len(v)
+    if not hits:
+        raise SystemExit(f"{db}: no kernel named {base!r} among {sorted(per)}")
+    steps = max(len(per[h]) for h in hits)
+    return hits, sum(sum(per[h]) for h in hits) / steps, steps
 
 
 def ingest_pmc(key, kernel, fetch_db, write_db, calib_fetch_db, calib_write_db, calib_bytes, commands):
-    """Store `kernel`'s HBM traffic per launch: FETCH_SIZE and WRITE_SIZE (KiB
-    per dispatch, mean over that kernel's dispatches only), each scaled by
-    bytes / counter of a plain device copy of known size."""
-    kname, fetch, nf = _one_kernel(_pmc_per_dispatch(fetch_db, "FETCH_SIZE"), kernel, fetch_db)
+    """Store `kernel`'s HBM traffic per step: FETCH_SIZE and WRITE_SIZE (KiB,
+    summed over that kernel's dispatches of a step, every instantiation of it,
+    mean over the steps), each scaled by bytes / counter of a plain device
+    copy of known size."""
+    knames, fetch, nf = _one_kernel(_pmc_per_dispatch(fetch_db, "FETCH_SIZE"), kernel, fetch_db)
     _, write, nw = _one_kernel(_pmc_per_dispatch(write_db, "WRITE_SIZE"), kernel, write_db)
     _, cf, _ = _one_kernel(_pmc_per_dispatch(calib_fetch_db, "FETCH_SIZE"), "__amd_rocclr_copyBuffer", calib_fetch_db)
     _, cw, _ = _one_kernel(_pmc_per_dispatch(calib_write_db, "WRITE_SIZE"), "__amd_rocclr_copyBuffer", calib_write_db)
     ff, fw = calib_bytes / (cf * 1024.0), calib_bytes / (cw * 1024.0)
-    rec = {"workload": key, "kernel": kname, "kernel_base": kernel, "source_sha": kernel_source_sha(),
-           "dispatches": [nf, nw],
-           "fetch_kib_per_dispatch": fetch, "write_kib_per_dispatch": write,
+    rec = {"workload": key, "kernels": knames, "kernel_base": kernel, "source_sha": kernel_source_sha(kernel),
+           "sources": list(kernel_sources(kernel)),
+           "steps": [nf, nw],
+           "fetch_kib_per_step": fetch, "write_kib_per_step": write,
            "calib_copy_bytes": calib_bytes, "calib_fetch_kib": cf, "calib_write_kib": cw,
            "fetch_factor": ff, "write_factor": fw,
-           "traffic_bytes_per_launch": fetch * 1024.0 * ff + write * 1024.0 * fw,
+           "traffic_bytes_per_step": fetch * 1024.0 * ff + write * 1024.0 * fw,
            "commands": commands}
     with open(traffic_path(key), "w") as fh:
         json.dump(rec, fh, indent=1)
@@ -185,7 +202,7 @@ def trace_summary(db, title, command, kernel, bench_log=None, plain_log=None, pl
     rows = list(con.execute("select name, count(*), sum(duration), avg(duration), min(duration), max(duration) "
                             "from kernels group by name order by sum(duration) desc"))
     tot = sum(r[2] for r in rows)
-    out = [f"# {title}", "", "Command (from the repository root on the GPU box):", "", "```", command, "```", "",
+    out = [f"# {title}", "", "Command (on the GPU box; `<repo>` is the repository root):", "", "```", command, "```", "",
            "rocprofv3 kernel trace, per-kernel statistics (durations in microseconds):", "",
            "| kernel | calls | total us | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
     for n, c, s, a, mn, mx in rows:
@@ -193,11 +210,15 @@ def trace_summary(db, title, command, kernel, bench_log=None, plain_log=None, pl
                    f"{100 * s / tot:.1f} |")
     names = [r[0] for r in rows]
     hits = match_kernel(names, kernel)
-    if len(hits) != 1:
-        raise SystemExit(f"{len(hits)} kernels named {kernel!r} in {names}")
-    ts = [r[0] for r in con.execute("select duration from kernels where name = ? order by start", (hits[0],))]
-    out += ["", f"Dominant kernel `{kernel}` (exact name `{hits[0]}`): {len(ts)} dispatches, average "
-                f"{sum(ts) / len(ts) / 1e3:.2f} us, median {float(np.median(ts)) / 1e3:.2f} us."]
+    if not hits:
+        raise SystemExit(f"no kernel named {kernel!r} in {names}")
+    per = {h: [r[0] for r in con.execute("select duration from kernels where name = ? order by start", (h,))]
+           for h in hits}
+    steps = max(len(v) for v in per.values())
+    step_us = sum(sum(v) for v in per.values()) / steps / 1e3
+    desc = ", ".join(f"`{h}` ({len(v)} dispatches, average {sum(v) / len(v) / 1e3:.2f} us)" for h, v in per.items())
+    out += ["", f"Dominant kernel `{kernel}`: {desc}. One step launches each instantiation once: "
+                f"{steps} steps, {step_us:.2f} us of `{kernel}` per step (trace average)."]
     if bench_log:
         d = _bench_line(bench_log)
         if d:
@@ -209,8 +230,8 @@ def trace_summary(db, title, command, kernel, bench_log=None, plain_log=None, pl
                     f"{r['kernel_ms'] * 1e3:.1f} us per step (events) -> roofline frac {r['frac']:.3f} "
                     f"({r['bound']})."]
             if r["bound"] in ("alu", "hbm") and "achieved_units_per_step" in r:
-                fr = r["achieved_units_per_step"] / (sum(ts) / len(ts) / 1e9) / (r["peak"] * r["peak_scale"])
-                out.append(f"From the trace average instead: frac {fr:.3f}.")
+                fr = r["achieved_units_per_step"] / (step_us / 1e6) / (r["peak"] * r["peak_scale"])
+                out.append(f"From the trace's per-step average instead: frac {fr:.3f}.")
     if plain_log:
         p = _bench_line(plain_log)
         if p:
@@ -234,13 +255,14 @@ def pmc_summary(dbs, kernel, title, commands, trace_db=None):
         names = [r[0] for r in con.execute("select distinct counter_name from counters_collection")]
         for cn in names:
             per = _pmc_per_dispatch(db, cn)
-            kname, mean, nd = _one_kernel(per, kernel, db)
-            vals[cn] = (mean, nd, kname)
-    out = [f"# {title}", "", "Commands (from the repository root on the GPU box), one counter pass each:", "",
+            knames, v, nsteps = _one_kernel(per, kernel, db)
+            vals[cn] = (v, nsteps, knames)
+    kn = ", ".join(f"`{k}`" for k in next(iter(vals.values()))[2])
+    out = [f"# {title}", "", "Commands (on the GPU box; `<repo>` is the repository root), one counter pass each:", "",
            "```"] + commands + ["```", "",
-                                f"Per-dispatch means over the dispatches of `{kernel}` only "
-                                f"(exact name `{next(iter(vals.values()))[2]}`):", "",
-                                "| counter | value | dispatches |", "|---|---|---|"]
+                                f"Per-step values of `{kernel}` (summed over a step's dispatches of {kn}, "
+                                "mean over the steps):", "",
+                                "| counter | value per step | steps |", "|---|---|---|"]
     for cn in sorted(vals):
         out.append(f"| `{cn}` | {vals[cn][0]:.0f} | {vals[cn][1]} |")
     g = lambda c: vals[c][0] if c in vals else None
@@ -255,10 +277,10 @@ def pmc_summary(dbs, kernel, title, commands, trace_db=None):
         con = sqlite3.connect(trace_db)
         names = [r[0] for r in con.execute("select distinct name from kernels")]
         hits = match_kernel(names, kernel)
-        ts = [r[0] for r in con.execute("select duration from kernels where name = ?", (hits[0],))]
-        dur = sum(ts) / len(ts) / 1e9
+        per = {h: [r[0] for r in con.execute("select duration from kernels where name = ?", (h,))] for h in hits}
+        dur = sum(sum(v) for v in per.values()) / max(len(v) for v in per.values()) / 1e9
         cyc = dur * CLOCK_HZ
-        out.append(f"- average duration in the kernel trace: {dur * 1e6:.2f} us = {cyc:.0f} cycles at 2.4 GHz")
+        out.append(f"- duration per step in the kernel trace: {dur * 1e6:.2f} us = {cyc:.0f} cycles at 2.4 GHz")
         if g("SQ_INSTS_VALU") is not None:
             out.append(f"- VALU issue: {g('SQ_INSTS_VALU') / (cyc * N_CU):.3f} wave-instructions per CU per cycle "
                        "(limit 1: four SIMDs, each one 64-lane instruction per 4 cycles)")
