@@ -28,6 +28,7 @@ hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, int nmax, int nrmax, hipStream_t s);
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
 hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
+hipError_t launch_seed_cands(const JobDev* d_jobs, int njobs, int kmax, int nmax, hipStream_t s);
 hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s);
 hipError_t static_scratch(int device, char** ptr, size_t* bytes);
 struct JitRows {
@@ -59,6 +60,18 @@ constexpr int kStaticSources = 64;                // sources per dy_plan_select_
 constexpr uint32_t kStaticMinCand = 1024;         // candidate slots per source it needs at least
 constexpr int kClimbNodes = 8;                    // local-search seeds for problems of at most this many nodes
 constexpr int kClimbMinSources = 128;             // ... in calls of at least this many such sources (DY_OPT_CLIMB 1)
+// ROWS sources of at least kSplitRows rows under per-backend pressure
+// (generated kernels) are scored in two shares: the first 1/kSplitShare of the
+// rows, then the candidates gathered so far re-seed the thresholds
+// (k_seed_cands), then the rest.  The sampled seeds then only serve the first
+// share, so they are sparser (stride up to kSplitStride).  Under per-backend
+// pressure the prefilter works on the unpressured CP and passes most rows
+// unless the thresholds are near the optimum; under uniform pressure the
+// sampled seeds already abandon most rows early and a second share measured
+// no gain.
+constexpr uint64_t kSplitRows = 1ull << 22;
+constexpr uint64_t kSplitShare = 32;
+constexpr uint64_t kSplitStride = 512;
 constexpr double kU = 0x1p-24;                    // fp32 unit roundoff
 
 struct HostProb {
@@ -1156,12 +1169,22 @@ struct PassPlan {
 
 // Rows sources run the problem's generated
 // kernels (one launch per source; the host copies of the job carry the args).
-hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sample, hipStream_t s) {
+// Rows [r0, min(r1, count)) of the source for the scan (the sampler takes
+// the whole source).
+hipError_t launch_jit(const dy_plan* h, const JobDev& J, int problem, bool sample, hipStream_t s, uint64_t r0 = 0,
+                      uint64_t r1 = ~0ull) {
     const ProbDev& D = h->hdesc[problem];
     const JitRows& jr = h->jit[problem];
     const ProbDev* dp = h->d_probs + problem;
     unsigned long long rows_stride = J.stride, count = J.count, index_base = J.index_base;
     const unsigned char* rows = J.rows;
+    if (!sample) {
+        r1 = std::min<uint64_t>(r1, J.count);
+        if (r0 >= r1) return hipSuccess;
+        rows += r0 * J.stride;
+        count = r1 - r0;
+        index_base += r0;
+    }
     const float2* at = D.at;
     int rmax = D.rmax, bin_shift = D.bin_shift;
     int aligned = ((J.stride | (uint64_t)(uintptr_t)J.rows | (uint64_t)D.n) & 3u) == 0 ? 1 : 0;
@@ -1344,6 +1367,12 @@ bool jit_ready(dy_plan* h, int p) {
 
 }  // namespace
 
+// First share of a ROWS job scored in two shares (0: one pass).
+static uint64_t split_rows(const JobDev& J, const ProbDev& D) {
+    if (J.kind != DY_SOURCE_ROWS || D.obj || D.uniform || J.count < kSplitRows) return 0;
+    return J.count / kSplitShare;
+}
+
 // stat: dy_plan_select_static (per-call device memory in the fixed array, no
 // kernel compilation, direct launches, results copied back into the caller's
 // array); otherwise dy_plan_select.
@@ -1461,6 +1490,8 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         // the local search gives each level a seed near its optimum; the
         // sample then only backs it up (about 256 samples per source)
         if (!h->stride_fixed && J.climb) stride = std::max<uint64_t>(stride, std::min<uint64_t>(2048, sunits / 256));
+        if (!h->stride_fixed && g == G_JIT && split_rows(J, h->hdesc[src[j].problem]))
+            stride = std::max<uint64_t>(stride, std::min<uint64_t>(kSplitStride, sunits / kMinSamples));
         J.sample_stride = (uint32_t)stride;
         J.units = sweep ? J.nblk : J.count;
         ++pp.n[g];
@@ -1488,6 +1519,10 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         jobs[q] = J;
     }
     const int n3 = pp.before(G_JIT);  // jobs of the other groups; JIT jobs follow
+    // first share of a JIT rows job scored in two shares (0: one pass)
+    auto split_at = [&](const JobDev& J) { return split_rows(J, h->hdesc[(int)(J.prob - h->d_probs)]); };
+    bool any_split = false;
+    for (int q = n3; q < n3 + pp.n[G_JIT]; ++q) any_split = any_split || split_at(jobs[q]) != 0;
     bool any_climb = false;
     for (int q = 0; q < n3; ++q) any_climb = any_climb || jobs[q].climb != 0;
     // the job array is rebuilt every call but uploaded only when it changed
@@ -1509,11 +1544,16 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
     std::function<void(hipError_t, const char*)> chk = [&](hipError_t x, const char* what) {
         if (x != hipSuccess && st == DY_OK) st = hip_fail(&h->err, x, what);
     };
+    // share 0: every row; 1: the first share of split sources, every row of
+    // the others; 2: the rest of split sources
     auto jit_pass = [&](const JobDev* hjobs, int first, int n, bool sample, hipStream_t st,
-                        const std::function<void(hipError_t, const char*)>& ck) {
+                        const std::function<void(hipError_t, const char*)>& ck, int share = 0) {
         for (int q = first; q < first + n; ++q) {
             const int p = (int)(hjobs[q].prob - h->d_probs);
-            ck(launch_jit(h, hjobs[q], p, sample, st), sample ? "rows sample" : "rows scan");
+            const uint64_t cut = share ? split_at(hjobs[q]) : 0;
+            if (share == 2 && cut == 0) continue;
+            const uint64_t r0 = share == 2 ? cut : 0, r1 = share == 1 && cut ? cut : ~0ull;
+            ck(launch_jit(h, hjobs[q], p, sample, st, r0, r1), sample ? "rows sample" : "rows scan");
         }
     };
     using Check = std::function<void(hipError_t, const char*)>;
@@ -1529,7 +1569,16 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
     auto issue_mid = [&](hipStream_t st, const Check& ck) {
         if (h->timing) ck(hipEventRecord(h->ev[1], st), "hipEventRecord");
         launch_main(h, S.d_jobs, jobs.data(), pp, st, ck);
-        jit_pass(jobs.data(), n3, pp.n[G_JIT], false, st, ck);
+        if (any_split) {
+            jit_pass(jobs.data(), n3, pp.n[G_JIT], false, st, ck, 1);
+            for (int c = 0; c < pp.n[G_JIT]; c += 65535) {
+                const int m = std::min(65535, pp.n[G_JIT] - c);
+                ck(launch_seed_cands(S.d_jobs + n3 + c, m, pp.kmax, h->nmax, st), "seed from candidates");
+            }
+            jit_pass(jobs.data(), n3, pp.n[G_JIT], false, st, ck, 2);
+        } else {
+            jit_pass(jobs.data(), n3, pp.n[G_JIT], false, st, ck);
+        }
         if (h->timing) ck(hipEventRecord(h->ev[2], st), "hipEventRecord");
     };
     auto issue_post = [&](hipStream_t st, const Check& ck) {

@@ -342,7 +342,10 @@ __device__ bool last_block(uint32_t* counter, uint32_t expected) {
 // Per level candidate threshold T_k from the seed slots, and the 64-bin
 // prefilter table (and, for problems with a generated sweep, its 256-bin
 // table); resets the job's candidate count and flags for the scoring pass.  Called by every thread of one block (>= 64 threads).
-__device__ void build_table(JD J, PD P) {
+// reset: also empty the candidate list and clear the flags (before a scoring
+// pass; a rebuild between the shares of a source keeps what the first share
+// gathered)
+__device__ void build_table(JD J, PD P, bool reset = true) {
     __shared__ float s_thr[KMAX];
     const int lane = threadIdx.x;
     const bool obj = P->obj != 0;
@@ -395,7 +398,7 @@ __device__ void build_table(JD J, PD P) {
             J->table2[i] = __float_as_uint(g);
         }
     }
-    if (lane == 0) {
+    if (reset && lane == 0) {
         *J->ncand = 0u;
         *J->flags = 0;
     }
@@ -1388,6 +1391,14 @@ __global__ void k_table(JobDev* __restrict__ jobs, int njobs) {
     build_table(J, cs(J->prob));
 }
 
+// The thresholds and tables again from the seeds, the candidate list kept.
+__global__ void k_retable(JobDev* __restrict__ jobs, int njobs) {
+    const int j = blockIdx.x;
+    if (j >= njobs) return;
+    JD J = cs(jobs + j);
+    build_table(J, cs(J->prob), false);
+}
+
 // ---------------------------------------------------------------------------
 // generic per-plan path: ROWS sources, non-uniform pressure, per-plan scores
 // ---------------------------------------------------------------------------
@@ -1924,6 +1935,44 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs,
         J->cert_d[k * CERT_WAVES + g] = bd;
     }
     if (last_block(J->sync, (uint32_t)(J->cert_waves * P->k))) merge_cert(J, P);
+}
+
+// Seeds from the first share of a long ROWS source (corr / SLO mode): every
+// candidate gathered so far whose fp32 corr would raise level k's seed and
+// whose CP is inside the level's band is re-evaluated exactly in fp64; a
+// certainly-feasible one (the definition's CP_k <= SLO) becomes the level's
+// seed, with its fp32 corr.  Any certainly-feasible plan gives a valid
+// threshold, so the rest of the source is then scored against thresholds
+// near the best plan of that share instead of the best of a sparse sample.
+// One wave per (source, level); the seed slots are written by this block
+// only.  Dynamic LDS: N doubles and N id bytes per lane.
+__global__ void __launch_bounds__(64) k_seed_cands(const JobDev* __restrict__ jobs) {
+    extern __shared__ double s_dyn64[];
+    JD J = cs(jobs + blockIdx.x);
+    PD P = cs(J->prob);
+    const int k = blockIdx.y, lane = threadIdx.x;
+    if (k >= P->k || P->obj) return;
+    const int N = P->n, R = P->rmax;
+    double* f = s_dyn64 + lane;
+    uint8_t* ids = (uint8_t*)(s_dyn64 + (size_t)N * 64) + lane;
+    const uint32_t nc = min(*J->ncand, J->cap);
+    uint32_t* slot = J->scert + k * NSLOT;
+    static_assert(NSLOT == 64, "one seed slot per lane");
+    const uint32_t e0 = wave_max_u32(slot[lane]);
+    const float sb0 = e0 ? __uint_as_float(e0 - 1u) : -1.0f;
+    float sb = sb0;
+    const double* lat = P->lat64 + (size_t)k * N * R;
+    const float hi = P->hi[k];
+    for (uint32_t i = lane; i < nc; i += 64) {
+        const Cand c = J->cand[i];
+        if (!(c.corr > sb && c.cp <= hi)) continue;
+        if (!job_ids(J, P, c.index, ids, 64)) continue;
+        double corr, cp, d;
+        cert_eval<false>(P, N, R, ids, f, P->a64, P->dem64, lat, corr, cp, d);
+        if (cp <= P->slo) sb = c.corr;
+    }
+    const uint32_t e = wave_max_u32(sb > sb0 ? __float_as_uint(sb) + 1u : 0u);
+    if (lane == 0 && e > e0) slot[0] = e;
 }
 
 // Overflow recovery: the candidates gathered before the list overflowed
@@ -2600,6 +2649,17 @@ hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, 
     const int tab_d = 3 * nrmax * (int)sizeof(double) <= CERT_LDS_TABLES ? 3 * nrmax : 0;
     const size_t lds = ((size_t)tab_d + (size_t)nmax * 64) * sizeof(double) + (size_t)nmax * 64;
     hipLaunchKernelGGL(k_certify, dim3(waves, njobs, kmax), dim3(64), lds, s, d_jobs, tab_d, nmax);
+    return hipGetLastError();
+}
+
+// k_seed_cands, then the thresholds and tables rebuilt from the new seeds
+hipError_t launch_seed_cands(const JobDev* d_jobs, int njobs, int kmax, int nmax, hipStream_t s) {
+    if (njobs == 0) return hipSuccess;
+    const size_t lds = (size_t)nmax * 64 * (sizeof(double) + 1);
+    hipLaunchKernelGGL(k_seed_cands, dim3(njobs, kmax), dim3(64), lds, s, d_jobs);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_retable, dim3(njobs), dim3(64), 0, s, const_cast<JobDev*>(d_jobs), njobs);
     return hipGetLastError();
 }
 

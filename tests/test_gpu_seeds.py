@@ -139,3 +139,29 @@ def test_rows_calls_repeat_choices_and_candidates(per_class):
     for i, (got, c) in enumerate(runs[1:], 1):
         assert_choices(got, [tuple(x) for x in first], f"call {i}")
         assert c == c0, f"call {i}: {c} candidates, first call {c0}"
+
+
+@pytest.mark.parametrize("per_class", [False, True])
+@pytest.mark.parametrize("winners", ["first share", "second share"])
+def test_rows_scored_in_two_shares(per_class, winners):
+    # a rows source of 2^22 rows or more under per-backend pressure is scored
+    # in two shares, the candidates of the first share (1/32 of the rows)
+    # re-seeding the thresholds of the second (uniform pressure: one pass):
+    # the choices equal the oracle's with every level's winner moved into the
+    # first share, or into the second
+    prob = wl.stream24()
+    if per_class:
+        prob = wl.per_class(prob)
+    n = (1 << 22) + 777
+    rows = wl.make_rows(n, 24, 36, row_begin=31 * n)
+    win = sorted({int(c[0]) for c in orc.select_rows(prob, rows, 0) if int(c[0]) >= 0})
+    for i, w in enumerate(win):
+        to = 5 + 97 * i if winners == "first share" else n - 1 - 97 * i
+        rows[[w, to]] = rows[[to, w]]
+    want = orc.select_rows(prob, rows, 0)
+    assert all(int(c[0]) < n // 32 for c in want if int(c[0]) >= 0) == (winners == "first share")
+    d = torch.from_numpy(rows).cuda()
+    with D.Plan(prob) as plan:
+        for call in range(2):  # the second call replays the captured graph
+            got = plan.select([D.rows_source(0, d, n, 24, 0)], stream=stream())[0]
+            assert_choices(got, want, f"{prob.name}, winners in the {winners}, call {call}")
