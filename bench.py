@@ -153,16 +153,27 @@ def _pmc_per_dispatch(db, counter):
     return per
 
 
+def _steps(counts, hits):
+    """Steps in a profiled run: every selection call certifies once (one
+    k_certify dispatch for up to 65,535 sources); without it (the score
+    bench) each step launches each matched kernel once.  A step may launch
+    a kernel several times: one instantiation per group of sources (k_sweep
+    with and without prefix sinks), or one launch per share of a rows source
+    scored in two shares."""
+    cert = match_kernel(counts.keys(), "k_certify")
+    if cert:
+        return counts[cert[0]]
+    return max(counts[h] for h in hits)
+
+
 def _one_kernel(per, base, db):
-    """(names, per-step value, steps) of the dispatches of the kernels whose base
-    name is `base`: one step launches each instantiation of it once (the
-    library launches one per group of sources, e.g. k_sweep with and without
-    prefix sinks), so the per-step value is the sum over the matched
-    dispatches divided by the dispatch count of the most frequent one."""
+    """(names, per-step value, steps) of the dispatches of the kernels whose
+    base name is `base`: the sum over the matched dispatches divided by the
+    number of steps."""
     hits = match_kernel(per.keys(), base)
     if not hits:
         raise SystemExit(f"{db}: no kernel named {base!r} among {sorted(per)}")
-    steps = max(len(per[h]) for h in hits)
+    steps = _steps({k: len(v) for k, v in per.items()}, hits)
     return hits, sum(sum(per[h]) for h in hits) / steps, steps
 
 
@@ -214,11 +225,11 @@ def trace_summary(db, title, command, kernel, bench_log=None, plain_log=None, pl
         raise SystemExit(f"no kernel named {kernel!r} in {names}")
     per = {h: [r[0] for r in con.execute("select duration from kernels where name = ? order by start", (h,))]
            for h in hits}
-    steps = max(len(v) for v in per.values())
+    steps = _steps({r[0]: r[1] for r in rows}, hits)
     step_us = sum(sum(v) for v in per.values()) / steps / 1e3
     desc = ", ".join(f"`{h}` ({len(v)} dispatches, average {sum(v) / len(v) / 1e3:.2f} us)" for h, v in per.items())
-    out += ["", f"Dominant kernel `{kernel}`: {desc}. One step launches each instantiation once: "
-                f"{steps} steps, {step_us:.2f} us of `{kernel}` per step (trace average)."]
+    out += ["", f"Dominant kernel `{kernel}`: {desc}; {steps} steps (calls), {step_us:.2f} us of `{kernel}` per "
+                "step (trace average)."]
     if bench_log:
         d = _bench_line(bench_log)
         if d:
@@ -278,7 +289,8 @@ def pmc_summary(dbs, kernel, title, commands, trace_db=None):
         names = [r[0] for r in con.execute("select distinct name from kernels")]
         hits = match_kernel(names, kernel)
         per = {h: [r[0] for r in con.execute("select duration from kernels where name = ?", (h,))] for h in hits}
-        dur = sum(sum(v) for v in per.values()) / max(len(v) for v in per.values()) / 1e9
+        counts = {r[0]: r[1] for r in con.execute("select name, count(*) from kernels group by name")}
+        dur = sum(sum(v) for v in per.values()) / _steps(counts, hits) / 1e9
         cyc = dur * CLOCK_HZ
         out.append(f"- duration per step in the kernel trace: {dur * 1e6:.2f} us = {cyc:.0f} cycles at 2.4 GHz")
         if g("SQ_INSTS_VALU") is not None:
