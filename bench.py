@@ -295,7 +295,9 @@ def pmc_summary(dbs, kernel, title, commands, trace_db=None):
         out.append(f"- duration per step in the kernel trace: {dur * 1e6:.2f} us = {cyc:.0f} cycles at 2.4 GHz")
         if g("SQ_INSTS_VALU") is not None:
             out.append(f"- VALU issue: {g('SQ_INSTS_VALU') / (cyc * N_CU):.3f} wave-instructions per CU per cycle "
-                       "(limit 1: four SIMDs, each one 64-lane instruction per 4 cycles)")
+                       "(nominal rate 1: four SIMDs, each one 64-lane instruction per 4 cycles; readings at or "
+                       "slightly above it, as some instruction forms issue faster, mean the VALU pipes are "
+                       "saturated)")
         if g("SQ_WAVE_CYCLES") is not None:
             out.append(f"- mean resident waves per CU: {4 * g('SQ_WAVE_CYCLES') / (cyc * N_CU):.2f} of at most 32 "
                        "(SQ_WAVE_CYCLES counts quad-cycles: 4 SQ_WAVE_CYCLES / (duration x clock x CUs))")
