@@ -141,7 +141,7 @@ struct JobDev {
     int32_t* hflags;
     uint32_t* hdone;          // host-mapped completion word of the call (with hout), set last
     int32_t climb;            // RANGE source over its problem's whole plan space: local-search seeds
-    int32_t pad0;
+    int32_t gblk;             // library sweep: consecutive blocks per thread (units = nblk / gblk)
 };
 
 }  // namespace dyp

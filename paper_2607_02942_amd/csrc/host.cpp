@@ -69,6 +69,7 @@ constexpr int kClimbMinSources = 128;             // ... in calls of at least th
 // unless the thresholds are near the optimum; under uniform pressure the
 // sampled seeds already abandon most rows early and a second share measured
 // no gain.
+constexpr uint64_t kSweepRunMin = 1ull << 20;    // library sweep: runs of blocks per thread for groups of this many blocks
 constexpr uint64_t kSplitRows = 1ull << 22;
 constexpr uint64_t kSplitShare = 32;
 constexpr uint64_t kSplitStride = 512;
@@ -941,6 +942,7 @@ JobDev make_job(const dy_plan* h, const dy_source& s) {
     J.stride = s.row_stride;
     J.index_base = s.index_base;
     J.sample_stride = h->sample_stride;
+    J.gblk = 1;
     if (s.kind == DY_SOURCE_RANGE) {
         const uint64_t inner = (uint64_t)H.rx * (uint64_t)H.ry;
         J.blk_first = s.begin / inner;
@@ -1519,6 +1521,33 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         jobs[q] = J;
     }
     const int n3 = pp.before(G_JIT);  // jobs of the other groups; JIT jobs follow
+    // library sweep of the corr / SLO groups with a compile-time prefix
+    // length: a source whose blocks are aligned runs of G (G dividing the
+    // last prefix node's radix, up to 12) gives each thread G blocks that
+    // share the prefix but its last node; only in groups of many blocks, so
+    // that the fewer threads still fill the device (batch6's 85 M blocks:
+    // sweep 1.61 -> 1.53 ms with runs of 12, 1.59 with runs of 4)
+    for (int g = G_SWEEP; g <= G_SWEEP_S2; ++g) {
+        const int npc = pp.npre_c[g];
+        if (npc != 2 && npc != 4 && npc != 6 && npc != 8) continue;
+        const int q0 = pp.before(g), q1 = pp.before(g) + pp.n[g] - pp.njit[g];
+        uint64_t total = 0;
+        for (int q = q0; q < q1; ++q) total += jobs[q].nblk;
+        if (total < kSweepRunMin) continue;
+        uint64_t units = 0;
+        for (int q = q0; q < q1; ++q) {
+            JobDev& J = jobs[q];
+            const int last = h->hdesc[(int)(J.prob - h->d_probs)].radix[npc - 1];
+            for (int G : {12, 6, 4, 3, 2})
+                if (last % G == 0 && J.blk_first % (uint64_t)G == 0 && J.nblk % (uint64_t)G == 0) {
+                    J.gblk = G;
+                    J.units = J.nblk / (uint64_t)G;
+                    break;
+                }
+            units = std::max(units, J.units);
+        }
+        pp.units[g] = units;
+    }
     // first share of a JIT rows job scored in two shares (0: one pass)
     auto split_at = [&](const JobDev& J) { return split_rows(J, h->hdesc[(int)(J.prob - h->d_probs)]); };
     bool any_split = false;
@@ -1687,6 +1716,10 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
                 if (grp[j] != g) continue;
                 const HostProb& H = h->hp[src[j].problem];
                 JobDev J = jobs[q];
+                if (g < kSweepGroups) {  // the rescoring sweep takes one block per thread
+                    J.gblk = 1;
+                    J.units = J.nblk;
+                }
                 if (round < kReseedRounds) {
                     ++rp.n[g];
                     if (g < G_JIT) rp.units[g] = std::max(rp.units[g], J.units);

@@ -550,6 +550,78 @@ __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big, float* 
     return Prefix{pc, px, py, s, pd};
 }
 
+// Prefix of a run of blocks b0 .. b0 + G - 1 that differ only in the last
+// prefix node's digit (b0 a multiple of G, G dividing that node's radix, so
+// the digits never carry): the nodes before the last are evaluated once by
+// prefix_head, the last one per block by prefix_tail.  Same operations in
+// the same order as prefix_eval, so the same values: the product takes the
+// last node's factor last, and the maxima are exact.
+struct PrefixHead {
+    float pc;      // product of the factors of nodes 0 .. NPRE-2
+    float m;       // the last node's predecessor maximum
+    float px, py, s;  // the maxima into x, into y and over the prefix sinks, nodes 0 .. NPRE-2
+    uint32_t d;    // the last node's digit in b0
+};
+
+template <int NPRE, int RAD>
+__device__ __forceinline__ PrefixHead prefix_head(PD P, uint64_t b0, int big, const float2* s_pat) {
+    static_assert(NPRE > 1, "a head and a last node");
+    const int rmax = P->rmax;
+    float f[NPRE - 1];
+    float pc = 1.0f;
+    uint32_t dg[NPRE];
+    if constexpr (RAD > 0) {
+        uint32_t x = (uint32_t)b0;
+#pragma unroll
+        for (int n = NPRE - 1; n >= 0; --n) {
+            dg[n] = x % (uint32_t)RAD;
+            x /= (uint32_t)RAD;
+        }
+    } else {
+#pragma unroll
+        for (int n = 0; n < NPRE; ++n) dg[n] = prefix_digit(P, n, b0, big);
+    }
+#pragma unroll
+    for (int n = 0; n < NPRE - 1; ++n) {
+        const float2 v = s_pat ? s_pat[n * rmax + dg[n]] : cs(P->at)[n * rmax + dg[n]];
+        pc = pc * v.x;
+        float m = 0.0f;
+        const uint32_t pm = P->pred[n];
+#pragma unroll
+        for (int u = 0; u < n; ++u)
+            if (pm >> u & 1u) m = fmaxf(m, f[u]);
+        f[n] = v.y + m;
+    }
+    float m = 0.0f, px = 0.0f, py = 0.0f, s = 0.0f;
+    const uint32_t pml = P->pred[NPRE - 1];
+    const int xn = P->xnode;
+    const uint32_t pmx = xn >= 0 ? P->pred[xn] : 0u;
+    const uint32_t pmy = P->pred[P->ynode] & (xn >= 0 ? ~(1u << xn) : ~0u);
+    const uint32_t pms = P->pre_sinks;
+#pragma unroll
+    for (int u = 0; u < NPRE - 1; ++u) {
+        if (pml >> u & 1u) m = fmaxf(m, f[u]);
+        if (pmx >> u & 1u) px = fmaxf(px, f[u]);
+        if (pmy >> u & 1u) py = fmaxf(py, f[u]);
+        if (pms >> u & 1u) s = fmaxf(s, f[u]);
+    }
+    return PrefixHead{pc, m, px, py, s, dg[NPRE - 1]};
+}
+
+template <int NPRE>
+__device__ __forceinline__ Prefix prefix_tail(PD P, const PrefixHead& h, int g, const float2* s_pat) {
+    constexpr int n = NPRE - 1;
+    const uint32_t d = h.d + (uint32_t)g;
+    const float2 v = s_pat ? s_pat[n * P->rmax + d] : cs(P->at)[n * P->rmax + d];
+    const float fl = v.y + h.m;
+    const int xn = P->xnode;
+    const bool inx = xn >= 0 && (P->pred[xn] >> n & 1u);
+    const bool iny = (P->pred[P->ynode] >> n & 1u) && n != xn;
+    const bool ins = P->pre_sinks >> n & 1u;
+    return Prefix{h.pc * v.x, inx ? fmaxf(h.px, fl) : h.px, iny ? fmaxf(h.py, fl) : h.py,
+                  ins ? fmaxf(h.s, fl) : h.s, 0.0f};
+}
+
 // One plan of the inner sweep: corr = cx * a_y, CP = max(tau_y + M, S2); the
 // prefilter threshold of CP's bin is read from the 64-entry LDS table (a
 // random LDS read issues in about half the time of a lane permute on gfx950):
@@ -709,38 +781,17 @@ __device__ void general_row(PD P, JD J, uint64_t b, int big, int ix, float cx, f
 // B256: every source of the launch has the 256-bin table (P->jsh = 18).
 // RAD > 0: every prefix node of every source has RAD implementations and the
 // block indices fit 32 bits (constant-divisor digits).
-template <bool HAS_S2, int RY, int NPRE, bool B256, int RAD>
-__global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, uint64_t unit_off) {
-    extern __shared__ float s_f[];
-    JD J = cs(jobs + blockIdx.y);
-    PD P = cs(J->prob);
-    const uint64_t nblk = J->nblk;
-    const uint64_t t0 = unit_off + (uint64_t)blockIdx.x * WG;
-    if (t0 >= nblk) return;
-    const uint64_t t = t0 + threadIdx.x;
-    const bool live = t < nblk;
-    const uint64_t b = J->blk_first + (live ? t : nblk - 1);
-    __shared__ float s_bins[B256 ? NBINS2 : NBINS];
-    if (B256) {
-        s_bins[threadIdx.x] = __uint_as_float(J->table2[threadIdx.x]);
-        static_assert(!B256 || NBINS2 == WG, "one bin per thread");
-    } else if (threadIdx.x < NBINS) {
-        s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
-    }
-    const float2* pat = stage_prefix_rows<false>(P, (float2*)(s_f + (size_t)max(P->npre, 1) * WG), nullptr);
-    const Prefix pf = prefix_eval<NPRE, false, RAD>(P, b, J->big, s_f, pat, nullptr);
-
+// The inner sweep of block b (the prefix pf evaluated): every (x, y) pair,
+// the prefilter per plan, the exact test in the rare path.
+template <bool HAS_S2, int RY, int NPRE, bool B256>
+__device__ __forceinline__ void sweep_block(PD P, JD J, uint64_t b, bool live, const Prefix& pf,
+                                            const float2 (&vyr)[RY > 0 ? RY : 1], const float* s_bins,
+                                            float* s_f) {
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* atx = cs(P->atx);
     const CS float2* aty = cs(P->aty);
     const int rx = P->rx, ry = P->ry;
     const bool exy = P->edge_xy != 0;
-
-    float2 vyr[RY > 0 ? RY : 1];
-    if (RY > 0) {
-#pragma unroll
-        for (int iy = 0; iy < RY; ++iy) vyr[iy] = aty[iy];
-    }
     for (int ix = 0; ix < rx; ++ix) {
         const float2 vx = atx[ix];
         const float fx = vx.y + pf.px;
@@ -779,6 +830,49 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
                 }
             }
         }
+    }
+}
+
+// Work unit = J->gblk consecutive blocks per thread (J->units of them per
+// source): with a compile-time prefix length (NPRE > 0) the host may give a
+// source whose blocks are aligned runs of G (G dividing the last prefix
+// node's radix) G blocks per thread, which share the prefix but its last node
+// (prefix_head once, prefix_tail per block); NPRE == 0 takes one block per
+// thread.
+template <bool HAS_S2, int RY, int NPRE, bool B256, int RAD>
+__global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, uint64_t unit_off) {
+    extern __shared__ float s_f[];
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    const uint64_t units = J->units;
+    const int G = NPRE > 0 ? J->gblk : 1;
+    const uint64_t t0 = unit_off + (uint64_t)blockIdx.x * WG;
+    if (t0 >= units) return;
+    const uint64_t t = t0 + threadIdx.x;
+    const bool live = t < units;
+    const uint64_t b0 = J->blk_first + (live ? t : units - 1) * (uint64_t)G;
+    __shared__ float s_bins[B256 ? NBINS2 : NBINS];
+    if (B256) {
+        s_bins[threadIdx.x] = __uint_as_float(J->table2[threadIdx.x]);
+        static_assert(!B256 || NBINS2 == WG, "one bin per thread");
+    } else if (threadIdx.x < NBINS) {
+        s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
+    }
+    const float2* pat = stage_prefix_rows<false>(P, (float2*)(s_f + (size_t)max(P->npre, 1) * WG), nullptr);
+    float2 vyr[RY > 0 ? RY : 1];
+    if (RY > 0) {
+        const CS float2* aty = cs(P->aty);
+#pragma unroll
+        for (int iy = 0; iy < RY; ++iy) vyr[iy] = aty[iy];
+    }
+    if constexpr (NPRE > 0) {
+        const PrefixHead ph = prefix_head<NPRE, RAD>(P, b0, J->big, pat);
+        for (int g = 0; g < G; ++g)
+            sweep_block<HAS_S2, RY, NPRE, B256>(P, J, b0 + (uint64_t)g, live, prefix_tail<NPRE>(P, ph, g, pat), vyr,
+                                                s_bins, s_f);
+    } else {
+        const Prefix pf = prefix_eval<NPRE, false, RAD>(P, b0, J->big, s_f, pat, nullptr);
+        sweep_block<HAS_S2, RY, NPRE, B256>(P, J, b0, live, pf, vyr, s_bins, s_f);
     }
 }
 

@@ -645,3 +645,23 @@ def test_graph_replay_matches_eager_calls():
             assert plan.stats().main_ms > 0
         plan.set_option(D.DY_OPT_GRAPH, 0)
         assert_choices(plan.select(list(a), stream=stream())[0], want_a, "eager")
+
+
+@pytest.mark.parametrize("begin,count", [(0, 12 ** 8), (144 * 12, 144 * 1048584), (144 * 6, 144 * 1048580 + 77),
+                                         (144 * 7 + 5, 144 * 1048576 + 1000)])
+def test_library_sweep_block_runs(begin, count):
+    # the library sweep (DY_OPT_JIT 0) gives each thread a run of up to 12
+    # blocks that share the prefix but its last node, when the source's blocks
+    # align (runs of 12, 6, ..., else single blocks; ragged ends): the choices
+    # equal the generated sweep's, which the oracle pins on the same kind of
+    # ranges, and on the whole space the stored oracle selection
+    prob = wl.forkjoin8()
+    src = [D.range_source(0, begin, count)]
+    with D.Plan(prob) as plan:
+        plan.set_option(D.DY_OPT_JIT, 0)
+        lib = plan.select(src, stream=stream())[0]
+        plan.set_option(D.DY_OPT_JIT, 2)
+        gen = plan.select(src, stream=stream())[0]
+    assert_choices(lib, [tuple(c) for c in gen], f"forkjoin8 [{begin}+{count}] library vs generated sweep")
+    if (begin, count) == (0, 12 ** 8):
+        assert_choices(lib, golden("forkjoin8")[1], "forkjoin8 whole space, library sweep")
