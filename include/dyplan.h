@@ -219,10 +219,11 @@ enum {
                                    HIP graph of its launches (default 1; calls with DY_OPT_TIMING on
                                    launch directly); results are identical */
     DY_OPT_CLIMB = 7            /* local-search seeds: RANGE sources that cover the whole plan space of a
-                                   corr / SLO problem of at most 8 nodes also seed each level's threshold
-                                   from a local search over the plans (the sampling pass then thins out).
-                                   0: never; 1 (default): in calls of at least 128 such sources; 2: for
-                                   every such source.  Results are identical */
+                                   problem of at most 8 nodes also seed each level's threshold from a
+                                   local search over the plans (the sampling pass then thins out); under
+                                   the additive objective only when lambda_l and every lambda_ld L_k are
+                                   not negative.  0: never; 1 (default): in calls of at least 128 such
+                                   sources; 2: for every such source.  Results are identical */
 };
 
 /*

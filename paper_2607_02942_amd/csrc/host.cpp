@@ -29,7 +29,7 @@ hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, 
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
 hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_seed_cands(const JobDev* d_jobs, int njobs, int kmax, int nmax, hipStream_t s);
-hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s);
+hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, hipStream_t s);
 hipError_t static_scratch(int device, char** ptr, size_t* bytes);
 struct JitRows {
     hipModule_t mod = nullptr;
@@ -1433,13 +1433,13 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
                 src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_use(p) && h->jit[p].sweep)
                 jsw[j] = 1;
         }
-    // local-search seeds (whole-space RANGE sources of corr / SLO problems of at
-    // most kClimbNodes nodes): in calls of many such sources, where they replace
+    // local-search seeds (whole-space RANGE sources of problems of at most
+    // kClimbNodes nodes, either objective): in calls of many such sources, where they replace
     // most of the sampling and of the certification work; a call of a few
     // sources waits for the searches' latency instead (tens of microseconds)
     auto climb_ok = [&](int j) {
         const HostProb& H = h->hp[src[j].problem];
-        return !h->force_fp64 && !H.obj && H.n <= kClimbNodes && src[j].kind == DY_SOURCE_RANGE &&
+        return !h->force_fp64 && H.n <= kClimbNodes && src[j].kind == DY_SOURCE_RANGE &&
                src[j].begin == 0 && !H.plans_saturated && src[j].count == H.n_plans;
     };
     int n_climb = 0;
@@ -1521,13 +1521,13 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         jobs[q] = J;
     }
     const int n3 = pp.before(G_JIT);  // jobs of the other groups; JIT jobs follow
-    // library sweep of the corr / SLO groups with a compile-time prefix
-    // length: a source whose blocks are aligned runs of G (G dividing the
-    // last prefix node's radix, up to 12) gives each thread G blocks that
-    // share the prefix but its last node; only in groups of many blocks, so
-    // that the fewer threads still fill the device (batch6's 85 M blocks:
-    // sweep 1.61 -> 1.53 ms with runs of 12, 1.59 with runs of 4)
-    for (int g = G_SWEEP; g <= G_SWEEP_S2; ++g) {
+    // library sweep (both objectives) with a compile-time prefix length: a
+    // source whose blocks are aligned runs of G (G dividing the last prefix
+    // node's radix, up to 12) gives each thread G blocks that share the
+    // prefix but its last node; only in groups of many blocks, so that the
+    // fewer threads still fill the device (batch6's 85 M blocks: sweep 1.61
+    // -> 1.53 ms with runs of 12, 1.59 with runs of 4)
+    for (int g = 0; g < kSweepGroups; ++g) {
         const int npc = pp.npre_c[g];
         if (npc != 2 && npc != 4 && npc != 6 && npc != 8) continue;
         const int q0 = pp.before(g), q1 = pp.before(g) + pp.n[g] - pp.njit[g];
@@ -1553,7 +1553,12 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
     bool any_split = false;
     for (int q = n3; q < n3 + pp.n[G_JIT]; ++q) any_split = any_split || split_at(jobs[q]) != 0;
     bool any_climb = false;
-    for (int q = 0; q < n3; ++q) any_climb = any_climb || jobs[q].climb != 0;
+    int climb_modes = 0;  // bit 0: a corr / SLO source climbs, bit 1: an objective one
+    for (int q = 0; q < n3; ++q)
+        if (jobs[q].climb) {
+            any_climb = true;
+            climb_modes |= h->hdesc[(int)(jobs[q].prob - h->d_probs)].obj ? 2 : 1;
+        }
     // the job array is rebuilt every call but uploaded only when it changed
     const bool changed =
         stat || S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0;
@@ -1591,7 +1596,7 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         launch_seed(h, S.d_jobs, jobs.data(), pp, st, ck);
         if (any_climb)
             for (int c = 0; c < n3; c += 65535)
-                ck(launch_climb(S.d_jobs + c, std::min(65535, n3 - c), pp.kmax, st), "climb");
+                ck(launch_climb(S.d_jobs + c, std::min(65535, n3 - c), pp.kmax, climb_modes, st), "climb");
         jit_pass(jobs.data(), n3, pp.n[G_JIT], true, st, ck);
         launch_table_all(S.d_jobs, n_src, st, ck);
     };

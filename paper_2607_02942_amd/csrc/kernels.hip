@@ -557,18 +557,19 @@ __device__ __forceinline__ Prefix prefix_eval(PD P, uint64_t b, int big, float* 
 // the same order as prefix_eval, so the same values: the product takes the
 // last node's factor last, and the maxima are exact.
 struct PrefixHead {
-    float pc;      // product of the factors of nodes 0 .. NPRE-2
+    float pc;      // product of the factors of nodes 0 .. NPRE-2 (objective mode: sum of u)
+    float pd;      // objective mode: sum of d over nodes 0 .. NPRE-2
     float m;       // the last node's predecessor maximum
     float px, py, s;  // the maxima into x, into y and over the prefix sinks, nodes 0 .. NPRE-2
     uint32_t d;    // the last node's digit in b0
 };
 
-template <int NPRE, int RAD>
-__device__ __forceinline__ PrefixHead prefix_head(PD P, uint64_t b0, int big, const float2* s_pat) {
+template <int NPRE, bool OBJ, int RAD>
+__device__ __forceinline__ PrefixHead prefix_head(PD P, uint64_t b0, int big, const float2* s_pat, const float* s_pd) {
     static_assert(NPRE > 1, "a head and a last node");
     const int rmax = P->rmax;
     float f[NPRE - 1];
-    float pc = 1.0f;
+    float pc = OBJ ? 0.0f : 1.0f, pd = 0.0f;
     uint32_t dg[NPRE];
     if constexpr (RAD > 0) {
         uint32_t x = (uint32_t)b0;
@@ -584,7 +585,12 @@ __device__ __forceinline__ PrefixHead prefix_head(PD P, uint64_t b0, int big, co
 #pragma unroll
     for (int n = 0; n < NPRE - 1; ++n) {
         const float2 v = s_pat ? s_pat[n * rmax + dg[n]] : cs(P->at)[n * rmax + dg[n]];
-        pc = pc * v.x;
+        if (OBJ) {
+            pc = pc + v.x;
+            pd = pd + (s_pat ? s_pd[n * rmax + dg[n]] : cs(P->dem)[n * rmax + dg[n]]);
+        } else {
+            pc = pc * v.x;
+        }
         float m = 0.0f;
         const uint32_t pm = P->pred[n];
 #pragma unroll
@@ -605,21 +611,23 @@ __device__ __forceinline__ PrefixHead prefix_head(PD P, uint64_t b0, int big, co
         if (pmy >> u & 1u) py = fmaxf(py, f[u]);
         if (pms >> u & 1u) s = fmaxf(s, f[u]);
     }
-    return PrefixHead{pc, m, px, py, s, dg[NPRE - 1]};
+    return PrefixHead{pc, pd, m, px, py, s, dg[NPRE - 1]};
 }
 
-template <int NPRE>
-__device__ __forceinline__ Prefix prefix_tail(PD P, const PrefixHead& h, int g, const float2* s_pat) {
+template <int NPRE, bool OBJ>
+__device__ __forceinline__ Prefix prefix_tail(PD P, const PrefixHead& h, int g, const float2* s_pat,
+                                              const float* s_pd) {
     constexpr int n = NPRE - 1;
-    const uint32_t d = h.d + (uint32_t)g;
-    const float2 v = s_pat ? s_pat[n * P->rmax + d] : cs(P->at)[n * P->rmax + d];
+    const int e = n * P->rmax + (int)(h.d + (uint32_t)g);
+    const float2 v = s_pat ? s_pat[e] : cs(P->at)[e];
     const float fl = v.y + h.m;
     const int xn = P->xnode;
     const bool inx = xn >= 0 && (P->pred[xn] >> n & 1u);
     const bool iny = (P->pred[P->ynode] >> n & 1u) && n != xn;
     const bool ins = P->pre_sinks >> n & 1u;
-    return Prefix{h.pc * v.x, inx ? fmaxf(h.px, fl) : h.px, iny ? fmaxf(h.py, fl) : h.py,
-                  ins ? fmaxf(h.s, fl) : h.s, 0.0f};
+    const float pc = OBJ ? h.pc + v.x : h.pc * v.x;
+    const float pd = OBJ ? h.pd + (s_pat ? s_pd[e] : cs(P->dem)[e]) : 0.0f;
+    return Prefix{pc, inx ? fmaxf(h.px, fl) : h.px, iny ? fmaxf(h.py, fl) : h.py, ins ? fmaxf(h.s, fl) : h.s, pd};
 }
 
 // One plan of the inner sweep: corr = cx * a_y, CP = max(tau_y + M, S2); the
@@ -866,10 +874,10 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
         for (int iy = 0; iy < RY; ++iy) vyr[iy] = aty[iy];
     }
     if constexpr (NPRE > 0) {
-        const PrefixHead ph = prefix_head<NPRE, RAD>(P, b0, J->big, pat);
+        const PrefixHead ph = prefix_head<NPRE, false, RAD>(P, b0, J->big, pat, nullptr);
         for (int g = 0; g < G; ++g)
-            sweep_block<HAS_S2, RY, NPRE, B256>(P, J, b0 + (uint64_t)g, live, prefix_tail<NPRE>(P, ph, g, pat), vyr,
-                                                s_bins, s_f);
+            sweep_block<HAS_S2, RY, NPRE, B256>(P, J, b0 + (uint64_t)g, live, prefix_tail<NPRE, false>(P, ph, g, pat, nullptr),
+                                                vyr, s_bins, s_f);
     } else {
         const Prefix pf = prefix_eval<NPRE, false, RAD>(P, b0, J->big, s_f, pat, nullptr);
         sweep_block<HAS_S2, RY, NPRE, B256>(P, J, b0, live, pf, vyr, s_bins, s_f);
@@ -1012,12 +1020,15 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
 
 // ---------------------------------------------------------------------------
 // Local-search seeds (RANGE sources that cover their problem's whole plan
-// space, corr / SLO selection)
+// space)
 //
 // Any certainly-feasible plan gives a valid candidate threshold through its
 // fp32 corr, exactly as a sampled plan does, and the nearer that corr is to
 // the level's optimum, the fewer plans pass the prefilter and reach fp64
-// certification.  One wave per (source, level) climbs: it starts at the plan
+// certification.  Under the additive objective every plan is admissible and
+// any plan's fp32 estimate of J_k (computed as the sweep computes it) gives a
+// valid threshold; the search then climbs that estimate from the plan that
+// gives every node its best entry by u - lambda_l tau - lambda_ld L_k d.  One wave per (source, level) climbs: it starts at the plan
 // that gives every node its fastest implementation at the level (the least
 // CP of all plans: the longest path is monotone in every duration, in fp32
 // too) and, while some plan that differs from the current one in one node --
@@ -1068,6 +1079,36 @@ __device__ __forceinline__ void climb_eval(PD P, int N, const float (&a)[NN], co
     }
 }
 
+// Objective mode: the fp32 estimate of J_k of the same plan, in the sweep's
+// operations and order: U and D summed in node order, T the longest path,
+// G = fma(-lambda_l, T, U), estimate = fma(-m_k, D, G).
+template <int NN>
+__device__ __forceinline__ float climb_est(PD P, int N, const float (&u)[NN], const float (&t)[NN],
+                                           const float (&d)[NN], int n1, float u1, float t1, float d1, int n2,
+                                           float u2, float t2, float d2, float m) {
+    float f[NN];
+    float U = 0.0f, D = 0.0f, T = 0.0f;
+#pragma unroll
+    for (int n = 0; n < NN; ++n) {
+        f[n] = 0.0f;
+        if (n < N) {
+            const float un = n == n1 ? u1 : (n == n2 ? u2 : u[n]);
+            const float tn = n == n1 ? t1 : (n == n2 ? t2 : t[n]);
+            const float dn = n == n1 ? d1 : (n == n2 ? d2 : d[n]);
+            U = U + un;
+            D = D + dn;
+            float mx = 0.0f;
+            const uint32_t pm = P->pred[n];
+#pragma unroll
+            for (int v = 0; v < n; ++v)
+                if (pm >> v & 1u) mx = fmaxf(mx, f[v]);
+            f[n] = tn + mx;
+            if (P->sinks >> n & 1u) T = fmaxf(T, f[n]);
+        }
+    }
+    return fmaf(-m, D, fmaf(-P->lam_l, T, U));
+}
+
 // One wave per (source, level): grid (levels, sources), 64 threads.  The
 // current plan is held by every lane in registers; each lane evaluates a
 // share of the moves, a wave reduction picks the best.  Moves only use each
@@ -1078,9 +1119,10 @@ __device__ __forceinline__ void climb_eval(PD P, int N, const float (&a)[NN], co
 // The block has blockDim.x = 64 W threads (W waves): few (source, level)
 // pairs take W = 16, so that each move pass is one short round (the pass is
 // latency-bound), many take W = 1.
-template <int NN>
+template <int NN, bool OBJ>
 __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs) {
     __shared__ float s_a[CLIMB_ENTRIES], s_t[CLIMB_ENTRIES];  // node tables, entry off[n] + i
+    __shared__ float s_d[OBJ ? CLIMB_ENTRIES : 1];             // objective mode: d
     __shared__ uint8_t s_node[CLIMB_ENTRIES];                 // node of entry e
     __shared__ uint8_t s_keep[CLIMB_ENTRIES];                 // entry e is Pareto-optimal at the level
     __shared__ int16_t s_fe[CLIMB_ENTRIES];                   // the kept entries, node by node
@@ -1092,8 +1134,12 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
     PD P = cs(J->prob);
     const int k = blockIdx.x;
     const int N = P->n, R = P->rmax, lane = threadIdx.x & 63, tid = threadIdx.x, nt = blockDim.x;
-    if (k >= P->k || P->obj || N > NN) return;
-    const bool uni = P->uniform != 0;
+    if (k >= P->k || (P->obj != 0) != OBJ || N > NN) return;
+    // objective mode: a greater u and a smaller tau and d never lower J_k
+    // only when lambda_l and lambda_ld L_k are not negative
+    const float mk = OBJ ? P->m32[k] : 0.0f;
+    if (OBJ && (!(P->lam_l >= 0.0f) || !(mk >= 0.0f))) return;
+    const bool uni = OBJ || P->uniform != 0;
     // durations the band is tested on: the unpressured ones against lo_k
     // (uniform pressure), else the level's own against the exact band
     const CS float2* at = cs(P->at);
@@ -1113,6 +1159,7 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
             const float2 v = at[n * R + i];
             s_a[off[n] + i] = v.x;
             s_t[off[n] + i] = uni ? v.y : lt[n * R + i];
+            if (OBJ) s_d[off[n] + i] = cs(P->dem)[n * R + i];
             s_node[off[n] + i] = (uint8_t)n;
         }
     __syncthreads();
@@ -1125,11 +1172,11 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
                 lo = off[m];
                 hi = off[m + 1];
             }
-        const float a = s_a[e], t = s_t[e];
+        const float a = s_a[e], t = s_t[e], d = OBJ ? s_d[e] : 0.0f;
         bool keep = true;
         for (int q = lo; q < hi && keep; ++q) {
-            const float a2 = s_a[q], t2 = s_t[q];
-            if (q != e && a2 >= a && t2 <= t && (a2 > a || t2 < t || q < e)) keep = false;
+            const float a2 = s_a[q], t2 = s_t[q], d2 = OBJ ? s_d[q] : 0.0f;
+            if (q != e && a2 >= a && t2 <= t && d2 <= d && (a2 > a || t2 < t || d2 < d || q < e)) keep = false;
         }
         s_keep[e] = keep ? 1 : 0;
     }
@@ -1152,28 +1199,41 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
     }
     foff[NN] = ftot;
     __syncthreads();
-    // start: every node's fastest kept implementation (the fastest of all)
+    // start: every node's fastest kept implementation (the fastest of all);
+    // objective mode: every node's best kept entry by u - lambda_l tau - m_k d
     int cur[NN];
-    float ca[NN], ct[NN];
+    float ca[NN], ct[NN], cd[NN];
 #pragma unroll
     for (int n = 0; n < NN; ++n) {
         cur[n] = 0;
-        ca[n] = 1.0f;
+        ca[n] = OBJ ? 0.0f : 1.0f;
         ct[n] = 0.0f;
+        cd[n] = 0.0f;
         if (n < N) {
-            float best = INFINITY;
-            for (int f = foff[n]; f < foff[n + 1]; ++f)
-                if (s_t[s_fe[f]] < best) {
-                    best = s_t[s_fe[f]];
-                    cur[n] = s_fe[f] - off[n];
+            float best = OBJ ? -INFINITY : INFINITY;
+            for (int f = foff[n]; f < foff[n + 1]; ++f) {
+                const int e = s_fe[f];
+                const float sc = OBJ ? s_a[e] - P->lam_l * s_t[e] - mk * s_d[e] : s_t[e];
+                if (OBJ ? sc > best : sc < best) {
+                    best = sc;
+                    cur[n] = e - off[n];
                 }
+            }
             ca[n] = s_a[off[n] + cur[n]];
-            ct[n] = best;
+            ct[n] = s_t[off[n] + cur[n]];
+            if (OBJ) cd[n] = s_d[off[n] + cur[n]];
         }
     }
-    float cc, ccp;
-    climb_eval<NN>(P, N, ca, ct, -1, 0.0f, 0.0f, -1, 0.0f, 0.0f, cc, ccp);
-    if (!(ccp <= band)) return;  // no plan is certainly feasible at this level
+    float cc, ccp = 0.0f;
+    if (OBJ) {
+        cc = climb_est<NN>(P, N, ca, ct, cd, -1, 0.0f, 0.0f, 0.0f, -1, 0.0f, 0.0f, 0.0f, mk);
+    } else {
+        climb_eval<NN>(P, N, ca, ct, -1, 0.0f, 0.0f, -1, 0.0f, 0.0f, cc, ccp);
+        if (!(ccp <= band)) return;  // no plan is certainly feasible at this level
+    }
+    // move keys order by the value: corr bits (non-negative), or the
+    // order-preserving key of the estimate
+    auto vkey = [&](float v) -> uint32_t { return OBJ ? fkey(v) : __float_as_uint(v); };
     uint32_t pairs = 0;
 #pragma unroll
     for (int n = 0; n < NN; ++n)
@@ -1221,10 +1281,13 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
                     on = off[m];
                 }
             if (e - on == cn) continue;
-            float c, cp;
-            climb_eval<NN>(P, N, ca, ct, n, s_a[e], s_t[e], -1, 0.0f, 0.0f, c, cp);
-            if (c > cc && cp <= band) {
-                const uint64_t key = (uint64_t)__float_as_uint(c) << 32 | (uint32_t)(0xffffffffu - (uint32_t)e);
+            float c, cp = 0.0f;
+            if (OBJ)
+                c = climb_est<NN>(P, N, ca, ct, cd, n, s_a[e], s_t[e], s_d[e], -1, 0.0f, 0.0f, 0.0f, mk);
+            else
+                climb_eval<NN>(P, N, ca, ct, n, s_a[e], s_t[e], -1, 0.0f, 0.0f, c, cp);
+            if (c > cc && (OBJ || cp <= band)) {
+                const uint64_t key = (uint64_t)vkey(c) << 32 | (uint32_t)(0xffffffffu - (uint32_t)e);
                 best = key > best ? key : best;
             }
         }
@@ -1260,12 +1323,16 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
                 const int j2 = x - j1 * F2;
                 const int e1 = s_fe[f1 + j1], e2 = s_fe[f2 + j2];
                 if (e1 - o1 == c1 || e2 - o2 == c2) continue;
-                if (!(s_a[e1] * s_a[e2] > s_a[o1 + c1] * s_a[o2 + c2])) continue;  // cannot raise corr
-                float c, cp;
-                climb_eval<NN>(P, N, ca, ct, n1, s_a[e1], s_t[e1], n2, s_a[e2], s_t[e2], c, cp);
-                if (c > cc && cp <= band) {
+                if (!OBJ && !(s_a[e1] * s_a[e2] > s_a[o1 + c1] * s_a[o2 + c2])) continue;  // cannot raise corr
+                float c, cp = 0.0f;
+                if (OBJ)
+                    c = climb_est<NN>(P, N, ca, ct, cd, n1, s_a[e1], s_t[e1], s_d[e1], n2, s_a[e2], s_t[e2], s_d[e2],
+                                      mk);
+                else
+                    climb_eval<NN>(P, N, ca, ct, n1, s_a[e1], s_t[e1], n2, s_a[e2], s_t[e2], c, cp);
+                if (c > cc && (OBJ || cp <= band)) {
                     const uint32_t id = (uint32_t)(n1 * NMAX + n2) << 16 | (uint32_t)(e1 - o1) << 8 | (uint32_t)(e2 - o2);
-                    const uint64_t key = (uint64_t)__float_as_uint(c) << 32 | (uint32_t)(0xffffffffu - id);
+                    const uint64_t key = (uint64_t)vkey(c) << 32 | (uint32_t)(0xffffffffu - id);
                     best = key > best ? key : best;
                 }
             }
@@ -1275,7 +1342,7 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
         if (mv == 0) break;
         // every lane applies the move to its copy of the plan
         const uint32_t id = 0xffffffffu - (uint32_t)mv;
-        cc = __uint_as_float((uint32_t)(mv >> 32));
+        cc = OBJ ? fkey_value((uint32_t)(mv >> 32)) : __uint_as_float((uint32_t)(mv >> 32));
         int mn1, mi1, mn2 = -1, mi2 = 0;
         if (pair) {
             mn1 = (int)(id >> 16) / NMAX;
@@ -1296,10 +1363,12 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
                 cur[m] = m == mn1 ? mi1 : mi2;
                 ca[m] = s_a[off[m] + cur[m]];
                 ct[m] = s_t[off[m] + cur[m]];
+                if (OBJ) cd[m] = s_d[off[m] + cur[m]];
             }
         }
     }
-    if (tid == 0) atomicMax(J->scert + k * NSLOT, __float_as_uint(cc) + 1u);
+    // the seed slot's format: corr bits + 1, or the estimate's key
+    if (tid == 0) atomicMax(J->scert + k * NSLOT, OBJ ? fkey(cc) : __float_as_uint(cc) + 1u);
 }
 
 // ---------------------------------------------------------------------------
@@ -1321,33 +1390,20 @@ __device__ __forceinline__ ObjPlan obj_plan(const float2 vy, float dy, float M, 
     return ObjPlan{fmaf(nl, T, ux + vy.x), dx + dy};
 }
 
-template <bool HAS_S2>
+template <bool HAS_S2, bool B256 = false>
 __device__ __forceinline__ uint64_t sweep_test_obj(const float2 vy, float dy, float M, float S2, float ux, float dx,
                                                    float nl, uint32_t sh, const float* s_bins) {
     const ObjPlan q = obj_plan<HAS_S2>(vy, dy, M, S2, ux, dx, nl);
-    const uint32_t off = (__float_as_uint(q.D) >> sh) & 0xfcu;
+    const uint32_t off = B256 ? (__float_as_uint(q.D) >> 16) & 0x3fcu : (__float_as_uint(q.D) >> sh) & 0xfcu;
     const float thr = *(const float*)((const char*)s_bins + off);
     return __ballot(q.G >= thr);
 }
 
-template <bool HAS_S2, int RY, int NPRE>
-__global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ jobs, uint64_t unit_off) {
-    extern __shared__ float s_f[];
-    JD J = cs(jobs + blockIdx.y);
-    PD P = cs(J->prob);
-    const uint64_t nblk = J->nblk;
-    const uint64_t t0 = unit_off + (uint64_t)blockIdx.x * WG;
-    if (t0 >= nblk) return;
-    const uint64_t t = t0 + threadIdx.x;
-    const bool live = t < nblk;
-    const uint64_t b = J->blk_first + (live ? t : nblk - 1);
-    __shared__ float s_bins[NBINS];
-    if (threadIdx.x < NBINS) s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
-    float2* s_pat = (float2*)(s_f + (size_t)max(P->npre, 1) * WG);
-    float* s_pd = (float*)(s_pat + PAT_MAX);
-    const float2* pat = stage_prefix_rows<true>(P, s_pat, s_pd);
-    const Prefix pf = prefix_eval<NPRE, true>(P, b, J->big, s_f, pat, s_pd);
-
+// The objective-mode inner sweep of block b (the prefix pf evaluated).
+template <bool HAS_S2, int RY, bool B256>
+__device__ __forceinline__ void sweep_block_obj(PD P, JD J, uint64_t b, bool live, const Prefix& pf,
+                                                const float2 (&vyr)[RY > 0 ? RY : 1],
+                                                const float (&dyr)[RY > 0 ? RY : 1], const float* s_bins) {
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* atx = cs(P->atx);
     const CS float2* aty = cs(P->aty);
@@ -1356,16 +1412,6 @@ __global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ job
     const int rx = P->rx, ry = P->ry;
     const bool exy = P->edge_xy != 0;
     const float nl = -P->lam_l;
-
-    float2 vyr[RY > 0 ? RY : 1];
-    float dyr[RY > 0 ? RY : 1];
-    if (RY > 0) {
-#pragma unroll
-        for (int iy = 0; iy < RY; ++iy) {
-            vyr[iy] = aty[iy];
-            dyr[iy] = dyt[iy];
-        }
-    }
     for (int ix = 0; ix < rx; ++ix) {
         const float2 vx = atx[ix];
         const float fx = vx.y + pf.px;
@@ -1378,18 +1424,18 @@ __global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ job
         if (RY > 0) {
 #pragma unroll
             for (int j = 0; j < (RY > 0 ? RY : 1); ++j)
-                hit |= sweep_test_obj<HAS_S2>(vyr[j], dyr[j], M, S2, ux, dx, nl, sh, s_bins);
+                hit |= sweep_test_obj<HAS_S2, B256>(vyr[j], dyr[j], M, S2, ux, dx, nl, sh, s_bins);
             iy = ry;
         }
         for (; iy + 4 <= ry; iy += 4) {
             const float2 v0 = aty[iy], v1 = aty[iy + 1], v2 = aty[iy + 2], v3 = aty[iy + 3];
             const float d0 = dyt[iy], d1 = dyt[iy + 1], d2 = dyt[iy + 2], d3 = dyt[iy + 3];
-            hit |= sweep_test_obj<HAS_S2>(v0, d0, M, S2, ux, dx, nl, sh, s_bins);
-            hit |= sweep_test_obj<HAS_S2>(v1, d1, M, S2, ux, dx, nl, sh, s_bins);
-            hit |= sweep_test_obj<HAS_S2>(v2, d2, M, S2, ux, dx, nl, sh, s_bins);
-            hit |= sweep_test_obj<HAS_S2>(v3, d3, M, S2, ux, dx, nl, sh, s_bins);
+            hit |= sweep_test_obj<HAS_S2, B256>(v0, d0, M, S2, ux, dx, nl, sh, s_bins);
+            hit |= sweep_test_obj<HAS_S2, B256>(v1, d1, M, S2, ux, dx, nl, sh, s_bins);
+            hit |= sweep_test_obj<HAS_S2, B256>(v2, d2, M, S2, ux, dx, nl, sh, s_bins);
+            hit |= sweep_test_obj<HAS_S2, B256>(v3, d3, M, S2, ux, dx, nl, sh, s_bins);
         }
-        for (; iy < ry; ++iy) hit |= sweep_test_obj<HAS_S2>(aty[iy], dyt[iy], M, S2, ux, dx, nl, sh, s_bins);
+        for (; iy < ry; ++iy) hit |= sweep_test_obj<HAS_S2, B256>(aty[iy], dyt[iy], M, S2, ux, dx, nl, sh, s_bins);
         if (hit) {
             // rare: re-score this lane's row with the exact per-level test
             const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
@@ -1401,6 +1447,52 @@ __global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ job
                 }
             }
         }
+    }
+}
+
+// Work units as in k_sweep (runs of J->gblk blocks per thread with NPRE > 0);
+// B256: the 256 bins of D's pattern on shift 18 (one AND per plan).
+template <bool HAS_S2, int RY, int NPRE, bool B256 = false, int RAD = 0>
+__global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ jobs, uint64_t unit_off) {
+    extern __shared__ float s_f[];
+    JD J = cs(jobs + blockIdx.y);
+    PD P = cs(J->prob);
+    const uint64_t units = J->units;
+    const int G = NPRE > 0 ? J->gblk : 1;
+    const uint64_t t0 = unit_off + (uint64_t)blockIdx.x * WG;
+    if (t0 >= units) return;
+    const uint64_t t = t0 + threadIdx.x;
+    const bool live = t < units;
+    const uint64_t b0 = J->blk_first + (live ? t : units - 1) * (uint64_t)G;
+    __shared__ float s_bins[B256 ? NBINS2 : NBINS];
+    if (B256) {
+        s_bins[threadIdx.x] = __uint_as_float(J->table2[threadIdx.x]);
+        static_assert(!B256 || NBINS2 == WG, "one bin per thread");
+    } else if (threadIdx.x < NBINS) {
+        s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
+    }
+    float2* s_pat = (float2*)(s_f + (size_t)max(P->npre, 1) * WG);
+    float* s_pd = (float*)(s_pat + PAT_MAX);
+    const float2* pat = stage_prefix_rows<true>(P, s_pat, s_pd);
+    float2 vyr[RY > 0 ? RY : 1];
+    float dyr[RY > 0 ? RY : 1];
+    if (RY > 0) {
+        const CS float2* aty = cs(P->aty);
+        const CS float* dyt = cs(P->demy);
+#pragma unroll
+        for (int iy = 0; iy < RY; ++iy) {
+            vyr[iy] = aty[iy];
+            dyr[iy] = dyt[iy];
+        }
+    }
+    if constexpr (NPRE > 0) {
+        const PrefixHead ph = prefix_head<NPRE, true, RAD>(P, b0, J->big, pat, s_pd);
+        for (int g = 0; g < G; ++g)
+            sweep_block_obj<HAS_S2, RY, B256>(P, J, b0 + (uint64_t)g, live,
+                                              prefix_tail<NPRE, true>(P, ph, g, pat, s_pd), vyr, dyr, s_bins);
+    } else {
+        const Prefix pf = prefix_eval<NPRE, true>(P, b0, J->big, s_f, pat, s_pd);
+        sweep_block_obj<HAS_S2, RY, B256>(P, J, b0, live, pf, vyr, dyr, s_bins);
     }
 }
 
@@ -2617,11 +2709,15 @@ hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s) {
 }
 
 // Problems above CLIMB_NODES nodes take no climb (the kernel returns for them).
-hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, hipStream_t s) {
+// modes: bit 0 sources of corr / SLO problems climb, bit 1 of objective ones
+hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, hipStream_t s) {
     if (njobs == 0) return hipSuccess;
     // few (source, level) pairs: 16 waves each (latency); many: one wave each
     const int threads = (size_t)njobs * (size_t)kmax <= 1024 ? 1024 : 64;
-    hipLaunchKernelGGL(k_climb<CLIMB_NODES>, dim3(kmax, njobs), dim3(threads), 0, s, d_jobs);
+    if (modes & 1) hipLaunchKernelGGL((k_climb<CLIMB_NODES, false>), dim3(kmax, njobs), dim3(threads), 0, s, d_jobs);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !(modes & 2)) return e;
+    hipLaunchKernelGGL((k_climb<CLIMB_NODES, true>), dim3(kmax, njobs), dim3(threads), 0, s, d_jobs);
     return hipGetLastError();
 }
 
@@ -2677,7 +2773,12 @@ hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint
         const dim3 grid((uint32_t)gx, n);
 #define DYP_SWEEP(S2, RYV, NP)                                                                             \
     do {                                                                                                   \
-        if (obj)                                                                                           \
+        if (obj && b256 && rad12 && RYV == 12 && NP > 0)                                                   \
+            hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP, true, (RYV == 12 && NP > 0) ? 12 : 0>), grid, dim3(WG), \
+                               lds, s, d_jobs, off);                                                       \
+        else if (obj && b256)                                                                              \
+            hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP, true, 0>), grid, dim3(WG), lds, s, d_jobs, off);  \
+        else if (obj)                                                                                      \
             hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off);          \
         else if (b256 && rad12 && RYV == 12 && NP > 0)                                                     \
             hipLaunchKernelGGL((k_sweep<S2, RYV, NP, true, (RYV == 12 && NP > 0) ? 12 : 0>), grid, dim3(WG), lds, \

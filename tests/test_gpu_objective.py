@@ -10,6 +10,8 @@ over LLM nodes of the largest |u| + lambda_l T + lambda_ld L_k D (the derived
 bound is (N + 6) 2^-24 A_k <= 2.2e-6 A_k at N <= 32); U and D likewise.
 """
 import dataclasses
+import json
+import os
 
 import numpy as np
 import pytest
@@ -392,3 +394,71 @@ def test_score_odd_levels_unaligned_output():
     U, T, Dd, J = orc.obj_score(prob, obj, begin, cnt)
     check_scores(prob, obj, U, T, Dd, J, u.cpu().numpy(), j.cpu().numpy(), d.cpu().numpy(),
                  f.cpu().numpy().astype(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# local-search seeds under the objective
+# ---------------------------------------------------------------------------
+
+def _climb_select(prob, obj, total, climb):
+    with D.Plan((prob, obj)) as plan:
+        plan.set_option(D.DY_OPT_CLIMB, climb)
+        got = plan.select([D.range_source(0, 0, total)], stream=stream())[0]
+        return got, plan.stats().candidates
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_climb_small_dags_full_space(seed):
+    # DY_OPT_CLIMB 2: every whole-space source of at most 8 nodes seeds each
+    # level from a local search on the fp32 estimate of J_k; the choices equal
+    # the oracle's with and without it and the candidate list never grows.
+    # Seed 5 has lambda_l = 0 (the longest path does not count).
+    rng = np.random.default_rng(700 + seed)
+    n = int(rng.integers(2, 9))
+    radix = [int(x) for x in rng.integers(1, 7, n)]
+    prob = small_dag(n, radix, 900 + seed)
+    obj = wl.Objective(cost=(prob.tau * prob.size).astype(np.float32),
+                       levels=np.sort(rng.uniform(0, 4, 1 + seed % 4)).astype(np.float32),
+                       lambda_f=float(rng.uniform(-1, 2)), lambda_c=float(rng.uniform(-0.1, 0.2)),
+                       lambda_l=float(rng.uniform(0, 0.5)) if seed != 5 else 0.0,
+                       lambda_ld=float(rng.uniform(0, 0.3)),
+                       beta=float(rng.uniform(-1, 2)), effort=float(rng.uniform(0, 1)),
+                       is_tool=(rng.random(n) < 0.3).astype(np.int32))
+    total = int(np.prod(radix))
+    want = orc.obj_select_range(prob, obj, 0, total)
+    off, c_off = _climb_select(prob, obj, total, 0)
+    on, c_on = _climb_select(prob, obj, total, 2)
+    assert_obj_choices(off, want, f"dag{n} no climb")
+    assert_obj_choices(on, want, f"dag{n} climb")
+    assert c_on <= c_off, (c_on, c_off)
+
+
+def test_climb_batch6_objective_golden():
+    # 256 of batch6's requests under J_L, with and without the local search,
+    # against the stored oracle selections; a call mixing both objectives
+    # launches both searches
+    path = os.path.join(os.path.dirname(__file__), "golden", "select_batch6_objective.json")
+    want = [[(c[0], c[1], float(c[2]), float(c[3]), float(c[4])) for c in ch] for ch in json.load(open(path))["choices"]]
+    nreq = 256
+    probs = wl.batch6(nreq)
+    items = [(p, wl.paper_objective(p)) for p in probs]
+    srcs = [D.range_source(r, 0, 12 ** 6) for r in range(nreq)]
+    res = {}
+    for climb in (0, 2):
+        with D.Plan(items) as plan:
+            plan.set_option(D.DY_OPT_CLIMB, climb)
+            res[climb] = (plan.select(srcs, stream=stream()), plan.stats().candidates)
+    for r in range(nreq):
+        for climb in (0, 2):
+            assert_obj_choices(res[climb][0][r], want[r], f"batch6 objective [{r}], climb {climb}")
+    assert res[2][1] < res[0][1], (res[2][1], res[0][1])
+    mixed = [probs[0], items[1], probs[2], items[3]]
+    with D.Plan(mixed) as plan:
+        plan.set_option(D.DY_OPT_CLIMB, 2)
+        got = plan.select(srcs[:4], stream=stream())
+    for r in (1, 3):
+        assert_obj_choices(got[r], want[r], f"mixed [{r}]")
+    for r in (0, 2):
+        oc = orc.select_range(probs[r], 0, 12 ** 6)
+        for g, w in zip(got[r], oc):
+            assert (g[0], g[1]) == (int(w[0]), int(w[1])), f"mixed corr [{r}]"
