@@ -291,10 +291,10 @@ int dy_plan_score(dy_plan* h, const dy_source* src, float* corr, float* cp, floa
 
 /*
  * The HIP source of the kernels the library generates for one problem and
- * compiles at run time with hiprtc (the streamed-rows kernels, and for DAGs
- * of at least three nodes the range sweep and, for uniform pressure or the
- * objective, the per-plan score kernels), with the problem's structure and
- * constants written in.  Host-only (no HIP call): for inspection and offline
+ * compiles at run time with hiprtc (the streamed-rows kernels and, for
+ * uniform pressure or the objective, their per-plan score kernel; for DAGs
+ * of at least three nodes the range sweep and its seeding pass), with the
+ * problem's structure and constants written in.  Host-only (no HIP call): for inspection and offline
  * compilation.  Writes at most cap bytes, NUL-terminated when cap > 0, and
  * sets *len to the full length without the NUL.  Returns dy_plan_create's
  * status for an invalid problem (message in dy_plan_last_error(NULL)).

@@ -353,6 +353,55 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace
 
+// The kernel family that scores a source.
+// Sources of one call are launched in groups: the prefix-shared sweep (RANGE,
+// uniform pressure; with or without a second sink term; corr / SLO or the
+// additive objective), the generic per-plan path, and the generated rows kernels.
+enum Group { G_SWEEP = 0, G_SWEEP_S2 = 1, G_OSWEEP = 2, G_OSWEEP_S2 = 3, G_GENERIC = 4, G_JIT = 5 };
+constexpr int kGroups = 6, kSweepGroups = 4;
+
+struct PassPlan {
+    int n[kGroups] = {};                  // sources per group, stored in group order
+    uint64_t units[G_JIT] = {};           // largest main-pass work of the group
+    uint64_t samples[G_JIT] = {};         // largest seeding-pass work of the group
+    int npre[kSweepGroups] = {};
+    int ry[kSweepGroups] = {};            // R_y shared by every source of a sweep group, else -1
+    int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
+    int njit[kSweepGroups] = {};          // trailing sources of the group that run their generated sweep
+    bool b256[kSweepGroups] = {true, true, true, true};  // every library-sweep source has the 256-bin table
+    bool rad12[kSweepGroups] = {true, true, true, true}; // ... and 12 implementations per prefix node, 32-bit blocks
+    int kmax = 1;                         // most levels of any source
+    int ncol = 1;                         // most nodes of any source of the generic group
+    int before(int g) const {             // jobs stored ahead of group g
+        int t = 0;
+        for (int q = 0; q < g; ++q) t += n[q];
+        return t;
+    }
+};
+
+// What a selection call derives from its sources and the handle's state
+// before launching: the group of every source, the launch order, the job
+// array and the launch plan.  A call whose sources and state equal the
+// previous call's reuses it (for 4,096 sources deriving it takes about 130
+// microseconds of host time, during which the device would wait).
+struct CallPlan {
+    bool valid = false;
+    // the key: sources, candidate slots, scratch, options, generated-kernel states
+    std::vector<dy_source> src;
+    uint64_t cap = 0;
+    const void* scratch = nullptr;
+    int64_t opts[6] = {};
+    std::vector<int> jit_state;
+    // the derived plan
+    std::vector<int> grp, order;
+    std::vector<JobDev> jobs;
+    PassPlan pp;
+    int n3 = 0;
+    uint64_t plans = 0, all_units = 0;
+    bool any_split = false, any_climb = false;
+    int climb_modes = 0;
+};
+
 struct dy_plan {
     int device = 0;
     int kmax = 0;
@@ -384,6 +433,7 @@ struct dy_plan {
     int use_graph = 1;
     hipStream_t cap_stream = nullptr;
     hipGraphExec_t graph = nullptr;
+    CallPlan call;                    // the last dy_plan_select call's plan
     dy_stats stats{};
     std::string err;
 };
@@ -1143,31 +1193,6 @@ int dy_plan_get_stats(const dy_plan* h, dy_stats* out) {
 
 namespace {
 
-// The kernel family that scores a source.
-// Sources of one call are launched in groups: the prefix-shared sweep (RANGE,
-// uniform pressure; with or without a second sink term; corr / SLO or the
-// additive objective), the generic per-plan path, and the generated rows kernels.
-enum Group { G_SWEEP = 0, G_SWEEP_S2 = 1, G_OSWEEP = 2, G_OSWEEP_S2 = 3, G_GENERIC = 4, G_JIT = 5 };
-constexpr int kGroups = 6, kSweepGroups = 4;
-
-struct PassPlan {
-    int n[kGroups] = {};                  // sources per group, stored in group order
-    uint64_t units[G_JIT] = {};           // largest main-pass work of the group
-    uint64_t samples[G_JIT] = {};         // largest seeding-pass work of the group
-    int npre[kSweepGroups] = {};
-    int ry[kSweepGroups] = {};            // R_y shared by every source of a sweep group, else -1
-    int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
-    int njit[kSweepGroups] = {};          // trailing sources of the group that run their generated sweep
-    bool b256[kSweepGroups] = {true, true, true, true};  // every library-sweep source has the 256-bin table
-    bool rad12[kSweepGroups] = {true, true, true, true}; // ... and 12 implementations per prefix node, 32-bit blocks
-    int kmax = 1;                         // most levels of any source
-    int ncol = 1;                         // most nodes of any source of the generic group
-    int before(int g) const {             // jobs stored ahead of group g
-        int t = 0;
-        for (int q = 0; q < g; ++q) t += n[q];
-        return t;
-    }
-};
 
 // Rows sources run the problem's generated
 // kernels (one launch per source; the host copies of the job carry the args).
@@ -1409,159 +1434,191 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
     const int km = h->kmax;
     const int cert_waves = n_src <= 64 ? CERT_WAVES : 1;
 
-    std::vector<int> grp(n_src);
-    for (int j = 0; j < n_src; ++j) {
-        const int p = src[j].problem;
-        const HostProb& H = h->hp[p];
-        if (src[j].kind == DY_SOURCE_RANGE)
-            grp[j] = H.obj ? (H.has_s2 ? G_OSWEEP_S2 : G_OSWEEP) : (H.has_s2 ? G_SWEEP_S2 : G_SWEEP);
-        else if (src[j].kind == DY_SOURCE_ROWS && !h->force_fp64 && jit_use(p))
-            grp[j] = G_JIT;
-        else
-            grp[j] = G_GENERIC;
-    }
-    // RANGE sources of 32-bit plan indices run the sweep generated for their DAG, when the plan has few
-    // problems (one compilation each), the source is large enough to repay
-    // it (2^24 plans; every source with DY_OPT_JIT 2) and it compiles; they
-    // go last in their group, whose library sweep launch covers the others
-    std::vector<char> jsw(n_src, 0);
-    const uint64_t jit_min = h->use_jit >= 2 ? 1 : (1ull << 24);
-    if (h->use_jit && !h->force_fp64 && h->hp.size() <= 8)
-        for (int j = 0; j < n_src; ++j) {
-            const int p = src[j].problem;
-            if (src[j].kind == DY_SOURCE_RANGE && src[j].count >= jit_min &&
-                src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_use(p) && h->jit[p].sweep)
-                jsw[j] = 1;
-        }
-    // local-search seeds (whole-space RANGE sources of problems of at most
-    // kClimbNodes nodes, either objective): in calls of many such sources, where they replace
-    // most of the sampling and of the certification work; a call of a few
-    // sources waits for the searches' latency instead (tens of microseconds)
-    auto climb_ok = [&](int j) {
-        const HostProb& H = h->hp[src[j].problem];
-        return !h->force_fp64 && H.n <= kClimbNodes && src[j].kind == DY_SOURCE_RANGE &&
-               src[j].begin == 0 && !H.plans_saturated && src[j].count == H.n_plans;
-    };
-    int n_climb = 0;
-    for (int j = 0; j < n_src; ++j) n_climb += climb_ok(j) ? 1 : 0;
-    const bool climb = h->use_climb == 2 || (h->use_climb == 1 && n_climb >= kClimbMinSources);
-    std::vector<int> order;
-    order.reserve(n_src);
-    for (int g = 0; g < kGroups; ++g)
-        for (int pass = 0; pass < 2; ++pass)
-            for (int j = 0; j < n_src; ++j)
-                if (grp[j] == g && jsw[j] == pass) order.push_back(j);
-    uint64_t plans = 0, all_units = 0;
-    PassPlan pp;
-    std::vector<JobDev> jobs((size_t)n_src);
-    for (int q = 0; q < n_src; ++q) {
-        const int j = order[q];
-        const int g = grp[j];
-        const HostProb& H = h->hp[src[j].problem];
-        JobDev J = make_job(h, src[j]);
-        J.cap = (uint32_t)cap;
-        J.scert = S.scert + (size_t)q * KMAX * NSLOT;
-        J.thr = S.thr + (size_t)q * KMAX;
-        J.table = S.table + (size_t)q * NBINS;
-        J.table2 = S.table2 + (size_t)q * NBINS2;
-        J.cand = S.cand + (size_t)q * cap;
-        J.ncand = S.ncand + q;
-        J.flags = S.flags + q;
-        J.out = S.out + (size_t)j * km;
-        if (n_src <= kDirectResults && !stat) {  // few sources: certification writes the host copy directly
-            J.hout = (dy_choice*)S.d_hres + (size_t)j * km;
-            J.hncand = (uint32_t*)(S.d_hres + S.res_ncand_off) + q;
-            J.hflags = (int32_t*)(S.d_hres + S.res_flags_off) + q;
-            J.hdone = S.d_done + q;
-        }
-        J.fb_corr = S.fb_corr + (size_t)q * KMAX;
-        J.fb_index = S.fb_index + (size_t)q * KMAX;
-        J.cert_waves = cert_waves;
-        J.cert_c = S.cert_c + (size_t)q * KMAX * CERT_WAVES;
-        J.cert_i = S.cert_i + (size_t)q * KMAX * CERT_WAVES;
-        J.cert_cp = S.cert_cp + (size_t)q * KMAX * CERT_WAVES;
-        J.cert_d = S.cert_d + (size_t)q * KMAX * CERT_WAVES;
-        J.sync = S.sync + q;
-        J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
-        J.climb = climb && climb_ok(j) ? 1 : 0;
-        // seeding work units: rows of the inner sweep, or plans
-        const bool sweep = g < kSweepGroups;
-        const uint64_t sunits = sweep ? J.nblk * (uint64_t)H.rx : J.count;
-        uint64_t stride = h->sample_stride;
-        if (!h->stride_fixed) stride = std::max<uint64_t>(1, std::min<uint64_t>(stride, sunits / kMinSamples));
-        // the local search gives each level a seed near its optimum; the
-        // sample then only backs it up (about 256 samples per source)
-        if (!h->stride_fixed && J.climb) stride = std::max<uint64_t>(stride, std::min<uint64_t>(2048, sunits / 256));
-        if (!h->stride_fixed && g == G_JIT && split_rows(J, h->hdesc[src[j].problem]))
-            stride = std::max<uint64_t>(stride, std::min<uint64_t>(kSplitStride, sunits / kMinSamples));
-        J.sample_stride = (uint32_t)stride;
-        J.units = sweep ? J.nblk : J.count;
-        ++pp.n[g];
-        if (g < kSweepGroups && jsw[j]) ++pp.njit[g];
-        if (g < G_JIT) {
-            pp.units[g] = std::max(pp.units[g], J.units);
-            pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
-        }
-        pp.kmax = std::max(pp.kmax, H.k);
-        if (g == G_GENERIC) pp.ncol = std::max(pp.ncol, H.n);
-        if (sweep) {
-            if (!jsw[j] && h->hdesc[src[j].problem].jsh != 18) pp.b256[g] = false;
-            if (!jsw[j]) {
-                const ProbDev& Dp = h->hdesc[src[j].problem];
-                bool r12 = J.big == 0;
-                for (int n = 0; n < Dp.npre; ++n) r12 = r12 && Dp.radix[n] == 12;
-                if (!r12) pp.rad12[g] = false;
-            }
-            pp.npre[g] = std::max(pp.npre[g], H.npre);
-            pp.ry[g] = pp.n[g] == 1 ? H.ry : (pp.ry[g] == H.ry ? pp.ry[g] : -1);
-            pp.npre_c[g] = pp.n[g] == 1 ? H.npre : (pp.npre_c[g] == H.npre ? pp.npre_c[g] : -1);
-        }
-        all_units = std::max(all_units, J.count);
-        plans += J.count;
-        jobs[q] = J;
-    }
-    const int n3 = pp.before(G_JIT);  // jobs of the other groups; JIT jobs follow
-    // library sweep (both objectives) with a compile-time prefix length: a
-    // source whose blocks are aligned runs of G (G dividing the last prefix
-    // node's radix, up to 12) gives each thread G blocks that share the
-    // prefix but its last node; only in groups of many blocks, so that the
-    // fewer threads still fill the device (batch6's 85 M blocks: sweep 1.61
-    // -> 1.53 ms with runs of 12, 1.59 with runs of 4)
-    for (int g = 0; g < kSweepGroups; ++g) {
-        const int npc = pp.npre_c[g];
-        if (npc != 2 && npc != 4 && npc != 6 && npc != 8) continue;
-        const int q0 = pp.before(g), q1 = pp.before(g) + pp.n[g] - pp.njit[g];
-        uint64_t total = 0;
-        for (int q = q0; q < q1; ++q) total += jobs[q].nblk;
-        if (total < kSweepRunMin) continue;
-        uint64_t units = 0;
-        for (int q = q0; q < q1; ++q) {
-            JobDev& J = jobs[q];
-            const int last = h->hdesc[(int)(J.prob - h->d_probs)].radix[npc - 1];
-            for (int G : {12, 6, 4, 3, 2})
-                if (last % G == 0 && J.blk_first % (uint64_t)G == 0 && J.nblk % (uint64_t)G == 0) {
-                    J.gblk = G;
-                    J.units = J.nblk / (uint64_t)G;
-                    break;
-                }
-            units = std::max(units, J.units);
-        }
-        pp.units[g] = units;
-    }
+    // the sources' groups, launch order, jobs and launch plan: derived anew,
+    // or the previous call's when this call repeats it (same sources, slots,
+    // scratch, options and generated-kernel states)
+    CallPlan fresh;
+    CallPlan& C = stat ? fresh : h->call;
+    const int64_t opts[6] = {h->use_jit, h->use_climb, (int64_t)h->sample_stride, h->stride_fixed ? 1 : 0,
+                             h->force_fp64, cert_waves};
+    const bool reuse = !stat && C.valid && C.src.size() == (size_t)n_src && C.cap == cap &&
+                       C.scratch == (const void*)S.scert && std::memcmp(C.opts, opts, sizeof opts) == 0 &&
+                       C.jit_state == h->jit_state &&
+                       std::memcmp(C.src.data(), src, (size_t)n_src * sizeof(dy_source)) == 0;
+    std::vector<int>& grp = C.grp;
+    std::vector<int>& order = C.order;
+    std::vector<JobDev>& jobs = C.jobs;
+    PassPlan& pp = C.pp;
     // first share of a JIT rows job scored in two shares (0: one pass)
     auto split_at = [&](const JobDev& J) { return split_rows(J, h->hdesc[(int)(J.prob - h->d_probs)]); };
-    bool any_split = false;
-    for (int q = n3; q < n3 + pp.n[G_JIT]; ++q) any_split = any_split || split_at(jobs[q]) != 0;
-    bool any_climb = false;
-    int climb_modes = 0;  // bit 0: a corr / SLO source climbs, bit 1: an objective one
-    for (int q = 0; q < n3; ++q)
-        if (jobs[q].climb) {
-            any_climb = true;
-            climb_modes |= h->hdesc[(int)(jobs[q].prob - h->d_probs)].obj ? 2 : 1;
+    if (!reuse) {
+        C.valid = false;
+        grp.assign((size_t)n_src, 0);
+        for (int j = 0; j < n_src; ++j) {
+            const int p = src[j].problem;
+            const HostProb& H = h->hp[p];
+            if (src[j].kind == DY_SOURCE_RANGE)
+                grp[j] = H.obj ? (H.has_s2 ? G_OSWEEP_S2 : G_OSWEEP) : (H.has_s2 ? G_SWEEP_S2 : G_SWEEP);
+            else if (src[j].kind == DY_SOURCE_ROWS && !h->force_fp64 && jit_use(p))
+                grp[j] = G_JIT;
+            else
+                grp[j] = G_GENERIC;
         }
-    // the job array is rebuilt every call but uploaded only when it changed
-    const bool changed =
-        stat || S.uploaded != (size_t)n_src || std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0;
+        // RANGE sources of 32-bit plan indices run the sweep generated for their DAG, when the plan has few
+        // problems (one compilation each), the source is large enough to repay
+        // it (2^24 plans; every source with DY_OPT_JIT 2) and it compiles; they
+        // go last in their group, whose library sweep launch covers the others
+        std::vector<char> jsw(n_src, 0);
+        const uint64_t jit_min = h->use_jit >= 2 ? 1 : (1ull << 24);
+        if (h->use_jit && !h->force_fp64 && h->hp.size() <= 8)
+            for (int j = 0; j < n_src; ++j) {
+                const int p = src[j].problem;
+                if (src[j].kind == DY_SOURCE_RANGE && src[j].count >= jit_min &&
+                    src[j].begin + src[j].count - 1 <= 0xffffffffull && jit_use(p) && h->jit[p].sweep)
+                    jsw[j] = 1;
+            }
+        // local-search seeds (whole-space RANGE sources of problems of at most
+        // kClimbNodes nodes, either objective): in calls of many such sources, where they replace
+        // most of the sampling and of the certification work; a call of a few
+        // sources waits for the searches' latency instead (tens of microseconds)
+        auto climb_ok = [&](int j) {
+            const HostProb& H = h->hp[src[j].problem];
+            return !h->force_fp64 && H.n <= kClimbNodes && src[j].kind == DY_SOURCE_RANGE &&
+                   src[j].begin == 0 && !H.plans_saturated && src[j].count == H.n_plans;
+        };
+        int n_climb = 0;
+        for (int j = 0; j < n_src; ++j) n_climb += climb_ok(j) ? 1 : 0;
+        const bool climb = h->use_climb == 2 || (h->use_climb == 1 && n_climb >= kClimbMinSources);
+        order.clear();
+        order.reserve(n_src);
+        for (int g = 0; g < kGroups; ++g)
+            for (int pass = 0; pass < 2; ++pass)
+                for (int j = 0; j < n_src; ++j)
+                    if (grp[j] == g && jsw[j] == pass) order.push_back(j);
+        C.plans = 0;
+        C.all_units = 0;
+        pp = PassPlan();
+        jobs.resize((size_t)n_src);
+        for (int q = 0; q < n_src; ++q) {
+            const int j = order[q];
+            const int g = grp[j];
+            const HostProb& H = h->hp[src[j].problem];
+            JobDev J = make_job(h, src[j]);
+            J.cap = (uint32_t)cap;
+            J.scert = S.scert + (size_t)q * KMAX * NSLOT;
+            J.thr = S.thr + (size_t)q * KMAX;
+            J.table = S.table + (size_t)q * NBINS;
+            J.table2 = S.table2 + (size_t)q * NBINS2;
+            J.cand = S.cand + (size_t)q * cap;
+            J.ncand = S.ncand + q;
+            J.flags = S.flags + q;
+            J.out = S.out + (size_t)j * km;
+            if (n_src <= kDirectResults && !stat) {  // few sources: certification writes the host copy directly
+                J.hout = (dy_choice*)S.d_hres + (size_t)j * km;
+                J.hncand = (uint32_t*)(S.d_hres + S.res_ncand_off) + q;
+                J.hflags = (int32_t*)(S.d_hres + S.res_flags_off) + q;
+                J.hdone = S.d_done + q;
+            }
+            J.fb_corr = S.fb_corr + (size_t)q * KMAX;
+            J.fb_index = S.fb_index + (size_t)q * KMAX;
+            J.cert_waves = cert_waves;
+            J.cert_c = S.cert_c + (size_t)q * KMAX * CERT_WAVES;
+            J.cert_i = S.cert_i + (size_t)q * KMAX * CERT_WAVES;
+            J.cert_cp = S.cert_cp + (size_t)q * KMAX * CERT_WAVES;
+            J.cert_d = S.cert_d + (size_t)q * KMAX * CERT_WAVES;
+            J.sync = S.sync + q;
+            J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
+            J.climb = climb && climb_ok(j) ? 1 : 0;
+            // seeding work units: rows of the inner sweep, or plans
+            const bool sweep = g < kSweepGroups;
+            const uint64_t sunits = sweep ? J.nblk * (uint64_t)H.rx : J.count;
+            uint64_t stride = h->sample_stride;
+            if (!h->stride_fixed) stride = std::max<uint64_t>(1, std::min<uint64_t>(stride, sunits / kMinSamples));
+            // the local search gives each level a seed near its optimum; the
+            // sample then only backs it up (about 256 samples per source)
+            if (!h->stride_fixed && J.climb) stride = std::max<uint64_t>(stride, std::min<uint64_t>(2048, sunits / 256));
+            if (!h->stride_fixed && g == G_JIT && split_rows(J, h->hdesc[src[j].problem]))
+                stride = std::max<uint64_t>(stride, std::min<uint64_t>(kSplitStride, sunits / kMinSamples));
+            J.sample_stride = (uint32_t)stride;
+            J.units = sweep ? J.nblk : J.count;
+            ++pp.n[g];
+            if (g < kSweepGroups && jsw[j]) ++pp.njit[g];
+            if (g < G_JIT) {
+                pp.units[g] = std::max(pp.units[g], J.units);
+                pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
+            }
+            pp.kmax = std::max(pp.kmax, H.k);
+            if (g == G_GENERIC) pp.ncol = std::max(pp.ncol, H.n);
+            if (sweep) {
+                if (!jsw[j] && h->hdesc[src[j].problem].jsh != 18) pp.b256[g] = false;
+                if (!jsw[j]) {
+                    const ProbDev& Dp = h->hdesc[src[j].problem];
+                    bool r12 = J.big == 0;
+                    for (int n = 0; n < Dp.npre; ++n) r12 = r12 && Dp.radix[n] == 12;
+                    if (!r12) pp.rad12[g] = false;
+                }
+                pp.npre[g] = std::max(pp.npre[g], H.npre);
+                pp.ry[g] = pp.n[g] == 1 ? H.ry : (pp.ry[g] == H.ry ? pp.ry[g] : -1);
+                pp.npre_c[g] = pp.n[g] == 1 ? H.npre : (pp.npre_c[g] == H.npre ? pp.npre_c[g] : -1);
+            }
+            C.all_units = std::max(C.all_units, J.count);
+            C.plans += J.count;
+            jobs[q] = J;
+        }
+        C.n3 = pp.before(G_JIT);  // jobs of the other groups; JIT jobs follow
+        const int n3 = C.n3;
+        // library sweep (both objectives) with a compile-time prefix length: a
+        // source whose blocks are aligned runs of G (G dividing the last prefix
+        // node's radix, up to 12) gives each thread G blocks that share the
+        // prefix but its last node; only in groups of many blocks, so that the
+        // fewer threads still fill the device (batch6's 85 M blocks: sweep 1.61
+        // -> 1.53 ms with runs of 12, 1.59 with runs of 4)
+        for (int g = 0; g < kSweepGroups; ++g) {
+            const int npc = pp.npre_c[g];
+            if (npc != 2 && npc != 4 && npc != 6 && npc != 8) continue;
+            const int q0 = pp.before(g), q1 = pp.before(g) + pp.n[g] - pp.njit[g];
+            uint64_t total = 0;
+            for (int q = q0; q < q1; ++q) total += jobs[q].nblk;
+            if (total < kSweepRunMin) continue;
+            uint64_t units = 0;
+            for (int q = q0; q < q1; ++q) {
+                JobDev& J = jobs[q];
+                const int last = h->hdesc[(int)(J.prob - h->d_probs)].radix[npc - 1];
+                for (int G : {12, 6, 4, 3, 2})
+                    if (last % G == 0 && J.blk_first % (uint64_t)G == 0 && J.nblk % (uint64_t)G == 0) {
+                        J.gblk = G;
+                        J.units = J.nblk / (uint64_t)G;
+                        break;
+                    }
+                units = std::max(units, J.units);
+            }
+            pp.units[g] = units;
+        }
+        // whether any source is scored in two shares, or climbs
+        C.any_split = false;
+        for (int q = n3; q < n3 + pp.n[G_JIT]; ++q) C.any_split = C.any_split || split_at(jobs[q]) != 0;
+        C.any_climb = false;
+        C.climb_modes = 0;  // bit 0: a corr / SLO source climbs, bit 1: an objective one
+        for (int q = 0; q < n3; ++q)
+            if (jobs[q].climb) {
+                C.any_climb = true;
+                C.climb_modes |= h->hdesc[(int)(jobs[q].prob - h->d_probs)].obj ? 2 : 1;
+            }
+        C.src.assign(src, src + n_src);
+        C.cap = cap;
+        C.scratch = (const void*)S.scert;
+        std::memcpy(C.opts, opts, sizeof opts);
+        C.jit_state = h->jit_state;
+        C.valid = !stat;
+    }
+    const int n3 = C.n3;
+    const uint64_t plans = C.plans, all_units = C.all_units;
+    const bool any_split = C.any_split, any_climb = C.any_climb;
+    const int climb_modes = C.climb_modes;
+    // the job array is uploaded only when it changed (a reused plan's jobs are
+    // the ones the previous call uploaded)
+    const bool changed = stat || S.uploaded != (size_t)n_src ||
+                         (!reuse && std::memcmp(S.h_jobs, jobs.data(), (size_t)n_src * sizeof(JobDev)) != 0);
     if (changed) {
         if (!stat) drop_graph(h);
         hipError_t e = hipStreamSynchronize(s);  // a previous upload may still read the pinned buffer
@@ -1767,9 +1824,15 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         stats.candidates = 0;
         for (int q = 0; q < n_src; ++q) stats.candidates += std::min<uint64_t>(S.h_ncand[q], cap);
     }
-    for (int j = 0; j < n_src; ++j) {
-        const int K = h->hp[src[j].problem].k;
-        std::memcpy(out + (size_t)j * km, S.h_out + (size_t)j * km, (size_t)K * sizeof(dy_choice));
+    bool all_km = true;
+    for (int j = 0; j < n_src && all_km; ++j) all_km = h->hp[src[j].problem].k == km;
+    if (all_km) {  // one copy; else columns past a problem's levels stay untouched
+        std::memcpy(out, S.h_out, (size_t)n_src * km * sizeof(dy_choice));
+    } else {
+        for (int j = 0; j < n_src; ++j) {
+            const int K = h->hp[src[j].problem].k;
+            std::memcpy(out + (size_t)j * km, S.h_out + (size_t)j * km, (size_t)K * sizeof(dy_choice));
+        }
     }
     bool flagged = false;
     for (int q = 0; q < n_src; ++q) flagged = flagged || S.h_flags[q] != 0;

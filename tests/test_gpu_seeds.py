@@ -165,3 +165,34 @@ def test_rows_scored_in_two_shares(per_class, winners):
         for call in range(2):  # the second call replays the captured graph
             got = plan.select([D.rows_source(0, d, n, 24, 0)], stream=stream())[0]
             assert_choices(got, want, f"{prob.name}, winners in the {winners}, call {call}")
+
+
+def test_repeated_calls_reuse_and_rebuild_the_call_plan():
+    # a call whose sources, options and state repeat the previous call's reuses
+    # the plan derived for it (groups, order, jobs); any change derives it
+    # again: two source sets alternating, options changed between calls with
+    # the same sources, a score call in between
+    prob = wl.forkjoin8()
+    a = [D.range_source(0, 0, 1 << 22)]
+    b = [D.range_source(0, 5000, 1 << 21), D.range_source(0, 777777, 123457)]
+    want = {"a": [orc.select_range(prob, 0, 1 << 22)],
+            "b": [orc.select_range(prob, 5000, 1 << 21), orc.select_range(prob, 777777, 123457)]}
+    srcs = {"a": a, "b": b}
+
+    def check(plan, key, ctx):
+        got = plan.select(srcs[key], stream=stream())
+        for s, (g, w) in enumerate(zip(got, want[key])):
+            assert_choices(g, w, f"{ctx}, source {s}")
+
+    with D.Plan(prob) as plan:
+        for i, key in enumerate("aabba"):
+            check(plan, key, f"call {i} ({key})")
+        plan.set_option(D.DY_OPT_SAMPLE_STRIDE, 7)
+        check(plan, "a", "stride 7")
+        check(plan, "a", "stride 7, again")
+        plan.set_option(D.DY_OPT_CAND_CAPACITY, 1024)
+        check(plan, "b", "1024 candidate slots")
+        check(plan, "b", "1024 candidate slots, again")
+        corr = torch.empty(1000, dtype=torch.float32, device="cuda")
+        plan.score(D.range_source(0, 0, 1000), corr, None, None, None, stream=stream())
+        check(plan, "b", "after a score call")
