@@ -317,7 +317,7 @@ def edge_count(prob):
     return len({(int(u), int(v)) for u, v in prob.edges})
 
 
-def sweep_work_per_plan(prob):
+def sweep_work_per_plan(prob, ydiv=False):
     """Algorithmic fp32 operations per plan of the prefix-shared sweep.
 
     Per plan: 1 multiply (corr), 1 add (CP), 1 compare (prefilter); per row of
@@ -325,6 +325,13 @@ def sweep_work_per_plan(prob):
     y's predecessors; per block (R_x R_y plans): the prefix products and one
     max/add per prefix edge.  Counted like the full recurrence, operation by
     operation, so the figure never exceeds the work actually done.
+
+    ydiv: the sweep compares x's product (the rest of a plan's corr) with
+    thresholds divided ahead by each implementation of y's factor, so a plan
+    costs 1 add (CP) and 1 selection operation (the min of its CP bin's
+    threshold into its row's least threshold; the row's last one is the
+    compare with x's product) and no multiply.  The bin's address (an AND of
+    the CP's pattern) is addressing, not counted.
     """
     n = prob.n_nodes
     rx = int(prob.radix[n - 2]) if n >= 2 else 1
@@ -334,7 +341,7 @@ def sweep_work_per_plan(prob):
     pre_edges = sum(1 for u, v in edges if v < npre)
     x_pred = sum(1 for u, v in edges if v == n - 2)
     y_pred = sum(1 for u, v in edges if v == n - 1 and u != n - 2)
-    per_plan = 3.0
+    per_plan = 2.0 if ydiv else 3.0
     per_row = 2.0 + (1.0 if (n - 2, n - 1) in edges and y_pred > 0 else 0.0)
     per_block = max(npre - 1, 0) + pre_edges + x_pred + y_pred
     return per_plan + per_row / ry + per_block / (rx * ry)
@@ -655,7 +662,7 @@ def main():
     def timed_loop(tag, collect):
         # collect: read the library's per-call statistics after every step
         # (the caller-side loop does not, as a caller needs only the choices)
-        cands, main_ms, gen = [], [], []
+        cands, main_ms, gen, ydiv = [], [], [], []
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -667,16 +674,17 @@ def main():
                 main_ms.append(s.main_ms)
                 cands.append(s.candidates)
                 gen.append(s.generated_jobs)
+                ydiv.append(s.ydiv_jobs)
             if i == 0 or (i + 1) % max(1, args.steps // 4) == 0:
                 print(f"[bench] {tag} step {i + 1}/{args.steps}", file=sys.stderr, flush=True)
         ev1.record(stream)
         torch.cuda.synchronize()
-        return ev0.elapsed_time(ev1) / args.steps, main_ms, cands, gen
+        return ev0.elapsed_time(ev1) / args.steps, main_ms, cands, gen, ydiv
 
     # 1) the steps as a caller runs them: repeated calls replay one HIP graph
     for _ in range(args.warmup):
         step()
-    ms_per_step, _, _, _ = timed_loop("step", False)
+    ms_per_step, _, _, _, _ = timed_loop("step", False)
     value = plans / (ms_per_step / 1e3)
     got_graph = [[out[j * plan.kmax + k].as_tuple() for k in range(K)] for j in range(len(sources))]
     # 2) the same calls with the library's HIP events around the scoring kernel
@@ -684,7 +692,7 @@ def main():
     plan.set_option(D.DY_OPT_TIMING, 1)
     for _ in range(max(1, args.warmup // 2)):
         step()
-    ms_per_step_timed, main_ms, cands, gen = timed_loop("timed", True)
+    ms_per_step_timed, main_ms, cands, gen, ydiv = timed_loop("timed", True)
     got_timed = [[out[j * plan.kmax + k].as_tuple() for k in range(K)] for j in range(len(sources))]
     generated = bool(gen) and max(gen) > 0  # the library ran a kernel generated for the problem
     kern_ms = float(np.mean(main_ms))
@@ -698,8 +706,15 @@ def main():
                 "traffic": stored_traffic(tkey, kbase), "per_unit": "24 B of row per plan", "kernel_ms": kern_ms,
                 "achieved_units_per_step": units, "peak_scale": 1e9}
     else:
-        wfn = obj_sweep_work_per_plan if objs else sweep_work_per_plan
-        units = sum(wfn(probs[p]) * c for _, p, _, c in specs)
+        # sources whose sweep took the pre-divided thresholds (every one or none
+        # in these workloads: one DAG, or requests of one shape)
+        yd = max(ydiv) if ydiv else 0
+        if yd not in (0, len(sources)):
+            raise RuntimeError(f"{yd} of {len(sources)} sources took the pre-divided thresholds")
+        if objs:
+            units = sum(obj_sweep_work_per_plan(probs[p]) * c for _, p, _, c in specs)
+        else:
+            units = sum(sweep_work_per_plan(probs[p], yd > 0) * c for _, p, _, c in specs)
         f = units / plans
         achieved = units / (kern_ms / 1e3)
         if generated:
@@ -713,6 +728,7 @@ def main():
                 "peak_packed_fp32": PEAK_VALU_PACKED / 1e12, "frac_vs_packed_fp32": achieved / PEAK_VALU_PACKED,
                 "traffic": stored_traffic(tkey, kbase),
                 "per_unit": f"{f:.4f} fp32 ops per plan (prefix-shared sweep{', objective' if objs else ''}"
+                            + (", thresholds divided ahead by y's factor" if yd else "")
                             + (", mean over the requests' DAGs" if len(specs) > 1 else "") + ")",
                 "kernel_ms": kern_ms, "achieved_units_per_step": units, "peak_scale": 1e12}
         if not objs:

@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define DY_ABI_VERSION 3
+#define DY_ABI_VERSION 4
 
 #define DY_MAX_NODES 32      /* nodes per problem */
 #define DY_MAX_RADIX 255     /* implementations per node (ids fit a uint8 row byte) */
@@ -201,7 +201,9 @@ typedef struct dy_stats {
     float main_ms;           /* duration of the main scoring kernel(s), when timing is on */
     float total_ms;          /* launch of the first kernel to the end of the last */
     int32_t generated_jobs;  /* sources whose main pass ran a kernel generated for their problem */
-    int32_t reserved;        /* 0 */
+    int32_t ydiv_jobs;       /* sources whose sweep compared each plan with its CP bin's threshold divided
+                                ahead by node y's factor (per plan the CP add and a min into the row's
+                                threshold, no corr product) */
 } dy_stats;
 
 /* Options for dy_plan_set_option. */

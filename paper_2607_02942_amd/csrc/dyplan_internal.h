@@ -96,6 +96,11 @@ struct ProbDev {
     float ty_min;             // smallest duration tau of node y
     uint8_t yord[64];         // ids of node y by decreasing fp32 factor a (ties by id), radix <= 64
     float lymin[KMAX];        // per-backend pressure: per level, node y's smallest fp32 duration
+    // per implementation j of node y (j < 64): r_j <= 1 / (a_j (1 + 2^-22)),
+    // rounded down to fp32; 0 when a_j < 2^-20.  A bin threshold T scaled by
+    // r_j is a threshold on the rest of the product: fp32(c a_j) >= T implies
+    // c >= fp32(T r_j) for T > 2^-60 (see ydiv_threshold).
+    float yinv[64];
 };
 
 struct Cand {

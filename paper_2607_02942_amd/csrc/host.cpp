@@ -22,7 +22,7 @@ hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_samples,
                                int npre_max, int npre_c, int kmax, hipStream_t s);
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
-                        int npre_c, int ry, bool b256, bool rad12, hipStream_t s);
+                        int npre_c, int ry, bool b256, bool rad12, int pat, hipStream_t s);
 hipError_t launch_sample_generic(const JobDev* d_jobs, int n, uint64_t max_samples, int ncol, hipStream_t s);
 hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol, hipStream_t s);
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, int nmax, int nrmax, hipStream_t s);
@@ -367,6 +367,8 @@ struct PassPlan {
     int npre[kSweepGroups] = {};
     int ry[kSweepGroups] = {};            // R_y shared by every source of a sweep group, else -1
     int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
+    int pat[kSweepGroups] = {};           // largest prefix-row table (npre x rmax entries) of a sweep group
+    int ydiv_jit[kSweepGroups] = {};      // generated sweeps (corr mode) on thresholds pre-divided by y's factor
     int njit[kSweepGroups] = {};          // trailing sources of the group that run their generated sweep
     bool b256[kSweepGroups] = {true, true, true, true};  // every library-sweep source has the 256-bin table
     bool rad12[kSweepGroups] = {true, true, true, true}; // ... and 12 implementations per prefix node, 32-bit blocks
@@ -924,6 +926,17 @@ int stage_problems(dy_plan* h, const dy_problem* probs, int32_t n_probs, std::st
             for (int i = 0; i < ry; ++i) ord[i] = i;
             std::stable_sort(ord.begin(), ord.end(), [&](int u, int v) { return ay[u].x > ay[v].x; });
             for (int i = 0; i < 64; ++i) D.yord[i] = (uint8_t)(i < ry ? ord[i] : 0);
+            // reciprocal factors of y, rounded down with a margin of 2^-22
+            // relative (two fp32 roundings, 2^-24 each, plus this fp64 one)
+            for (int i = 0; i < 64; ++i) {
+                float r = 0.0f;
+                if (i < ry && (double)ay[i].x >= 0x1p-20) {
+                    const double v = 1.0 / ((double)ay[i].x * (1.0 + 0x1p-22));
+                    r = (float)v;
+                    if ((double)r > v) r = std::nextafter(r, 0.0f);
+                }
+                D.yinv[i] = r;
+            }
         }
         for (int k = 0; k < KMAX; ++k) {
             float m = INFINITY;
@@ -1347,7 +1360,7 @@ void launch_main(const dy_plan* h, const JobDev* d, const JobDev* hjobs, const P
     for (int g = 0; g < kSweepGroups; ++g) {
         chunks(d + pp.before(g), pp.n[g] - pp.njit[g], [&](const JobDev* b, int n) {
             chk(launch_sweep(b, n, (g & 1) != 0, g >= G_OSWEEP, pp.units[g], pp.npre[g], pp.npre_c[g], pp.ry[g],
-                             pp.b256[g], pp.rad12[g], s),
+                             pp.b256[g], pp.rad12[g], pp.pat[g], s),
                 "sweep");
         });
         for (int q = pp.before(g) + pp.n[g] - pp.njit[g]; q < pp.before(g) + pp.n[g]; ++q)
@@ -1543,6 +1556,9 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
             J.units = sweep ? J.nblk : J.count;
             ++pp.n[g];
             if (g < kSweepGroups && jsw[j]) ++pp.njit[g];
+            if ((g == G_SWEEP || g == G_SWEEP_S2) && jsw[j] && h->hdesc[src[j].problem].jsh != 0 && H.ry >= 1 &&
+                H.ry <= 64)
+                ++pp.ydiv_jit[g];
             if (g < G_JIT) {
                 pp.units[g] = std::max(pp.units[g], J.units);
                 pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
@@ -1558,6 +1574,7 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
                     if (!r12) pp.rad12[g] = false;
                 }
                 pp.npre[g] = std::max(pp.npre[g], H.npre);
+                pp.pat[g] = std::max(pp.pat[g], H.npre * H.rmax);
                 pp.ry[g] = pp.n[g] == 1 ? H.ry : (pp.ry[g] == H.ry ? pp.ry[g] : -1);
                 pp.npre_c[g] = pp.n[g] == 1 ? H.npre : (pp.npre_c[g] == H.npre ? pp.npre_c[g] : -1);
             }
@@ -1749,6 +1766,10 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
     stats.n_jobs = n_src;
     stats.generated_jobs = pp.n[G_JIT];
     for (int g = 0; g < kSweepGroups; ++g) stats.generated_jobs += pp.njit[g];
+    // the library sweep takes the pre-divided thresholds for groups on 256
+    // bins with R_y = 12 (corr mode)
+    for (int g : {(int)G_SWEEP, (int)G_SWEEP_S2})
+        stats.ydiv_jobs += pp.ydiv_jit[g] + (pp.b256[g] && pp.ry[g] == 12 ? pp.n[g] - pp.njit[g] : 0);
     if (h->timing) {
         float ms = 0.0f;
         if (hipEventElapsedTime(&ms, h->ev[1], h->ev[2]) == hipSuccess) stats.main_ms = ms;
@@ -1786,6 +1807,7 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
                     ++rp.n[g];
                     if (g < G_JIT) rp.units[g] = std::max(rp.units[g], J.units);
                     if (g < kSweepGroups) rp.npre[g] = std::max(rp.npre[g], H.npre);
+                    if (g < kSweepGroups) rp.pat[g] = std::max(rp.pat[g], H.npre * H.rmax);
                     if (g < kSweepGroups && h->hdesc[src[j].problem].jsh != 18) rp.b256[g] = false;
                     rp.rad12[g] = false;  // reseeded sources take the general kernel
                     if (g == G_GENERIC) rp.ncol = std::max(rp.ncol, H.n);

@@ -298,12 +298,25 @@ void gen_sweep(std::ostringstream& o, const ProbDev& D) {
     const int nb = D.jsh ? NBINS2 : NBINS;
     const int sh = (D.jsh ? D.jsh : D.bin_shift) - 2;
     const unsigned msk = (unsigned)(nb - 1) << 2;
+    // corr mode on 256 bins: the bins' thresholds held per implementation of
+    // y, divided by its factor (rounded down, so that a plan the product test
+    // admits is admitted: see the library's ydiv_threshold); a row's test is
+    // then cx >= the least threshold of its plans' bins, every threshold being
+    // +0, positive or +inf, so that their fp32 patterns order as the values
+    const bool ydiv = !obj && D.jsh != 0 && D.ry >= 1 && D.ry <= 64;
     auto maxof = [&](uint32_t mask, const char* pre) {
         std::string m;
         for (int u = 0; u < NP; ++u)
             if (mask >> u & 1u) m = m.empty() ? std::string(pre) + std::to_string(u) : "fmaxf(" + m + ", " + pre + std::to_string(u) + ")";
         return m.empty() ? std::string("0.0f") : m;
     };
+    if (ydiv)
+        o << R"(
+__device__ __forceinline__ float dy_ydiv(float T, float r) {
+  if (T == __builtin_inff()) return T;
+  return T > 0x1p-60f ? T * r : 0.0f;
+}
+)";
     o << R"(
 extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     unsigned long long unit_off, unsigned long long blk_first, unsigned long long nblk, unsigned long long begin,
@@ -312,14 +325,23 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     const float* __restrict__ demy, const float* __restrict__ lat, int rmax, const unsigned* __restrict__ table,
     const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap, unsigned* __restrict__ ncand,
     int* __restrict__ flags) {
-  __shared__ float s_bins[)" << nb << R"(];
+  __shared__ float s_bins[)" << (ydiv ? D.ry * NBINS2 : nb) << R"(];
   __shared__ float2 s_pat[)" << NP << R"( * 64];
 )";
     if (obj) o << "  __shared__ float s_pd[" << NP << " * 64];\n";
     o << R"(  const unsigned long long t0 = unit_off + (unsigned long long)blockIdx.x * 256ull;
   if (t0 >= nblk) return;
-  for (int i = threadIdx.x; i < )" << nb << R"(; i += 256) s_bins[i] = __uint_as_float(table[i]);
-  for (int i = threadIdx.x; i < )" << NP << R"( * 64; i += 256) {
+)";
+    if (ydiv) {
+        static_assert(NBINS2 == 256, "one bin per thread");
+        o << "  {\n    const float T = __uint_as_float(table[threadIdx.x]);\n";
+        for (int j = 0; j < D.ry; ++j)
+            o << "    s_bins[" << j * NBINS2 << " + threadIdx.x] = dy_ydiv(T, " << flit(D.yinv[j]) << ");\n";
+        o << "  }\n";
+    } else {
+        o << "  for (int i = threadIdx.x; i < " << nb << "; i += 256) s_bins[i] = __uint_as_float(table[i]);\n";
+    }
+    o << R"(  for (int i = threadIdx.x; i < )" << NP << R"( * 64; i += 256) {
     const int n = i >> 6, e = i & 63;
     s_pat[i] = e < rmax ? at[n * rmax + e] : make_float2(1.0f, 0.0f);
 )";
@@ -382,13 +404,31 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
             o << ind << "const float bv = cp;\n";
         }
     };
-    o << "    unsigned long long hit = 0ull;\n";
-    o << "#pragma unroll\n    for (int j = 0; j < " << D.ry << "; ++j) {\n";
-    plan("      ", "vy", "dy");
-    o << "      const float th = *(const float*)((const char*)s_bins + ((__float_as_uint(bv) >> " << sh << "u) & " << msk
-      << "u));\n";
-    o << "      hit |= __builtin_amdgcn_ballot_w64(cc >= th);\n    }\n";
-    o << "    if (hit && live && (hit >> (threadIdx.x & 63) & 1ull)) {\n";
+    if (ydiv) {
+        // y's implementation j reads its own 256 bins (a constant offset)
+        auto thr_j = [&](const char* ind, const char* j) {
+            o << ind << "float cp = vy[" << j << "].y + M;\n";
+            if (s2) o << ind << "cp = fmaxf(cp, S2);\n";
+            o << ind << "const unsigned th = *(const unsigned*)((const char*)s_bins + " << NBINS2 * 4 << " * (" << j
+              << ") + ((__float_as_uint(cp) >> 16) & 0x3fcu));\n";
+        };
+        o << "    unsigned m;\n    {\n";
+        thr_j("      ", "0");
+        o << "      m = th;\n    }\n";
+        o << "#pragma unroll\n    for (int j = 1; j < " << D.ry << "; ++j) {\n";
+        thr_j("      ", "j");
+        o << "      m = min(m, th);\n    }\n";
+        o << "    const bool mine_ = cx >= __uint_as_float(m);\n";
+    } else {
+        o << "    unsigned long long hit = 0ull;\n";
+        o << "#pragma unroll\n    for (int j = 0; j < " << D.ry << "; ++j) {\n";
+        plan("      ", "vy", "dy");
+        o << "      const float th = *(const float*)((const char*)s_bins + ((__float_as_uint(bv) >> " << sh << "u) & "
+          << msk << "u));\n";
+        o << "      hit |= __builtin_amdgcn_ballot_w64(cc >= th);\n    }\n";
+        o << "    const bool mine_ = hit && ((hit >> (threadIdx.x & 63)) & 1ull);\n";
+    }
+    o << "    if (live && mine_) {\n";
     o << "      const unsigned long long base = (b * " << D.rx << "ull + (unsigned long long)ix) * " << D.ry << "ull;\n";
     if (!obj && !D.uniform) {
         // per-backend pressure: per level, the row's exact fp32 CP_k from the

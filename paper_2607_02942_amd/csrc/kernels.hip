@@ -426,9 +426,9 @@ struct Prefix {
 constexpr int PAT_MAX = 1024;  // entries
 
 template <bool OBJ>
-__device__ __forceinline__ const float2* stage_prefix_rows(PD P, float2* s_pat, float* s_pd) {
+__device__ __forceinline__ const float2* stage_prefix_rows(PD P, float2* s_pat, float* s_pd, int cap = PAT_MAX) {
     const int n = P->npre * P->rmax;
-    const bool fit = n <= PAT_MAX;
+    const bool fit = n <= cap;
     if (fit)
         for (int i = threadIdx.x; i < n; i += WG) {
             s_pat[i] = cs(P->at)[i];
@@ -647,6 +647,32 @@ __device__ __forceinline__ uint64_t sweep_test(const float2 vy, float M, float S
     return __ballot(cc >= thr);
 }
 
+// Threshold on the rest of the product for implementation j of y (r_j =
+// P->yinv[j]): whenever fp32(c a_j) >= T, c >= the value returned.  For T >
+// 2^-60, fp32(c a_j) >= T gives c a_j >= T / (1 + 2^-24) (both normal), and
+// fp32(T r_j) <= T r_j (1 + 2^-24) <= T / (a_j (1 + 2^-24)) since r_j <= 1 /
+// (a_j (1 + 2^-22)); smaller T, and r_j = 0 (a_j < 2^-20), give 0, which
+// every c >= 0 meets; T = +inf (no level in the bin) stays +inf.
+__device__ __forceinline__ float ydiv_threshold(float T, float r) {
+    if (T == INFINITY) return T;
+    return T > 0x1p-60f ? T * r : 0.0f;
+}
+
+// One plan of the inner sweep with the thresholds of y's implementation
+// pre-divided (s_t: its 256 bins): CP = max(tau_y + M, S2) picks the bin, whose
+// threshold on cx (the rest of the product) is returned as its fp32 pattern.
+// Every such threshold is +0, positive or +inf, so the patterns order as the
+// values do: the row's test is cx >= the least of its plans' thresholds (no
+// per-plan product or compare).  A plan that the product test admits is
+// admitted here; the rare path scores the admitted rows exactly.
+template <bool HAS_S2>
+__device__ __forceinline__ uint32_t sweep_thr_ydiv(float ty, float M, float S2, const float* s_t) {
+    float cp = ty + M;
+    if (HAS_S2) cp = fmaxf(cp, S2);
+    const uint32_t off = (__float_as_uint(cp) >> 16) & 0x3fcu;
+    return *(const uint32_t*)((const char*)s_t + off);
+}
+
 // Per-backend pressure (not uniform): the level-k state of a row of the
 // sweep, for the exact per-level tests of the seeding pass and of the rare
 // path.  `dg` holds the prefix digits of the block.  NPRE > 0: the prefix has
@@ -786,11 +812,45 @@ __device__ void general_row(PD P, JD J, uint64_t b, int big, int ix, float cx, f
 // RY > 0: every source of the launch has R_y = RY; the y table is loaded once
 // per workgroup into scalar registers and the y loop is fully unrolled, so the
 // inner sweep issues no memory load and no wait other than its LDS bin reads.
-// B256: every source of the launch has the 256-bin table (P->jsh = 18).
+// B256: every source of the launch has the 256-bin table (P->jsh = 18); with
+// RY > 0 the table is held per implementation of y, pre-divided by its factor
+// (s_bins[j][256], sweep_test_ydiv).
 // RAD > 0: every prefix node of every source has RAD implementations and the
 // block indices fit 32 bits (constant-divisor digits).
 // The inner sweep of block b (the prefix pf evaluated): every (x, y) pair,
 // the prefilter per plan, the exact test in the rare path.
+// Rare path of the sweep: a lane whose row (x = ix) of block b passed the
+// prefilter (mine) re-scores it with the exact test.
+template <bool HAS_S2, int NPRE>
+__device__ __forceinline__ void sweep_rare(PD P, JD J, uint64_t b, bool live, int ix, float cx, float M, float S2,
+                                           bool mine, float* s_f) {
+    if (!(live && mine)) return;
+    if (!P->uniform) {
+        general_row<HAS_S2, NPRE>(P, J, b, J->big, ix, cx, M, S2, s_f);
+        return;
+    }
+    const CS float2* aty = cs(P->aty);
+    const int ry = P->ry;
+    const uint64_t base = (b * (uint64_t)P->rx + (uint64_t)ix) * (uint64_t)ry;
+    for (int iy = 0; iy < ry; ++iy) {
+        const float2 vy = aty[iy];
+        float cp = vy.y + M;
+        if (HAS_S2) cp = fmaxf(cp, S2);
+        const float cc = cx * vy.x;
+        const uint64_t idx = base + (uint64_t)iy;
+        if (idx - J->begin < J->count && is_candidate(P, J, cp, cc)) append_cand(J, idx, cc, cp);
+    }
+}
+
+// The row's least pre-divided threshold (see sweep_thr_ydiv).
+template <bool HAS_S2, int RY>
+__device__ __forceinline__ uint32_t sweep_row_ydiv(const float2 (&vyr)[RY], float M, float S2, const float* s_bins) {
+    uint32_t m = sweep_thr_ydiv<HAS_S2>(vyr[0].y, M, S2, s_bins);
+#pragma unroll
+    for (int j = 1; j < RY; ++j) m = min(m, sweep_thr_ydiv<HAS_S2>(vyr[j].y, M, S2, s_bins + j * NBINS2));
+    return m;
+}
+
 template <bool HAS_S2, int RY, int NPRE, bool B256>
 __device__ __forceinline__ void sweep_block(PD P, JD J, uint64_t b, bool live, const Prefix& pf,
                                             const float2 (&vyr)[RY > 0 ? RY : 1], const float* s_bins,
@@ -799,7 +859,20 @@ __device__ __forceinline__ void sweep_block(PD P, JD J, uint64_t b, bool live, c
     const CS float2* atx = cs(P->atx);
     const CS float2* aty = cs(P->aty);
     const int rx = P->rx, ry = P->ry;
-    const bool exy = P->edge_xy != 0;
+    // without a second sink x is no sink, so it feeds y
+    const bool exy = !HAS_S2 || P->edge_xy != 0;
+    if constexpr (B256 && RY > 0) {
+        for (int ix = 0; ix < rx; ++ix) {
+            const float2 vx = atx[ix];
+            const float fx = vx.y + pf.px;
+            const float cx = pf.pc * vx.x;
+            const float M = exy ? fmaxf(pf.py, fx) : pf.py;
+            const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
+            const bool mine = cx >= __uint_as_float(sweep_row_ydiv<HAS_S2, RY>(vyr, M, S2, s_bins));
+            if (live && mine) sweep_rare<HAS_S2, NPRE>(P, J, b, live, ix, cx, M, S2, mine, s_f);
+        }
+        return;
+    }
     for (int ix = 0; ix < rx; ++ix) {
         const float2 vx = atx[ix];
         const float fx = vx.y + pf.px;
@@ -810,8 +883,7 @@ __device__ __forceinline__ void sweep_block(PD P, JD J, uint64_t b, bool live, c
         int iy = 0;
         if (RY > 0) {
 #pragma unroll
-            for (int j = 0; j < (RY > 0 ? RY : 1); ++j)
-                hit |= sweep_test<HAS_S2, B256>(vyr[j], M, S2, cx, sh, s_bins);
+            for (int j = 0; j < (RY > 0 ? RY : 1); ++j) hit |= sweep_test<HAS_S2, B256>(vyr[j], M, S2, cx, sh, s_bins);
             iy = ry;
         }
         for (; iy + 4 <= ry; iy += 4) {
@@ -822,22 +894,7 @@ __device__ __forceinline__ void sweep_block(PD P, JD J, uint64_t b, bool live, c
             hit |= sweep_test<HAS_S2, B256>(v3, M, S2, cx, sh, s_bins);
         }
         for (; iy < ry; ++iy) hit |= sweep_test<HAS_S2, B256>(aty[iy], M, S2, cx, sh, s_bins);
-        if (hit) {
-            // rare: re-score this lane's row of the inner sweep with the exact test
-            const uint64_t base = (b * (uint64_t)rx + (uint64_t)ix) * (uint64_t)ry;
-            if (live && (hit >> (threadIdx.x & 63) & 1ull) && !P->uniform) {
-                general_row<HAS_S2, NPRE>(P, J, b, J->big, ix, cx, M, S2, s_f);
-            } else if (live && (hit >> (threadIdx.x & 63) & 1ull)) {
-                for (int iy = 0; iy < ry; ++iy) {
-                    const float2 vy = aty[iy];
-                    float cp = vy.y + M;
-                    if (HAS_S2) cp = fmaxf(cp, S2);
-                    const float cc = cx * vy.x;
-                    const uint64_t idx = base + (uint64_t)iy;
-                    if (idx - J->begin < J->count && is_candidate(P, J, cp, cc)) append_cand(J, idx, cc, cp);
-                }
-            }
-        }
+        if (hit) sweep_rare<HAS_S2, NPRE>(P, J, b, live, ix, cx, M, S2, (hit >> (threadIdx.x & 63)) & 1ull, s_f);
     }
 }
 
@@ -848,7 +905,7 @@ __device__ __forceinline__ void sweep_block(PD P, JD J, uint64_t b, bool live, c
 // (prefix_head once, prefix_tail per block); NPRE == 0 takes one block per
 // thread.
 template <bool HAS_S2, int RY, int NPRE, bool B256, int RAD>
-__global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, uint64_t unit_off) {
+__global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, uint64_t unit_off, int pat_cap) {
     extern __shared__ float s_f[];
     JD J = cs(jobs + blockIdx.y);
     PD P = cs(J->prob);
@@ -859,19 +916,43 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
     const uint64_t t = t0 + threadIdx.x;
     const bool live = t < units;
     const uint64_t b0 = J->blk_first + (live ? t : units - 1) * (uint64_t)G;
-    __shared__ float s_bins[B256 ? NBINS2 : NBINS];
+    constexpr bool YDIV = B256 && RY > 0;
+    __shared__ float s_bins[YDIV ? (RY > 0 ? RY : 1) * NBINS2 : (B256 ? NBINS2 : NBINS)];
     if (B256) {
-        s_bins[threadIdx.x] = __uint_as_float(J->table2[threadIdx.x]);
         static_assert(!B256 || NBINS2 == WG, "one bin per thread");
+        const float thr = __uint_as_float(J->table2[threadIdx.x]);
+        if constexpr (YDIV) {
+#pragma unroll
+            for (int j = 0; j < (RY > 0 ? RY : 1); ++j)
+                s_bins[j * NBINS2 + threadIdx.x] = ydiv_threshold(thr, P->yinv[j]);
+        } else {
+            s_bins[threadIdx.x] = thr;
+        }
     } else if (threadIdx.x < NBINS) {
         s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
     }
-    const float2* pat = stage_prefix_rows<false>(P, (float2*)(s_f + (size_t)max(P->npre, 1) * WG), nullptr);
+    // dynamic LDS: one f_n column per prefix node and thread (NPRE == 0
+    // only), then the prefix nodes' rows (pat_cap entries)
+    float2* s_pat = (float2*)(s_f + (NPRE > 0 ? (size_t)0 : (size_t)max(P->npre, 1) * WG));
+    const float2* pat = stage_prefix_rows<false>(P, s_pat, nullptr, pat_cap);
+    // a wave whose lanes all lie past the last unit has nothing to score (no
+    // barrier follows)
+    if (t0 + (threadIdx.x & ~63u) >= units) return;
     float2 vyr[RY > 0 ? RY : 1];
     if (RY > 0) {
         const CS float2* aty = cs(P->aty);
 #pragma unroll
-        for (int iy = 0; iy < RY; ++iy) vyr[iy] = aty[iy];
+        for (int iy = 0; iy < RY; ++iy) {
+            vyr[iy] = aty[iy];
+            if constexpr (YDIV) {
+                // only the durations are read in the loop; keep them in
+                // scalar registers (a reload per row would wait on the LDS
+                // reads too, both counting on lgkmcnt)
+                uint32_t v = __float_as_uint(vyr[iy].y);
+                asm volatile("" : "+s"(v));
+                vyr[iy].y = __uint_as_float(v);
+            }
+        }
     }
     if constexpr (NPRE > 0) {
         const PrefixHead ph = prefix_head<NPRE, false, RAD>(P, b0, J->big, pat, nullptr);
@@ -1453,7 +1534,7 @@ __device__ __forceinline__ void sweep_block_obj(PD P, JD J, uint64_t b, bool liv
 // Work units as in k_sweep (runs of J->gblk blocks per thread with NPRE > 0);
 // B256: the 256 bins of D's pattern on shift 18 (one AND per plan).
 template <bool HAS_S2, int RY, int NPRE, bool B256 = false, int RAD = 0>
-__global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ jobs, uint64_t unit_off) {
+__global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ jobs, uint64_t unit_off, int pat_cap) {
     extern __shared__ float s_f[];
     JD J = cs(jobs + blockIdx.y);
     PD P = cs(J->prob);
@@ -1471,9 +1552,10 @@ __global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ job
     } else if (threadIdx.x < NBINS) {
         s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
     }
-    float2* s_pat = (float2*)(s_f + (size_t)max(P->npre, 1) * WG);
-    float* s_pd = (float*)(s_pat + PAT_MAX);
-    const float2* pat = stage_prefix_rows<true>(P, s_pat, s_pd);
+    // dynamic LDS as in k_sweep, then the prefix nodes' d terms (pat_cap entries)
+    float2* s_pat = (float2*)(s_f + (NPRE > 0 ? (size_t)0 : (size_t)max(P->npre, 1) * WG));
+    float* s_pd = (float*)(s_pat + pat_cap);
+    const float2* pat = stage_prefix_rows<true>(P, s_pat, s_pd, pat_cap);
     float2 vyr[RY > 0 ? RY : 1];
     float dyr[RY > 0 ? RY : 1];
     if (RY > 0) {
@@ -2762,10 +2844,15 @@ hipError_t launch_sample_sweep(const JobDev* d_jobs, int n, bool has_s2, bool ob
 }
 
 hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint64_t max_units, int npre_max,
-                        int npre_c, int ry, bool b256, bool rad12, hipStream_t s) {
+                        int npre_c, int ry, bool b256, bool rad12, int pat, hipStream_t s) {
     if (n == 0) return hipSuccess;
-    const size_t lds = (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float) +
-                       (size_t)PAT_MAX * (sizeof(float2) + (obj ? sizeof(float) : 0));
+    // prefix rows staged in LDS: the group's largest table (npre x rmax
+    // entries), at least one entry, at most PAT_MAX (larger ones are read
+    // from global memory); f_n columns only without a compile-time prefix length
+    int pat_cap = std::min(std::max(pat, 1), PAT_MAX);
+    const bool fixed = npre_c == 2 || npre_c == 4 || npre_c == 6 || npre_c == 8;
+    const size_t lds = (fixed ? (size_t)0 : (size_t)(npre_max > 0 ? npre_max : 1) * WG * sizeof(float)) +
+                       (size_t)pat_cap * (sizeof(float2) + (obj ? sizeof(float) : 0));
     for (uint64_t off = 0; off < max_units; off += MAX_GRID_X * WG) {
         uint64_t left = max_units - off;
         uint64_t gx = (left + WG - 1) / WG;
@@ -2775,18 +2862,19 @@ hipError_t launch_sweep(const JobDev* d_jobs, int n, bool has_s2, bool obj, uint
     do {                                                                                                   \
         if (obj && b256 && rad12 && RYV == 12 && NP > 0)                                                   \
             hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP, true, (RYV == 12 && NP > 0) ? 12 : 0>), grid, dim3(WG), \
-                               lds, s, d_jobs, off);                                                       \
+                               lds, s, d_jobs, off, pat_cap);                                              \
         else if (obj && b256)                                                                              \
-            hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP, true, 0>), grid, dim3(WG), lds, s, d_jobs, off);  \
+            hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP, true, 0>), grid, dim3(WG), lds, s, d_jobs, off,   \
+                               pat_cap);                                                                   \
         else if (obj)                                                                                      \
-            hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off);          \
+            hipLaunchKernelGGL((k_sweep_obj<S2, RYV, NP>), grid, dim3(WG), lds, s, d_jobs, off, pat_cap); \
         else if (b256 && rad12 && RYV == 12 && NP > 0)                                                     \
             hipLaunchKernelGGL((k_sweep<S2, RYV, NP, true, (RYV == 12 && NP > 0) ? 12 : 0>), grid, dim3(WG), lds, \
-                               s, d_jobs, off);                                                            \
+                               s, d_jobs, off, pat_cap);                                                   \
         else if (b256)                                                                                     \
-            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, true, 0>), grid, dim3(WG), lds, s, d_jobs, off);     \
+            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, true, 0>), grid, dim3(WG), lds, s, d_jobs, off, pat_cap); \
         else                                                                                               \
-            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, false, 0>), grid, dim3(WG), lds, s, d_jobs, off);    \
+            hipLaunchKernelGGL((k_sweep<S2, RYV, NP, false, 0>), grid, dim3(WG), lds, s, d_jobs, off, pat_cap); \
     } while (0)
 #define DYP_SWEEP_NP(S2, RYV)            \
     switch (npre_c) {                    \

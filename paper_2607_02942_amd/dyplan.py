@@ -78,7 +78,7 @@ class DyChoice(ctypes.Structure):
 class DyStats(ctypes.Structure):
     _fields_ = [("plans", ctypes.c_uint64), ("candidates", ctypes.c_uint64), ("fallbacks", ctypes.c_int32),
                 ("n_jobs", ctypes.c_int32), ("main_ms", ctypes.c_float), ("total_ms", ctypes.c_float),
-                ("generated_jobs", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("generated_jobs", ctypes.c_int32), ("ydiv_jobs", ctypes.c_int32)]
 
 
 class DyplanError(RuntimeError):

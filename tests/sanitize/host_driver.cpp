@@ -20,7 +20,7 @@ struct JitRows;
 hipError_t launch_init(JobDev*, int, hipStream_t) { STUB }
 hipError_t launch_table(JobDev*, int, hipStream_t) { STUB }
 hipError_t launch_sample_sweep(const JobDev*, int, bool, bool, uint64_t, int, int, int, hipStream_t) { STUB }
-hipError_t launch_sweep(const JobDev*, int, bool, bool, uint64_t, int, int, int, bool, bool, hipStream_t) { STUB }
+hipError_t launch_sweep(const JobDev*, int, bool, bool, uint64_t, int, int, int, bool, bool, int, hipStream_t) { STUB }
 hipError_t launch_sample_generic(const JobDev*, int, uint64_t, int, hipStream_t) { STUB }
 hipError_t launch_scan(const JobDev*, int, uint64_t, int, hipStream_t) { STUB }
 hipError_t launch_certify(const JobDev*, int, int, int, int, int, hipStream_t) { STUB }

@@ -45,7 +45,7 @@ def test_exports_equal_header_declarations():
 
 def test_abi_version_status_strings_and_selftest():
     lib = D.lib()
-    assert lib.dy_abi_version() == 3
+    assert lib.dy_abi_version() == 4
     assert lib.dy_selftest() == 0
     for st in (D.DY_OK, D.DY_EINVAL, D.DY_ENOTDAG, D.DY_ELIMIT, D.DY_ENOMEM, D.DY_EDEVICE):
         assert lib.dy_status_str(st).decode() not in ("", "unknown status")

@@ -147,7 +147,11 @@ def test_forkjoin8_full_golden():
     g, want = golden("forkjoin8")
     prob = wl.forkjoin8()
     assert prob.slo == g["slo"]
-    assert_choices(select(prob, [D.range_source(0, 0, 12 ** 8)])[0], want, "forkjoin8 full")
+    with D.Plan(prob) as plan:
+        got = plan.select([D.range_source(0, 0, 12 ** 8)], stream=stream())[0]
+        # the generated sweep on 256 bins, thresholds divided ahead by y's factor
+        assert plan.stats().ydiv_jobs == 1
+    assert_choices(got, want, "forkjoin8 full")
 
 
 def test_layered10_full_golden():
@@ -162,6 +166,8 @@ def test_batch6_full_golden():
     probs = wl.batch6()
     with D.Plan(probs) as plan:
         got = plan.select([D.range_source(r, 0, 12 ** 6) for r in range(wl.N_BATCH)], stream=stream())
+        # the library sweep on 256 bins, R_y = 12: thresholds divided ahead by y's factor
+        assert plan.stats().ydiv_jobs == wl.N_BATCH
     for r in range(wl.N_BATCH):
         assert_choices(got[r], want[r], f"batch6[{r}]")
 
@@ -665,3 +671,34 @@ def test_library_sweep_block_runs(begin, count):
     assert_choices(lib, [tuple(c) for c in gen], f"forkjoin8 [{begin}+{count}] library vs generated sweep")
     if (begin, count) == (0, 12 ** 8):
         assert_choices(lib, golden("forkjoin8")[1], "forkjoin8 whole space, library sweep")
+
+
+@pytest.mark.parametrize("case", ["mixed", "tiny", "zero"])
+def test_predivided_thresholds_small_and_zero_factors(case):
+    # The sweeps compare x's product with bin thresholds divided ahead by each
+    # implementation of y's factor a = 1 - w (1 - p).  Factors of 0 and below
+    # 2^-20 take the threshold 0 (every plan of them passes the prefilter and
+    # the exact test decides); factors near 1e-6 give thresholds near 1e-6.
+    # Library sweep (jit 0) and generated sweep (jit 2), whole plan space of a
+    # 6-node request with 12 implementations per node, against the oracle.
+    import dataclasses
+    base = wl.batch6_request(7)
+    p = base.p.copy()
+    w = base.w.copy()
+    y = base.n_nodes - 1
+    w[y] = 1.0  # a = p for node y
+    if case == "mixed":
+        p[y, :12] = np.array([0, 1e-7, 5e-7, 1e-6, 3e-6, 1e-3, 0.05, 0.2, 0.5, 0.7, 0.9, 1.0], np.float32)
+    elif case == "tiny":
+        p[y, :12] = np.linspace(2e-6, 9e-6, 12).astype(np.float32)
+    else:
+        p[y, :12] = 0.0
+    prob = dataclasses.replace(base, p=p, w=w)
+    n = prob.n_plans()
+    want = orc.select_range(prob, 0, n)
+    for jit in (0, 2):
+        with D.Plan(prob) as plan:
+            plan.set_option(D.DY_OPT_JIT, jit)
+            got = plan.select([D.range_source(0, 0, n)], stream=stream())[0]
+            assert plan.stats().ydiv_jobs in (0, 1)
+        assert_choices(got, want, f"{case}, jit {jit}")
