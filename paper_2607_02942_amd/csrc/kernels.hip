@@ -842,6 +842,26 @@ __device__ __forceinline__ void sweep_rare(PD P, JD J, uint64_t b, bool live, in
     }
 }
 
+// A row of the sweep that passed the prefilter, parked in its wave's LDS
+// queue until the queue fills (or the wave's work ends), when every lane of
+// the wave re-scores one parked row: the exact test then runs on the whole
+// wave at once instead of stalling it for a single lane.
+struct RareRow {
+    uint64_t b;      // block
+    uint32_t ix;     // implementation of x
+    float cx, M, S2;
+};
+constexpr int RQ = 64;  // parked rows per wave
+
+template <bool HAS_S2, int NPRE>
+__device__ __forceinline__ void flush_rare(PD P, JD J, const RareRow* q, uint32_t n, float* s_f) {
+    const uint32_t lane = threadIdx.x & 63;
+    if (lane < n) {
+        const RareRow e = q[lane];
+        sweep_rare<HAS_S2, NPRE>(P, J, e.b, true, (int)e.ix, e.cx, e.M, e.S2, true, s_f);
+    }
+}
+
 // The row's least pre-divided threshold (see sweep_thr_ydiv).
 template <bool HAS_S2, int RY>
 __device__ __forceinline__ uint32_t sweep_row_ydiv(const float2 (&vyr)[RY], float M, float S2, const float* s_bins) {
@@ -851,10 +871,12 @@ __device__ __forceinline__ uint32_t sweep_row_ydiv(const float2 (&vyr)[RY], floa
     return m;
 }
 
+// q, qn, live_mask: the wave's queue of parked rows (B256 with RY > 0 only;
+// qn is wave-uniform) and the ballot of its live lanes.
 template <bool HAS_S2, int RY, int NPRE, bool B256>
 __device__ __forceinline__ void sweep_block(PD P, JD J, uint64_t b, bool live, const Prefix& pf,
                                             const float2 (&vyr)[RY > 0 ? RY : 1], const float* s_bins,
-                                            float* s_f) {
+                                            float* s_f, RareRow* q, uint32_t& qn, uint64_t live_mask) {
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* atx = cs(P->atx);
     const CS float2* aty = cs(P->aty);
@@ -868,8 +890,22 @@ __device__ __forceinline__ void sweep_block(PD P, JD J, uint64_t b, bool live, c
             const float cx = pf.pc * vx.x;
             const float M = exy ? fmaxf(pf.py, fx) : pf.py;
             const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
-            const bool mine = cx >= __uint_as_float(sweep_row_ydiv<HAS_S2, RY>(vyr, M, S2, s_bins));
-            if (live && mine) sweep_rare<HAS_S2, NPRE>(P, J, b, live, ix, cx, M, S2, mine, s_f);
+            const uint64_t hit =
+                __ballot(cx >= __uint_as_float(sweep_row_ydiv<HAS_S2, RY>(vyr, M, S2, s_bins))) & live_mask;
+            if (hit) {
+                const uint32_t nh = (uint32_t)__popcll(hit);
+                if (qn + nh > (uint32_t)RQ) {
+                    flush_rare<HAS_S2, NPRE>(P, J, q, qn, s_f);
+                    qn = 0;
+                }
+                const uint32_t lane = threadIdx.x & 63;
+                if (hit >> lane & 1ull) {
+                    const uint32_t o = qn + __builtin_amdgcn_mbcnt_hi((uint32_t)(hit >> 32),
+                                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)hit, 0u));
+                    q[o] = RareRow{b, (uint32_t)ix, cx, M, S2};
+                }
+                qn += nh;
+            }
         }
         return;
     }
@@ -954,15 +990,20 @@ __global__ void __launch_bounds__(WG) k_sweep(const JobDev* __restrict__ jobs, u
             }
         }
     }
+    __shared__ RareRow s_q[YDIV ? WG / 64 : 1][RQ];
+    RareRow* q = s_q[YDIV ? threadIdx.x >> 6 : 0];
+    uint32_t qn = 0;
+    const uint64_t live_mask = __ballot(live);
     if constexpr (NPRE > 0) {
         const PrefixHead ph = prefix_head<NPRE, false, RAD>(P, b0, J->big, pat, nullptr);
         for (int g = 0; g < G; ++g)
             sweep_block<HAS_S2, RY, NPRE, B256>(P, J, b0 + (uint64_t)g, live, prefix_tail<NPRE, false>(P, ph, g, pat, nullptr),
-                                                vyr, s_bins, s_f);
+                                                vyr, s_bins, s_f, q, qn, live_mask);
     } else {
         const Prefix pf = prefix_eval<NPRE, false, RAD>(P, b0, J->big, s_f, pat, nullptr);
-        sweep_block<HAS_S2, RY, NPRE, B256>(P, J, b0, live, pf, vyr, s_bins, s_f);
+        sweep_block<HAS_S2, RY, NPRE, B256>(P, J, b0, live, pf, vyr, s_bins, s_f, q, qn, live_mask);
     }
+    if (YDIV && qn) flush_rare<HAS_S2, NPRE>(P, J, q, qn, s_f);
 }
 
 // Work unit of sample j: one unit of the window [j S, min((j+1) S, n)), at a
