@@ -29,7 +29,7 @@ hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, 
 hipError_t launch_exhaust(const JobDev* d_jobs, int njobs, uint64_t max_units, hipStream_t s);
 hipError_t launch_reseed(const JobDev* d_jobs, int njobs, hipStream_t s);
 hipError_t launch_seed_cands(const JobDev* d_jobs, int njobs, int kmax, int nmax, hipStream_t s);
-hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, hipStream_t s);
+hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, int entries, hipStream_t s);
 hipError_t static_scratch(int device, char** ptr, size_t* bytes);
 struct JitRows {
     hipModule_t mod = nullptr;
@@ -373,6 +373,7 @@ struct PassPlan {
     bool b256[kSweepGroups] = {true, true, true, true};  // every library-sweep source has the 256-bin table
     bool rad12[kSweepGroups] = {true, true, true, true}; // ... and 12 implementations per prefix node, 32-bit blocks
     int kmax = 1;                         // most levels of any source
+    int climb_e = 0;                      // largest sum of radices of a source that climbs
     int ncol = 1;                         // most nodes of any source of the generic group
     int before(int g) const {             // jobs stored ahead of group g
         int t = 0;
@@ -1542,6 +1543,11 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
             J.sync = S.sync + q;
             J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
             J.climb = climb && climb_ok(j) ? 1 : 0;
+            if (J.climb) {
+                int e = 0;
+                for (int n = 0; n < H.n; ++n) e += h->hdesc[src[j].problem].radix[n];
+                pp.climb_e = std::max(pp.climb_e, e);
+            }
             // seeding work units: rows of the inner sweep, or plans
             const bool sweep = g < kSweepGroups;
             const uint64_t sunits = sweep ? J.nblk * (uint64_t)H.rx : J.count;
@@ -1615,11 +1621,16 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         C.any_split = false;
         for (int q = n3; q < n3 + pp.n[G_JIT]; ++q) C.any_split = C.any_split || split_at(jobs[q]) != 0;
         C.any_climb = false;
-        C.climb_modes = 0;  // bit 0: a corr / SLO source climbs, bit 1: an objective one
+        // bit 0: a corr / SLO source climbs, bit 1: an objective one; bit 2:
+        // every corr / SLO source that climbs is under uniform pressure (its
+        // levels can share one search)
+        C.climb_modes = 4;
         for (int q = 0; q < n3; ++q)
             if (jobs[q].climb) {
+                const ProbDev& Dq = h->hdesc[(int)(jobs[q].prob - h->d_probs)];
                 C.any_climb = true;
-                C.climb_modes |= h->hdesc[(int)(jobs[q].prob - h->d_probs)].obj ? 2 : 1;
+                C.climb_modes |= Dq.obj ? 2 : 1;
+                if (!Dq.obj && !Dq.uniform) C.climb_modes &= ~4;
             }
         C.src.assign(src, src + n_src);
         C.cap = cap;
@@ -1670,7 +1681,8 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         launch_seed(h, S.d_jobs, jobs.data(), pp, st, ck);
         if (any_climb)
             for (int c = 0; c < n3; c += 65535)
-                ck(launch_climb(S.d_jobs + c, std::min(65535, n3 - c), pp.kmax, climb_modes, st), "climb");
+                ck(launch_climb(S.d_jobs + c, std::min(65535, n3 - c), pp.kmax, climb_modes, pp.climb_e, st),
+                   "climb");
         jit_pass(jobs.data(), n3, pp.n[G_JIT], true, st, ck);
         launch_table_all(S.d_jobs, n_src, st, ck);
     };

@@ -348,6 +348,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     if (obj) o << "    s_pd[i] = e < rmax ? dem[n * rmax + e] : 0.0f;\n";
     o << R"(  }
   __syncthreads();
+  if (t0 + (threadIdx.x & ~63u) >= nblk) return;  // a wave past the last block (no barrier follows)
   const unsigned long long t = t0 + threadIdx.x;
   const bool live = t < nblk;
   const unsigned long long b = blk_first + (live ? t : nblk - 1);

@@ -1241,32 +1241,65 @@ __device__ __forceinline__ float climb_est(PD P, int N, const float (&u)[NN], co
 // The block has blockDim.x = 64 W threads (W waves): few (source, level)
 // pairs take W = 16, so that each move pass is one short round (the pass is
 // latency-bound), many take W = 1.
-template <int NN, bool OBJ>
-__global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs) {
-    __shared__ float s_a[CLIMB_ENTRIES], s_t[CLIMB_ENTRIES];  // node tables, entry off[n] + i
-    __shared__ float s_d[OBJ ? CLIMB_ENTRIES : 1];             // objective mode: d
-    __shared__ uint8_t s_node[CLIMB_ENTRIES];                 // node of entry e
-    __shared__ uint8_t s_keep[CLIMB_ENTRIES];                 // entry e is Pareto-optimal at the level
-    __shared__ int16_t s_fe[CLIMB_ENTRIES];                   // the kept entries, node by node
-    __shared__ int32_t s_pn[NN * (NN - 1) / 2 + 1];           // pair p = (n1, n2): n1 * NMAX + n2
-    __shared__ int32_t s_po[NN * (NN - 1) / 2 + 1];           // first move of pair p (flat pair-move order)
+// Bytes of one search's LDS tables for E entries: a, tau (and d in objective
+// mode) as fp32, the kept entries as int16, node and kept flag as bytes.
+__host__ __device__ constexpr size_t climb_slot_bytes(int E, bool obj) {
+    return ((size_t)E * (4 + 4 + (obj ? 4 : 0) + 2 + 1 + 1) + 7) & ~(size_t)7;
+}
+
+// Wave-level sync of a packed search (its wave is alone in its tables), or
+// the block's barrier when the block's waves share one search.
+__device__ __forceinline__ void climb_sync(bool pack) {
+    if (pack) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    } else {
+        __syncthreads();
+    }
+}
+
+// Launch shapes: blockDim.x = 256 packs four searches per block, one per
+// wave, search blockIdx.x * 4 + wave = (source, level) in source-major order
+// (nsearch searches in all); blockDim.x = 1024 gives one search, source
+// blockIdx.y and level blockIdx.x, to all 16 waves.  E: entries of the
+// largest table set (the sum of a problem's radices) of the launch, at most
+// CLIMB_ENTRIES; dynamic LDS holds climb_slot_bytes(E) per search.
+template <int NN, bool OBJ, bool CHAIN = false>
+__global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs, int nsearch, int kmax, int E) {
+    extern __shared__ uint64_t s_climb_dyn[];
+    __shared__ int32_t s_pn[4][NN * (NN - 1) / 2 + 1];  // pair p = (n1, n2): n1 * NMAX + n2
+    __shared__ int32_t s_po[4][NN * (NN - 1) / 2 + 1];  // first move of pair p (flat pair-move order)
     __shared__ uint64_t s_red[16];
-    JD J = cs(jobs + blockIdx.y);
+    const bool pack = blockDim.x == 256;
+    // the wave's slot, wave-uniform (scalar), so that its tables' addresses are too
+    const int slot = pack ? __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) : 0;
+    int ji = blockIdx.y, k = blockIdx.x;
+    if (pack) {
+        const int q = (int)blockIdx.x * 4 + slot;
+        if (q >= nsearch) return;
+        ji = CHAIN ? q : q / kmax;
+        k = CHAIN ? 0 : q % kmax;
+    }
+    // this search's tables: node tables (entry off[n] + i), node of entry e,
+    // entry e is Pareto-optimal at the level, the kept entries node by node
+    char* tb = (char*)s_climb_dyn + (size_t)slot * climb_slot_bytes(E, OBJ);
+    float* s_a = (float*)tb;
+    float* s_t = s_a + E;
+    float* s_d = s_t + (OBJ ? E : 0);  // objective mode: d
+    int16_t* s_fe = (int16_t*)(s_t + E + (OBJ ? E : 0));
+    uint8_t* s_node = (uint8_t*)(s_fe + E);
+    uint8_t* s_keep = s_node + E;
+    int32_t* s_pnv = s_pn[slot];
+    int32_t* s_pov = s_po[slot];
+    JD J = cs(jobs + ji);
     if (!J->climb) return;
     PD P = cs(J->prob);
-    const int k = blockIdx.x;
-    const int N = P->n, R = P->rmax, lane = threadIdx.x & 63, tid = threadIdx.x, nt = blockDim.x;
-    if (k >= P->k || (P->obj != 0) != OBJ || N > NN) return;
-    // objective mode: a greater u and a smaller tau and d never lower J_k
-    // only when lambda_l and lambda_ld L_k are not negative
-    const float mk = OBJ ? P->m32[k] : 0.0f;
-    if (OBJ && (!(P->lam_l >= 0.0f) || !(mk >= 0.0f))) return;
+    const int N = P->n, R = P->rmax, lane = threadIdx.x & 63;
+    const int tid = pack ? lane : (int)threadIdx.x, nt = pack ? 64 : (int)blockDim.x;
+    if ((P->obj != 0) != OBJ || N > NN) return;
     const bool uni = OBJ || P->uniform != 0;
-    // durations the band is tested on: the unpressured ones against lo_k
-    // (uniform pressure), else the level's own against the exact band
     const CS float2* at = cs(P->at);
-    const CS float* lt = uni ? nullptr : cs(P->lat) + (size_t)k * N * R;
-    const float band = uni ? P->lo[k] : P->glo;
     int off[NN + 1];
     int tot = 0;
 #pragma unroll
@@ -1275,7 +1308,46 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
         if (n < N) tot += P->radix[n];
     }
     off[NN] = tot;
-    if (tot > CLIMB_ENTRIES) return;
+    if (tot > E) return;
+    // CHAIN: the wave climbs every level of its source in turn.  Under
+    // uniform pressure the levels share the tables, their Pareto sets and the
+    // start, and are taken from the tightest band to the loosest, each from
+    // the plan the previous one reached (feasible at any looser band too);
+    // otherwise each level is set up and started afresh.
+    const bool chain = CHAIN && P->uniform != 0;
+    const int nlev = CHAIN ? P->k : 1;
+    const int ksel = k;
+    int foff[NN + 1];
+    int ftot = 0;
+    int cur[NN];
+    float ca[NN], ct[NN], cd[NN];
+    bool pairs_ok = false;
+    const int npairs = N * (N - 1) / 2;
+    // move keys order by the value: corr bits (non-negative), or the
+    // order-preserving key of the estimate
+    auto vkey = [&](float v) -> uint32_t { return OBJ ? fkey(v) : __float_as_uint(v); };
+    auto block_max = [&](uint64_t v) {
+        v = wave_max_u64(v);
+        if (nt == 64) return v;
+        if (lane == 0) s_red[tid >> 6] = v;
+        climb_sync(pack);
+        uint64_t b = 0;
+        for (int w = 0; w < (nt >> 6); ++w) b = s_red[w] > b ? s_red[w] : b;
+        climb_sync(pack);
+        return b;
+    };
+    for (int li = 0; li < nlev; ++li) {
+    const int k = CHAIN ? (chain ? P->lvl_order[P->k - 1 - li] : li) : ksel;
+    if (k >= P->k) continue;
+    // objective mode: a greater u and a smaller tau and d never lower J_k
+    // only when lambda_l and lambda_ld L_k are not negative
+    const float mk = OBJ ? P->m32[k] : 0.0f;
+    if (OBJ && (!(P->lam_l >= 0.0f) || !(mk >= 0.0f))) continue;
+    // durations the band is tested on: the unpressured ones against lo_k
+    // (uniform pressure), else the level's own against the exact band
+    const CS float* lt = uni ? nullptr : cs(P->lat) + (size_t)k * N * R;
+    const float band = uni ? P->lo[k] : P->glo;
+    if (li == 0 || !chain) {
     for (int n = 0; n < N; ++n)
         for (int i = tid; i < P->radix[n]; i += nt) {
             const float2 v = at[n * R + i];
@@ -1284,7 +1356,7 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
             if (OBJ) s_d[off[n] + i] = cs(P->dem)[n * R + i];
             s_node[off[n] + i] = (uint8_t)n;
         }
-    __syncthreads();
+    climb_sync(pack);
     for (int e = tid; e < tot; e += nt) {
         const int n = s_node[e];
         int lo = 0, hi = 0;
@@ -1302,10 +1374,9 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
         }
         s_keep[e] = keep ? 1 : 0;
     }
-    __syncthreads();
+    climb_sync(pack);
     // compact the kept entries per node (ballot and prefix count)
-    int foff[NN + 1];
-    int ftot = 0;
+    ftot = 0;
 #pragma unroll
     for (int n = 0; n < NN; ++n) {
         foff[n] = ftot;
@@ -1320,11 +1391,9 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
             }
     }
     foff[NN] = ftot;
-    __syncthreads();
+    climb_sync(pack);
     // start: every node's fastest kept implementation (the fastest of all);
     // objective mode: every node's best kept entry by u - lambda_l tau - m_k d
-    int cur[NN];
-    float ca[NN], ct[NN], cd[NN];
 #pragma unroll
     for (int n = 0; n < NN; ++n) {
         cur[n] = 0;
@@ -1346,22 +1415,11 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
             if (OBJ) cd[n] = s_d[off[n] + cur[n]];
         }
     }
-    float cc, ccp = 0.0f;
-    if (OBJ) {
-        cc = climb_est<NN>(P, N, ca, ct, cd, -1, 0.0f, 0.0f, 0.0f, -1, 0.0f, 0.0f, 0.0f, mk);
-    } else {
-        climb_eval<NN>(P, N, ca, ct, -1, 0.0f, 0.0f, -1, 0.0f, 0.0f, cc, ccp);
-        if (!(ccp <= band)) return;  // no plan is certainly feasible at this level
-    }
-    // move keys order by the value: corr bits (non-negative), or the
-    // order-preserving key of the estimate
-    auto vkey = [&](float v) -> uint32_t { return OBJ ? fkey(v) : __float_as_uint(v); };
     uint32_t pairs = 0;
 #pragma unroll
     for (int n = 0; n < NN; ++n)
         if (n < N) pairs += (uint32_t)(foff[n + 1] - foff[n]) * (uint32_t)(ftot - foff[n + 1]);
-    const bool pairs_ok = pairs <= CLIMB_PAIRS;
-    const int npairs = N * (N - 1) / 2;
+    pairs_ok = pairs <= CLIMB_PAIRS;
     if (tid == 0) {  // pairs in (n1, n2) order and where their moves start
         int p = 0, o = 0;
         for (int n1 = 0; n1 < N; ++n1)
@@ -1372,24 +1430,22 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
                     if (m == n1) F1 = foff[m + 1] - foff[m];
                     if (m == n2) F2 = foff[m + 1] - foff[m];
                 }
-                s_pn[p] = n1 * NMAX + n2;
-                s_po[p] = o;
+                s_pnv[p] = n1 * NMAX + n2;
+                s_pov[p] = o;
                 o += F1 * F2;
                 ++p;
             }
-        s_po[p] = o;
+        s_pov[p] = o;
     }
-    __syncthreads();
-    auto block_max = [&](uint64_t v) {
-        v = wave_max_u64(v);
-        if (nt == 64) return v;
-        if (lane == 0) s_red[tid >> 6] = v;
-        __syncthreads();
-        uint64_t b = 0;
-        for (int w = 0; w < (nt >> 6); ++w) b = s_red[w] > b ? s_red[w] : b;
-        __syncthreads();
-        return b;
-    };
+    climb_sync(pack);
+    }  // set-up of the level
+    float cc, ccp = 0.0f;
+    if (OBJ) {
+        cc = climb_est<NN>(P, N, ca, ct, cd, -1, 0.0f, 0.0f, 0.0f, -1, 0.0f, 0.0f, 0.0f, mk);
+    } else {
+        climb_eval<NN>(P, N, ca, ct, -1, 0.0f, 0.0f, -1, 0.0f, 0.0f, cc, ccp);
+        if (!(ccp <= band)) continue;  // no plan is certainly feasible at this level
+    }
     for (int step = 0; step < CLIMB_STEPS; ++step) {
         // single moves over the kept entries; key = (corr bits, reversed move order), 0 = none
         uint64_t best = 0;
@@ -1417,12 +1473,12 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
         bool pair = false;
         if (mv == 0 && pairs_ok) {
             // two-node moves (n1 < n2, kept entries e1 and e2) in one flat order
-            // (n1, n2, e1, e2); t -> pair p (its moves start at s_po[p]) -> (j1, j2)
-            const int total = s_po[npairs];
+            // (n1, n2, e1, e2); t -> pair p (its moves start at s_pov[p]) -> (j1, j2)
+            const int total = s_pov[npairs];
             int p = 0;
             for (int t = tid; t < total; t += nt) {
-                while (s_po[p + 1] <= t) ++p;
-                const int n1 = s_pn[p] / NMAX, n2 = s_pn[p] % NMAX;
+                while (s_pov[p + 1] <= t) ++p;
+                const int n1 = s_pnv[p] / NMAX, n2 = s_pnv[p] % NMAX;
                 int c1 = 0, o1 = 0, f1 = 0, c2 = 0, o2 = 0, f2 = 0, F2 = 1;
 #pragma unroll
                 for (int m = 0; m < NN; ++m) {
@@ -1438,9 +1494,9 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
                         F2 = foff[m + 1] - foff[m];
                     }
                 }
-                // t - s_po[p] = j1 F2 + j2; the float quotient is exact: (x + 0.5) / F2
+                // t - s_pov[p] = j1 F2 + j2; the float quotient is exact: (x + 0.5) / F2
                 // stays at least 0.5 / F2 >= 2^-10 away from an integer, far above its error
-                const int x = t - s_po[p];
+                const int x = t - s_pov[p];
                 const int j1 = (int)(((float)x + 0.5f) / (float)F2);
                 const int j2 = x - j1 * F2;
                 const int e1 = s_fe[f1 + j1], e2 = s_fe[f2 + j2];
@@ -1491,6 +1547,7 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs)
     }
     // the seed slot's format: corr bits + 1, or the estimate's key
     if (tid == 0) atomicMax(J->scert + k * NSLOT, OBJ ? fkey(cc) : __float_as_uint(cc) + 1u);
+    }  // levels
 }
 
 // ---------------------------------------------------------------------------
@@ -2833,14 +2890,29 @@ hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s) {
 
 // Problems above CLIMB_NODES nodes take no climb (the kernel returns for them).
 // modes: bit 0 sources of corr / SLO problems climb, bit 1 of objective ones
-hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, hipStream_t s) {
+hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, int entries, hipStream_t s) {
     if (njobs == 0) return hipSuccess;
-    // few (source, level) pairs: 16 waves each (latency); many: one wave each
-    const int threads = (size_t)njobs * (size_t)kmax <= 1024 ? 1024 : 64;
-    if (modes & 1) hipLaunchKernelGGL((k_climb<CLIMB_NODES, false>), dim3(kmax, njobs), dim3(threads), 0, s, d_jobs);
+    const int E = std::min(std::max(entries, 1), CLIMB_ENTRIES);
+    // few (source, level) pairs: 16 waves each (latency); many: one wave
+    // each, four to a block (a CU holds few blocks, so one-wave blocks would
+    // leave it short of waves)
+    const int nsearch = njobs * kmax;
+    const bool coop = nsearch <= 1024;
+    const dim3 grid = coop ? dim3(kmax, njobs) : dim3((unsigned)((nsearch + 3) / 4));
+    const dim3 block(coop ? 1024 : 256);
+    const int slots = coop ? 1 : 4;
+    // corr mode, many sources, each under uniform pressure: one wave per
+    // source climbs its levels in turn
+    if ((modes & 1) && (modes & 4) && !coop)
+        hipLaunchKernelGGL((k_climb<CLIMB_NODES, false, true>), dim3((unsigned)((njobs + 3) / 4)), block,
+                           slots * climb_slot_bytes(E, false), s, d_jobs, njobs, kmax, E);
+    else if (modes & 1)
+        hipLaunchKernelGGL((k_climb<CLIMB_NODES, false>), grid, block, slots * climb_slot_bytes(E, false), s, d_jobs,
+                           nsearch, kmax, E);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !(modes & 2)) return e;
-    hipLaunchKernelGGL((k_climb<CLIMB_NODES, true>), dim3(kmax, njobs), dim3(threads), 0, s, d_jobs);
+    hipLaunchKernelGGL((k_climb<CLIMB_NODES, true>), grid, block, slots * climb_slot_bytes(E, true), s, d_jobs, nsearch,
+                       kmax, E);
     return hipGetLastError();
 }
 
