@@ -2029,6 +2029,7 @@ __device__ __forceinline__ void wave_best4(double& c, uint64_t& i, double& cp, d
 
 constexpr int CERT_LDS_TABLES = 32 * 1024;  // fp64 tables staged in LDS when they fit
 constexpr int CERT_CACHE = 512;             // candidates cached in LDS by each certification wave
+constexpr int CERT_PACK_CACHE = 64;         // ... when four waves share a block
 
 // Merge of a source's certification waves into its K choices, by the block
 // that finishes certification last (64 threads).  When no list overflowed and
@@ -2170,17 +2171,39 @@ __device__ __forceinline__ void cert_eval(PD P, int N, int R, const uint8_t* ids
 // lane walks its candidates once per block instead of once per level.
 // Dynamic LDS: tab_d doubles for the fp64 tables (0: read from global memory),
 // then the recurrence column f [nf][64] (fp64) and the ids [nf][64], nf >= N.
-__global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs, int tab_d, int nf) {
+// Dynamic LDS of one certification wave, in doubles: the fp64 tables (tab_d),
+// nf node values and nf id bytes per lane, `cache` candidates.
+__host__ __device__ constexpr size_t cert_slot_doubles(int tab_d, int nf, int cache) {
+    return (size_t)tab_d + (size_t)nf * 64 + ((size_t)nf * 64 + 7) / 8 + (size_t)cache * (sizeof(Cand) / 8);
+}
+
+// PACK = false: grid (waves, sources, levels), 64 threads, the source's
+// cert_waves waves per level, `cache` = CERT_CACHE candidates in LDS.
+// PACK = true (every source has one wave per level and no host-mapped copy):
+// blockDim 256, four (source, level) searches per block, one per wave,
+// search blockIdx.x * 4 + wave in source-major order (nsearch in all), each
+// with its own LDS slot (a CU holds few one-wave blocks).
+template <bool PACK>
+__global__ void __launch_bounds__(256) k_certify(const JobDev* __restrict__ jobs, int tab_d, int nf, int cache,
+                                                 int nsearch, int kmax) {
     extern __shared__ double s_dyn64[];
-    double* s_tab = s_dyn64;
-    double* s_f = s_dyn64 + tab_d;
+    const int slot = PACK ? __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) : 0;
+    double* s_tab = s_dyn64 + (size_t)slot * cert_slot_doubles(tab_d, nf, cache);
+    double* s_f = s_tab + tab_d;
     uint8_t* s_id = (uint8_t*)(s_f + (size_t)nf * 64);
-    __shared__ Cand s_cand[CERT_CACHE];
-    JD J = cs(jobs + blockIdx.y);
+    Cand* s_cand = (Cand*)(s_f + (size_t)nf * 64 + ((size_t)nf * 64 + 7) / 8);
+    int ji = blockIdx.y, g = blockIdx.x, k = blockIdx.z;
+    if (PACK) {
+        const int q = (int)blockIdx.x * 4 + slot;
+        if (q >= nsearch) return;
+        ji = q / kmax;
+        k = q % kmax;
+        g = 0;
+    }
+    JD J = cs(jobs + ji);
     PD P = cs(J->prob);
-    const int g = blockIdx.x, k = blockIdx.z;
     if (g >= J->cert_waves || k >= P->k) return;
-    const int N = P->n, R = P->rmax, lane = threadIdx.x;
+    const int N = P->n, R = P->rmax, lane = threadIdx.x & 63;
     const uint32_t nc = min(*J->ncand, J->cap);
     uint8_t* ids = s_id + lane;
     double* f = s_f + lane;
@@ -2202,10 +2225,16 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs,
     }
     static_assert(NSLOT == 64, "one seed slot per lane");
     const uint32_t sl = J->scert[k * NSLOT + lane];
-    const uint32_t ncache = min(nc, (uint32_t)CERT_CACHE);
+    const uint32_t ncache = min(nc, (uint32_t)cache);
 #pragma unroll 8
     for (uint32_t i = lane; i < ncache; i += 64) s_cand[i] = J->cand[i];
-    __syncthreads();
+    if (PACK) {  // the wave is alone in its slot
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    } else {
+        __syncthreads();
+    }
     const uint32_t step = 64u * (uint32_t)J->cert_waves;
     double bc = -INFINITY, bcp = 0.0, bd = 0.0;
     uint64_t bi = ~0ull;
@@ -2294,6 +2323,7 @@ __global__ void __launch_bounds__(64) k_certify(const JobDev* __restrict__ jobs,
         }
         return;
     }
+    if (PACK) return;  // not reached: PACK launches have one wave per level and no host copy
     if (lane == 0) {
         J->cert_c[k * CERT_WAVES + g] = bc;
         J->cert_i[k * CERT_WAVES + g] = bi;
@@ -3043,8 +3073,20 @@ hipError_t launch_scan(const JobDev* d_jobs, int n, uint64_t max_units, int ncol
 hipError_t launch_certify(const JobDev* d_jobs, int njobs, int waves, int kmax, int nmax, int nrmax, hipStream_t s) {
     // LDS sized by the plan's largest DAG (a fixed 58 KB let two blocks share a CU)
     const int tab_d = 3 * nrmax * (int)sizeof(double) <= CERT_LDS_TABLES ? 3 * nrmax : 0;
-    const size_t lds = ((size_t)tab_d + (size_t)nmax * 64) * sizeof(double) + (size_t)nmax * 64;
-    hipLaunchKernelGGL(k_certify, dim3(waves, njobs, kmax), dim3(64), lds, s, d_jobs, tab_d, nmax);
+    // one wave per (source, level): four to a block, CERT_PACK_CACHE
+    // candidates cached per wave (the rest are read from global memory), the
+    // fp64 tables in LDS up to 8 KB per wave, at most 64 KB per block
+    const int tab_p = 3 * nrmax * (int)sizeof(double) <= 8192 ? 3 * nrmax : 0;
+    const size_t lds_p = 4 * cert_slot_doubles(tab_p, nmax, CERT_PACK_CACHE) * sizeof(double);
+    if (waves == 1 && lds_p <= 65536) {
+        const int nsearch = njobs * kmax;
+        hipLaunchKernelGGL(k_certify<true>, dim3((unsigned)((nsearch + 3) / 4)), dim3(256), lds_p, s, d_jobs, tab_p,
+                           nmax, CERT_PACK_CACHE, nsearch, kmax);
+        return hipGetLastError();
+    }
+    const size_t lds = cert_slot_doubles(tab_d, nmax, CERT_CACHE) * sizeof(double);
+    hipLaunchKernelGGL(k_certify<false>, dim3(waves, njobs, kmax), dim3(64), lds, s, d_jobs, tab_d, nmax, CERT_CACHE,
+                       0, kmax);
     return hipGetLastError();
 }
 
