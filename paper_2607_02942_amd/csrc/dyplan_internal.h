@@ -15,6 +15,7 @@ constexpr int NBINS = 64;        // lane-resident prefilter table: one bin per l
 constexpr int NBINS2 = 256;      // bins of the generated sweep's prefilter (one shift-and-mask operation)
 constexpr int NSLOT = 64;        // per-level atomic slots of the seeding pass (spreads contention)
 constexpr int CERT_WAVES = 8;    // waves per source in certification when sources are few
+constexpr int CLIMB_ENTRIES = 512;  // local search: largest sum of a problem's radices (its tables in LDS), else none
 
 // Unsigned 32-bit division by an invariant divisor (Granlund & Montgomery,
 // PLDI 1994, Fig. 4.1): q = (t + ((x - t) >> sh1)) >> sh2, t = mulhi(m, x).

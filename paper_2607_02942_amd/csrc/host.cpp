@@ -369,6 +369,7 @@ struct PassPlan {
     int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
     int pat[kSweepGroups] = {};           // largest prefix-row table (npre x rmax entries) of a sweep group
     int ydiv_jit[kSweepGroups] = {};      // generated sweeps (corr mode) on thresholds pre-divided by y's factor
+    int sample_lib[kSweepGroups] = {};    // library-sweep sources the sampling pass seeds (see launch_seed)
     int njit[kSweepGroups] = {};          // trailing sources of the group that run their generated sweep
     bool b256[kSweepGroups] = {true, true, true, true};  // every library-sweep source has the 256-bin table
     bool rad12[kSweepGroups] = {true, true, true, true}; // ... and 12 implementations per prefix node, 32-bit blocks
@@ -1298,7 +1299,7 @@ void launch_seed(const dy_plan* h, const JobDev* d, const JobDev* hjobs, const P
                                     pp.kmax, s),
                 "sample");
         };
-        chunks(d + pp.before(g), lib, lib_launch);
+        if (pp.sample_lib[g] > 0) chunks(d + pp.before(g), lib, lib_launch);
         for (int q = pp.before(g) + lib; q < pp.before(g) + pp.n[g]; ++q) {
             const int p = (int)(hjobs[q].prob - h->d_probs);
             if (h->jit[p].seed)
@@ -1543,10 +1544,10 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
             J.sync = S.sync + q;
             J.fb_levels = h->force_fp64 ? (H.k == 32 ? 0xffffffffu : ((1u << H.k) - 1u)) : 0u;
             J.climb = climb && climb_ok(j) ? 1 : 0;
+            int climb_entries = 0;  // the search's table entries (it runs when they fit CLIMB_ENTRIES)
             if (J.climb) {
-                int e = 0;
-                for (int n = 0; n < H.n; ++n) e += h->hdesc[src[j].problem].radix[n];
-                pp.climb_e = std::max(pp.climb_e, e);
+                for (int n = 0; n < H.n; ++n) climb_entries += h->hdesc[src[j].problem].radix[n];
+                pp.climb_e = std::max(pp.climb_e, climb_entries);
             }
             // seeding work units: rows of the inner sweep, or plans
             const bool sweep = g < kSweepGroups;
@@ -1569,6 +1570,16 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
                 pp.units[g] = std::max(pp.units[g], J.units);
                 pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
             }
+            // a corr / SLO source of more than 2^21 plans under uniform
+            // pressure whose levels are seeded by the local search needs no
+            // sample: the search starts from the plan of least CP, so a level
+            // it cannot seed has no certainly feasible plan at all, and on so
+            // large a space a sample of about 256 rows rarely beats the
+            // search's seed (on smaller spaces, and under per-backend pressure,
+            // where each level's search starts afresh, it does now and then)
+            const bool climb_only =
+                J.climb && !H.obj && H.uniform && climb_entries <= CLIMB_ENTRIES && J.count > (1ull << 21);
+            if (g < kSweepGroups && !jsw[j] && !climb_only) ++pp.sample_lib[g];
             pp.kmax = std::max(pp.kmax, H.k);
             if (g == G_GENERIC) pp.ncol = std::max(pp.ncol, H.n);
             if (sweep) {

@@ -1161,7 +1161,6 @@ __global__ void __launch_bounds__(WG) k_sample_sweep(const JobDev* __restrict__ 
 // only the work that reaches it shrinks.
 // ---------------------------------------------------------------------------
 constexpr int CLIMB_STEPS = 64;          // moves per (source, level) at most
-constexpr int CLIMB_ENTRIES = 512;       // sum of the radices whose tables fit the wave's LDS (else no climb)
 constexpr uint32_t CLIMB_PAIRS = 16384;  // two-node moves per pass at most (else single moves only)
 constexpr int CLIMB_NODES = 8;           // problems of at most this many nodes climb (the plan sits in registers)
 
