@@ -2918,10 +2918,13 @@ hipError_t launch_init(JobDev* d_jobs, int njobs, hipStream_t s) {
 }
 
 // Problems above CLIMB_NODES nodes take no climb (the kernel returns for them).
-// modes: bit 0 sources of corr / SLO problems climb, bit 1 of objective ones
-hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, int entries, hipStream_t s) {
-    if (njobs == 0) return hipSuccess;
-    const int E = std::min(std::max(entries, 1), CLIMB_ENTRIES);
+// modes: bit 0 sources of corr / SLO problems climb, bit 1 of objective ones,
+// bit 2 every corr / SLO one is under uniform pressure.
+// The unrolled plan (NN registers per node array, NN (NN - 1) / 2 predecessor
+// tests per evaluated move) is sized by the launch's largest DAG: 6 nodes or
+// fewer take NN = 6, else NN = CLIMB_NODES.
+template <int NN>
+static hipError_t launch_climb_nn(const JobDev* d_jobs, int njobs, int kmax, int modes, int E, hipStream_t s) {
     // few (source, level) pairs: 16 waves each (latency); many: one wave
     // each, four to a block (a CU holds few blocks, so one-wave blocks would
     // leave it short of waves)
@@ -2933,16 +2936,23 @@ hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, in
     // corr mode, many sources, each under uniform pressure: one wave per
     // source climbs its levels in turn
     if ((modes & 1) && (modes & 4) && !coop)
-        hipLaunchKernelGGL((k_climb<CLIMB_NODES, false, true>), dim3((unsigned)((njobs + 3) / 4)), block,
+        hipLaunchKernelGGL((k_climb<NN, false, true>), dim3((unsigned)((njobs + 3) / 4)), block,
                            slots * climb_slot_bytes(E, false), s, d_jobs, njobs, kmax, E);
     else if (modes & 1)
-        hipLaunchKernelGGL((k_climb<CLIMB_NODES, false>), grid, block, slots * climb_slot_bytes(E, false), s, d_jobs,
+        hipLaunchKernelGGL((k_climb<NN, false>), grid, block, slots * climb_slot_bytes(E, false), s, d_jobs,
                            nsearch, kmax, E);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !(modes & 2)) return e;
-    hipLaunchKernelGGL((k_climb<CLIMB_NODES, true>), grid, block, slots * climb_slot_bytes(E, true), s, d_jobs, nsearch,
+    hipLaunchKernelGGL((k_climb<NN, true>), grid, block, slots * climb_slot_bytes(E, true), s, d_jobs, nsearch,
                        kmax, E);
     return hipGetLastError();
+}
+
+hipError_t launch_climb(const JobDev* d_jobs, int njobs, int kmax, int modes, int entries, int nodes, hipStream_t s) {
+    if (njobs == 0) return hipSuccess;
+    const int E = std::min(std::max(entries, 1), CLIMB_ENTRIES);
+    return nodes <= 6 ? launch_climb_nn<6>(d_jobs, njobs, kmax, modes, E, s)
+                      : launch_climb_nn<CLIMB_NODES>(d_jobs, njobs, kmax, modes, E, s);
 }
 
 hipError_t launch_table(JobDev* d_jobs, int njobs, hipStream_t s) {

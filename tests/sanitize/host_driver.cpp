@@ -27,7 +27,7 @@ hipError_t launch_certify(const JobDev*, int, int, int, int, int, hipStream_t) {
 hipError_t launch_exhaust(const JobDev*, int, uint64_t, hipStream_t) { STUB }
 hipError_t launch_reseed(const JobDev*, int, hipStream_t) { STUB }
 hipError_t launch_seed_cands(const JobDev*, int, int, int, hipStream_t) { STUB }
-hipError_t launch_climb(const JobDev*, int, int, int, int, hipStream_t) { STUB }
+hipError_t launch_climb(const JobDev*, int, int, int, int, int, hipStream_t) { STUB }
 hipError_t static_scratch(int, char**, size_t*) { STUB }
 hipError_t launch_score(const JobDev&, uint64_t, float*, float*, float*, uint32_t*, int, int, int, bool, bool, hipStream_t) {
     STUB
