@@ -1164,12 +1164,14 @@ constexpr int CLIMB_STEPS = 64;          // moves per (source, level) at most
 constexpr uint32_t CLIMB_PAIRS = 16384;  // two-node moves per pass at most (else single moves only)
 constexpr int CLIMB_NODES = 8;           // problems of at most this many nodes climb (the plan sits in registers)
 
+// Wave-wide maximum of a 64-bit key, every lane active: the greatest high
+// word, then the greatest low word among the lanes holding it, each through
+// the DPP reduction (lane permutes through the LDS crossbar took several
+// times as long per round).
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t w = __shfl_xor(v, o);
-        v = w > v ? w : v;
-    }
-    return v;
+    const uint32_t hi = wave_max_u32((uint32_t)(v >> 32));
+    const uint32_t lo = wave_max_u32((uint32_t)(v >> 32) == hi ? (uint32_t)v : 0u);
+    return (uint64_t)hi << 32 | lo;
 }
 
 // fp32 corr (node-order product) and CP of the plan whose node n has factor
