@@ -347,7 +347,7 @@ def sweep_work_per_plan(prob, ydiv=False):
     return per_plan + per_row / ry + per_block / (rx * ry)
 
 
-def obj_sweep_work_per_plan(prob):
+def obj_sweep_work_per_plan(prob, yshift=False):
     """Algorithmic fp32 operations per plan of the objective-mode sweep.
 
     Per plan: the add of y's duration (T), the max with the prefix sinks' path
@@ -355,6 +355,12 @@ def obj_sweep_work_per_plan(prob):
     multiply-add G = U - lambda_l T and the prefilter compare; per row: the
     adds of node x (its path, utility and d) and the max of y's predecessors;
     per block: the prefix sums of u and d and one max/add per prefix edge.
+
+    yshift: the sweep compares the row's R = ux - lambda_l M (one fused
+    multiply-add per row) with bin thresholds lowered ahead by each
+    implementation of y's utility and latency term, so a plan costs the add of
+    its D and 1 selection operation (the min of its D bin's threshold into the
+    row's least threshold; the row's last one is the compare with R).
     """
     n = prob.n_nodes
     rx = int(prob.radix[n - 2]) if n >= 2 else 1
@@ -366,8 +372,8 @@ def obj_sweep_work_per_plan(prob):
     y_pred = sum(1 for u, v in edges if v == n - 1 and u != n - 2)
     pre_sinks = any(all(u != m for u, v in edges) for m in range(npre))
     has_s2 = pre_sinks or (n - 2, n - 1) not in edges
-    per_plan = 5.0 + (1.0 if has_s2 else 0.0)
-    per_row = 3.0 + (1.0 if (n - 2, n - 1) in edges and y_pred > 0 else 0.0)
+    per_plan = 2.0 if yshift else 5.0 + (1.0 if has_s2 else 0.0)
+    per_row = (4.0 if yshift else 3.0) + (1.0 if (n - 2, n - 1) in edges and y_pred > 0 else 0.0)
     per_block = 2 * max(npre - 1, 0) + pre_edges + x_pred + y_pred
     return per_plan + per_row / ry + per_block / (rx * ry)
 
@@ -712,7 +718,7 @@ def main():
         if yd not in (0, len(sources)):
             raise RuntimeError(f"{yd} of {len(sources)} sources took the pre-divided thresholds")
         if objs:
-            units = sum(obj_sweep_work_per_plan(probs[p]) * c for _, p, _, c in specs)
+            units = sum(obj_sweep_work_per_plan(probs[p], yd > 0) * c for _, p, _, c in specs)
         else:
             units = sum(sweep_work_per_plan(probs[p], yd > 0) * c for _, p, _, c in specs)
         f = units / plans
@@ -728,7 +734,8 @@ def main():
                 "peak_packed_fp32": PEAK_VALU_PACKED / 1e12, "frac_vs_packed_fp32": achieved / PEAK_VALU_PACKED,
                 "traffic": stored_traffic(tkey, kbase),
                 "per_unit": f"{f:.4f} fp32 ops per plan (prefix-shared sweep{', objective' if objs else ''}"
-                            + (", thresholds divided ahead by y's factor" if yd else "")
+                            + ((", thresholds lowered ahead by y's terms" if objs else
+                                ", thresholds divided ahead by y's factor") if yd else "")
                             + (", mean over the requests' DAGs" if len(specs) > 1 else "") + ")",
                 "kernel_ms": kern_ms, "achieved_units_per_step": units, "peak_scale": 1e12}
         if not objs:

@@ -201,9 +201,9 @@ typedef struct dy_stats {
     float main_ms;           /* duration of the main scoring kernel(s), when timing is on */
     float total_ms;          /* launch of the first kernel to the end of the last */
     int32_t generated_jobs;  /* sources whose main pass ran a kernel generated for their problem */
-    int32_t ydiv_jobs;       /* sources whose sweep compared each plan with its CP bin's threshold divided
-                                ahead by node y's factor (per plan the CP add and a min into the row's
-                                threshold, no corr product) */
+    int32_t ydiv_jobs;       /* sources whose sweep took its bin thresholds divided (corr) or lowered
+                                (objective) ahead by each implementation of node y: per plan one add (CP, or
+                                the demand D) and a min into the row's threshold, one compare per row */
 } dy_stats;
 
 /* Options for dy_plan_set_option. */

@@ -102,6 +102,10 @@ struct ProbDev {
     // r_j is a threshold on the rest of the product: fp32(c a_j) >= T implies
     // c >= fp32(T r_j) for T > 2^-60 (see ydiv_threshold).
     float yinv[64];
+    // objective mode, per implementation j of y (j < 64): c_j >= u_j -
+    // lambda_l tau_j + E (E bounds the roundings of a plan's G and of its
+    // row's fma(-lambda_l, M, ux)), rounded up to fp32; see yshift_key
+    float ysub[64];
 };
 
 struct Cand {

@@ -668,6 +668,27 @@ void stage_objective(const dy_problem& pb, ProbDev& D, float2* at, float2* atx, 
         D.err2[k] = 2.0 * E * (1.0 + 0x1p-40);
         D.lvl_order[k] = k;
     }
+    // Offsets of the sweep's shifted thresholds, per implementation j of y
+    // (the last node): c_j >= u_j - lambda_l tau_j + E_s.  A plan's fp32 G and
+    // its row's fp32 R = fma(-lambda_l, M, ux) take four roundings between
+    // them (tau_j + M, ux + u_j, the fma of G, that of R), each of a value of
+    // magnitude below A_0 = sum of the largest |u| + lambda_l T_max (fp32 sums
+    // inflated by grow), the first scaled by lambda_l: E_s = 4 u A_0 (1 +
+    // 2^-10) plus (4 + 4 lambda_l) 2^-149 for subnormal results.  lambda_l
+    // tau_j is exact in fp64 (24 x 24 bits); the sum's own rounding is covered
+    // by the 2^-50 margin before rounding up.
+    const double A0 = (su + D.lam_l64 * tmax) * grow;
+    const double Es = 4.0 * kU * A0 * (1.0 + 0x1p-10) + (4.0 + 4.0 * D.lam_l64) * 0x1p-149;
+    const int ry = std::min(pb.radix[N - 1], 64);
+    for (int i = 0; i < 64; ++i) {
+        float c = 0.0f;
+        if (i < ry) {
+            const float2 v = at[(size_t)(N - 1) * R + i];
+            const double w = (double)v.x - D.lam_l64 * (double)v.y;
+            c = round_up(w + Es + (std::fabs(w) + Es) * 0x1p-50);
+        }
+        D.ysub[i] = c;
+    }
 }
 
 // dry: derive the descriptors and tables on the host only (no HIP call); the
@@ -1801,9 +1822,9 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
     stats.n_jobs = n_src;
     stats.generated_jobs = pp.n[G_JIT];
     for (int g = 0; g < kSweepGroups; ++g) stats.generated_jobs += pp.njit[g];
-    // the library sweep takes the pre-divided thresholds for groups on 256
-    // bins with R_y = 12 (corr mode)
-    for (int g : {(int)G_SWEEP, (int)G_SWEEP_S2})
+    // the library sweep takes the thresholds divided (corr) or lowered
+    // (objective) ahead by y's terms for groups on 256 bins with R_y = 12
+    for (int g : {(int)G_SWEEP, (int)G_SWEEP_S2, (int)G_OSWEEP, (int)G_OSWEEP_S2})
         stats.ydiv_jobs += pp.ydiv_jit[g] + (pp.b256[g] && pp.ry[g] == 12 ? pp.n[g] - pp.njit[g] : 0);
     if (h->timing) {
         float ms = 0.0f;

@@ -1579,11 +1579,73 @@ __device__ __forceinline__ uint64_t sweep_test_obj(const float2 vy, float dy, fl
     return __ballot(q.G >= thr);
 }
 
-// The objective-mode inner sweep of block b (the prefix pf evaluated).
+// Objective mode, bin thresholds lowered ahead by each implementation j of y.
+// A row fixes ux (utility through x) and M (fp32 path into y without y's own
+// duration); its plan j has G = fma(-lambda_l, T, ux + u_j) with T =
+// max(fp32(tau_j + M), S2) >= fp32(tau_j + M), so, lambda_l being >= 0, G is
+// at most ux - lambda_l M + u_j - lambda_l tau_j plus the rounding of its
+// three operations, and R = fp32 fma(-lambda_l, M, ux) is at least ux -
+// lambda_l M less one rounding.  With c_j = P->ysub[j] >= u_j - lambda_l tau_j
+// + (a bound on those four roundings), a plan whose G reaches a bin threshold
+// t has R >= t - c_j.  Returned: the order key (fkey) of an fp32 value <= t -
+// c_j, so the row's test is fkey(R) >= the least key of its plans' bins.
+__device__ __forceinline__ uint32_t yshift_key(float t, float c) {
+    float x = t;
+    if (t != INFINITY && t != -INFINITY) {
+        x = t - c;  // nearest: within half an ulp of t - c
+        if (x != -INFINITY) {
+            const uint32_t b = __float_as_uint(x);
+            if (x > 0.0f) x = __uint_as_float(b - 1u);       // one ulp down (+inf: the largest finite)
+            else if (x < 0.0f) x = __uint_as_float(b + 1u);  // one ulp down
+        }
+        if (x == 0.0f) x = -0.0f;  // -0 keys below +0; a zero R (either sign) still passes
+    }
+    return fkey(x);
+}
+
+// The rare path of the shifted sweep: the row's plans with the sweep's own
+// per-plan prefilter (G against its D bin's threshold, s_thr) and the exact
+// per-level test.
+template <bool HAS_S2>
+__device__ __forceinline__ void sweep_rare_obj(PD P, JD J, uint64_t b, int ix, float ux, float dx, float M, float S2,
+                                               const float* s_thr) {
+    const CS float2* aty = cs(P->aty);
+    const CS float* dyt = cs(P->demy);
+    const int ry = P->ry;
+    const float nl = -P->lam_l;
+    const uint64_t base = (b * (uint64_t)P->rx + (uint64_t)ix) * (uint64_t)ry;
+    for (int iy = 0; iy < ry; ++iy) {
+        const ObjPlan q = obj_plan<HAS_S2>(aty[iy], dyt[iy], M, S2, ux, dx, nl);
+        const float thr = *(const float*)((const char*)s_thr + ((__float_as_uint(q.D) >> 16) & 0x3fcu));
+        const uint64_t idx = base + (uint64_t)iy;
+        if (q.G >= thr && idx - J->begin < J->count && is_candidate_obj(P, J, q.G, q.D)) append_cand(J, idx, q.G, q.D);
+    }
+}
+
+// A row of the shifted sweep parked in its wave's queue (as RareRow).
+struct ObjRareRow {
+    uint64_t b;
+    uint32_t ix;
+    float ux, dx, M, S2;
+};
+
+template <bool HAS_S2>
+__device__ __forceinline__ void flush_rare_obj(PD P, JD J, const ObjRareRow* q, uint32_t n, const float* s_thr) {
+    const uint32_t lane = threadIdx.x & 63;
+    if (lane < n) {
+        const ObjRareRow e = q[lane];
+        sweep_rare_obj<HAS_S2>(P, J, e.b, (int)e.ix, e.ux, e.dx, e.M, e.S2, s_thr);
+    }
+}
+
+// The objective-mode inner sweep of block b (the prefix pf evaluated).  B256
+// with RY > 0: the shifted thresholds (s_bins: the 256 bin thresholds, then
+// RY x 256 keys of yshift_key), one test per row, rows that pass parked in q.
 template <bool HAS_S2, int RY, bool B256>
 __device__ __forceinline__ void sweep_block_obj(PD P, JD J, uint64_t b, bool live, const Prefix& pf,
                                                 const float2 (&vyr)[RY > 0 ? RY : 1],
-                                                const float (&dyr)[RY > 0 ? RY : 1], const float* s_bins) {
+                                                const float (&dyr)[RY > 0 ? RY : 1], const float* s_bins,
+                                                ObjRareRow* q, uint32_t& qn, uint64_t live_mask) {
     const uint32_t sh = (uint32_t)P->bin_shift - 2u;
     const CS float2* atx = cs(P->atx);
     const CS float2* aty = cs(P->aty);
@@ -1592,6 +1654,40 @@ __device__ __forceinline__ void sweep_block_obj(PD P, JD J, uint64_t b, bool liv
     const int rx = P->rx, ry = P->ry;
     const bool exy = P->edge_xy != 0;
     const float nl = -P->lam_l;
+    if constexpr (B256 && RY > 0) {
+        const uint32_t* s_key = (const uint32_t*)(s_bins + NBINS2);
+        for (int ix = 0; ix < rx; ++ix) {
+            const float2 vx = atx[ix];
+            const float fx = vx.y + pf.px;
+            const float ux = pf.pc + vx.x;
+            const float dx = pf.pd + dxt[ix];
+            const float M = exy ? fmaxf(pf.py, fx) : pf.py;
+            const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
+            const float R = fmaf(nl, M, ux);
+            uint32_t m = 0xffffffffu;
+#pragma unroll
+            for (int j = 0; j < (RY > 0 ? RY : 1); ++j) {
+                const float D = dx + dyr[j];
+                m = min(m, *(const uint32_t*)((const char*)(s_key + j * NBINS2) + ((__float_as_uint(D) >> 16) & 0x3fcu)));
+            }
+            const uint64_t hit = __ballot(fkey(R) >= m) & live_mask;
+            if (hit) {
+                const uint32_t nh = (uint32_t)__popcll(hit);
+                if (qn + nh > (uint32_t)RQ) {
+                    flush_rare_obj<HAS_S2>(P, J, q, qn, s_bins);
+                    qn = 0;
+                }
+                const uint32_t lane = threadIdx.x & 63;
+                if (hit >> lane & 1ull) {
+                    const uint32_t o = qn + __builtin_amdgcn_mbcnt_hi((uint32_t)(hit >> 32),
+                                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)hit, 0u));
+                    q[o] = ObjRareRow{b, (uint32_t)ix, ux, dx, M, S2};
+                }
+                qn += nh;
+            }
+        }
+        return;
+    }
     for (int ix = 0; ix < rx; ++ix) {
         const float2 vx = atx[ix];
         const float fx = vx.y + pf.px;
@@ -1644,10 +1740,17 @@ __global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ job
     const uint64_t t = t0 + threadIdx.x;
     const bool live = t < units;
     const uint64_t b0 = J->blk_first + (live ? t : units - 1) * (uint64_t)G;
-    __shared__ float s_bins[B256 ? NBINS2 : NBINS];
+    constexpr bool YSH = B256 && RY > 0;
+    __shared__ float s_bins[YSH ? (1 + (RY > 0 ? RY : 1)) * NBINS2 : (B256 ? NBINS2 : NBINS)];
     if (B256) {
-        s_bins[threadIdx.x] = __uint_as_float(J->table2[threadIdx.x]);
         static_assert(!B256 || NBINS2 == WG, "one bin per thread");
+        const float thr = __uint_as_float(J->table2[threadIdx.x]);
+        s_bins[threadIdx.x] = thr;
+        if constexpr (YSH) {
+            uint32_t* s_key = (uint32_t*)(s_bins + NBINS2);
+#pragma unroll
+            for (int j = 0; j < (RY > 0 ? RY : 1); ++j) s_key[j * NBINS2 + threadIdx.x] = yshift_key(thr, P->ysub[j]);
+        }
     } else if (threadIdx.x < NBINS) {
         s_bins[threadIdx.x] = __uint_as_float(J->table[threadIdx.x]);
     }
@@ -1655,6 +1758,9 @@ __global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ job
     float2* s_pat = (float2*)(s_f + (NPRE > 0 ? (size_t)0 : (size_t)max(P->npre, 1) * WG));
     float* s_pd = (float*)(s_pat + pat_cap);
     const float2* pat = stage_prefix_rows<true>(P, s_pat, s_pd, pat_cap);
+    // a wave whose lanes all lie past the last unit has nothing to score (no
+    // barrier follows)
+    if (t0 + (threadIdx.x & ~63u) >= units) return;
     float2 vyr[RY > 0 ? RY : 1];
     float dyr[RY > 0 ? RY : 1];
     if (RY > 0) {
@@ -1664,17 +1770,30 @@ __global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ job
         for (int iy = 0; iy < RY; ++iy) {
             vyr[iy] = aty[iy];
             dyr[iy] = dyt[iy];
+            if constexpr (YSH) {
+                // the shifted sweep reads only y's d terms; keep them in
+                // scalar registers
+                uint32_t v = __float_as_uint(dyr[iy]);
+                asm volatile("" : "+s"(v));
+                dyr[iy] = __uint_as_float(v);
+            }
         }
     }
+    __shared__ ObjRareRow s_q[YSH ? WG / 64 : 1][RQ];
+    ObjRareRow* q = s_q[YSH ? threadIdx.x >> 6 : 0];
+    uint32_t qn = 0;
+    const uint64_t live_mask = __ballot(live);
     if constexpr (NPRE > 0) {
         const PrefixHead ph = prefix_head<NPRE, true, RAD>(P, b0, J->big, pat, s_pd);
         for (int g = 0; g < G; ++g)
             sweep_block_obj<HAS_S2, RY, B256>(P, J, b0 + (uint64_t)g, live,
-                                              prefix_tail<NPRE, true>(P, ph, g, pat, s_pd), vyr, dyr, s_bins);
+                                              prefix_tail<NPRE, true>(P, ph, g, pat, s_pd), vyr, dyr, s_bins, q, qn,
+                                              live_mask);
     } else {
         const Prefix pf = prefix_eval<NPRE, true>(P, b0, J->big, s_f, pat, s_pd);
-        sweep_block_obj<HAS_S2, RY, B256>(P, J, b0, live, pf, vyr, dyr, s_bins);
+        sweep_block_obj<HAS_S2, RY, B256>(P, J, b0, live, pf, vyr, dyr, s_bins, q, qn, live_mask);
     }
+    if (YSH && qn) flush_rare_obj<HAS_S2>(P, J, q, qn, s_bins);
 }
 
 // Seeding pre-pass of the objective sweep: one hashed row per window of S

@@ -177,6 +177,34 @@ def test_forkjoin8_generated_sweep(begin, count):
     assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"forkjoin8[{begin}+{count}] generated")
 
 
+@pytest.mark.parametrize("case", ["batch6", "lambda_l0", "negative", "two_sinks", "x_sink", "ragged"])
+def test_shifted_thresholds_library_sweep(case):
+    # DY_OPT_JIT 0: the library sweep of a 6-node problem with 12
+    # implementations of node y tests each row's fma(-lambda_l, M, ux) against
+    # bin thresholds lowered ahead by every implementation of y (ydiv_jobs
+    # counts the source).  batch6 DAGs have one sink; two_sinks adds a second
+    # one (the path into it bounds T from below), x_sink leaves x without a
+    # successor; negative makes most utilities negative (negative
+    # thresholds); lambda_l0 drops the latency term; ragged cuts blocks.
+    begin, count = 0, 12 ** 6
+    if case in ("two_sinks", "x_sink"):
+        edges = [(0, 1), (1, 2), (2, 3), (0, 4), (4, 5)] if case == "two_sinks" else \
+                [(0, 1), (1, 2), (2, 3), (3, 5), (0, 4)]
+        prob = small_dag(6, [12] * 6, 31 if case == "two_sinks" else 32, edges)
+        obj = wl.paper_objective(prob, lambda_l=0.3)
+    else:
+        prob = wl.batch6_request(11)
+        w = {"lambda_l0": dict(lambda_l=0.0), "negative": dict(lambda_c=2.0, lambda_l=0.3)}.get(case, {})
+        obj = wl.paper_objective(prob, **w)
+        if case == "ragged":
+            begin, count = 777, 3 * 12 ** 5 + 55
+    with D.Plan((prob, obj)) as plan:
+        plan.set_option(D.DY_OPT_JIT, 0)
+        got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+        assert plan.stats().ydiv_jobs == 1
+    assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"{case}[{begin}+{count}]")
+
+
 def test_batch_mixed_with_corr_selection():
     # objective and corr / SLO problems in one call: both sweep groups run together
     probs = [wl.batch6_request(r) for r in range(4)]
