@@ -369,7 +369,7 @@ struct PassPlan {
     int ry[kSweepGroups] = {};            // R_y shared by every source of a sweep group, else -1
     int npre_c[kSweepGroups] = {};        // prefix length shared by every source of a sweep group, else -1
     int pat[kSweepGroups] = {};           // largest prefix-row table (npre x rmax entries) of a sweep group
-    int ydiv_jit[kSweepGroups] = {};      // generated sweeps (corr mode) on thresholds pre-divided by y's factor
+    int ydiv_jit[kSweepGroups] = {};      // generated sweeps on thresholds divided (corr) or lowered (objective) by y's terms
     int sample_lib[kSweepGroups] = {};    // library-sweep sources the sampling pass seeds (see launch_seed)
     int njit[kSweepGroups] = {};          // trailing sources of the group that run their generated sweep
     bool b256[kSweepGroups] = {true, true, true, true};  // every library-sweep source has the 256-bin table
@@ -1587,8 +1587,7 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
             J.units = sweep ? J.nblk : J.count;
             ++pp.n[g];
             if (g < kSweepGroups && jsw[j]) ++pp.njit[g];
-            if ((g == G_SWEEP || g == G_SWEEP_S2) && jsw[j] && h->hdesc[src[j].problem].jsh != 0 && H.ry >= 1 &&
-                H.ry <= 64)
+            if (g < kSweepGroups && jsw[j] && h->hdesc[src[j].problem].jsh != 0 && H.ry >= 1 && H.ry <= 64)
                 ++pp.ydiv_jit[g];
             if (g < G_JIT) {
                 pp.units[g] = std::max(pp.units[g], J.units);

@@ -304,6 +304,12 @@ void gen_sweep(std::ostringstream& o, const ProbDev& D) {
     // then cx >= the least threshold of its plans' bins, every threshold being
     // +0, positive or +inf, so that their fp32 patterns order as the values
     const bool ydiv = !obj && D.jsh != 0 && D.ry >= 1 && D.ry <= 64;
+    // objective mode on 256 bins: the first 256 entries hold the bins'
+    // thresholds on G, then per implementation j of y the order keys of those
+    // thresholds lowered by c_j (see the library's yshift_key); a row's test
+    // is the key of its fma(-lambda_l, M, ux) >= the least key of its plans'
+    // D bins, and the rare path keeps the per-plan test on G
+    const bool ysh = obj && D.jsh != 0 && D.ry >= 1 && D.ry <= 64;
     auto maxof = [&](uint32_t mask, const char* pre) {
         std::string m;
         for (int u = 0; u < NP; ++u)
@@ -317,6 +323,22 @@ __device__ __forceinline__ float dy_ydiv(float T, float r) {
   return T > 0x1p-60f ? T * r : 0.0f;
 }
 )";
+    if (ysh)  // dy_fkey: the objective preamble's order key
+        o << R"(
+__device__ __forceinline__ unsigned dy_yshift(float t, float c) {
+  float x = t;
+  if (t != __builtin_inff() && t != -__builtin_inff()) {
+    x = t - c;
+    if (x != -__builtin_inff()) {
+      const unsigned b = __float_as_uint(x);
+      if (x > 0.0f) x = __uint_as_float(b - 1u);
+      else if (x < 0.0f) x = __uint_as_float(b + 1u);
+    }
+    if (x == 0.0f) x = -0.0f;
+  }
+  return dy_fkey(x);
+}
+)";
     o << R"(
 extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     unsigned long long unit_off, unsigned long long blk_first, unsigned long long nblk, unsigned long long begin,
@@ -325,7 +347,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     const float* __restrict__ demy, const float* __restrict__ lat, int rmax, const unsigned* __restrict__ table,
     const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap, unsigned* __restrict__ ncand,
     int* __restrict__ flags) {
-  __shared__ float s_bins[)" << (ydiv ? D.ry * NBINS2 : nb) << R"(];
+  __shared__ float s_bins[)" << (ydiv ? D.ry * NBINS2 : ysh ? (1 + D.ry) * NBINS2 : nb) << R"(];
   __shared__ float2 s_pat[)" << NP << R"( * 64];
 )";
     if (obj) o << "  __shared__ float s_pd[" << NP << " * 64];\n";
@@ -337,6 +359,12 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
         o << "  {\n    const float T = __uint_as_float(table[threadIdx.x]);\n";
         for (int j = 0; j < D.ry; ++j)
             o << "    s_bins[" << j * NBINS2 << " + threadIdx.x] = dy_ydiv(T, " << flit(D.yinv[j]) << ");\n";
+        o << "  }\n";
+    } else if (ysh) {
+        o << "  {\n    const float T = __uint_as_float(table[threadIdx.x]);\n    s_bins[threadIdx.x] = T;\n";
+        for (int j = 0; j < D.ry; ++j)
+            o << "    ((unsigned*)s_bins)[" << (j + 1) * NBINS2 << " + threadIdx.x] = dy_yshift(T, " << flit(D.ysub[j])
+              << ");\n";
         o << "  }\n";
     } else {
         o << "  for (int i = threadIdx.x; i < " << nb << "; i += 256) s_bins[i] = __uint_as_float(table[i]);\n";
@@ -420,6 +448,14 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
         thr_j("      ", "j");
         o << "      m = min(m, th);\n    }\n";
         o << "    const bool mine_ = cx >= __uint_as_float(m);\n";
+    } else if (ysh) {
+        o << "    const float R = fmaf(" << flit(-D.lam_l) << ", M, ux);\n";
+        o << "    unsigned m = 0xffffffffu;\n";
+        o << "#pragma unroll\n    for (int j = 0; j < " << D.ry << "; ++j) {\n";
+        o << "      const float bv = dx + dy[j];\n";
+        o << "      m = min(m, *(const unsigned*)((const char*)s_bins + " << NBINS2 * 4
+          << " * (j + 1) + ((__float_as_uint(bv) >> 16) & 0x3fcu)));\n    }\n";
+        o << "    const bool mine_ = dy_fkey(R) >= m;\n";
     } else {
         o << "    unsigned long long hit = 0ull;\n";
         o << "#pragma unroll\n    for (int j = 0; j < " << D.ry << "; ++j) {\n";
@@ -490,6 +526,8 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     plan("        ", "aty", "demy");
     o << "        const unsigned long long idx = base + (unsigned long long)j;\n";
     o << "        bool want = false;\n";
+    if (ysh)
+        o << "        if (!(cc >= *(const float*)((const char*)s_bins + ((__float_as_uint(bv) >> 16) & 0x3fcu)))) continue;\n";
     for (int k = 0; k < D.k; ++k) {
         if (obj)
             o << "        want = want || (fma(-" << dlit(D.m64[k]) << ", (double)bv, (double)cc) >= (double)thr[" << k << "]);\n";
