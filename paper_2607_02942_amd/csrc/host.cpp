@@ -1593,15 +1593,16 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
                 pp.units[g] = std::max(pp.units[g], J.units);
                 pp.samples[g] = std::max(pp.samples[g], (sunits + stride - 1) / stride);
             }
-            // a corr / SLO source of more than 2^21 plans under uniform
-            // pressure whose levels are seeded by the local search needs no
-            // sample: the search starts from the plan of least CP, so a level
-            // it cannot seed has no certainly feasible plan at all, and on so
-            // large a space a sample of about 256 rows rarely beats the
-            // search's seed (on smaller spaces, and under per-backend pressure,
-            // where each level's search starts afresh, it does now and then)
-            const bool climb_only =
-                J.climb && !H.obj && H.uniform && climb_entries <= CLIMB_ENTRIES && J.count > (1ull << 21);
+            // a source of more than 2^21 plans whose levels are seeded by the
+            // local search needs no sample in corr / SLO mode under uniform
+            // pressure (the search starts from the plan of least CP, so a
+            // level it cannot seed has no certainly feasible plan at all) and
+            // in objective mode (every plan is admissible, so every level's
+            // search seeds it); on so large a space a sample of about 256 rows
+            // rarely beats the search's seed (on smaller spaces, and under
+            // per-backend pressure, it does now and then)
+            const bool climb_only = J.climb && (H.obj || H.uniform) && climb_entries <= CLIMB_ENTRIES &&
+                                    J.count > (1ull << 21);
             if (g < kSweepGroups && !jsw[j] && !climb_only) ++pp.sample_lib[g];
             pp.kmax = std::max(pp.kmax, H.k);
             if (g == G_GENERIC) pp.ncol = std::max(pp.ncol, H.n);
