@@ -461,6 +461,25 @@ def test_climb_small_dags_full_space(seed):
     assert c_on <= c_off, (c_on, c_off)
 
 
+def test_batch6_objective_graph_replays():
+    # 1,024 requests under J_L, repeated (graph replays): every call against
+    # the stored oracle selections, the same candidate count each time
+    path = os.path.join(os.path.dirname(__file__), "golden", "select_batch6_objective.json")
+    want = [[(c[0], c[1], float(c[2]), float(c[3]), float(c[4])) for c in ch] for ch in json.load(open(path))["choices"]]
+    nreq = 1024
+    probs = wl.batch6(nreq)
+    items = [(p, wl.paper_objective(p)) for p in probs]
+    srcs = [D.range_source(r, 0, 12 ** 6) for r in range(nreq)]
+    cands = []
+    with D.Plan(items) as plan:
+        for call in range(3):
+            got = plan.select(srcs, stream=stream())
+            cands.append(plan.stats().candidates)
+            for r in range(nreq):
+                assert_obj_choices(got[r], want[r], f"batch6 objective [{r}] call {call}")
+    assert len(set(cands)) == 1, cands
+
+
 def test_climb_batch6_objective_golden():
     # 256 of batch6's requests under J_L, with and without the local search,
     # against the stored oracle selections; a call mixing both objectives

@@ -172,6 +172,23 @@ def test_batch6_full_golden():
         assert_choices(got[r], want[r], f"batch6[{r}]")
 
 
+def test_batch6_graph_replays():
+    # Repeated calls of the 4,096 sources replay the captured graph of the
+    # call (local search, table, sweep, certification, copy-out): every call
+    # gives the stored selections and the same candidate count.
+    g, want = golden("batch6")
+    probs = wl.batch6()
+    srcs = [D.range_source(r, 0, 12 ** 6) for r in range(wl.N_BATCH)]
+    cands = []
+    with D.Plan(probs) as plan:
+        for call in range(4):
+            got = plan.select(srcs, stream=stream())
+            cands.append(plan.stats().candidates)
+            for r in range(wl.N_BATCH):
+                assert_choices(got[r], want[r], f"batch6[{r}] call {call}")
+    assert len(set(cands)) == 1, cands
+
+
 def test_stream24_full_golden():
     g, want = golden("stream24")
     prob = wl.stream24()
