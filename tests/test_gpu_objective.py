@@ -177,7 +177,7 @@ def test_forkjoin8_generated_sweep(begin, count):
     assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"forkjoin8[{begin}+{count}] generated")
 
 
-@pytest.mark.parametrize("case", ["batch6", "lambda_l0", "negative", "two_sinks", "x_sink", "ragged"])
+@pytest.mark.parametrize("case", ["batch6", "lambda_l0", "negative", "two_sinks", "x_sink", "ragged", "subnormal"])
 def test_shifted_thresholds_library_sweep(case):
     # DY_OPT_JIT 0: the library sweep of a 6-node problem with 12
     # implementations of node y tests each row's fma(-lambda_l, M, ux) against
@@ -185,7 +185,9 @@ def test_shifted_thresholds_library_sweep(case):
     # counts the source).  batch6 DAGs have one sink; two_sinks adds a second
     # one (the path into it bounds T from below), x_sink leaves x without a
     # successor; negative makes most utilities negative (negative
-    # thresholds); lambda_l0 drops the latency term; ragged cuts blocks.
+    # thresholds); lambda_l0 drops the latency term; ragged cuts blocks;
+    # subnormal makes every quality, hence every utility and G, subnormal
+    # in fp32 (the bound's subnormal term), with a subnormal lambda_l.
     begin, count = 0, 12 ** 6
     if case in ("two_sinks", "x_sink"):
         edges = [(0, 1), (1, 2), (2, 3), (0, 4), (4, 5)] if case == "two_sinks" else \
@@ -194,7 +196,10 @@ def test_shifted_thresholds_library_sweep(case):
         obj = wl.paper_objective(prob, lambda_l=0.3)
     else:
         prob = wl.batch6_request(11)
-        w = {"lambda_l0": dict(lambda_l=0.0), "negative": dict(lambda_c=2.0, lambda_l=0.3)}.get(case, {})
+        w = {"lambda_l0": dict(lambda_l=0.0), "negative": dict(lambda_c=2.0, lambda_l=0.3),
+             "subnormal": dict(lambda_f=0.0, lambda_c=0.0, lambda_l=1e-44)}.get(case, {})
+        if case == "subnormal":
+            prob = dataclasses.replace(prob, p=(prob.p.astype(np.float64) * 1e-39).astype(np.float32))
         obj = wl.paper_objective(prob, **w)
         if case == "ragged":
             begin, count = 777, 3 * 12 ** 5 + 55
