@@ -1447,7 +1447,10 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
         h->err = "src/out is NULL or n_src < 1";
         return DY_EINVAL;
     }
-    for (int j = 0; j < n_src; ++j) {
+    // sources identical to the previous call's passed these checks then
+    const bool same_src = !stat && h->call.valid && h->call.src.size() == (size_t)n_src &&
+                          std::memcmp(h->call.src.data(), src, (size_t)n_src * sizeof(dy_source)) == 0;
+    for (int j = 0; j < n_src && !same_src; ++j) {
         int st = check_source(h, src[j], j, &h->err);
         if (st != DY_OK) return st;
     }
@@ -1479,10 +1482,8 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
     CallPlan& C = stat ? fresh : h->call;
     const int64_t opts[6] = {h->use_jit, h->use_climb, (int64_t)h->sample_stride, h->stride_fixed ? 1 : 0,
                              h->force_fp64, cert_waves};
-    const bool reuse = !stat && C.valid && C.src.size() == (size_t)n_src && C.cap == cap &&
-                       C.scratch == (const void*)S.scert && std::memcmp(C.opts, opts, sizeof opts) == 0 &&
-                       C.jit_state == h->jit_state &&
-                       std::memcmp(C.src.data(), src, (size_t)n_src * sizeof(dy_source)) == 0;
+    const bool reuse = same_src && C.cap == cap && C.scratch == (const void*)S.scert &&
+                       std::memcmp(C.opts, opts, sizeof opts) == 0 && C.jit_state == h->jit_state;
     std::vector<int>& grp = C.grp;
     std::vector<int>& order = C.order;
     std::vector<JobDev>& jobs = C.jobs;
@@ -1833,18 +1834,20 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
     }
     if (h->force_fp64)
         for (int j = 0; j < n_src; ++j) stats.fallbacks += h->hp[src[j].problem].k;
+    int32_t any_flag = 0;  // the union of the sources' flags
     for (int q = 0; q < n_src; ++q) {
         stats.candidates += std::min<uint64_t>(S.h_ncand[q], cap);
-        if (S.h_flags[q] & JF_BAD_ROW) {
-            h->err = "a row holds an implementation id >= radix of its node";
-            return DY_EINVAL;
-        }
+        any_flag |= S.h_flags[q];
+    }
+    if (any_flag & JF_BAD_ROW) {
+        h->err = "a row holds an implementation id >= radix of its node";
+        return DY_EINVAL;
     }
     // candidate-list overflow: reseed from the gathered candidates and score
     // those sources again (each round raises the thresholds); whatever still
     // overflows after kReseedRounds is decided exhaustively
     constexpr int kReseedRounds = 3;
-    for (int round = 0; round <= kReseedRounds && !h->force_fp64; ++round) {
+    for (int round = 0; round <= kReseedRounds && !h->force_fp64 && (any_flag & JF_OVERFLOW); ++round) {
         PassPlan rp;
         std::vector<JobDev> re, ex;
         uint64_t fb_units = 0;
@@ -1912,8 +1915,11 @@ static int select_impl(dy_plan* h, const dy_source* src, int32_t n_src, dy_choic
             std::memcpy(out + (size_t)j * km, S.h_out + (size_t)j * km, (size_t)K * sizeof(dy_choice));
         }
     }
-    bool flagged = false;
-    for (int q = 0; q < n_src; ++q) flagged = flagged || S.h_flags[q] != 0;
+    bool flagged = any_flag != 0;  // rescan only when a flag was raised (reseeding may clear it)
+    if (flagged) {
+        flagged = false;
+        for (int q = 0; q < n_src; ++q) flagged = flagged || S.h_flags[q] != 0;
+    }
     S.clean = !exhausted && !flagged;
     h->stats = stats;
     return DY_OK;
