@@ -213,7 +213,7 @@ def trace_summary(db, title, command, kernel, bench_log=None, plain_log=None, pl
     rows = list(con.execute("select name, count(*), sum(duration), avg(duration), min(duration), max(duration) "
                             "from kernels group by name order by sum(duration) desc"))
     tot = sum(r[2] for r in rows)
-    out = [f"# {title}", "", "Command (on the GPU box; `<repo>` is the repository root):", "", "```", command, "```", "",
+    out = [f"# {title}", "", "Command (on the MI355X machine; `<repo>` is the repository root):", "", "```", command, "```", "",
            "rocprofv3 kernel trace, per-kernel statistics (durations in microseconds):", "",
            "| kernel | calls | total us | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
     for n, c, s, a, mn, mx in rows:
@@ -248,7 +248,7 @@ def trace_summary(db, title, command, kernel, bench_log=None, plain_log=None, pl
         if p:
             pr = p["roofline"]
             out += ["", f"The same command without the profiler (`{plain_command or ''}`), run just before on the "
-                        f"same box: {p['value']:.4g} plans/s, step {p['ms_per_step']:.4f} ms, `{kernel}` "
+                        f"same machine: {p['value']:.4g} plans/s, step {p['ms_per_step']:.4f} ms, `{kernel}` "
                         f"{pr['kernel_ms'] * 1e3:.1f} us per step (events) -> roofline frac {pr['frac']:.3f}. "
                         "Bench line:", "", "```", json.dumps(p), "```"]
     print("\n".join(out))
@@ -269,7 +269,7 @@ def pmc_summary(dbs, kernel, title, commands, trace_db=None):
             knames, v, nsteps = _one_kernel(per, kernel, db)
             vals[cn] = (v, nsteps, knames)
     kn = ", ".join(f"`{k}`" for k in next(iter(vals.values()))[2])
-    out = [f"# {title}", "", "Commands (on the GPU box; `<repo>` is the repository root), one counter pass each:", "",
+    out = [f"# {title}", "", "Commands (on the MI355X machine; `<repo>` is the repository root), one counter pass each:", "",
            "```"] + commands + ["```", "",
                                 f"Per-step values of `{kernel}` (summed over a step's dispatches of {kn}, "
                                 "mean over the steps):", "",
