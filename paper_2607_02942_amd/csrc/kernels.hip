@@ -1313,9 +1313,12 @@ __global__ void __launch_bounds__(1024) k_climb(const JobDev* __restrict__ jobs,
     // CHAIN: the wave climbs every level of its source in turn.  Under
     // uniform pressure the levels share the tables, their Pareto sets and the
     // start, and are taken from the tightest band to the loosest, each from
-    // the plan the previous one reached (feasible at any looser band too);
-    // otherwise each level is set up and started afresh.
-    const bool chain = CHAIN && P->uniform != 0;
+    // the plan the previous one reached (feasible at any looser band too); in
+    // objective mode the tables and Pareto sets do not depend on the level
+    // either and every plan is admissible, so each level starts from the
+    // plan the previous one reached; otherwise each level is set up and
+    // started afresh.
+    const bool chain = CHAIN && (OBJ || P->uniform != 0);
     const int nlev = CHAIN ? P->k : 1;
     const int ksel = k;
     int foff[NN + 1];
@@ -3064,8 +3067,14 @@ static hipError_t launch_climb_nn(const JobDev* d_jobs, int njobs, int kmax, int
                            nsearch, kmax, E);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !(modes & 2)) return e;
-    hipLaunchKernelGGL((k_climb<NN, true>), grid, block, slots * climb_slot_bytes(E, true), s, d_jobs, nsearch,
-                       kmax, E);
+    // objective mode, many sources: one wave per source climbs its levels in
+    // turn (every plan is admissible at every level)
+    if (!coop)
+        hipLaunchKernelGGL((k_climb<NN, true, true>), dim3((unsigned)((njobs + 3) / 4)), block,
+                           slots * climb_slot_bytes(E, true), s, d_jobs, njobs, kmax, E);
+    else
+        hipLaunchKernelGGL((k_climb<NN, true>), grid, block, slots * climb_slot_bytes(E, true), s, d_jobs, nsearch,
+                           kmax, E);
     return hipGetLastError();
 }
 
