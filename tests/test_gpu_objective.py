@@ -177,12 +177,14 @@ def test_forkjoin8_generated_sweep(begin, count):
     assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"forkjoin8[{begin}+{count}] generated")
 
 
+@pytest.mark.parametrize("jit", [0, 2])
 @pytest.mark.parametrize("case", ["batch6", "lambda_l0", "negative", "two_sinks", "x_sink", "ragged", "subnormal"])
-def test_shifted_thresholds_library_sweep(case):
+def test_shifted_thresholds_both_sweeps(case, jit):
     # DY_OPT_JIT 0: the library sweep of a 6-node problem with 12
     # implementations of node y tests each row's fma(-lambda_l, M, ux) against
     # bin thresholds lowered ahead by every implementation of y (ydiv_jobs
-    # counts the source).  batch6 DAGs have one sink; two_sinks adds a second
+    # counts the source); DY_OPT_JIT 2: the sweep generated for the DAG, with
+    # the same test and the offsets as literals.  batch6 DAGs have one sink; two_sinks adds a second
     # one (the path into it bounds T from below), x_sink leaves x without a
     # successor; negative makes most utilities negative (negative
     # thresholds); lambda_l0 drops the latency term; ragged cuts blocks;
@@ -204,10 +206,11 @@ def test_shifted_thresholds_library_sweep(case):
         if case == "ragged":
             begin, count = 777, 3 * 12 ** 5 + 55
     with D.Plan((prob, obj)) as plan:
-        plan.set_option(D.DY_OPT_JIT, 0)
+        plan.set_option(D.DY_OPT_JIT, jit)
         got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
         assert plan.stats().ydiv_jobs == 1
-    assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"{case}[{begin}+{count}]")
+        assert plan.stats().generated_jobs == (1 if jit else 0)
+    assert_obj_choices(got, orc.obj_select_range(prob, obj, begin, count), f"{case}[{begin}+{count}] jit {jit}")
 
 
 def test_batch_mixed_with_corr_selection():
