@@ -1362,12 +1362,23 @@ hipError_t launch_jit_sweep(const dy_plan* h, const JobDev& J, int p, hipStream_
     unsigned cap = J.cap;
     unsigned* ncand = J.ncand;
     int* flags = J.flags;
+    // runs of G blocks per thread that share every prefix digit but the
+    // last: G divides the last prefix node's radix, the first block and the
+    // block count (every block of a run then lies in the source)
+    unsigned G = 1;
+    const int last = D.radix[D.npre - 1];
+    for (unsigned c : {3u, 2u})
+        if (D.obj && last % (int)c == 0 && blk_first % c == 0 && nblk % c == 0) {
+            G = c;
+            break;
+        }
+    const unsigned long long units = nblk / G;
     constexpr unsigned long long kMaxBlocks = 1ull << 22;
-    for (unsigned long long off = 0; off < nblk; off += kMaxBlocks * 256ull) {
+    for (unsigned long long off = 0; off < units; off += kMaxBlocks * 256ull) {
         unsigned long long unit_off = off;
-        const unsigned gx = (unsigned)std::min<unsigned long long>((nblk - off + 255) / 256, kMaxBlocks);
+        const unsigned gx = (unsigned)std::min<unsigned long long>((units - off + 255) / 256, kMaxBlocks);
         void* args[] = {&unit_off, &blk_first, &nblk, &begin, &count, &at, &atx, &aty, &dem, &demx, &demy, &lat,
-                        &rmax, &table, &thr, &cand, &cap, &ncand, &flags};
+                        &rmax, &table, &thr, &cand, &cap, &ncand, &flags, &G};
         const hipError_t e = hipModuleLaunchKernel(h->jit[p].sweep, gx, 1, 1, 256, 1, 1, 0, s, args, nullptr);
         if (e != hipSuccess) return e;
     }

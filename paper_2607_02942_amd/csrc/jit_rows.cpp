@@ -346,13 +346,14 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     const float2* __restrict__ aty, const float* __restrict__ dem, const float* __restrict__ demx,
     const float* __restrict__ demy, const float* __restrict__ lat, int rmax, const unsigned* __restrict__ table,
     const float* __restrict__ thr, DyCand* __restrict__ cand, unsigned cap, unsigned* __restrict__ ncand,
-    int* __restrict__ flags) {
+    int* __restrict__ flags, unsigned G) {
   __shared__ float s_bins[)" << (ydiv ? D.ry * NBINS2 : ysh ? (1 + D.ry) * NBINS2 : nb) << R"(];
   __shared__ float2 s_pat[)" << NP << R"( * 64];
 )";
     if (obj) o << "  __shared__ float s_pd[" << NP << " * 64];\n";
     o << R"(  const unsigned long long t0 = unit_off + (unsigned long long)blockIdx.x * 256ull;
-  if (t0 >= nblk) return;
+  const unsigned long long units = nblk / G;  // runs of G blocks that share the prefix but its last node
+  if (t0 >= units) return;
 )";
     if (ydiv) {
         static_assert(NBINS2 == 256, "one bin per thread");
@@ -376,11 +377,11 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     if (obj) o << "    s_pd[i] = e < rmax ? dem[n * rmax + e] : 0.0f;\n";
     o << R"(  }
   __syncthreads();
-  if (t0 + (threadIdx.x & ~63u) >= nblk) return;  // a wave past the last block (no barrier follows)
+  if (t0 + (threadIdx.x & ~63u) >= units) return;  // a wave past the last run (no barrier follows)
   const unsigned long long t = t0 + threadIdx.x;
-  const bool live = t < nblk;
-  const unsigned long long b = blk_first + (live ? t : nblk - 1);
-  unsigned x_ = (unsigned)b;
+  const bool live = t < units;
+  const unsigned long long b0 = blk_first + (live ? t : units - 1) * G;
+  unsigned x_ = (unsigned)b0;
 )";
     for (int n = NP - 1; n >= 0; --n) {
         o << "  const unsigned d" << n << " = x_ % " << D.radix[n] << "u;";
@@ -389,24 +390,46 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     }
     // prefix: corr mode the product of the factors, objective mode the sums
     // of u and of d (node order, as the library's prefix evaluation)
+    // objective mode: runs of G blocks per thread, nodes 0..NP-2 once per
+    // run and the last prefix node (digit + g) per block (the prefix sums
+    // cost more than corr mode's products, and only they gained); corr
+    // mode: one block per thread (G = 1), the whole prefix straight
+    const bool runs = obj;
     o << "  float pc = " << (obj ? "0.0f" : "1.0f") << ";\n";
     if (obj) o << "  float pd = 0.0f;\n";
     for (int n = 0; n < NP; ++n) {
-        o << "  const float2 v" << n << " = s_pat[" << n * 64 << " + d" << n << "];\n";
-        o << "  pc = pc " << (obj ? "+" : "*") << " v" << n << ".x;\n";
-        if (obj) o << "  pd = pd + s_pd[" << n * 64 << " + d" << n << "];\n";
         std::string m;
         for (int u = 0; u < n; ++u)
             if (D.pred[n] >> u & 1u) m = m.empty() ? "f" + std::to_string(u) : "fmaxf(" + m + ", f" + std::to_string(u) + ")";
+        if (runs && n == NP - 1) {
+            o << "  const float ml = " << (m.empty() ? "0.0f" : m) << ";\n";
+            o << "  const float pch = pc;\n";
+            if (obj) o << "  const float pdh = pd;\n";
+            break;
+        }
+        o << "  const float2 v" << n << " = s_pat[" << n * 64 << " + d" << n << "];\n";
+        o << "  pc = pc " << (obj ? "+" : "*") << " v" << n << ".x;\n";
+        if (obj) o << "  pd = pd + s_pd[" << n * 64 << " + d" << n << "];\n";
         o << "  const float f" << n << " = v" << n << ".y + " << (m.empty() ? "0.0f" : m) << ";\n";
     }
-    o << "  const float px = " << maxof(pmx, "f") << ", py = " << maxof(pmy, "f") << ", ps = " << maxof(pms, "f")
-      << ";\n";
     o << "  float2 vy[" << D.ry << "];\n";
     if (obj) o << "  float dy[" << D.ry << "];\n";
     o << "#pragma unroll\n  for (int j = 0; j < " << D.ry << "; ++j) {\n    vy[j] = aty[j];\n";
     if (obj) o << "    dy[j] = demy[j];\n";
     o << "  }\n";
+    if (!runs) {
+        o << "  const unsigned long long b = b0;\n";
+    } else {
+        o << "#pragma unroll 1\n  for (unsigned g = 0; g < G; ++g) {\n";
+        o << "  const unsigned long long b = b0 + g;\n";
+        const int n = NP - 1;
+        o << "  const float2 v" << n << " = s_pat[" << n * 64 << " + d" << n << " + g];\n";
+        o << "  const float pc = pch " << (obj ? "+" : "*") << " v" << n << ".x;\n";
+        if (obj) o << "  const float pd = pdh + s_pd[" << n * 64 << " + d" << n << " + g];\n";
+        o << "  const float f" << n << " = v" << n << ".y + ml;\n";
+    }
+    o << "  const float px = " << maxof(pmx, "f") << ", py = " << maxof(pmy, "f") << ", ps = " << maxof(pms, "f")
+      << ";\n";
     o << "#pragma unroll 1\n";  // one copy of the row and its rare path (code size)
     o << "  for (int ix = 0; ix < " << D.rx << "; ++ix) {\n";
     o << "    const float2 vx = atx[ix];\n";
@@ -538,7 +561,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     o << "          const unsigned slot = atomicAdd(ncand, 1u);\n";
     o << "          if (slot < cap) {\n            cand[slot].index = idx;\n            cand[slot].corr = cc;\n"
          "            cand[slot].cp = bv;\n          } else {\n            atomicOr(flags, " << (int)JF_OVERFLOW << ");\n"
-         "          }\n        }\n      }\n    }\n  }\n}\n";
+         "          }\n        }\n      }\n    }\n  }\n" << (runs ? "  }\n" : "") << "}\n";
 }
 
 // Seeding pass of the generated sweep (uniform pressure, corr mode): one
