@@ -517,3 +517,41 @@ def test_climb_batch6_objective_golden():
         oc = orc.select_range(probs[r], 0, 12 ** 6)
         for g, w in zip(got[r], oc):
             assert (g[0], g[1]) == (int(w[0]), int(w[1])), f"mixed corr [{r}]"
+
+
+@pytest.mark.parametrize("objective", [False, True])
+@pytest.mark.parametrize("shape", ["npre9", "big"])
+def test_library_sweep_odd_prefix_and_64bit_blocks(shape, objective):
+    # The library sweep with R_y = 12 on 256 bins (thresholds divided ahead
+    # by y's factor, or lowered by y's terms) for a prefix length without an
+    # unrolled variant (nine prefix nodes: the recurrence in LDS columns) and
+    # for block indices above 2^32 (64-bit digits), each on a ragged range
+    # near the end of the space, in corr / SLO mode and under J_L.
+    radix = [7] * 9 + [5, 12] if shape == "npre9" else [9] * 11 + [5, 12]
+    n = len(radix)
+    prob = small_dag(n, radix, 77 if shape == "npre9" else 78)
+    total = int(np.prod(radix, dtype=np.float64))
+    count = 4_000_037
+    begin = total - count - 12345
+    if objective:
+        obj = wl.paper_objective(prob, lambda_l=0.2)
+        item = (prob, obj)
+        want = orc.obj_select_range(prob, obj, begin, count)
+    else:
+        t = prob.tau.astype(np.float64)
+        prob = dataclasses.replace(prob, rho=np.array([[0.0], [0.3], [0.6]], np.float32),
+                                   slo=np.float32(0.8 * n * t.mean()))
+        item = prob
+        want = orc.select_range(prob, begin, count)
+    with D.Plan(item) as plan:
+        plan.set_option(D.DY_OPT_JIT, 0)
+        got = plan.select([D.range_source(0, begin, count)], stream=stream())[0]
+        assert plan.stats().ydiv_jobs == 1
+    ctx = f"{shape} objective={objective}"
+    if objective:
+        assert_obj_choices(got, want, ctx)
+    else:
+        for k, (g, w) in enumerate(zip(got, want)):
+            assert (g[0], g[1]) == (int(w[0]), int(w[1])), f"{ctx} level {k}: gpu {g} oracle {w}"
+            if int(w[1]):
+                assert g[2] == f32(w[2]) and g[3] == f32(w[3]) and g[4] == f32(w[4]), f"{ctx} level {k}"
