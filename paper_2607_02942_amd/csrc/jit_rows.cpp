@@ -323,9 +323,13 @@ __device__ __forceinline__ float dy_ydiv(float T, float r) {
   return T > 0x1p-60f ? T * r : 0.0f;
 }
 )";
-    if (ysh)  // dy_fkey: the objective preamble's order key
+    if (ysh)  // dy_skey: signed order key of a float (as the library's skey)
         o << R"(
-__device__ __forceinline__ unsigned dy_yshift(float t, float c) {
+__device__ __forceinline__ int dy_skey(float x) {
+  const int b = __float_as_int(x);
+  return b ^ ((b >> 31) & 0x7fffffff);
+}
+__device__ __forceinline__ int dy_yshift(float t, float c) {
   float x = t;
   if (t != __builtin_inff() && t != -__builtin_inff()) {
     x = t - c;
@@ -336,7 +340,7 @@ __device__ __forceinline__ unsigned dy_yshift(float t, float c) {
     }
     if (x == 0.0f) x = -0.0f;
   }
-  return dy_fkey(x);
+  return dy_skey(x);
 }
 )";
     o << R"(
@@ -364,7 +368,7 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
     } else if (ysh) {
         o << "  {\n    const float T = __uint_as_float(table[threadIdx.x]);\n    s_bins[threadIdx.x] = T;\n";
         for (int j = 0; j < D.ry; ++j)
-            o << "    ((unsigned*)s_bins)[" << (j + 1) * NBINS2 << " + threadIdx.x] = dy_yshift(T, " << flit(D.ysub[j])
+            o << "    ((int*)s_bins)[" << (j + 1) * NBINS2 << " + threadIdx.x] = dy_yshift(T, " << flit(D.ysub[j])
               << ");\n";
         o << "  }\n";
     } else {
@@ -473,12 +477,12 @@ extern "C" __global__ void __launch_bounds__(256) dy_sweep(
         o << "    const bool mine_ = cx >= __uint_as_float(m);\n";
     } else if (ysh) {
         o << "    const float R = fmaf(" << flit(-D.lam_l) << ", M, ux);\n";
-        o << "    unsigned m = 0xffffffffu;\n";
+        o << "    int m = 0x7fffffff;\n";
         o << "#pragma unroll\n    for (int j = 0; j < " << D.ry << "; ++j) {\n";
         o << "      const float bv = dx + dy[j];\n";
-        o << "      m = min(m, *(const unsigned*)((const char*)s_bins + " << NBINS2 * 4
+        o << "      m = min(m, *(const int*)((const char*)s_bins + " << NBINS2 * 4
           << " * (j + 1) + ((__float_as_uint(bv) >> 16) & 0x3fcu)));\n    }\n";
-        o << "    const bool mine_ = dy_fkey(R) >= m;\n";
+        o << "    const bool mine_ = dy_skey(R) >= m;\n";
     } else {
         o << "    unsigned long long hit = 0ull;\n";
         o << "#pragma unroll\n    for (int j = 0; j < " << D.ry << "; ++j) {\n";

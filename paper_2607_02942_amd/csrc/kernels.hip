@@ -1591,8 +1591,15 @@ __device__ __forceinline__ uint64_t sweep_test_obj(const float2 vy, float dy, fl
 // lambda_l M less one rounding.  With c_j = P->ysub[j] >= u_j - lambda_l tau_j
 // + (a bound on those four roundings), a plan whose G reaches a bin threshold
 // t has R >= t - c_j.  Returned: the order key (fkey) of an fp32 value <= t -
-// c_j, so the row's test is fkey(R) >= the least key of its plans' bins.
-__device__ __forceinline__ uint32_t yshift_key(float t, float c) {
+// c_j, so the row's test is skey(R) >= the least key of its plans' bins.
+// skey: the signed order key of a float (the magnitude bits of a negative
+// value flipped; -0 keys just below +0), three operations.
+__device__ __forceinline__ int32_t skey(float x) {
+    const int32_t b = __float_as_int(x);
+    return b ^ ((b >> 31) & 0x7fffffff);
+}
+
+__device__ __forceinline__ int32_t yshift_key(float t, float c) {
     float x = t;
     if (t != INFINITY && t != -INFINITY) {
         x = t - c;  // nearest: within half an ulp of t - c
@@ -1603,7 +1610,7 @@ __device__ __forceinline__ uint32_t yshift_key(float t, float c) {
         }
         if (x == 0.0f) x = -0.0f;  // -0 keys below +0; a zero R (either sign) still passes
     }
-    return fkey(x);
+    return skey(x);
 }
 
 // The rare path of the shifted sweep: the row's plans with the sweep's own
@@ -1655,10 +1662,11 @@ __device__ __forceinline__ void sweep_block_obj(PD P, JD J, uint64_t b, bool liv
     const CS float* dxt = cs(P->demx);
     const CS float* dyt = cs(P->demy);
     const int rx = P->rx, ry = P->ry;
-    const bool exy = P->edge_xy != 0;
+    // without a second sink x is no sink, so it feeds y
+    const bool exy = !HAS_S2 || P->edge_xy != 0;
     const float nl = -P->lam_l;
     if constexpr (B256 && RY > 0) {
-        const uint32_t* s_key = (const uint32_t*)(s_bins + NBINS2);
+        const int32_t* s_key = (const int32_t*)(s_bins + NBINS2);
         for (int ix = 0; ix < rx; ++ix) {
             const float2 vx = atx[ix];
             const float fx = vx.y + pf.px;
@@ -1667,13 +1675,13 @@ __device__ __forceinline__ void sweep_block_obj(PD P, JD J, uint64_t b, bool liv
             const float M = exy ? fmaxf(pf.py, fx) : pf.py;
             const float S2 = exy ? pf.s : fmaxf(pf.s, fx);
             const float R = fmaf(nl, M, ux);
-            uint32_t m = 0xffffffffu;
+            int32_t m = INT32_MAX;
 #pragma unroll
             for (int j = 0; j < (RY > 0 ? RY : 1); ++j) {
                 const float D = dx + dyr[j];
-                m = min(m, *(const uint32_t*)((const char*)(s_key + j * NBINS2) + ((__float_as_uint(D) >> 16) & 0x3fcu)));
+                m = min(m, *(const int32_t*)((const char*)(s_key + j * NBINS2) + ((__float_as_uint(D) >> 16) & 0x3fcu)));
             }
-            const uint64_t hit = __ballot(fkey(R) >= m) & live_mask;
+            const uint64_t hit = __ballot(skey(R) >= m) & live_mask;
             if (hit) {
                 const uint32_t nh = (uint32_t)__popcll(hit);
                 if (qn + nh > (uint32_t)RQ) {
@@ -1750,7 +1758,7 @@ __global__ void __launch_bounds__(WG) k_sweep_obj(const JobDev* __restrict__ job
         const float thr = __uint_as_float(J->table2[threadIdx.x]);
         s_bins[threadIdx.x] = thr;
         if constexpr (YSH) {
-            uint32_t* s_key = (uint32_t*)(s_bins + NBINS2);
+            int32_t* s_key = (int32_t*)(s_bins + NBINS2);
 #pragma unroll
             for (int j = 0; j < (RY > 0 ? RY : 1); ++j) s_key[j * NBINS2 + threadIdx.x] = yshift_key(thr, P->ysub[j]);
         }
